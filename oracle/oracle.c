@@ -1,0 +1,1232 @@
+/*
+ * EntroPack CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-threaded C implementation of what the EntroPack paper
+ * (arXiv 2609.34185, "EntroPack: Fast and Accurate Entropy-Coded Weight
+ * Compression at Arbitrary Bitrates") defines: row normalisation, the
+ * Conway-Sloane nearest-E8 quantiser, the integer field map, the
+ * coset-conditioned model, sampled-row rate estimation with geometric scale
+ * search, row-scale refit, the tiled interleaved rANS encoder and decoder, and
+ * reconstruction with dtype snapping.
+ *
+ * Only the test suite, the smoke check and the benchmark's CPU-baseline leg
+ * may load this library.  It shares no code with the GPU library.  All
+ * floating-point work is FP64 unless the paper fixes another precision
+ * (weights are FP32 after input conversion; row scales are stored as FP32;
+ * reconstruction multiplies in FP32).
+ *
+ * Readings taken where the paper is silent (each is listed in the design
+ * notes of the repository):
+ *   - coset tie: the integer-coset candidate wins unless the half-integer one
+ *     is strictly closer;
+ *   - "alphabet" for the capacity check = index range max-min+1 of a table;
+ *   - frequency normalisation = floor, then largest-remainder top-up, then
+ *     decrement of the largest frequency (ties to the smaller symbol);
+ *   - sample rows: ceil(2^18 / (C/8)) whole rows chosen by a partial
+ *     Fisher-Yates shuffle driven by SplitMix64 seeded with (R<<32)^C;
+ *   - rANS renormalisation threshold f*2^(31-b), states start at 2^15, words
+ *     are consumed in (step ascending, lane ascending) order;
+ *   - tile-local vector i belongs to lane i mod 32;
+ *   - container routes: delta_r = fp32(amax_r/448) (FP8 e4m3fn) or
+ *     fp32(amax_r/127) (INT8, symmetric), amax 0 gives delta 1, the quotient
+ *     W/delta is formed in FP64 and rounded once into the container.
+ *
+ * Parity status of every function is stated in its comment; pins live in the
+ * CPU tests.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---- constants of the method (paper section in brackets) ---------------- */
+#define ORA_J 32u                    /* interleaved states per tile [3.6] */
+#define ORA_L (1u << 15)             /* state lower bound [App. C.3] */
+#define ORA_ETA 1e-12                /* eta of the row RMS and refit [3.2, 3.5] */
+#define ORA_NTAB 17                  /* 1 coset + 2 x 8 field tables [3.3] */
+
+/* ---- format constants (this repository's stored representation) -------- */
+#define ORA_MAGIC 0x314B5045u        /* "EPK1" little-endian */
+#define ORA_VERSION 1u
+#define ORA_HEADER_BYTES 48u
+
+/* dtype codes (inputs: 1..3; outputs: 1..5, 100) */
+enum { O_BF16 = 1, O_FP16 = 2, O_FP32 = 3, O_FP8 = 4, O_INT8 = 5, O_COORD2 = 100 };
+enum { O_CONT_DIRECT = 0, O_CONT_FP8 = 1, O_CONT_INT8 = 2 };
+enum { O_OK = 0, O_ERR_ARG = -1, O_ERR_FORMAT = -2, O_ERR_UNSUPPORTED = -3,
+       O_ERR_NOMEM = -4, O_ERR_CORRUPT = -6 };
+
+typedef struct {
+  double target_bpp;
+  int32_t tile_vectors;
+  int32_t prob_bits;       /* 0: 11 for targets <= 7 bpp, else 12 [App. C.1] */
+  int32_t search_steps;    /* I_s = 12 [App. C.1] */
+  int32_t container;
+  double scale_lo, scale_hi; /* [1e-3, 8] [App. C.1] */
+  int64_t sample_vectors;  /* 2^18 [App. C.1] */
+  double state_credit_bits; /* bits credited per terminal state in [3.4, eq. estimate]:
+                             * the equation prints 16; a state started at 2^15 retains
+                             * log2(x/2^15) bits, 8 on average, and 8 is the default
+                             * reading (16 stays selectable). */
+} ora_params;
+
+/* indices into the stats array filled by ora_encode */
+enum {
+  ST_SCALE = 0, ST_B, ST_RHAT_SUB, ST_R_STORED, ST_BYTES, ST_PAYLOAD_BITS, ST_CCE_FULL,
+  ST_N_TILES, ST_MAX_A, ST_EREL_CODED, ST_EREL_ORIG, ST_MEAN_STATE_BITS,
+  ST_TABLE_BYTES, ST_SAMPLE_ROWS, ST_ESCALATIONS, ST_COARSENINGS, ST_N_STATS = 32
+};
+
+/* ========================================================================= */
+/* Dtype conversions, written from the format definitions.                    */
+/* ========================================================================= */
+
+/* Round-to-nearest-even of |y| onto a binary format with `mant` fraction bits,
+ * minimum normal exponent `emin`, saturating at `maxv` (snap_tau of [3.7,
+ * eq. recon]; saturation instead of overflow).  Subnormals use the quantum of
+ * emin.  y is an exactly representable double; the division by a power of two
+ * is exact, so nearbyint sees the true value. */
+static double snap_binary(double y, int mant, int emin, double maxv) {
+  if (y == 0.0) return y;
+  double a = fabs(y);
+  int e;
+  frexp(a, &e);            /* a = m * 2^e with m in [0.5, 1) */
+  e -= 1;                  /* a in [2^e, 2^(e+1)) */
+  if (e < emin) e = emin;
+  double q = ldexp(1.0, e - mant);
+  double r = nearbyint(a / q) * q;
+  if (r > maxv) r = maxv;
+  return y < 0 ? -r : r;
+}
+
+static const double BF16_MAX = 3.38953138925153547590470800371487866880e+38; /* (2-2^-7)*2^127 */
+
+static double snap_bf16(double y) { return snap_binary(y, 7, -126, BF16_MAX); }
+static double snap_fp16(double y) { return snap_binary(y, 10, -14, 65504.0); }
+static double snap_e4m3(double y) { return snap_binary(y, 3, -6, 448.0); }
+
+static uint16_t bf16_bits(double r) { /* r already a bf16 value: exact as float */
+  float f = (float)r;
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  return (uint16_t)(u >> 16);
+}
+
+static uint16_t fp16_bits(double r) { /* r already an fp16 value */
+  uint16_t s = (r < 0 || (r == 0 && signbit(r))) ? 0x8000 : 0;
+  double a = fabs(r);
+  if (a == 0) return s;
+  if (a < ldexp(1.0, -14)) return (uint16_t)(s | (uint16_t)(a / ldexp(1.0, -24)));
+  int e;
+  frexp(a, &e);
+  e -= 1;
+  uint16_t mant = (uint16_t)((a / ldexp(1.0, e) - 1.0) * 1024.0);
+  return (uint16_t)(s | ((uint16_t)(e + 15) << 10) | mant);
+}
+
+static uint8_t e4m3_bits(double r) { /* r already an e4m3fn value, |r| <= 448 */
+  uint8_t s = (r < 0 || (r == 0 && signbit(r))) ? 0x80 : 0;
+  double a = fabs(r);
+  if (a == 0) return s;
+  if (a < ldexp(1.0, -6)) return (uint8_t)(s | (uint8_t)(a / ldexp(1.0, -9)));
+  int e;
+  frexp(a, &e);
+  e -= 1;
+  uint8_t mant = (uint8_t)((a / ldexp(1.0, e) - 1.0) * 8.0);
+  return (uint8_t)(s | ((uint8_t)(e + 7) << 3) | mant);
+}
+
+static double bf16_value(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+static double fp16_value(uint16_t h) {
+  int s = h >> 15, e = (h >> 10) & 31, m = h & 1023;
+  double v;
+  if (e == 0) v = ldexp((double)m, -24);
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = ldexp(1.0 + m / 1024.0, e - 15);
+  return s ? -v : v;
+}
+
+static double e4m3_value(uint8_t b) {
+  int s = b >> 7, e = (b >> 3) & 15, m = b & 7;
+  double v;
+  if (e == 15 && m == 7) v = NAN;
+  else if (e == 0) v = ldexp((double)m, -9);
+  else v = ldexp(1.0 + m / 8.0, e - 7);
+  return s ? -v : v;
+}
+
+/* Test hook: snap doubles to an output dtype and write its bit patterns.
+ * INT8 is clamp(RNE(y), -128, 127).  Pinned against torch CPU casts. */
+int ora_snap(const double* y, int64_t n, int dtype, void* out) {
+  for (int64_t i = 0; i < n; i++) {
+    double v = y[i];
+    switch (dtype) {
+      case O_BF16: ((uint16_t*)out)[i] = bf16_bits(snap_bf16(v)); break;
+      case O_FP16: ((uint16_t*)out)[i] = fp16_bits(snap_fp16(v)); break;
+      case O_FP32: ((float*)out)[i] = (float)v; break;
+      case O_FP8: ((uint8_t*)out)[i] = e4m3_bits(snap_e4m3(v)); break;
+      case O_INT8: {
+        double r = nearbyint(v);
+        if (r > 127) r = 127;
+        if (r < -128) r = -128;
+        ((int8_t*)out)[i] = (int8_t)r;
+        break;
+      }
+      default: return O_ERR_ARG;
+    }
+  }
+  return O_OK;
+}
+
+/* ========================================================================= */
+/* Nearest lattice points [3.2, eq. d8 and eq. quantize].                     */
+/* Pinned by brute force over 3^8 neighbourhoods and by constructed ties.     */
+/* ========================================================================= */
+
+/* Nearest D8 point: round each coordinate half-to-even; if the coordinate sum
+ * is odd, move the coordinate with the largest rounding residual (first index
+ * on ties) one step towards y, with sign(0) = +1. */
+static void nearest_d8(const double y[8], double z[8]) {
+  double d[8];
+  double sum = 0;
+  for (int j = 0; j < 8; j++) {
+    z[j] = nearbyint(y[j]);
+    d[j] = y[j] - z[j];
+    sum += z[j];
+  }
+  if (fmod(fabs(sum), 2.0) == 1.0) {
+    int js = 0;
+    for (int j = 1; j < 8; j++)
+      if (fabs(d[j]) > fabs(d[js])) js = j;
+    z[js] += (d[js] >= 0) ? 1.0 : -1.0;
+  }
+}
+
+static double dist2(const double y[8], const double p[8]) {
+  double acc = 0;
+  for (int j = 0; j < 8; j++) acc += (y[j] - p[j]) * (y[j] - p[j]);
+  return acc;
+}
+
+/* Nearest E8 point written as doubled integer coordinates 2p; returns the
+ * coset (0: D8, 1: D8 + 1/2).  The D8 candidate is kept unless the shifted
+ * candidate is strictly closer. */
+static int nearest_e8(const double y[8], int32_t two_p[8]) {
+  double a[8], ys[8], bb[8];
+  nearest_d8(y, a);
+  for (int j = 0; j < 8; j++) ys[j] = y[j] - 0.5;
+  nearest_d8(ys, bb);
+  for (int j = 0; j < 8; j++) bb[j] += 0.5;
+  if (dist2(y, bb) < dist2(y, a)) {
+    for (int j = 0; j < 8; j++) two_p[j] = (int32_t)(2.0 * bb[j]);
+    return 1;
+  }
+  for (int j = 0; j < 8; j++) two_p[j] = (int32_t)(2.0 * a[j]);
+  return 0;
+}
+
+int ora_nearest_d8(const double* y, int64_t nvec, int32_t* z) {
+  for (int64_t v = 0; v < nvec; v++) {
+    double t[8];
+    nearest_d8(y + 8 * v, t);
+    for (int j = 0; j < 8; j++) z[8 * v + j] = (int32_t)t[j];
+  }
+  return O_OK;
+}
+
+int ora_nearest_e8(const double* y, int64_t nvec, int32_t* two_p, int32_t* coset) {
+  for (int64_t v = 0; v < nvec; v++) coset[v] = nearest_e8(y + 8 * v, two_p + 8 * v);
+  return O_OK;
+}
+
+/* ========================================================================= */
+/* Field map [3.2, eq. parity and eq. point_inverse].  Pinned by round trips.  */
+/* fields per vector: c, z1..z7, m                                            */
+/* ========================================================================= */
+
+static void point_to_fields(const int32_t two_p[8], int32_t f9[9]) {
+  int32_t c = two_p[0] & 1;              /* odd doubled coordinate <=> half-integer coset */
+  int32_t z[8];
+  for (int j = 0; j < 8; j++) z[j] = (two_p[j] - c) / 2;   /* exact: two_p - c is even */
+  int32_t s7 = 0;
+  for (int j = 0; j < 7; j++) s7 += z[j];
+  int32_t pi = s7 & 1;                   /* non-negative residue mod 2 */
+  f9[0] = c;
+  for (int j = 0; j < 7; j++) f9[1 + j] = z[j];
+  f9[8] = (z[7] - pi) / 2;               /* exact: z8 - pi is even on D8 */
+}
+
+static void fields_to_point(const int32_t f9[9], int32_t two_p[8]) {
+  int32_t c = f9[0];
+  int32_t s7 = 0;
+  for (int j = 0; j < 7; j++) s7 += f9[1 + j];
+  int32_t pi = s7 & 1;
+  for (int j = 0; j < 7; j++) two_p[j] = 2 * f9[1 + j] + c;
+  two_p[7] = 2 * (2 * f9[8] + pi) + c;
+}
+
+int ora_fields(const int32_t* two_p, int64_t nvec, int32_t* fields) {
+  for (int64_t v = 0; v < nvec; v++) point_to_fields(two_p + 8 * v, fields + 9 * v);
+  return O_OK;
+}
+
+int ora_points(const int32_t* fields, int64_t nvec, int32_t* two_p) {
+  for (int64_t v = 0; v < nvec; v++) fields_to_point(fields + 9 * v, two_p + 8 * v);
+  return O_OK;
+}
+
+/* ========================================================================= */
+/* Coset-conditioned model [3.3, eq. cond and eq. length].                    */
+/* Table index: 0 = coset; 1 + 8c + (i-1) = field i (1..8) under coset c.     */
+/* ========================================================================= */
+
+typedef struct {
+  int32_t min;        /* value of symbol index 0 */
+  int32_t A;          /* index range max-min+1 (0 if the table saw nothing) */
+  uint64_t* n;        /* counts over the index range */
+  uint32_t* f;        /* normalised frequencies */
+} table_t;
+
+static int table_of(int field, int c) { return field == 0 ? 0 : 1 + 8 * c + (field - 1); }
+
+static void tables_free(table_t* T) {
+  for (int t = 0; t < ORA_NTAB; t++) {
+    free(T[t].n);
+    free(T[t].f);
+    T[t].n = NULL;
+    T[t].f = NULL;
+    T[t].A = 0;
+  }
+}
+
+/* Count field values over a list of vectors (fields stored 9 per vector). */
+static int tables_count(const int32_t* fields, int64_t nvec, table_t* T) {
+  int32_t lo[ORA_NTAB], hi[ORA_NTAB];
+  for (int t = 0; t < ORA_NTAB; t++) {
+    lo[t] = INT32_MAX;
+    hi[t] = INT32_MIN;
+  }
+  lo[0] = 0;
+  hi[0] = 1;                              /* coset table always has 2 symbols */
+  for (int64_t v = 0; v < nvec; v++) {
+    const int32_t* f9 = fields + 9 * v;
+    for (int i = 1; i <= 8; i++) {
+      int t = table_of(i, f9[0]);
+      if (f9[i] < lo[t]) lo[t] = f9[i];
+      if (f9[i] > hi[t]) hi[t] = f9[i];
+    }
+  }
+  for (int t = 0; t < ORA_NTAB; t++) {
+    T[t].min = (hi[t] >= lo[t]) ? lo[t] : 0;
+    T[t].A = (hi[t] >= lo[t]) ? (int32_t)((int64_t)hi[t] - lo[t] + 1) : 0;
+    T[t].n = (uint64_t*)calloc(T[t].A ? (size_t)T[t].A : 1, sizeof(uint64_t));
+    T[t].f = (uint32_t*)calloc(T[t].A ? (size_t)T[t].A : 1, sizeof(uint32_t));
+    if (!T[t].n || !T[t].f) return O_ERR_NOMEM;
+  }
+  for (int64_t v = 0; v < nvec; v++) {
+    const int32_t* f9 = fields + 9 * v;
+    T[0].n[f9[0]]++;
+    for (int i = 1; i <= 8; i++) {
+      int t = table_of(i, f9[0]);
+      T[t].n[f9[i] - T[t].min]++;
+    }
+  }
+  return O_OK;
+}
+
+/* Integer frequencies summing to M = 2^b, positive exactly on observed
+ * symbols [3.3].  Requires #observed <= M.  Procedure (the paper gives none):
+ * f = max(1, floor(M n / N)); the units still missing go, one each, to the
+ * observed symbols with the largest shortfall M n - f N (ties: smaller
+ * symbol); a surplus is removed one unit at a time from the largest frequency
+ * above 1 (ties: smaller symbol). */
+typedef struct {
+  int64_t prio;
+  int32_t z;
+} prio_t;
+
+static int cmp_prio(const void* a, const void* b) {
+  const prio_t* x = (const prio_t*)a;
+  const prio_t* y = (const prio_t*)b;
+  if (x->prio != y->prio) return x->prio > y->prio ? -1 : 1;
+  return (x->z > y->z) - (x->z < y->z);
+}
+
+static int normalize_counts(const uint64_t* n, int32_t A, int b, uint32_t* f) {
+  const uint64_t M = 1ull << b;
+  uint64_t N = 0, K = 0;
+  for (int32_t z = 0; z < A; z++) {
+    N += n[z];
+    K += n[z] > 0;
+  }
+  for (int32_t z = 0; z < A; z++) f[z] = 0;
+  if (N == 0) return O_OK;
+  if (K > M) return O_ERR_ARG;
+  int64_t sum = 0;
+  for (int32_t z = 0; z < A; z++) {
+    if (!n[z]) continue;
+    uint64_t q = (M * n[z]) / N;
+    f[z] = (uint32_t)(q ? q : 1);
+    sum += f[z];
+  }
+  int64_t delta = (int64_t)M - sum;
+  if (delta > 0) { /* fewer than K units are missing, so each symbol gains at most one */
+    prio_t* order = (prio_t*)malloc((size_t)K * sizeof(prio_t));
+    if (!order) return O_ERR_NOMEM;
+    int64_t k = 0;
+    for (int32_t z = 0; z < A; z++)
+      if (n[z]) {
+        order[k].prio = (int64_t)(M * n[z]) - (int64_t)f[z] * (int64_t)N;
+        order[k].z = z;
+        k++;
+      }
+    qsort(order, (size_t)k, sizeof(prio_t), cmp_prio);
+    for (int64_t i = 0; i < delta; i++) f[order[i].z]++;
+    free(order);
+  }
+  while (delta < 0) {
+    int32_t best = -1;
+    for (int32_t z = 0; z < A; z++)
+      if (f[z] > 1 && (best < 0 || f[z] > f[best])) best = z;
+    f[best]--;
+    delta++;
+  }
+  return O_OK;
+}
+
+int ora_normalize(const uint64_t* n, int32_t A, int32_t b, uint32_t* f) {
+  return normalize_counts(n, A, b, f);
+}
+
+/* Modelled code length C_CE = sum n (b - log2 f) over observed symbols [3.3, eq. length]. */
+static double code_length_table(const uint64_t* n, const uint32_t* f, int32_t A, int b) {
+  double acc = 0;
+  for (int32_t z = 0; z < A; z++)
+    if (n[z]) acc += (double)n[z] * ((double)b - log2((double)f[z]));
+  return acc;
+}
+
+double ora_code_length(const uint64_t* n, const uint32_t* f, int32_t A, int32_t b) {
+  return code_length_table(n, f, A, b);
+}
+
+/* Serialized table bytes: coset (2 x u16) + per field table (i32 min, u32 A,
+ * u16 f[A], padded to 4 bytes). */
+static uint64_t tables_bytes(const table_t* T) {
+  uint64_t bytes = 4;
+  for (int t = 1; t < ORA_NTAB; t++) bytes += 8 + ((2ull * (uint64_t)T[t].A + 3) & ~3ull);
+  return bytes;
+}
+
+static int32_t tables_max_A(const table_t* T) {
+  int32_t m = 0;
+  for (int t = 1; t < ORA_NTAB; t++)
+    if (T[t].A > m) m = T[t].A;
+  return m;
+}
+
+static int tables_normalize(table_t* T, int b) {
+  for (int t = 0; t < ORA_NTAB; t++) {
+    int rc = normalize_counts(T[t].n, T[t].A, b, T[t].f);
+    if (rc) return rc;
+  }
+  return O_OK;
+}
+
+static double tables_code_length(const table_t* T, int b) {
+  double acc = 0;
+  for (int t = 0; t < ORA_NTAB; t++) acc += code_length_table(T[t].n, T[t].f, T[t].A, b);
+  return acc;
+}
+
+/* ========================================================================= */
+/* Stored-size estimate [3.4, eq. estimate and eq. outer_estimate].           */
+/* ========================================================================= */
+
+static uint64_t n_tiles_of(uint64_t nvec, uint32_t V) { return (nvec + V - 1) / V; }
+
+/* Tile metadata bytes: J 32-bit terminal states and one 32-bit offset per tile,
+ * plus one final boundary offset [App. C.3]. */
+static uint64_t restart_bytes(uint64_t n_tiles) { return 132ull * n_tiles + 4ull; }
+
+static double estimate_bits(double cce, uint64_t n_tiles, double kappa, const table_t* T,
+                            uint64_t rows, int container) {
+  double x = cce - kappa * (double)ORA_J * (double)n_tiles;
+  if (x < 0) x = 0;
+  double payload = 16.0 * ceil(x / 16.0);
+  double pad = fmod(payload / 16.0, 2.0) == 1.0 ? 16.0 : 0.0; /* payload padded to 4 bytes */
+  double restart = 8.0 * (double)restart_bytes(n_tiles);
+  double tables = 8.0 * (double)tables_bytes(T);
+  double scales = 32.0 * (double)rows * (container ? 2.0 : 1.0);
+  double other = 8.0 * ORA_HEADER_BYTES;
+  return payload + pad + restart + tables + scales + other;
+}
+
+/* ========================================================================= */
+/* Input conversion, containers and row normalisation [3.2, App. A.6/B.1].    */
+/* ========================================================================= */
+
+static double input_value(const void* w, int dtype, int64_t i) {
+  switch (dtype) {
+    case O_BF16: return bf16_value(((const uint16_t*)w)[i]);
+    case O_FP16: return fp16_value(((const uint16_t*)w)[i]);
+    default: return (double)((const float*)w)[i];
+  }
+}
+
+/* Fills x (coded values, FP32-exact) and delta (container scales).  Returns an
+ * error for non-finite input. */
+static int prepare_values(const void* w, int dtype, int64_t R, int64_t C, int container,
+                          float* x, float* delta) {
+  for (int64_t r = 0; r < R; r++) {
+    double amax = 0;
+    for (int64_t j = 0; j < C; j++) {
+      double v = (double)(float)input_value(w, dtype, r * C + j); /* x = fp32(W) */
+      if (!isfinite(v)) return O_ERR_ARG;
+      x[r * C + j] = (float)v;
+      if (fabs(v) > amax) amax = fabs(v);
+    }
+    if (container == O_CONT_DIRECT) continue;
+    double qmax = container == O_CONT_FP8 ? 448.0 : 127.0;
+    float d = amax > 0 ? (float)(amax / qmax) : 1.0f;
+    delta[r] = d;
+    for (int64_t j = 0; j < C; j++) {
+      double q = (double)x[r * C + j] / (double)d;
+      double cv;
+      if (container == O_CONT_FP8) {
+        cv = snap_e4m3(q);
+      } else {
+        cv = nearbyint(q);
+        if (cv > 127) cv = 127;
+        if (cv < -127) cv = -127;
+      }
+      x[r * C + j] = (float)cv;
+    }
+  }
+  return O_OK;
+}
+
+/* mu_r = max(sqrt(C^-1 sum_j x_rj^2), eta) [3.2] */
+static double row_rms(const float* xr, int64_t C) {
+  double acc = 0;
+  for (int64_t j = 0; j < C; j++) acc += (double)xr[j] * (double)xr[j];
+  double mu = sqrt(acc / (double)C);
+  return mu > ORA_ETA ? mu : ORA_ETA;
+}
+
+/* Quantise whole rows at scale s: fields (9 per vector) and optionally 2p. */
+static void quantize_rows(const float* x, const double* mu, int64_t C, const int64_t* rows,
+                          int64_t nrows, double s, int32_t* fields, int32_t* two_p_out) {
+  int64_t cvec = C / 8;
+  for (int64_t k = 0; k < nrows; k++) {
+    int64_t r = rows[k];
+    for (int64_t jv = 0; jv < cvec; jv++) {
+      double y[8];
+      int32_t tp[8];
+      for (int j = 0; j < 8; j++) y[j] = ((double)x[r * C + 8 * jv + j] / mu[r]) / s;
+      nearest_e8(y, tp);
+      int64_t v = k * cvec + jv;
+      point_to_fields(tp, fields + 9 * v);
+      if (two_p_out)
+        for (int j = 0; j < 8; j++) two_p_out[8 * v + j] = tp[j];
+    }
+  }
+}
+
+/* SplitMix64 (Steele, Lea, Flood 2014). */
+static uint64_t splitmix64(uint64_t* st) {
+  uint64_t z = (*st += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+static int cmp_i64(const void* a, const void* b) {
+  int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+  return (x > y) - (x < y);
+}
+
+/* Fixed sample of whole rows [3.4 "Sampled rate evaluation", App. C.1]. */
+static int64_t choose_sample_rows(int64_t R, int64_t C, int64_t sample_vectors, int64_t* rows) {
+  int64_t cvec = C / 8;
+  int64_t k = (sample_vectors + cvec - 1) / cvec;
+  for (int64_t r = 0; r < R; r++) rows[r] = r;
+  if (k >= R) return R;
+  uint64_t st = ((uint64_t)R << 32) ^ (uint64_t)C;
+  for (int64_t i = 0; i < k; i++) {
+    int64_t j = i + (int64_t)(splitmix64(&st) % (uint64_t)(R - i));
+    int64_t t = rows[i];
+    rows[i] = rows[j];
+    rows[j] = t;
+  }
+  qsort(rows, (size_t)k, sizeof(int64_t), cmp_i64);
+  return k;
+}
+
+/* ========================================================================= */
+/* Encoder [3.4 Alg. rate selection, 3.5 refit, 3.6 rANS, App. C].            */
+/* ========================================================================= */
+
+typedef struct {
+  uint16_t* w;
+  uint64_t n, cap;
+} wordbuf;
+
+static int wb_push(wordbuf* b, uint16_t v) {
+  if (b->n == b->cap) {
+    uint64_t nc = b->cap ? 2 * b->cap : 1024;
+    uint16_t* p = (uint16_t*)realloc(b->w, nc * sizeof(uint16_t));
+    if (!p) return O_ERR_NOMEM;
+    b->w = p;
+    b->cap = nc;
+  }
+  b->w[b->n++] = v;
+  return O_OK;
+}
+
+static void put32(uint8_t* p, uint32_t v) { memcpy(p, &v, 4); }
+static void put64(uint8_t* p, uint64_t v) { memcpy(p, &v, 8); }
+static uint32_t get32(const uint8_t* p) { uint32_t v; memcpy(&v, p, 4); return v; }
+static uint64_t get64(const uint8_t* p) { uint64_t v; memcpy(&v, p, 8); return v; }
+
+/* Symbol index (table, zero-based index) of field i of vector v. */
+static void symbol_of(const int32_t* f9, int i, const table_t* T, int* t, int32_t* idx) {
+  if (i == 0) {
+    *t = 0;
+    *idx = f9[0];
+  } else {
+    *t = table_of(i, f9[0]);
+    *idx = f9[i] - T[*t].min;
+  }
+}
+
+int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params* prm,
+               uint8_t** out_blob, uint64_t* out_size, double* stats) {
+  if (!w || !prm || !out_blob || !out_size || R <= 0 || C <= 0 || C % 8) return O_ERR_ARG;
+  if (dtype != O_BF16 && dtype != O_FP16 && dtype != O_FP32) return O_ERR_ARG;
+  if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0) return O_ERR_ARG;
+  if (prm->container < 0 || prm->container > 2) return O_ERR_ARG;
+  if (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) return O_ERR_ARG;
+  if ((R * C) / 8 > 0xFFFFFFFFll || R > 0xFFFFFFFFll || C > 0xFFFFFFFFll) return O_ERR_ARG;
+
+  const int64_t N = R * C, nvec = N / 8, cvec = C / 8;
+  const uint32_t V = (uint32_t)prm->tile_vectors;
+  const int cont = prm->container;
+  double st_local[ST_N_STATS];
+  double* st = stats ? stats : st_local;
+  for (int i = 0; i < ST_N_STATS; i++) st[i] = 0;
+
+  int rc = O_OK;
+  float* x = (float*)malloc((size_t)N * sizeof(float));
+  float* delta = (float*)calloc((size_t)R, sizeof(float));
+  double* mu = (double*)malloc((size_t)R * sizeof(double));
+  int64_t* rows = (int64_t*)malloc((size_t)R * sizeof(int64_t));
+  int64_t* all_rows = (int64_t*)malloc((size_t)R * sizeof(int64_t));
+  int32_t* fields = (int32_t*)malloc((size_t)nvec * 9 * sizeof(int32_t));
+  int32_t* two_p = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+  int32_t* sfields = NULL;
+  float* sigma = (float*)malloc((size_t)R * sizeof(float));
+  table_t T[ORA_NTAB], TS[ORA_NTAB];
+  memset(T, 0, sizeof T);
+  memset(TS, 0, sizeof TS);
+  wordbuf pay = {0};
+  uint32_t* states = NULL;
+  uint32_t* offsets = NULL;
+  uint8_t* blob = NULL;
+  if (!x || !delta || !mu || !rows || !all_rows || !fields || !two_p || !sigma) {
+    rc = O_ERR_NOMEM;
+    goto done;
+  }
+
+  rc = prepare_values(w, dtype, R, C, cont, x, delta);
+  if (rc) goto done;
+  for (int64_t r = 0; r < R; r++) {
+    mu[r] = row_rms(x + r * C, C);
+    all_rows[r] = r;
+  }
+
+  /* sample of whole rows */
+  int64_t nsr = choose_sample_rows(R, C, prm->sample_vectors, rows);
+  int64_t snvec = nsr * cvec;
+  sfields = (int32_t*)malloc((size_t)snvec * 9 * sizeof(int32_t));
+  if (!sfields) {
+    rc = O_ERR_NOMEM;
+    goto done;
+  }
+  const uint64_t s_tiles = n_tiles_of((uint64_t)snvec, V);
+  const double Nsub = (double)(nsr * C);
+
+  int b0 = prm->prob_bits ? prm->prob_bits : (prm->target_bpp <= 7.0 ? 11 : 12);
+  int b = b0, accepted = 0;
+  double s = 1.0, rhat = 0;
+  for (b = b0; b <= 15; b++) {
+    double lo = prm->scale_lo, hi = prm->scale_hi;
+    for (int it = 0; it < prm->search_steps; it++) {
+      s = sqrt(lo * hi);
+      quantize_rows(x, mu, C, rows, nsr, s, sfields, NULL);
+      tables_free(TS);
+      rc = tables_count(sfields, snvec, TS);
+      if (rc) goto done;
+      if (tables_max_A(TS) > (1 << b)) {
+        rhat = INFINITY;
+      } else {
+        rc = tables_normalize(TS, b);
+        if (rc) goto done;
+        double cce = tables_code_length(TS, b);
+        rhat = estimate_bits(cce, s_tiles, prm->state_credit_bits, TS, (uint64_t)nsr, cont) / Nsub;
+      }
+      if (rhat > prm->target_bpp) lo = s;
+      else hi = s;
+    }
+    s = sqrt(lo * hi);
+    quantize_rows(x, mu, C, all_rows, R, s, fields, two_p);
+    tables_free(T);
+    rc = tables_count(fields, nvec, T);
+    if (rc) goto done;
+    if (tables_max_A(T) <= (1 << b)) {
+      accepted = 1;
+      break;
+    }
+    st[ST_ESCALATIONS] += 1;
+  }
+  if (!accepted) { /* coarsen at the largest precision [App. C.1] */
+    b = 15;
+    while (tables_max_A(T) > (1 << b)) {
+      s = 1.05 * s * (double)tables_max_A(T) / (double)(1 << b);
+      quantize_rows(x, mu, C, all_rows, R, s, fields, two_p);
+      tables_free(T);
+      rc = tables_count(fields, nvec, T);
+      if (rc) goto done;
+      st[ST_COARSENINGS] += 1;
+    }
+  }
+  rc = tables_normalize(T, b);
+  if (rc) goto done;
+
+  /* row-scale refit [3.5, eq. scale_fit] */
+  for (int64_t r = 0; r < R; r++) {
+    double num = 0, den = 0;
+    for (int64_t j = 0; j < C; j++) {
+      double p = two_p[r * C + j] / 2.0;
+      num += (double)x[r * C + j] * p;
+      den += p * p;
+    }
+    double sg;
+    if (den > 0) {
+      sg = num / den;
+      if (sg < ORA_ETA) sg = ORA_ETA;
+    } else {
+      sg = s * mu[r];
+    }
+    sigma[r] = (float)sg;
+  }
+
+  /* tiled interleaved rANS [3.6, eq. rans_encode; App. C.3] */
+  const uint64_t n_tiles = n_tiles_of((uint64_t)nvec, V);
+  const uint32_t M = 1u << b;
+  states = (uint32_t*)malloc(n_tiles * ORA_J * sizeof(uint32_t));
+  offsets = (uint32_t*)malloc((n_tiles + 1) * sizeof(uint32_t));
+  uint32_t* cumul[ORA_NTAB];
+  memset(cumul, 0, sizeof cumul);
+  if (!states || !offsets) {
+    rc = O_ERR_NOMEM;
+    goto done;
+  }
+  for (int t = 0; t < ORA_NTAB; t++) {
+    cumul[t] = (uint32_t*)calloc((size_t)T[t].A + 1, sizeof(uint32_t));
+    if (!cumul[t]) {
+      rc = O_ERR_NOMEM;
+      for (int u = 0; u < t; u++) free(cumul[u]);
+      goto done;
+    }
+    for (int32_t z = 0; z < T[t].A; z++) cumul[t][z + 1] = cumul[t][z] + T[t].f[z];
+  }
+  double state_bits = 0;
+  offsets[0] = 0;
+  for (uint64_t tile = 0; tile < n_tiles; tile++) {
+    uint64_t v0 = tile * V;
+    uint64_t nv = (uint64_t)nvec - v0 < V ? (uint64_t)nvec - v0 : V;
+    uint64_t steps = 9 * ((nv + ORA_J - 1) / ORA_J);
+    uint32_t xs[ORA_J];
+    for (uint32_t l = 0; l < ORA_J; l++) xs[l] = ORA_L;
+    uint64_t start = pay.n;
+    for (uint64_t step = steps; step-- > 0;) {
+      uint64_t k = step / 9;
+      int i = (int)(step % 9);
+      for (uint32_t l = ORA_J; l-- > 0;) {
+        uint64_t li = l + ORA_J * k;
+        if (li >= nv) continue;
+        int t;
+        int32_t idx;
+        symbol_of(fields + 9 * (v0 + li), i, T, &t, &idx);
+        uint32_t f = T[t].f[idx], F = cumul[t][idx];
+        uint64_t xx = xs[l];
+        if (xx >= ((uint64_t)f << (31 - b))) {
+          rc = wb_push(&pay, (uint16_t)(xx & 0xFFFF));
+          if (rc) goto done_cumul;
+          xx >>= 16;
+        }
+        xx = (xx / f) * M + (xx % f) + F;
+        xs[l] = (uint32_t)xx;
+      }
+    }
+    for (uint64_t a = start, z = pay.n - 1; pay.n && a < z; a++, z--) { /* emitted backwards */
+      uint16_t tmp = pay.w[a];
+      pay.w[a] = pay.w[z];
+      pay.w[z] = tmp;
+    }
+    if (pay.n > 0xFFFFFFFFull) {
+      rc = O_ERR_UNSUPPORTED;
+      goto done_cumul;
+    }
+    for (uint32_t l = 0; l < ORA_J; l++) {
+      states[tile * ORA_J + l] = xs[l];
+      state_bits += log2((double)xs[l] / (double)ORA_L);
+    }
+    offsets[tile + 1] = (uint32_t)pay.n;
+  }
+
+  /* serialise */
+  {
+    uint64_t tb = tables_bytes(T);
+    uint64_t off_tables = ORA_HEADER_BYTES;
+    uint64_t off_sigma = off_tables + tb;
+    uint64_t off_delta = off_sigma + 4ull * (uint64_t)R;
+    uint64_t off_states = off_delta + (cont ? 4ull * (uint64_t)R : 0);
+    uint64_t off_offsets = off_states + 4ull * ORA_J * n_tiles;
+    uint64_t off_payload = off_offsets + 4ull * (n_tiles + 1);
+    uint64_t total = off_payload + ((2ull * pay.n + 3) & ~3ull);
+    blob = (uint8_t*)calloc((size_t)total, 1);
+    if (!blob) {
+      rc = O_ERR_NOMEM;
+      goto done_cumul;
+    }
+    put32(blob + 0, ORA_MAGIC);
+    put32(blob + 4, ORA_VERSION);
+    put32(blob + 8, (uint32_t)R);
+    put32(blob + 12, (uint32_t)C);
+    put32(blob + 16, (uint32_t)b);
+    put32(blob + 20, V);
+    put32(blob + 24, (uint32_t)n_tiles);
+    put32(blob + 28, (uint32_t)cont);
+    put32(blob + 32, (uint32_t)tb);
+    put32(blob + 36, (uint32_t)pay.n);
+    put64(blob + 40, total);
+    uint8_t* p = blob + off_tables;
+    uint16_t f0 = (uint16_t)T[0].f[0], f1 = (uint16_t)T[0].f[1];
+    memcpy(p, &f0, 2);
+    memcpy(p + 2, &f1, 2);
+    p += 4;
+    for (int t = 1; t < ORA_NTAB; t++) {
+      put32(p, (uint32_t)T[t].min);
+      put32(p + 4, (uint32_t)T[t].A);
+      for (int32_t z = 0; z < T[t].A; z++) {
+        uint16_t fz = (uint16_t)T[t].f[z];
+        memcpy(p + 8 + 2 * z, &fz, 2);
+      }
+      p += 8 + ((2ull * (uint64_t)T[t].A + 3) & ~3ull);
+    }
+    memcpy(blob + off_sigma, sigma, 4ull * (uint64_t)R);
+    if (cont) memcpy(blob + off_delta, delta, 4ull * (uint64_t)R);
+    memcpy(blob + off_states, states, 4ull * ORA_J * n_tiles);
+    memcpy(blob + off_offsets, offsets, 4ull * (n_tiles + 1));
+    if (pay.n) memcpy(blob + off_payload, pay.w, 2ull * pay.n);
+
+    /* statistics */
+    double cce_full = tables_code_length(T, b);
+    double err_c = 0, ref_c = 0, err_o = 0, ref_o = 0;
+    int rdt = cont == O_CONT_FP8 ? O_FP8 : cont == O_CONT_INT8 ? O_INT8 : dtype;
+    for (int64_t r = 0; r < R; r++) {
+      for (int64_t j = 0; j < C; j++) {
+        double y = (double)(float)((double)sigma[r] * (two_p[r * C + j] / 2.0));
+        double wh;
+        switch (rdt) {
+          case O_BF16: wh = snap_bf16(y); break;
+          case O_FP16: wh = snap_fp16(y); break;
+          case O_FP8: wh = snap_e4m3(y); break;
+          case O_INT8: {
+            wh = nearbyint(y);
+            if (wh > 127) wh = 127;
+            if (wh < -128) wh = -128;
+            break;
+          }
+          default: wh = y;
+        }
+        double xc = x[r * C + j];
+        err_c += (wh - xc) * (wh - xc);
+        ref_c += xc * xc;
+        double wo = (double)(float)input_value(w, dtype, r * C + j);
+        double who = cont ? wh * (double)delta[r] : wh;
+        err_o += (who - wo) * (who - wo);
+        ref_o += wo * wo;
+      }
+    }
+    st[ST_SCALE] = s;
+    st[ST_B] = b;
+    st[ST_RHAT_SUB] = rhat;
+    st[ST_R_STORED] = 8.0 * (double)total / (double)N;
+    st[ST_BYTES] = (double)total;
+    st[ST_PAYLOAD_BITS] = 16.0 * (double)pay.n;
+    st[ST_CCE_FULL] = cce_full;
+    st[ST_N_TILES] = (double)n_tiles;
+    st[ST_MAX_A] = tables_max_A(T);
+    st[ST_EREL_CODED] = ref_c > 0 ? sqrt(err_c / ref_c) : 0;
+    st[ST_EREL_ORIG] = ref_o > 0 ? sqrt(err_o / ref_o) : 0;
+    st[ST_MEAN_STATE_BITS] = state_bits / (double)(ORA_J * n_tiles);
+    st[ST_TABLE_BYTES] = (double)tb;
+    st[ST_SAMPLE_ROWS] = (double)nsr;
+    *out_blob = blob;
+    *out_size = total;
+    blob = NULL;
+  }
+
+done_cumul:
+  for (int t = 0; t < ORA_NTAB; t++) free(cumul[t]);
+done:
+  free(x);
+  free(delta);
+  free(mu);
+  free(rows);
+  free(all_rows);
+  free(fields);
+  free(two_p);
+  free(sfields);
+  free(sigma);
+  free(states);
+  free(offsets);
+  free(pay.w);
+  free(blob);
+  tables_free(T);
+  tables_free(TS);
+  return rc;
+}
+
+void ora_blob_free(uint8_t* blob) { free(blob); }
+
+/* Test hook: 2p of every vector at a given scale s, with the same input
+ * conversion, container route and row normalisation as the encoder. */
+int ora_quantize(const void* w, int dtype, int64_t R, int64_t C, int container, double s,
+                 int32_t* two_p, float* coded_values, double* mu_out) {
+  if (!w || R <= 0 || C <= 0 || C % 8 || !(s > 0)) return O_ERR_ARG;
+  int64_t N = R * C;
+  float* x = (float*)malloc((size_t)N * sizeof(float));
+  float* delta = (float*)calloc((size_t)R, sizeof(float));
+  double* mu = (double*)malloc((size_t)R * sizeof(double));
+  int64_t* rows = (int64_t*)malloc((size_t)R * sizeof(int64_t));
+  int32_t* fields = (int32_t*)malloc((size_t)(N / 8) * 9 * sizeof(int32_t));
+  int rc = O_OK;
+  if (!x || !delta || !mu || !rows || !fields) {
+    rc = O_ERR_NOMEM;
+    goto out;
+  }
+  rc = prepare_values(w, dtype, R, C, container, x, delta);
+  if (rc) goto out;
+  for (int64_t r = 0; r < R; r++) {
+    mu[r] = row_rms(x + r * C, C);
+    rows[r] = r;
+    if (mu_out) mu_out[r] = mu[r];
+  }
+  quantize_rows(x, mu, C, rows, R, s, fields, two_p);
+  if (coded_values) memcpy(coded_values, x, (size_t)N * sizeof(float));
+out:
+  free(x);
+  free(delta);
+  free(mu);
+  free(rows);
+  free(fields);
+  return rc;
+}
+
+/* Test hook: sampled rows chosen for an R x C tensor. */
+int64_t ora_sample_rows(int64_t R, int64_t C, int64_t sample_vectors, int64_t* rows) {
+  if (R <= 0 || C <= 0 || C % 8) return O_ERR_ARG;
+  return choose_sample_rows(R, C, sample_vectors, rows);
+}
+
+/* ========================================================================= */
+/* Decoder [3.7, eq. rans_decode, eq. point_inverse, eq. recon; App. C.3].    */
+/* ========================================================================= */
+
+typedef struct {
+  uint32_t R, C, b, V, n_tiles, container, tb, n_words;
+  uint64_t total;
+  const uint8_t* tables;
+  const float* sigma;
+  const float* delta;
+  const uint32_t* states;
+  const uint32_t* offsets;
+  const uint16_t* payload;
+} blobview;
+
+static int parse_blob(const uint8_t* blob, uint64_t n, blobview* bv, table_t* T) {
+  if (!blob || n < ORA_HEADER_BYTES) return O_ERR_FORMAT;
+  if (get32(blob) != ORA_MAGIC || get32(blob + 4) != ORA_VERSION) return O_ERR_FORMAT;
+  bv->R = get32(blob + 8);
+  bv->C = get32(blob + 12);
+  bv->b = get32(blob + 16);
+  bv->V = get32(blob + 20);
+  bv->n_tiles = get32(blob + 24);
+  bv->container = get32(blob + 28);
+  bv->tb = get32(blob + 32);
+  bv->n_words = get32(blob + 36);
+  bv->total = get64(blob + 40);
+  if (bv->total != n || bv->R == 0 || bv->C == 0 || bv->C % 8 || bv->b < 9 || bv->b > 15 ||
+      bv->V == 0 || bv->container > 2)
+    return O_ERR_FORMAT;
+  uint64_t nvec = (uint64_t)bv->R * bv->C / 8;
+  if (bv->n_tiles != n_tiles_of(nvec, bv->V)) return O_ERR_FORMAT;
+  uint64_t off_tables = ORA_HEADER_BYTES;
+  uint64_t off_sigma = off_tables + bv->tb;
+  uint64_t off_delta = off_sigma + 4ull * bv->R;
+  uint64_t off_states = off_delta + (bv->container ? 4ull * bv->R : 0);
+  uint64_t off_offsets = off_states + 4ull * ORA_J * bv->n_tiles;
+  uint64_t off_payload = off_offsets + 4ull * (bv->n_tiles + 1);
+  if (off_payload + ((2ull * bv->n_words + 3) & ~3ull) != n) return O_ERR_FORMAT;
+  bv->tables = blob + off_tables;
+  bv->sigma = (const float*)(blob + off_sigma);
+  bv->delta = bv->container ? (const float*)(blob + off_delta) : NULL;
+  bv->states = (const uint32_t*)(blob + off_states);
+  bv->offsets = (const uint32_t*)(blob + off_offsets);
+  bv->payload = (const uint16_t*)(blob + off_payload);
+  /* tables */
+  const uint32_t M = 1u << bv->b;
+  const uint8_t* p = bv->tables;
+  const uint8_t* end = bv->tables + bv->tb;
+  if (p + 4 > end) return O_ERR_FORMAT;
+  uint16_t f0, f1;
+  memcpy(&f0, p, 2);
+  memcpy(&f1, p + 2, 2);
+  if ((uint32_t)f0 + f1 != M) return O_ERR_FORMAT;
+  T[0].min = 0;
+  T[0].A = 2;
+  T[0].f = (uint32_t*)malloc(2 * sizeof(uint32_t));
+  if (!T[0].f) return O_ERR_NOMEM;
+  T[0].f[0] = f0;
+  T[0].f[1] = f1;
+  p += 4;
+  for (int t = 1; t < ORA_NTAB; t++) {
+    if (p + 8 > end) return O_ERR_FORMAT;
+    T[t].min = (int32_t)get32(p);
+    uint32_t A = get32(p + 4);
+    if (A > M) return O_ERR_FORMAT;
+    T[t].A = (int32_t)A;
+    uint64_t sz = 8 + ((2ull * A + 3) & ~3ull);
+    if (p + sz > end) return O_ERR_FORMAT;
+    T[t].f = (uint32_t*)calloc(A ? A : 1, sizeof(uint32_t));
+    if (!T[t].f) return O_ERR_NOMEM;
+    uint64_t sum = 0;
+    for (uint32_t z = 0; z < A; z++) {
+      uint16_t fz;
+      memcpy(&fz, p + 8 + 2 * z, 2);
+      T[t].f[z] = fz;
+      sum += fz;
+    }
+    if (A && sum != M) return O_ERR_FORMAT;
+    /* a table that can be selected (its coset has non-zero frequency) must exist */
+    int c = (t - 1) / 8;
+    if (!A && T[0].f[c]) return O_ERR_FORMAT;
+    p += sz;
+  }
+  if (p != end) return O_ERR_FORMAT;
+  if (bv->offsets[0] != 0 || bv->offsets[bv->n_tiles] != bv->n_words) return O_ERR_FORMAT;
+  for (uint32_t t = 0; t < bv->n_tiles; t++)
+    if (bv->offsets[t] > bv->offsets[t + 1]) return O_ERR_FORMAT;
+  return O_OK;
+}
+
+/* Header information for tests: R, C, b, V, n_tiles, container, table bytes,
+ * payload words, total bytes. */
+int ora_blob_header(const uint8_t* blob, uint64_t n, uint64_t* out9) {
+  blobview bv;
+  table_t T[ORA_NTAB];
+  memset(T, 0, sizeof T);
+  int rc = parse_blob(blob, n, &bv, T);
+  for (int t = 0; t < ORA_NTAB; t++) free(T[t].f);
+  if (rc) return rc;
+  out9[0] = bv.R;
+  out9[1] = bv.C;
+  out9[2] = bv.b;
+  out9[3] = bv.V;
+  out9[4] = bv.n_tiles;
+  out9[5] = bv.container;
+  out9[6] = bv.tb;
+  out9[7] = bv.n_words;
+  out9[8] = bv.total;
+  return O_OK;
+}
+
+static void write_output(void* out, int dtype, uint64_t e, float y) {
+  double v = (double)y;
+  switch (dtype) {
+    case O_BF16: ((uint16_t*)out)[e] = bf16_bits(snap_bf16(v)); break;
+    case O_FP16: ((uint16_t*)out)[e] = fp16_bits(snap_fp16(v)); break;
+    case O_FP32: ((float*)out)[e] = y; break;
+    case O_FP8: ((uint8_t*)out)[e] = e4m3_bits(snap_e4m3(v)); break;
+    case O_INT8: {
+      double r = nearbyint(v);
+      if (r > 127) r = 127;
+      if (r < -128) r = -128;
+      ((int8_t*)out)[e] = (int8_t)r;
+      break;
+    }
+  }
+}
+
+/* Decode tiles [t0, t1) of a blob into a full R x C output (row-major, only
+ * the elements of those tiles are written).  dequant (optional) receives
+ * delta_r for every row whose first vector lies in a decoded tile.  Returns
+ * O_ERR_CORRUPT if a terminal state differs from 2^15 or a tile does not end
+ * exactly at its successor's offset. */
+int ora_decode(const uint8_t* blob, uint64_t n, int out_dtype, void* out, float* dequant,
+               uint32_t t0, uint32_t t1) {
+  blobview bv;
+  table_t T[ORA_NTAB];
+  memset(T, 0, sizeof T);
+  uint32_t* cumul[ORA_NTAB];
+  int32_t* slot_sym[ORA_NTAB];
+  memset(cumul, 0, sizeof cumul);
+  memset(slot_sym, 0, sizeof slot_sym);
+  int rc = parse_blob(blob, n, &bv, T);
+  if (rc) goto out;
+  if (out_dtype != O_BF16 && out_dtype != O_FP16 && out_dtype != O_FP32 && out_dtype != O_FP8 &&
+      out_dtype != O_INT8 && out_dtype != O_COORD2) {
+    rc = O_ERR_ARG;
+    goto out;
+  }
+  if (t0 > t1 || t1 > bv.n_tiles || !out) {
+    rc = O_ERR_ARG;
+    goto out;
+  }
+  const uint32_t b = bv.b, M = 1u << b;
+  /* slot -> symbol: the symbol s with F_s <= u < F_s + f_s */
+  for (int t = 0; t < ORA_NTAB; t++) {
+    cumul[t] = (uint32_t*)calloc((size_t)T[t].A + 1, sizeof(uint32_t));
+    slot_sym[t] = (int32_t*)malloc(M * sizeof(int32_t));
+    if (!cumul[t] || !slot_sym[t]) {
+      rc = O_ERR_NOMEM;
+      goto out;
+    }
+    for (int32_t z = 0; z < T[t].A; z++) cumul[t][z + 1] = cumul[t][z] + T[t].f[z];
+    for (uint32_t u = 0; u < M; u++) slot_sym[t][u] = -1;
+    for (int32_t z = 0; z < T[t].A; z++)
+      for (uint32_t u = cumul[t][z]; u < cumul[t][z + 1]; u++) slot_sym[t][u] = z;
+  }
+  const uint64_t nvec = (uint64_t)bv.R * bv.C / 8, cvec = bv.C / 8;
+  for (uint32_t tile = t0; tile < t1; tile++) {
+    uint64_t v0 = (uint64_t)tile * bv.V;
+    uint64_t nv = nvec - v0 < bv.V ? nvec - v0 : bv.V;
+    uint64_t steps = 9 * ((nv + ORA_J - 1) / ORA_J);
+    uint32_t xs[ORA_J];
+    int32_t f9[ORA_J][9];
+    for (uint32_t l = 0; l < ORA_J; l++) xs[l] = bv.states[(uint64_t)tile * ORA_J + l];
+    uint64_t ptr = bv.offsets[tile], pend = bv.offsets[tile + 1];
+    for (uint64_t step = 0; step < steps; step++) {
+      uint64_t k = step / 9;
+      int i = (int)(step % 9);
+      for (uint32_t l = 0; l < ORA_J; l++) {
+        uint64_t li = l + ORA_J * k;
+        if (li >= nv) continue;
+        int t = i == 0 ? 0 : table_of(i, f9[l][0]);
+        if (xs[l] < ORA_L || xs[l] >= 0x80000000u || T[t].A == 0) {
+          rc = O_ERR_CORRUPT;
+          goto out;
+        }
+        uint32_t u = xs[l] & (M - 1);
+        int32_t z = slot_sym[t][u];
+        if (z < 0) {
+          rc = O_ERR_CORRUPT;
+          goto out;
+        }
+        uint32_t f = T[t].f[z], F = cumul[t][z];
+        uint32_t xn = f * (xs[l] >> b) + u - F;
+        if (xn < ORA_L) {
+          if (ptr >= pend) {
+            rc = O_ERR_CORRUPT;
+            goto out;
+          }
+          xn = (xn << 16) | bv.payload[ptr++];
+        }
+        xs[l] = xn;
+        f9[l][i] = (i == 0) ? z : z + T[t].min;
+        if (i == 8) { /* whole vector recovered: inverse field map and reconstruction */
+          int32_t tp[8];
+          fields_to_point(f9[l], tp);
+          uint64_t v = v0 + li;
+          uint64_t r = v / cvec;
+          for (int j = 0; j < 8; j++) {
+            uint64_t e = 8 * v + j;
+            if (out_dtype == O_COORD2) {
+              ((int32_t*)out)[e] = tp[j];
+            } else {
+              float y = (float)((double)bv.sigma[r] * (tp[j] / 2.0)); /* FP32 product */
+              write_output(out, out_dtype, e, y);
+            }
+          }
+        }
+      }
+    }
+    for (uint32_t l = 0; l < ORA_J; l++)
+      if (xs[l] != ORA_L) {
+        rc = O_ERR_CORRUPT;
+        goto out;
+      }
+    if (ptr != pend) {
+      rc = O_ERR_CORRUPT;
+      goto out;
+    }
+    if (dequant && bv.container) {
+      for (uint64_t r = (v0 + cvec - 1) / cvec; r * cvec < v0 + nv; r++) dequant[r] = bv.delta[r];
+    }
+  }
+out:
+  for (int t = 0; t < ORA_NTAB; t++) {
+    free(T[t].f);
+    free(cumul[t]);
+    free(slot_sym[t]);
+  }
+  return rc;
+}
+
+/* Test hook: the stored-size estimate and code length of a given field set
+ * (9 int32 per vector) at precision b, as the encoder evaluates it. */
+int ora_estimate(const int32_t* fields, int64_t nvec, int64_t rows, int32_t b, int32_t V,
+                 double kappa, int32_t container, double* out3) {
+  table_t T[ORA_NTAB];
+  memset(T, 0, sizeof T);
+  int rc = tables_count(fields, nvec, T);
+  if (!rc && tables_max_A(T) > (1 << b)) rc = O_ERR_ARG;
+  if (!rc) rc = tables_normalize(T, b);
+  if (!rc) {
+    double cce = tables_code_length(T, b);
+    uint64_t nt = n_tiles_of((uint64_t)nvec, (uint32_t)V);
+    out3[0] = cce;
+    out3[1] = estimate_bits(cce, nt, kappa, T, (uint64_t)rows, container);
+    out3[2] = (double)tables_bytes(T);
+  }
+  tables_free(T);
+  return rc;
+}
+
+/* Test hook: values of output bit patterns (BF16, FP16, FP32, FP8 e4m3fn,
+ * INT8, or 2p as int32) as doubles. */
+int ora_values(const void* bits, int64_t n, int dtype, double* out) {
+  for (int64_t i = 0; i < n; i++) {
+    switch (dtype) {
+      case O_BF16: out[i] = bf16_value(((const uint16_t*)bits)[i]); break;
+      case O_FP16: out[i] = fp16_value(((const uint16_t*)bits)[i]); break;
+      case O_FP32: out[i] = ((const float*)bits)[i]; break;
+      case O_FP8: out[i] = e4m3_value(((const uint8_t*)bits)[i]); break;
+      case O_INT8: out[i] = ((const int8_t*)bits)[i]; break;
+      case O_COORD2: out[i] = ((const int32_t*)bits)[i] / 2.0; break;
+      default: return O_ERR_ARG;
+    }
+  }
+  return O_OK;
+}
