@@ -1,0 +1,207 @@
+"""Decode-throughput benchmark of the fused EntroPack decode on one MI355X.
+
+Default workload (the 27B-class LLM MLP set): gate and up 17408 x 5120 and
+down 5120 x 17408 BF16 weights (seeded synthetic, Gaussian rows with
+lognormal std and 0.05 % x8 outliers), each converted to the row-scaled FP8
+e4m3 container and EntroPack-coded at 4.0 bits/weight with 4096-weight tiles
+by the library's CPU encoder.  One step decodes all three tensors to FP8 e4m3
+plus per-row dequant scales in a single ep_decode_layers launch, with the
+blobs already resident in HBM.
+
+Reported: decoded weights/s (value), achieved GB/s of the decode kernel
+against the 8 TB/s HBM3E peak (algorithmic bytes = every compressed byte read
++ every weight and dequant byte written), and the CPU oracle decoder's
+throughput on the same blobs on this host's cores.
+
+Other workloads (--workload): attn_fp16 (3072 x 3072 at 3.0 bpp to FP16),
+dit_stack (30 diffusion-transformer blocks, 180 layers at 2.5 bpp to BF16 in one
+launch), mlp_down_int8 (the MLP down projection in the INT8 container at
+6.0 bpp to INT8).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decoded weights/s and achieved HBM GB/s (% roofline), 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def workload(name, E, W, threads):
+    """Returns (description dict, [(label, blob, out_dtype)])."""
+    if name == "mlp_fp8":
+        d = W.llm_mlp()
+        items = []
+        for n in ("gate", "up", "down"):
+            b, st = E.encode(d[n], 4.0, container=E.CONT_FP8_ROW, nthreads=threads)
+            log(f"encoded {n}: {b.size} B, {st['rate_stored']:.4f} bpp")
+            items.append((n, b, E.FP8_E4M3))
+        desc = {"workload": "27B-class LLM MLP set: gate+up 17408x5120, down 5120x17408; FP8-e4m3 "
+                            "row container coded at 4.0 bpp, 4096-weight tiles; decoded to FP8 e4m3 "
+                            "+ per-row dequant in one launch",
+                "tensors": 3, "target_bpp": 4.0, "tile_weights": 4096, "out": "fp8_e4m3+dequant"}
+    elif name == "attn_fp16":
+        b, st = E.encode(W.attention_projection(), 3.0, nthreads=threads)
+        items = [("attn", b, E.FP16)]
+        desc = {"workload": "attention projection 3072x3072 at 3.0 bpp, decoded to FP16",
+                "tensors": 1, "target_bpp": 3.0, "tile_weights": 4096, "out": "fp16"}
+    elif name == "mlp_down_int8":
+        d = W.llm_mlp()
+        b, st = E.encode(d["down"], 6.0, container=E.CONT_INT8_ROW, nthreads=threads)
+        items = [("down", b, E.INT8)]
+        desc = {"workload": "MLP down 5120x17408, INT8 row container at 6.0 bpp, decoded to INT8 "
+                            "+ per-row dequant", "tensors": 1, "target_bpp": 6.0,
+                "tile_weights": 4096, "out": "int8+dequant"}
+    elif name == "dit_stack":
+        items = []
+        for blk in range(30):
+            for lname, w in W.dit_block(blk):
+                b, st = E.encode(w, 2.5, nthreads=threads)
+                items.append((lname, b, E.BF16))
+            log(f"encoded block {blk}")
+        desc = {"workload": "diffusion-transformer stack: 30 blocks x (4 x 3840x3840, 10240x3840, "
+                            "3840x10240) at 2.5 bpp, 180 layers decoded to BF16 in one launch",
+                "tensors": 180, "target_bpp": 2.5, "tile_weights": 4096, "out": "bf16"}
+    else:
+        raise SystemExit(f"unknown workload {name}")
+    return desc, items
+
+
+def cpu_baseline(items, threads):
+    """The oracle decoder on the same blobs, tiles split over `threads` host threads."""
+    import numpy as np
+    from oracle import oracle as O
+    ocode = {1: O.BF16, 2: O.FP16, 3: O.FP32, 4: O.FP8, 5: O.INT8}
+    jobs = []
+    outs = []
+    weights = 0
+    for label, blob, dt in items:
+        h = O.header(blob)
+        out = np.zeros((h["rows"], h["cols"]), dtype=O.OUT_NPTYPE[ocode[dt]])
+        dq = np.zeros(h["rows"], dtype=np.float32)
+        outs.append((out, dq))
+        weights += h["rows"] * h["cols"]
+        n = h["n_tiles"]
+        parts = max(1, min(threads, n))
+        for p in range(parts):
+            jobs.append((blob, ocode[dt], out, dq, n * p // parts, n * (p + 1) // parts))
+
+    def run(j):
+        blob, code, out, dq, t0, t1 = j
+        O.decode(blob, code, t0, t1, out=out, dequant=dq)
+
+    t = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(run, jobs))
+    sec = time.perf_counter() - t
+    return {"value": weights / sec, "unit": "weights/s", "cores": threads, "kind": "oracle",
+            "sample": f"all {len(items)} tensors ({weights} weights) decoded once by the plain C "
+                      f"oracle, tiles split over {threads} threads", "seconds": round(sec, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mlp_fp8")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the decode shards by tile range with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_34185_amd import entropack as E
+    from paper_2609_34185_amd import workloads as W
+
+    E.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    threads = min(16, len(os.sched_getaffinity(0)))
+
+    t = time.perf_counter()
+    desc, items = workload(args.workload, E, W, threads)
+    log(f"workload ready in {time.perf_counter() - t:.1f} s")
+
+    layers, keep = [], []
+    weights, algo_bytes = 0, 0
+    for label, blob, dt in items:
+        info = E.blob_info(blob)
+        d_blob = E.to_device(blob, dev)
+        out = torch.empty((info.rows, info.cols), dtype=E.torch_dtype(dt), device=dev)
+        dq = torch.empty(info.rows, dtype=torch.float32, device=dev) if info.container else None
+        keep += [d_blob, out, dq]
+        layers.append((info, d_blob.data_ptr(), out.data_ptr(), dq.data_ptr() if dq is not None else 0, dt))
+        weights += info.rows * info.cols
+        algo_bytes += blob.size + info.rows * info.cols * E.ITEMSIZE[dt] + (4 * info.rows if info.container else 0)
+    stored_bpp = 8.0 * sum(b.size for _, b, _ in items) / weights
+    ws = max(1, E.decode_layers_workspace(len(layers)))
+    d_ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        E.decode_layers(layers, d_ws.data_ptr(), ws, status.data_ptr(), stream.cuda_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = start.elapsed_time(end) / args.steps
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+
+    sec = ms / 1e3
+    gbps = algo_bytes / sec / 1e9
+    line = {
+        "metric": METRIC,
+        "value": weights / sec,
+        "unit": "weights/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": dict(desc, weights=weights, stored_bpp=round(stored_bpp, 4),
+                       bytes_per_step=algo_bytes, wall_s=round(wall, 4)),
+        "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": gbps / HBM_PEAK_GBPS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle decoder")
+        line["cpu_baseline"] = cpu_baseline(items, threads)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

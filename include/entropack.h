@@ -1,0 +1,212 @@
+/*
+ * entropack.h -- C ABI of the MI355X EntroPack library (libentropack.so).
+ *
+ * EntroPack (arXiv 2609.34185) stores a weight matrix W (R x C, C % 8 == 0)
+ * as row-normalised E8 lattice points written as integer fields
+ * (c, z1..z7, m) and coded with 32-state interleaved rANS in independently
+ * decodable tiles (Sections 3.2-3.6, Appendix C.3).  This library provides
+ *   - a CPU encoder (ep_encode_cpu),
+ *   - validation/inspection of an encoded blob on the host (ep_blob_info),
+ *   - fused GPU decode on gfx950: rANS symbol decode with the coset-conditional
+ *     tables, field inverse, row rescale and dtype snap, with no intermediate
+ *     symbol tensor (ep_decode_tiles, ep_decode_layers; Section 3.7),
+ *   - an INT8 MFMA matrix product for decode-then-GEMM (ep_gemm_i8_nt).
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: EP_OK (0) or a negative ep_status.  ep_last_error() gives a
+ *     thread-local message for the last failing call on the calling thread.
+ *     No C++ exception crosses this ABI.
+ *   - "d_" pointers are device pointers (hipMalloc'd or equivalent) on the
+ *     current HIP device; all other pointers are host pointers.
+ *   - GPU calls are asynchronous on the given hipStream_t (passed as void*,
+ *     NULL = default stream).  They allocate no device memory and never
+ *     synchronise; the caller owns every buffer.
+ *   - Outputs must not alias the blob or each other.
+ *
+ * Stored representation (all little-endian; every section starts on a 4-byte
+ * boundary; offsets in bytes from the start of the blob):
+ *   header   48 B : u32 magic "EPK1", u32 version 1, u32 R, u32 C, u32 b,
+ *                   u32 V (vectors per tile), u32 n_tiles, u32 container,
+ *                   u32 table_bytes, u32 payload_words, u64 total_bytes
+ *   tables        : u16 f0, u16 f1 (coset frequencies), then for coset
+ *                   c = 0,1 and field i = 1..8 (z1..z7, m):
+ *                   i32 min, u32 A, u16 f[A], padded to 4 B
+ *   sigma         : f32[R]   row reconstruction scales (Section 3.5)
+ *   delta         : f32[R]   container dequant scales (containers only)
+ *   states        : u32[n_tiles][32] terminal rANS states (Appendix C.3)
+ *   offsets       : u32[n_tiles + 1] payload offsets in 16-bit words
+ *   payload       : u16[payload_words], padded to 4 B
+ * Tile t holds vectors [tV, min((t+1)V, R*C/8)) (vector v = elements
+ * 8v..8v+7 of the row-major matrix); tile-local vector i is coded by lane
+ * i mod 32; each lane codes its vectors in order as [c, z1..z7, m]; the
+ * decoder consumes words in (step ascending, lane ascending) order.
+ */
+#ifndef ENTROPACK_H
+#define ENTROPACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status, dtypes, containers ----------------------------------------- */
+enum ep_status {
+  EP_OK = 0,
+  EP_ERR_ARG = -1,         /* invalid argument (shape, pointer, range, dtype) */
+  EP_ERR_FORMAT = -2,      /* blob fails validation */
+  EP_ERR_UNSUPPORTED = -3, /* valid request this build does not handle */
+  EP_ERR_NOMEM = -4,       /* host allocation failed (encoder only) */
+  EP_ERR_HIP = -5,         /* a HIP runtime call failed (launch error) */
+  EP_ERR_CORRUPT = -6      /* decoded stream inconsistent (terminal state/offset) */
+};
+
+enum ep_dtype {
+  EP_BF16 = 1,             /* round to nearest even, saturating at +-max finite */
+  EP_FP16 = 2,             /* round to nearest even incl. subnormals, saturating at +-65504 */
+  EP_FP32 = 3,             /* the FP32 product itself */
+  EP_FP8_E4M3 = 4,         /* OCP e4m3fn, nearest even incl. subnormals, saturating at +-448 */
+  EP_INT8 = 5,             /* clamp(round-half-even(y), -128, 127) */
+  EP_COORD2_I32 = 100      /* debug: the doubled lattice coordinates 2p as int32 */
+};
+
+enum ep_container {
+  EP_CONT_DIRECT = 0,      /* the input values are coded directly */
+  EP_CONT_FP8_ROW = 1,     /* row-scaled FP8 e4m3fn container (Appendix A.6, B.1) */
+  EP_CONT_INT8_ROW = 2     /* row-scaled symmetric INT8 container (Appendix B.1) */
+};
+
+/* Bits of *d_status set by the decode kernels (OR-ed; the caller zeroes it). */
+enum ep_status_bits {
+  EP_STATUS_PAYLOAD_OVERRUN = 1,  /* a tile tried to read past its payload window */
+  EP_STATUS_BAD_FINAL_STATE = 2,  /* a terminal state was not 2^15 after decoding */
+  EP_STATUS_BAD_END_OFFSET = 4    /* a tile ended before its successor's offset */
+};
+
+/* ---- encoder ------------------------------------------------------------- */
+typedef struct {
+  double target_bpp;        /* requested stored rate R_tgt in bits per weight (> 0) */
+  int32_t tile_vectors;     /* V: vectors per tile (>= 1); 512 = 4096 weights */
+  int32_t prob_bits;        /* b0: 0 = 11 if target <= 7 else 12 (App. C.1); else 9..15 */
+  int32_t search_steps;     /* geometric bisection steps I_s (App. C.1: 12) */
+  int32_t container;        /* ep_container */
+  double scale_lo, scale_hi;/* initial bracket of s (App. C.1: 1e-3, 8) */
+  int64_t sample_vectors;   /* nominal sample size in 8-vectors (App. C.1: 2^18) */
+  double state_credit_bits; /* bits credited per terminal state in eq. estimate (8) */
+  int32_t nthreads;         /* worker threads, 0 = hardware concurrency */
+  int32_t reserved;
+} ep_encode_params;
+
+typedef struct {
+  uint8_t* data;            /* malloc'd by ep_encode_cpu; release with ep_blob_free */
+  uint64_t size;
+} ep_blob;
+
+typedef struct {
+  double scale;             /* selected quantisation scale s */
+  double rate_estimate_sample; /* R_hat_sub at the last search step */
+  double rate_stored;       /* R_stored = 8 B_stored / N (eq. objective) */
+  double code_length_bits;  /* C_CE of the final tables on the full tensor */
+  double erel_coded;        /* E_rel vs the coded values (container units for containers) */
+  double erel_original;     /* E_rel vs the original input */
+  double mean_state_bits;   /* mean log2(x_T / 2^15) over terminal states */
+  uint64_t bytes;           /* blob size */
+  uint64_t payload_bits;
+  uint32_t prob_bits;       /* final b */
+  uint32_t n_tiles;
+  uint32_t max_alphabet;    /* largest field-table index range */
+  uint32_t sample_rows;
+  uint32_t escalations;     /* precision increases */
+  uint32_t coarsenings;     /* coarsening steps after b = 15 */
+} ep_encode_stats;
+
+/* Default parameters of the paper (App. C.1) with V = 512 and 8 credited bits. */
+void ep_encode_params_default(ep_encode_params* p);
+
+/* Encode W (R x C row-major; w_dtype EP_BF16 / EP_FP16 bit patterns or EP_FP32)
+ * at p->target_bpp (Section 3.1 objective; Alg. rate selection in 3.4; refit
+ * 3.5; rANS 3.6).  On success out->data holds the blob (caller frees with
+ * ep_blob_free) and *stats (nullable) is filled.  The output is independent of
+ * nthreads.  Errors: EP_ERR_ARG (C % 8 != 0, R or C <= 0, non-finite input,
+ * target <= 0, bad parameters), EP_ERR_NOMEM. */
+int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
+                  const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats);
+void ep_blob_free(ep_blob* blob);
+
+/* ---- inspection ---------------------------------------------------------- */
+typedef struct {
+  uint32_t rows, cols, prob_bits, tile_vectors, n_tiles, container;
+  uint32_t table_bytes, payload_words;
+  uint64_t total_bytes;
+  uint64_t off_tables, off_sigma, off_delta, off_states, off_offsets, off_payload;
+  /* derived by ep_blob_info for kernel selection */
+  uint32_t max_alphabet;     /* largest field-table index range A */
+  int32_t coord2_min;        /* smallest doubled coordinate value any table can produce */
+  int32_t coord2_max;        /* largest one */
+  float max_abs_weight;      /* upper bound of |fp32(sigma_r * p)| over the tensor */
+  uint32_t path;             /* decode kernel family chosen for this tensor (internal) */
+  uint32_t sum_alphabet;     /* sum of the field tables' index ranges */
+  uint32_t table_off[16];    /* byte offset of field table 1 + 8c + (i-1) in the blob */
+  int32_t table_min[16];     /* its min value */
+  uint32_t table_A[16];      /* its index range */
+  uint32_t coset_f0, coset_f1;
+} ep_tensor_info;
+
+/* Validate a host copy of a blob (n bytes) and fill *info: magic/version,
+ * section bounds against n, n_tiles = ceil(R*C/8 / V), monotone offsets
+ * ending at payload_words, every field table's frequencies summing to 2^b
+ * with A <= 2^b, coset frequencies summing to 2^b, 9 <= b <= 15, finite
+ * scales.  The device copy of the blob must be byte-identical.
+ * Errors: EP_ERR_ARG (NULL), EP_ERR_FORMAT. */
+int ep_blob_info(const void* host_blob, uint64_t n, ep_tensor_info* info);
+
+/* ---- GPU decode ---------------------------------------------------------- */
+/* Decode tiles [tile_begin, tile_end) of one tensor (Section 3.7: eq.
+ * rans_decode, eq. point_inverse, eq. recon).  d_out receives R x C
+ * elements of out_dtype (row-major); only the elements of the given tiles are
+ * written.  For containers, d_dequant (nullable) receives delta_r for each row
+ * whose first vector lies in a decoded tile.  d_status (nullable, device
+ * int32, zeroed by the caller) receives ep_status_bits for corrupt streams;
+ * the kernels never read or write outside the blob's tile windows and the
+ * output.  Errors (host side, before launch): EP_ERR_ARG, EP_ERR_UNSUPPORTED,
+ * EP_ERR_HIP. */
+int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtype, void* d_out,
+                    float* d_dequant, uint32_t tile_begin, uint32_t tile_end, int32_t* d_status,
+                    void* hip_stream);
+
+/* One layer of a stack decode. */
+typedef struct {
+  ep_tensor_info info;       /* from ep_blob_info on the host copy */
+  const void* d_blob;
+  void* d_out;
+  float* d_dequant;          /* nullable */
+  int32_t out_dtype;
+  int32_t reserved;
+} ep_layer;
+
+/* Workspace bytes ep_decode_layers needs for n layers (device memory). */
+uint64_t ep_decode_layers_workspace(int n);
+
+/* Decode n whole layers with a single kernel launch.  The per-layer
+ * descriptors are staged into d_workspace (>= ep_decode_layers_workspace(n)
+ * bytes) with one asynchronous host-to-device copy from an internal pinned
+ * host buffer; d_workspace must stay untouched until the launch completes.
+ * Errors: as ep_decode_tiles. */
+int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
+                     int32_t* d_status, void* hip_stream);
+
+/* ---- decode-then-GEMM ---------------------------------------------------- */
+/* Y[M x N] (int32, row-major) = A[M x K] (int8, row-major) * B[N x K]^T
+ * (int8, row-major: both operands K-contiguous) on MFMA, exact int32
+ * accumulation.  Requires K % 64 == 0.  Errors: EP_ERR_ARG, EP_ERR_HIP. */
+int ep_gemm_i8_nt(const int8_t* d_a, const int8_t* d_b, int32_t* d_y, int64_t m, int64_t n,
+                  int64_t k, void* hip_stream);
+
+/* ---- errors -------------------------------------------------------------- */
+const char* ep_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

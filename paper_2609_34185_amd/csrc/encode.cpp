@@ -1,0 +1,700 @@
+// CPU encoder of the MI355X EntroPack library (ep_encode_cpu).
+//
+// Implements the paper's encoding pipeline (Figure "pipeline", upper path):
+// row normalisation and nearest-E8 quantisation (Section 3.2), the integer
+// field map (eq. parity), the 17-table coset-conditioned model with b-bit
+// frequencies (Section 3.3), sampled-row rate estimation with geometric scale
+// search and precision escalation (Section 3.4, Alg. rate selection,
+// Appendix C.1), the least-squares row-scale refit (Section 3.5, eq.
+// scale_fit), and tiled 32-state interleaved rANS (Section 3.6,
+// Appendix C.3).  The byte layout is documented in include/entropack.h.
+//
+// Work is split over rows (quantisation, refit), per-thread histograms
+// (counts) and tiles (rANS); every reduction that involves rounding runs in a
+// fixed order, so the blob does not depend on the thread count.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <functional>
+#include <limits>
+#include <new>
+#include <thread>
+#include <vector>
+
+#include "../../include/entropack.h"
+#include "common.h"
+
+namespace ep {
+namespace {
+
+constexpr uint32_t kLanes = 32;        // interleaved states per tile
+constexpr uint32_t kStateLow = 1u << 15;
+constexpr double kEta = 1e-12;
+constexpr int kTables = 17;            // coset + (8 fields x 2 cosets)
+
+// ---- small parallel-for over [0, n) with static contiguous chunks ---------
+void parallel_for(int64_t n, int nthreads, const std::function<void(int64_t, int64_t, int)>& fn) {
+  if (n <= 0) return;
+  int T = (int)std::min<int64_t>(nthreads, n);
+  if (T <= 1) {
+    fn(0, n, 0);
+    return;
+  }
+  std::vector<std::thread> th;
+  th.reserve(T);
+  for (int t = 0; t < T; t++) {
+    int64_t b = n * t / T, e = n * (t + 1) / T;
+    th.emplace_back([&fn, b, e, t] { fn(b, e, t); });
+  }
+  for (auto& x : th) x.join();
+}
+
+// ---- rounding to the stored formats ---------------------------------------
+// Round-half-even of v onto a binary float format with `frac` fraction bits,
+// minimum normal exponent emin and largest finite value vmax (saturating).
+double round_to_format(double v, int frac, int emin, double vmax) {
+  if (v == 0.0) return v;
+  double mag = std::fabs(v);
+  int ex = std::ilogb(mag);                  // mag in [2^ex, 2^(ex+1))
+  if (ex < emin) ex = emin;
+  double ulp = std::ldexp(1.0, ex - frac);
+  double q = std::nearbyint(mag / ulp) * ulp;
+  if (q > vmax) q = vmax;
+  return std::signbit(v) ? -q : q;
+}
+
+double to_e4m3(double v) { return round_to_format(v, 3, -6, 448.0); }
+double to_bf16(double v) { return round_to_format(v, 7, -126, 3.3895313892515355e38); }
+double to_fp16(double v) { return round_to_format(v, 10, -14, 65504.0); }
+
+double int8_snap(double v) {
+  double r = std::nearbyint(v);
+  return r > 127 ? 127 : (r < -128 ? -128 : r);
+}
+
+double half_bits_to_double(uint16_t h) {
+  int e = (h >> 10) & 0x1F, m = h & 0x3FF;
+  double v = e == 0 ? std::ldexp((double)m, -24)
+                    : (e == 31 ? (m ? NAN : INFINITY) : std::ldexp(1024.0 + m, e - 25));
+  return (h & 0x8000) ? -v : v;
+}
+
+double input_at(const void* w, int dt, int64_t i) {
+  if (dt == EP_FP32) return (double)static_cast<const float*>(w)[i];
+  uint16_t h = static_cast<const uint16_t*>(w)[i];
+  if (dt == EP_FP16) return half_bits_to_double(h);
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+// ---- lattice -------------------------------------------------------------
+// Nearest point of D8: coordinate rounding (ties to even), then, if the sum is
+// odd, the coordinate with the largest residual (first on ties) moves by one
+// towards its input (a zero residual moves up).  Section 3.2, eq. d8.
+inline void d8_point(const double* y, double* z) {
+  double r[8], tot = 0;
+  for (int j = 0; j < 8; j++) {
+    z[j] = std::nearbyint(y[j]);
+    r[j] = y[j] - z[j];
+    tot += z[j];
+  }
+  if (std::fmod(std::fabs(tot), 2.0) == 1.0) {
+    int k = 0;
+    double best = std::fabs(r[0]);
+    for (int j = 1; j < 8; j++) {
+      double a = std::fabs(r[j]);
+      if (a > best) {
+        best = a;
+        k = j;
+      }
+    }
+    z[k] += r[k] < 0 ? -1.0 : 1.0;
+  }
+}
+
+inline double sqdist(const double* y, const double* p) {
+  double s = 0;
+  for (int j = 0; j < 8; j++) s += (y[j] - p[j]) * (y[j] - p[j]);
+  return s;
+}
+
+// Nearest E8 point as doubled coordinates; the shifted coset replaces the D8
+// candidate only when strictly closer.
+inline void e8_point(const double* y, int32_t* p2) {
+  double a[8], h[8], yh[8];
+  d8_point(y, a);
+  for (int j = 0; j < 8; j++) yh[j] = y[j] - 0.5;
+  d8_point(yh, h);
+  for (int j = 0; j < 8; j++) h[j] += 0.5;
+  const double* win = sqdist(y, h) < sqdist(y, a) ? h : a;
+  for (int j = 0; j < 8; j++) p2[j] = (int32_t)(2.0 * win[j]);
+}
+
+// Field tuple (c, z1..z7, m) of a doubled point (eq. parity).
+inline void split_fields(const int32_t* p2, int32_t* f) {
+  int32_t c = p2[0] & 1, par = 0;
+  for (int j = 0; j < 7; j++) {
+    f[1 + j] = (p2[j] - c) >> 1;
+    par += f[1 + j];
+  }
+  f[0] = c;
+  int32_t z8 = (p2[7] - c) >> 1;
+  f[8] = (z8 - (par & 1)) >> 1;
+}
+
+inline int table_index(int field, int c) { return field == 0 ? 0 : 1 + 8 * c + field - 1; }
+
+// ---- model ---------------------------------------------------------------
+struct Table {
+  int32_t lo = 0;
+  int32_t A = 0;
+  std::vector<uint64_t> n;
+  std::vector<uint32_t> f;
+};
+
+struct Model {
+  Table t[kTables];
+  int32_t max_field_alphabet() const {
+    int32_t m = 0;
+    for (int i = 1; i < kTables; i++) m = std::max(m, t[i].A);
+    return m;
+  }
+  uint64_t serialized_bytes() const {
+    uint64_t s = 4;
+    for (int i = 1; i < kTables; i++) s += 8 + ((2ull * (uint64_t)t[i].A + 3) / 4) * 4;
+    return s;
+  }
+};
+
+// Counts of the field values of nv vectors (9 int32 each), built with
+// per-thread histograms.
+void count_fields(const int32_t* fl, int64_t nv, int nthreads, Model& md) {
+  int T = (int)std::max<int64_t>(1, std::min<int64_t>(nthreads, nv / 4096 + 1));
+  std::vector<std::array<int32_t, 2 * kTables>> ext(T);
+  for (auto& e : ext)
+    for (int i = 0; i < kTables; i++) {
+      e[2 * i] = std::numeric_limits<int32_t>::max();
+      e[2 * i + 1] = std::numeric_limits<int32_t>::min();
+    }
+  parallel_for(nv, T, [&](int64_t b, int64_t e, int tid) {
+    auto& x = ext[tid];
+    for (int64_t v = b; v < e; v++) {
+      const int32_t* q = fl + 9 * v;
+      for (int i = 1; i <= 8; i++) {
+        int ti = table_index(i, q[0]);
+        x[2 * ti] = std::min(x[2 * ti], q[i]);
+        x[2 * ti + 1] = std::max(x[2 * ti + 1], q[i]);
+      }
+    }
+  });
+  for (int i = 0; i < kTables; i++) {
+    int32_t lo = std::numeric_limits<int32_t>::max(), hi = std::numeric_limits<int32_t>::min();
+    if (i == 0) {
+      lo = 0;
+      hi = 1;
+    }
+    for (auto& x : ext) {
+      lo = std::min(lo, x[2 * i]);
+      hi = std::max(hi, x[2 * i + 1]);
+    }
+    Table& tb = md.t[i];
+    tb.lo = hi >= lo ? lo : 0;
+    tb.A = hi >= lo ? (int32_t)((int64_t)hi - lo + 1) : 0;
+    tb.n.assign((size_t)tb.A, 0);
+    tb.f.assign((size_t)tb.A, 0);
+  }
+  // counting: per-thread arrays when small, else a single pass
+  uint64_t cells = 0;
+  for (int i = 0; i < kTables; i++) cells += md.t[i].A;
+  std::vector<std::vector<uint64_t>> part(T, std::vector<uint64_t>(cells, 0));
+  std::vector<uint64_t> base(kTables, 0);
+  for (int i = 1; i < kTables; i++) base[i] = base[i - 1] + md.t[i - 1].A;
+  parallel_for(nv, T, [&](int64_t b, int64_t e, int tid) {
+    uint64_t* h = part[tid].data();
+    for (int64_t v = b; v < e; v++) {
+      const int32_t* q = fl + 9 * v;
+      h[q[0]]++;
+      for (int i = 1; i <= 8; i++) {
+        int ti = table_index(i, q[0]);
+        h[base[ti] + (q[i] - md.t[ti].lo)]++;
+      }
+    }
+  });
+  for (int i = 0; i < kTables; i++)
+    for (int32_t z = 0; z < md.t[i].A; z++) {
+      uint64_t s = 0;
+      for (int t = 0; t < T; t++) s += part[t][base[i] + z];
+      md.t[i].n[z] = s;
+    }
+}
+
+// b-bit frequencies: floor share (at least 1 for observed symbols); missing
+// units to the largest shortfall M n - f N (smaller symbol first); surplus
+// taken one unit at a time from the largest frequency above 1 (smaller symbol
+// first).  Section 3.3 requires only sum = 2^b and f > 0 on observed symbols.
+bool quantize_freqs(Table& tb, int b) {
+  const uint64_t M = 1ull << b;
+  uint64_t N = 0, K = 0;
+  for (auto c : tb.n) {
+    N += c;
+    K += c != 0;
+  }
+  std::fill(tb.f.begin(), tb.f.end(), 0u);
+  if (!N) return true;
+  if (K > M) return false;
+  int64_t assigned = 0;
+  for (int32_t z = 0; z < tb.A; z++) {
+    if (!tb.n[z]) continue;
+    uint64_t share = (M * tb.n[z]) / N;
+    tb.f[z] = (uint32_t)std::max<uint64_t>(1, share);
+    assigned += tb.f[z];
+  }
+  int64_t missing = (int64_t)M - assigned;
+  if (missing > 0) {
+    std::vector<std::pair<int64_t, int32_t>> cand;
+    cand.reserve(K);
+    for (int32_t z = 0; z < tb.A; z++)
+      if (tb.n[z]) cand.emplace_back((int64_t)(M * tb.n[z]) - (int64_t)tb.f[z] * (int64_t)N, z);
+    std::sort(cand.begin(), cand.end(), [](const auto& a, const auto& b) {
+      return a.first != b.first ? a.first > b.first : a.second < b.second;
+    });
+    for (int64_t i = 0; i < missing; i++) tb.f[cand[i].second]++;
+  }
+  for (; missing < 0; missing++) {
+    int32_t arg = -1;
+    for (int32_t z = 0; z < tb.A; z++)
+      if (tb.f[z] > 1 && (arg < 0 || tb.f[z] > tb.f[arg])) arg = z;
+    tb.f[arg]--;
+  }
+  return true;
+}
+
+// Model code length C_CE in bits (eq. length), summed per table then over
+// tables in index order.
+double model_bits(const Model& md, int b) {
+  double total = 0;
+  for (int i = 0; i < kTables; i++) {
+    double part = 0;
+    const Table& tb = md.t[i];
+    for (int32_t z = 0; z < tb.A; z++)
+      if (tb.n[z]) part += (double)tb.n[z] * ((double)b - std::log2((double)tb.f[z]));
+    total += part;
+  }
+  return total;
+}
+
+// Stored-size estimate in bits (eq. estimate, eq. outer_estimate); all terms
+// except the payload are the exact serialized sizes.
+double estimated_bits(double cce, uint64_t tiles, double credit, const Model& md, uint64_t rows,
+                      int container) {
+  double rest = cce - credit * (double)kLanes * (double)tiles;
+  if (rest < 0) rest = 0;
+  double words = std::ceil(rest / 16.0);
+  double payload = 16.0 * words;
+  double pad = std::fmod(words, 2.0) == 1.0 ? 16.0 : 0.0;
+  double meta = 8.0 * (double)(132ull * tiles + 4ull);
+  double tables = 8.0 * (double)md.serialized_bytes();
+  double scales = 32.0 * (double)rows * (container ? 2.0 : 1.0);
+  double header = 8.0 * kHeaderBytes;
+  return payload + pad + meta + tables + scales + header;
+}
+
+// ---- sampling --------------------------------------------------------------
+uint64_t splitmix_next(uint64_t& s) {
+  s += 0x9E3779B97F4A7C15ull;
+  uint64_t z = s;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+std::vector<int64_t> pick_rows(int64_t R, int64_t C, int64_t nominal_vectors) {
+  int64_t per_row = C / 8;
+  int64_t want = (nominal_vectors + per_row - 1) / per_row;
+  std::vector<int64_t> idx((size_t)R);
+  for (int64_t r = 0; r < R; r++) idx[r] = r;
+  if (want >= R) return idx;
+  uint64_t s = ((uint64_t)R << 32) ^ (uint64_t)C;
+  for (int64_t i = 0; i < want; i++) {
+    int64_t j = i + (int64_t)(splitmix_next(s) % (uint64_t)(R - i));
+    std::swap(idx[i], idx[j]);
+  }
+  idx.resize((size_t)want);
+  std::sort(idx.begin(), idx.end());
+  return idx;
+}
+
+struct Encoder {
+  const void* w;
+  int dt;
+  int64_t R, C, cvec;
+  ep_encode_params p;
+  int T;
+  std::vector<float> x;       // coded values (fp32-exact)
+  std::vector<float> delta;   // container scales
+  std::vector<double> mu;     // row RMS
+
+  // quantise rows `rows` into fields fl (9 per vector); optional refit sums
+  void quantize(const std::vector<int64_t>& rows, double s, int32_t* fl, double* num,
+                double* den) {
+    parallel_for((int64_t)rows.size(), T, [&](int64_t b, int64_t e, int) {
+      for (int64_t k = b; k < e; k++) {
+        int64_t r = rows[k];
+        const float* xr = x.data() + r * C;
+        double sn = 0, sd = 0;
+        for (int64_t jv = 0; jv < cvec; jv++) {
+          double y[8];
+          int32_t p2[8];
+          for (int j = 0; j < 8; j++) y[j] = ((double)xr[8 * jv + j] / mu[r]) / s;
+          e8_point(y, p2);
+          split_fields(p2, fl + 9 * (k * cvec + jv));
+          if (num)
+            for (int j = 0; j < 8; j++) {
+              double pj = p2[j] / 2.0;
+              sn += (double)xr[8 * jv + j] * pj;
+              sd += pj * pj;
+            }
+        }
+        if (num) {
+          num[r] = sn;
+          den[r] = sd;
+        }
+      }
+    });
+  }
+};
+
+}  // namespace
+
+int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
+               ep_blob* out, ep_encode_stats* stats) {
+  if (!w || !prm || !out) return fail(EP_ERR_ARG, "ep_encode_cpu: null argument");
+  out->data = nullptr;
+  out->size = 0;
+  if (R <= 0 || C <= 0 || C % 8) return fail(EP_ERR_ARG, "ep_encode_cpu: need R, C > 0 and C % 8 == 0");
+  if (w_dtype != EP_BF16 && w_dtype != EP_FP16 && w_dtype != EP_FP32)
+    return fail(EP_ERR_ARG, "ep_encode_cpu: input dtype must be BF16, FP16 or FP32");
+  if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0 ||
+      prm->container < 0 || prm->container > 2 || !(prm->scale_lo > 0) ||
+      !(prm->scale_hi > prm->scale_lo) || prm->sample_vectors < 1 ||
+      (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)))
+    return fail(EP_ERR_ARG, "ep_encode_cpu: invalid parameters");
+  if (R > 0xFFFFFFFFll || C > 0xFFFFFFFFll || (R * C) / 8 > 0xFFFFFFFFll)
+    return fail(EP_ERR_ARG, "ep_encode_cpu: tensor too large");
+
+  try {
+    Encoder E;
+    E.w = w;
+    E.dt = w_dtype;
+    E.R = R;
+    E.C = C;
+    E.cvec = C / 8;
+    E.p = *prm;
+    int hw = (int)std::thread::hardware_concurrency();
+    E.T = prm->nthreads > 0 ? prm->nthreads : std::max(1, hw);
+    const int64_t N = R * C, nvec = N / 8;
+    const int cont = prm->container;
+    const uint32_t V = (uint32_t)prm->tile_vectors;
+
+    // input values, container route, row RMS (Section 3.2; App. A.6, B.1)
+    E.x.resize((size_t)N);
+    E.delta.assign((size_t)R, 0.0f);
+    E.mu.resize((size_t)R);
+    std::vector<char> bad((size_t)R, 0);
+    parallel_for(R, E.T, [&](int64_t b, int64_t e, int) {
+      for (int64_t r = b; r < e; r++) {
+        double amax = 0;
+        float* xr = E.x.data() + r * C;
+        for (int64_t j = 0; j < C; j++) {
+          float v = (float)input_at(w, w_dtype, r * C + j);
+          if (!std::isfinite(v)) bad[r] = 1;
+          xr[j] = v;
+          amax = std::max(amax, std::fabs((double)v));
+        }
+        if (cont) {
+          float d = amax > 0 ? (float)(amax / (cont == EP_CONT_FP8_ROW ? 448.0 : 127.0)) : 1.0f;
+          E.delta[r] = d;
+          for (int64_t j = 0; j < C; j++) {
+            double q = (double)xr[j] / (double)d;
+            double cv = cont == EP_CONT_FP8_ROW ? to_e4m3(q) : std::nearbyint(q);
+            if (cont == EP_CONT_INT8_ROW) cv = std::min(127.0, std::max(-127.0, cv));
+            xr[j] = (float)cv;
+          }
+        }
+        double ss = 0;
+        for (int64_t j = 0; j < C; j++) ss += (double)xr[j] * (double)xr[j];
+        double m = std::sqrt(ss / (double)C);
+        E.mu[r] = m > kEta ? m : kEta;
+      }
+    });
+    for (char c : bad)
+      if (c) return fail(EP_ERR_ARG, "ep_encode_cpu: non-finite input value");
+
+    // scale search on a fixed row sample (Alg. rate selection; App. C.1)
+    std::vector<int64_t> srows = pick_rows(R, C, prm->sample_vectors);
+    std::vector<int64_t> all((size_t)R);
+    for (int64_t r = 0; r < R; r++) all[r] = r;
+    const int64_t snv = (int64_t)srows.size() * E.cvec;
+    const uint64_t stiles = ((uint64_t)snv + V - 1) / V;
+    const double nsub = (double)((int64_t)srows.size() * C);
+    std::vector<int32_t> sfl((size_t)snv * 9);
+    std::vector<int32_t> fl((size_t)nvec * 9);
+    std::vector<double> num((size_t)R), den((size_t)R);
+
+    const int b_first = prm->prob_bits ? prm->prob_bits : (prm->target_bpp <= 7.0 ? 11 : 12);
+    int b = b_first;
+    double s = 1.0, rhat = 0;
+    uint32_t escal = 0, coarse = 0;
+    bool fits = false;
+    Model full;
+    for (; b <= 15 && !fits; b++) {
+      double lo = prm->scale_lo, hi = prm->scale_hi;
+      for (int it = 0; it < prm->search_steps; it++) {
+        s = std::sqrt(lo * hi);
+        E.quantize(srows, s, sfl.data(), nullptr, nullptr);
+        Model sm;
+        count_fields(sfl.data(), snv, E.T, sm);
+        if (sm.max_field_alphabet() > (1 << b)) {
+          rhat = std::numeric_limits<double>::infinity();
+        } else {
+          for (auto& tb : sm.t) quantize_freqs(tb, b);
+          rhat = estimated_bits(model_bits(sm, b), stiles, prm->state_credit_bits, sm,
+                                srows.size(), cont) / nsub;
+        }
+        if (rhat > prm->target_bpp) lo = s;
+        else hi = s;
+      }
+      s = std::sqrt(lo * hi);
+      E.quantize(all, s, fl.data(), num.data(), den.data());
+      full = Model();
+      count_fields(fl.data(), nvec, E.T, full);
+      fits = full.max_field_alphabet() <= (1 << b);
+      if (!fits) escal++;
+    }
+    if (fits) b--;  // the loop advanced past the accepted precision
+    else {
+      b = 15;
+      while (full.max_field_alphabet() > (1 << b)) {
+        s = 1.05 * s * (double)full.max_field_alphabet() / (double)(1 << b);
+        E.quantize(all, s, fl.data(), num.data(), den.data());
+        full = Model();
+        count_fields(fl.data(), nvec, E.T, full);
+        coarse++;
+      }
+    }
+    for (auto& tb : full.t) quantize_freqs(tb, b);
+
+    // row reconstruction scales (eq. scale_fit)
+    std::vector<float> sigma((size_t)R);
+    for (int64_t r = 0; r < R; r++) {
+      double sg;
+      if (den[r] > 0) {
+        sg = num[r] / den[r];
+        if (sg < kEta) sg = kEta;
+      } else {
+        sg = s * E.mu[r];
+      }
+      sigma[r] = (float)sg;
+    }
+
+    // interleaved rANS per tile (eq. rans_encode; App. C.3)
+    const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
+    const uint32_t M = 1u << b;
+    std::vector<std::vector<uint32_t>> cum(kTables);
+    for (int i = 0; i < kTables; i++) {
+      cum[i].assign((size_t)full.t[i].A + 1, 0);
+      for (int32_t z = 0; z < full.t[i].A; z++) cum[i][z + 1] = cum[i][z] + full.t[i].f[z];
+    }
+    std::vector<uint32_t> states(tiles * kLanes);
+    std::vector<std::vector<uint16_t>> tile_words(tiles);
+    std::vector<double> sbits(tiles, 0.0);
+    parallel_for((int64_t)tiles, E.T, [&](int64_t tb, int64_t te, int) {
+      for (int64_t t = tb; t < te; t++) {
+        uint64_t v0 = (uint64_t)t * V;
+        uint64_t nv = std::min<uint64_t>(V, (uint64_t)nvec - v0);
+        uint64_t rounds = (nv + kLanes - 1) / kLanes;
+        uint32_t st[kLanes];
+        for (auto& q : st) q = kStateLow;
+        std::vector<uint16_t>& out_w = tile_words[t];
+        for (uint64_t step = 9 * rounds; step-- > 0;) {
+          uint64_t k = step / 9;
+          int fi = (int)(step % 9);
+          for (int l = (int)kLanes - 1; l >= 0; l--) {
+            uint64_t li = (uint64_t)l + kLanes * k;
+            if (li >= nv) continue;
+            const int32_t* q = fl.data() + 9 * (v0 + li);
+            int ti = table_index(fi, q[0]);
+            int32_t z = fi == 0 ? q[0] : q[fi] - full.t[ti].lo;
+            uint64_t f = full.t[ti].f[z], F = cum[ti][z];
+            uint64_t xs = st[l];
+            if (xs >= (f << (31 - b))) {
+              out_w.push_back((uint16_t)(xs & 0xFFFF));
+              xs >>= 16;
+            }
+            st[l] = (uint32_t)((xs / f) * M + xs % f + F);
+          }
+        }
+        std::reverse(out_w.begin(), out_w.end());
+        double acc = 0;
+        for (uint32_t l = 0; l < kLanes; l++) {
+          states[t * kLanes + l] = st[l];
+          acc += std::log2((double)st[l] / (double)kStateLow);
+        }
+        sbits[t] = acc;
+      }
+    });
+    uint64_t words = 0;
+    std::vector<uint32_t> offs(tiles + 1);
+    for (uint64_t t = 0; t < tiles; t++) {
+      offs[t] = (uint32_t)words;
+      words += tile_words[t].size();
+      if (words > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_encode_cpu: payload too large");
+    }
+    offs[tiles] = (uint32_t)words;
+
+    // serialise
+    Layout L = layout_of((uint32_t)R, (uint32_t)full.serialized_bytes(), (uint32_t)tiles,
+                         (uint32_t)cont, (uint32_t)words);
+    uint8_t* blob = static_cast<uint8_t*>(std::calloc((size_t)L.total, 1));
+    if (!blob) return fail(EP_ERR_NOMEM, "ep_encode_cpu: out of host memory");
+    auto w32 = [&](uint64_t off, uint32_t v) { std::memcpy(blob + off, &v, 4); };
+    w32(0, kMagic);
+    w32(4, kVersion);
+    w32(8, (uint32_t)R);
+    w32(12, (uint32_t)C);
+    w32(16, (uint32_t)b);
+    w32(20, V);
+    w32(24, (uint32_t)tiles);
+    w32(28, (uint32_t)cont);
+    w32(32, (uint32_t)full.serialized_bytes());
+    w32(36, (uint32_t)words);
+    std::memcpy(blob + 40, &L.total, 8);
+    uint8_t* q = blob + L.off_tables;
+    uint16_t cf[2] = {(uint16_t)full.t[0].f[0], (uint16_t)full.t[0].f[1]};
+    std::memcpy(q, cf, 4);
+    q += 4;
+    for (int i = 1; i < kTables; i++) {
+      const Table& tb = full.t[i];
+      std::memcpy(q, &tb.lo, 4);
+      uint32_t A = (uint32_t)tb.A;
+      std::memcpy(q + 4, &A, 4);
+      for (int32_t z = 0; z < tb.A; z++) {
+        uint16_t v = (uint16_t)tb.f[z];
+        std::memcpy(q + 8 + 2 * z, &v, 2);
+      }
+      q += 8 + ((2ull * A + 3) / 4) * 4;
+    }
+    std::memcpy(blob + L.off_sigma, sigma.data(), 4 * (size_t)R);
+    if (cont) std::memcpy(blob + L.off_delta, E.delta.data(), 4 * (size_t)R);
+    std::memcpy(blob + L.off_states, states.data(), 4 * states.size());
+    std::memcpy(blob + L.off_offsets, offs.data(), 4 * offs.size());
+    parallel_for((int64_t)tiles, E.T, [&](int64_t tb, int64_t te, int) {
+      for (int64_t t = tb; t < te; t++)
+        if (!tile_words[t].empty())
+          std::memcpy(blob + L.off_payload + 2ull * offs[t], tile_words[t].data(),
+                      2 * tile_words[t].size());
+    });
+    out->data = blob;
+    out->size = L.total;
+
+    if (stats) {
+      // reconstruction error in the dtype of the coded values
+      int rdt = cont == EP_CONT_FP8_ROW ? EP_FP8_E4M3 : cont == EP_CONT_INT8_ROW ? EP_INT8 : w_dtype;
+      std::vector<double> acc((size_t)R * 4, 0.0);
+      std::vector<int32_t> p2((size_t)8);
+      parallel_for(R, E.T, [&](int64_t rb, int64_t re, int) {
+        for (int64_t r = rb; r < re; r++) {
+          double ec = 0, rc = 0, eo = 0, ro = 0;
+          for (int64_t jv = 0; jv < E.cvec; jv++) {
+            const int32_t* f = fl.data() + 9 * (r * E.cvec + jv);
+            int32_t par = 0, two[8];
+            for (int j = 0; j < 7; j++) {
+              par += f[1 + j];
+              two[j] = 2 * f[1 + j] + f[0];
+            }
+            two[7] = 2 * (2 * f[8] + (par & 1)) + f[0];
+            for (int j = 0; j < 8; j++) {
+              double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
+              double v = rdt == EP_BF16 ? to_bf16(y) : rdt == EP_FP16 ? to_fp16(y)
+                       : rdt == EP_FP8_E4M3 ? to_e4m3(y) : rdt == EP_INT8 ? int8_snap(y) : y;
+              double xc = E.x[r * C + 8 * jv + j];
+              ec += (v - xc) * (v - xc);
+              rc += xc * xc;
+              double wo = (double)(float)input_at(w, w_dtype, r * C + 8 * jv + j);
+              double vo = cont ? v * (double)E.delta[r] : v;
+              eo += (vo - wo) * (vo - wo);
+              ro += wo * wo;
+            }
+          }
+          acc[4 * r] = ec;
+          acc[4 * r + 1] = rc;
+          acc[4 * r + 2] = eo;
+          acc[4 * r + 3] = ro;
+        }
+      });
+      double ec = 0, rc = 0, eo = 0, ro = 0, sb = 0;
+      for (int64_t r = 0; r < R; r++) {
+        ec += acc[4 * r];
+        rc += acc[4 * r + 1];
+        eo += acc[4 * r + 2];
+        ro += acc[4 * r + 3];
+      }
+      for (double v : sbits) sb += v;
+      stats->scale = s;
+      stats->rate_estimate_sample = rhat;
+      stats->rate_stored = 8.0 * (double)L.total / (double)N;
+      stats->code_length_bits = model_bits(full, b);
+      stats->erel_coded = rc > 0 ? std::sqrt(ec / rc) : 0;
+      stats->erel_original = ro > 0 ? std::sqrt(eo / ro) : 0;
+      stats->mean_state_bits = sb / (double)(tiles * kLanes);
+      stats->bytes = L.total;
+      stats->payload_bits = 16ull * words;
+      stats->prob_bits = (uint32_t)b;
+      stats->n_tiles = (uint32_t)tiles;
+      stats->max_alphabet = (uint32_t)full.max_field_alphabet();
+      stats->sample_rows = (uint32_t)srows.size();
+      stats->escalations = escal;
+      stats->coarsenings = coarse;
+    }
+    return EP_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(EP_ERR_NOMEM, "ep_encode_cpu: out of host memory");
+  }
+}
+
+}  // namespace ep
+
+extern "C" {
+
+void ep_encode_params_default(ep_encode_params* p) {
+  if (!p) return;
+  std::memset(p, 0, sizeof(*p));
+  p->target_bpp = 4.0;
+  p->tile_vectors = 512;
+  p->prob_bits = 0;
+  p->search_steps = 12;
+  p->container = EP_CONT_DIRECT;
+  p->scale_lo = 1e-3;
+  p->scale_hi = 8.0;
+  p->sample_vectors = 1 << 18;
+  p->state_credit_bits = 8.0;
+  p->nthreads = 0;
+}
+
+int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
+                  const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats) {
+  return ep::encode_cpu(w, w_dtype, rows, cols, params, out, stats);
+}
+
+void ep_blob_free(ep_blob* blob) {
+  if (!blob) return;
+  std::free(blob->data);
+  blob->data = nullptr;
+  blob->size = 0;
+}
+
+}  // extern "C"

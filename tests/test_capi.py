@@ -1,0 +1,139 @@
+"""CPU tests of the product library: it loads, exports the C ABI, its encoder
+reproduces the oracle's blobs byte for byte, and its host validation accepts
+valid blobs and refuses malformed ones.  No GPU call is made here."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_34185_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def E():
+    from paper_2609_34185_amd import entropack
+    if not os.path.exists(entropack.LIB_PATH):
+        from paper_2609_34185_amd import build
+        build.build()
+    return entropack
+
+
+def test_library_exports_every_declared_symbol(E):
+    header = open(os.path.join(ROOT, "include", "entropack.h")).read()
+    declared = set(re.findall(r"\b(ep_[a-z0-9_]+)\s*\(", header))
+    assert {"ep_encode_cpu", "ep_decode_tiles", "ep_decode_layers", "ep_blob_info"} <= declared
+    lib = E.lib()
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert set(E.EXPORTS) == declared
+
+
+CASES = [
+    ("cfg1", lambda: W.single_linear(), 4.0, dict(prob_bits=12)),
+    ("cfg2_rows", lambda: W.attention_projection()[:700], 3.0, {}),
+    ("ragged", lambda: W.ragged_tensor(1, 37, 136), 3.3, dict(tile_vectors=45)),
+    ("c8", lambda: W.ragged_tensor(2, 300, 8), 4.0, dict(tile_vectors=33)),
+    ("fp8_container", lambda: W.ragged_tensor(3, 128, 512, scale=0.05), 4.0, dict(container=1)),
+    ("int8_container", lambda: W.ragged_tensor(4, 128, 512, scale=0.05), 6.0, dict(container=2)),
+    ("high_rate", lambda: W.ragged_tensor(5, 64, 1024), 9.0, {}),
+    ("b9", lambda: W.ragged_tensor(6, 64, 256), 2.0, dict(prob_bits=9)),
+    ("literal_credit", lambda: W.ragged_tensor(7, 96, 512), 3.0, dict(state_credit_bits=16.0)),
+]
+
+
+@pytest.mark.parametrize("name,gen,target,kw", CASES, ids=[c[0] for c in CASES])
+def test_encoder_matches_oracle_bytes(E, oracle, name, gen, target, kw):
+    w = gen()
+    b_or, s_or = oracle.encode(w, target, **kw)
+    b_pr, s_pr = E.encode(w, target, **kw)
+    assert np.array_equal(b_pr, b_or)
+    assert s_pr["scale"] == s_or["scale"] and s_pr["prob_bits"] == s_or["b"]
+
+
+def test_encoder_escalation_matches_oracle(E, oracle):
+    R, Cc = 40, 65536
+    rng = np.random.default_rng(12)
+    w = (rng.standard_normal((R, Cc)) * 1e-3).astype(np.float32)
+    outside = [r for r in range(R) if r not in set(oracle.sample_rows(R, Cc).tolist())]
+    w[outside, 5] = 0.02
+    b_or, s_or = oracle.encode(w, 10.0, prob_bits=11)
+    b_pr, s_pr = E.encode(w, 10.0, prob_bits=11)
+    assert s_pr["escalations"] == s_or["escalations"] > 0
+    assert np.array_equal(b_pr, b_or)
+
+
+def test_encoder_fp16_input_matches_oracle(E, oracle):
+    rng = np.random.default_rng(8)
+    h = (rng.standard_normal((64, 256)) * 0.03).astype(np.float16).view(np.uint16)
+    b_or, _ = oracle.encode(h, 4.0, dtype=oracle.FP16)
+    b_pr, _ = E.encode(h, 4.0, dtype=E.FP16)
+    assert np.array_equal(b_pr, b_or)
+
+
+def test_encoder_independent_of_thread_count(E):
+    w = W.attention_projection()[:400]
+    ref, _ = E.encode(w, 3.0, nthreads=1)
+    for t in (2, 3, 8):
+        b, _ = E.encode(w, 3.0, nthreads=t)
+        assert np.array_equal(b, ref)
+
+
+def test_encoder_argument_errors(E):
+    with pytest.raises(E.EntroPackError) as e:
+        E.encode(np.zeros((4, 12), dtype=np.float32), 4.0)
+    assert e.value.code == E.ERR_ARG
+    bad = np.zeros((4, 16), dtype=np.float32)
+    bad[1, 3] = np.nan
+    with pytest.raises(E.EntroPackError) as e:
+        E.encode(bad, 4.0)
+    assert e.value.code == E.ERR_ARG
+    with pytest.raises(E.EntroPackError):
+        E.encode(np.zeros((4, 16), dtype=np.float32), 0.0)
+
+
+def test_blob_info_fields(E, oracle):
+    w = W.single_linear()
+    blob, _ = oracle.encode(w, 4.0, prob_bits=12)
+    info = E.blob_info(blob)
+    h = oracle.header(blob)
+    assert (info.rows, info.cols, info.prob_bits, info.tile_vectors, info.n_tiles) == (
+        h["rows"], h["cols"], h["b"], h["V"], h["n_tiles"])
+    assert info.total_bytes == blob.size and info.payload_words == h["payload_words"]
+    tp, _ = oracle.decode(blob, oracle.COORD2)
+    assert info.coord2_min <= tp.min() and tp.max() <= info.coord2_max
+    sigma = blob[info.off_sigma: info.off_sigma + 4 * info.rows].view(np.float32)
+    assert np.abs(sigma[:, None] * tp / 2.0).max() <= info.max_abs_weight
+
+
+def test_blob_info_refuses_malformed(E, oracle):
+    w = W.ragged_tensor(2, 64, 256)
+    blob, _ = oracle.encode(w, 4.0)
+    info = E.blob_info(blob)
+
+    def refused(b):
+        with pytest.raises(E.EntroPackError) as e:
+            E.blob_info(b)
+        return e.value.code == E.ERR_FORMAT
+
+    assert refused(blob[:-4])
+    for off, val in [(0, 1), (4, 2), (16, 8), (16, 16), (21, 0), (24, 7)]:
+        b = blob.copy()
+        b[off] = val
+        assert refused(b)
+    b = blob.copy()   # coset frequencies no longer sum to 2^b
+    b[48] ^= 1
+    assert refused(b)
+    b = blob.copy()   # a field frequency changed
+    b[info.table_off[0]] ^= 1
+    assert refused(b)
+    b = blob.copy()   # offsets out of order
+    o = b[info.off_offsets: info.off_offsets + 4 * (info.n_tiles + 1)].view(np.uint32)
+    if info.n_tiles > 1:
+        o[1] = o[2] + 1
+        assert refused(b)
+    b = blob.copy()   # non-finite row scale
+    b[info.off_sigma: info.off_sigma + 4].view(np.float32)[0] = np.inf
+    assert refused(b)

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP decode (through the C ABI) against the oracle decoder.
+
+Every blob here comes from the oracle encoder; the GPU output must equal the
+oracle's bit for bit (doubled coordinates, weights in every output dtype, and
+the container dequant scales), with a clean status word.
+"""
+import os
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+from paper_2609_34185_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+DTYPES = ["COORD2", "BF16", "FP16", "FP32", "FP8", "INT8"]
+
+
+def say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+@pytest.fixture(scope="module")
+def E():
+    from paper_2609_34185_amd import entropack
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    entropack.lib()
+    return entropack
+
+
+def codes(E, oracle, name):
+    return {"COORD2": (E.COORD2_I32, oracle.COORD2), "BF16": (E.BF16, oracle.BF16),
+            "FP16": (E.FP16, oracle.FP16), "FP32": (E.FP32, oracle.FP32),
+            "FP8": (E.FP8_E4M3, oracle.FP8), "INT8": (E.INT8, oracle.INT8)}[name]
+
+
+def gpu_bits(t):
+    """Host numpy view of a device tensor's bits, matching the oracle's arrays."""
+    t = t.cpu()
+    if t.dtype in (torch.bfloat16, torch.float16):
+        return t.view(torch.int16).numpy().view(np.uint16)
+    if t.dtype == torch.float8_e4m3fn:
+        return t.view(torch.uint8).numpy()
+    return t.numpy()
+
+
+def check_blob(E, oracle, blob, dtypes=DTYPES, tag=""):
+    info = E.blob_info(blob)
+    d_blob = E.to_device(blob)
+    for name in dtypes:
+        ecode, ocode = codes(E, oracle, name)
+        say(f"  decode {tag} {info.rows}x{info.cols} b={info.prob_bits} path={info.path} -> {name}")
+        out, dq, st = E.decode(blob, ecode, d_blob=d_blob, info=info)
+        torch.cuda.synchronize()
+        ref, ref_dq = oracle.decode(blob, ocode)
+        assert int(st.item()) == 0
+        got = gpu_bits(out)
+        if not np.array_equal(got, ref):
+            bad = np.argwhere(got != ref)
+            r, c = bad[0]
+            raise AssertionError(f"{name}: {len(bad)} mismatches, first at {r},{c}: "
+                                 f"gpu {got[r, c]} oracle {ref[r, c]}")
+        if info.container:
+            assert np.array_equal(dq.cpu().numpy(), ref_dq)
+    return info
+
+
+def test_config1_all_dtypes_search_path(E, oracle):
+    blob, st = oracle.encode(W.single_linear(), 4.0, prob_bits=12)
+    info = check_blob(E, oracle, blob, tag="cfg1")
+    assert info.path == 2
+
+
+def test_config1_all_dtypes_lut_path(E, oracle):
+    blob, st = oracle.encode(W.single_linear(), 4.0, prob_bits=11)
+    info = check_blob(E, oracle, blob, tag="cfg1-b11")
+    assert info.path == 1
+
+
+def test_config2_fp16_bf16(E, oracle):
+    blob, st = oracle.encode(W.attention_projection(), 3.0)
+    check_blob(E, oracle, blob, dtypes=["COORD2", "FP16", "BF16"], tag="cfg2")
+
+
+@pytest.mark.parametrize("b", [9, 10, 11, 12, 13, 14, 15])
+def test_every_probability_precision(E, oracle, b):
+    w = W.ragged_tensor(20 + b, 96, 704)
+    blob, st = oracle.encode(w, 4.5, prob_bits=b)
+    check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"b{b}")
+
+
+@pytest.mark.parametrize("shape,V", [((1, 8), 512), ((3, 24), 32), ((7, 400), 45),
+                                     ((33, 264), 512), ((130, 72), 100), ((300, 8), 33),
+                                     ((65, 1000), 77), ((1, 4096), 1)])
+def test_ragged_shapes_and_tiles(E, oracle, shape, V):
+    w = W.ragged_tensor(8, *shape)
+    blob, st = oracle.encode(w, 3.0, tile_vectors=V)
+    check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "FP8"], tag=f"V{V}")
+
+
+def test_tile_ranges_write_only_their_tiles(E, oracle):
+    blob, st = oracle.encode(W.ragged_tensor(3, 200, 520), 3.5, tile_vectors=64)
+    info = E.blob_info(blob)
+    d_blob = E.to_device(blob)
+    full, _ = oracle.decode(blob, oracle.BF16)
+    out = torch.full((info.rows, info.cols), 7, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+    st_t = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for t0, t1 in [(0, 3), (3, 4), (4, 4), (5, info.n_tiles)]:
+        E.decode(blob, E.BF16, d_blob=d_blob, info=info, tile_begin=t0, tile_end=t1, out=out,
+                 status=st_t)
+    torch.cuda.synchronize()
+    got = gpu_bits(out).reshape(-1)
+    ref = full.reshape(-1)
+    V8 = 64 * 8
+    assert np.array_equal(got[:4 * V8], ref[:4 * V8])
+    assert np.all(got[4 * V8:5 * V8] == 7)                 # tile 4 was never decoded
+    assert np.array_equal(got[5 * V8:], ref[5 * V8:])
+    assert int(st_t.item()) == 0
+
+
+def test_degenerate_tensors(E, oracle):
+    # all zeros: one coset, zero scales-by-fallback, every output zero
+    z = np.zeros((64, 128), dtype=np.float32)
+    blob, st = oracle.encode(z, 4.0)
+    info = check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "INT8"], tag="zeros")
+    assert info.coset_f1 == 0
+    # constant rows
+    c = np.full((16, 64), 0.25, dtype=np.float32)
+    blob, st = oracle.encode(c, 2.0)
+    check_blob(E, oracle, blob, dtypes=["COORD2", "FP16"], tag="const")
+
+
+def test_saturation(E, oracle):
+    rng = np.random.default_rng(4)
+    w = (rng.standard_normal((32, 256)) * 3e4).astype(np.float32)
+    w[0, :8] = 1e5
+    blob, st = oracle.encode(w, 5.0)
+    check_blob(E, oracle, blob, dtypes=["FP16", "FP8", "INT8", "BF16"], tag="sat")
+
+
+def test_corrupt_payload_sets_status_without_fault(E, oracle):
+    blob, st = oracle.encode(W.ragged_tensor(6, 128, 512), 4.0)
+    info = E.blob_info(blob)
+    bad = blob.copy()
+    bad[info.off_payload + 200: info.off_payload + 260] ^= 0x5A
+    assert oracle.decode_status(bad) == oracle.ERR_CORRUPT
+    out, dq, stt = E.decode(bad, E.COORD2_I32)
+    torch.cuda.synchronize()
+    assert int(stt.item()) != 0
+
+
+# ---- the paper-shaped workloads at full size ------------------------------------
+
+@pytest.fixture(scope="module")
+def mlp():
+    say("  generating the 27B-class MLP set (seed 2)")
+    return W.llm_mlp()
+
+
+@pytest.fixture(scope="module")
+def mlp_fp8_blobs(oracle, mlp):
+    names = ["gate", "up", "down"]
+    with ThreadPoolExecutor(3) as ex:
+        res = list(ex.map(lambda n: oracle.encode(mlp[n], 4.0, container=oracle.CONT_FP8), names))
+    return {n: r[0] for n, r in zip(names, res)}
+
+
+def test_config3_full_size_fp8_in_one_launch(E, oracle, mlp_fp8_blobs):
+    """The benchmark's configuration: gate, up and down decoded by one ep_decode_layers call."""
+    names = ["gate", "up", "down"]
+    infos = {n: E.blob_info(mlp_fp8_blobs[n]) for n in names}
+    dev = {n: E.to_device(mlp_fp8_blobs[n]) for n in names}
+    outs = {n: torch.zeros((infos[n].rows, infos[n].cols), dtype=torch.float8_e4m3fn, device="cuda")
+            for n in names}
+    dqs = {n: torch.zeros(infos[n].rows, dtype=torch.float32, device="cuda") for n in names}
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    layers = [(infos[n], dev[n].data_ptr(), outs[n].data_ptr(), dqs[n].data_ptr(), E.FP8_E4M3)
+              for n in names]
+    ws = max(1, E.decode_layers_workspace(len(layers)))
+    d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
+    say("  ep_decode_layers over gate/up/down")
+    E.decode_layers(layers, d_ws.data_ptr(), ws, st.data_ptr(),
+                    torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    with ThreadPoolExecutor(3) as ex:
+        refs = dict(zip(names, ex.map(lambda n: oracle.decode(mlp_fp8_blobs[n], oracle.FP8), names)))
+    for n in names:
+        assert infos[n].path == 1
+        assert np.array_equal(gpu_bits(outs[n]), refs[n][0]), n
+        assert np.array_equal(dqs[n].cpu().numpy(), refs[n][1]), n
+
+
+def test_config3_product_encoder_reproduces_oracle_blobs(E, mlp, mlp_fp8_blobs):
+    """The benchmark encodes with the library's encoder; at full size it emits the same bytes."""
+    for n in ["gate", "down"]:
+        b, _ = E.encode(mlp[n], 4.0, container=E.CONT_FP8_ROW)
+        assert np.array_equal(b, mlp_fp8_blobs[n]), n
+
+
+def test_config5_down_int8_container(E, oracle, mlp):
+    blob, st = oracle.encode(mlp["down"], 6.0, container=oracle.CONT_INT8)
+    check_blob(E, oracle, blob, dtypes=["INT8", "COORD2"], tag="cfg5")
+
+
+def test_config4_stack_two_blocks_one_launch(E, oracle):
+    """Two diffusion-transformer blocks (12 layers at full layer shapes) in one
+    ep_decode_layers launch; more than 8 layers use the workspace descriptor list."""
+    say("  generating 2 DiT blocks")
+    layers_np = W.dit_stack(2, workers=2)
+    with ThreadPoolExecutor(8) as ex:
+        blobs = list(ex.map(lambda lw: oracle.encode(lw[1], 2.5)[0], layers_np))
+    infos = [E.blob_info(b) for b in blobs]
+    dev = [E.to_device(b) for b in blobs]
+    outs = [torch.zeros((i.rows, i.cols), dtype=torch.bfloat16, device="cuda") for i in infos]
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    layers = [(i, d.data_ptr(), o.data_ptr(), 0, E.BF16) for i, d, o in zip(infos, dev, outs)]
+    ws = E.decode_layers_workspace(len(layers))
+    assert ws > 0
+    d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
+    say("  ep_decode_layers over 12 layers")
+    E.decode_layers(layers, d_ws.data_ptr(), ws, st.data_ptr(),
+                    torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    with ThreadPoolExecutor(8) as ex:
+        refs = list(ex.map(lambda b: oracle.decode(b, oracle.BF16)[0], blobs))
+    for (name, _), o, r in zip(layers_np, outs, refs):
+        assert np.array_equal(gpu_bits(o), r), name
