@@ -51,6 +51,8 @@ struct LayerDev {
   uint32_t out_dtype, saturate;
   uint32_t coset_f0, coset_f1;
   uint32_t sum_A, search_iters;
+  uint32_t pay_bytes;             // payload section bytes (bounds of the buffer resource)
+  uint32_t div_magic, div_shift, div_pow2;  // floor(v / (C/8))
   uint64_t off_sigma, off_delta, off_states, off_offsets, off_payload;
   uint32_t tab_off[16];
   int32_t tab_min[16];
@@ -205,37 +207,89 @@ __device__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum)
 }
 
 // ---- the decode of one two-tile task -------------------------------------------
-struct WaveCtx {
-  uint32_t half, l, lt_mask;
+// Payload staging: each half-wave owns a 512-word ring in LDS.  Word w of the
+// payload section lives in slot w & 511.  Chunks of 256 words (aligned to 256
+// in w) are fetched with four coalesced buffer_load_dword per lane (a raw
+// buffer resource bounds every read to the payload section) into registers,
+// and written to the ring ("committed") only when the consumer gets within 64
+// words of the committed end, by which time the loads have long returned; the
+// following chunk is requested right after each commit.  A commit overwrites
+// the slots of words [Qc - 512, Qc - 256), all consumed by then.
+constexpr uint32_t kRingWords = 512;
+constexpr uint32_t kChunkWords = 256;
+constexpr uint32_t kRingBytesPerWave = 2 * 2 * kRingWords;   // two halves, u16 words
+constexpr uint32_t kRingBytes = kWavesPerGroup * kRingBytesPerWave;
+
+struct Stage {
+  __amdgpu_buffer_rsrc_t rsrc;   // payload section
+  uint32_t ring;                 // LDS byte address of this half's ring
+  uint32_t Qc;                   // committed end (words)
+  uint32_t T;                    // commit trigger: P >= T
+  uint32_t Pend;
+  uint32_t pend[4];              // fetched, not yet committed chunk
 };
 
-// Refill states below 2^15 from the half-wave's word stream (lane order).
-__device__ __forceinline__ void renorm(uint32_t& x, bool act, uint32_t& P, uint32_t Pend,
-                                       const uint16_t* pay, const WaveCtx& w, uint32_t& err) {
-  const bool need = act && x < kStateLow;
-  const uint64_t m = __ballot(need);
-  const uint32_t mh = w.half ? (uint32_t)(m >> 32) : (uint32_t)m;
-  if (need) {
-    const uint32_t idx = P + (uint32_t)__builtin_popcount(mh & w.lt_mask);
-    uint32_t word = 0;
-    if (idx < Pend) word = pay[idx];
-    else err |= EP_STATUS_PAYLOAD_OVERRUN;
-    x = (x << 16) | word;
-  }
-  P += (uint32_t)__builtin_popcount(mh);
+__device__ __forceinline__ void fetch_chunk(Stage& S, uint32_t l, uint32_t start) {
+#pragma unroll
+  for (int k = 0; k < 4; k++)
+    S.pend[k] = __builtin_amdgcn_raw_buffer_load_b32(S.rsrc, 2 * start + 4 * (l + 32 * k), 0, 0);
 }
 
-template <int PATH>
+__device__ __forceinline__ void store_chunk(uint8_t* lds_base, const Stage& S, uint32_t l,
+                                            uint32_t start) {
+#pragma unroll
+  for (int k = 0; k < 4; k++) {
+    const uint32_t slot = (start + 2 * (l + 32 * k)) & (kRingWords - 1);
+    *reinterpret_cast<uint32_t*>(lds_base + S.ring + 2 * slot) = S.pend[k];
+  }
+}
+
+// Commit the pending chunk if this half is within 64 words of the committed end.
+__device__ __forceinline__ void stage_check(uint8_t* lds_base, Stage& S, uint32_t P, uint32_t l) {
+  const bool due = P >= S.T;
+  if (__ballot(due)) {
+    if (due) {
+      store_chunk(lds_base, S, l, S.Qc);
+      S.Qc += kChunkWords;
+      S.T = S.Qc - 64;
+      if (S.Qc < S.Pend) fetch_chunk(S, l, S.Qc);
+    }
+  }
+}
+
+// Refill states below 2^15 from the half-wave's ring (lane order inside each half).
+__device__ __forceinline__ void renorm(uint32_t& x, bool act, uint32_t& P, const uint8_t* lds_base,
+                                       const Stage& S, uint32_t half) {
+  const uint64_t m = __ballot(act && x < kStateLow);
+  const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+  uint32_t idx;
+  if (half) {
+    idx = __builtin_amdgcn_mbcnt_hi(hi, P);
+    P += (uint32_t)__builtin_popcount(hi);
+  } else {
+    idx = __builtin_amdgcn_mbcnt_lo(lo, P);
+    P += (uint32_t)__builtin_popcount(lo);
+  }
+  if (act && x < kStateLow) {
+    const uint32_t word =
+        *reinterpret_cast<const uint16_t*>(lds_base + S.ring + 2 * (idx & (kRingWords - 1)));
+    x = (x << 16) | word;
+  }
+}
+
+// One field symbol.  Slot-table path: entry = lut[(8c + i - 1) * 2^B + u]; the
+// coset part cb = 8c * 2^B is per lane, the field part a constant offset.
+template <int PATH, int B>
 __device__ __forceinline__ void decode_field(const LayerDev& L, const uint32_t* lds, int field,
-                                             uint32_t c, uint32_t& x, int32_t& dval) {
-  const uint32_t mask = (1u << L.b) - 1;
-  const uint32_t u = x & mask;
-  const uint32_t t = c * 8 + (uint32_t)(field - 1);
+                                             uint32_t cb, uint32_t c, uint32_t& x, int32_t& dval) {
   if (PATH == kPathLut) {
-    const uint32_t e = lds[(t << L.b) + u];
-    x = (e & 0xFFFu) * (x >> L.b) + ((e >> 12) & 0x7FFu);
+    constexpr uint32_t M = 1u << B;
+    const uint32_t u = x & (M - 1);
+    const uint32_t e = lds[cb + u + (uint32_t)(field - 1) * M];
+    x = __umul24(e & 0xFFFu, x >> B) + ((e >> 12) & 0x7FFu);
     dval = (int32_t)e >> 23;
   } else {
+    const uint32_t u = x & ((1u << L.b) - 1);
     const uint32_t base = c ? L.tab_base[8 + field - 1] : L.tab_base[field - 1];
     const uint32_t A = c ? L.tab_A[8 + field - 1] : L.tab_A[field - 1];
     uint32_t s = 0, n = A;
@@ -245,55 +299,83 @@ __device__ __forceinline__ void decode_field(const LayerDev& L, const uint32_t* 
       n -= h;
     }
     const uint32_t e = lds[base + s];
-    x = (e >> 16) * (x >> L.b) + u - (e & 0xFFFFu);
+    x = __umul24(e >> 16, x >> L.b) + u - (e & 0xFFFFu);
     const int32_t mn = c ? L.tab_min[8 + field - 1] : L.tab_min[field - 1];
     dval = doubled_value((int32_t)s + mn, field, c);
   }
 }
 
-template <int PATH>
-__device__ void decode_task(const LayerDev& L, const uint32_t* lds, uint32_t task,
-                            int32_t* status) {
-  const uint32_t lane = threadIdx.x & 63;
-  WaveCtx w;
-  w.half = lane >> 5;
-  w.l = lane & 31;
-  w.lt_mask = (1u << w.l) - 1u;
-  const uint32_t tile = L.tile_begin + 2 * task + w.half;
+// floor(v / C8) with the host-computed magic (Granlund-Montgomery).
+__device__ __forceinline__ uint32_t row_of(const LayerDev& L, uint32_t v) {
+  if (L.div_pow2) return v >> L.div_shift;
+  const uint32_t q = __umulhi(v, L.div_magic);
+  return (q + ((v - q) >> 1)) >> L.div_shift;
+}
+
+template <int PATH, int B>
+__device__ void decode_task(const LayerDev& L, const uint32_t* lds, uint8_t* lds_base,
+                            uint32_t ring_area, uint32_t task, int32_t* status) {
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t half = lane >> 5, l = lane & 31;
+  const uint32_t tile = L.tile_begin + 2 * task + half;
   const bool tile_ok = tile < L.tile_end;
   const uint32_t nvec = L.rows * L.cvec;
   const uint32_t v0 = tile_ok ? tile * L.V : 0;
   const uint32_t nv = tile_ok ? min(L.V, nvec - v0) : 0;
-  const uint32_t n_l = w.l < nv ? (nv - 1 - w.l) / 32 + 1 : 0;
+  const uint32_t n_l = l < nv ? (nv - 1 - l) / 32 + 1 : 0;
   const uint32_t r_here = (nv + 31) / 32;
   const uint32_t rounds = max(__builtin_amdgcn_readlane(r_here, 0), __builtin_amdgcn_readlane(r_here, 32));
 
   const uint32_t* states = reinterpret_cast<const uint32_t*>(L.blob + L.off_states);
   const uint32_t* offs = reinterpret_cast<const uint32_t*>(L.blob + L.off_offsets);
-  const uint16_t* pay = reinterpret_cast<const uint16_t*>(L.blob + L.off_payload);
   const float* sigma = reinterpret_cast<const float*>(L.blob + L.off_sigma);
-  uint32_t x = tile_ok ? states[(uint64_t)tile * 32 + w.l] : kStateLow;
-  uint32_t P = tile_ok ? offs[tile] : 0, Pend = tile_ok ? offs[tile + 1] : 0;
-  uint32_t err = 0;
+  uint32_t x = tile_ok ? states[(uint64_t)tile * 32 + l] : kStateLow;
+  const uint32_t P0 = tile_ok ? offs[tile] : 0;
+  Stage S;
+  S.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(L.blob + L.off_payload), (short)0,
+                                             (int)L.pay_bytes, 0x00020000);
+  S.ring = ring_area + wave * kRingBytesPerWave + half * (2 * kRingWords);
+  S.Pend = tile_ok ? offs[tile + 1] : 0;
+  const uint32_t C0 = P0 & ~(kChunkWords - 1);
+  S.Qc = C0;
+  S.T = 0xFFFFFFFFu;
+  if (tile_ok) {
+    fetch_chunk(S, l, C0);
+    store_chunk(lds_base, S, l, C0);
+    S.Qc = C0 + kChunkWords;
+    if (S.Qc < S.Pend) {
+      fetch_chunk(S, l, S.Qc);
+      store_chunk(lds_base, S, l, S.Qc);
+    }
+    S.Qc += kChunkWords;
+    S.T = S.Qc - 64;
+    if (S.Qc < S.Pend) fetch_chunk(S, l, S.Qc);
+  }
+  uint32_t P = P0;
   const uint32_t mask = (1u << L.b) - 1;
 
   for (uint32_t k = 0; k < rounds; k++) {
     const bool act = k < n_l;
+    const uint32_t v = v0 + l + 32 * k;
+    const float sg = act ? sigma[row_of(L, v)] : 0.0f;
     // coset symbol
-    uint32_t c = 0;
+    uint32_t c = 0, cb = 0;
     if (act) {
       const uint32_t u = x & mask;
       c = u >= L.coset_f0 ? 1u : 0u;
       const uint32_t f = c ? L.coset_f1 : L.coset_f0;
       const uint32_t F = c ? L.coset_f0 : 0u;
-      x = f * (x >> L.b) + u - F;
+      x = __umul24(f, x >> L.b) + u - F;
+      cb = c << (L.b + 3);
     }
-    renorm(x, act, P, Pend, pay, w, err);
+    stage_check(lds_base, S, P, l);
+    renorm(x, act, P, lds_base, S, half);
     int32_t d[9];
 #pragma unroll
     for (int i = 1; i <= 8; i++) {
-      if (act) decode_field<PATH>(L, lds, i, c, x, d[i]);
-      renorm(x, act, P, Pend, pay, w, err);
+      if (act) decode_field<PATH, B>(L, lds, i, cb, c, x, d[i]);
+      stage_check(lds_base, S, P, l);
+      renorm(x, act, P, lds_base, S, half);
     }
     if (act) {
       // field inverse: 2p_i = 2 z_i + c; 2p_8 = 4m + c + 2 pi, pi = sum z_1..7 mod 2
@@ -305,28 +387,34 @@ __device__ void decode_task(const LayerDev& L, const uint32_t* lds, uint32_t tas
         acc += d[i];
       }
       p2[7] = d[8] + (acc & 2);
-      const uint32_t v = v0 + w.l + 32 * k;
-      const uint32_t r = v / L.cvec;
-      store_vector(L, v, p2, 0.5f * sigma[r]);
+      store_vector(L, v, p2, 0.5f * sg);
     }
   }
+  uint32_t err = 0;
   if (tile_ok) {
     if (x != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
-    if (w.l == 0 && P != Pend) err |= EP_STATUS_BAD_END_OFFSET;
+    if (l == 0 && P != S.Pend) err |= P > S.Pend ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
     if (L.container && L.dequant) {
       const float* delta = reinterpret_cast<const float*>(L.blob + L.off_delta);
       const uint32_t r_first = (v0 + L.cvec - 1) / L.cvec;
       const uint32_t r_last = (v0 + nv - 1) / L.cvec;
-      for (uint32_t r = r_first + w.l; r <= r_last; r += 32) L.dequant[r] = delta[r];
+      for (uint32_t r = r_first + l; r <= r_last; r += 32) L.dequant[r] = delta[r];
     }
   }
   if (err && status) atomicOr(status, (int32_t)err);
 }
 
+// LDS byte offset of the payload rings: after the slot table (LUT path) or
+// after the cumulative table (search path).
+template <int PATH>
+__device__ __forceinline__ uint32_t ring_offset(const LayerDev& L) {
+  return PATH == kPathLut ? (64u << L.b) : ((4u * L.sum_A + 15u) & ~15u);
+}
+
 template <int PATH>
 __device__ void build_tables(const LayerDev& L, uint32_t* lds) {
   if (PATH == kPathLut) {
-    uint32_t* cum = lds + (16u << L.b);
+    uint32_t* cum = lds + (16u << L.b);   // scratch inside the ring area
     build_cumulative(L, cum);
     __syncthreads();
     build_lut(L, lds, cum);
@@ -354,8 +442,14 @@ __device__ void run_layers(const LayerDev* layers, int n_layers, uint32_t total,
     __syncthreads();
     build_tables<PATH>(L, lds);
     __syncthreads();
-    for (uint32_t task = seg + wave; task < seg_end; task += kWavesPerGroup)
-      decode_task<PATH>(L, lds, task - L.task_begin, status);
+    const uint32_t ring_area = ring_offset<PATH>(L);
+    uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
+    for (uint32_t task = seg + wave; task < seg_end; task += kWavesPerGroup) {
+      if (PATH == kPathSearch) decode_task<PATH, 0>(L, lds, lb, ring_area, task - L.task_begin, status);
+      else if (L.b == 11) decode_task<PATH, 11>(L, lds, lb, ring_area, task - L.task_begin, status);
+      else if (L.b == 10) decode_task<PATH, 10>(L, lds, lb, ring_area, task - L.task_begin, status);
+      else decode_task<PATH, 9>(L, lds, lb, ring_area, task - L.task_begin, status);
+    }
     seg = seg_end;
   }
 }
@@ -406,8 +500,8 @@ DeviceProps device_props() {
 }
 
 uint32_t lds_bytes(uint32_t path, const ep_tensor_info& I) {
-  if (path == kPathLut) return 4u * (16u << I.prob_bits) + 4u * I.sum_alphabet;
-  return 4u * I.sum_alphabet + 4u;
+  if (path == kPathLut) return (64u << I.prob_bits) + kRingBytes;
+  return ((4u * I.sum_alphabet + 15u) & ~15u) + kRingBytes;
 }
 
 float dtype_max(int dt) {
@@ -456,6 +550,21 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
   for (int t = 0; t < 16; t++) amax = std::max(amax, I.table_A[t]);
   while ((1u << it) < amax) it++;
   D.search_iters = it;
+  const uint64_t pay = (2ull * I.payload_words + 3) / 4 * 4;
+  if (pay > 0xFFFFFFF0ull) return fail(EP_ERR_UNSUPPORTED, "decode: payload section above 4 GiB");
+  D.pay_bytes = (uint32_t)pay;
+  const uint32_t d = D.cvec;
+  if ((d & (d - 1)) == 0) {
+    D.div_pow2 = 1;
+    D.div_shift = 0;
+    while ((1u << D.div_shift) < d) D.div_shift++;
+  } else {
+    uint32_t lg = 0;
+    while ((1ull << lg) < d) lg++;
+    D.div_pow2 = 0;
+    D.div_magic = (uint32_t)(((1ull << 32) * ((1ull << lg) - d)) / d + 1);
+    D.div_shift = lg - 1;
+  }
   D.off_sigma = I.off_sigma;
   D.off_delta = I.off_delta;
   D.off_states = I.off_states;

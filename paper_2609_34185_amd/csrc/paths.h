@@ -17,12 +17,12 @@ enum DecodePath : uint32_t {
 constexpr uint32_t kLutMaxBits = 11;
 constexpr int32_t kLutValueMin = -256;   // packed doubled coordinate: signed 9 bits
 constexpr int32_t kLutValueMax = 255;
-constexpr uint32_t kSearchLdsBytes = 152 * 1024;
+constexpr uint32_t kSearchLdsBytes = 128 * 1024;   // the payload rings take the other 32 KiB
 
 inline uint32_t choose_path(const ep_tensor_info& I) {
   if (I.prob_bits <= kLutMaxBits && I.coord2_min >= kLutValueMin && I.coord2_max <= kLutValueMax)
     return kPathLut;
-  if (4ull * I.sum_alphabet + 256 <= kSearchLdsBytes) return kPathSearch;
+  if (4ull * I.sum_alphabet + 16 <= kSearchLdsBytes) return kPathSearch;
   return kPathNone;
 }
 
