@@ -41,6 +41,11 @@ constexpr int kWavesPerGroup = 16;
 constexpr int kThreads = kWaveSize * kWavesPerGroup;
 constexpr uint32_t kStateLow = 1u << 15;
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ uint32_t wave_id() {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
 struct LayerDev {
   const uint8_t* blob;
   void* out;
@@ -59,6 +64,58 @@ struct LayerDev {
   uint32_t tab_A[16];
   uint32_t tab_base[16];          // prefix of tab_A (search path)
 };
+
+// The scalars the decode loop needs, read once per layer segment and forced
+// into scalar registers (whatever memory the descriptor list lives in).
+struct Hot {
+  const uint8_t* blob;
+  void* out;
+  float* dequant;
+  uint32_t rows, cvec, V, tile_begin, tile_end, b, container;
+  uint32_t out_dtype, saturate, coset_f0, coset_f1;
+  uint32_t pay_bytes, div_magic, div_shift, div_pow2;
+  uint32_t search_iters, meta;    // search path: LDS index of the table metadata
+  uint32_t off_sigma, off_delta, off_states, off_offsets, off_payload;
+};
+
+__device__ __forceinline__ uint32_t uni(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+template <class T>
+__device__ __forceinline__ T* uni_ptr(T* p) {
+  const uint64_t a = (uint64_t)p;
+  return (T*)((uint64_t)uni((uint32_t)a) | ((uint64_t)uni((uint32_t)(a >> 32)) << 32));
+}
+
+__device__ __forceinline__ Hot make_hot(const LayerDev& L) {
+  Hot H;
+  H.blob = uni_ptr(L.blob);
+  H.out = uni_ptr(L.out);
+  H.dequant = uni_ptr(L.dequant);
+  H.rows = uni(L.rows);
+  H.cvec = uni(L.cvec);
+  H.V = uni(L.V);
+  H.tile_begin = uni(L.tile_begin);
+  H.tile_end = uni(L.tile_end);
+  H.b = uni(L.b);
+  H.container = uni(L.container);
+  H.out_dtype = uni(L.out_dtype);
+  H.saturate = uni(L.saturate);
+  H.coset_f0 = uni(L.coset_f0);
+  H.coset_f1 = uni(L.coset_f1);
+  H.pay_bytes = uni(L.pay_bytes);
+  H.div_magic = uni(L.div_magic);
+  H.div_shift = uni(L.div_shift);
+  H.div_pow2 = uni(L.div_pow2);
+  H.search_iters = uni(L.search_iters);
+  H.meta = uni(L.sum_A);
+  H.off_sigma = uni((uint32_t)L.off_sigma);
+  H.off_delta = uni((uint32_t)L.off_delta);
+  H.off_states = uni((uint32_t)L.off_states);
+  H.off_offsets = uni((uint32_t)L.off_offsets);
+  H.off_payload = uni((uint32_t)L.off_payload);
+  return H;
+}
 
 // ---- output snapping (eq. recon) --------------------------------------------
 __device__ __forceinline__ float sat(float y, float m) { return __builtin_amdgcn_fmed3f(y, -m, m); }
@@ -96,7 +153,7 @@ __device__ __forceinline__ uint32_t int8_quad(float a, float b, float c, float d
 }
 
 // Store the eight weights of vector v (elements 8v..8v+7).
-__device__ __forceinline__ void store_vector(const LayerDev& L, uint32_t v, const int32_t* p2,
+__device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int32_t* p2,
                                              float half_sigma) {
   float y[8];
 #pragma unroll
@@ -151,8 +208,8 @@ __device__ __forceinline__ void store_vector(const LayerDev& L, uint32_t v, cons
 // ---- table construction in LDS ------------------------------------------------
 // Cumulative entries F_s | f_s << 16 of the 16 field tables at lds[base_t + s];
 // wave w scans table w (and w + 16 ... when fewer waves exist).
-__device__ void build_cumulative(const LayerDev& L, uint32_t* cum) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+__device__ __forceinline__ void build_cumulative(const LayerDev& L, uint32_t* cum) {
+  const int lane = threadIdx.x & 63, wave = (int)wave_id();
   for (int t = wave; t < 16; t += kWavesPerGroup) {
     const uint16_t* f = reinterpret_cast<const uint16_t*>(L.blob + L.tab_off[t]);
     const uint32_t A = L.tab_A[t], base = L.tab_base[t];
@@ -177,7 +234,7 @@ __device__ __forceinline__ int32_t doubled_value(int32_t z, int field, uint32_t 
 }
 
 // Packed slot table: lut[t * M + u] for the 16 field tables (b <= 11).
-__device__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum) {
+__device__ __forceinline__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum) {
   const uint32_t M = 1u << L.b;
   const uint32_t per = M / 64;                     // slots per thread: 16 tables x 64 threads
   const int t = threadIdx.x >> 6, j = threadIdx.x & 63;
@@ -206,81 +263,128 @@ __device__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum)
   }
 }
 
-// ---- the decode of one two-tile task -------------------------------------------
-// Payload staging: each half-wave owns a 512-word ring in LDS.  Word w of the
-// payload section lives in slot w & 511.  Chunks of 256 words (aligned to 256
-// in w) are fetched with four coalesced buffer_load_dword per lane (a raw
-// buffer resource bounds every read to the payload section) into registers,
-// and written to the ring ("committed") only when the consumer gets within 64
-// words of the committed end, by which time the loads have long returned; the
-// following chunk is requested right after each commit.  A commit overwrites
-// the slots of words [Qc - 512, Qc - 256), all consumed by then.
-constexpr uint32_t kRingWords = 512;
-constexpr uint32_t kChunkWords = 256;
-constexpr uint32_t kRingBytesPerWave = 2 * 2 * kRingWords;   // two halves, u16 words
-constexpr uint32_t kRingBytes = kWavesPerGroup * kRingBytesPerWave;
+// LDS bytes of the payload rings of a workgroup (all waves, all halves).
+constexpr uint32_t kRingBytes = 32 * 1024;
 
-struct Stage {
-  __amdgpu_buffer_rsrc_t rsrc;   // payload section
-  uint32_t ring;                 // LDS byte address of this half's ring
-  uint32_t Qc;                   // committed end (words)
-  uint32_t T;                    // commit trigger: P >= T
-  uint32_t Pend;
-  uint32_t pend[4];              // fetched, not yet committed chunk
+// ---- the decode of one wave task ---------------------------------------------------
+// A wave task is NC chains; chain j decodes two tiles, the first on lanes 0-31
+// (half A), the second on lanes 32-63 (half B).  Every half owns a payload ring
+// in LDS: a logical ring of RW words stored twice (physical slots s and s + RW
+// hold the same word), so the up-to-32 words a step reads never wrap.  Chunks
+// of CW = RW/2 words are fetched with bounded raw-buffer loads into registers
+// and written to the ring ("committed") when the consumer pointer reaches the
+// last CW committed words; the next chunk is requested right after.  A commit
+// overwrites words [Qc - RW, Qc - CW), all consumed by then.  The read pointer
+// of each half is kept as a wave-uniform LDS byte address; the per-lane word
+// address is base + 2 * (prefix of the 64-lane refill ballot, corrected for
+// the upper half).
+template <int NC>
+struct RingGeom {
+  static constexpr uint32_t RW = NC == 1 ? 256 : 128;   // logical ring words
+  static constexpr uint32_t CW = RW / 2;                 // chunk words
+  static constexpr uint32_t DW = CW / 64;                // chunk dwords per lane
+  static constexpr uint32_t HALF_BYTES = 4 * RW;         // two copies of RW u16 words
+};
+static_assert(kWavesPerGroup * 2 * 1 * RingGeom<1>::HALF_BYTES <= kRingBytes, "ring area");
+static_assert(kWavesPerGroup * 2 * 2 * RingGeom<2>::HALF_BYTES <= kRingBytes, "ring area");
+
+template <int NC>
+struct HalfRing {          // wave-uniform state of one half's ring
+  uint32_t rbase;          // LDS byte address of the ring
+  uint32_t S2;             // LDS byte address of the next word to read
+  uint32_t T2;             // commit when S2 >= T2
+  uint32_t Qc;             // committed end (payload words)
+  uint32_t base;           // payload word held at physical slot 0 (mod RW)
+  uint32_t C0;             // first chunk start of the tile
+  uint32_t Pend;           // end of the tile's payload window
 };
 
-__device__ __forceinline__ void fetch_chunk(Stage& S, uint32_t l, uint32_t start) {
+template <int NC>
+__device__ __forceinline__ void fetch(uint32_t* pend, __amdgpu_buffer_rsrc_t rsrc, uint32_t l,
+                                      uint32_t start) {
 #pragma unroll
-  for (int k = 0; k < 4; k++)
-    S.pend[k] = __builtin_amdgcn_raw_buffer_load_b32(S.rsrc, 2 * start + 4 * (l + 32 * k), 0, 0);
+  for (uint32_t k = 0; k < RingGeom<NC>::DW; k++)
+    pend[k] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, 2 * start + 4 * (l + 32 * k), 0, 0);
 }
 
-__device__ __forceinline__ void store_chunk(uint8_t* lds_base, const Stage& S, uint32_t l,
-                                            uint32_t start) {
+template <int NC>
+__device__ __forceinline__ void commit_lanes(uint8_t* lds, const uint32_t* pend, uint32_t rbase,
+                                             uint32_t slot0, uint32_t l) {
+  constexpr uint32_t RW = RingGeom<NC>::RW;
 #pragma unroll
-  for (int k = 0; k < 4; k++) {
-    const uint32_t slot = (start + 2 * (l + 32 * k)) & (kRingWords - 1);
-    *reinterpret_cast<uint32_t*>(lds_base + S.ring + 2 * slot) = S.pend[k];
+  for (uint32_t k = 0; k < RingGeom<NC>::DW; k++) {
+    const uint32_t a = rbase + 2 * (slot0 + 2 * (l + 32 * k));
+    *reinterpret_cast<uint32_t*>(lds + a) = pend[k];
+    *reinterpret_cast<uint32_t*>(lds + a + 2 * RW) = pend[k];
   }
 }
 
-// Commit the pending chunk if this half is within 64 words of the committed end.
-__device__ __forceinline__ void stage_check(uint8_t* lds_base, Stage& S, uint32_t P, uint32_t l) {
-  const bool due = P >= S.T;
-  if (__ballot(due)) {
-    if (due) {
-      store_chunk(lds_base, S, l, S.Qc);
-      S.Qc += kChunkWords;
-      S.T = S.Qc - 64;
-      if (S.Qc < S.Pend) fetch_chunk(S, l, S.Qc);
+// Commit the pending chunk of one half (lanes of that half write), advance the
+// window, rebase the read address, and request the following chunk.
+template <int NC>
+__device__ __forceinline__ void commit_half(uint8_t* lds, HalfRing<NC>& R, uint32_t* pend,
+                                            __amdgpu_buffer_rsrc_t rsrc, bool mine, uint32_t l) {
+  constexpr uint32_t RW = RingGeom<NC>::RW, CW = RingGeom<NC>::CW;
+  if (mine) commit_lanes<NC>(lds, pend, R.rbase, (R.Qc - R.C0) & (RW - 1), l);
+  R.Qc += CW;
+  R.T2 += 2 * CW;
+  if (R.S2 - R.rbase >= 2 * RW) {
+    R.S2 -= 2 * RW;
+    R.T2 -= 2 * RW;
+    R.base += RW;
+  }
+  if (mine && R.Qc < R.Pend) fetch<NC>(pend, rsrc, l, R.Qc);
+}
+
+template <int NC>
+__device__ __forceinline__ void ring_start(uint8_t* lds, HalfRing<NC>& R, uint32_t* pend,
+                                           __amdgpu_buffer_rsrc_t rsrc, bool mine, uint32_t l,
+                                           uint32_t P0, uint32_t Pend, uint32_t rbase) {
+  constexpr uint32_t RW = RingGeom<NC>::RW, CW = RingGeom<NC>::CW;
+  R.rbase = rbase;
+  R.C0 = P0 & ~(CW - 1);
+  R.base = R.C0;
+  R.Pend = Pend;
+  R.S2 = rbase + 2 * (P0 - R.C0);
+  if (mine) {
+    fetch<NC>(pend, rsrc, l, R.C0);
+    commit_lanes<NC>(lds, pend, rbase, 0, l);
+    if (R.C0 + CW < Pend) {
+      fetch<NC>(pend, rsrc, l, R.C0 + CW);
+      commit_lanes<NC>(lds, pend, rbase, CW, l);
     }
   }
+  R.Qc = R.C0 + RW;
+  R.T2 = rbase + 2 * CW;
+  if (mine && R.Qc < Pend) fetch<NC>(pend, rsrc, l, R.Qc);
 }
 
-// Refill states below 2^15 from the half-wave's ring (lane order inside each half).
-__device__ __forceinline__ void renorm(uint32_t& x, bool act, uint32_t& P, const uint8_t* lds_base,
-                                       const Stage& S, uint32_t half) {
-  const uint64_t m = __ballot(act && x < kStateLow);
+// One refill step of one chain: 64-lane ballot of states below 2^15, words read
+// from each half's ring in lane order, uniform pointers advanced, commits done.
+template <int NC, bool FULL>
+__device__ __forceinline__ void refill(uint32_t& x, bool act, uint64_t act_mask, HalfRing<NC>& A,
+                                       HalfRing<NC>& Bh, uint8_t* lds, uint32_t* pend,
+                                       __amdgpu_buffer_rsrc_t rsrc, uint32_t half, uint32_t l) {
+  uint64_t m = __ballot(x < kStateLow);
+  if (!FULL) m &= act_mask;
   const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
-  uint32_t idx;
-  if (half) {
-    idx = __builtin_amdgcn_mbcnt_hi(hi, P);
-    P += (uint32_t)__builtin_popcount(hi);
-  } else {
-    idx = __builtin_amdgcn_mbcnt_lo(lo, P);
-    P += (uint32_t)__builtin_popcount(lo);
-  }
-  if (act && x < kStateLow) {
-    const uint32_t word =
-        *reinterpret_cast<const uint16_t*>(lds_base + S.ring + 2 * (idx & (kRingWords - 1)));
-    x = (x << 16) | word;
-  }
+  const uint32_t clo = (uint32_t)__builtin_popcount(lo), chi = (uint32_t)__builtin_popcount(hi);
+  const uint32_t pre = __builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
+  const int32_t dd = (int32_t)((Bh.S2 - A.S2) >> 1) - (int32_t)clo;
+  const uint32_t widx = (uint32_t)(__mul24((int32_t)half, dd) + (int32_t)pre);
+  const uint32_t w = *reinterpret_cast<const uint16_t*>(lds + A.S2 + 2 * widx);
+  const bool need = (FULL || act) && x < kStateLow;
+  x = need ? ((x << 16) | w) : x;
+  A.S2 += 2 * clo;
+  Bh.S2 += 2 * chi;
+  if (A.S2 >= A.T2) commit_half<NC>(lds, A, pend, rsrc, half == 0, l);
+  if (Bh.S2 >= Bh.T2) commit_half<NC>(lds, Bh, pend, rsrc, half == 1, l);
 }
 
 // One field symbol.  Slot-table path: entry = lut[(8c + i - 1) * 2^B + u]; the
 // coset part cb = 8c * 2^B is per lane, the field part a constant offset.
 template <int PATH, int B>
-__device__ __forceinline__ void decode_field(const LayerDev& L, const uint32_t* lds, int field,
+__device__ __forceinline__ void decode_field(const Hot& L, const uint32_t* lds, int field,
                                              uint32_t cb, uint32_t c, uint32_t& x, int32_t& dval) {
   if (PATH == kPathLut) {
     constexpr uint32_t M = 1u << B;
@@ -289,9 +393,11 @@ __device__ __forceinline__ void decode_field(const LayerDev& L, const uint32_t* 
     x = __umul24(e & 0xFFFu, x >> B) + ((e >> 12) & 0x7FFu);
     dval = (int32_t)e >> 23;
   } else {
+    // table metadata after the cumulative entries: base[16], A[16], min[16]
     const uint32_t u = x & ((1u << L.b) - 1);
-    const uint32_t base = c ? L.tab_base[8 + field - 1] : L.tab_base[field - 1];
-    const uint32_t A = c ? L.tab_A[8 + field - 1] : L.tab_A[field - 1];
+    const uint32_t t = 8 * c + (uint32_t)(field - 1);
+    const uint32_t base = lds[L.meta + t];
+    const uint32_t A = lds[L.meta + 16 + t];
     uint32_t s = 0, n = A;
     for (uint32_t it = 0; it < L.search_iters; it++) {
       const uint32_t h = n >> 1;
@@ -300,104 +406,335 @@ __device__ __forceinline__ void decode_field(const LayerDev& L, const uint32_t* 
     }
     const uint32_t e = lds[base + s];
     x = __umul24(e >> 16, x >> L.b) + u - (e & 0xFFFFu);
-    const int32_t mn = c ? L.tab_min[8 + field - 1] : L.tab_min[field - 1];
+    const int32_t mn = (int32_t)lds[L.meta + 32 + t];
     dval = doubled_value((int32_t)s + mn, field, c);
   }
 }
 
-// floor(v / C8) with the host-computed magic (Granlund-Montgomery).
-__device__ __forceinline__ uint32_t row_of(const LayerDev& L, uint32_t v) {
+// floor(v / (C/8)) with the host-computed magic (Granlund-Montgomery).
+__device__ __forceinline__ uint32_t row_of(const Hot& L, uint32_t v) {
   if (L.div_pow2) return v >> L.div_shift;
   const uint32_t q = __umulhi(v, L.div_magic);
   return (q + ((v - q) >> 1)) >> L.div_shift;
 }
 
-template <int PATH, int B>
-__device__ void decode_task(const LayerDev& L, const uint32_t* lds, uint8_t* lds_base,
+template <int PATH, int B, int NC, bool FULL>
+__device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, uint8_t* lds,
                             uint32_t ring_area, uint32_t task, int32_t* status) {
-  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t lane = threadIdx.x & 63, wave = wave_id();
   const uint32_t half = lane >> 5, l = lane & 31;
-  const uint32_t tile = L.tile_begin + 2 * task + half;
-  const bool tile_ok = tile < L.tile_end;
   const uint32_t nvec = L.rows * L.cvec;
-  const uint32_t v0 = tile_ok ? tile * L.V : 0;
-  const uint32_t nv = tile_ok ? min(L.V, nvec - v0) : 0;
-  const uint32_t n_l = l < nv ? (nv - 1 - l) / 32 + 1 : 0;
-  const uint32_t r_here = (nv + 31) / 32;
-  const uint32_t rounds = max(__builtin_amdgcn_readlane(r_here, 0), __builtin_amdgcn_readlane(r_here, 32));
-
   const uint32_t* states = reinterpret_cast<const uint32_t*>(L.blob + L.off_states);
   const uint32_t* offs = reinterpret_cast<const uint32_t*>(L.blob + L.off_offsets);
   const float* sigma = reinterpret_cast<const float*>(L.blob + L.off_sigma);
-  uint32_t x = tile_ok ? states[(uint64_t)tile * 32 + l] : kStateLow;
-  const uint32_t P0 = tile_ok ? offs[tile] : 0;
-  Stage S;
-  S.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(L.blob + L.off_payload), (short)0,
-                                             (int)L.pay_bytes, 0x00020000);
-  S.ring = ring_area + wave * kRingBytesPerWave + half * (2 * kRingWords);
-  S.Pend = tile_ok ? offs[tile + 1] : 0;
-  const uint32_t C0 = P0 & ~(kChunkWords - 1);
-  S.Qc = C0;
-  S.T = 0xFFFFFFFFu;
-  if (tile_ok) {
-    fetch_chunk(S, l, C0);
-    store_chunk(lds_base, S, l, C0);
-    S.Qc = C0 + kChunkWords;
-    if (S.Qc < S.Pend) {
-      fetch_chunk(S, l, S.Qc);
-      store_chunk(lds_base, S, l, S.Qc);
-    }
-    S.Qc += kChunkWords;
-    S.T = S.Qc - 64;
-    if (S.Qc < S.Pend) fetch_chunk(S, l, S.Qc);
-  }
-  uint32_t P = P0;
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_payload), (short)0, (int)L.pay_bytes, 0x00020000);
   const uint32_t mask = (1u << L.b) - 1;
 
+  uint32_t x[NC], v0[NC], n_l[NC], pend[NC][RingGeom<NC>::DW];
+  uint64_t am[NC];
+  HalfRing<NC> RA[NC], RB[NC];
+  uint32_t rounds = 0;
+#pragma unroll
+  for (int j = 0; j < NC; j++) {
+    const uint32_t tA = L.tile_begin + 2 * (NC * task + j);      // uniform
+    const uint32_t tB = tA + 1;
+    const bool okA = tA < L.tile_end, okB = tB < L.tile_end;   // uniform
+    const uint32_t tile = half ? tB : tA;
+    const bool ok = half ? okB : okA;
+    v0[j] = ok ? tile * L.V : 0;
+    const uint32_t nv = ok ? min(L.V, nvec - v0[j]) : 0;
+    n_l[j] = l < nv ? (nv - 1 - l) / 32 + 1 : 0;
+    const uint32_t nvA = okA ? min(L.V, nvec - tA * L.V) : 0;
+    const uint32_t nvB = okB ? min(L.V, nvec - tB * L.V) : 0;
+    rounds = max(rounds, (max(nvA, nvB) + 31) / 32);
+    x[j] = ok ? states[(uint64_t)tile * 32 + l] : kStateLow;
+    const uint32_t rb = ring_area + (wave * NC + j) * 2 * RingGeom<NC>::HALF_BYTES;
+    const uint32_t pa0 = okA ? offs[tA] : 0, pa1 = okA ? offs[tA + 1] : 0;
+    const uint32_t pb0 = okB ? offs[tB] : 0, pb1 = okB ? offs[tB + 1] : 0;
+    ring_start<NC>(lds, RA[j], pend[j], rsrc, half == 0 && okA, l, pa0, pa1, rb);
+    ring_start<NC>(lds, RB[j], pend[j], rsrc, half == 1 && okB, l, pb0, pb1,
+                   rb + RingGeom<NC>::HALF_BYTES);
+  }
+
   for (uint32_t k = 0; k < rounds; k++) {
-    const bool act = k < n_l;
-    const uint32_t v = v0 + l + 32 * k;
-    const float sg = act ? sigma[row_of(L, v)] : 0.0f;
-    // coset symbol
-    uint32_t c = 0, cb = 0;
-    if (act) {
-      const uint32_t u = x & mask;
-      c = u >= L.coset_f0 ? 1u : 0u;
-      const uint32_t f = c ? L.coset_f1 : L.coset_f0;
-      const uint32_t F = c ? L.coset_f0 : 0u;
-      x = __umul24(f, x >> L.b) + u - F;
-      cb = c << (L.b + 3);
+    uint32_t c[NC], cb[NC], v[NC];
+    float sg[NC];
+    bool act[NC];
+    int32_t d[NC][9];
+#pragma unroll
+    for (int j = 0; j < NC; j++) {
+      act[j] = FULL || k < n_l[j];
+      am[j] = FULL ? ~0ull : __ballot(act[j]);
+      v[j] = v0[j] + l + 32 * k;
+      sg[j] = act[j] ? sigma[row_of(L, v[j])] : 0.0f;
+      c[j] = 0;
+      cb[j] = 0;
+      if (act[j]) {   // coset symbol
+        const uint32_t u = x[j] & mask;
+        c[j] = u >= L.coset_f0 ? 1u : 0u;
+        const uint32_t f = c[j] ? L.coset_f1 : L.coset_f0;
+        const uint32_t F = c[j] ? L.coset_f0 : 0u;
+        x[j] = __umul24(f, x[j] >> L.b) + u - F;
+        cb[j] = c[j] << (L.b + 3);
+      }
     }
-    stage_check(lds_base, S, P, l);
-    renorm(x, act, P, lds_base, S, half);
-    int32_t d[9];
+#pragma unroll
+    for (int j = 0; j < NC; j++)
+      refill<NC, FULL>(x[j], act[j], am[j], RA[j], RB[j], lds, pend[j], rsrc, half, l);
 #pragma unroll
     for (int i = 1; i <= 8; i++) {
-      if (act) decode_field<PATH, B>(L, lds, i, cb, c, x, d[i]);
-      stage_check(lds_base, S, P, l);
-      renorm(x, act, P, lds_base, S, half);
-    }
-    if (act) {
-      // field inverse: 2p_i = 2 z_i + c; 2p_8 = 4m + c + 2 pi, pi = sum z_1..7 mod 2
-      int32_t p2[8];
-      int32_t acc = (int32_t)c;
 #pragma unroll
-      for (int i = 1; i <= 7; i++) {
-        p2[i - 1] = d[i];
-        acc += d[i];
+      for (int j = 0; j < NC; j++)
+        if (act[j]) decode_field<PATH, B>(L, tab, i, cb[j], c[j], x[j], d[j][i]);
+#pragma unroll
+      for (int j = 0; j < NC; j++)
+        refill<NC, FULL>(x[j], act[j], am[j], RA[j], RB[j], lds, pend[j], rsrc, half, l);
+    }
+#pragma unroll
+    for (int j = 0; j < NC; j++) {
+      if (act[j]) {
+        // field inverse: 2p_i = 2 z_i + c; 2p_8 = 4m + c + 2 pi, pi = sum z_1..7 mod 2
+        int32_t p2[8];
+        int32_t acc = (int32_t)c[j];
+#pragma unroll
+        for (int i = 1; i <= 7; i++) {
+          p2[i - 1] = d[j][i];
+          acc += d[j][i];
+        }
+        p2[7] = d[j][8] | (acc & 2);
+        store_vector(L, v[j], p2, 0.5f * sg[j]);
       }
-      p2[7] = d[8] + (acc & 2);
-      store_vector(L, v, p2, 0.5f * sg);
     }
   }
+
   uint32_t err = 0;
-  if (tile_ok) {
-    if (x != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
-    if (l == 0 && P != S.Pend) err |= P > S.Pend ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
+#pragma unroll
+  for (int j = 0; j < NC; j++) {
+    const uint32_t tile = L.tile_begin + 2 * (NC * task + j) + half;
+    if (tile < L.tile_end) {
+      if (x[j] != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
+      const HalfRing<NC>& R = half ? RB[j] : RA[j];
+      const uint32_t P = R.base + (R.S2 - R.rbase) / 2;
+      if (l == 0 && P != R.Pend) err |= P > R.Pend ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
+      if (L.container && L.dequant) {
+        const float* delta = reinterpret_cast<const float*>(L.blob + L.off_delta);
+        const uint32_t nv = min(L.V, nvec - v0[j]);
+        const uint32_t r_first = (v0[j] + L.cvec - 1) / L.cvec;
+        const uint32_t r_last = (v0[j] + nv - 1) / L.cvec;
+        for (uint32_t r = r_first + l; r <= r_last; r += 32) L.dequant[r] = delta[r];
+      }
+    }
+  }
+  if (err && status) atomicOr(status, (int32_t)err);
+}
+
+// ---- hand-scheduled steady state: slot-table path, full tasks, two chains --------
+// Each asm block advances both chains of the wave by one symbol: two slot-table
+// reads issued back to back, the rANS state update (eq. rans_decode), then per
+// chain the 64-lane refill ballot, the per-half word index from v_mbcnt
+// (upper-half lanes corrected by the uniform distance between the two rings),
+// the ring read, and the scalar advance of both ring pointers.  The merge of
+// the refilled states waits for both ring reads at the end.
+#define EP_REFILL(X, T, W, CLO, CHI, SA, SB, SAVE)                  \
+  "v_cmp_gt_u32_e32 vcc, 0x8000, %[" X "]\n\t"                        \
+  "s_bcnt1_i32_b32 %[" CLO "], vcc_lo\n\t"                           \
+  "s_bcnt1_i32_b32 %[" CHI "], vcc_hi\n\t"                           \
+  "v_mbcnt_lo_u32_b32 %[" T "], vcc_lo, 0\n\t"                        \
+  "v_mbcnt_hi_u32_b32 %[" T "], vcc_hi, %[" T "]\n\t"                 \
+  "s_sub_u32 %[dd], %[" SB "], %[" SA "]\n\t"                        \
+  "s_ashr_i32 %[dd], %[dd], 1\n\t"                                    \
+  "s_sub_u32 %[dd], %[dd], %[" CLO "]\n\t"                           \
+  "v_mad_i32_i24 %[" T "], %[vH], %[dd], %[" T "]\n\t"                \
+  "v_lshl_add_u32 %[" T "], %[" T "], 1, %[" SA "]\n\t"               \
+  "ds_read_u16 %[" W "], %[" T "]\n\t"                                \
+  SAVE                                                                \
+  "s_lshl1_add_u32 %[" SA "], %[" CLO "], %[" SA "]\n\t"             \
+  "s_lshl1_add_u32 %[" SB "], %[" CHI "], %[" SB "]\n\t"
+
+#define EP_MERGE                                                      \
+  "s_waitcnt lgkmcnt(0)\n\t"                                          \
+  "v_lshl_or_b32 %[w0], %[x0], 16, %[w0]\n\t"                        \
+  "v_cndmask_b32_e64 %[x0], %[x0], %[w0], %[m0]\n\t"                 \
+  "v_lshl_or_b32 %[w1], %[x1], 16, %[w1]\n\t"                        \
+  "v_cndmask_b32_e32 %[x1], %[x1], %[w1], vcc\n\t"
+
+#define EP_STEP_OUTS                                                                      \
+  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(SA0), [SB0] "+s"(SB0), [SA1] "+s"(SA1),        \
+      [SB1] "+s"(SB1), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),    \
+      [g0] "=&v"(g0), [g1] "=&v"(g1), [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0),     \
+      [w1] "=&v"(w1), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo),          \
+      [c1hi] "=&s"(c1hi), [dd] "=&s"(dd), [m0] "=&s"(m0)
+
+// Field symbol (table 8c + FIELD - 1) for both chains, then refill.
+template <int B, int FIELD>
+__device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
+                                            int32_t& d0, int32_t& d1, uint32_t& SA0, uint32_t& SB0,
+                                            uint32_t& SA1, uint32_t& SB1, uint32_t vH) {
+  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd;
+  uint64_t m0;
+  asm volatile(
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
+      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
+      "v_lshl_add_u32 %[u0], %[u0], 2, %[cb0]\n\t"
+      "v_lshl_add_u32 %[u1], %[u1], 2, %[cb1]\n\t"
+      "ds_read_b32 %[e0], %[u0] offset:%[off]\n\t"
+      "ds_read_b32 %[e1], %[u1] offset:%[off]\n\t"
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
+      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
+      "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
+      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
+      "v_ashrrev_i32 %[d0], 23, %[e0]\n\t"
+      "v_and_b32 %[u1], 0xfff, %[e1]\n\t"
+      "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"
+      "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"
+      "v_ashrrev_i32 %[d1], 23, %[e1]\n\t"
+      EP_REFILL("x0", "t0", "w0", "c0lo", "c0hi", "SA0", "SB0", "s_mov_b64 %[m0], vcc\n\t")
+      EP_REFILL("x1", "t1", "w1", "c1lo", "c1hi", "SA1", "SB1", "")
+      EP_MERGE
+      : EP_STEP_OUTS, [d0] "=&v"(d0), [d1] "=&v"(d1)
+      : [cb0] "v"(cb0), [cb1] "v"(cb1), [vH] "v"(vH), [mk] "i"((1 << B) - 1), [b] "i"(B),
+        [off] "i"((FIELD - 1) * (4 << B))
+      : "vcc", "scc", "memory");
+}
+
+// Coset symbol (two-entry table f0, f1) for both chains, then refill.  Returns
+// c and the per-lane LDS byte base of its slot tables, cb = 4 * 8c * 2^B.
+template <int B>
+__device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t& c0, uint32_t& c1,
+                                            uint32_t& cb0, uint32_t& cb1, uint32_t f0, uint32_t vf1,
+                                            uint32_t& SA0, uint32_t& SB0, uint32_t& SA1,
+                                            uint32_t& SB1, uint32_t vH) {
+  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd;
+  uint64_t m0;
+  asm volatile(
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
+      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
+      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
+      "v_cmp_le_u32_e32 vcc, %[vf0], %[u0]\n\t"
+      "v_cndmask_b32_e32 %[e0], %[vf0], %[vf1], vcc\n\t"
+      "v_cndmask_b32_e32 %[t0], 0, %[vf0], vcc\n\t"
+      "v_cndmask_b32_e64 %[c0], 0, 1, vcc\n\t"
+      "v_mad_u32_u24 %[x0], %[e0], %[g0], %[u0]\n\t"
+      "v_sub_u32_e32 %[x0], %[x0], %[t0]\n\t"
+      "v_cmp_le_u32_e32 vcc, %[vf0], %[u1]\n\t"
+      "v_cndmask_b32_e32 %[e1], %[vf0], %[vf1], vcc\n\t"
+      "v_cndmask_b32_e32 %[t1], 0, %[vf0], vcc\n\t"
+      "v_cndmask_b32_e64 %[c1], 0, 1, vcc\n\t"
+      "v_mad_u32_u24 %[x1], %[e1], %[g1], %[u1]\n\t"
+      "v_sub_u32_e32 %[x1], %[x1], %[t1]\n\t"
+      "v_lshlrev_b32 %[cb0], %[b3], %[c0]\n\t"
+      "v_lshlrev_b32 %[cb1], %[b3], %[c1]\n\t"
+      EP_REFILL("x0", "t0", "w0", "c0lo", "c0hi", "SA0", "SB0", "s_mov_b64 %[m0], vcc\n\t")
+      EP_REFILL("x1", "t1", "w1", "c1lo", "c1hi", "SA1", "SB1", "")
+      EP_MERGE
+      : EP_STEP_OUTS, [c0] "=&v"(c0), [c1] "=&v"(c1), [cb0] "=&v"(cb0), [cb1] "=&v"(cb1)
+      : [vf0] "v"(f0), [vf1] "v"(vf1), [vH] "v"(vH), [mk] "i"((1 << B) - 1), [b] "i"(B),
+        [b3] "i"(B + 5)
+      : "vcc", "scc", "memory");
+}
+
+template <int B>
+__device__ __forceinline__ void commit_checks(uint8_t* lds, HalfRing<2>* RA, HalfRing<2>* RB,
+                                              uint32_t (*pend)[1], __amdgpu_buffer_rsrc_t rsrc,
+                                              uint32_t half, uint32_t l) {
+#pragma unroll
+  for (int j = 0; j < 2; j++) {
+    if (RA[j].S2 >= RA[j].T2) commit_half<2>(lds, RA[j], pend[j], rsrc, half == 0, l);
+    if (RB[j].S2 >= RB[j].T2) commit_half<2>(lds, RB[j], pend[j], rsrc, half == 1, l);
+  }
+}
+
+// The steady-state task: four full tiles (two chains), slot-table path.
+template <int B>
+__device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uint32_t ring_area,
+                                                 uint32_t task, int32_t* status) {
+  constexpr int NC = 2;
+  const uint32_t lane = threadIdx.x & 63, wave = wave_id();
+  const uint32_t half = lane >> 5, l = lane & 31;
+  const uint32_t* states = reinterpret_cast<const uint32_t*>(L.blob + L.off_states);
+  const uint32_t* offs = reinterpret_cast<const uint32_t*>(L.blob + L.off_offsets);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_payload), (short)0, (int)L.pay_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_sigma), (short)0, (int)(4 * L.rows), 0x00020000);
+
+  uint32_t x[NC], v0[NC], row[NC], col[NC], pend[NC][1];
+  HalfRing<NC> RA[NC], RB[NC];
+#pragma unroll
+  for (int j = 0; j < NC; j++) {
+    const uint32_t tA = L.tile_begin + 2 * (NC * task + j);
+    const uint32_t tB = tA + 1;
+    const uint32_t tile = half ? tB : tA;
+    v0[j] = tile * L.V;
+    x[j] = states[(uint64_t)tile * 32 + l];
+    const uint32_t vv = v0[j] + l;
+    row[j] = row_of(L, vv);
+    col[j] = vv - row[j] * L.cvec;
+    const uint32_t rb = ring_area + (wave * NC + j) * 2 * RingGeom<NC>::HALF_BYTES;
+    ring_start<NC>(lds, RA[j], pend[j], rsrc, half == 0, l, uni(offs[tA]), uni(offs[tA + 1]), rb);
+    ring_start<NC>(lds, RB[j], pend[j], rsrc, half == 1, l, uni(offs[tB]), uni(offs[tB + 1]),
+                   rb + RingGeom<NC>::HALF_BYTES);
+  }
+  const uint32_t vH = half;
+  const uint32_t vf1 = L.coset_f1;
+  const uint32_t rounds = L.V / 32;
+  const bool wide = L.cvec >= 32;
+
+  for (uint32_t k = 0; k < rounds; k++) {
+    float sg[NC];
+#pragma unroll
+    for (int j = 0; j < NC; j++)
+      sg[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row[j], 0, 0));
+    uint32_t c[NC], cb[NC];
+    int32_t d[NC][9];
+    coset_step2<B>(x[0], x[1], c[0], c[1], cb[0], cb[1], L.coset_f0, vf1, RA[0].S2, RB[0].S2,
+                   RA[1].S2, RB[1].S2, vH);
+    commit_checks<B>(lds, RA, RB, pend, rsrc, half, l);
+#define EP_FIELD(I)                                                                            \
+  field_step2<B, I>(x[0], x[1], cb[0], cb[1], d[0][I], d[1][I], RA[0].S2, RB[0].S2, RA[1].S2,  \
+                    RB[1].S2, vH);                                                             \
+  commit_checks<B>(lds, RA, RB, pend, rsrc, half, l);
+    EP_FIELD(1) EP_FIELD(2) EP_FIELD(3) EP_FIELD(4) EP_FIELD(5) EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
+#undef EP_FIELD
+#pragma unroll
+    for (int j = 0; j < NC; j++) {
+      int32_t p2[8];
+      int32_t acc = (int32_t)c[j];
+#pragma unroll
+      for (int i = 1; i <= 7; i++) {
+        p2[i - 1] = d[j][i];
+        acc += d[j][i];
+      }
+      p2[7] = d[j][8] | (acc & 2);
+      store_vector(L, v0[j] + l + 32 * k, p2, 0.5f * sg[j]);
+      // next vector of this lane: 32 vectors further
+      if (wide) {
+        col[j] += 32;
+        if (col[j] >= L.cvec) {
+          col[j] -= L.cvec;
+          row[j] += 1;
+        }
+      } else {
+        row[j] = row_of(L, v0[j] + l + 32 * (k + 1));
+      }
+    }
+  }
+
+  uint32_t err = 0;
+#pragma unroll
+  for (int j = 0; j < NC; j++) {
+    if (x[j] != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
+    const HalfRing<NC>& R = half ? RB[j] : RA[j];
+    const uint32_t P = R.base + (R.S2 - R.rbase) / 2;
+    if (l == 0 && P != R.Pend) err |= P > R.Pend ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
     if (L.container && L.dequant) {
       const float* delta = reinterpret_cast<const float*>(L.blob + L.off_delta);
-      const uint32_t r_first = (v0 + L.cvec - 1) / L.cvec;
-      const uint32_t r_last = (v0 + nv - 1) / L.cvec;
+      const uint32_t r_first = (v0[j] + L.cvec - 1) / L.cvec;
+      const uint32_t r_last = (v0[j] + L.V - 1) / L.cvec;
       for (uint32_t r = r_first + l; r <= r_last; r += 32) L.dequant[r] = delta[r];
     }
   }
@@ -408,11 +745,11 @@ __device__ void decode_task(const LayerDev& L, const uint32_t* lds, uint8_t* lds
 // after the cumulative table (search path).
 template <int PATH>
 __device__ __forceinline__ uint32_t ring_offset(const LayerDev& L) {
-  return PATH == kPathLut ? (64u << L.b) : ((4u * L.sum_A + 15u) & ~15u);
+  return PATH == kPathLut ? (64u << L.b) : ((4u * (L.sum_A + 48u) + 15u) & ~15u);
 }
 
 template <int PATH>
-__device__ void build_tables(const LayerDev& L, uint32_t* lds) {
+__device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
   if (PATH == kPathLut) {
     uint32_t* cum = lds + (16u << L.b);   // scratch inside the ring area
     build_cumulative(L, cum);
@@ -420,19 +757,55 @@ __device__ void build_tables(const LayerDev& L, uint32_t* lds) {
     build_lut(L, lds, cum);
   } else {
     build_cumulative(L, lds);
+    if (threadIdx.x < 48) {
+      const uint32_t t = threadIdx.x & 15, k = threadIdx.x >> 4;
+      lds[L.sum_A + threadIdx.x] = k == 0 ? L.tab_base[t] : k == 1 ? L.tab_A[t] : (uint32_t)L.tab_min[t];
+    }
   }
+}
+
+// Tiles per wave task and the specialisation of a task: all of its tiles full
+// (V vectors, V a multiple of 32) or not.
+constexpr int kChains = 2;
+constexpr uint32_t kTilesPerTask = 2 * kChains;
+static_assert(kChains == 2, "the hand-scheduled steady state advances two chains per wave");
+
+template <int PATH, int B>
+__device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_t* lb,
+                                       uint32_t ring_area, uint32_t task, int32_t* status) {
+  const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
+  const uint32_t nvec = L.rows * L.cvec;
+  const bool full = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
+                    (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
+  if constexpr (PATH == kPathLut) {
+    if (full) {
+      decode_task_fast<B>(L, lb, ring_area, task, status);
+      return;
+    }
+  }
+  if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, task, status);
+  else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, task, status);
+}
+
+template <int PATH>
+__device__ __forceinline__ void dispatch_task(const Hot& L, const uint32_t* tab, uint8_t* lb,
+                                              uint32_t ring_area, uint32_t task, int32_t* status) {
+  if (PATH == kPathSearch) task_b<PATH, 0>(L, tab, lb, ring_area, task, status);
+  else if (L.b == 11) task_b<PATH, 11>(L, tab, lb, ring_area, task, status);
+  else if (L.b == 10) task_b<PATH, 10>(L, tab, lb, ring_area, task, status);
+  else task_b<PATH, 9>(L, tab, lb, ring_area, task, status);
 }
 
 // Decode global tasks [t_begin, t_end) of a layer list: per layer segment the
 // workgroup builds that layer's tables, then its waves take tasks in turn.
 template <int PATH>
-__device__ void run_layers(const LayerDev* layers, int n_layers, uint32_t total,
+__device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers, uint32_t total,
                            uint32_t per_group, int32_t* status) {
   extern __shared__ uint32_t lds[];
   const uint32_t t_begin = blockIdx.x * per_group;
   const uint32_t t_end = min(total, t_begin + per_group);
   if (t_begin >= t_end) return;
-  const uint32_t wave = threadIdx.x >> 6;
+  const uint32_t wave = wave_id();
   int li = 0;
   while (li + 1 < n_layers && layers[li + 1].task_begin <= t_begin) li++;
   for (uint32_t seg = t_begin; seg < t_end && li < n_layers; li++) {
@@ -442,14 +815,12 @@ __device__ void run_layers(const LayerDev* layers, int n_layers, uint32_t total,
     __syncthreads();
     build_tables<PATH>(L, lds);
     __syncthreads();
-    const uint32_t ring_area = ring_offset<PATH>(L);
+    const uint32_t ring_area = uni(ring_offset<PATH>(L));
+    const uint32_t first = uni(L.task_begin);
+    const Hot H = make_hot(L);
     uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
-    for (uint32_t task = seg + wave; task < seg_end; task += kWavesPerGroup) {
-      if (PATH == kPathSearch) decode_task<PATH, 0>(L, lds, lb, ring_area, task - L.task_begin, status);
-      else if (L.b == 11) decode_task<PATH, 11>(L, lds, lb, ring_area, task - L.task_begin, status);
-      else if (L.b == 10) decode_task<PATH, 10>(L, lds, lb, ring_area, task - L.task_begin, status);
-      else decode_task<PATH, 9>(L, lds, lb, ring_area, task - L.task_begin, status);
-    }
+    for (uint32_t task = seg + wave; task < seg_end; task += kWavesPerGroup)
+      dispatch_task<PATH>(H, lds, lb, ring_area, task - first, status);
     seg = seg_end;
   }
 }
@@ -466,11 +837,20 @@ template <int PATH>
 __global__ __launch_bounds__(kThreads) void decode_args_kernel(const LayerList list, int n_layers,
                                                                uint32_t total, uint32_t per_group,
                                                                int32_t* status) {
-  run_layers<PATH>(list.L, n_layers, total, per_group, status);
+  // The list is the first kernel argument: index it in the kernel-argument
+  // segment itself (scalar loads) instead of copying the by-value struct.
+#if defined(__HIP_DEVICE_COMPILE__)
+  (void)list;
+  const LayerDev* layers = (const LayerDev*)__builtin_amdgcn_kernarg_segment_ptr();
+#else
+  const LayerDev* layers = list.L;
+#endif
+  run_layers<PATH>(layers, n_layers, total, per_group, status);
 }
 
 template <int PATH>
-__global__ __launch_bounds__(kThreads) void decode_ws_kernel(const LayerDev* layers, int n_layers,
+__global__ __launch_bounds__(kThreads) void decode_ws_kernel(const LayerDev* __restrict__ layers,
+                                                             int n_layers,
                                                              uint32_t total, uint32_t per_group,
                                                              int32_t* status) {
   run_layers<PATH>(layers, n_layers, total, per_group, status);
@@ -501,7 +881,7 @@ DeviceProps device_props() {
 
 uint32_t lds_bytes(uint32_t path, const ep_tensor_info& I) {
   if (path == kPathLut) return (64u << I.prob_bits) + kRingBytes;
-  return ((4u * I.sum_alphabet + 15u) & ~15u) + kRingBytes;
+  return ((4u * (I.sum_alphabet + 48u) + 15u) & ~15u) + kRingBytes;
 }
 
 float dtype_max(int dt) {
@@ -540,7 +920,7 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
   D.container = I.container;
   D.tile_begin = t0;
   D.tile_end = t1;
-  D.n_tasks = (t1 - t0 + 1) / 2;
+  D.n_tasks = (t1 - t0 + kTilesPerTask - 1) / kTilesPerTask;
   D.out_dtype = (uint32_t)out_dtype;
   D.saturate = I.max_abs_weight >= dtype_max(out_dtype) ? 1u : 0u;
   D.coset_f0 = I.coset_f0;

@@ -22,7 +22,7 @@ constexpr uint32_t kSearchLdsBytes = 128 * 1024;   // the payload rings take the
 inline uint32_t choose_path(const ep_tensor_info& I) {
   if (I.prob_bits <= kLutMaxBits && I.coord2_min >= kLutValueMin && I.coord2_max <= kLutValueMax)
     return kPathLut;
-  if (4ull * I.sum_alphabet + 16 <= kSearchLdsBytes) return kPathSearch;
+  if (4ull * (I.sum_alphabet + 48) + 16 <= kSearchLdsBytes) return kPathSearch;
   return kPathNone;
 }
 
