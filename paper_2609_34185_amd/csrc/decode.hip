@@ -46,6 +46,17 @@ __device__ __forceinline__ uint32_t wave_id() {
   return (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 }
 
+// Global-memory views of the caller's pointers.  Accesses through them are
+// global (not flat) instructions, so they count only against vmcnt and never
+// delay the waits for LDS reads.
+#define EP_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ EP_GLOBAL T* gptr(const void* p) {
+  return (EP_GLOBAL T*)const_cast<void*>(p);
+}
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 struct LayerDev {
   const uint8_t* blob;
   void* out;
@@ -131,6 +142,9 @@ __device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
 }
 
 __device__ __forceinline__ uint32_t fp16_pair(float a, float b) {
+  // The product is rounded to FP32 first: keep the compiler from fusing the
+  // multiply into a mixed-precision FMA that rounds once, to FP16.
+  asm("" : "+v"(a), "+v"(b));
   _Float16 ha = (_Float16)a, hb = (_Float16)b;
   uint16_t ua, ub;
   __builtin_memcpy(&ua, &ha, 2);
@@ -152,56 +166,68 @@ __device__ __forceinline__ uint32_t int8_quad(float a, float b, float c, float d
          ((uint32_t)(id & 0xFF) << 24);
 }
 
-// Store the eight weights of vector v (elements 8v..8v+7).
-__device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int32_t* p2,
-                                             float half_sigma) {
+// Store the eight weights of vector v (elements 8v..8v+7), output type DT,
+// saturating to the type's finite range when SAT.
+template <int DT, bool SAT>
+__device__ __forceinline__ void store_vec(void* out, uint32_t v, const int32_t* p2,
+                                          float half_sigma) {
   float y[8];
 #pragma unroll
   for (int j = 0; j < 8; j++) y[j] = half_sigma * (float)p2[j];
+  if constexpr (DT == EP_BF16) {
+    if constexpr (SAT)
+#pragma unroll
+      for (int j = 0; j < 8; j++) y[j] = sat(y[j], 3.38953139e38f);
+    const u32x4 o = {bf16_pair(y[0], y[1]), bf16_pair(y[2], y[3]), bf16_pair(y[4], y[5]),
+                     bf16_pair(y[6], y[7])};
+    gptr<u32x4>(out)[v] = o;
+  } else if constexpr (DT == EP_FP16) {
+    if constexpr (SAT)
+#pragma unroll
+      for (int j = 0; j < 8; j++) y[j] = sat(y[j], 65504.0f);
+    const u32x4 o = {fp16_pair(y[0], y[1]), fp16_pair(y[2], y[3]), fp16_pair(y[4], y[5]),
+                     fp16_pair(y[6], y[7])};
+    gptr<u32x4>(out)[v] = o;
+  } else if constexpr (DT == EP_FP32) {
+    EP_GLOBAL u32x4* o = gptr<u32x4>(out) + 2ull * v;
+    o[0] = u32x4{__float_as_uint(y[0]), __float_as_uint(y[1]), __float_as_uint(y[2]),
+                 __float_as_uint(y[3])};
+    o[1] = u32x4{__float_as_uint(y[4]), __float_as_uint(y[5]), __float_as_uint(y[6]),
+                 __float_as_uint(y[7])};
+  } else if constexpr (DT == EP_FP8_E4M3) {
+    if constexpr (SAT)
+#pragma unroll
+      for (int j = 0; j < 8; j++) y[j] = sat(y[j], 448.0f);
+    const u32x2 o = {fp8_quad(y[0], y[1], y[2], y[3]), fp8_quad(y[4], y[5], y[6], y[7])};
+    gptr<u32x2>(out)[v] = o;
+  } else if constexpr (DT == EP_INT8) {
+    const u32x2 o = {int8_quad(y[0], y[1], y[2], y[3]), int8_quad(y[4], y[5], y[6], y[7])};
+    gptr<u32x2>(out)[v] = o;
+  } else {  // EP_COORD2_I32
+    EP_GLOBAL u32x4* o = gptr<u32x4>(out) + 2ull * v;
+    o[0] = u32x4{(uint32_t)p2[0], (uint32_t)p2[1], (uint32_t)p2[2], (uint32_t)p2[3]};
+    o[1] = u32x4{(uint32_t)p2[4], (uint32_t)p2[5], (uint32_t)p2[6], (uint32_t)p2[7]};
+  }
+}
+
+__device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int32_t* p2,
+                                             float half_sigma) {
   switch (L.out_dtype) {
-    case EP_BF16: {
-      if (L.saturate)
-#pragma unroll
-        for (int j = 0; j < 8; j++) y[j] = sat(y[j], 3.38953139e38f);
-      uint4 o = {bf16_pair(y[0], y[1]), bf16_pair(y[2], y[3]), bf16_pair(y[4], y[5]),
-                 bf16_pair(y[6], y[7])};
-      reinterpret_cast<uint4*>(L.out)[v] = o;
+    case EP_BF16:
+      if (L.saturate) store_vec<EP_BF16, true>(L.out, v, p2, half_sigma);
+      else store_vec<EP_BF16, false>(L.out, v, p2, half_sigma);
       break;
-    }
-    case EP_FP16: {
-      if (L.saturate)
-#pragma unroll
-        for (int j = 0; j < 8; j++) y[j] = sat(y[j], 65504.0f);
-      uint4 o = {fp16_pair(y[0], y[1]), fp16_pair(y[2], y[3]), fp16_pair(y[4], y[5]),
-                 fp16_pair(y[6], y[7])};
-      reinterpret_cast<uint4*>(L.out)[v] = o;
+    case EP_FP16:
+      if (L.saturate) store_vec<EP_FP16, true>(L.out, v, p2, half_sigma);
+      else store_vec<EP_FP16, false>(L.out, v, p2, half_sigma);
       break;
-    }
-    case EP_FP32: {
-      float4* o = reinterpret_cast<float4*>(L.out) + 2ull * v;
-      o[0] = make_float4(y[0], y[1], y[2], y[3]);
-      o[1] = make_float4(y[4], y[5], y[6], y[7]);
+    case EP_FP32: store_vec<EP_FP32, false>(L.out, v, p2, half_sigma); break;
+    case EP_FP8_E4M3:
+      if (L.saturate) store_vec<EP_FP8_E4M3, true>(L.out, v, p2, half_sigma);
+      else store_vec<EP_FP8_E4M3, false>(L.out, v, p2, half_sigma);
       break;
-    }
-    case EP_FP8_E4M3: {
-      if (L.saturate)
-#pragma unroll
-        for (int j = 0; j < 8; j++) y[j] = sat(y[j], 448.0f);
-      uint2 o = {fp8_quad(y[0], y[1], y[2], y[3]), fp8_quad(y[4], y[5], y[6], y[7])};
-      reinterpret_cast<uint2*>(L.out)[v] = o;
-      break;
-    }
-    case EP_INT8: {
-      uint2 o = {int8_quad(y[0], y[1], y[2], y[3]), int8_quad(y[4], y[5], y[6], y[7])};
-      reinterpret_cast<uint2*>(L.out)[v] = o;
-      break;
-    }
-    default: {  // EP_COORD2_I32
-      int4* o = reinterpret_cast<int4*>(L.out) + 2ull * v;
-      o[0] = make_int4(p2[0], p2[1], p2[2], p2[3]);
-      o[1] = make_int4(p2[4], p2[5], p2[6], p2[7]);
-      break;
-    }
+    case EP_INT8: store_vec<EP_INT8, false>(L.out, v, p2, half_sigma); break;
+    default: store_vec<EP_COORD2_I32, false>(L.out, v, p2, half_sigma); break;
   }
 }
 
@@ -211,7 +237,7 @@ __device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int
 __device__ __forceinline__ void build_cumulative(const LayerDev& L, uint32_t* cum) {
   const int lane = threadIdx.x & 63, wave = (int)wave_id();
   for (int t = wave; t < 16; t += kWavesPerGroup) {
-    const uint16_t* f = reinterpret_cast<const uint16_t*>(L.blob + L.tab_off[t]);
+    const EP_GLOBAL uint16_t* f = gptr<const uint16_t>(L.blob + L.tab_off[t]);
     const uint32_t A = L.tab_A[t], base = L.tab_base[t];
     uint32_t running = 0;
     for (uint32_t s0 = 0; s0 < A; s0 += kWaveSize) {
@@ -233,11 +259,12 @@ __device__ __forceinline__ int32_t doubled_value(int32_t z, int field, uint32_t 
   return field < 8 ? 2 * z + (int32_t)c : 4 * z + (int32_t)c;
 }
 
-// Packed slot table: lut[t * M + u] for the 16 field tables (b <= 11).
-__device__ __forceinline__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum) {
+// Packed slot table: lut[t * M + u] for the 16 field tables (b <= 11).  Wave
+// w fills tables w, w + kWavesPerGroup, ...; each lane a run of M/64 slots.
+__device__ __forceinline__ void build_lut_table(const LayerDev& L, uint32_t* lut,
+                                                const uint32_t* cum, int t, int j) {
   const uint32_t M = 1u << L.b;
-  const uint32_t per = M / 64;                     // slots per thread: 16 tables x 64 threads
-  const int t = threadIdx.x >> 6, j = threadIdx.x & 63;
+  const uint32_t per = M / 64;
   const uint32_t A = L.tab_A[t], base = L.tab_base[t];
   const uint32_t u0 = j * per;
   uint32_t* row = lut + t * M;
@@ -261,6 +288,11 @@ __device__ __forceinline__ void build_lut(const LayerDev& L, uint32_t* lut, cons
     int32_t val = doubled_value((int32_t)s + L.tab_min[t], field, c);
     row[u] = f | ((u - F) << 12) | (((uint32_t)val & 0x1FFu) << 23);
   }
+}
+
+__device__ __forceinline__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum) {
+  for (int t = (int)wave_id(); t < 16; t += kWavesPerGroup)
+    build_lut_table(L, lut, cum, t, threadIdx.x & 63);
 }
 
 // LDS bytes of the payload rings of a workgroup (all waves, all halves).
@@ -424,9 +456,9 @@ __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, u
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
   const uint32_t half = lane >> 5, l = lane & 31;
   const uint32_t nvec = L.rows * L.cvec;
-  const uint32_t* states = reinterpret_cast<const uint32_t*>(L.blob + L.off_states);
-  const uint32_t* offs = reinterpret_cast<const uint32_t*>(L.blob + L.off_offsets);
-  const float* sigma = reinterpret_cast<const float*>(L.blob + L.off_sigma);
+  const EP_GLOBAL uint32_t* states = gptr<const uint32_t>(L.blob + L.off_states);
+  const EP_GLOBAL uint32_t* offs = gptr<const uint32_t>(L.blob + L.off_offsets);
+  const EP_GLOBAL float* sigma = gptr<const float>(L.blob + L.off_sigma);
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(L.blob + L.off_payload), (short)0, (int)L.pay_bytes, 0x00020000);
   const uint32_t mask = (1u << L.b) - 1;
@@ -518,11 +550,11 @@ __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, u
       const uint32_t P = R.base + (R.S2 - R.rbase) / 2;
       if (l == 0 && P != R.Pend) err |= P > R.Pend ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
       if (L.container && L.dequant) {
-        const float* delta = reinterpret_cast<const float*>(L.blob + L.off_delta);
+        const EP_GLOBAL float* delta = gptr<const float>(L.blob + L.off_delta);
         const uint32_t nv = min(L.V, nvec - v0[j]);
         const uint32_t r_first = (v0[j] + L.cvec - 1) / L.cvec;
         const uint32_t r_last = (v0[j] + nv - 1) / L.cvec;
-        for (uint32_t r = r_first + l; r <= r_last; r += 32) L.dequant[r] = delta[r];
+        for (uint32_t r = r_first + l; r <= r_last; r += 32) gptr<float>(L.dequant)[r] = delta[r];
       }
     }
   }
@@ -530,27 +562,78 @@ __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, u
 }
 
 // ---- hand-scheduled steady state: slot-table path, full tasks, two chains --------
-// Each asm block advances both chains of the wave by one symbol: two slot-table
-// reads issued back to back, the rANS state update (eq. rans_decode), then per
-// chain the 64-lane refill ballot, the per-half word index from v_mbcnt
-// (upper-half lanes corrected by the uniform distance between the two rings),
-// the ring read, and the scalar advance of both ring pointers.  The merge of
-// the refilled states waits for both ring reads at the end.
-#define EP_REFILL(X, T, W, CLO, CHI, SA, SB, SAVE)                  \
+// Payload staging.  Each half (one tile's stream) owns a 512-byte ring in LDS
+// (256 words) that is addressed modulo its size, so a step's reads need no
+// second copy of the ring.  Words arrive in 128-word blocks, one dwordx2 per
+// lane of the half: a block is requested into registers (pend) and committed
+// to the ring at a later symbol round, once the ring has room for it.  The
+// output of a round waits for the global loads in flight, so a block requested
+// at the start of a round has landed by the start of the next one; there is no
+// other wait on global memory in the loop.  Between commits the reads of a
+// step stay inside committed words: a step reads at most 32 words per half,
+// and the committed margin is restored to >= 128 words at the start of a
+// round and to >= 96 words after steps 3 and 6.
+constexpr uint32_t kFastRingBytes = 512;
+constexpr uint32_t kFastRingWords = kFastRingBytes / 2;
+constexpr uint32_t kFastBlockWords = 128;
+constexpr uint32_t kFastChainBytes = 2 * kFastRingBytes;
+constexpr uint32_t kFastOob = 0x80000000u;   // buffer offset past any payload section
+static_assert(kWavesPerGroup * 2 * kFastChainBytes <= kRingBytes, "fast ring area");
+
+struct FastChain {     // wave-uniform, in payload words
+  uint32_t OA, OB;     // read position, from the first block of each half's stream
+  uint32_t QA, QB;     // committed end, same origin
+  uint32_t CA, CB;     // payload word index of that first block
+  uint32_t EA, EB;     // end of each tile's stream, same origin as CA / CB
+};
+
+// Commit the staged block of half A (lanes 0-31, registers pendA) if its
+// margin is below `limit`, and request its next block; likewise half B (lanes
+// 32-63, pendB).  The positions stay wave-uniform (scalar registers); only the
+// commit and the request are per lane.  Separate staging registers per half
+// keep a commit of one half from waiting for the other half's request.
+__device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pendB, uint8_t* lds,
+                                           uint32_t vrb8,
+                                           uint32_t vl8, __amdgpu_buffer_rsrc_t rsrc,
+                                           uint32_t half, uint32_t limit) {
+  const bool cA = uni(F.QA - F.OA) < limit, cB = uni(F.QB - F.OB) < limit;
+  if (cA || cB) {
+    if (cA && half == 0) {
+      *reinterpret_cast<u32x2*>(lds + vrb8 + 2 * (F.QA & (kFastRingWords - 1))) = pendA;
+      const uint32_t a = F.QA + kFastBlockWords;
+      pendA = __builtin_amdgcn_raw_buffer_load_b64(
+          rsrc, uni(a < F.EA ? 2 * (F.CA + a) : kFastOob) + vl8, 0, 0);
+    }
+    if (cB && half == 1) {
+      *reinterpret_cast<u32x2*>(lds + vrb8 + 2 * (F.QB & (kFastRingWords - 1))) = pendB;
+      const uint32_t a = F.QB + kFastBlockWords;
+      pendB = __builtin_amdgcn_raw_buffer_load_b64(
+          rsrc, uni(a < F.EB ? 2 * (F.CB + a) : kFastOob) + vl8, 0, 0);
+    }
+    F.QA = uni(F.QA + (cA ? kFastBlockWords : 0u));
+    F.QB = uni(F.QB + (cB ? kFastBlockWords : 0u));
+  }
+}
+
+// One refill of one chain inside the step: 64-lane ballot of states below
+// 2^15, the per-half word index from v_mbcnt (upper-half lanes corrected by
+// the distance between the two read positions), the ring read at byte
+// vrb | (2 (O + index) mod 512), and the scalar advance of both positions.
+#define EP_REFILL(X, T, W, CLO, CHI, SA, SB, VRB, SAVE)             \
   "v_cmp_gt_u32_e32 vcc, 0x8000, %[" X "]\n\t"                        \
   "s_bcnt1_i32_b32 %[" CLO "], vcc_lo\n\t"                           \
   "s_bcnt1_i32_b32 %[" CHI "], vcc_hi\n\t"                           \
   "v_mbcnt_lo_u32_b32 %[" T "], vcc_lo, 0\n\t"                        \
   "v_mbcnt_hi_u32_b32 %[" T "], vcc_hi, %[" T "]\n\t"                 \
   "s_sub_u32 %[dd], %[" SB "], %[" SA "]\n\t"                        \
-  "s_ashr_i32 %[dd], %[dd], 1\n\t"                                    \
   "s_sub_u32 %[dd], %[dd], %[" CLO "]\n\t"                           \
   "v_mad_i32_i24 %[" T "], %[vH], %[dd], %[" T "]\n\t"                \
-  "v_lshl_add_u32 %[" T "], %[" T "], 1, %[" SA "]\n\t"               \
+  "v_add_lshl_u32 %[" T "], %[" T "], %[" SA "], 1\n\t"               \
+  "v_and_or_b32 %[" T "], %[" T "], %[rmask], %[" VRB "]\n\t"         \
   "ds_read_u16 %[" W "], %[" T "]\n\t"                                \
   SAVE                                                                \
-  "s_lshl1_add_u32 %[" SA "], %[" CLO "], %[" SA "]\n\t"             \
-  "s_lshl1_add_u32 %[" SB "], %[" CHI "], %[" SB "]\n\t"
+  "s_add_u32 %[" SA "], %[" SA "], %[" CLO "]\n\t"                   \
+  "s_add_u32 %[" SB "], %[" SB "], %[" CHI "]\n\t"
 
 #define EP_MERGE                                                      \
   "s_waitcnt lgkmcnt(0)\n\t"                                          \
@@ -559,18 +642,26 @@ __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, u
   "v_lshl_or_b32 %[w1], %[x1], 16, %[w1]\n\t"                        \
   "v_cndmask_b32_e32 %[x1], %[x1], %[w1], vcc\n\t"
 
+#define EP_REFILL2                                                                          \
+  EP_REFILL("x0", "t0", "w0", "c0lo", "c0hi", "SA0", "SB0", "vrb0", "s_mov_b64 %[m0], vcc\n\t") \
+  EP_REFILL("x1", "t1", "w1", "c1lo", "c1hi", "SA1", "SB1", "vrb1", "")                        \
+  EP_MERGE
+
 #define EP_STEP_OUTS                                                                      \
-  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(SA0), [SB0] "+s"(SB0), [SA1] "+s"(SA1),        \
-      [SB1] "+s"(SB1), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),    \
+  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [SB0] "+s"(F0.OB), [SA1] "+s"(F1.OA),  \
+      [SB1] "+s"(F1.OB), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),  \
       [g0] "=&v"(g0), [g1] "=&v"(g1), [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0),     \
       [w1] "=&v"(w1), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo),          \
       [c1hi] "=&s"(c1hi), [dd] "=&s"(dd), [m0] "=&s"(m0)
 
+#define EP_STEP_INS \
+  [vH] "v"(vH), [vrb0] "v"(vrb0), [vrb1] "v"(vrb1), [rmask] "s"(kFastRingBytes - 1)
+
 // Field symbol (table 8c + FIELD - 1) for both chains, then refill.
 template <int B, int FIELD>
 __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
-                                            int32_t& d0, int32_t& d1, uint32_t& SA0, uint32_t& SB0,
-                                            uint32_t& SA1, uint32_t& SB1, uint32_t vH) {
+                                            int32_t& d0, int32_t& d1, FastChain& F0, FastChain& F1,
+                                            uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
   uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd;
   uint64_t m0;
   asm volatile(
@@ -585,18 +676,16 @@ __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t
       "s_waitcnt lgkmcnt(0)\n\t"
       "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
       "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
-      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
-      "v_ashrrev_i32 %[d0], 23, %[e0]\n\t"
       "v_and_b32 %[u1], 0xfff, %[e1]\n\t"
       "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"
+      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
       "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"
+      "v_ashrrev_i32 %[d0], 23, %[e0]\n\t"
       "v_ashrrev_i32 %[d1], 23, %[e1]\n\t"
-      EP_REFILL("x0", "t0", "w0", "c0lo", "c0hi", "SA0", "SB0", "s_mov_b64 %[m0], vcc\n\t")
-      EP_REFILL("x1", "t1", "w1", "c1lo", "c1hi", "SA1", "SB1", "")
-      EP_MERGE
+      EP_REFILL2
       : EP_STEP_OUTS, [d0] "=&v"(d0), [d1] "=&v"(d1)
-      : [cb0] "v"(cb0), [cb1] "v"(cb1), [vH] "v"(vH), [mk] "i"((1 << B) - 1), [b] "i"(B),
-        [off] "i"((FIELD - 1) * (4 << B))
+      : [cb0] "v"(cb0), [cb1] "v"(cb1), [mk] "i"((1 << B) - 1), [b] "i"(B),
+        [off] "i"((FIELD - 1) * (4 << B)), EP_STEP_INS
       : "vcc", "scc", "memory");
 }
 
@@ -604,9 +693,9 @@ __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t
 // c and the per-lane LDS byte base of its slot tables, cb = 4 * 8c * 2^B.
 template <int B>
 __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t& c0, uint32_t& c1,
-                                            uint32_t& cb0, uint32_t& cb1, uint32_t f0, uint32_t vf1,
-                                            uint32_t& SA0, uint32_t& SB0, uint32_t& SA1,
-                                            uint32_t& SB1, uint32_t vH) {
+                                            uint32_t& cb0, uint32_t& cb1, uint32_t vf0, uint32_t vf1,
+                                            FastChain& F0, FastChain& F1, uint32_t vH,
+                                            uint32_t vrb0, uint32_t vrb1) {
   uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd;
   uint64_t m0;
   asm volatile(
@@ -626,82 +715,111 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
       "v_cndmask_b32_e64 %[c1], 0, 1, vcc\n\t"
       "v_mad_u32_u24 %[x1], %[e1], %[g1], %[u1]\n\t"
       "v_sub_u32_e32 %[x1], %[x1], %[t1]\n\t"
-      "v_lshlrev_b32 %[cb0], %[b3], %[c0]\n\t"
-      "v_lshlrev_b32 %[cb1], %[b3], %[c1]\n\t"
-      EP_REFILL("x0", "t0", "w0", "c0lo", "c0hi", "SA0", "SB0", "s_mov_b64 %[m0], vcc\n\t")
-      EP_REFILL("x1", "t1", "w1", "c1lo", "c1hi", "SA1", "SB1", "")
-      EP_MERGE
+      "v_lshlrev_b32 %[cb0], %[b5], %[c0]\n\t"
+      "v_lshlrev_b32 %[cb1], %[b5], %[c1]\n\t"
+      EP_REFILL2
       : EP_STEP_OUTS, [c0] "=&v"(c0), [c1] "=&v"(c1), [cb0] "=&v"(cb0), [cb1] "=&v"(cb1)
-      : [vf0] "v"(f0), [vf1] "v"(vf1), [vH] "v"(vH), [mk] "i"((1 << B) - 1), [b] "i"(B),
-        [b3] "i"(B + 5)
+      : [vf0] "v"(vf0), [vf1] "v"(vf1), [mk] "i"((1 << B) - 1), [b] "i"(B), [b5] "i"(B + 5),
+        EP_STEP_INS
       : "vcc", "scc", "memory");
 }
 
-template <int B>
-__device__ __forceinline__ void commit_checks(uint8_t* lds, HalfRing<2>* RA, HalfRing<2>* RB,
-                                              uint32_t (*pend)[1], __amdgpu_buffer_rsrc_t rsrc,
-                                              uint32_t half, uint32_t l) {
-#pragma unroll
-  for (int j = 0; j < 2; j++) {
-    if (RA[j].S2 >= RA[j].T2) commit_half<2>(lds, RA[j], pend[j], rsrc, half == 0, l);
-    if (RB[j].S2 >= RB[j].T2) commit_half<2>(lds, RB[j], pend[j], rsrc, half == 1, l);
-  }
+// Set up one chain (tiles tA on lanes 0-31, tA + 1 on lanes 32-63) from the
+// word offsets pA0..pA1 and pB0..pB1 of the two streams: request the first two
+// blocks of each stream (returned, for the ring) and the third (into pend).
+__device__ __forceinline__ u32x4 fast_start(FastChain& F, u32x2& pend, __amdgpu_buffer_rsrc_t rsrc,
+                                            uint32_t half, uint32_t l, uint32_t pA0, uint32_t pA1,
+                                            uint32_t pB0, uint32_t pB1) {
+  F.CA = pA0 & ~(kFastBlockWords - 1);
+  F.CB = pB0 & ~(kFastBlockWords - 1);
+  F.OA = pA0 - F.CA;
+  F.OB = pB0 - F.CB;
+  F.QA = F.QB = kFastRingWords;
+  F.EA = pA1 - F.CA;
+  F.EB = pB1 - F.CB;
+  const uint32_t c = half ? F.CB : F.CA, e = half ? F.EB : F.EA;
+  const u32x4 first = __builtin_amdgcn_raw_buffer_load_b128(rsrc, 2 * c + 16 * l, 0, 0);
+  pend = __builtin_amdgcn_raw_buffer_load_b64(
+      rsrc, (kFastRingWords < e ? 2 * (c + kFastRingWords) : kFastOob) + 8 * l, 0, 0);
+  return first;
 }
 
-// The steady-state task: four full tiles (two chains), slot-table path.
-template <int B>
+// The steady-state task: four full tiles (two chains), slot-table path,
+// output type DT.
+template <int B, int DT, bool SAT>
 __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                                  uint32_t task, int32_t* status) {
-  constexpr int NC = 2;
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
   const uint32_t half = lane >> 5, l = lane & 31;
-  const uint32_t* states = reinterpret_cast<const uint32_t*>(L.blob + L.off_states);
-  const uint32_t* offs = reinterpret_cast<const uint32_t*>(L.blob + L.off_offsets);
+  const EP_GLOBAL uint32_t* states = gptr<const uint32_t>(L.blob + L.off_states);
+  const EP_GLOBAL uint32_t* offs = gptr<const uint32_t>(L.blob + L.off_offsets);
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(L.blob + L.off_payload), (short)0, (int)L.pay_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(L.blob + L.off_sigma), (short)0, (int)(4 * L.rows), 0x00020000);
 
-  uint32_t x[NC], v0[NC], row[NC], col[NC], pend[NC][1];
-  HalfRing<NC> RA[NC], RB[NC];
+  const uint32_t t0 = L.tile_begin + 4 * task;      // tiles t0 .. t0 + 3, all full
+  const uint32_t vrb0 = ring_area + wave * 2 * kFastChainBytes + half * kFastRingBytes;
+  const uint32_t vrb1 = vrb0 + kFastChainBytes;
+  const uint32_t vl8 = 8 * l;
+  // Tile offsets, states and the first blocks are all requested before the
+  // one wait below.
+  uint32_t o[5];
 #pragma unroll
-  for (int j = 0; j < NC; j++) {
-    const uint32_t tA = L.tile_begin + 2 * (NC * task + j);
-    const uint32_t tB = tA + 1;
-    const uint32_t tile = half ? tB : tA;
+  for (int i = 0; i < 5; i++) o[i] = offs[t0 + i];
+  uint32_t x[2], v0[2], row[2], col[2];
+#pragma unroll
+  for (int j = 0; j < 2; j++) {
+    const uint32_t tile = t0 + 2 * j + half;
     v0[j] = tile * L.V;
     x[j] = states[(uint64_t)tile * 32 + l];
     const uint32_t vv = v0[j] + l;
     row[j] = row_of(L, vv);
     col[j] = vv - row[j] * L.cvec;
-    const uint32_t rb = ring_area + (wave * NC + j) * 2 * RingGeom<NC>::HALF_BYTES;
-    ring_start<NC>(lds, RA[j], pend[j], rsrc, half == 0, l, uni(offs[tA]), uni(offs[tA + 1]), rb);
-    ring_start<NC>(lds, RB[j], pend[j], rsrc, half == 1, l, uni(offs[tB]), uni(offs[tB + 1]),
-                   rb + RingGeom<NC>::HALF_BYTES);
   }
+  FastChain F0, F1;
+  u32x2 pend0, pend1, pendB0, pendB1;
+#pragma unroll
+  for (int i = 0; i < 5; i++) o[i] = uni(o[i]);
+  const u32x4 fill0 = fast_start(F0, pend0, rsrc, half, l, o[0], o[1], o[1], o[2]);
+  const u32x4 fill1 = fast_start(F1, pend1, rsrc, half, l, o[2], o[3], o[3], o[4]);
+  // One wait for everything requested so far, so that no load is in flight
+  // when the loop starts (the loop's own waits then stay one round behind).
+  __builtin_amdgcn_s_waitcnt(0);
+  *reinterpret_cast<u32x4*>(lds + vrb0 + 16 * l) = fill0;
+  *reinterpret_cast<u32x4*>(lds + vrb1 + 16 * l) = fill1;
+  pendB0 = pend0;   // pend* serve lanes 0-31, pendB* lanes 32-63
+  pendB1 = pend1;
+
   const uint32_t vH = half;
-  const uint32_t vf1 = L.coset_f1;
+  const uint32_t vf0 = L.coset_f0, vf1 = L.coset_f1;
   const uint32_t rounds = L.V / 32;
   const bool wide = L.cvec >= 32;
+  const uint32_t vrb08 = vrb0 + vl8, vrb18 = vrb1 + vl8;
 
   for (uint32_t k = 0; k < rounds; k++) {
-    float sg[NC];
+    // room for a block: margin <= ring - block
+    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, kFastRingWords - kFastBlockWords + 1);
+    fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, kFastRingWords - kFastBlockWords + 1);
+    float sg[2];
 #pragma unroll
-    for (int j = 0; j < NC; j++)
+    for (int j = 0; j < 2; j++)
       sg[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row[j], 0, 0));
-    uint32_t c[NC], cb[NC];
-    int32_t d[NC][9];
-    coset_step2<B>(x[0], x[1], c[0], c[1], cb[0], cb[1], L.coset_f0, vf1, RA[0].S2, RB[0].S2,
-                   RA[1].S2, RB[1].S2, vH);
-    commit_checks<B>(lds, RA, RB, pend, rsrc, half, l);
-#define EP_FIELD(I)                                                                            \
-  field_step2<B, I>(x[0], x[1], cb[0], cb[1], d[0][I], d[1][I], RA[0].S2, RB[0].S2, RA[1].S2,  \
-                    RB[1].S2, vH);                                                             \
-  commit_checks<B>(lds, RA, RB, pend, rsrc, half, l);
-    EP_FIELD(1) EP_FIELD(2) EP_FIELD(3) EP_FIELD(4) EP_FIELD(5) EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
+    uint32_t c[2], cb[2];
+    int32_t d[2][9];
+    coset_step2<B>(x[0], x[1], c[0], c[1], cb[0], cb[1], vf0, vf1, F0, F1, vH, vrb0, vrb1);
+#define EP_FIELD(I) \
+  field_step2<B, I>(x[0], x[1], cb[0], cb[1], d[0][I], d[1][I], F0, F1, vH, vrb0, vrb1);
+    EP_FIELD(1) EP_FIELD(2)
+    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
+    fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, 3 * 32);
+    EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
+    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
+    fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, 3 * 32);
+    EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
 #undef EP_FIELD
 #pragma unroll
-    for (int j = 0; j < NC; j++) {
+    for (int j = 0; j < 2; j++) {
       int32_t p2[8];
       int32_t acc = (int32_t)c[j];
 #pragma unroll
@@ -710,7 +828,7 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
         acc += d[j][i];
       }
       p2[7] = d[j][8] | (acc & 2);
-      store_vector(L, v0[j] + l + 32 * k, p2, 0.5f * sg[j]);
+      store_vec<DT, SAT>(L.out, v0[j] + l + 32 * k, p2, 0.5f * sg[j]);
       // next vector of this lane: 32 vectors further
       if (wide) {
         col[j] += 32;
@@ -726,19 +844,51 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 
   uint32_t err = 0;
 #pragma unroll
-  for (int j = 0; j < NC; j++) {
+  for (int j = 0; j < 2; j++) {
     if (x[j] != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
-    const HalfRing<NC>& R = half ? RB[j] : RA[j];
-    const uint32_t P = R.base + (R.S2 - R.rbase) / 2;
-    if (l == 0 && P != R.Pend) err |= P > R.Pend ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
+    const FastChain& F = j ? F1 : F0;
+    const uint32_t P = half ? F.OB : F.OA, E = half ? F.EB : F.EA;
+    if (l == 0 && P != E) err |= P > E ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
     if (L.container && L.dequant) {
-      const float* delta = reinterpret_cast<const float*>(L.blob + L.off_delta);
+      const EP_GLOBAL float* delta = gptr<const float>(L.blob + L.off_delta);
       const uint32_t r_first = (v0[j] + L.cvec - 1) / L.cvec;
       const uint32_t r_last = (v0[j] + L.V - 1) / L.cvec;
-      for (uint32_t r = r_first + l; r <= r_last; r += 32) L.dequant[r] = delta[r];
+      for (uint32_t r = r_first + l; r <= r_last; r += 32) gptr<float>(L.dequant)[r] = delta[r];
     }
   }
   if (err && status) atomicOr(status, (int32_t)err);
+}
+
+// Output-type dispatch of a full slot-table task.  Returns false for the
+// combinations the steady state does not cover (they take the generic loop).
+template <int B>
+__device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
+                                                     uint32_t task, int32_t* status) {
+  switch (L.out_dtype) {
+    case EP_BF16:
+      if (L.saturate) return false;
+      decode_task_fast<B, EP_BF16, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_FP16:
+      if (L.saturate) decode_task_fast<B, EP_FP16, true>(L, lds, ring_area, task, status);
+      else decode_task_fast<B, EP_FP16, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_FP8_E4M3:
+      if (L.saturate) decode_task_fast<B, EP_FP8_E4M3, true>(L, lds, ring_area, task, status);
+      else decode_task_fast<B, EP_FP8_E4M3, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_INT8:
+      decode_task_fast<B, EP_INT8, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_FP32:
+      decode_task_fast<B, EP_FP32, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_COORD2_I32:
+      decode_task_fast<B, EP_COORD2_I32, false>(L, lds, ring_area, task, status);
+      return true;
+    default:
+      return false;
+  }
 }
 
 // LDS byte offset of the payload rings: after the slot table (LUT path) or
@@ -778,10 +928,8 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
   const bool full = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
                     (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
   if constexpr (PATH == kPathLut) {
-    if (full) {
-      decode_task_fast<B>(L, lb, ring_area, task, status);
+    if (full && L.pay_bytes < kFastOob && decode_task_fast_any<B>(L, lb, ring_area, task, status))
       return;
-    }
   }
   if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, task, status);
   else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, task, status);
