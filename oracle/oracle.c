@@ -1230,3 +1230,28 @@ int ora_values(const void* bits, int64_t n, int dtype, double* out) {
   }
   return O_OK;
 }
+
+/* ---- decode-then-GEMM reference ------------------------------------------
+ * Y[m x n] = A[m x k] * B[n x k]^T for int8 operands, both stored row-major
+ * (k contiguous), accumulated exactly in int64 and returned as int32.  This is
+ * the plain definition of the product the decoded INT8 weights feed; it only
+ * computes the rows listed in `rows` (all rows when rows == NULL), so a test
+ * can check sampled rows of a large product.  Returns O_ERR_ARG if a sum
+ * leaves the int32 range.  Pinned against an independent int64 matrix product
+ * and hand-computed cases in the CPU tests. */
+int ora_gemm_i8_nt(const int8_t* a, const int8_t* b, int32_t* y, int64_t m, int64_t n, int64_t k,
+                   const int64_t* rows, int64_t nrows) {
+  if (!a || !b || !y || m <= 0 || n <= 0 || k <= 0) return O_ERR_ARG;
+  const int64_t count = rows ? nrows : m;
+  for (int64_t q = 0; q < count; q++) {
+    const int64_t i = rows ? rows[q] : q;
+    if (i < 0 || i >= m) return O_ERR_ARG;
+    for (int64_t j = 0; j < n; j++) {
+      int64_t s = 0;
+      for (int64_t t = 0; t < k; t++) s += (int64_t)a[i * k + t] * (int64_t)b[j * k + t];
+      if (s < INT32_MIN || s > INT32_MAX) return O_ERR_ARG;
+      y[q * n + j] = (int32_t)s;
+    }
+  }
+  return O_OK;
+}

@@ -246,3 +246,25 @@ def estimate(f9: np.ndarray, rows: int, b: int, V: int = 512, kappa: float = 16.
     _chk(lib().ora_estimate(_ptr(f), f.shape[0], rows, b, V, kappa, container, _ptr(out)),
          "ora_estimate")
     return float(out[0]), float(out[1]), float(out[2])
+
+
+def gemm_i8_nt(a: np.ndarray, b: np.ndarray, rows=None) -> np.ndarray:
+    """Exact int32 Y = A B^T (int8 A[m,k], B[n,k]); only `rows` of Y if given."""
+    a = np.ascontiguousarray(a, dtype=np.int8)
+    b = np.ascontiguousarray(b, dtype=np.int8)
+    m, k = a.shape
+    n = b.shape[0]
+    assert b.shape[1] == k
+    L = lib()
+    L.ora_gemm_i8_nt.restype = C.c_int
+    L.ora_gemm_i8_nt.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_int64,
+                                 C.c_int64, C.c_void_p, C.c_int64]
+    if rows is None:
+        y = np.zeros((m, n), dtype=np.int32)
+        rc = L.ora_gemm_i8_nt(_ptr(a), _ptr(b), _ptr(y), m, n, k, None, 0)
+    else:
+        r = np.ascontiguousarray(rows, dtype=np.int64)
+        y = np.zeros((r.size, n), dtype=np.int32)
+        rc = L.ora_gemm_i8_nt(_ptr(a), _ptr(b), _ptr(y), m, n, k, _ptr(r), r.size)
+    _chk(rc, "gemm_i8_nt")
+    return y
