@@ -16,11 +16,22 @@ throughput on the same blobs on this host's cores.
 Other workloads (--workload): attn_fp16 (3072 x 3072 at 3.0 bpp to FP16),
 dit_stack (30 diffusion-transformer blocks, 180 layers at 2.5 bpp to BF16 in one
 launch), mlp_down_int8 (the MLP down projection in the INT8 container at
-6.0 bpp to INT8).
+6.0 bpp to INT8, followed by the INT8 MFMA product with 8192 x 17408
+activations, timed separately: decode time over product time is reported).
+
+The roofline's `traffic` field is the decode kernel's measured HBM bytes per
+launch, read from the committed rocprofv3 counter summary of this workload
+(FETCH_SIZE and WRITE_SIZE, each scaled by the factor the same counter shows
+for a plain device copy of known size); it is null when the summary is absent
+or was taken from a different decode kernel source than the one built.
+
+--copy-calibration runs only a plain 1 GiB device-to-device copy (five times),
+the reference kernel for those counter factors.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +44,9 @@ if ROOT not in sys.path:
 
 METRIC = "decoded weights/s and achieved HBM GB/s (% roofline), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
+INT8_PEAK_TOPS = 5000.0   # dense MFMA int8, MI355X
+DECODE_SRC = os.path.join(ROOT, "paper_2609_34185_amd", "csrc", "decode.hip")
+COPY_BYTES = 1 << 30
 
 
 def log(*a):
@@ -79,6 +93,91 @@ def workload(name, E, W, threads):
     return desc, items
 
 
+def source_digest() -> str:
+    with open(DECODE_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload_name: str):
+    """HBM bytes per decode launch from profiles/decode_<workload>_traffic.txt, or None.
+
+    The summary holds `key: value` lines; the figures count only when the
+    recorded decode source digest equals the current one."""
+    path = os.path.join(ROOT, "profiles", f"decode_{workload_name}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith(("#", " ", "\t")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    try:
+        if kv.get("decode_source_sha256") != source_digest():
+            return None
+        fetch = float(kv["fetch_kib_per_launch"]) * float(kv["copy_fetch_factor"])
+        write = float(kv["write_kib_per_launch"]) * float(kv["copy_write_factor"])
+        return 1024.0 * (fetch + write)
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    """A plain device copy of COPY_BYTES, five times: the counters' reference kernel."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 5}), flush=True)
+
+
+def gemm_leg(E, W, out, info, reps=10):
+    """Time the INT8 MFMA product of the decoded weights with the 8192 x 17408 activations."""
+    import torch
+    act = torch.from_numpy(W.llm_activations()).cuda()
+    m, n, k = act.shape[0], info.rows, info.cols
+    y = torch.empty((m, n), dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream()
+
+    def run():
+        E.gemm_i8_nt(act.data_ptr(), out.data_ptr(), y.data_ptr(), m, n, k, s.cuda_stream)
+
+    run()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(reps):
+        run()
+    b.record(s)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    tops = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+    return {"shape": [m, n, k], "ms": ms, "tops": tops,
+            "roofline": {"bound": "mfma", "achieved": tops, "peak": INT8_PEAK_TOPS,
+                         "unit": "TOP/s", "frac": tops / INT8_PEAK_TOPS}}
+
+
+def cold_cache_ms(step, reps=15):
+    """Per-launch times with the 256 MB last-level cache flushed before each launch."""
+    import torch
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+    times = []
+    for _ in range(reps):
+        flush.zero_()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        step()
+        b.record(s)
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    times.sort()
+    return {"min": times[0], "median": times[len(times) // 2], "reps": reps}
+
+
 def cpu_baseline(items, threads):
     """The oracle decoder on the same blobs, tiles split over `threads` host threads."""
     import numpy as np
@@ -118,6 +217,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mlp_fp8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -133,6 +233,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     threads = min(16, len(os.sched_getaffinity(0)))
 
     t = time.perf_counter()
@@ -177,8 +280,16 @@ def main():
     ms = start.elapsed_time(end) / args.steps
     assert int(status.item()) == 0, "decode reported a corrupt stream"
 
+    cold = cold_cache_ms(step)
+    gemm = None
+    if args.workload == "mlp_down_int8":
+        log("timing the INT8 product of the decoded weights")
+        gemm = gemm_leg(E, W, keep[1], layers[0][0])
+        gemm["decode_over_gemm"] = ms / gemm["ms"]
+
     sec = ms / 1e3
     gbps = algo_bytes / sec / 1e9
+    traffic = measured_traffic(args.workload)
     line = {
         "metric": METRIC,
         "value": weights / sec,
@@ -193,10 +304,13 @@ def main():
         "dtype": "u32",
         "data": "synthetic",
         "config": dict(desc, weights=weights, stored_bpp=round(stored_bpp, 4),
-                       bytes_per_step=algo_bytes, wall_s=round(wall, 4)),
+                       bytes_per_step=algo_bytes, wall_s=round(wall, 4),
+                       cold_cache_ms=cold),
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": gbps / HBM_PEAK_GBPS, "traffic": None},
+                     "frac": gbps / HBM_PEAK_GBPS, "traffic": traffic},
     }
+    if gemm is not None:
+        line["config"]["gemm"] = gemm
     if not args.no_cpu_baseline:
         log("timing the CPU oracle decoder")
         line["cpu_baseline"] = cpu_baseline(items, threads)

@@ -66,7 +66,7 @@ struct LayerDev {
   uint32_t task_begin, n_tasks;   // this layer's slice of the global task list
   uint32_t out_dtype, saturate;
   uint32_t coset_f0, coset_f1;
-  uint32_t sum_A, search_iters;
+  uint32_t sum_A;
   uint32_t pay_bytes;             // payload section bytes (bounds of the buffer resource)
   uint32_t div_magic, div_shift, div_pow2;  // floor(v / (C/8))
   uint64_t off_sigma, off_delta, off_states, off_offsets, off_payload;
@@ -85,7 +85,7 @@ struct Hot {
   uint32_t rows, cvec, V, tile_begin, tile_end, b, container;
   uint32_t out_dtype, saturate, coset_f0, coset_f1;
   uint32_t pay_bytes, div_magic, div_shift, div_pow2;
-  uint32_t search_iters, meta;    // search path: LDS index of the table metadata
+  uint32_t meta, bucket;          // search path: u32 index of the metadata, u16 index of the buckets
   uint32_t off_sigma, off_delta, off_states, off_offsets, off_payload;
 };
 
@@ -118,8 +118,8 @@ __device__ __forceinline__ Hot make_hot(const LayerDev& L) {
   H.div_magic = uni(L.div_magic);
   H.div_shift = uni(L.div_shift);
   H.div_pow2 = uni(L.div_pow2);
-  H.search_iters = uni(L.search_iters);
-  H.meta = uni(L.sum_A);
+  H.meta = uni(search_layout(L.sum_A).meta / 4);
+  H.bucket = uni(search_layout(L.sum_A).bucket / 2);
   H.off_sigma = uni((uint32_t)L.off_sigma);
   H.off_delta = uni((uint32_t)L.off_delta);
   H.off_states = uni((uint32_t)L.off_states);
@@ -232,13 +232,15 @@ __device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int
 }
 
 // ---- table construction in LDS ------------------------------------------------
-// Cumulative entries F_s | f_s << 16 of the 16 field tables at lds[base_t + s];
-// wave w scans table w (and w + 16 ... when fewer waves exist).
-__device__ __forceinline__ void build_cumulative(const LayerDev& L, uint32_t* cum) {
+// Prefix sums of the 16 field tables' frequencies: put(t, s, F_s, f_s) for every
+// symbol s of table t, and end(t, M) once per table with the total (= 2^b).
+// Wave w scans table w (and w + kWavesPerGroup ... when fewer waves exist).
+template <class Put, class End>
+__device__ __forceinline__ void scan_tables(const LayerDev& L, Put put, End end) {
   const int lane = threadIdx.x & 63, wave = (int)wave_id();
   for (int t = wave; t < 16; t += kWavesPerGroup) {
     const EP_GLOBAL uint16_t* f = gptr<const uint16_t>(L.blob + L.tab_off[t]);
-    const uint32_t A = L.tab_A[t], base = L.tab_base[t];
+    const uint32_t A = L.tab_A[t];
     uint32_t running = 0;
     for (uint32_t s0 = 0; s0 < A; s0 += kWaveSize) {
       uint32_t s = s0 + lane;
@@ -249,10 +251,17 @@ __device__ __forceinline__ void build_cumulative(const LayerDev& L, uint32_t* cu
         uint32_t o = __shfl_up(incl, d, kWaveSize);
         if (lane >= d) incl += o;
       }
-      if (s < A) cum[base + s] = (running + incl - fs) | (fs << 16);
+      if (s < A) put(t, s, running + incl - fs, fs);
       running += __shfl(incl, kWaveSize - 1, kWaveSize);
     }
+    if (lane == 0) end(t, running);
   }
+}
+
+// Cumulative entries F_s | f_s << 16 at cum[base_t + s] (slot-table build).
+__device__ __forceinline__ void build_cumulative(const LayerDev& L, uint32_t* cum) {
+  scan_tables(L, [&](int t, uint32_t s, uint32_t F, uint32_t f) { cum[L.tab_base[t] + s] = F | (f << 16); },
+              [](int, uint32_t) {});
 }
 
 __device__ __forceinline__ int32_t doubled_value(int32_t z, int field, uint32_t c) {
@@ -425,21 +434,23 @@ __device__ __forceinline__ void decode_field(const Hot& L, const uint32_t* lds, 
     x = __umul24(e & 0xFFFu, x >> B) + ((e >> 12) & 0x7FFu);
     dval = (int32_t)e >> 23;
   } else {
-    // table metadata after the cumulative entries: base[16], A[16], min[16]
+    // Bucketed search: the bucket of u (its top 8 bits) bounds the symbol to
+    // [bk[j], bk[j + 1]]; a binary search on the u16 cumulative table narrows it.
+    const uint16_t* cum = reinterpret_cast<const uint16_t*>(lds);
     const uint32_t u = x & ((1u << L.b) - 1);
     const uint32_t t = 8 * c + (uint32_t)(field - 1);
     const uint32_t base = lds[L.meta + t];
-    const uint32_t A = lds[L.meta + 16 + t];
-    uint32_t s = 0, n = A;
-    for (uint32_t it = 0; it < L.search_iters; it++) {
-      const uint32_t h = n >> 1;
-      if ((lds[base + s + h] & 0xFFFFu) <= u) s += h;
-      n -= h;
+    const uint16_t* bk = cum + L.bucket + t * kBuckets1;
+    const uint32_t j = u >> (L.b - kBucketBits);
+    uint32_t lo = bk[j], hi = bk[j + 1];
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) >> 1;
+      if (cum[base + mid] <= u) lo = mid;
+      else hi = mid - 1;
     }
-    const uint32_t e = lds[base + s];
-    x = __umul24(e >> 16, x >> L.b) + u - (e & 0xFFFFu);
-    const int32_t mn = (int32_t)lds[L.meta + 32 + t];
-    dval = doubled_value((int32_t)s + mn, field, c);
+    const uint32_t F = cum[base + lo], Fn = cum[base + lo + 1];
+    x = __umul24(Fn - F, x >> L.b) + u - F;
+    dval = doubled_value((int32_t)lo + (int32_t)lds[L.meta + 16 + t], field, c);
   }
 }
 
@@ -892,10 +903,47 @@ __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds,
 }
 
 // LDS byte offset of the payload rings: after the slot table (LUT path) or
-// after the cumulative table (search path).
+// after the search tables (search path).
 template <int PATH>
 __device__ __forceinline__ uint32_t ring_offset(const LayerDev& L) {
-  return PATH == kPathLut ? (64u << L.b) : ((4u * (L.sum_A + 48u) + 15u) & ~15u);
+  return PATH == kPathLut ? (64u << L.b) : search_table_bytes(L.sum_A);
+}
+
+// Search-path tables (byte layout from search_layout): u16 cumulative values
+// of table t at [base_t + t, base_t + t + A_t] (the last one = 2^b), the u16
+// bucket bounds bk[t][0..256], and u32 metadata base'[16], min[16].
+__device__ __forceinline__ void build_search(const LayerDev& L, uint32_t* lds) {
+  uint16_t* cum = reinterpret_cast<uint16_t*>(lds);
+  const SearchLayout S = search_layout(L.sum_A);
+  scan_tables(L, [&](int t, uint32_t s, uint32_t F, uint32_t) { cum[L.tab_base[t] + t + s] = (uint16_t)F; },
+              [&](int t, uint32_t M) { cum[L.tab_base[t] + t + L.tab_A[t]] = (uint16_t)M; });
+  if (threadIdx.x < 32) {
+    const uint32_t t = threadIdx.x & 15;
+    lds[S.meta / 4 + threadIdx.x] = threadIdx.x < 16 ? L.tab_base[t] + t : (uint32_t)L.tab_min[t];
+  }
+  __syncthreads();
+  // bk[t][j] = largest s < A_t with F_s <= j * 2^(b - 8); bk[t][256] = A_t - 1.
+  uint16_t* bk = cum + S.bucket / 2;
+  const uint32_t w = 1u << (L.b - kBucketBits);
+  for (uint32_t k = threadIdx.x; k < 16 * kBuckets1; k += kThreads) {
+    const uint32_t t = k / kBuckets1, j = k % kBuckets1, A = L.tab_A[t];
+    const uint32_t base = L.tab_base[t] + t;
+    uint32_t s = 0;
+    if (A == 0) {
+      s = 0;
+    } else if (j == kBuckets1 - 1) {
+      s = A - 1;
+    } else {
+      uint32_t lo = 0, hi = A - 1;
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi + 1) >> 1;
+        if (cum[base + mid] <= j * w) lo = mid;
+        else hi = mid - 1;
+      }
+      s = lo;
+    }
+    bk[k] = (uint16_t)s;
+  }
 }
 
 template <int PATH>
@@ -906,11 +954,7 @@ __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
     __syncthreads();
     build_lut(L, lds, cum);
   } else {
-    build_cumulative(L, lds);
-    if (threadIdx.x < 48) {
-      const uint32_t t = threadIdx.x & 15, k = threadIdx.x >> 4;
-      lds[L.sum_A + threadIdx.x] = k == 0 ? L.tab_base[t] : k == 1 ? L.tab_A[t] : (uint32_t)L.tab_min[t];
-    }
+    build_search(L, lds);
   }
 }
 
@@ -1029,7 +1073,7 @@ DeviceProps device_props() {
 
 uint32_t lds_bytes(uint32_t path, const ep_tensor_info& I) {
   if (path == kPathLut) return (64u << I.prob_bits) + kRingBytes;
-  return ((4u * (I.sum_alphabet + 48u) + 15u) & ~15u) + kRingBytes;
+  return search_table_bytes(I.sum_alphabet) + kRingBytes;
 }
 
 float dtype_max(int dt) {
@@ -1074,10 +1118,6 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
   D.coset_f0 = I.coset_f0;
   D.coset_f1 = I.coset_f1;
   D.sum_A = I.sum_alphabet;
-  uint32_t amax = 1, it = 0;
-  for (int t = 0; t < 16; t++) amax = std::max(amax, I.table_A[t]);
-  while ((1u << it) < amax) it++;
-  D.search_iters = it;
   const uint64_t pay = (2ull * I.payload_words + 3) / 4 * 4;
   if (pay > 0xFFFFFFF0ull) return fail(EP_ERR_UNSUPPORTED, "decode: payload section above 4 GiB");
   D.pay_bytes = (uint32_t)pay;

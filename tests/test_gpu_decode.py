@@ -93,6 +93,36 @@ def test_every_probability_precision(E, oracle, b):
     check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"b{b}")
 
 
+@pytest.mark.parametrize("target", [6.0, 8.0, 10.0])
+def test_high_rates_large_alphabets(E, oracle, target):
+    """High targets give wide coordinate ranges and large tables (b = 12 at 8 bpp): the
+    bucketed-search path decodes them; its tables are built in LDS from the blob."""
+    w = W.attention_projection()[:512, :2048]
+    blob, st = oracle.encode(w, target)
+    info = check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "FP16"], tag=f"rate{target}")
+    assert info.path == 2
+    say(f"    b={info.prob_bits} sum_A={info.sum_alphabet} coord2 [{info.coord2_min}, {info.coord2_max}]")
+
+
+def test_escalated_precision_blobs(E, oracle):
+    """Blobs whose precision was escalated (b > 11) or whose scale was coarsened at b = 15
+    either decode exactly or are refused with EP_ERR_UNSUPPORTED before any launch."""
+    R, Cc = 40, 65536
+    rng = np.random.default_rng(12)
+    w = (rng.standard_normal((R, Cc)) * 1e-3).astype(np.float32)
+    outside = [r for r in range(R) if r not in set(oracle.sample_rows(R, Cc).tolist())]
+    for val, target in ((0.02, 10.0), (0.5, 14.0)):
+        w[outside, 5] = val
+        blob, st = oracle.encode(w, target, prob_bits=11)
+        info = E.blob_info(blob)
+        say(f"    target {target}: b={info.prob_bits} sum_A={info.sum_alphabet} path={info.path}")
+        if info.path:
+            check_blob(E, oracle, blob, dtypes=["COORD2"], tag=f"esc{target}")
+        else:
+            with pytest.raises(RuntimeError, match="decode path"):
+                E.decode(blob, E.COORD2_I32, info=info)
+
+
 @pytest.mark.parametrize("shape,V", [((1, 8), 512), ((3, 24), 32), ((7, 400), 45),
                                      ((33, 264), 512), ((130, 72), 100), ((300, 8), 33),
                                      ((65, 1000), 77), ((1, 4096), 1)])
