@@ -185,21 +185,29 @@ typedef struct {
   int32_t reserved;
 } ep_layer;
 
-/* Workspace bytes ep_decode_layers needs for n layers (device memory). */
+/* Workspace bytes ep_decode_layers needs for n layers (device memory): 0 for
+ * n <= 8 (the descriptors travel as kernel arguments), else n descriptors. */
 uint64_t ep_decode_layers_workspace(int n);
 
-/* Decode n whole layers with a single kernel launch.  The per-layer
- * descriptors are staged into d_workspace (>= ep_decode_layers_workspace(n)
- * bytes) with one asynchronous host-to-device copy from an internal pinned
- * host buffer; d_workspace must stay untouched until the launch completes.
- * Errors: as ep_decode_tiles. */
+/* Decode every tile of n layers with a single kernel launch.  Up to 8 layer descriptors are passed as kernel
+ * arguments; longer lists are copied into d_workspace (>=
+ * ep_decode_layers_workspace(n) bytes, device memory owned by the caller) by
+ * one hipMemcpyAsync on the same stream, which has read the host list by the
+ * time it returns; d_workspace must stay untouched until the launch completes.
+ * All layers must select the same decode path (ep_tensor_info.path).  The
+ * layers array is host memory and is not retained.  Errors: as
+ * ep_decode_tiles, and EP_ERR_ARG for a missing or short workspace. */
 int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      int32_t* d_status, void* hip_stream);
 
 /* ---- decode-then-GEMM ---------------------------------------------------- */
 /* Y[M x N] (int32, row-major) = A[M x K] (int8, row-major) * B[N x K]^T
  * (int8, row-major: both operands K-contiguous) on MFMA, exact int32
- * accumulation.  Requires K % 64 == 0.  Errors: EP_ERR_ARG, EP_ERR_HIP. */
+ * accumulation: the product of decoded INT8 weights (B) with INT8
+ * activations, as in the compressed-storage INT8 route of the paper's
+ * Appendix B.1.  All pointers are device memory owned by the caller; A and B
+ * 16-byte aligned.  Requires M, N > 0, K > 0, K % 16 == 0 and K <= 2^24.
+ * Asynchronous on hip_stream.  Errors: EP_ERR_ARG, EP_ERR_HIP. */
 int ep_gemm_i8_nt(const int8_t* d_a, const int8_t* d_b, int32_t* d_y, int64_t m, int64_t n,
                   int64_t k, void* hip_stream);
 
