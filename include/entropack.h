@@ -200,6 +200,35 @@ uint64_t ep_decode_layers_workspace(int n);
 int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      int32_t* d_status, void* hip_stream);
 
+/* ---- prepared stacks ------------------------------------------------------ */
+/* A layer list whose device descriptors were written once by ep_stack_prepare,
+ * so that every later decode of the same blobs into the same outputs (one per
+ * forward pass of a compressed model) is a single kernel launch with no copy. */
+typedef struct {
+  void* d_workspace;         /* device descriptor list (caller-owned memory) */
+  int32_t n_layers;
+  uint32_t path;             /* decode path shared by all layers */
+  uint32_t total_tasks;      /* 4-tile tasks over all layers */
+  uint32_t lds_bytes;        /* LDS of the launch */
+  uint32_t reserved[4];
+} ep_stack;
+
+/* Device bytes ep_stack_prepare needs for n layers. */
+uint64_t ep_stack_workspace(int n);
+
+/* Validate n layers (as for ep_decode_layers), write their descriptors into
+ * d_workspace (>= ep_stack_workspace(n) bytes, device memory owned by the
+ * caller, which must outlive every ep_stack_decode of this stack) and fill
+ * *stack.  Synchronous: returns after the copy on hip_stream has completed.
+ * Errors: as ep_decode_layers, EP_ERR_ARG for a null stack or short workspace. */
+int ep_stack_prepare(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
+                     ep_stack* stack, void* hip_stream);
+
+/* Decode every tile of a prepared stack: one kernel launch on hip_stream, no
+ * host-to-device copy, no allocation.  d_status as for ep_decode_tiles.
+ * Errors: EP_ERR_ARG for an unprepared stack, EP_ERR_UNSUPPORTED, EP_ERR_HIP. */
+int ep_stack_decode(const ep_stack* stack, int32_t* d_status, void* hip_stream);
+
 /* ---- decode-then-GEMM ---------------------------------------------------- */
 /* Y[M x N] (int32, row-major) = A[M x K] (int8, row-major) * B[N x K]^T
  * (int8, row-major: both operands K-contiguous) on MFMA, exact int32

@@ -1167,21 +1167,50 @@ int set_lds_limit(size_t bytes) {
   return (e1 == hipSuccess && e2 == hipSuccess) ? EP_OK : EP_ERR_HIP;
 }
 
+// Grid of a launch over `total` tasks: G workgroups of `per` consecutive tasks.
+int launch_geometry(uint32_t path, uint32_t total, uint32_t lds, uint32_t& G, uint32_t& per) {
+  DeviceProps P = device_props();
+  if (!P.cus) return fail(EP_ERR_HIP, "decode: no HIP device");
+  if (lds > P.max_lds) return fail(EP_ERR_UNSUPPORTED, "decode: tables exceed the device LDS");
+  G = groups_for(path, lds, total, P);
+  per = (total + G - 1) / G;
+  G = (total + per - 1) / per;
+  int rc = path == kPathLut ? set_lds_limit<kPathLut>(lds) : set_lds_limit<kPathSearch>(lds);
+  if (rc) return fail(EP_ERR_HIP, "decode: cannot raise the kernel's LDS limit");
+  return EP_OK;
+}
+
+// Launch over a descriptor list already in device memory.
+int launch_list(uint32_t path, const LayerDev* dl, int n, uint32_t total, uint32_t lds,
+                int32_t* d_status, hipStream_t s, const char* who) {
+  uint32_t G = 0, per = 0;
+  int rc = launch_geometry(path, total, lds, G, per);
+  if (rc) return rc;
+  if (path == kPathLut)
+    hipLaunchKernelGGL(decode_ws_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
+  else
+    hipLaunchKernelGGL(decode_ws_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
+  if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (std::string(who) + ": launch failed").c_str());
+  return EP_OK;
+}
+
 // Launch the layers of one decode path: by-value descriptors when they fit,
 // else from d_ws (copied there first on the same stream).
 int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total, uint32_t lds,
                   void* d_ws, uint64_t ws_bytes, int32_t* d_status, hipStream_t s,
                   const char* who) {
-  DeviceProps P = device_props();
-  if (!P.cus) return fail(EP_ERR_HIP, "decode: no HIP device");
-  if (lds > P.max_lds) return fail(EP_ERR_UNSUPPORTED, "decode: tables exceed the device LDS");
-  uint32_t G = groups_for(path, lds, total, P);
-  uint32_t per = (total + G - 1) / G;
-  G = (total + per - 1) / per;
   const int n = (int)D.size();
-  int rc = path == kPathLut ? set_lds_limit<kPathLut>(lds) : set_lds_limit<kPathSearch>(lds);
-  if (rc) return fail(EP_ERR_HIP, "decode: cannot raise the kernel's LDS limit");
-  if (n <= kArgLayers) {
+  if (n > kArgLayers) {
+    if (!d_ws || ws_bytes < sizeof(LayerDev) * (uint64_t)n)
+      return fail(EP_ERR_ARG, "ep_decode_layers: workspace too small");
+    if (hipMemcpyAsync(d_ws, D.data(), sizeof(LayerDev) * D.size(), hipMemcpyHostToDevice, s) != hipSuccess)
+      return fail(EP_ERR_HIP, "ep_decode_layers: descriptor copy failed");
+    return launch_list(path, static_cast<const LayerDev*>(d_ws), n, total, lds, d_status, s, who);
+  }
+  uint32_t G = 0, per = 0;
+  int rc = launch_geometry(path, total, lds, G, per);
+  if (rc) return rc;
+  {
     LayerList list;
     std::memset(&list, 0, sizeof list);
     for (int i = 0; i < n; i++) list.L[i] = D[i];
@@ -1189,16 +1218,6 @@ int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total,
       hipLaunchKernelGGL(decode_args_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
     else
       hipLaunchKernelGGL(decode_args_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
-  } else {
-    if (!d_ws || ws_bytes < sizeof(LayerDev) * (uint64_t)n)
-      return fail(EP_ERR_ARG, "ep_decode_layers: workspace too small");
-    if (hipMemcpyAsync(d_ws, D.data(), sizeof(LayerDev) * D.size(), hipMemcpyHostToDevice, s) != hipSuccess)
-      return fail(EP_ERR_HIP, "ep_decode_layers: descriptor copy failed");
-    const LayerDev* dl = static_cast<const LayerDev*>(d_ws);
-    if (path == kPathLut)
-      hipLaunchKernelGGL(decode_ws_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
-    else
-      hipLaunchKernelGGL(decode_ws_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
   }
   if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (std::string(who) + ": launch failed").c_str());
   return EP_OK;
@@ -1219,27 +1238,78 @@ uint64_t decode_layers_workspace(int n) {
   return n > kArgLayers ? (uint64_t)n * sizeof(LayerDev) : 0;
 }
 
-int decode_layers(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, int32_t* d_status,
-                  void* stream) {
-  if (n < 0 || (n > 0 && !layers)) return fail(EP_ERR_ARG, "ep_decode_layers: bad layer list");
-  if (n == 0) return EP_OK;
-  const uint32_t path = layers[0].info.path;
-  std::vector<LayerDev> D((size_t)n);
-  uint32_t total = 0, lds = 0;
+// Device descriptors of a layer list, the common decode path, the total task
+// count and the LDS bytes of the launch.
+int describe_layers(const ep_layer* layers, int n, const char* who, std::vector<LayerDev>& D,
+                    uint32_t& path, uint32_t& total, uint32_t& lds) {
+  if (n < 0 || (n > 0 && !layers)) return fail(EP_ERR_ARG, (std::string(who) + ": bad layer list").c_str());
+  D.assign((size_t)n, LayerDev{});
+  path = n ? layers[0].info.path : 0;
+  total = 0;
+  lds = 0;
+  uint64_t tasks = 0;
   for (int i = 0; i < n; i++) {
     const ep_layer& Lr = layers[i];
     if (Lr.info.path != path)
-      return fail(EP_ERR_UNSUPPORTED, "ep_decode_layers: layers need different decode paths");
+      return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": layers need different decode paths").c_str());
     int rc = fill_layer(Lr.info, Lr.d_blob, Lr.out_dtype, Lr.d_out, Lr.d_dequant, 0,
                         Lr.info.n_tiles, D[i]);
     if (rc) return rc;
-    D[i].task_begin = total;
-    total += D[i].n_tasks;
+    D[i].task_begin = (uint32_t)tasks;
+    tasks += D[i].n_tasks;
     lds = std::max(lds, lds_bytes(path, Lr.info));
   }
+  if (tasks > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": too many tiles").c_str());
+  total = (uint32_t)tasks;
+  return EP_OK;
+}
+
+int decode_layers(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, int32_t* d_status,
+                  void* stream) {
+  std::vector<LayerDev> D;
+  uint32_t path = 0, total = 0, lds = 0;
+  int rc = describe_layers(layers, n, "ep_decode_layers", D, path, total, lds);
+  if (rc) return rc;
   if (total == 0) return EP_OK;
   return launch_layers(path, D, total, lds, d_ws, ws_bytes, d_status,
                        static_cast<hipStream_t>(stream), "ep_decode_layers");
+}
+
+uint64_t stack_workspace(int n) { return n > 0 ? (uint64_t)n * sizeof(LayerDev) : 0; }
+
+int stack_prepare(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, ep_stack* st,
+                  void* stream) {
+  if (!st) return fail(EP_ERR_ARG, "ep_stack_prepare: null stack");
+  std::memset(st, 0, sizeof *st);
+  std::vector<LayerDev> D;
+  uint32_t path = 0, total = 0, lds = 0;
+  int rc = describe_layers(layers, n, "ep_stack_prepare", D, path, total, lds);
+  if (rc) return rc;
+  if (n > 0) {
+    if (!d_ws || ws_bytes < stack_workspace(n))
+      return fail(EP_ERR_ARG, "ep_stack_prepare: workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (hipMemcpyAsync(d_ws, D.data(), sizeof(LayerDev) * D.size(), hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return fail(EP_ERR_HIP, "ep_stack_prepare: descriptor copy failed");
+  }
+  st->d_workspace = d_ws;
+  st->n_layers = n;
+  st->path = path;
+  st->total_tasks = total;
+  st->lds_bytes = lds;
+  return EP_OK;
+}
+
+int stack_decode(const ep_stack* st, int32_t* d_status, void* stream) {
+  if (!st || st->n_layers < 0 || (st->n_layers > 0 && !st->d_workspace))
+    return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
+  if (st->total_tasks == 0) return EP_OK;
+  if (st->path != kPathLut && st->path != kPathSearch)
+    return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
+  return launch_list(st->path, static_cast<const LayerDev*>(st->d_workspace), st->n_layers,
+                     st->total_tasks, st->lds_bytes, d_status, static_cast<hipStream_t>(stream),
+                     "ep_stack_decode");
 }
 
 }  // namespace ep
@@ -1258,6 +1328,17 @@ uint64_t ep_decode_layers_workspace(int n) { return ep::decode_layers_workspace(
 int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      int32_t* d_status, void* hip_stream) {
   return ep::decode_layers(layers, n, d_workspace, ws_bytes, d_status, hip_stream);
+}
+
+uint64_t ep_stack_workspace(int n) { return ep::stack_workspace(n); }
+
+int ep_stack_prepare(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
+                     ep_stack* stack, void* hip_stream) {
+  return ep::stack_prepare(layers, n, d_workspace, ws_bytes, stack, hip_stream);
+}
+
+int ep_stack_decode(const ep_stack* stack, int32_t* d_status, void* hip_stream) {
+  return ep::stack_decode(stack, d_status, hip_stream);
 }
 
 }  // extern "C"

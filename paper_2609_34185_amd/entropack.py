@@ -69,6 +69,12 @@ class Layer(C.Structure):
                 ("d_dequant", C.c_void_p), ("out_dtype", C.c_int32), ("reserved", C.c_int32)]
 
 
+class Stack(C.Structure):
+    _fields_ = [("d_workspace", C.c_void_p), ("n_layers", C.c_int32), ("path", C.c_uint32),
+                ("total_tasks", C.c_uint32), ("lds_bytes", C.c_uint32),
+                ("reserved", C.c_uint32 * 4)]
+
+
 class EntroPackError(RuntimeError):
     def __init__(self, code: int, what: str, msg: str):
         super().__init__(f"{what}: status {code}: {msg}")
@@ -97,6 +103,10 @@ def lib():
         L.ep_decode_layers_workspace.argtypes = [C.c_int]
         L.ep_decode_layers_workspace.restype = u64
         L.ep_decode_layers.argtypes = [C.POINTER(Layer), C.c_int, vp, u64, vp, vp]
+        L.ep_stack_workspace.argtypes = [C.c_int]
+        L.ep_stack_workspace.restype = u64
+        L.ep_stack_prepare.argtypes = [C.POINTER(Layer), C.c_int, vp, u64, C.POINTER(Stack), vp]
+        L.ep_stack_decode.argtypes = [C.POINTER(Stack), vp, vp]
         L.ep_gemm_i8_nt.argtypes = [vp, vp, vp, i64, i64, i64, vp]
         L.ep_last_error.restype = C.c_char_p
         _lib = L
@@ -104,7 +114,8 @@ def lib():
 
 
 EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_blob_free", "ep_blob_info",
-           "ep_decode_tiles", "ep_decode_layers_workspace", "ep_decode_layers", "ep_gemm_i8_nt",
+           "ep_decode_tiles", "ep_decode_layers_workspace", "ep_decode_layers",
+           "ep_stack_workspace", "ep_stack_prepare", "ep_stack_decode", "ep_gemm_i8_nt",
            "ep_last_error"]
 
 
@@ -160,8 +171,7 @@ def decode_layers_workspace(n: int) -> int:
     return int(lib().ep_decode_layers_workspace(n))
 
 
-def decode_layers(layers, d_ws: int, ws_bytes: int, d_status: int = 0, stream: int = 0):
-    """layers: sequence of (TensorInfo, d_blob, d_out, d_dequant, out_dtype)."""
+def _layer_array(layers):
     arr = (Layer * len(layers))()
     for i, (info, blob, out, dq, dt) in enumerate(layers):
         arr[i].info = info
@@ -169,8 +179,31 @@ def decode_layers(layers, d_ws: int, ws_bytes: int, d_status: int = 0, stream: i
         arr[i].d_out = out
         arr[i].d_dequant = dq or None
         arr[i].out_dtype = dt
+    return arr
+
+
+def decode_layers(layers, d_ws: int, ws_bytes: int, d_status: int = 0, stream: int = 0):
+    """layers: sequence of (TensorInfo, d_blob, d_out, d_dequant, out_dtype)."""
+    arr = _layer_array(layers)
     _check(lib().ep_decode_layers(arr, len(layers), d_ws, ws_bytes, d_status or None,
                                   stream or None), "ep_decode_layers")
+
+
+def stack_workspace(n: int) -> int:
+    return int(lib().ep_stack_workspace(n))
+
+
+def stack_prepare(layers, d_ws: int, ws_bytes: int, stream: int = 0) -> Stack:
+    """Write the device descriptors of `layers` once; returns the prepared stack."""
+    st = Stack()
+    arr = _layer_array(layers)
+    _check(lib().ep_stack_prepare(arr, len(layers), d_ws, ws_bytes, C.byref(st), stream or None),
+           "ep_stack_prepare")
+    return st
+
+
+def stack_decode(st: Stack, d_status: int = 0, stream: int = 0):
+    _check(lib().ep_stack_decode(C.byref(st), d_status or None, stream or None), "ep_stack_decode")
 
 
 def gemm_i8_nt(d_a: int, d_b: int, d_y: int, m: int, n: int, k: int, stream: int = 0):

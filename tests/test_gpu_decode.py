@@ -225,6 +225,45 @@ def test_config3_full_size_fp8_in_one_launch(E, oracle, mlp_fp8_blobs):
         assert np.array_equal(dqs[n].cpu().numpy(), refs[n][1]), n
 
 
+def test_prepared_stack_decodes_like_the_oracle(E, oracle, mlp_fp8_blobs):
+    """ep_stack_prepare once, then ep_stack_decode twice into cleared outputs: both decodes
+    equal the oracle (the descriptors stay valid across launches)."""
+    names = ["gate", "up", "down"]
+    infos = {n: E.blob_info(mlp_fp8_blobs[n]) for n in names}
+    dev = {n: E.to_device(mlp_fp8_blobs[n]) for n in names}
+    outs = {n: torch.zeros((infos[n].rows, infos[n].cols), dtype=torch.float8_e4m3fn, device="cuda")
+            for n in names}
+    dqs = {n: torch.zeros(infos[n].rows, dtype=torch.float32, device="cuda") for n in names}
+    layers = [(infos[n], dev[n].data_ptr(), outs[n].data_ptr(), dqs[n].data_ptr(), E.FP8_E4M3)
+              for n in names]
+    ws = E.stack_workspace(len(layers))
+    d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    st = E.stack_prepare(layers, d_ws.data_ptr(), ws, stream)
+    assert st.n_layers == 3 and st.path == 1 and st.total_tasks == 65280 // 4
+    refs = {n: oracle.decode(mlp_fp8_blobs[n], oracle.FP8) for n in names}
+    for rep in range(2):
+        for n in names:
+            outs[n].view(torch.uint8).fill_(0x55)
+            dqs[n].fill_(-1.0)
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        say(f"  ep_stack_decode, launch {rep}")
+        E.stack_decode(st, status.data_ptr(), stream)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        for n in names:
+            assert np.array_equal(gpu_bits(outs[n]), refs[n][0]), (rep, n)
+            assert np.array_equal(dqs[n].cpu().numpy(), refs[n][1]), (rep, n)
+
+
+def test_stack_rejects_bad_arguments(E):
+    st = E.Stack()
+    assert E.lib().ep_stack_decode(None, None, None) == E.ERR_ARG
+    st.n_layers = 2   # never prepared: no workspace
+    assert E.lib().ep_stack_decode(E.C.byref(st), None, None) == E.ERR_ARG
+    assert E.lib().ep_stack_prepare(None, 1, None, 0, E.C.byref(st), None) == E.ERR_ARG
+
+
 def test_config3_product_encoder_reproduces_oracle_blobs(E, mlp, mlp_fp8_blobs):
     """The benchmark encodes with the library's encoder; at full size it emits the same bytes."""
     for n in ["gate", "down"]:
