@@ -86,6 +86,7 @@ struct Hot {
   uint32_t out_dtype, saturate, coset_f0, coset_f1;
   uint32_t pay_bytes, div_magic, div_shift, div_pow2;
   uint32_t meta, bucket;          // search path: u32 index of the metadata, u16 index of the buckets
+  uint32_t bucket_shift, bucket_n1; // search path: b - k and 2^k + 1
   uint32_t off_sigma, off_delta, off_states, off_offsets, off_payload;
 };
 
@@ -118,8 +119,13 @@ __device__ __forceinline__ Hot make_hot(const LayerDev& L) {
   H.div_magic = uni(L.div_magic);
   H.div_shift = uni(L.div_shift);
   H.div_pow2 = uni(L.div_pow2);
-  H.meta = uni(search_layout(L.sum_A).meta / 4);
-  H.bucket = uni(search_layout(L.sum_A).bucket / 2);
+  {
+    const SearchLayout S = search_layout(L.b, L.sum_A);
+    H.meta = uni(S.meta / 4);
+    H.bucket = uni(S.bucket / 2);
+    H.bucket_shift = uni(L.b - S.bucket_bits);
+    H.bucket_n1 = uni((1u << S.bucket_bits) + 1);
+  }
   H.off_sigma = uni((uint32_t)L.off_sigma);
   H.off_delta = uni((uint32_t)L.off_delta);
   H.off_states = uni((uint32_t)L.off_states);
@@ -434,15 +440,16 @@ __device__ __forceinline__ void decode_field(const Hot& L, const uint32_t* lds, 
     x = __umul24(e & 0xFFFu, x >> B) + ((e >> 12) & 0x7FFu);
     dval = (int32_t)e >> 23;
   } else {
-    // Bucketed search: the bucket of u (its top 8 bits) bounds the symbol to
-    // [bk[j], bk[j + 1]]; a binary search on the u16 cumulative table narrows it.
+    // Bucketed search: the bucket j of u (its top k bits) bounds the symbol to
+    // [bk[j], bk[j + 1]]; a binary search on the u16 cumulative table narrows
+    // it (nothing to search when buckets are single slots).
     const uint16_t* cum = reinterpret_cast<const uint16_t*>(lds);
     const uint32_t u = x & ((1u << L.b) - 1);
     const uint32_t t = 8 * c + (uint32_t)(field - 1);
     const uint32_t base = lds[L.meta + t];
-    const uint16_t* bk = cum + L.bucket + t * kBuckets1;
-    const uint32_t j = u >> (L.b - kBucketBits);
-    uint32_t lo = bk[j], hi = bk[j + 1];
+    const uint16_t* bk = cum + L.bucket + t * L.bucket_n1;
+    const uint32_t j = u >> L.bucket_shift;
+    uint32_t lo = bk[j], hi = L.bucket_shift ? bk[j + 1] : lo;
     while (lo < hi) {
       const uint32_t mid = (lo + hi + 1) >> 1;
       if (cum[base + mid] <= u) lo = mid;
@@ -590,6 +597,10 @@ constexpr uint32_t kFastBlockWords = 128;
 constexpr uint32_t kFastChainBytes = 2 * kFastRingBytes;
 constexpr uint32_t kFastOob = 0x80000000u;   // buffer offset past any payload section
 static_assert(kWavesPerGroup * 2 * kFastChainBytes <= kRingBytes, "fast ring area");
+static_assert(search_layout(11, 0).total % kFastRingBytes == 0 &&
+                  search_layout(12, 12345).total % kFastRingBytes == 0 &&
+                  (64u << 9) % kFastRingBytes == 0,
+              "ring areas start on a ring-size boundary (rings are addressed as base | offset)");
 
 struct FastChain {     // wave-uniform, in payload words
   uint32_t OA, OB;     // read position, from the first block of each half's stream
@@ -735,6 +746,51 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
       : "vcc", "scc", "memory");
 }
 
+// The same refill in plain code, for the search path's steady state.
+__device__ __forceinline__ void refill_staged(uint32_t& x, uint32_t& SA, uint32_t& SB,
+                                              const uint8_t* lds, uint32_t vrb, uint32_t vH) {
+  const uint64_t m = __ballot(x < kStateLow);
+  const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+  const uint32_t clo = uni((uint32_t)__builtin_popcount(lo));
+  const uint32_t chi = uni((uint32_t)__builtin_popcount(hi));
+  const uint32_t pre = __builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
+  const int32_t dd = (int32_t)(SB - SA) - (int32_t)clo;
+  const uint32_t idx = (uint32_t)(__mul24((int32_t)vH, dd) + (int32_t)pre);
+  const uint32_t a = vrb | (((idx + SA) << 1) & (kFastRingBytes - 1));
+  const uint32_t w = *reinterpret_cast<const uint16_t*>(lds + a);
+  if (x < kStateLow) x = (x << 16) | w;
+  SA = uni(SA + clo);
+  SB = uni(SB + chi);
+}
+
+// Coset and field steps of the search path for both chains (plain code).
+__device__ __forceinline__ void coset_step_search(const Hot& L, uint32_t* x, uint32_t* c,
+                                                  FastChain& F0, FastChain& F1, const uint8_t* lds,
+                                                  uint32_t vrb0, uint32_t vrb1, uint32_t vH) {
+  const uint32_t mask = (1u << L.b) - 1;
+#pragma unroll
+  for (int j = 0; j < 2; j++) {
+    const uint32_t u = x[j] & mask;
+    c[j] = u >= L.coset_f0 ? 1u : 0u;
+    const uint32_t f = c[j] ? L.coset_f1 : L.coset_f0;
+    const uint32_t F = c[j] ? L.coset_f0 : 0u;
+    x[j] = __umul24(f, x[j] >> L.b) + u - F;
+  }
+  refill_staged(x[0], F0.OA, F0.OB, lds, vrb0, vH);
+  refill_staged(x[1], F1.OA, F1.OB, lds, vrb1, vH);
+}
+
+template <int FIELD>
+__device__ __forceinline__ void field_step_search(const Hot& L, const uint32_t* tab, uint32_t* x,
+                                                  const uint32_t* c, int32_t (*d)[9], FastChain& F0,
+                                                  FastChain& F1, const uint8_t* lds, uint32_t vrb0,
+                                                  uint32_t vrb1, uint32_t vH) {
+#pragma unroll
+  for (int j = 0; j < 2; j++) decode_field<kPathSearch, 0>(L, tab, FIELD, 0, c[j], x[j], d[j][FIELD]);
+  refill_staged(x[0], F0.OA, F0.OB, lds, vrb0, vH);
+  refill_staged(x[1], F1.OA, F1.OB, lds, vrb1, vH);
+}
+
 // Set up one chain (tiles tA on lanes 0-31, tA + 1 on lanes 32-63) from the
 // word offsets pA0..pA1 and pB0..pB1 of the two streams: request the first two
 // blocks of each stream (returned, for the ring) and the third (into pend).
@@ -755,11 +811,13 @@ __device__ __forceinline__ u32x4 fast_start(FastChain& F, u32x2& pend, __amdgpu_
   return first;
 }
 
-// The steady-state task: four full tiles (two chains), slot-table path,
-// output type DT.
-template <int B, int DT, bool SAT>
+// The steady-state task: four full tiles (two chains), output type DT.  The
+// slot-table path runs the hand-scheduled steps, the search path plain ones;
+// staging, reconstruction and stores are shared.
+template <int PATH, int B, int DT, bool SAT>
 __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                                  uint32_t task, int32_t* status) {
+  const uint32_t* tab = reinterpret_cast<const uint32_t*>(lds);
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
   const uint32_t half = lane >> 5, l = lane & 31;
   const EP_GLOBAL uint32_t* states = gptr<const uint32_t>(L.blob + L.off_states);
@@ -818,9 +876,15 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
       sg[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row[j], 0, 0));
     uint32_t c[2], cb[2];
     int32_t d[2][9];
-    coset_step2<B>(x[0], x[1], c[0], c[1], cb[0], cb[1], vf0, vf1, F0, F1, vH, vrb0, vrb1);
-#define EP_FIELD(I) \
-  field_step2<B, I>(x[0], x[1], cb[0], cb[1], d[0][I], d[1][I], F0, F1, vH, vrb0, vrb1);
+    if constexpr (PATH == kPathLut)
+      coset_step2<B>(x[0], x[1], c[0], c[1], cb[0], cb[1], vf0, vf1, F0, F1, vH, vrb0, vrb1);
+    else
+      coset_step_search(L, x, c, F0, F1, lds, vrb0, vrb1, vH);
+#define EP_FIELD(I)                                                                              \
+  if constexpr (PATH == kPathLut)                                                                \
+    field_step2<B, I>(x[0], x[1], cb[0], cb[1], d[0][I], d[1][I], F0, F1, vH, vrb0, vrb1);      \
+  else                                                                                           \
+    field_step_search<I>(L, tab, x, c, d, F0, F1, lds, vrb0, vrb1, vH);
     EP_FIELD(1) EP_FIELD(2)
     fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
     fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, 3 * 32);
@@ -872,30 +936,30 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 
 // Output-type dispatch of a full slot-table task.  Returns false for the
 // combinations the steady state does not cover (they take the generic loop).
-template <int B>
+template <int PATH, int B>
 __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                                      uint32_t task, int32_t* status) {
   switch (L.out_dtype) {
     case EP_BF16:
       if (L.saturate) return false;
-      decode_task_fast<B, EP_BF16, false>(L, lds, ring_area, task, status);
+      decode_task_fast<PATH, B, EP_BF16, false>(L, lds, ring_area, task, status);
       return true;
     case EP_FP16:
-      if (L.saturate) decode_task_fast<B, EP_FP16, true>(L, lds, ring_area, task, status);
-      else decode_task_fast<B, EP_FP16, false>(L, lds, ring_area, task, status);
+      if (L.saturate) decode_task_fast<PATH, B, EP_FP16, true>(L, lds, ring_area, task, status);
+      else decode_task_fast<PATH, B, EP_FP16, false>(L, lds, ring_area, task, status);
       return true;
     case EP_FP8_E4M3:
-      if (L.saturate) decode_task_fast<B, EP_FP8_E4M3, true>(L, lds, ring_area, task, status);
-      else decode_task_fast<B, EP_FP8_E4M3, false>(L, lds, ring_area, task, status);
+      if (L.saturate) decode_task_fast<PATH, B, EP_FP8_E4M3, true>(L, lds, ring_area, task, status);
+      else decode_task_fast<PATH, B, EP_FP8_E4M3, false>(L, lds, ring_area, task, status);
       return true;
     case EP_INT8:
-      decode_task_fast<B, EP_INT8, false>(L, lds, ring_area, task, status);
+      decode_task_fast<PATH, B, EP_INT8, false>(L, lds, ring_area, task, status);
       return true;
     case EP_FP32:
-      decode_task_fast<B, EP_FP32, false>(L, lds, ring_area, task, status);
+      decode_task_fast<PATH, B, EP_FP32, false>(L, lds, ring_area, task, status);
       return true;
     case EP_COORD2_I32:
-      decode_task_fast<B, EP_COORD2_I32, false>(L, lds, ring_area, task, status);
+      decode_task_fast<PATH, B, EP_COORD2_I32, false>(L, lds, ring_area, task, status);
       return true;
     default:
       return false;
@@ -906,43 +970,33 @@ __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds,
 // after the search tables (search path).
 template <int PATH>
 __device__ __forceinline__ uint32_t ring_offset(const LayerDev& L) {
-  return PATH == kPathLut ? (64u << L.b) : search_table_bytes(L.sum_A);
+  return PATH == kPathLut ? (64u << L.b) : search_layout(L.b, L.sum_A).total;
 }
 
 // Search-path tables (byte layout from search_layout): u16 cumulative values
 // of table t at [base_t + t, base_t + t + A_t] (the last one = 2^b), the u16
-// bucket bounds bk[t][0..256], and u32 metadata base'[16], min[16].
+// bucket bounds bk[t][0 .. 2^k] (bk[t][j] = the symbol whose slot range holds
+// slot j * 2^(b-k); bk[t][2^k] = A_t - 1), and u32 metadata base'[16], min[16].
+// Each symbol writes the bucket starts inside its own slot range.
 __device__ __forceinline__ void build_search(const LayerDev& L, uint32_t* lds) {
   uint16_t* cum = reinterpret_cast<uint16_t*>(lds);
-  const SearchLayout S = search_layout(L.sum_A);
-  scan_tables(L, [&](int t, uint32_t s, uint32_t F, uint32_t) { cum[L.tab_base[t] + t + s] = (uint16_t)F; },
-              [&](int t, uint32_t M) { cum[L.tab_base[t] + t + L.tab_A[t]] = (uint16_t)M; });
+  const SearchLayout S = search_layout(L.b, L.sum_A);
+  uint16_t* bk = cum + S.bucket / 2;
+  const uint32_t shift = L.b - S.bucket_bits, n1 = (1u << S.bucket_bits) + 1;
+  scan_tables(
+      L,
+      [&](int t, uint32_t s, uint32_t F, uint32_t f) {
+        cum[L.tab_base[t] + t + s] = (uint16_t)F;
+        const uint32_t j0 = (F + (1u << shift) - 1) >> shift, j1 = (F + f + (1u << shift) - 1) >> shift;
+        for (uint32_t j = j0; j < j1; j++) bk[t * n1 + j] = (uint16_t)s;
+      },
+      [&](int t, uint32_t M) {
+        cum[L.tab_base[t] + t + L.tab_A[t]] = (uint16_t)M;
+        bk[t * n1 + n1 - 1] = (uint16_t)(L.tab_A[t] ? L.tab_A[t] - 1 : 0);
+      });
   if (threadIdx.x < 32) {
     const uint32_t t = threadIdx.x & 15;
     lds[S.meta / 4 + threadIdx.x] = threadIdx.x < 16 ? L.tab_base[t] + t : (uint32_t)L.tab_min[t];
-  }
-  __syncthreads();
-  // bk[t][j] = largest s < A_t with F_s <= j * 2^(b - 8); bk[t][256] = A_t - 1.
-  uint16_t* bk = cum + S.bucket / 2;
-  const uint32_t w = 1u << (L.b - kBucketBits);
-  for (uint32_t k = threadIdx.x; k < 16 * kBuckets1; k += kThreads) {
-    const uint32_t t = k / kBuckets1, j = k % kBuckets1, A = L.tab_A[t];
-    const uint32_t base = L.tab_base[t] + t;
-    uint32_t s = 0;
-    if (A == 0) {
-      s = 0;
-    } else if (j == kBuckets1 - 1) {
-      s = A - 1;
-    } else {
-      uint32_t lo = 0, hi = A - 1;
-      while (lo < hi) {
-        const uint32_t mid = (lo + hi + 1) >> 1;
-        if (cum[base + mid] <= j * w) lo = mid;
-        else hi = mid - 1;
-      }
-      s = lo;
-    }
-    bk[k] = (uint16_t)s;
   }
 }
 
@@ -971,10 +1025,8 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
   const uint32_t nvec = L.rows * L.cvec;
   const bool full = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
                     (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
-  if constexpr (PATH == kPathLut) {
-    if (full && L.pay_bytes < kFastOob && decode_task_fast_any<B>(L, lb, ring_area, task, status))
-      return;
-  }
+  if (full && L.pay_bytes < kFastOob && decode_task_fast_any<PATH, B>(L, lb, ring_area, task, status))
+    return;
   if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, task, status);
   else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, task, status);
 }
@@ -1073,7 +1125,7 @@ DeviceProps device_props() {
 
 uint32_t lds_bytes(uint32_t path, const ep_tensor_info& I) {
   if (path == kPathLut) return (64u << I.prob_bits) + kRingBytes;
-  return search_table_bytes(I.sum_alphabet) + kRingBytes;
+  return search_layout(I.prob_bits, I.sum_alphabet).total + kRingBytes;
 }
 
 float dtype_max(int dt) {

@@ -19,31 +19,40 @@ constexpr int32_t kLutValueMin = -256;   // packed doubled coordinate: signed 9 
 constexpr int32_t kLutValueMax = 255;
 constexpr uint32_t kSearchLdsBytes = 128 * 1024;   // the payload rings take the other 32 KiB
 
-// Search path: 2^8 buckets per table (257 bounds), u16 cumulative tables.
-constexpr uint32_t kBucketBits = 8;
-constexpr uint32_t kBuckets1 = (1u << kBucketBits) + 1;
+// Search path: u16 cumulative tables plus, per table, 2^k + 1 u16 bucket
+// bounds (bucket j starts at slot j * 2^(b-k)); k is the largest of
+// min(b, 11) .. 8 whose tables fit, so that for b <= 11 and moderate table
+// sizes every bucket is a single slot and no search remains.
+constexpr uint32_t kBucketBitsMin = 8;
+constexpr uint32_t kBucketBitsMax = 11;
 
 struct SearchLayout {
+  uint32_t bucket_bits;           // k (0 when no k fits)
   uint32_t bucket, meta, total;   // byte offsets of the buckets and metadata; bytes in all
 };
 
-constexpr SearchLayout search_layout(uint32_t sum_A) {
+constexpr SearchLayout search_layout_k(uint32_t sum_A, uint32_t k) {
   // u16 cumulative values: sum_A + one end value per table, padded to 4 bytes
   const uint32_t cum = (2 * (sum_A + 16) + 3) & ~3u;
   const uint32_t bucket = cum;
-  const uint32_t meta = (bucket + 2 * 16 * kBuckets1 + 3) & ~3u;
-  const uint32_t total = (meta + 4 * 32 + 15) & ~15u;
-  return SearchLayout{bucket, meta, total};
+  const uint32_t meta = (bucket + 2 * 16 * ((1u << k) + 1) + 3) & ~3u;
+  // the payload rings that follow are addressed as base | offset: 512-byte aligned
+  const uint32_t total = (meta + 4 * 32 + 511) & ~511u;
+  return SearchLayout{k, bucket, meta, total};
 }
 
-constexpr uint32_t search_table_bytes(uint32_t sum_A) {
-  return search_layout(sum_A).total;
+constexpr SearchLayout search_layout(uint32_t b, uint32_t sum_A) {
+  for (uint32_t k = (b < kBucketBitsMax ? b : kBucketBitsMax); k >= kBucketBitsMin; k--) {
+    const SearchLayout S = search_layout_k(sum_A, k);
+    if (S.total <= kSearchLdsBytes) return S;
+  }
+  return SearchLayout{0, 0, 0, 0};
 }
 
 inline uint32_t choose_path(const ep_tensor_info& I) {
   if (I.prob_bits <= kLutMaxBits && I.coord2_min >= kLutValueMin && I.coord2_max <= kLutValueMax)
     return kPathLut;
-  if (I.sum_alphabet <= 0xFFFF0u && search_table_bytes(I.sum_alphabet) <= kSearchLdsBytes)
+  if (I.sum_alphabet <= 0xFFFF0u && search_layout(I.prob_bits, I.sum_alphabet).bucket_bits)
     return kPathSearch;
   return kPathNone;
 }
