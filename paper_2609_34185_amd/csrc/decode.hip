@@ -637,55 +637,67 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
   }
 }
 
-// One refill of one chain inside the step: 64-lane ballot of states below
-// 2^15, the per-half word index from v_mbcnt (upper-half lanes corrected by
-// the distance between the two read positions), the ring read at byte
-// vrb | (2 (O + index) mod 512), and the scalar advance of both positions.
-#define EP_REFILL(X, T, W, CLO, CHI, SA, SB, VRB, SAVE)             \
-  "v_cmp_gt_u32_e32 vcc, 0x8000, %[" X "]\n\t"                        \
-  "s_bcnt1_i32_b32 %[" CLO "], vcc_lo\n\t"                           \
-  "s_bcnt1_i32_b32 %[" CHI "], vcc_hi\n\t"                           \
-  "v_mbcnt_lo_u32_b32 %[" T "], vcc_lo, 0\n\t"                        \
-  "v_mbcnt_hi_u32_b32 %[" T "], vcc_hi, %[" T "]\n\t"                 \
-  "s_sub_u32 %[dd], %[" SB "], %[" SA "]\n\t"                        \
-  "s_sub_u32 %[dd], %[dd], %[" CLO "]\n\t"                           \
-  "v_mad_i32_i24 %[" T "], %[vH], %[dd], %[" T "]\n\t"                \
-  "v_add_lshl_u32 %[" T "], %[" T "], %[" SA "], 1\n\t"               \
-  "v_and_or_b32 %[" T "], %[" T "], %[rmask], %[" VRB "]\n\t"         \
-  "ds_read_u16 %[" W "], %[" T "]\n\t"                                \
-  SAVE                                                                \
-  "s_add_u32 %[" SA "], %[" SA "], %[" CLO "]\n\t"                   \
-  "s_add_u32 %[" SB "], %[" SB "], %[" CHI "]\n\t"
-
-#define EP_MERGE                                                      \
-  "s_waitcnt lgkmcnt(0)\n\t"                                          \
-  "v_lshl_or_b32 %[w0], %[x0], 16, %[w0]\n\t"                        \
-  "v_cndmask_b32_e64 %[x0], %[x0], %[w0], %[m0]\n\t"                 \
-  "v_lshl_or_b32 %[w1], %[x1], 16, %[w1]\n\t"                        \
-  "v_cndmask_b32_e32 %[x1], %[x1], %[w1], vcc\n\t"
-
-#define EP_REFILL2                                                                          \
-  EP_REFILL("x0", "t0", "w0", "c0lo", "c0hi", "SA0", "SB0", "vrb0", "s_mov_b64 %[m0], vcc\n\t") \
-  EP_REFILL("x1", "t1", "w1", "c1lo", "c1hi", "SA1", "SB1", "vrb1", "")                        \
-  EP_MERGE
+// One symbol step of both chains.  Chain 0's refill ballot lives in VCC,
+// chain 1's in s[94:95] (clobbered), so the two refills can be interleaved
+// instruction by instruction.  Per chain: 64-lane ballot of states below
+// 2^15, per-half word index from v_mbcnt (upper-half lanes corrected by the
+// distance between the two read positions, dd = SB - SA - popcount(lower
+// half)), the ring read at byte vrb | (2 (SA + index) mod 512), the scalar
+// advance of both read positions, and the merge x = need ? x << 16 | w : x.
+#define EP_REFILL_BOTH                                                      \
+  "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
+  "v_cmp_gt_u32_e64 s[94:95], %[k15], %[x1]\n\t"                            \
+  "s_bcnt1_i32_b32 %[c0lo], vcc_lo\n\t"                                    \
+  "v_mbcnt_lo_u32_b32 %[t0], vcc_lo, 0\n\t"                                 \
+  "s_bcnt1_i32_b32 %[c0hi], vcc_hi\n\t"                                    \
+  "v_mbcnt_lo_u32_b32 %[t1], s94, 0\n\t"                                    \
+  "s_sub_u32 %[d0], %[SB0], %[SA0]\n\t"                                     \
+  "v_mbcnt_hi_u32_b32 %[t0], vcc_hi, %[t0]\n\t"                             \
+  "s_sub_u32 %[d0], %[d0], %[c0lo]\n\t"                                    \
+  "v_mbcnt_hi_u32_b32 %[t1], s95, %[t1]\n\t"                                \
+  "s_bcnt1_i32_b32 %[c1lo], s94\n\t"                                       \
+  "v_mad_i32_i24 %[t0], %[vH], %[d0], %[t0]\n\t"                            \
+  "s_bcnt1_i32_b32 %[c1hi], s95\n\t"                                       \
+  "v_add_lshl_u32 %[t0], %[t0], %[SA0], 1\n\t"                              \
+  "s_sub_u32 %[d1], %[SB1], %[SA1]\n\t"                                     \
+  "v_and_or_b32 %[t0], %[t0], %[rmask], %[vrb0]\n\t"                        \
+  "s_sub_u32 %[d1], %[d1], %[c1lo]\n\t"                                    \
+  "ds_read_u16 %[w0], %[t0]\n\t"                                            \
+  "v_mad_i32_i24 %[t1], %[vH], %[d1], %[t1]\n\t"                            \
+  "s_add_u32 %[SA0], %[SA0], %[c0lo]\n\t"                                  \
+  "v_add_lshl_u32 %[t1], %[t1], %[SA1], 1\n\t"                              \
+  "s_add_u32 %[SB0], %[SB0], %[c0hi]\n\t"                                  \
+  "v_and_or_b32 %[t1], %[t1], %[rmask], %[vrb1]\n\t"                        \
+  "s_add_u32 %[SA1], %[SA1], %[c1lo]\n\t"                                  \
+  "ds_read_u16 %[w1], %[t1]\n\t"                                            \
+  "s_add_u32 %[SB1], %[SB1], %[c1hi]\n\t"                                  \
+  "s_waitcnt lgkmcnt(1)\n\t"                                                \
+  "v_lshl_or_b32 %[w0], %[x0], 16, %[w0]\n\t"                               \
+  "v_cndmask_b32_e32 %[x0], %[x0], %[w0], vcc\n\t"                          \
+  "s_waitcnt lgkmcnt(0)\n\t"                                                \
+  "v_lshl_or_b32 %[w1], %[x1], 16, %[w1]\n\t"                               \
+  "v_cndmask_b32_e64 %[x1], %[x1], %[w1], s[94:95]\n\t"
 
 #define EP_STEP_OUTS                                                                      \
   [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [SB0] "+s"(F0.OB), [SA1] "+s"(F1.OA),  \
       [SB1] "+s"(F1.OB), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),  \
       [g0] "=&v"(g0), [g1] "=&v"(g1), [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0),     \
       [w1] "=&v"(w1), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo),          \
-      [c1hi] "=&s"(c1hi), [dd] "=&s"(dd), [m0] "=&s"(m0)
+      [c1hi] "=&s"(c1hi), [d0] "=&s"(dd0), [d1] "=&s"(dd1)
 
-#define EP_STEP_INS \
-  [vH] "v"(vH), [vrb0] "v"(vrb0), [vrb1] "v"(vrb1), [rmask] "s"(kFastRingBytes - 1)
+#define EP_STEP_INS                                                                          \
+  [vH] "v"(vH), [vrb0] "v"(vrb0), [vrb1] "v"(vrb1), [rmask] "s"(kFastRingBytes - 1),         \
+      [k15] "s"(kStateLow)
 
-// Field symbol (table 8c + FIELD - 1) for both chains, then refill.
+#define EP_STEP_CLOBBERS "vcc", "scc", "s94", "s95", "memory"
+
+// Field symbol (table 8c + FIELD - 1) for both chains, then refill.  Chain
+// 0's decode starts as soon as its own table read returns.
 template <int B, int FIELD>
 __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
                                             int32_t& d0, int32_t& d1, FastChain& F0, FastChain& F1,
                                             uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
-  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd;
-  uint64_t m0;
+  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;
   asm volatile(
       "v_and_b32 %[u0], %[mk], %[x0]\n\t"
       "v_and_b32 %[u1], %[mk], %[x1]\n\t"
@@ -695,20 +707,21 @@ __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t
       "ds_read_b32 %[e1], %[u1] offset:%[off]\n\t"
       "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
       "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
-      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_waitcnt lgkmcnt(1)\n\t"
       "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
       "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
+      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
+      "v_ashrrev_i32 %[dv0], 23, %[e0]\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
       "v_and_b32 %[u1], 0xfff, %[e1]\n\t"
       "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"
-      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
       "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"
-      "v_ashrrev_i32 %[d0], 23, %[e0]\n\t"
-      "v_ashrrev_i32 %[d1], 23, %[e1]\n\t"
-      EP_REFILL2
-      : EP_STEP_OUTS, [d0] "=&v"(d0), [d1] "=&v"(d1)
+      "v_ashrrev_i32 %[dv1], 23, %[e1]\n\t"
+      EP_REFILL_BOTH
+      : EP_STEP_OUTS, [dv0] "=&v"(d0), [dv1] "=&v"(d1)
       : [cb0] "v"(cb0), [cb1] "v"(cb1), [mk] "i"((1 << B) - 1), [b] "i"(B),
         [off] "i"((FIELD - 1) * (4 << B)), EP_STEP_INS
-      : "vcc", "scc", "memory");
+      : EP_STEP_CLOBBERS);
 }
 
 // Coset symbol (two-entry table f0, f1) for both chains, then refill.  Returns
@@ -718,8 +731,7 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
                                             uint32_t& cb0, uint32_t& cb1, uint32_t vf0, uint32_t vf1,
                                             FastChain& F0, FastChain& F1, uint32_t vH,
                                             uint32_t vrb0, uint32_t vrb1) {
-  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd;
-  uint64_t m0;
+  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;
   asm volatile(
       "v_and_b32 %[u0], %[mk], %[x0]\n\t"
       "v_and_b32 %[u1], %[mk], %[x1]\n\t"
@@ -739,11 +751,11 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
       "v_sub_u32_e32 %[x1], %[x1], %[t1]\n\t"
       "v_lshlrev_b32 %[cb0], %[b5], %[c0]\n\t"
       "v_lshlrev_b32 %[cb1], %[b5], %[c1]\n\t"
-      EP_REFILL2
+      EP_REFILL_BOTH
       : EP_STEP_OUTS, [c0] "=&v"(c0), [c1] "=&v"(c1), [cb0] "=&v"(cb0), [cb1] "=&v"(cb1)
       : [vf0] "v"(vf0), [vf1] "v"(vf1), [mk] "i"((1 << B) - 1), [b] "i"(B), [b5] "i"(B + 5),
         EP_STEP_INS
-      : "vcc", "scc", "memory");
+      : EP_STEP_CLOBBERS);
 }
 
 // The same refill in plain code, for the search path's steady state.
