@@ -159,7 +159,8 @@ __device__ __forceinline__ uint32_t fp16_pair(float a, float b) {
 }
 
 __device__ __forceinline__ uint32_t fp8_quad(float a, float b, float c, float d) {
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  // the first conversion fills the low half; its high half is overwritten next
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)__float_as_uint(a), false);
   w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
   return (uint32_t)w;
 }
@@ -643,7 +644,8 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
 // 2^15, per-half word index from v_mbcnt (upper-half lanes corrected by the
 // distance between the two read positions, dd = SB - SA - popcount(lower
 // half)), the ring read at byte vrb | (2 (SA + index) mod 512), the scalar
-// advance of both read positions, and the merge x = need ? x << 16 | w : x.
+// advance of both read positions, and the merge x = x << 16 | w on the
+// refilling lanes only (EXEC narrowed to each chain's ballot, then restored).
 #define EP_REFILL_BOTH                                                      \
   "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
   "v_cmp_gt_u32_e64 s[94:95], %[k15], %[x1]\n\t"                            \
@@ -671,25 +673,26 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
   "s_add_u32 %[SA1], %[SA1], %[c1lo]\n\t"                                  \
   "ds_read_u16 %[w1], %[t1]\n\t"                                            \
   "s_add_u32 %[SB1], %[SB1], %[c1hi]\n\t"                                  \
+  "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
   "s_waitcnt lgkmcnt(1)\n\t"                                                \
-  "v_lshl_or_b32 %[w0], %[x0], 16, %[w0]\n\t"                               \
-  "v_cndmask_b32_e32 %[x0], %[x0], %[w0], vcc\n\t"                          \
+  "v_lshl_or_b32 %[x0], %[x0], 16, %[w0]\n\t"                               \
+  "s_and_b64 exec, %[ex], s[94:95]\n\t"                                     \
   "s_waitcnt lgkmcnt(0)\n\t"                                                \
-  "v_lshl_or_b32 %[w1], %[x1], 16, %[w1]\n\t"                               \
-  "v_cndmask_b32_e64 %[x1], %[x1], %[w1], s[94:95]\n\t"
+  "v_lshl_or_b32 %[x1], %[x1], 16, %[w1]\n\t"                               \
+  "s_mov_b64 exec, %[ex]\n\t"
 
 #define EP_STEP_OUTS                                                                      \
   [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [SB0] "+s"(F0.OB), [SA1] "+s"(F1.OA),  \
       [SB1] "+s"(F1.OB), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),  \
       [g0] "=&v"(g0), [g1] "=&v"(g1), [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0),     \
       [w1] "=&v"(w1), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo),          \
-      [c1hi] "=&s"(c1hi), [d0] "=&s"(dd0), [d1] "=&s"(dd1)
+      [c1hi] "=&s"(c1hi), [d0] "=&s"(dd0), [d1] "=&s"(dd1), [ex] "=&s"(ex)
 
 #define EP_STEP_INS                                                                          \
   [vH] "v"(vH), [vrb0] "v"(vrb0), [vrb1] "v"(vrb1), [rmask] "s"(kFastRingBytes - 1),         \
       [k15] "s"(kStateLow)
 
-#define EP_STEP_CLOBBERS "vcc", "scc", "s94", "s95", "memory"
+#define EP_STEP_CLOBBERS "vcc", "scc", "exec", "s94", "s95", "memory"
 
 // Field symbol (table 8c + FIELD - 1) for both chains, then refill.  Chain
 // 0's decode starts as soon as its own table read returns.
@@ -698,6 +701,7 @@ __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t
                                             int32_t& d0, int32_t& d1, FastChain& F0, FastChain& F1,
                                             uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
   uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;
+  uint64_t ex;
   asm volatile(
       "v_and_b32 %[u0], %[mk], %[x0]\n\t"
       "v_and_b32 %[u1], %[mk], %[x1]\n\t"
@@ -732,6 +736,7 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
                                             FastChain& F0, FastChain& F1, uint32_t vH,
                                             uint32_t vrb0, uint32_t vrb1) {
   uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;
+  uint64_t ex;
   asm volatile(
       "v_and_b32 %[u0], %[mk], %[x0]\n\t"
       "v_and_b32 %[u1], %[mk], %[x1]\n\t"
