@@ -1218,11 +1218,15 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
   return EP_OK;
 }
 
+// Workgroups of a launch: as many as the CUs hold (one per CU when the tables
+// take most of the LDS), but never more than there are tasks.  A small layer
+// list is spread over all CUs rather than packed into few workgroups: a task
+// is a long serial chain of symbol rounds, so a lightly loaded CU finishes it
+// sooner.
 uint32_t groups_for(uint32_t path, uint32_t lds, uint32_t tasks, const DeviceProps& P) {
   uint32_t per_cu = path == kPathLut ? 1u : (uint32_t)std::max<size_t>(1, std::min<size_t>(2, 160 * 1024 / std::max<uint32_t>(lds, 1)));
   uint32_t g = (uint32_t)P.cus * per_cu;
-  uint32_t need = (tasks + kWavesPerGroup - 1) / kWavesPerGroup;
-  return std::max(1u, std::min(g, need));
+  return std::max(1u, std::min(g, tasks));
 }
 
 }  // namespace
