@@ -121,12 +121,14 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_i8_nt_kernel(const int8_t* 
   for (int64_t s = 0; s < steps; s += 2) {
     fetch_tile<kTileM>(ra, m, k, m0, (s + 2) * kTileK, t, ga0);
     fetch_tile<kTileN>(rb, n, k, n0, (s + 2) * kTileK, t, gb0);
+    __builtin_amdgcn_sched_barrier(0);   // issue the loads before this step's MFMAs
     compute(lds);
     stash_tile<kTileM>(lds + kStageBytes, t, ga1);
     stash_tile<kTileN>(lds + kStageBytes + kABytes, t, gb1);
     __syncthreads();
     fetch_tile<kTileM>(ra, m, k, m0, (s + 3) * kTileK, t, ga1);
     fetch_tile<kTileN>(rb, n, k, n0, (s + 3) * kTileK, t, gb1);
+    __builtin_amdgcn_sched_barrier(0);
     compute(lds + kStageBytes);
     stash_tile<kTileM>(lds, t, ga0);
     stash_tile<kTileN>(lds + kABytes, t, gb0);
