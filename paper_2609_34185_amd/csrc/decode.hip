@@ -646,6 +646,8 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
 // half)), the ring read at byte vrb | (2 (SA + index) mod 512), the scalar
 // advance of both read positions, and the merge x = x << 16 | w on the
 // refilling lanes only (EXEC narrowed to each chain's ballot, then restored).
+// The wave's issue priority drops back to 0 once both ring reads are in
+// flight (a field step raises it while its table entries are in hand).
 #define EP_REFILL_BOTH                                                      \
   "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
   "v_cmp_gt_u32_e64 s[94:95], %[k15], %[x1]\n\t"                            \
@@ -672,6 +674,7 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
   "v_and_or_b32 %[t1], %[t1], %[rmask], %[vrb1]\n\t"                        \
   "s_add_u32 %[SA1], %[SA1], %[c1lo]\n\t"                                  \
   "ds_read_u16 %[w1], %[t1]\n\t"                                            \
+  "s_setprio 0\n\t"                                                        \
   "s_add_u32 %[SB1], %[SB1], %[c1hi]\n\t"                                  \
   "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
   "s_waitcnt lgkmcnt(1)\n\t"                                                \
@@ -695,7 +698,10 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
 #define EP_STEP_CLOBBERS "vcc", "scc", "exec", "s94", "s95", "memory"
 
 // Field symbol (table 8c + FIELD - 1) for both chains, then refill.  Chain
-// 0's decode starts as soon as its own table read returns.
+// 0's decode starts as soon as its own table read returns.  From then until
+// the ring reads are issued the wave runs at raised issue priority: the
+// dependent ALU chain of a wave whose table reads have landed goes ahead of
+// waves that are still waiting, which shortens every wave's step latency.
 template <int B, int FIELD>
 __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
                                             int32_t& d0, int32_t& d1, FastChain& F0, FastChain& F1,
@@ -712,6 +718,7 @@ __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t
       "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
       "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
       "s_waitcnt lgkmcnt(1)\n\t"
+      "s_setprio 2\n\t"
       "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
       "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
       "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
