@@ -604,7 +604,8 @@ static_assert(search_layout(11, 0).total % kFastRingBytes == 0 &&
               "ring areas start on a ring-size boundary (rings are addressed as base | offset)");
 
 struct FastChain {     // wave-uniform, in payload words
-  uint32_t OA, OB;     // read position, from the first block of each half's stream
+  uint32_t OA, D;      // read position of half A, from the first block of its stream, and
+                       // the read position of half B (same origin for B) minus OA
   uint32_t QA, QB;     // committed end, same origin
   uint32_t CA, CB;     // payload word index of that first block
   uint32_t EA, EB;     // end of each tile's stream, same origin as CA / CB
@@ -619,7 +620,7 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
                                            uint32_t vrb8,
                                            uint32_t vl8, __amdgpu_buffer_rsrc_t rsrc,
                                            uint32_t half, uint32_t limit) {
-  const bool cA = uni(F.QA - F.OA) < limit, cB = uni(F.QB - F.OB) < limit;
+  const bool cA = uni(F.QA - F.OA) < limit, cB = uni(F.QB - F.OA - F.D) < limit;
   if (cA || cB) {
     if (cA && half == 0) {
       *reinterpret_cast<u32x2*>(lds + vrb8 + 2 * (F.QA & (kFastRingWords - 1))) = pendA;
@@ -642,9 +643,11 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
 // chain 1's in s[94:95] (clobbered), so the two refills can be interleaved
 // instruction by instruction.  Per chain: 64-lane ballot of states below
 // 2^15, per-half word index from v_mbcnt (upper-half lanes corrected by the
-// distance between the two read positions, dd = SB - SA - popcount(lower
-// half)), the ring read at byte vrb | (2 (SA + index) mod 512), the scalar
-// advance of both read positions, and the merge x = x << 16 | w on the
+// distance between the two read positions less the lower half's count, dd =
+// D - popcount(lower half), where the chain keeps D = SB - SA in place of
+// SB), the ring read at byte vrb | (2 (SA + index) mod 512), the scalar
+// advance SA += popcount(lower), D = dd + popcount(upper), and the merge
+// x = x << 16 | w on the
 // refilling lanes only (EXEC narrowed to each chain's ballot, then restored).
 // The wave's issue priority drops back to 0 once both ring reads are in
 // flight (a field step raises it while its table entries are in hand).
@@ -655,27 +658,25 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
   "v_mbcnt_lo_u32_b32 %[t0], vcc_lo, 0\n\t"                                 \
   "s_bcnt1_i32_b32 %[c0hi], vcc_hi\n\t"                                    \
   "v_mbcnt_lo_u32_b32 %[t1], s94, 0\n\t"                                    \
-  "s_sub_u32 %[d0], %[SB0], %[SA0]\n\t"                                     \
   "v_mbcnt_hi_u32_b32 %[t0], vcc_hi, %[t0]\n\t"                             \
-  "s_sub_u32 %[d0], %[d0], %[c0lo]\n\t"                                    \
+  "s_sub_u32 %[d0], %[D0], %[c0lo]\n\t"                                    \
   "v_mbcnt_hi_u32_b32 %[t1], s95, %[t1]\n\t"                                \
   "s_bcnt1_i32_b32 %[c1lo], s94\n\t"                                       \
   "v_mad_i32_i24 %[t0], %[vH], %[d0], %[t0]\n\t"                            \
   "s_bcnt1_i32_b32 %[c1hi], s95\n\t"                                       \
   "v_add_lshl_u32 %[t0], %[t0], %[SA0], 1\n\t"                              \
-  "s_sub_u32 %[d1], %[SB1], %[SA1]\n\t"                                     \
   "v_and_or_b32 %[t0], %[t0], %[rmask], %[vrb0]\n\t"                        \
-  "s_sub_u32 %[d1], %[d1], %[c1lo]\n\t"                                    \
+  "s_sub_u32 %[d1], %[D1], %[c1lo]\n\t"                                    \
   "ds_read_u16 %[w0], %[t0]\n\t"                                            \
   "v_mad_i32_i24 %[t1], %[vH], %[d1], %[t1]\n\t"                            \
   "s_add_u32 %[SA0], %[SA0], %[c0lo]\n\t"                                  \
   "v_add_lshl_u32 %[t1], %[t1], %[SA1], 1\n\t"                              \
-  "s_add_u32 %[SB0], %[SB0], %[c0hi]\n\t"                                  \
+  "s_add_u32 %[D0], %[d0], %[c0hi]\n\t"                                  \
   "v_and_or_b32 %[t1], %[t1], %[rmask], %[vrb1]\n\t"                        \
   "s_add_u32 %[SA1], %[SA1], %[c1lo]\n\t"                                  \
   "ds_read_u16 %[w1], %[t1]\n\t"                                            \
   "s_setprio 0\n\t"                                                        \
-  "s_add_u32 %[SB1], %[SB1], %[c1hi]\n\t"                                  \
+  "s_add_u32 %[D1], %[d1], %[c1hi]\n\t"                                  \
   "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
   "s_waitcnt lgkmcnt(1)\n\t"                                                \
   "v_lshl_or_b32 %[x0], %[x0], 16, %[w0]\n\t"                               \
@@ -685,8 +686,8 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
   "s_mov_b64 exec, %[ex]\n\t"
 
 #define EP_STEP_OUTS                                                                      \
-  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [SB0] "+s"(F0.OB), [SA1] "+s"(F1.OA),  \
-      [SB1] "+s"(F1.OB), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),  \
+  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [D0] "+s"(F0.D), [SA1] "+s"(F1.OA),  \
+      [D1] "+s"(F1.D), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),  \
       [g0] "=&v"(g0), [g1] "=&v"(g1), [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0),     \
       [w1] "=&v"(w1), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo),          \
       [c1hi] "=&s"(c1hi), [d0] "=&s"(dd0), [d1] "=&s"(dd1), [ex] "=&s"(ex)
@@ -771,20 +772,20 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
 }
 
 // The same refill in plain code, for the search path's steady state.
-__device__ __forceinline__ void refill_staged(uint32_t& x, uint32_t& SA, uint32_t& SB,
+__device__ __forceinline__ void refill_staged(uint32_t& x, uint32_t& SA, uint32_t& D,
                                               const uint8_t* lds, uint32_t vrb, uint32_t vH) {
   const uint64_t m = __ballot(x < kStateLow);
   const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
   const uint32_t clo = uni((uint32_t)__builtin_popcount(lo));
   const uint32_t chi = uni((uint32_t)__builtin_popcount(hi));
   const uint32_t pre = __builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
-  const int32_t dd = (int32_t)(SB - SA) - (int32_t)clo;
+  const int32_t dd = (int32_t)D - (int32_t)clo;
   const uint32_t idx = (uint32_t)(__mul24((int32_t)vH, dd) + (int32_t)pre);
   const uint32_t a = vrb | (((idx + SA) << 1) & (kFastRingBytes - 1));
   const uint32_t w = *reinterpret_cast<const uint16_t*>(lds + a);
   if (x < kStateLow) x = (x << 16) | w;
   SA = uni(SA + clo);
-  SB = uni(SB + chi);
+  D = uni((uint32_t)dd + chi);
 }
 
 // Coset and field steps of the search path for both chains (plain code).
@@ -800,8 +801,8 @@ __device__ __forceinline__ void coset_step_search(const Hot& L, uint32_t* x, uin
     const uint32_t F = c[j] ? L.coset_f0 : 0u;
     x[j] = __umul24(f, x[j] >> L.b) + u - F;
   }
-  refill_staged(x[0], F0.OA, F0.OB, lds, vrb0, vH);
-  refill_staged(x[1], F1.OA, F1.OB, lds, vrb1, vH);
+  refill_staged(x[0], F0.OA, F0.D, lds, vrb0, vH);
+  refill_staged(x[1], F1.OA, F1.D, lds, vrb1, vH);
 }
 
 template <int FIELD>
@@ -811,20 +812,45 @@ __device__ __forceinline__ void field_step_search(const Hot& L, const uint32_t* 
                                                   uint32_t vrb1, uint32_t vH) {
 #pragma unroll
   for (int j = 0; j < 2; j++) decode_field<kPathSearch, 0>(L, tab, FIELD, 0, c[j], x[j], d[j][FIELD]);
-  refill_staged(x[0], F0.OA, F0.OB, lds, vrb0, vH);
-  refill_staged(x[1], F1.OA, F1.OB, lds, vrb1, vH);
+  refill_staged(x[0], F0.OA, F0.D, lds, vrb0, vH);
+  refill_staged(x[1], F1.OA, F1.D, lds, vrb1, vH);
 }
 
 // Set up one chain (tiles tA on lanes 0-31, tA + 1 on lanes 32-63) from the
 // word offsets pA0..pA1 and pB0..pB1 of the two streams: request the first two
 // blocks of each stream (returned, for the ring) and the third (into pend).
+// Minimum of two wave-uniform values on the scalar unit (left to itself the
+// compiler computes it on the vector unit and reads the result back).
+__device__ __forceinline__ uint32_t smin(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("s_min_u32 %0, %1, %2" : "=s"(r) : "s"(a), "s"(b));
+  return r;
+}
+
+// Both chains' staging at one point of the round: a single scalar test of the
+// smallest of the four margins skips the per-half work when no half needs it
+// (the common case: at typical rates a half consumes well under a block per
+// round).
+__device__ __forceinline__ void fast_stage_both(FastChain& F0, FastChain& F1, u32x2& pendA0,
+                                                u32x2& pendB0, u32x2& pendA1, u32x2& pendB1,
+                                                uint8_t* lds, uint32_t vrb08, uint32_t vrb18,
+                                                uint32_t vl8, __amdgpu_buffer_rsrc_t rsrc,
+                                                uint32_t half, uint32_t limit) {
+  const uint32_t m = smin(smin(F0.QA - F0.OA, F0.QB - F0.OA - F0.D),
+                          smin(F1.QA - F1.OA, F1.QB - F1.OA - F1.D));
+  if (__builtin_expect(m < limit, 0)) {
+    fast_stage(F0, pendA0, pendB0, lds, vrb08, vl8, rsrc, half, limit);
+    fast_stage(F1, pendA1, pendB1, lds, vrb18, vl8, rsrc, half, limit);
+  }
+}
+
 __device__ __forceinline__ u32x4 fast_start(FastChain& F, u32x2& pend, __amdgpu_buffer_rsrc_t rsrc,
                                             uint32_t half, uint32_t l, uint32_t pA0, uint32_t pA1,
                                             uint32_t pB0, uint32_t pB1) {
   F.CA = pA0 & ~(kFastBlockWords - 1);
   F.CB = pB0 & ~(kFastBlockWords - 1);
   F.OA = pA0 - F.CA;
-  F.OB = pB0 - F.CB;
+  F.D = (pB0 - F.CB) - F.OA;
   F.QA = F.QB = kFastRingWords;
   F.EA = pA1 - F.CA;
   F.EB = pB1 - F.CB;
@@ -892,8 +918,8 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 
   for (uint32_t k = 0; k < rounds; k++) {
     // room for a block: margin <= ring - block
-    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, kFastRingWords - kFastBlockWords + 1);
-    fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, kFastRingWords - kFastBlockWords + 1);
+    fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half,
+                    kFastRingWords - kFastBlockWords + 1);
     float sg[2];
 #pragma unroll
     for (int j = 0; j < 2; j++)
@@ -910,11 +936,9 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
   else                                                                                           \
     field_step_search<I>(L, tab, x, c, d, F0, F1, lds, vrb0, vrb1, vH);
     EP_FIELD(1) EP_FIELD(2)
-    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
-    fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, 3 * 32);
+    fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
-    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
-    fast_stage(F1, pend1, pendB1, lds, vrb18, vl8, rsrc, half, 3 * 32);
+    fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
 #undef EP_FIELD
 #pragma unroll
@@ -946,7 +970,7 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
   for (int j = 0; j < 2; j++) {
     if (x[j] != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
     const FastChain& F = j ? F1 : F0;
-    const uint32_t P = half ? F.OB : F.OA, E = half ? F.EB : F.EA;
+    const uint32_t P = half ? F.OA + F.D : F.OA, E = half ? F.EB : F.EA;
     if (l == 0 && P != E) err |= P > E ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
     if (L.container && L.dequant) {
       const EP_GLOBAL float* delta = gptr<const float>(L.blob + L.off_delta);
