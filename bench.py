@@ -22,8 +22,10 @@ activations, timed separately: decode time over product time is reported).
 The roofline's `traffic` field is the decode kernel's measured HBM bytes per
 launch, read from the committed rocprofv3 counter summary of this workload
 (FETCH_SIZE and WRITE_SIZE, each scaled by the factor the same counter shows
-for a plain device copy of known size); it is null when the summary is absent
-or was taken from a different decode kernel source than the one built.
+for a plain device copy of known size); `counters` carries the kernel's VALU,
+SALU and LDS utilisation from the committed SQ counter summary.  Both are null
+when their summary is absent or was taken from a different decode kernel
+source than the one built.
 
 --copy-calibration runs only a plain 1 GiB device-to-device copy (five times),
 the reference kernel for those counter factors.
@@ -98,12 +100,10 @@ def source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(workload_name: str):
-    """HBM bytes per decode launch from profiles/decode_<workload>_traffic.txt, or None.
-
-    The summary holds `key: value` lines; the figures count only when the
-    recorded decode source digest equals the current one."""
-    path = os.path.join(ROOT, "profiles", f"decode_{workload_name}_traffic.txt")
+def profile_summary(name: str):
+    """The `key: value` lines of profiles/<name>, or None when the file is
+    absent or was taken from a decode kernel source other than the one built."""
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     kv = {}
@@ -112,9 +112,31 @@ def measured_traffic(workload_name: str):
             if ":" in line and not line.startswith(("#", " ", "\t")):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
+    return kv if kv.get("decode_source_sha256") == source_digest() else None
+
+
+def measured_counters(workload_name: str):
+    """Unit utilisation of the decode kernel from its committed SQ counter summary, or None."""
+    kv = profile_summary(f"decode_{workload_name}_sq_counters.txt")
+    if kv is None:
+        return None
     try:
-        if kv.get("decode_source_sha256") != source_digest():
-            return None
+        return {"valu_busy": float(kv["valu_busy_pct"]) / 100,
+                "salu_busy": float(kv["salu_busy_pct"]) / 100,
+                "lds_busy": float(kv["lds_busy_pct"]) / 100,
+                "lds_bank_conflict_stall": float(kv["lds_bank_conflict_pct"]) / 100,
+                "valu_lane_ops_per_weight": float(kv["valu_lane_ops_per_weight"]),
+                "source": f"profiles/decode_{workload_name}_sq_counters.txt"}
+    except (KeyError, ValueError):
+        return None
+
+
+def measured_traffic(workload_name: str):
+    """HBM bytes per decode launch from profiles/decode_<workload>_traffic.txt, or None."""
+    kv = profile_summary(f"decode_{workload_name}_traffic.txt")
+    if kv is None:
+        return None
+    try:
         fetch = float(kv["fetch_kib_per_launch"]) * float(kv["copy_fetch_factor"])
         write = float(kv["write_kib_per_launch"]) * float(kv["copy_write_factor"])
         return 1024.0 * (fetch + write)
@@ -311,6 +333,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gbps / HBM_PEAK_GBPS, "traffic": traffic},
     }
+    line["counters"] = measured_counters(args.workload)
     if gemm is not None:
         line["config"]["gemm"] = gemm
     if not args.no_cpu_baseline:
