@@ -16,8 +16,10 @@
 // waves walk the range.  Two table families exist:
 //   kPathLut    packed slot table, one LDS read per symbol: for table
 //               (field i, coset c) and slot u in [0, 2^b) the 32-bit entry
-//               holds f (bits 0-11), u - F (bits 12-22) and the doubled
-//               coordinate value (bits 23-31, signed) -- b <= 11 only;
+//               holds f (bits 0-11), u - F (bits 12-22) and, as a signed
+//               byte in bits 24-31, the integer part z of the coordinate
+//               (2p_i = 2z + c; for field 8, z = 2m, so 2p_8 = 2(z + pi) + c)
+//               -- b <= 11 only;
 //   kPathSearch per-symbol cumulative table (F | f << 16) searched with a
 //               fixed-trip binary search -- any b, alphabets up to the LDS size.
 #include <hip/hip_runtime.h>
@@ -277,6 +279,10 @@ __device__ __forceinline__ int32_t doubled_value(int32_t z, int field, uint32_t 
 
 // Packed slot table: lut[t * M + u] for the 16 field tables (b <= 11).  Wave
 // w fills tables w, w + kWavesPerGroup, ...; each lane a run of M/64 slots.
+// The byte z of an entry is the field value for fields 1-7 and twice the
+// value m for field 8, so that every coordinate is 2z + c before field 8's
+// parity bit (2 pi) is added; the host admits a tensor to this path only when
+// every doubled coordinate lies in [-256, 255], i.e. z fits a signed byte.
 __device__ __forceinline__ void build_lut_table(const LayerDev& L, uint32_t* lut,
                                                 const uint32_t* cum, int t, int j) {
   const uint32_t M = 1u << L.b;
@@ -296,13 +302,13 @@ __device__ __forceinline__ void build_lut_table(const LayerDev& L, uint32_t* lut
     n -= h;
   }
   const int field = (t & 7) + 1;
-  const uint32_t c = (uint32_t)t >> 3;
   uint32_t e = cum[base + s];
   for (uint32_t u = u0; u < u0 + per; u++) {
     while (s + 1 < A && (e & 0xFFFF) + (e >> 16) <= u) e = cum[base + ++s];
     uint32_t F = e & 0xFFFF, f = e >> 16;
-    int32_t val = doubled_value((int32_t)s + L.tab_min[t], field, c);
-    row[u] = f | ((u - F) << 12) | (((uint32_t)val & 0x1FFu) << 23);
+    const int32_t v = (int32_t)s + L.tab_min[t];
+    const int32_t z = field < 8 ? v : 2 * v;
+    row[u] = f | ((u - F) << 12) | ((uint32_t)(z & 0xFF) << 24);
   }
 }
 
@@ -439,7 +445,7 @@ __device__ __forceinline__ void decode_field(const Hot& L, const uint32_t* lds, 
     const uint32_t u = x & (M - 1);
     const uint32_t e = lds[cb + u + (uint32_t)(field - 1) * M];
     x = __umul24(e & 0xFFFu, x >> B) + ((e >> 12) & 0x7FFu);
-    dval = (int32_t)e >> 23;
+    dval = 2 * ((int32_t)e >> 24) + (int32_t)c;
   } else {
     // Bucketed search: the bucket j of u (its top k bits) bounds the symbol to
     // [bk[j], bk[j + 1]]; a binary search on the u16 cumulative table narrows
@@ -580,7 +586,7 @@ __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, u
   if (err && status) atomicOr(status, (int32_t)err);
 }
 
-// ---- hand-scheduled steady state: slot-table path, full tasks, two chains --------
+// ---- steady state of the bucketed-search path: full four-tile tasks, two chains ---
 // Payload staging.  Each half (one tile's stream) owns a 512-byte ring in LDS
 // (256 words) that is addressed modulo its size, so a step's reads need no
 // second copy of the ring.  Words arrive in 128-word blocks, one dwordx2 per
@@ -637,138 +643,6 @@ __device__ __forceinline__ void fast_stage(FastChain& F, u32x2& pendA, u32x2& pe
     F.QA = uni(F.QA + (cA ? kFastBlockWords : 0u));
     F.QB = uni(F.QB + (cB ? kFastBlockWords : 0u));
   }
-}
-
-// One symbol step of both chains.  Chain 0's refill ballot lives in VCC,
-// chain 1's in s[94:95] (clobbered), so the two refills can be interleaved
-// instruction by instruction.  Per chain: 64-lane ballot of states below
-// 2^15, per-half word index from v_mbcnt (upper-half lanes corrected by the
-// distance between the two read positions less the lower half's count, dd =
-// D - popcount(lower half), where the chain keeps D = SB - SA in place of
-// SB), the ring read at byte vrb | (2 (SA + index) mod 512), the scalar
-// advance SA += popcount(lower), D = dd + popcount(upper), and the merge
-// x = x << 16 | w on the
-// refilling lanes only (EXEC narrowed to each chain's ballot, then restored).
-// The wave's issue priority drops back to 0 once both ring reads are in
-// flight (a field step raises it while its table entries are in hand).
-#define EP_REFILL_BOTH                                                      \
-  "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
-  "v_cmp_gt_u32_e64 s[94:95], %[k15], %[x1]\n\t"                            \
-  "s_bcnt1_i32_b32 %[c0lo], vcc_lo\n\t"                                    \
-  "v_mbcnt_lo_u32_b32 %[t0], vcc_lo, 0\n\t"                                 \
-  "s_bcnt1_i32_b32 %[c0hi], vcc_hi\n\t"                                    \
-  "v_mbcnt_lo_u32_b32 %[t1], s94, 0\n\t"                                    \
-  "v_mbcnt_hi_u32_b32 %[t0], vcc_hi, %[t0]\n\t"                             \
-  "s_sub_u32 %[d0], %[D0], %[c0lo]\n\t"                                    \
-  "v_mbcnt_hi_u32_b32 %[t1], s95, %[t1]\n\t"                                \
-  "s_bcnt1_i32_b32 %[c1lo], s94\n\t"                                       \
-  "v_mad_i32_i24 %[t0], %[vH], %[d0], %[t0]\n\t"                            \
-  "s_bcnt1_i32_b32 %[c1hi], s95\n\t"                                       \
-  "v_add_lshl_u32 %[t0], %[t0], %[SA0], 1\n\t"                              \
-  "v_and_or_b32 %[t0], %[t0], %[rmask], %[vrb0]\n\t"                        \
-  "s_sub_u32 %[d1], %[D1], %[c1lo]\n\t"                                    \
-  "ds_read_u16 %[w0], %[t0]\n\t"                                            \
-  "v_mad_i32_i24 %[t1], %[vH], %[d1], %[t1]\n\t"                            \
-  "s_add_u32 %[SA0], %[SA0], %[c0lo]\n\t"                                  \
-  "v_add_lshl_u32 %[t1], %[t1], %[SA1], 1\n\t"                              \
-  "s_add_u32 %[D0], %[d0], %[c0hi]\n\t"                                  \
-  "v_and_or_b32 %[t1], %[t1], %[rmask], %[vrb1]\n\t"                        \
-  "s_add_u32 %[SA1], %[SA1], %[c1lo]\n\t"                                  \
-  "ds_read_u16 %[w1], %[t1]\n\t"                                            \
-  "s_setprio 0\n\t"                                                        \
-  "s_add_u32 %[D1], %[d1], %[c1hi]\n\t"                                  \
-  "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
-  "s_waitcnt lgkmcnt(1)\n\t"                                                \
-  "v_lshl_or_b32 %[x0], %[x0], 16, %[w0]\n\t"                               \
-  "s_and_b64 exec, %[ex], s[94:95]\n\t"                                     \
-  "s_waitcnt lgkmcnt(0)\n\t"                                                \
-  "v_lshl_or_b32 %[x1], %[x1], 16, %[w1]\n\t"                               \
-  "s_mov_b64 exec, %[ex]\n\t"
-
-#define EP_STEP_OUTS                                                                      \
-  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [D0] "+s"(F0.D), [SA1] "+s"(F1.OA),  \
-      [D1] "+s"(F1.D), [u0] "=&v"(u0), [u1] "=&v"(u1), [e0] "=&v"(e0), [e1] "=&v"(e1),  \
-      [g0] "=&v"(g0), [g1] "=&v"(g1), [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0),     \
-      [w1] "=&v"(w1), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo),          \
-      [c1hi] "=&s"(c1hi), [d0] "=&s"(dd0), [d1] "=&s"(dd1), [ex] "=&s"(ex)
-
-#define EP_STEP_INS                                                                          \
-  [vH] "v"(vH), [vrb0] "v"(vrb0), [vrb1] "v"(vrb1), [rmask] "s"(kFastRingBytes - 1),         \
-      [k15] "s"(kStateLow)
-
-#define EP_STEP_CLOBBERS "vcc", "scc", "exec", "s94", "s95", "memory"
-
-// Field symbol (table 8c + FIELD - 1) for both chains, then refill.  Chain
-// 0's decode starts as soon as its own table read returns.  From then until
-// the ring reads are issued the wave runs at raised issue priority: the
-// dependent ALU chain of a wave whose table reads have landed goes ahead of
-// waves that are still waiting, which shortens every wave's step latency.
-template <int B, int FIELD>
-__device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
-                                            int32_t& d0, int32_t& d1, FastChain& F0, FastChain& F1,
-                                            uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
-  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;
-  uint64_t ex;
-  asm volatile(
-      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
-      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
-      "v_lshl_add_u32 %[u0], %[u0], 2, %[cb0]\n\t"
-      "v_lshl_add_u32 %[u1], %[u1], 2, %[cb1]\n\t"
-      "ds_read_b32 %[e0], %[u0] offset:%[off]\n\t"
-      "ds_read_b32 %[e1], %[u1] offset:%[off]\n\t"
-      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
-      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
-      "s_waitcnt lgkmcnt(1)\n\t"
-      "s_setprio 2\n\t"
-      "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
-      "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
-      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
-      "v_ashrrev_i32 %[dv0], 23, %[e0]\n\t"
-      "s_waitcnt lgkmcnt(0)\n\t"
-      "v_and_b32 %[u1], 0xfff, %[e1]\n\t"
-      "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"
-      "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"
-      "v_ashrrev_i32 %[dv1], 23, %[e1]\n\t"
-      EP_REFILL_BOTH
-      : EP_STEP_OUTS, [dv0] "=&v"(d0), [dv1] "=&v"(d1)
-      : [cb0] "v"(cb0), [cb1] "v"(cb1), [mk] "i"((1 << B) - 1), [b] "i"(B),
-        [off] "i"((FIELD - 1) * (4 << B)), EP_STEP_INS
-      : EP_STEP_CLOBBERS);
-}
-
-// Coset symbol (two-entry table f0, f1) for both chains, then refill.  Returns
-// c and the per-lane LDS byte base of its slot tables, cb = 4 * 8c * 2^B.
-template <int B>
-__device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t& c0, uint32_t& c1,
-                                            uint32_t& cb0, uint32_t& cb1, uint32_t vf0, uint32_t vf1,
-                                            FastChain& F0, FastChain& F1, uint32_t vH,
-                                            uint32_t vrb0, uint32_t vrb1) {
-  uint32_t u0, u1, e0, e1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;
-  uint64_t ex;
-  asm volatile(
-      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
-      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
-      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
-      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
-      "v_cmp_le_u32_e32 vcc, %[vf0], %[u0]\n\t"
-      "v_cndmask_b32_e32 %[e0], %[vf0], %[vf1], vcc\n\t"
-      "v_cndmask_b32_e32 %[t0], 0, %[vf0], vcc\n\t"
-      "v_cndmask_b32_e64 %[c0], 0, 1, vcc\n\t"
-      "v_mad_u32_u24 %[x0], %[e0], %[g0], %[u0]\n\t"
-      "v_sub_u32_e32 %[x0], %[x0], %[t0]\n\t"
-      "v_cmp_le_u32_e32 vcc, %[vf0], %[u1]\n\t"
-      "v_cndmask_b32_e32 %[e1], %[vf0], %[vf1], vcc\n\t"
-      "v_cndmask_b32_e32 %[t1], 0, %[vf0], vcc\n\t"
-      "v_cndmask_b32_e64 %[c1], 0, 1, vcc\n\t"
-      "v_mad_u32_u24 %[x1], %[e1], %[g1], %[u1]\n\t"
-      "v_sub_u32_e32 %[x1], %[x1], %[t1]\n\t"
-      "v_lshlrev_b32 %[cb0], %[b5], %[c0]\n\t"
-      "v_lshlrev_b32 %[cb1], %[b5], %[c1]\n\t"
-      EP_REFILL_BOTH
-      : EP_STEP_OUTS, [c0] "=&v"(c0), [c1] "=&v"(c1), [cb0] "=&v"(cb0), [cb1] "=&v"(cb1)
-      : [vf0] "v"(vf0), [vf1] "v"(vf1), [mk] "i"((1 << B) - 1), [b] "i"(B), [b5] "i"(B + 5),
-        EP_STEP_INS
-      : EP_STEP_CLOBBERS);
 }
 
 // The same refill in plain code, for the search path's steady state.
@@ -861,9 +735,8 @@ __device__ __forceinline__ u32x4 fast_start(FastChain& F, u32x2& pend, __amdgpu_
   return first;
 }
 
-// The steady-state task: four full tiles (two chains), output type DT.  The
-// slot-table path runs the hand-scheduled steps, the search path plain ones;
-// staging, reconstruction and stores are shared.
+// The steady-state task of the search path: four full tiles (two chains),
+// output type DT.
 template <int PATH, int B, int DT, bool SAT>
 __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                                  uint32_t task, int32_t* status) {
@@ -911,7 +784,6 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
   pendB1 = pend1;
 
   const uint32_t vH = half;
-  const uint32_t vf0 = L.coset_f0, vf1 = L.coset_f1;
   const uint32_t rounds = L.V / 32;
   const bool wide = L.cvec >= 32;
   const uint32_t vrb08 = vrb0 + vl8, vrb18 = vrb1 + vl8;
@@ -924,17 +796,10 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 #pragma unroll
     for (int j = 0; j < 2; j++)
       sg[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row[j], 0, 0));
-    uint32_t c[2], cb[2];
+    uint32_t c[2];
     int32_t d[2][9];
-    if constexpr (PATH == kPathLut)
-      coset_step2<B>(x[0], x[1], c[0], c[1], cb[0], cb[1], vf0, vf1, F0, F1, vH, vrb0, vrb1);
-    else
-      coset_step_search(L, x, c, F0, F1, lds, vrb0, vrb1, vH);
-#define EP_FIELD(I)                                                                              \
-  if constexpr (PATH == kPathLut)                                                                \
-    field_step2<B, I>(x[0], x[1], cb[0], cb[1], d[0][I], d[1][I], F0, F1, vH, vrb0, vrb1);      \
-  else                                                                                           \
-    field_step_search<I>(L, tab, x, c, d, F0, F1, lds, vrb0, vrb1, vH);
+    coset_step_search(L, x, c, F0, F1, lds, vrb0, vrb1, vH);
+#define EP_FIELD(I) field_step_search<I>(L, tab, x, c, d, F0, F1, lds, vrb0, vrb1, vH);
     EP_FIELD(1) EP_FIELD(2)
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
@@ -982,8 +847,374 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
   if (err && status) atomicOr(status, (int32_t)err);
 }
 
-// Output-type dispatch of a full slot-table task.  Returns false for the
-// combinations the steady state does not cover (they take the generic loop).
+// ---- hand-scheduled steady state of the slot-table path: full tasks, two chains -------
+// Same staging as the search path's steady state (512-byte rings, 128-word
+// blocks, commits at a round's start and after steps 3 and 6).  One symbol
+// step of both chains: chain 0's refill ballot lives in VCC, chain 1's in
+// s[94:95] (clobbered), so the two refills interleave instruction by
+// instruction.  Per chain: 64-lane ballot of states below 2^15, per-half word
+// index from v_mbcnt (upper-half lanes corrected by the distance between the
+// two read positions less the lower half's count, dd = D - popcount(lower
+// half), where the chain keeps D = SB - SA in place of SB), the ring read at
+// byte vrb | (2 (SA + index) mod 512), the scalar advance SA += popcount(lower),
+// D = dd + popcount(upper), and the merge x = x << 16 | w on the refilling
+// lanes only (EXEC narrowed to each chain's ballot, then restored).  The wave's
+// issue priority drops back to 0 once both ring reads are in flight (a field
+// step raises it while its table entries are in hand).
+#define EP_REFILL_BOTH                                                      \
+  "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
+  "v_cmp_gt_u32_e64 s[94:95], %[k15], %[x1]\n\t"                            \
+  "s_bcnt1_i32_b32 %[c0lo], vcc_lo\n\t"                                    \
+  "v_mbcnt_lo_u32_b32 %[t0], vcc_lo, 0\n\t"                                 \
+  "s_bcnt1_i32_b32 %[c0hi], vcc_hi\n\t"                                    \
+  "v_mbcnt_lo_u32_b32 %[t1], s94, 0\n\t"                                    \
+  "v_mbcnt_hi_u32_b32 %[t0], vcc_hi, %[t0]\n\t"                             \
+  "s_sub_u32 %[d0], %[D0], %[c0lo]\n\t"                                    \
+  "v_mbcnt_hi_u32_b32 %[t1], s95, %[t1]\n\t"                                \
+  "s_bcnt1_i32_b32 %[c1lo], s94\n\t"                                       \
+  "v_mad_i32_i24 %[t0], %[vH], %[d0], %[t0]\n\t"                            \
+  "s_bcnt1_i32_b32 %[c1hi], s95\n\t"                                       \
+  "v_add_lshl_u32 %[t0], %[t0], %[SA0], 1\n\t"                              \
+  "v_and_or_b32 %[t0], %[t0], %[rmask], %[vrb0]\n\t"                        \
+  "s_sub_u32 %[d1], %[D1], %[c1lo]\n\t"                                    \
+  "ds_read_u16 %[w0], %[t0]\n\t"                                            \
+  "v_mad_i32_i24 %[t1], %[vH], %[d1], %[t1]\n\t"                            \
+  "s_add_u32 %[SA0], %[SA0], %[c0lo]\n\t"                                  \
+  "v_add_lshl_u32 %[t1], %[t1], %[SA1], 1\n\t"                              \
+  "s_add_u32 %[D0], %[d0], %[c0hi]\n\t"                                  \
+  "v_and_or_b32 %[t1], %[t1], %[rmask], %[vrb1]\n\t"                        \
+  "s_add_u32 %[SA1], %[SA1], %[c1lo]\n\t"                                  \
+  "ds_read_u16 %[w1], %[t1]\n\t"                                            \
+  "s_setprio 0\n\t"                                                        \
+  "s_add_u32 %[D1], %[d1], %[c1hi]\n\t"                                  \
+  "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
+  "s_waitcnt lgkmcnt(1)\n\t"                                                \
+  "v_lshl_or_b32 %[x0], %[x0], 16, %[w0]\n\t"                               \
+  "s_and_b64 exec, %[ex], s[94:95]\n\t"                                     \
+  "s_waitcnt lgkmcnt(0)\n\t"                                                \
+  "v_lshl_or_b32 %[x1], %[x1], 16, %[w1]\n\t"                               \
+  "s_mov_b64 exec, %[ex]\n\t"
+
+#define EP_STEP_OUTS                                                                      \
+  [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [D0] "+s"(F0.D), [SA1] "+s"(F1.OA),  \
+      [D1] "+s"(F1.D), [u0] "=&v"(u0), [u1] "=&v"(u1), [g0] "=&v"(g0), [g1] "=&v"(g1),  \
+      [t0] "=&v"(t0), [t1] "=&v"(t1), [w0] "=&v"(w0), [w1] "=&v"(w1),                     \
+      [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi), [c1lo] "=&s"(c1lo), [c1hi] "=&s"(c1hi),     \
+      [d0] "=&s"(dd0), [d1] "=&s"(dd1), [ex] "=&s"(ex)
+
+#define EP_STEP_TEMPS                                                                     \
+  uint32_t u0, u1, g0, g1, t0, t1, w0, w1, c0lo, c0hi, c1lo, c1hi, dd0, dd1;             \
+  uint64_t ex
+
+#define EP_STEP_INS                                                                          \
+  [vH] "v"(vH), [vrb0] "v"(vrb0), [vrb1] "v"(vrb1), [rmask] "s"(kFastRingBytes - 1),         \
+      [k15] "s"(kStateLow), [mk] "i"((1 << B) - 1), [b] "i"(B)
+
+#define EP_STEP_CLOBBERS "vcc", "scc", "exec", "s94", "s95", "memory"
+
+// Field symbol (table 8c + FIELD - 1, entry at byte cb + 4u + (FIELD - 1) 4 * 2^B)
+// for both chains, then the refill; e0, e1 receive the slot entries, kept for the
+// reconstruction.  Chain 0's decode starts as soon as its own table read
+// returns.  From then until the ring reads are issued the wave runs at raised
+// issue priority: the dependent ALU chain of a wave whose table reads have
+// landed goes ahead of waves that are still waiting, which shortens every
+// wave's step latency.
+template <int B, int FIELD>
+__device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
+                                            uint32_t& e0, uint32_t& e1, FastChain& F0, FastChain& F1,
+                                            uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
+  EP_STEP_TEMPS;
+  asm volatile(
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
+      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
+      "v_lshl_add_u32 %[u0], %[u0], 2, %[cb0]\n\t"
+      "v_lshl_add_u32 %[u1], %[u1], 2, %[cb1]\n\t"
+      "ds_read_b32 %[e0], %[u0] offset:%[off]\n\t"
+      "ds_read_b32 %[e1], %[u1] offset:%[off]\n\t"
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
+      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
+      "s_waitcnt lgkmcnt(1)\n\t"
+      "s_setprio 2\n\t"
+      "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
+      "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
+      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "v_and_b32 %[u1], 0xfff, %[e1]\n\t"
+      "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"
+      "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"
+      EP_REFILL_BOTH
+      : EP_STEP_OUTS, [e0] "=&v"(e0), [e1] "=&v"(e1)
+      : [cb0] "v"(cb0), [cb1] "v"(cb1), [off] "i"((FIELD - 1) * (4 << B)), EP_STEP_INS
+      : EP_STEP_CLOBBERS);
+}
+
+// Coset symbol (two-entry table f0, f1) for both chains, then the refill.
+// Returns cb = 4 * 8c * 2^B (the byte offset of the lane's coset tables) and
+// hc = c * sg / 2 (half the row scale when the point lies in the half-integer
+// coset, else 0).
+template <int B>
+__device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t& cb0, uint32_t& cb1,
+                                            float& hc0, float& hc1, float sg0, float sg1,
+                                            uint32_t vf0, uint32_t vf1, uint32_t vcb, FastChain& F0,
+                                            FastChain& F1, uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
+  EP_STEP_TEMPS;
+  asm volatile(
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
+      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
+      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
+      "v_cmp_le_u32_e32 vcc, %[vf0], %[u0]\n\t"
+      "v_cndmask_b32_e32 %[w0], %[vf0], %[vf1], vcc\n\t"
+      "v_cndmask_b32_e32 %[t0], 0, %[vf0], vcc\n\t"
+      "v_cndmask_b32_e32 %[cb0], 0, %[vcb], vcc\n\t"
+      "v_mad_u32_u24 %[x0], %[w0], %[g0], %[u0]\n\t"
+      "v_mul_f32_e32 %[w0], 0.5, %[sg0]\n\t"
+      "v_cndmask_b32_e32 %[hc0], 0, %[w0], vcc\n\t"
+      "v_sub_u32_e32 %[x0], %[x0], %[t0]\n\t"
+      "v_cmp_le_u32_e32 vcc, %[vf0], %[u1]\n\t"
+      "v_cndmask_b32_e32 %[w1], %[vf0], %[vf1], vcc\n\t"
+      "v_cndmask_b32_e32 %[t1], 0, %[vf0], vcc\n\t"
+      "v_cndmask_b32_e32 %[cb1], 0, %[vcb], vcc\n\t"
+      "v_mad_u32_u24 %[x1], %[w1], %[g1], %[u1]\n\t"
+      "v_mul_f32_e32 %[w1], 0.5, %[sg1]\n\t"
+      "v_cndmask_b32_e32 %[hc1], 0, %[w1], vcc\n\t"
+      "v_sub_u32_e32 %[x1], %[x1], %[t1]\n\t"
+      EP_REFILL_BOTH
+      : EP_STEP_OUTS, [cb0] "=&v"(cb0), [cb1] "=&v"(cb1), [hc0] "=&v"(hc0), [hc1] "=&v"(hc1)
+      : [vf0] "v"(vf0), [vf1] "v"(vf1), [vcb] "v"(vcb), [sg0] "v"(sg0), [sg1] "v"(sg1), EP_STEP_INS
+      : EP_STEP_CLOBBERS);
+}
+
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Reconstruction of one vector as its slot entries arrive (eq. point_inverse,
+// eq. recon).  Bit 24 of an entry is the low bit of its z, so bit 24 of
+// e1 ^ ... ^ e7 is pi = (z_1 + ... + z_7) mod 2, and field 8's z becomes z + pi
+// (z is even there).  Each weight is fp32(sigma * (z + c/2)), formed as the
+// single rounding fma(sigma, z, c * sigma / 2) -- equal to the product of the
+// FP32 row scale with the coordinate -- and snapped to the output type.  The
+// entry of an odd field waits in `ep` for its even partner; the pair is then
+// converted and packed into the output words w.
+struct QAcc {
+  uint32_t X;     // xor of the entries of fields 1..7 so far
+  uint32_t ep;    // entry of the pending odd field
+  uint32_t w[8];  // packed output words (the output type uses 2, 4 or 8 of them)
+};
+
+template <int DT, bool SAT>
+__device__ __forceinline__ float q_weight(uint32_t e, float sg, float hc) {
+  float y = __builtin_fmaf(sg, (float)((int32_t)e >> 24), hc);
+  if constexpr (SAT) {
+    constexpr float m = DT == EP_FP8_E4M3 ? 448.0f : DT == EP_FP16 ? 65504.0f : 3.38953139e38f;
+    y = sat(y, m);
+  }
+  return y;
+}
+
+__device__ __forceinline__ uint32_t int8_pair(float a, float b) {
+  int ia = min((int)__builtin_rintf(sat(a, 128.0f)), 127), ib = min((int)__builtin_rintf(sat(b, 128.0f)), 127);
+  return (uint32_t)(ia & 0xFF) | ((uint32_t)(ib & 0xFF) << 8);
+}
+
+template <int DT, bool SAT, int FIELD>
+__device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float sg, float hc, uint32_t c) {
+  if constexpr (FIELD % 2 == 1) {
+    if constexpr (FIELD == 7) a.X ^= e;
+    a.ep = e;
+    return;
+  } else {
+    if constexpr (FIELD == 2) a.X = a.ep ^ e;
+    else if constexpr (FIELD < 8) a.X = xor3(a.X, a.ep, e);
+    else e |= a.X & (1u << 24);
+    constexpr int p = FIELD / 2 - 1;   // pair index 0..3
+    if constexpr (DT == EP_COORD2_I32) {
+      a.w[2 * p] = (uint32_t)(2 * ((int32_t)a.ep >> 24) + (int32_t)c);
+      a.w[2 * p + 1] = (uint32_t)(2 * ((int32_t)e >> 24) + (int32_t)c);
+      return;
+    }
+    const float y0 = q_weight<DT, SAT>(a.ep, sg, hc), y1 = q_weight<DT, SAT>(e, sg, hc);
+    if constexpr (DT == EP_BF16) {
+      a.w[p] = bf16_pair(y0, y1);
+    } else if constexpr (DT == EP_FP16) {
+      a.w[p] = fp16_pair(y0, y1);
+    } else if constexpr (DT == EP_FP32) {
+      a.w[2 * p] = __float_as_uint(y0);
+      a.w[2 * p + 1] = __float_as_uint(y1);
+    } else if constexpr (DT == EP_FP8_E4M3) {
+      // the low half is written first; its high half is overwritten by the next pair
+      a.w[p / 2] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(
+          y0, y1, (int)(p & 1 ? a.w[p / 2] : __float_as_uint(y0)), (p & 1) != 0);
+    } else {  // EP_INT8
+      const uint32_t h = int8_pair(y0, y1);
+      a.w[p / 2] = p & 1 ? (a.w[p / 2] | (h << 16)) : h;
+    }
+  }
+}
+
+// Store the packed vector at base + off.
+template <int DT>
+__device__ __forceinline__ void q_put(EP_GLOBAL uint8_t* base, uint32_t off, const QAcc& a) {
+  if constexpr (DT == EP_BF16 || DT == EP_FP16) {
+    *reinterpret_cast<EP_GLOBAL u32x4*>(base + off) = u32x4{a.w[0], a.w[1], a.w[2], a.w[3]};
+  } else if constexpr (DT == EP_FP8_E4M3 || DT == EP_INT8) {
+    *reinterpret_cast<EP_GLOBAL u32x2*>(base + off) = u32x2{a.w[0], a.w[1]};
+  } else {
+    EP_GLOBAL u32x4* o = reinterpret_cast<EP_GLOBAL u32x4*>(base + off);
+    o[0] = u32x4{a.w[0], a.w[1], a.w[2], a.w[3]};
+    o[1] = u32x4{a.w[4], a.w[5], a.w[6], a.w[7]};
+  }
+}
+
+// Bytes of one 8-weight vector in output type DT.
+template <int DT>
+constexpr uint32_t vec_bytes() {
+  return DT == EP_FP8_E4M3 || DT == EP_INT8 ? 8u : (DT == EP_BF16 || DT == EP_FP16) ? 16u : 32u;
+}
+
+// The steady-state task of the slot-table path: four full tiles t0 .. t0 + 3
+// (two chains).  TWO: every lane's vectors v, v + 32, ... of a tile lie in at
+// most two rows (C/8 >= V - 32), so each lane holds both row scales and
+// switches at round kc; otherwise the row scale is loaded every round.
+template <int B, int DT, bool SAT, bool TWO>
+__device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ring_area, uint32_t t0,
+                                         int32_t* status) {
+  const uint32_t lane = threadIdx.x & 63, wave = wave_id();
+  const uint32_t half = lane >> 5, l = lane & 31;
+  const EP_GLOBAL uint32_t* states = gptr<const uint32_t>(L.blob + L.off_states);
+  const EP_GLOBAL uint32_t* offs = gptr<const uint32_t>(L.blob + L.off_offsets);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_payload), (short)0, (int)L.pay_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_sigma), (short)0, (int)(4 * L.rows), 0x00020000);
+  constexpr uint32_t VB = vec_bytes<DT>();
+
+  const uint32_t vrb0 = ring_area + wave * 2 * kFastChainBytes + half * kFastRingBytes;
+  const uint32_t vrb1 = vrb0 + kFastChainBytes;
+  const uint32_t vl8 = 8 * l;
+  uint32_t o[5];
+#pragma unroll
+  for (int i = 0; i < 5; i++) o[i] = offs[t0 + i];
+  uint32_t x[2], vb[2], voff[2], kc[2];
+  float sa[2], sb[2];
+#pragma unroll
+  for (int j = 0; j < 2; j++) {
+    const uint32_t tile = t0 + 2 * j + half;
+    x[j] = states[(uint64_t)tile * 32 + l];
+    vb[j] = tile * L.V + l;
+    voff[j] = ((2 * j + half) * L.V + l) * VB;
+    if constexpr (TWO) {
+      const uint32_t r = row_of(L, vb[j]);
+      kc[j] = ((r + 1) * L.cvec - vb[j] + 31) >> 5;
+      sa[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r, 0, 0));
+      sb[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r + 4, 0, 0));
+    }
+  }
+  FastChain F0, F1;
+  u32x2 pend0, pend1, pendB0, pendB1;
+#pragma unroll
+  for (int i = 0; i < 5; i++) o[i] = uni(o[i]);
+  const u32x4 fill0 = fast_start(F0, pend0, rsrc, half, l, o[0], o[1], o[1], o[2]);
+  const u32x4 fill1 = fast_start(F1, pend1, rsrc, half, l, o[2], o[3], o[3], o[4]);
+  // One wait for everything requested so far, so that no load is in flight
+  // when the loop starts (the loop's own waits then stay one round behind).
+  __builtin_amdgcn_s_waitcnt(0);
+  *reinterpret_cast<u32x4*>(lds + vrb0 + 16 * l) = fill0;
+  *reinterpret_cast<u32x4*>(lds + vrb1 + 16 * l) = fill1;
+  pendB0 = pend0;   // pend* serve lanes 0-31, pendB* lanes 32-63
+  pendB1 = pend1;
+
+  EP_GLOBAL uint8_t* obase = gptr<uint8_t>(L.out) + (uint64_t)t0 * L.V * VB;
+  const uint32_t vH = half;
+  const uint32_t vf0 = L.coset_f0, vf1 = L.coset_f1, vcb = 32u << B;
+  const uint32_t rounds = L.V / 32;
+  const uint32_t vrb08 = vrb0 + vl8, vrb18 = vrb1 + vl8;
+
+  for (uint32_t k = 0; k < rounds; k++) {
+    // room for a block: margin <= ring - block
+    fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half,
+                    kFastRingWords - kFastBlockWords + 1);
+    float sg[2], hc[2];
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      if constexpr (TWO) sg[j] = k < kc[j] ? sa[j] : sb[j];
+      else sg[j] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row_of(L, vb[j] + 32 * k), 0, 0));
+    }
+    uint32_t cb[2], e0, e1;
+    QAcc acc[2];
+    coset_step2<B>(x[0], x[1], cb[0], cb[1], hc[0], hc[1], sg[0], sg[1], vf0, vf1, vcb, F0, F1, vH,
+                   vrb0, vrb1);
+#define EP_FIELD(I)                                                                           \
+  field_step2<B, I>(x[0], x[1], cb[0], cb[1], e0, e1, F0, F1, vH, vrb0, vrb1);               \
+  q_take<DT, SAT, I>(acc[0], e0, sg[0], hc[0], cb[0] >> (B + 5));                             \
+  q_take<DT, SAT, I>(acc[1], e1, sg[1], hc[1], cb[1] >> (B + 5));
+    EP_FIELD(1) EP_FIELD(2)
+    fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
+    EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
+    fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
+    EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
+#undef EP_FIELD
+    q_put<DT>(obase, voff[0], acc[0]);
+    q_put<DT>(obase, voff[1], acc[1]);
+    obase += 32 * VB;
+  }
+
+  uint32_t err = 0;
+#pragma unroll
+  for (int j = 0; j < 2; j++) {
+    if (x[j] != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
+    const FastChain& F = j ? F1 : F0;
+    const uint32_t P = half ? F.OA + F.D : F.OA, E = half ? F.EB : F.EA;
+    if (l == 0 && P != E) err |= P > E ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
+    if (L.container && L.dequant) {
+      const EP_GLOBAL float* delta = gptr<const float>(L.blob + L.off_delta);
+      const uint32_t v0 = (t0 + 2 * j + half) * L.V;
+      const uint32_t r_first = (v0 + L.cvec - 1) / L.cvec;
+      const uint32_t r_last = (v0 + L.V - 1) / L.cvec;
+      for (uint32_t r = r_first + l; r <= r_last; r += 32) gptr<float>(L.dequant)[r] = delta[r];
+    }
+  }
+  if (err && status) atomicOr(status, (int32_t)err);
+}
+
+template <int B, int DT, bool SAT>
+__device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32_t ring_area,
+                                              uint32_t t0, int32_t* status) {
+  if (L.cvec + 32 >= L.V) lut_task<B, DT, SAT, true>(L, lds, ring_area, t0, status);
+  else lut_task<B, DT, SAT, false>(L, lds, ring_area, t0, status);
+}
+
+// Output-type dispatch of a full four-tile slot-table task.  Returns false for
+// the combinations the steady state does not cover (they take the generic loop).
+template <int B>
+__device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
+                                             uint32_t t0, int32_t* status) {
+  switch (L.out_dtype) {
+    case EP_BF16:
+      if (L.saturate) lut_task_rows<B, EP_BF16, true>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_BF16, false>(L, lds, ring_area, t0, status);
+      return true;
+    case EP_FP16:
+      if (L.saturate) lut_task_rows<B, EP_FP16, true>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_FP16, false>(L, lds, ring_area, t0, status);
+      return true;
+    case EP_FP8_E4M3:
+      if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_FP8_E4M3, false>(L, lds, ring_area, t0, status);
+      return true;
+    case EP_INT8: lut_task_rows<B, EP_INT8, false>(L, lds, ring_area, t0, status); return true;
+    case EP_FP32: lut_task_rows<B, EP_FP32, false>(L, lds, ring_area, t0, status); return true;
+    case EP_COORD2_I32: lut_task_rows<B, EP_COORD2_I32, false>(L, lds, ring_area, t0, status); return true;
+    default: return false;
+  }
+}
+
+// Output-type dispatch of a full search-path task (four tiles, two chains).  Returns
+// false for the combinations the steady state does not cover (they take the generic loop).
 template <int PATH, int B>
 __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                                      uint32_t task, int32_t* status) {
@@ -1060,23 +1291,43 @@ __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
   }
 }
 
-// Tiles per wave task and the specialisation of a task: all of its tiles full
-// (V vectors, V a multiple of 32) or not.
-constexpr int kChains = 2;
-constexpr uint32_t kTilesPerTask = 2 * kChains;
-static_assert(kChains == 2, "the hand-scheduled steady state advances two chains per wave");
+// A wave task is eight tiles.  When all eight are full (V vectors each, V a
+// multiple of 32) both paths decode them in two four-tile steady-state passes
+// (two chains each); otherwise the generic loop takes the task as two
+// four-tile halves.
+constexpr int kChains = 2;                 // chains of the generic loop
+constexpr uint32_t kTilesPerTask = 8;
+static_assert(kChains == 2, "the generic loop and the search steady state advance two chains");
+static_assert(kTilesPerTask == 4 * kChains, "task granularity: two four-tile passes");
 
 template <int PATH, int B>
 __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                        uint32_t ring_area, uint32_t task, int32_t* status) {
   const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
   const uint32_t nvec = L.rows * L.cvec;
-  const bool full = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
-                    (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
-  if (full && L.pay_bytes < kFastOob && decode_task_fast_any<PATH, B>(L, lb, ring_area, task, status))
-    return;
-  if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, task, status);
-  else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, task, status);
+  const bool full8 = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
+                     (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
+  if (full8 && L.pay_bytes < kFastOob) {
+    if constexpr (PATH == kPathLut) {
+      if (lut_task_any<B>(L, lb, ring_area, t0, status)) {
+        lut_task_any<B>(L, lb, ring_area, t0 + 4, status);
+        return;
+      }
+    } else {
+      if (decode_task_fast_any<PATH, B>(L, lb, ring_area, 2 * task, status)) {
+        decode_task_fast_any<PATH, B>(L, lb, ring_area, 2 * task + 1, status);
+        return;
+      }
+    }
+  }
+  // generic loop: halves of four tiles (decode_task's task unit)
+  for (uint32_t h = 0; h < 2; h++) {
+    const uint32_t s0 = t0 + 4 * h;
+    if (s0 >= L.tile_end) break;
+    const bool full = (L.V % 32 == 0) && s0 + 4 <= L.tile_end && (uint64_t)(s0 + 4) * L.V <= nvec;
+    if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, 2 * task + h, status);
+    else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, 2 * task + h, status);
+  }
 }
 
 template <int PATH>
