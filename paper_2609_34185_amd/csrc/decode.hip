@@ -860,8 +860,9 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 // D = dd + popcount(upper), and the merge x = x << 16 | w on the refilling
 // lanes only (EXEC narrowed to each chain's ballot, then restored).  The wave's
 // issue priority drops back to 0 once both ring reads are in flight (a field
-// step raises it while its table entries are in hand).
-#define EP_REFILL_BOTH                                                      \
+// step raises it while its table entries are in hand).  WORK is independent
+// vector work placed in the wait for the ring words.
+#define EP_REFILL_BOTH_W(WORK)                                              \
   "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
   "v_cmp_gt_u32_e64 s[94:95], %[k15], %[x1]\n\t"                            \
   "s_bcnt1_i32_b32 %[c0lo], vcc_lo\n\t"                                    \
@@ -887,6 +888,7 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
   "ds_read_u16 %[w1], %[t1]\n\t"                                            \
   "s_setprio 0\n\t"                                                        \
   "s_add_u32 %[D1], %[d1], %[c1hi]\n\t"                                  \
+  WORK                                                                     \
   "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
   "s_waitcnt lgkmcnt(1)\n\t"                                                \
   "v_lshl_or_b32 %[x0], %[x0], 16, %[w0]\n\t"                               \
@@ -894,6 +896,8 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
   "s_waitcnt lgkmcnt(0)\n\t"                                                \
   "v_lshl_or_b32 %[x1], %[x1], 16, %[w1]\n\t"                               \
   "s_mov_b64 exec, %[ex]\n\t"
+
+#define EP_REFILL_BOTH EP_REFILL_BOTH_W("")
 
 #define EP_STEP_OUTS                                                                      \
   [x0] "+v"(x0), [x1] "+v"(x1), [SA0] "+s"(F0.OA), [D0] "+s"(F0.D), [SA1] "+s"(F1.OA),  \
@@ -919,33 +923,67 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 // issue priority: the dependent ALU chain of a wave whose table reads have
 // landed goes ahead of waves that are still waiting, which shortens every
 // wave's step latency.
-template <int B, int FIELD>
+//
+// While the ring words are in flight the step turns its own entries into
+// weights (YM = 1: y = fma(sg, z, hc); YM = 2: also clamped to [-m, m]; YM = 0:
+// nothing), z being the entry's top byte.  For field 8 the parity bit of
+// z_1 + ... + z_7 (bit 24 of X) is first merged into the entry.
+#define EP_Y_CVT                                                                      \
+  "v_cvt_f32_i32_sdwa %[y0], sext(%[e0]) dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3\n\t" \
+  "v_cvt_f32_i32_sdwa %[y1], sext(%[e1]) dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3\n\t" \
+  "v_fma_f32 %[y0], %[sg0], %[y0], %[hc0]\n\t"                                        \
+  "v_fma_f32 %[y1], %[sg1], %[y1], %[hc1]\n\t"
+#define EP_Y_SAT                                                                      \
+  "v_med3_f32 %[y0], %[y0], %[nm], %[m]\n\t"                                          \
+  "v_med3_f32 %[y1], %[y1], %[nm], %[m]\n\t"
+#define EP_Y_PAR                                                                      \
+  "v_and_or_b32 %[e0], %[X0], %[bit], %[e0]\n\t"                                      \
+  "v_and_or_b32 %[e1], %[X1], %[bit], %[e1]\n\t"
+
+#define EP_FIELD_ASM(WORK)                                                               \
+  asm volatile(                                                                          \
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"                                                \
+      "v_and_b32 %[u1], %[mk], %[x1]\n\t"                                                \
+      "v_lshl_add_u32 %[u0], %[u0], 2, %[cb0]\n\t"                                       \
+      "v_lshl_add_u32 %[u1], %[u1], 2, %[cb1]\n\t"                                       \
+      "ds_read_b32 %[e0], %[u0] offset:%[off]\n\t"                                       \
+      "ds_read_b32 %[e1], %[u1] offset:%[off]\n\t"                                       \
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"                                             \
+      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"                                             \
+      "s_waitcnt lgkmcnt(1)\n\t"                                                         \
+      "s_setprio 2\n\t"                                                                  \
+      "v_and_b32 %[u0], 0xfff, %[e0]\n\t"                                                \
+      "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"                                               \
+      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"                                     \
+      "s_waitcnt lgkmcnt(0)\n\t"                                                         \
+      "v_and_b32 %[u1], 0xfff, %[e1]\n\t"                                                \
+      "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"                                               \
+      "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"                                     \
+      EP_REFILL_BOTH_W(WORK)                                                             \
+      : EP_STEP_OUTS, [e0] "=&v"(e0), [e1] "=&v"(e1), [y0] "=&v"(y0), [y1] "=&v"(y1)     \
+      : [cb0] "v"(cb0), [cb1] "v"(cb1), [off] "i"((FIELD - 1) * (4 << B)), [sg0] "v"(sg0), \
+        [sg1] "v"(sg1), [hc0] "v"(hc0), [hc1] "v"(hc1), [m] "s"(m), [nm] "v"(-m),        \
+        [X0] "v"(X0), [X1] "v"(X1), [bit] "s"(1u << 24), EP_STEP_INS                     \
+      : EP_STEP_CLOBBERS)
+
+template <int B, int FIELD, int YM>
 __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
-                                            uint32_t& e0, uint32_t& e1, FastChain& F0, FastChain& F1,
-                                            uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
+                                            uint32_t& e0, uint32_t& e1, float& y0, float& y1,
+                                            float sg0, float sg1, float hc0, float hc1,
+                                            uint32_t X0, uint32_t X1, float m, FastChain& F0,
+                                            FastChain& F1, uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
   EP_STEP_TEMPS;
-  asm volatile(
-      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
-      "v_and_b32 %[u1], %[mk], %[x1]\n\t"
-      "v_lshl_add_u32 %[u0], %[u0], 2, %[cb0]\n\t"
-      "v_lshl_add_u32 %[u1], %[u1], 2, %[cb1]\n\t"
-      "ds_read_b32 %[e0], %[u0] offset:%[off]\n\t"
-      "ds_read_b32 %[e1], %[u1] offset:%[off]\n\t"
-      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
-      "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"
-      "s_waitcnt lgkmcnt(1)\n\t"
-      "s_setprio 2\n\t"
-      "v_and_b32 %[u0], 0xfff, %[e0]\n\t"
-      "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"
-      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"
-      "s_waitcnt lgkmcnt(0)\n\t"
-      "v_and_b32 %[u1], 0xfff, %[e1]\n\t"
-      "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"
-      "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"
-      EP_REFILL_BOTH
-      : EP_STEP_OUTS, [e0] "=&v"(e0), [e1] "=&v"(e1)
-      : [cb0] "v"(cb0), [cb1] "v"(cb1), [off] "i"((FIELD - 1) * (4 << B)), EP_STEP_INS
-      : EP_STEP_CLOBBERS);
+  if constexpr (YM == 0) {
+    EP_FIELD_ASM("");
+  } else if constexpr (FIELD == 8 && YM == 1) {
+    EP_FIELD_ASM(EP_Y_PAR EP_Y_CVT);
+  } else if constexpr (FIELD == 8) {
+    EP_FIELD_ASM(EP_Y_PAR EP_Y_CVT EP_Y_SAT);
+  } else if constexpr (YM == 1) {
+    EP_FIELD_ASM(EP_Y_CVT);
+  } else {
+    EP_FIELD_ASM(EP_Y_CVT EP_Y_SAT);
+  }
 }
 
 // Coset symbol (two-entry table f0, f1) for both chains, then the refill.
@@ -998,45 +1036,40 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
 // single rounding fma(sigma, z, c * sigma / 2) -- equal to the product of the
 // FP32 row scale with the coordinate -- and snapped to the output type.  The
 // entry of an odd field waits in `ep` for its even partner; the pair is then
-// converted and packed into the output words w.
+// converted and packed into the output words w.  The weights themselves are
+// formed inside the symbol steps (field_step2).
 struct QAcc {
   uint32_t X;     // xor of the entries of fields 1..7 so far
   uint32_t ep;    // entry of the pending odd field
+  float yp;       // its weight
   uint32_t w[8];  // packed output words (the output type uses 2, 4 or 8 of them)
 };
-
-template <int DT, bool SAT>
-__device__ __forceinline__ float q_weight(uint32_t e, float sg, float hc) {
-  float y = __builtin_fmaf(sg, (float)((int32_t)e >> 24), hc);
-  if constexpr (SAT) {
-    constexpr float m = DT == EP_FP8_E4M3 ? 448.0f : DT == EP_FP16 ? 65504.0f : 3.38953139e38f;
-    y = sat(y, m);
-  }
-  return y;
-}
 
 __device__ __forceinline__ uint32_t int8_pair(float a, float b) {
   int ia = min((int)__builtin_rintf(sat(a, 128.0f)), 127), ib = min((int)__builtin_rintf(sat(b, 128.0f)), 127);
   return (uint32_t)(ia & 0xFF) | ((uint32_t)(ib & 0xFF) << 8);
 }
 
-template <int DT, bool SAT, int FIELD>
-__device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float sg, float hc, uint32_t c) {
+// Fold field FIELD's entry e and weight y (computed in the step, see
+// field_step2) into the chain's accumulator; c is the coset bit.
+template <int DT, int FIELD>
+__device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float y, uint32_t c) {
   if constexpr (FIELD % 2 == 1) {
     if constexpr (FIELD == 7) a.X ^= e;
     a.ep = e;
+    a.yp = y;
     return;
   } else {
     if constexpr (FIELD == 2) a.X = a.ep ^ e;
     else if constexpr (FIELD < 8) a.X = xor3(a.X, a.ep, e);
-    else e |= a.X & (1u << 24);
     constexpr int p = FIELD / 2 - 1;   // pair index 0..3
     if constexpr (DT == EP_COORD2_I32) {
+      if constexpr (FIELD == 8) e |= a.X & (1u << 24);
       a.w[2 * p] = (uint32_t)(2 * ((int32_t)a.ep >> 24) + (int32_t)c);
       a.w[2 * p + 1] = (uint32_t)(2 * ((int32_t)e >> 24) + (int32_t)c);
       return;
     }
-    const float y0 = q_weight<DT, SAT>(a.ep, sg, hc), y1 = q_weight<DT, SAT>(e, sg, hc);
+    const float y0 = a.yp, y1 = y;
     if constexpr (DT == EP_BF16) {
       a.w[p] = bf16_pair(y0, y1);
     } else if constexpr (DT == EP_FP16) {
@@ -1091,6 +1124,10 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
   const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(L.blob + L.off_sigma), (short)0, (int)(4 * L.rows), 0x00020000);
   constexpr uint32_t VB = vec_bytes<DT>();
+  // weights formed in the steps: none for the doubled-coordinate output,
+  // clamped to the type's finite range when SAT
+  constexpr int YM = DT == EP_COORD2_I32 ? 0 : SAT ? 2 : 1;
+  const float ymax = DT == EP_FP8_E4M3 ? 448.0f : DT == EP_FP16 ? 65504.0f : 3.38953139e38f;
 
   const uint32_t vrb0 = ring_area + wave * 2 * kFastChainBytes + half * kFastRingBytes;
   const uint32_t vrb1 = vrb0 + kFastChainBytes;
@@ -1145,13 +1182,16 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
           __builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row_of(L, vb[j] + 32 * k), 0, 0));
     }
     uint32_t cb[2], e0, e1;
+    float y0, y1;
     QAcc acc[2];
+    acc[0].X = acc[1].X = 0;
     coset_step2<B>(x[0], x[1], cb[0], cb[1], hc[0], hc[1], sg[0], sg[1], vf0, vf1, vcb, F0, F1, vH,
                    vrb0, vrb1);
 #define EP_FIELD(I)                                                                           \
-  field_step2<B, I>(x[0], x[1], cb[0], cb[1], e0, e1, F0, F1, vH, vrb0, vrb1);               \
-  q_take<DT, SAT, I>(acc[0], e0, sg[0], hc[0], cb[0] >> (B + 5));                             \
-  q_take<DT, SAT, I>(acc[1], e1, sg[1], hc[1], cb[1] >> (B + 5));
+  field_step2<B, I, YM>(x[0], x[1], cb[0], cb[1], e0, e1, y0, y1, sg[0], sg[1], hc[0], hc[1],  \
+                        acc[0].X, acc[1].X, ymax, F0, F1, vH, vrb0, vrb1);                    \
+  q_take<DT, I>(acc[0], e0, y0, cb[0] >> (B + 5));                                            \
+  q_take<DT, I>(acc[1], e1, y1, cb[1] >> (B + 5));
     EP_FIELD(1) EP_FIELD(2)
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
