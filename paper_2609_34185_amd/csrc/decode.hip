@@ -20,6 +20,9 @@
 //               byte in bits 24-31, the integer part z of the coordinate
 //               (2p_i = 2z + c; for field 8, z = 2m, so 2p_8 = 2(z + pi) + c)
 //               -- b <= 11 only;
+//   kPathWide   the same table with wide entries for larger coordinates:
+//               f - 1 (bits 0-10), u - F (bits 11-21) and z as a signed
+//               10-bit field (bits 22-31); one more add per symbol;
 //   kPathSearch per-symbol cumulative table (F | f << 16) searched with a
 //               fixed-trip binary search -- any b, alphabets up to the LDS size.
 #include <hip/hip_runtime.h>
@@ -283,6 +286,10 @@ __device__ __forceinline__ int32_t doubled_value(int32_t z, int field, uint32_t 
 // value m for field 8, so that every coordinate is 2z + c before field 8's
 // parity bit (2 pi) is added; the host admits a tensor to this path only when
 // every doubled coordinate lies in [-256, 255], i.e. z fits a signed byte.
+// Wide entries (WIDE) hold f - 1 in 11 bits (f = 2^b only for a one-symbol
+// table), u - F in 11 bits and z in a signed 10-bit field: doubled coordinates
+// in [-1024, 1023].
+template <bool WIDE>
 __device__ __forceinline__ void build_lut_table(const LayerDev& L, uint32_t* lut,
                                                 const uint32_t* cum, int t, int j) {
   const uint32_t M = 1u << L.b;
@@ -308,13 +315,15 @@ __device__ __forceinline__ void build_lut_table(const LayerDev& L, uint32_t* lut
     uint32_t F = e & 0xFFFF, f = e >> 16;
     const int32_t v = (int32_t)s + L.tab_min[t];
     const int32_t z = field < 8 ? v : 2 * v;
-    row[u] = f | ((u - F) << 12) | ((uint32_t)(z & 0xFF) << 24);
+    row[u] = WIDE ? (f - 1) | ((u - F) << 11) | ((uint32_t)(z & 0x3FF) << 22)
+                  : f | ((u - F) << 12) | ((uint32_t)(z & 0xFF) << 24);
   }
 }
 
+template <bool WIDE>
 __device__ __forceinline__ void build_lut(const LayerDev& L, uint32_t* lut, const uint32_t* cum) {
   for (int t = (int)wave_id(); t < 16; t += kWavesPerGroup)
-    build_lut_table(L, lut, cum, t, threadIdx.x & 63);
+    build_lut_table<WIDE>(L, lut, cum, t, threadIdx.x & 63);
 }
 
 // LDS bytes of the payload rings of a workgroup (all waves, all halves).
@@ -446,6 +455,13 @@ __device__ __forceinline__ void decode_field(const Hot& L, const uint32_t* lds, 
     const uint32_t e = lds[cb + u + (uint32_t)(field - 1) * M];
     x = __umul24(e & 0xFFFu, x >> B) + ((e >> 12) & 0x7FFu);
     dval = 2 * ((int32_t)e >> 24) + (int32_t)c;
+  } else if (PATH == kPathWide) {
+    constexpr uint32_t M = 1u << B;
+    const uint32_t u = x & (M - 1);
+    const uint32_t e = lds[cb + u + (uint32_t)(field - 1) * M];
+    const uint32_t g = x >> B;
+    x = __umul24(e & 0x7FFu, g) + g + ((e >> 11) & 0x7FFu);   // (f - 1) g + g + (u - F)
+    dval = 2 * ((int32_t)e >> 22) + (int32_t)c;
   } else {
     // Bucketed search: the bucket j of u (its top k bits) bounds the symbol to
     // [bk[j], bk[j + 1]]; a binary search on the u16 cumulative table narrows
@@ -926,11 +942,19 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 //
 // While the ring words are in flight the step turns its own entries into
 // weights (YM = 1: y = fma(sg, z, hc); YM = 2: also clamped to [-m, m]; YM = 0:
-// nothing), z being the entry's top byte.  For field 8 the parity bit of
-// z_1 + ... + z_7 (bit 24 of X) is first merged into the entry.
+// nothing), z being the entry's top byte (top 10 bits for wide entries).  For
+// field 8 the parity bit of z_1 + ... + z_7 (the low bit of z in X) is first
+// merged into the entry.
 #define EP_Y_CVT                                                                      \
   "v_cvt_f32_i32_sdwa %[y0], sext(%[e0]) dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3\n\t" \
   "v_cvt_f32_i32_sdwa %[y1], sext(%[e1]) dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3\n\t" \
+  "v_fma_f32 %[y0], %[sg0], %[y0], %[hc0]\n\t"                                        \
+  "v_fma_f32 %[y1], %[sg1], %[y1], %[hc1]\n\t"
+#define EP_Y_CVT_WIDE                                                                 \
+  "v_ashrrev_i32 %[y0], 22, %[e0]\n\t"                                                \
+  "v_ashrrev_i32 %[y1], 22, %[e1]\n\t"                                                \
+  "v_cvt_f32_i32_e32 %[y0], %[y0]\n\t"                                                \
+  "v_cvt_f32_i32_e32 %[y1], %[y1]\n\t"                                                \
   "v_fma_f32 %[y0], %[sg0], %[y0], %[hc0]\n\t"                                        \
   "v_fma_f32 %[y1], %[sg1], %[y1], %[hc1]\n\t"
 #define EP_Y_SAT                                                                      \
@@ -939,8 +963,19 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
 #define EP_Y_PAR                                                                      \
   "v_and_or_b32 %[e0], %[X0], %[bit], %[e0]\n\t"                                      \
   "v_and_or_b32 %[e1], %[X1], %[bit], %[e1]\n\t"
+// x = f (x >> b) + (u - F) from a narrow entry, chain j
+#define EP_DEC(j)                                                                     \
+  "v_and_b32 %[u" #j "], 0xfff, %[e" #j "]\n\t"                                        \
+  "v_bfe_u32 %[t" #j "], %[e" #j "], 12, 11\n\t"                                       \
+  "v_mad_u32_u24 %[x" #j "], %[u" #j "], %[g" #j "], %[t" #j "]\n\t"
+// the same from a wide entry: (f - 1) (x >> b) + (x >> b) + (u - F)
+#define EP_DEC_WIDE(j)                                                                \
+  "v_and_b32 %[u" #j "], 0x7ff, %[e" #j "]\n\t"                                        \
+  "v_bfe_u32 %[t" #j "], %[e" #j "], 11, 11\n\t"                                       \
+  "v_add_u32_e32 %[t" #j "], %[g" #j "], %[t" #j "]\n\t"                                \
+  "v_mad_u32_u24 %[x" #j "], %[u" #j "], %[g" #j "], %[t" #j "]\n\t"
 
-#define EP_FIELD_ASM(WORK)                                                               \
+#define EP_FIELD_ASM(DEC0, DEC1, WORK)                                                   \
   asm volatile(                                                                          \
       "v_and_b32 %[u0], %[mk], %[x0]\n\t"                                                \
       "v_and_b32 %[u1], %[mk], %[x1]\n\t"                                                \
@@ -952,37 +987,36 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
       "v_lshrrev_b32 %[g1], %[b], %[x1]\n\t"                                             \
       "s_waitcnt lgkmcnt(1)\n\t"                                                         \
       "s_setprio 2\n\t"                                                                  \
-      "v_and_b32 %[u0], 0xfff, %[e0]\n\t"                                                \
-      "v_bfe_u32 %[t0], %[e0], 12, 11\n\t"                                               \
-      "v_mad_u32_u24 %[x0], %[u0], %[g0], %[t0]\n\t"                                     \
+      DEC0                                                                               \
       "s_waitcnt lgkmcnt(0)\n\t"                                                         \
-      "v_and_b32 %[u1], 0xfff, %[e1]\n\t"                                                \
-      "v_bfe_u32 %[t1], %[e1], 12, 11\n\t"                                               \
-      "v_mad_u32_u24 %[x1], %[u1], %[g1], %[t1]\n\t"                                     \
+      DEC1                                                                               \
       EP_REFILL_BOTH_W(WORK)                                                             \
       : EP_STEP_OUTS, [e0] "=&v"(e0), [e1] "=&v"(e1), [y0] "=&v"(y0), [y1] "=&v"(y1)     \
       : [cb0] "v"(cb0), [cb1] "v"(cb1), [off] "i"((FIELD - 1) * (4 << B)), [sg0] "v"(sg0), \
         [sg1] "v"(sg1), [hc0] "v"(hc0), [hc1] "v"(hc1), [m] "s"(m), [nm] "v"(-m),        \
-        [X0] "v"(X0), [X1] "v"(X1), [bit] "s"(1u << 24), EP_STEP_INS                     \
+        [X0] "v"(X0), [X1] "v"(X1), [bit] "s"(zbit), EP_STEP_INS                         \
       : EP_STEP_CLOBBERS)
 
-template <int B, int FIELD, int YM>
+template <int B, int FIELD, int YM, bool WIDE>
 __device__ __forceinline__ void field_step2(uint32_t& x0, uint32_t& x1, uint32_t cb0, uint32_t cb1,
                                             uint32_t& e0, uint32_t& e1, float& y0, float& y1,
                                             float sg0, float sg1, float hc0, float hc1,
                                             uint32_t X0, uint32_t X1, float m, FastChain& F0,
                                             FastChain& F1, uint32_t vH, uint32_t vrb0, uint32_t vrb1) {
   EP_STEP_TEMPS;
-  if constexpr (YM == 0) {
-    EP_FIELD_ASM("");
-  } else if constexpr (FIELD == 8 && YM == 1) {
-    EP_FIELD_ASM(EP_Y_PAR EP_Y_CVT);
-  } else if constexpr (FIELD == 8) {
-    EP_FIELD_ASM(EP_Y_PAR EP_Y_CVT EP_Y_SAT);
-  } else if constexpr (YM == 1) {
-    EP_FIELD_ASM(EP_Y_CVT);
+  const uint32_t zbit = 1u << (WIDE ? 22 : 24);   // low bit of the entry's z
+  if constexpr (WIDE) {
+    if constexpr (YM == 0) EP_FIELD_ASM(EP_DEC_WIDE(0), EP_DEC_WIDE(1), "");
+    else if constexpr (FIELD == 8 && YM == 1) EP_FIELD_ASM(EP_DEC_WIDE(0), EP_DEC_WIDE(1), EP_Y_PAR EP_Y_CVT_WIDE);
+    else if constexpr (FIELD == 8) EP_FIELD_ASM(EP_DEC_WIDE(0), EP_DEC_WIDE(1), EP_Y_PAR EP_Y_CVT_WIDE EP_Y_SAT);
+    else if constexpr (YM == 1) EP_FIELD_ASM(EP_DEC_WIDE(0), EP_DEC_WIDE(1), EP_Y_CVT_WIDE);
+    else EP_FIELD_ASM(EP_DEC_WIDE(0), EP_DEC_WIDE(1), EP_Y_CVT_WIDE EP_Y_SAT);
   } else {
-    EP_FIELD_ASM(EP_Y_CVT EP_Y_SAT);
+    if constexpr (YM == 0) EP_FIELD_ASM(EP_DEC(0), EP_DEC(1), "");
+    else if constexpr (FIELD == 8 && YM == 1) EP_FIELD_ASM(EP_DEC(0), EP_DEC(1), EP_Y_PAR EP_Y_CVT);
+    else if constexpr (FIELD == 8) EP_FIELD_ASM(EP_DEC(0), EP_DEC(1), EP_Y_PAR EP_Y_CVT EP_Y_SAT);
+    else if constexpr (YM == 1) EP_FIELD_ASM(EP_DEC(0), EP_DEC(1), EP_Y_CVT);
+    else EP_FIELD_ASM(EP_DEC(0), EP_DEC(1), EP_Y_CVT EP_Y_SAT);
   }
 }
 
@@ -1045,15 +1079,23 @@ struct QAcc {
   uint32_t w[8];  // packed output words (the output type uses 2, 4 or 8 of them)
 };
 
+// clamp(RNE(a), -128, 127) and the same of b as two bytes (low half-word):
+// round to nearest even, convert (the conversion saturates to the int32
+// range), then an arithmetic shift by 0 with saturation to int8, packed into
+// the low half of the destination (whose high half the instruction leaves as
+// it was, hence the mask).
 __device__ __forceinline__ uint32_t int8_pair(float a, float b) {
-  int ia = min((int)__builtin_rintf(sat(a, 128.0f)), 127), ib = min((int)__builtin_rintf(sat(b, 128.0f)), 127);
-  return (uint32_t)(ia & 0xFF) | ((uint32_t)(ib & 0xFF) << 8);
+  const int ia = (int)__builtin_rintf(a), ib = (int)__builtin_rintf(b);
+  uint32_t r;
+  asm("v_ashr_pk_i8_i32 %0, %1, %2, 0" : "=v"(r) : "v"(ia), "v"(ib));
+  return r & 0xFFFFu;
 }
 
 // Fold field FIELD's entry e and weight y (computed in the step, see
 // field_step2) into the chain's accumulator; c is the coset bit.
-template <int DT, int FIELD>
+template <int DT, int FIELD, bool WIDE>
 __device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float y, uint32_t c) {
+  constexpr int ZS = WIDE ? 22 : 24;   // position of z in the entry
   if constexpr (FIELD % 2 == 1) {
     if constexpr (FIELD == 7) a.X ^= e;
     a.ep = e;
@@ -1064,9 +1106,9 @@ __device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float y, uint32_t c)
     else if constexpr (FIELD < 8) a.X = xor3(a.X, a.ep, e);
     constexpr int p = FIELD / 2 - 1;   // pair index 0..3
     if constexpr (DT == EP_COORD2_I32) {
-      if constexpr (FIELD == 8) e |= a.X & (1u << 24);
-      a.w[2 * p] = (uint32_t)(2 * ((int32_t)a.ep >> 24) + (int32_t)c);
-      a.w[2 * p + 1] = (uint32_t)(2 * ((int32_t)e >> 24) + (int32_t)c);
+      if constexpr (FIELD == 8) e |= a.X & (1u << ZS);
+      a.w[2 * p] = (uint32_t)(2 * ((int32_t)a.ep >> ZS) + (int32_t)c);
+      a.w[2 * p + 1] = (uint32_t)(2 * ((int32_t)e >> ZS) + (int32_t)c);
       return;
     }
     const float y0 = a.yp, y1 = y;
@@ -1112,7 +1154,7 @@ constexpr uint32_t vec_bytes() {
 // (two chains).  TWO: every lane's vectors v, v + 32, ... of a tile lie in at
 // most two rows (C/8 >= V - 32), so each lane holds both row scales and
 // switches at round kc; otherwise the row scale is loaded every round.
-template <int B, int DT, bool SAT, bool TWO>
+template <int B, int DT, bool SAT, bool TWO, bool WIDE>
 __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ring_area, uint32_t t0,
                                          int32_t* status) {
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
@@ -1188,10 +1230,10 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
     coset_step2<B>(x[0], x[1], cb[0], cb[1], hc[0], hc[1], sg[0], sg[1], vf0, vf1, vcb, F0, F1, vH,
                    vrb0, vrb1);
 #define EP_FIELD(I)                                                                           \
-  field_step2<B, I, YM>(x[0], x[1], cb[0], cb[1], e0, e1, y0, y1, sg[0], sg[1], hc[0], hc[1],  \
-                        acc[0].X, acc[1].X, ymax, F0, F1, vH, vrb0, vrb1);                    \
-  q_take<DT, I>(acc[0], e0, y0, cb[0] >> (B + 5));                                            \
-  q_take<DT, I>(acc[1], e1, y1, cb[1] >> (B + 5));
+  field_step2<B, I, YM, WIDE>(x[0], x[1], cb[0], cb[1], e0, e1, y0, y1, sg[0], sg[1], hc[0],  \
+                              hc[1], acc[0].X, acc[1].X, ymax, F0, F1, vH, vrb0, vrb1);       \
+  q_take<DT, I, WIDE>(acc[0], e0, y0, cb[0] >> (B + 5));                                      \
+  q_take<DT, I, WIDE>(acc[1], e1, y1, cb[1] >> (B + 5));
     EP_FIELD(1) EP_FIELD(2)
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
@@ -1221,34 +1263,35 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
   if (err && status) atomicOr(status, (int32_t)err);
 }
 
-template <int B, int DT, bool SAT>
+template <int B, int DT, bool SAT, bool WIDE>
 __device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                               uint32_t t0, int32_t* status) {
-  if (L.cvec + 32 >= L.V) lut_task<B, DT, SAT, true>(L, lds, ring_area, t0, status);
-  else lut_task<B, DT, SAT, false>(L, lds, ring_area, t0, status);
+  if (L.cvec + 32 >= L.V) lut_task<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
+  else lut_task<B, DT, SAT, false, WIDE>(L, lds, ring_area, t0, status);
 }
 
-// Output-type dispatch of a full four-tile slot-table task.  Returns false for
-// the combinations the steady state does not cover (they take the generic loop).
-template <int B>
+// Output-type dispatch of a full four-tile slot-table task (narrow or wide
+// entries).  Returns false for the combinations the steady state does not
+// cover (they take the generic loop).
+template <int B, bool WIDE>
 __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                              uint32_t t0, int32_t* status) {
   switch (L.out_dtype) {
     case EP_BF16:
-      if (L.saturate) lut_task_rows<B, EP_BF16, true>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_BF16, false>(L, lds, ring_area, t0, status);
+      if (L.saturate) lut_task_rows<B, EP_BF16, true, WIDE>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_BF16, false, WIDE>(L, lds, ring_area, t0, status);
       return true;
     case EP_FP16:
-      if (L.saturate) lut_task_rows<B, EP_FP16, true>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_FP16, false>(L, lds, ring_area, t0, status);
+      if (L.saturate) lut_task_rows<B, EP_FP16, true, WIDE>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_FP16, false, WIDE>(L, lds, ring_area, t0, status);
       return true;
     case EP_FP8_E4M3:
-      if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_FP8_E4M3, false>(L, lds, ring_area, t0, status);
+      if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true, WIDE>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_FP8_E4M3, false, WIDE>(L, lds, ring_area, t0, status);
       return true;
-    case EP_INT8: lut_task_rows<B, EP_INT8, false>(L, lds, ring_area, t0, status); return true;
-    case EP_FP32: lut_task_rows<B, EP_FP32, false>(L, lds, ring_area, t0, status); return true;
-    case EP_COORD2_I32: lut_task_rows<B, EP_COORD2_I32, false>(L, lds, ring_area, t0, status); return true;
+    case EP_INT8: lut_task_rows<B, EP_INT8, false, WIDE>(L, lds, ring_area, t0, status); return true;
+    case EP_FP32: lut_task_rows<B, EP_FP32, false, WIDE>(L, lds, ring_area, t0, status); return true;
+    case EP_COORD2_I32: lut_task_rows<B, EP_COORD2_I32, false, WIDE>(L, lds, ring_area, t0, status); return true;
     default: return false;
   }
 }
@@ -1289,7 +1332,7 @@ __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds,
 // after the search tables (search path).
 template <int PATH>
 __device__ __forceinline__ uint32_t ring_offset(const LayerDev& L) {
-  return PATH == kPathLut ? (64u << L.b) : search_layout(L.b, L.sum_A).total;
+  return PATH != kPathSearch ? (64u << L.b) : search_layout(L.b, L.sum_A).total;
 }
 
 // Search-path tables (byte layout from search_layout): u16 cumulative values
@@ -1321,20 +1364,33 @@ __device__ __forceinline__ void build_search(const LayerDev& L, uint32_t* lds) {
 
 template <int PATH>
 __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
-  if (PATH == kPathLut) {
+  if (PATH != kPathSearch && L.sum_A <= kRingBytes / 4) {
     uint32_t* cum = lds + (16u << L.b);   // scratch inside the ring area
     build_cumulative(L, cum);
     __syncthreads();
-    build_lut(L, lds, cum);
+    build_lut<PATH == kPathWide>(L, lds, cum);
+  } else if (PATH != kPathSearch) {
+    // more symbols than the scratch holds (wide tables): every lane fills the
+    // slot range of its own symbol straight from the table's prefix scan
+    scan_tables(L, [&](int t, uint32_t s, uint32_t F, uint32_t f) {
+      uint32_t* row = lds + ((uint32_t)t << L.b);
+      const int field = (t & 7) + 1;
+      const int32_t v = (int32_t)s + L.tab_min[t];
+      const uint32_t z = (uint32_t)(field < 8 ? v : 2 * v);
+      for (uint32_t i = 0; i < f; i++)
+        row[F + i] = PATH == kPathWide ? (f - 1) | (i << 11) | ((z & 0x3FF) << 22)
+                                       : f | (i << 12) | ((z & 0xFF) << 24);
+    }, [](int, uint32_t) {});
   } else {
     build_search(L, lds);
   }
 }
 
 // A wave task is eight tiles.  When all eight are full (V vectors each, V a
-// multiple of 32) both paths decode them in two four-tile steady-state passes
-// (two chains each); otherwise the generic loop takes the task as two
-// four-tile halves.
+// multiple of 32) every path decodes them in two four-tile steady-state passes
+// (two chains each) -- the slot-table paths at b = 11, the precision the
+// encoder starts from for targets up to 7 bpp; otherwise the generic loop
+// takes the task as two four-tile halves.
 constexpr int kChains = 2;                 // chains of the generic loop
 constexpr uint32_t kTilesPerTask = 8;
 static_assert(kChains == 2, "the generic loop and the search steady state advance two chains");
@@ -1347,13 +1403,13 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
   const uint32_t nvec = L.rows * L.cvec;
   const bool full8 = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
                      (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
-  if (full8 && L.pay_bytes < kFastOob) {
-    if constexpr (PATH == kPathLut) {
-      if (lut_task_any<B>(L, lb, ring_area, t0, status)) {
-        lut_task_any<B>(L, lb, ring_area, t0 + 4, status);
+  if (full8 && L.pay_bytes < kFastOob && (PATH == kPathSearch || B == 11)) {
+    if constexpr (PATH != kPathSearch && B == 11) {
+      if (lut_task_any<B, PATH == kPathWide>(L, lb, ring_area, t0, status)) {
+        lut_task_any<B, PATH == kPathWide>(L, lb, ring_area, t0 + 4, status);
         return;
       }
-    } else {
+    } else if constexpr (PATH == kPathSearch) {
       if (decode_task_fast_any<PATH, B>(L, lb, ring_area, 2 * task, status)) {
         decode_task_fast_any<PATH, B>(L, lb, ring_area, 2 * task + 1, status);
         return;
@@ -1463,7 +1519,7 @@ DeviceProps device_props() {
 }
 
 uint32_t lds_bytes(uint32_t path, const ep_tensor_info& I) {
-  if (path == kPathLut) return (64u << I.prob_bits) + kRingBytes;
+  if (path != kPathSearch) return (64u << I.prob_bits) + kRingBytes;
   return search_layout(I.prob_bits, I.sum_alphabet).total + kRingBytes;
 }
 
@@ -1546,7 +1602,7 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
 // is a long serial chain of symbol rounds, so a lightly loaded CU finishes it
 // sooner.
 uint32_t groups_for(uint32_t path, uint32_t lds, uint32_t tasks, const DeviceProps& P) {
-  uint32_t per_cu = path == kPathLut ? 1u : (uint32_t)std::max<size_t>(1, std::min<size_t>(2, 160 * 1024 / std::max<uint32_t>(lds, 1)));
+  uint32_t per_cu = path != kPathSearch ? 1u : (uint32_t)std::max<size_t>(1, std::min<size_t>(2, 160 * 1024 / std::max<uint32_t>(lds, 1)));
   uint32_t g = (uint32_t)P.cus * per_cu;
   return std::max(1u, std::min(g, tasks));
 }
@@ -1570,7 +1626,9 @@ int launch_geometry(uint32_t path, uint32_t total, uint32_t lds, uint32_t& G, ui
   G = groups_for(path, lds, total, P);
   per = (total + G - 1) / G;
   G = (total + per - 1) / per;
-  int rc = path == kPathLut ? set_lds_limit<kPathLut>(lds) : set_lds_limit<kPathSearch>(lds);
+  int rc = path == kPathLut ? set_lds_limit<kPathLut>(lds)
+           : path == kPathWide ? set_lds_limit<kPathWide>(lds)
+                               : set_lds_limit<kPathSearch>(lds);
   if (rc) return fail(EP_ERR_HIP, "decode: cannot raise the kernel's LDS limit");
   return EP_OK;
 }
@@ -1583,6 +1641,8 @@ int launch_list(uint32_t path, const LayerDev* dl, int n, uint32_t total, uint32
   if (rc) return rc;
   if (path == kPathLut)
     hipLaunchKernelGGL(decode_ws_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
+  else if (path == kPathWide)
+    hipLaunchKernelGGL(decode_ws_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
   else
     hipLaunchKernelGGL(decode_ws_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
   if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (std::string(who) + ": launch failed").c_str());
@@ -1611,6 +1671,8 @@ int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total,
     for (int i = 0; i < n; i++) list.L[i] = D[i];
     if (path == kPathLut)
       hipLaunchKernelGGL(decode_args_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else if (path == kPathWide)
+      hipLaunchKernelGGL(decode_args_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
     else
       hipLaunchKernelGGL(decode_args_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
   }
@@ -1700,7 +1762,7 @@ int stack_decode(const ep_stack* st, int32_t* d_status, void* stream) {
   if (!st || st->n_layers < 0 || (st->n_layers > 0 && !st->d_workspace))
     return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
   if (st->total_tasks == 0) return EP_OK;
-  if (st->path != kPathLut && st->path != kPathSearch)
+  if (st->path != kPathLut && st->path != kPathSearch && st->path != kPathWide)
     return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
   return launch_list(st->path, static_cast<const LayerDev*>(st->d_workspace), st->n_layers,
                      st->total_tasks, st->lds_bytes, d_status, static_cast<hipStream_t>(stream),

@@ -10,13 +10,16 @@ enum DecodePath : uint32_t {
   kPathNone = 0,    // no kernel family in this build can hold the tables
   kPathLut = 1,     // packed slot table in LDS: one 32-bit lookup per symbol
   kPathSearch = 2,  // cumulative table in LDS, branch-free binary search per symbol
+  kPathWide = 3,    // packed slot table with a 10-bit coordinate field (wider ranges)
 };
 
 // LDS bytes of the packed slot table (16 tables x 2^b slots x 4 B) and of the
 // cumulative scratch it is built from.
 constexpr uint32_t kLutMaxBits = 11;
-constexpr int32_t kLutValueMin = -256;   // packed doubled coordinate: signed 9 bits
+constexpr int32_t kLutValueMin = -256;   // doubled coordinates whose integer part fits a signed byte
 constexpr int32_t kLutValueMax = 255;
+constexpr int32_t kWideValueMin = -1024; // ... a signed 10-bit field (wide entries)
+constexpr int32_t kWideValueMax = 1023;
 constexpr uint32_t kSearchLdsBytes = 128 * 1024;   // the payload rings take the other 32 KiB
 
 // Search path: u16 cumulative tables plus, per table, 2^k + 1 u16 bucket
@@ -52,6 +55,8 @@ constexpr SearchLayout search_layout(uint32_t b, uint32_t sum_A) {
 inline uint32_t choose_path(const ep_tensor_info& I) {
   if (I.prob_bits <= kLutMaxBits && I.coord2_min >= kLutValueMin && I.coord2_max <= kLutValueMax)
     return kPathLut;
+  if (I.prob_bits <= kLutMaxBits && I.coord2_min >= kWideValueMin && I.coord2_max <= kWideValueMax)
+    return kPathWide;
   if (I.sum_alphabet <= 0xFFFF0u && search_layout(I.prob_bits, I.sum_alphabet).bucket_bits)
     return kPathSearch;
   return kPathNone;

@@ -93,15 +93,41 @@ def test_every_probability_precision(E, oracle, b):
     check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"b{b}")
 
 
+def expected_path(info):
+    """The decode path rule: narrow slot entries while every doubled coordinate lies in
+    [-256, 255], wide ones up to [-1024, 1023] (both for b <= 11), else bucketed search."""
+    if info.prob_bits <= 11 and -256 <= info.coord2_min and info.coord2_max <= 255:
+        return 1
+    if info.prob_bits <= 11 and -1024 <= info.coord2_min and info.coord2_max <= 1023:
+        return 3
+    return 2
+
+
 @pytest.mark.parametrize("target", [6.0, 8.0, 10.0])
 def test_high_rates_large_alphabets(E, oracle, target):
-    """High targets give wide coordinate ranges and large tables (b = 12 at 8 bpp): the
-    bucketed-search path decodes them; its tables are built in LDS from the blob."""
+    """High targets give wide coordinate ranges and large tables (b = 12 at 8 bpp): wide
+    slot entries or the bucketed-search path decode them; both build their tables in LDS
+    from the blob."""
     w = W.attention_projection()[:512, :2048]
     blob, st = oracle.encode(w, target)
     info = check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "FP16"], tag=f"rate{target}")
-    assert info.path == 2
+    assert info.path == expected_path(info) and info.path in (2, 3)
     say(f"    b={info.prob_bits} sum_A={info.sum_alphabet} coord2 [{info.coord2_min}, {info.coord2_max}]")
+
+
+@pytest.mark.parametrize("b", [9, 10, 11])
+def test_wide_slot_entries(E, oracle, b):
+    """Coordinates beyond a signed byte at b <= 11 take the wide slot entries (f - 1, u - F
+    and a 10-bit coordinate field): every output type, full and ragged tiles, both row
+    modes of the steady state (C/8 below and above V - 32)."""
+    for rows, cols in ((96, 2048), (131, 3000), (64, 4096)):
+        w = (W.ragged_tensor(40 + b, rows, cols).astype(np.uint32) << 16).view(np.float32).copy()
+        w[:, :8] *= 8.0   # a few large columns widen the coordinate range
+        blob, st = oracle.encode(w, 6.0, prob_bits=b)
+        info = E.blob_info(blob)
+        say(f"    {rows}x{cols} b={info.prob_bits} coord2 [{info.coord2_min}, {info.coord2_max}]")
+        assert info.path == 3, (info.prob_bits, info.coord2_min, info.coord2_max)
+        check_blob(E, oracle, blob, tag=f"wide{b}")
 
 
 def test_escalated_precision_blobs(E, oracle):
@@ -273,7 +299,8 @@ def test_config3_product_encoder_reproduces_oracle_blobs(E, mlp, mlp_fp8_blobs):
 
 def test_config5_down_int8_container(E, oracle, mlp):
     blob, st = oracle.encode(mlp["down"], 6.0, container=oracle.CONT_INT8)
-    check_blob(E, oracle, blob, dtypes=["INT8", "COORD2"], tag="cfg5")
+    info = check_blob(E, oracle, blob, dtypes=["INT8", "COORD2"], tag="cfg5")
+    assert info.path == 3   # coordinates beyond a signed byte: wide slot entries
 
 
 def test_config4_stack_two_blocks_one_launch(E, oracle):
