@@ -27,6 +27,12 @@ SALU and LDS utilisation from the committed SQ counter summary.  Both are null
 when their summary is absent or was taken from a different decode kernel
 source than the one built.
 
+Timing: the W warm-up steps are followed, untimed, by further steps until
+SETTLE_S seconds have passed since the warm-up began (config.settle_steps
+says how many), because a GPU fresh from idle runs its first milliseconds at
+lower clocks; then exactly K steps are timed with HIP events on the launch
+stream.
+
 --copy-calibration runs only a plain 1 GiB device-to-device copy (five times),
 the reference kernel for those counter factors.
 """
@@ -46,6 +52,7 @@ if ROOT not in sys.path:
 
 METRIC = "decoded weights/s and achieved HBM GB/s (% roofline), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
+SETTLE_S = 0.3
 INT8_PEAK_TOPS = 5000.0   # dense MFMA int8, MI355X
 DECODE_SRC = os.path.join(ROOT, "paper_2609_34185_amd", "csrc", "decode.hip")
 COPY_BYTES = 1 << 30
@@ -156,7 +163,7 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 5}), flush=True)
 
 
-def gemm_leg(E, W, out, info, reps=10):
+def gemm_leg(E, W, out, info, reps=20, warm=30):
     """Time the INT8 MFMA product of the decoded weights with the 8192 x 17408 activations."""
     import torch
     act = torch.from_numpy(W.llm_activations()).cuda()
@@ -167,7 +174,8 @@ def gemm_leg(E, W, out, info, reps=10):
     def run():
         E.gemm_i8_nt(act.data_ptr(), out.data_ptr(), y.data_ptr(), m, n, k, s.cuda_stream)
 
-    run()
+    for _ in range(warm):   # about 20 ms: lets the clocks settle under MFMA load
+        run()
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record(s)
@@ -286,9 +294,16 @@ def main():
     def step():
         E.stack_decode(stack, status.data_ptr(), stream.cuda_stream)
 
+    t0 = time.perf_counter()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    settle = 0
+    while time.perf_counter() - t0 < SETTLE_S:
+        for _ in range(10):
+            step()
+        settle += 10
+        torch.cuda.synchronize()
     assert int(status.item()) == 0, "decode reported a corrupt stream"
 
     start = torch.cuda.Event(enable_timing=True)
@@ -328,7 +343,7 @@ def main():
         "dtype": "u32",
         "data": "synthetic",
         "config": dict(desc, weights=weights, stored_bpp=round(stored_bpp, 4),
-                       bytes_per_step=algo_bytes, wall_s=round(wall, 4),
+                       bytes_per_step=algo_bytes, wall_s=round(wall, 4), settle_steps=settle,
                        cold_cache_ms=cold),
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gbps / HBM_PEAK_GBPS, "traffic": traffic},

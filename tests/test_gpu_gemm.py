@@ -41,8 +41,11 @@ def gemm_gpu(E, a: np.ndarray, b: np.ndarray) -> np.ndarray:
 
 
 @pytest.mark.parametrize("m,n,k", [(128, 128, 64), (200, 130, 208), (1, 1, 16), (257, 129, 1024),
-                                   (512, 384, 4096)])
+                                   (512, 384, 4096), (4300, 4000, 80), (4096, 2560, 48)])
 def test_gemm_matches_oracle_everywhere(E, oracle, m, n, k):
+    """Every element.  On a 256-CU device the launch takes the small shapes as half-width
+    tiles only, 4300 x 4000 as 256 whole tiles plus 16 tiles split in halves (ragged in
+    m, n and k), and 4096 x 2560 as whole tiles only."""
     rng = np.random.default_rng([11, m, n, k])
     a = rng.integers(-128, 128, (m, k), dtype=np.int8)
     b = rng.integers(-128, 128, (n, k), dtype=np.int8)
