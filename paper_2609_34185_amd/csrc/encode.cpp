@@ -25,13 +25,13 @@
 
 #include "../../include/entropack.h"
 #include "common.h"
+#include "encode_math.h"
 
 namespace ep {
 namespace {
 
 constexpr uint32_t kLanes = 32;        // interleaved states per tile
 constexpr uint32_t kStateLow = 1u << 15;
-constexpr double kEta = 1e-12;
 constexpr int kTables = 17;            // coset + (8 fields x 2 cosets)
 
 // ---- small parallel-for over [0, n) with static contiguous chunks ---------
@@ -51,28 +51,12 @@ void parallel_for(int64_t n, int nthreads, const std::function<void(int64_t, int
   for (auto& x : th) x.join();
 }
 
-// ---- rounding to the stored formats ---------------------------------------
-// Round-half-even of v onto a binary float format with `frac` fraction bits,
-// minimum normal exponent emin and largest finite value vmax (saturating).
-double round_to_format(double v, int frac, int emin, double vmax) {
-  if (v == 0.0) return v;
-  double mag = std::fabs(v);
-  int ex = std::ilogb(mag);                  // mag in [2^ex, 2^(ex+1))
-  if (ex < emin) ex = emin;
-  double ulp = std::ldexp(1.0, ex - frac);
-  double q = std::nearbyint(mag / ulp) * ulp;
-  if (q > vmax) q = vmax;
-  return std::signbit(v) ? -q : q;
-}
-
-double to_e4m3(double v) { return round_to_format(v, 3, -6, 448.0); }
-double to_bf16(double v) { return round_to_format(v, 7, -126, 3.3895313892515355e38); }
-double to_fp16(double v) { return round_to_format(v, 10, -14, 65504.0); }
-
-double int8_snap(double v) {
-  double r = std::nearbyint(v);
-  return r > 127 ? 127 : (r < -128 ? -128 : r);
-}
+using em::int8_snap;
+using em::kEta;
+using em::table_index;
+using em::to_bf16;
+using em::to_e4m3;
+using em::to_fp16;
 
 double half_bits_to_double(uint16_t h) {
   int e = (h >> 10) & 0x1F, m = h & 0x3FF;
@@ -91,62 +75,7 @@ double input_at(const void* w, int dt, int64_t i) {
   return f;
 }
 
-// ---- lattice -------------------------------------------------------------
-// Nearest point of D8: coordinate rounding (ties to even), then, if the sum is
-// odd, the coordinate with the largest residual (first on ties) moves by one
-// towards its input (a zero residual moves up).  Section 3.2, eq. d8.
-inline void d8_point(const double* y, double* z) {
-  double r[8], tot = 0;
-  for (int j = 0; j < 8; j++) {
-    z[j] = std::nearbyint(y[j]);
-    r[j] = y[j] - z[j];
-    tot += z[j];
-  }
-  if (std::fmod(std::fabs(tot), 2.0) == 1.0) {
-    int k = 0;
-    double best = std::fabs(r[0]);
-    for (int j = 1; j < 8; j++) {
-      double a = std::fabs(r[j]);
-      if (a > best) {
-        best = a;
-        k = j;
-      }
-    }
-    z[k] += r[k] < 0 ? -1.0 : 1.0;
-  }
-}
-
-inline double sqdist(const double* y, const double* p) {
-  double s = 0;
-  for (int j = 0; j < 8; j++) s += (y[j] - p[j]) * (y[j] - p[j]);
-  return s;
-}
-
-// Nearest E8 point as doubled coordinates; the shifted coset replaces the D8
-// candidate only when strictly closer.
-inline void e8_point(const double* y, int32_t* p2) {
-  double a[8], h[8], yh[8];
-  d8_point(y, a);
-  for (int j = 0; j < 8; j++) yh[j] = y[j] - 0.5;
-  d8_point(yh, h);
-  for (int j = 0; j < 8; j++) h[j] += 0.5;
-  const double* win = sqdist(y, h) < sqdist(y, a) ? h : a;
-  for (int j = 0; j < 8; j++) p2[j] = (int32_t)(2.0 * win[j]);
-}
-
-// Field tuple (c, z1..z7, m) of a doubled point (eq. parity).
-inline void split_fields(const int32_t* p2, int32_t* f) {
-  int32_t c = p2[0] & 1, par = 0;
-  for (int j = 0; j < 7; j++) {
-    f[1 + j] = (p2[j] - c) >> 1;
-    par += f[1 + j];
-  }
-  f[0] = c;
-  int32_t z8 = (p2[7] - c) >> 1;
-  f[8] = (z8 - (par & 1)) >> 1;
-}
-
-inline int table_index(int field, int c) { return field == 0 ? 0 : 1 + 8 * c + field - 1; }
+// ---- lattice: em::d8_point, em::e8_point, em::split_fields (encode_math.h)
 
 // ---- model ---------------------------------------------------------------
 struct Table {
@@ -328,30 +257,81 @@ std::vector<int64_t> pick_rows(int64_t R, int64_t C, int64_t nominal_vectors) {
   return idx;
 }
 
-struct Encoder {
+// ---- backends -----------------------------------------------------------
+// The search, refit, table and serialisation logic below is shared; a
+// backend supplies the bulk work on its own device:
+//   prep      coded values, container scales delta_r and row RMS mu_r;
+//   quantize  fields of a row set at scale s, model extents, counts (when
+//             every field table fits `cap`), refit sums;
+//   rans      terminal states and words per tile;
+//   payload   the tiles' words at their offsets;
+//   errors    per-row squared errors and norms for the statistics.
+struct CpuBackend {
   const void* w;
   int dt;
   int64_t R, C, cvec;
-  ep_encode_params p;
   int T;
   std::vector<float> x;       // coded values (fp32-exact)
   std::vector<float> delta;   // container scales
   std::vector<double> mu;     // row RMS
+  std::vector<int32_t> sfl, fl;                  // sample / full fields, 9 per vector
+  std::vector<std::vector<uint16_t>> tile_words;
 
-  // quantise rows `rows` into fields fl (9 per vector); optional refit sums
-  void quantize(const std::vector<int64_t>& rows, double s, int32_t* fl, double* num,
-                double* den) {
-    parallel_for((int64_t)rows.size(), T, [&](int64_t b, int64_t e, int) {
+  int prep(int cont) {
+    const int64_t N = R * C;
+    x.resize((size_t)N);
+    delta.assign((size_t)R, 0.0f);
+    mu.resize((size_t)R);
+    std::vector<char> bad((size_t)R, 0);
+    parallel_for(R, T, [&](int64_t b, int64_t e, int) {
+      for (int64_t r = b; r < e; r++) {
+        double amax = 0;
+        float* xr = x.data() + r * C;
+        for (int64_t j = 0; j < C; j++) {
+          float v = (float)input_at(w, dt, r * C + j);
+          if (!std::isfinite(v)) bad[r] = 1;
+          xr[j] = v;
+          amax = std::max(amax, std::fabs((double)v));
+        }
+        if (cont) {
+          float d = amax > 0 ? (float)(amax / (cont == EP_CONT_FP8_ROW ? 448.0 : 127.0)) : 1.0f;
+          delta[r] = d;
+          for (int64_t j = 0; j < C; j++) {
+            double q = (double)xr[j] / (double)d;
+            double cv = cont == EP_CONT_FP8_ROW ? to_e4m3(q) : std::nearbyint(q);
+            if (cont == EP_CONT_INT8_ROW) cv = std::min(127.0, std::max(-127.0, cv));
+            xr[j] = (float)cv;
+          }
+        }
+        double ss = 0;
+        for (int64_t j = 0; j < C; j++) ss += (double)xr[j] * (double)xr[j];
+        double m = std::sqrt(ss / (double)C);
+        mu[r] = m > kEta ? m : kEta;
+      }
+    });
+    for (char c : bad)
+      if (c) return fail(EP_ERR_ARG, "ep_encode: non-finite input value");
+    return EP_OK;
+  }
+
+  // quantise rows (all rows when `rows` is null) into fields; optional refit sums
+  int quantize(const std::vector<int64_t>* rows, double s, Model& md, int64_t /*cap*/,
+               double* num, double* den) {
+    const int64_t nr = rows ? (int64_t)rows->size() : R;
+    std::vector<int32_t>& out = rows ? sfl : fl;
+    out.resize((size_t)(nr * cvec * 9));
+    int32_t* f9 = out.data();
+    parallel_for(nr, T, [&](int64_t b, int64_t e, int) {
       for (int64_t k = b; k < e; k++) {
-        int64_t r = rows[k];
+        int64_t r = rows ? (*rows)[k] : k;
         const float* xr = x.data() + r * C;
         double sn = 0, sd = 0;
         for (int64_t jv = 0; jv < cvec; jv++) {
           double y[8];
           int32_t p2[8];
           for (int j = 0; j < 8; j++) y[j] = ((double)xr[8 * jv + j] / mu[r]) / s;
-          e8_point(y, p2);
-          split_fields(p2, fl + 9 * (k * cvec + jv));
+          em::e8_point(y, p2);
+          em::split_fields(p2, f9 + 9 * (k * cvec + jv));
           if (num)
             for (int j = 0; j < 8; j++) {
               double pj = p2[j] / 2.0;
@@ -365,157 +345,27 @@ struct Encoder {
         }
       }
     });
+    md = Model();
+    count_fields(f9, nr * cvec, T, md);
+    return EP_OK;
   }
-};
 
-}  // namespace
-
-int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
-               ep_blob* out, ep_encode_stats* stats) {
-  if (!w || !prm || !out) return fail(EP_ERR_ARG, "ep_encode_cpu: null argument");
-  out->data = nullptr;
-  out->size = 0;
-  if (R <= 0 || C <= 0 || C % 8) return fail(EP_ERR_ARG, "ep_encode_cpu: need R, C > 0 and C % 8 == 0");
-  if (w_dtype != EP_BF16 && w_dtype != EP_FP16 && w_dtype != EP_FP32)
-    return fail(EP_ERR_ARG, "ep_encode_cpu: input dtype must be BF16, FP16 or FP32");
-  if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0 ||
-      prm->container < 0 || prm->container > 2 || !(prm->scale_lo > 0) ||
-      !(prm->scale_hi > prm->scale_lo) || prm->sample_vectors < 1 ||
-      (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)))
-    return fail(EP_ERR_ARG, "ep_encode_cpu: invalid parameters");
-  if (R > 0xFFFFFFFFll || C > 0xFFFFFFFFll || (R * C) / 8 > 0xFFFFFFFFll)
-    return fail(EP_ERR_ARG, "ep_encode_cpu: tensor too large");
-
-  try {
-    Encoder E;
-    E.w = w;
-    E.dt = w_dtype;
-    E.R = R;
-    E.C = C;
-    E.cvec = C / 8;
-    E.p = *prm;
-    int hw = (int)std::thread::hardware_concurrency();
-    E.T = prm->nthreads > 0 ? prm->nthreads : std::max(1, hw);
-    const int64_t N = R * C, nvec = N / 8;
-    const int cont = prm->container;
-    const uint32_t V = (uint32_t)prm->tile_vectors;
-
-    // input values, container route, row RMS (Section 3.2; App. A.6, B.1)
-    E.x.resize((size_t)N);
-    E.delta.assign((size_t)R, 0.0f);
-    E.mu.resize((size_t)R);
-    std::vector<char> bad((size_t)R, 0);
-    parallel_for(R, E.T, [&](int64_t b, int64_t e, int) {
-      for (int64_t r = b; r < e; r++) {
-        double amax = 0;
-        float* xr = E.x.data() + r * C;
-        for (int64_t j = 0; j < C; j++) {
-          float v = (float)input_at(w, w_dtype, r * C + j);
-          if (!std::isfinite(v)) bad[r] = 1;
-          xr[j] = v;
-          amax = std::max(amax, std::fabs((double)v));
-        }
-        if (cont) {
-          float d = amax > 0 ? (float)(amax / (cont == EP_CONT_FP8_ROW ? 448.0 : 127.0)) : 1.0f;
-          E.delta[r] = d;
-          for (int64_t j = 0; j < C; j++) {
-            double q = (double)xr[j] / (double)d;
-            double cv = cont == EP_CONT_FP8_ROW ? to_e4m3(q) : std::nearbyint(q);
-            if (cont == EP_CONT_INT8_ROW) cv = std::min(127.0, std::max(-127.0, cv));
-            xr[j] = (float)cv;
-          }
-        }
-        double ss = 0;
-        for (int64_t j = 0; j < C; j++) ss += (double)xr[j] * (double)xr[j];
-        double m = std::sqrt(ss / (double)C);
-        E.mu[r] = m > kEta ? m : kEta;
-      }
-    });
-    for (char c : bad)
-      if (c) return fail(EP_ERR_ARG, "ep_encode_cpu: non-finite input value");
-
-    // scale search on a fixed row sample (Alg. rate selection; App. C.1)
-    std::vector<int64_t> srows = pick_rows(R, C, prm->sample_vectors);
-    std::vector<int64_t> all((size_t)R);
-    for (int64_t r = 0; r < R; r++) all[r] = r;
-    const int64_t snv = (int64_t)srows.size() * E.cvec;
-    const uint64_t stiles = ((uint64_t)snv + V - 1) / V;
-    const double nsub = (double)((int64_t)srows.size() * C);
-    std::vector<int32_t> sfl((size_t)snv * 9);
-    std::vector<int32_t> fl((size_t)nvec * 9);
-    std::vector<double> num((size_t)R), den((size_t)R);
-
-    const int b_first = prm->prob_bits ? prm->prob_bits : (prm->target_bpp <= 7.0 ? 11 : 12);
-    int b = b_first;
-    double s = 1.0, rhat = 0;
-    uint32_t escal = 0, coarse = 0;
-    bool fits = false;
-    Model full;
-    for (; b <= 15 && !fits; b++) {
-      double lo = prm->scale_lo, hi = prm->scale_hi;
-      for (int it = 0; it < prm->search_steps; it++) {
-        s = std::sqrt(lo * hi);
-        E.quantize(srows, s, sfl.data(), nullptr, nullptr);
-        Model sm;
-        count_fields(sfl.data(), snv, E.T, sm);
-        if (sm.max_field_alphabet() > (1 << b)) {
-          rhat = std::numeric_limits<double>::infinity();
-        } else {
-          for (auto& tb : sm.t) quantize_freqs(tb, b);
-          rhat = estimated_bits(model_bits(sm, b), stiles, prm->state_credit_bits, sm,
-                                srows.size(), cont) / nsub;
-        }
-        if (rhat > prm->target_bpp) lo = s;
-        else hi = s;
-      }
-      s = std::sqrt(lo * hi);
-      E.quantize(all, s, fl.data(), num.data(), den.data());
-      full = Model();
-      count_fields(fl.data(), nvec, E.T, full);
-      fits = full.max_field_alphabet() <= (1 << b);
-      if (!fits) escal++;
-    }
-    if (fits) b--;  // the loop advanced past the accepted precision
-    else {
-      b = 15;
-      while (full.max_field_alphabet() > (1 << b)) {
-        s = 1.05 * s * (double)full.max_field_alphabet() / (double)(1 << b);
-        E.quantize(all, s, fl.data(), num.data(), den.data());
-        full = Model();
-        count_fields(fl.data(), nvec, E.T, full);
-        coarse++;
-      }
-    }
-    for (auto& tb : full.t) quantize_freqs(tb, b);
-
-    // row reconstruction scales (eq. scale_fit)
-    std::vector<float> sigma((size_t)R);
-    for (int64_t r = 0; r < R; r++) {
-      double sg;
-      if (den[r] > 0) {
-        sg = num[r] / den[r];
-        if (sg < kEta) sg = kEta;
-      } else {
-        sg = s * E.mu[r];
-      }
-      sigma[r] = (float)sg;
-    }
-
-    // interleaved rANS per tile (eq. rans_encode; App. C.3)
-    const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
+  int rans(const Model& full, int b, uint32_t V, uint64_t tiles, std::vector<uint32_t>& states,
+           std::vector<uint64_t>& words) {
+    const uint64_t nvec = (uint64_t)(R * cvec);
     const uint32_t M = 1u << b;
     std::vector<std::vector<uint32_t>> cum(kTables);
     for (int i = 0; i < kTables; i++) {
       cum[i].assign((size_t)full.t[i].A + 1, 0);
       for (int32_t z = 0; z < full.t[i].A; z++) cum[i][z + 1] = cum[i][z] + full.t[i].f[z];
     }
-    std::vector<uint32_t> states(tiles * kLanes);
-    std::vector<std::vector<uint16_t>> tile_words(tiles);
-    std::vector<double> sbits(tiles, 0.0);
-    parallel_for((int64_t)tiles, E.T, [&](int64_t tb, int64_t te, int) {
+    states.assign(tiles * kLanes, 0);
+    words.assign(tiles, 0);
+    tile_words.assign(tiles, {});
+    parallel_for((int64_t)tiles, T, [&](int64_t tb, int64_t te, int) {
       for (int64_t t = tb; t < te; t++) {
         uint64_t v0 = (uint64_t)t * V;
-        uint64_t nv = std::min<uint64_t>(V, (uint64_t)nvec - v0);
+        uint64_t nv = std::min<uint64_t>(V, nvec - v0);
         uint64_t rounds = (nv + kLanes - 1) / kLanes;
         uint32_t st[kLanes];
         for (auto& q : st) q = kStateLow;
@@ -539,128 +389,261 @@ int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
           }
         }
         std::reverse(out_w.begin(), out_w.end());
-        double acc = 0;
-        for (uint32_t l = 0; l < kLanes; l++) {
-          states[t * kLanes + l] = st[l];
-          acc += std::log2((double)st[l] / (double)kStateLow);
-        }
-        sbits[t] = acc;
+        for (uint32_t l = 0; l < kLanes; l++) states[t * kLanes + l] = st[l];
+        words[t] = out_w.size();
       }
     });
-    uint64_t words = 0;
-    std::vector<uint32_t> offs(tiles + 1);
-    for (uint64_t t = 0; t < tiles; t++) {
-      offs[t] = (uint32_t)words;
-      words += tile_words[t].size();
-      if (words > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_encode_cpu: payload too large");
-    }
-    offs[tiles] = (uint32_t)words;
+    return EP_OK;
+  }
 
-    // serialise
-    Layout L = layout_of((uint32_t)R, (uint32_t)full.serialized_bytes(), (uint32_t)tiles,
-                         (uint32_t)cont, (uint32_t)words);
-    uint8_t* blob = static_cast<uint8_t*>(std::calloc((size_t)L.total, 1));
-    if (!blob) return fail(EP_ERR_NOMEM, "ep_encode_cpu: out of host memory");
-    auto w32 = [&](uint64_t off, uint32_t v) { std::memcpy(blob + off, &v, 4); };
-    w32(0, kMagic);
-    w32(4, kVersion);
-    w32(8, (uint32_t)R);
-    w32(12, (uint32_t)C);
-    w32(16, (uint32_t)b);
-    w32(20, V);
-    w32(24, (uint32_t)tiles);
-    w32(28, (uint32_t)cont);
-    w32(32, (uint32_t)full.serialized_bytes());
-    w32(36, (uint32_t)words);
-    std::memcpy(blob + 40, &L.total, 8);
-    uint8_t* q = blob + L.off_tables;
-    uint16_t cf[2] = {(uint16_t)full.t[0].f[0], (uint16_t)full.t[0].f[1]};
-    std::memcpy(q, cf, 4);
-    q += 4;
-    for (int i = 1; i < kTables; i++) {
-      const Table& tb = full.t[i];
-      std::memcpy(q, &tb.lo, 4);
-      uint32_t A = (uint32_t)tb.A;
-      std::memcpy(q + 4, &A, 4);
-      for (int32_t z = 0; z < tb.A; z++) {
-        uint16_t v = (uint16_t)tb.f[z];
-        std::memcpy(q + 8 + 2 * z, &v, 2);
-      }
-      q += 8 + ((2ull * A + 3) / 4) * 4;
-    }
-    std::memcpy(blob + L.off_sigma, sigma.data(), 4 * (size_t)R);
-    if (cont) std::memcpy(blob + L.off_delta, E.delta.data(), 4 * (size_t)R);
-    std::memcpy(blob + L.off_states, states.data(), 4 * states.size());
-    std::memcpy(blob + L.off_offsets, offs.data(), 4 * offs.size());
-    parallel_for((int64_t)tiles, E.T, [&](int64_t tb, int64_t te, int) {
+  int payload(uint8_t* dst, const std::vector<uint32_t>& offs) {
+    parallel_for((int64_t)tile_words.size(), T, [&](int64_t tb, int64_t te, int) {
       for (int64_t t = tb; t < te; t++)
         if (!tile_words[t].empty())
-          std::memcpy(blob + L.off_payload + 2ull * offs[t], tile_words[t].data(),
-                      2 * tile_words[t].size());
+          std::memcpy(dst + 2ull * offs[t], tile_words[t].data(), 2 * tile_words[t].size());
     });
-    out->data = blob;
-    out->size = L.total;
-
-    if (stats) {
-      // reconstruction error in the dtype of the coded values
-      int rdt = cont == EP_CONT_FP8_ROW ? EP_FP8_E4M3 : cont == EP_CONT_INT8_ROW ? EP_INT8 : w_dtype;
-      std::vector<double> acc((size_t)R * 4, 0.0);
-      std::vector<int32_t> p2((size_t)8);
-      parallel_for(R, E.T, [&](int64_t rb, int64_t re, int) {
-        for (int64_t r = rb; r < re; r++) {
-          double ec = 0, rc = 0, eo = 0, ro = 0;
-          for (int64_t jv = 0; jv < E.cvec; jv++) {
-            const int32_t* f = fl.data() + 9 * (r * E.cvec + jv);
-            int32_t par = 0, two[8];
-            for (int j = 0; j < 7; j++) {
-              par += f[1 + j];
-              two[j] = 2 * f[1 + j] + f[0];
-            }
-            two[7] = 2 * (2 * f[8] + (par & 1)) + f[0];
-            for (int j = 0; j < 8; j++) {
-              double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
-              double v = rdt == EP_BF16 ? to_bf16(y) : rdt == EP_FP16 ? to_fp16(y)
-                       : rdt == EP_FP8_E4M3 ? to_e4m3(y) : rdt == EP_INT8 ? int8_snap(y) : y;
-              double xc = E.x[r * C + 8 * jv + j];
-              ec += (v - xc) * (v - xc);
-              rc += xc * xc;
-              double wo = (double)(float)input_at(w, w_dtype, r * C + 8 * jv + j);
-              double vo = cont ? v * (double)E.delta[r] : v;
-              eo += (vo - wo) * (vo - wo);
-              ro += wo * wo;
-            }
-          }
-          acc[4 * r] = ec;
-          acc[4 * r + 1] = rc;
-          acc[4 * r + 2] = eo;
-          acc[4 * r + 3] = ro;
-        }
-      });
-      double ec = 0, rc = 0, eo = 0, ro = 0, sb = 0;
-      for (int64_t r = 0; r < R; r++) {
-        ec += acc[4 * r];
-        rc += acc[4 * r + 1];
-        eo += acc[4 * r + 2];
-        ro += acc[4 * r + 3];
-      }
-      for (double v : sbits) sb += v;
-      stats->scale = s;
-      stats->rate_estimate_sample = rhat;
-      stats->rate_stored = 8.0 * (double)L.total / (double)N;
-      stats->code_length_bits = model_bits(full, b);
-      stats->erel_coded = rc > 0 ? std::sqrt(ec / rc) : 0;
-      stats->erel_original = ro > 0 ? std::sqrt(eo / ro) : 0;
-      stats->mean_state_bits = sb / (double)(tiles * kLanes);
-      stats->bytes = L.total;
-      stats->payload_bits = 16ull * words;
-      stats->prob_bits = (uint32_t)b;
-      stats->n_tiles = (uint32_t)tiles;
-      stats->max_alphabet = (uint32_t)full.max_field_alphabet();
-      stats->sample_rows = (uint32_t)srows.size();
-      stats->escalations = escal;
-      stats->coarsenings = coarse;
-    }
     return EP_OK;
+  }
+
+  // per row: squared error and norm in coded units, then against the input
+  int errors(const std::vector<float>& sigma, int rdt, int cont, std::vector<double>& acc) {
+    acc.assign((size_t)R * 4, 0.0);
+    parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
+      for (int64_t r = rb; r < re; r++) {
+        double ec = 0, rc = 0, eo = 0, ro = 0;
+        for (int64_t jv = 0; jv < cvec; jv++) {
+          int32_t two[8];
+          em::join_fields(fl.data() + 9 * (r * cvec + jv), two);
+          for (int j = 0; j < 8; j++) {
+            double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
+            double v = rdt == EP_BF16 ? to_bf16(y) : rdt == EP_FP16 ? to_fp16(y)
+                     : rdt == EP_FP8_E4M3 ? to_e4m3(y) : rdt == EP_INT8 ? int8_snap(y) : y;
+            double xc = x[r * C + 8 * jv + j];
+            ec += (v - xc) * (v - xc);
+            rc += xc * xc;
+            double wo = (double)(float)input_at(w, dt, r * C + 8 * jv + j);
+            double vo = cont ? v * (double)delta[r] : v;
+            eo += (vo - wo) * (vo - wo);
+            ro += wo * wo;
+          }
+        }
+        acc[4 * r] = ec;
+        acc[4 * r + 1] = rc;
+        acc[4 * r + 2] = eo;
+        acc[4 * r + 3] = ro;
+      }
+    });
+    return EP_OK;
+  }
+};
+
+int check_args(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
+               ep_blob* out) {
+  if (!w || !prm || !out) return fail(EP_ERR_ARG, "ep_encode: null argument");
+  out->data = nullptr;
+  out->size = 0;
+  if (R <= 0 || C <= 0 || C % 8) return fail(EP_ERR_ARG, "ep_encode: need R, C > 0 and C % 8 == 0");
+  if (w_dtype != EP_BF16 && w_dtype != EP_FP16 && w_dtype != EP_FP32)
+    return fail(EP_ERR_ARG, "ep_encode: input dtype must be BF16, FP16 or FP32");
+  if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0 ||
+      prm->container < 0 || prm->container > 2 || !(prm->scale_lo > 0) ||
+      !(prm->scale_hi > prm->scale_lo) || prm->sample_vectors < 1 ||
+      (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)))
+    return fail(EP_ERR_ARG, "ep_encode: invalid parameters");
+  if (R > 0xFFFFFFFFll || C > 0xFFFFFFFFll || (R * C) / 8 > 0xFFFFFFFFll)
+    return fail(EP_ERR_ARG, "ep_encode: tensor too large");
+  return EP_OK;
+}
+
+#define EP_TRY(call)          \
+  do {                        \
+    int rc_ = (call);         \
+    if (rc_ != EP_OK) return rc_; \
+  } while (0)
+
+template <class BK>
+int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
+                ep_blob* out, ep_encode_stats* stats) {
+  const int64_t N = R * C, nvec = N / 8;
+  const int cont = prm->container;
+  const uint32_t V = (uint32_t)prm->tile_vectors;
+
+  // input values, container route, row RMS (Section 3.2; App. A.6, B.1)
+  EP_TRY(E.prep(cont));
+
+  // scale search on a fixed row sample (Alg. rate selection; App. C.1)
+  std::vector<int64_t> srows = pick_rows(R, C, prm->sample_vectors);
+  const bool sample_all = (int64_t)srows.size() == R;
+  const int64_t snv = (int64_t)srows.size() * (C / 8);
+  const uint64_t stiles = ((uint64_t)snv + V - 1) / V;
+  const double nsub = (double)((int64_t)srows.size() * C);
+  std::vector<double> num((size_t)R), den((size_t)R);
+
+  const int b_first = prm->prob_bits ? prm->prob_bits : (prm->target_bpp <= 7.0 ? 11 : 12);
+  int b = b_first;
+  double s = 1.0, rhat = 0;
+  uint32_t escal = 0, coarse = 0;
+  bool fits = false;
+  Model full;
+  for (; b <= 15 && !fits; b++) {
+    double lo = prm->scale_lo, hi = prm->scale_hi;
+    for (int it = 0; it < prm->search_steps; it++) {
+      s = std::sqrt(lo * hi);
+      Model sm;
+      EP_TRY(E.quantize(sample_all ? nullptr : &srows, s, sm, 1 << b, nullptr, nullptr));
+      if (sm.max_field_alphabet() > (1 << b)) {
+        rhat = std::numeric_limits<double>::infinity();
+      } else {
+        for (auto& tb : sm.t) quantize_freqs(tb, b);
+        rhat = estimated_bits(model_bits(sm, b), stiles, prm->state_credit_bits, sm,
+                              srows.size(), cont) / nsub;
+      }
+      if (rhat > prm->target_bpp) lo = s;
+      else hi = s;
+    }
+    s = std::sqrt(lo * hi);
+    EP_TRY(E.quantize(nullptr, s, full, 1 << b, num.data(), den.data()));
+    fits = full.max_field_alphabet() <= (1 << b);
+    if (!fits) escal++;
+  }
+  if (fits) b--;  // the loop advanced past the accepted precision
+  else {
+    b = 15;
+    while (full.max_field_alphabet() > (1 << b)) {
+      s = 1.05 * s * (double)full.max_field_alphabet() / (double)(1 << b);
+      EP_TRY(E.quantize(nullptr, s, full, 1 << b, num.data(), den.data()));
+      coarse++;
+    }
+  }
+  for (auto& tb : full.t) quantize_freqs(tb, b);
+
+  // row reconstruction scales (eq. scale_fit)
+  std::vector<float> sigma((size_t)R);
+  for (int64_t r = 0; r < R; r++) {
+    double sg;
+    if (den[r] > 0) {
+      sg = num[r] / den[r];
+      if (sg < kEta) sg = kEta;
+    } else {
+      sg = s * E.mu[r];
+    }
+    sigma[r] = (float)sg;
+  }
+
+  // interleaved rANS per tile (eq. rans_encode; App. C.3)
+  const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
+  std::vector<uint32_t> states;
+  std::vector<uint64_t> tw;
+  EP_TRY(E.rans(full, b, V, tiles, states, tw));
+  uint64_t words = 0;
+  std::vector<uint32_t> offs(tiles + 1);
+  for (uint64_t t = 0; t < tiles; t++) {
+    offs[t] = (uint32_t)words;
+    words += tw[t];
+    if (words > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_encode: payload too large");
+  }
+  offs[tiles] = (uint32_t)words;
+
+  // serialise
+  Layout L = layout_of((uint32_t)R, (uint32_t)full.serialized_bytes(), (uint32_t)tiles,
+                       (uint32_t)cont, (uint32_t)words);
+  uint8_t* blob = static_cast<uint8_t*>(std::calloc((size_t)L.total, 1));
+  if (!blob) return fail(EP_ERR_NOMEM, "ep_encode: out of host memory");
+  auto w32 = [&](uint64_t off, uint32_t v) { std::memcpy(blob + off, &v, 4); };
+  w32(0, kMagic);
+  w32(4, kVersion);
+  w32(8, (uint32_t)R);
+  w32(12, (uint32_t)C);
+  w32(16, (uint32_t)b);
+  w32(20, V);
+  w32(24, (uint32_t)tiles);
+  w32(28, (uint32_t)cont);
+  w32(32, (uint32_t)full.serialized_bytes());
+  w32(36, (uint32_t)words);
+  std::memcpy(blob + 40, &L.total, 8);
+  uint8_t* q = blob + L.off_tables;
+  uint16_t cf[2] = {(uint16_t)full.t[0].f[0], (uint16_t)full.t[0].f[1]};
+  std::memcpy(q, cf, 4);
+  q += 4;
+  for (int i = 1; i < kTables; i++) {
+    const Table& tb = full.t[i];
+    std::memcpy(q, &tb.lo, 4);
+    uint32_t A = (uint32_t)tb.A;
+    std::memcpy(q + 4, &A, 4);
+    for (int32_t z = 0; z < tb.A; z++) {
+      uint16_t v = (uint16_t)tb.f[z];
+      std::memcpy(q + 8 + 2 * z, &v, 2);
+    }
+    q += 8 + ((2ull * A + 3) / 4) * 4;
+  }
+  std::memcpy(blob + L.off_sigma, sigma.data(), 4 * (size_t)R);
+  if (cont) std::memcpy(blob + L.off_delta, E.delta.data(), 4 * (size_t)R);
+  std::memcpy(blob + L.off_states, states.data(), 4 * states.size());
+  std::memcpy(blob + L.off_offsets, offs.data(), 4 * offs.size());
+  int rc = E.payload(blob + L.off_payload, offs);
+  if (rc != EP_OK) {
+    std::free(blob);
+    return rc;
+  }
+
+  if (stats) {
+    // reconstruction error in the dtype of the coded values
+    int rdt = cont == EP_CONT_FP8_ROW ? EP_FP8_E4M3 : cont == EP_CONT_INT8_ROW ? EP_INT8 : w_dtype;
+    std::vector<double> acc;
+    rc = E.errors(sigma, rdt, cont, acc);
+    if (rc != EP_OK) {
+      std::free(blob);
+      return rc;
+    }
+    double ec = 0, rc2 = 0, eo = 0, ro = 0, sb = 0;
+    for (int64_t r = 0; r < R; r++) {
+      ec += acc[4 * r];
+      rc2 += acc[4 * r + 1];
+      eo += acc[4 * r + 2];
+      ro += acc[4 * r + 3];
+    }
+    for (uint64_t t = 0; t < tiles; t++) {
+      double a = 0;
+      for (uint32_t l = 0; l < kLanes; l++)
+        a += std::log2((double)states[t * kLanes + l] / (double)kStateLow);
+      sb += a;
+    }
+    stats->scale = s;
+    stats->rate_estimate_sample = rhat;
+    stats->rate_stored = 8.0 * (double)L.total / (double)N;
+    stats->code_length_bits = model_bits(full, b);
+    stats->erel_coded = rc2 > 0 ? std::sqrt(ec / rc2) : 0;
+    stats->erel_original = ro > 0 ? std::sqrt(eo / ro) : 0;
+    stats->mean_state_bits = sb / (double)(tiles * kLanes);
+    stats->bytes = L.total;
+    stats->payload_bits = 16ull * words;
+    stats->prob_bits = (uint32_t)b;
+    stats->n_tiles = (uint32_t)tiles;
+    stats->max_alphabet = (uint32_t)full.max_field_alphabet();
+    stats->sample_rows = (uint32_t)srows.size();
+    stats->escalations = escal;
+    stats->coarsenings = coarse;
+  }
+  out->data = blob;
+  out->size = L.total;
+  return EP_OK;
+}
+
+}  // namespace
+
+int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
+               ep_blob* out, ep_encode_stats* stats) {
+  EP_TRY(check_args(w, w_dtype, R, C, prm, out));
+  try {
+    CpuBackend E;
+    E.w = w;
+    E.dt = w_dtype;
+    E.R = R;
+    E.C = C;
+    E.cvec = C / 8;
+    int hw = (int)std::thread::hardware_concurrency();
+    E.T = prm->nthreads > 0 ? prm->nthreads : std::max(1, hw);
+    return encode_impl(E, w_dtype, R, C, prm, out, stats);
   } catch (const std::bad_alloc&) {
     return fail(EP_ERR_NOMEM, "ep_encode_cpu: out of host memory");
   }
