@@ -5,7 +5,8 @@
  * as row-normalised E8 lattice points written as integer fields
  * (c, z1..z7, m) and coded with 32-state interleaved rANS in independently
  * decodable tiles (Sections 3.2-3.6, Appendix C.3).  This library provides
- *   - a CPU encoder (ep_encode_cpu),
+ *   - a CPU encoder (ep_encode_cpu) and the same encoder with its bulk passes
+ *     on the GPU (ep_encode_gpu),
  *   - validation/inspection of an encoded blob on the host (ep_blob_info),
  *   - fused GPU decode on gfx950: rANS symbol decode with the coset-conditional
  *     tables, field inverse, row rescale and dtype snap, with no intermediate
@@ -20,7 +21,8 @@
  *     current HIP device; all other pointers are host pointers.
  *   - GPU calls are asynchronous on the given hipStream_t (passed as void*,
  *     NULL = default stream).  They allocate no device memory and never
- *     synchronise; the caller owns every buffer.
+ *     synchronise; the caller owns every buffer.  The one exception is the
+ *     GPU encoder (ep_encode_gpu), which returns a finished host blob.
  *   - Outputs must not alias the blob or each other.
  *
  * Stored representation (all little-endian; every section starts on a 4-byte
@@ -132,6 +134,20 @@ void ep_encode_params_default(ep_encode_params* p);
  * target <= 0, bad parameters), EP_ERR_NOMEM. */
 int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
                   const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats);
+
+/* The same encoder with its bulk passes on the GPU (quantisation, counts,
+ * refit sums, rANS, statistics; the scale search and table normalisation run
+ * on the host between passes).  d_w is a device array (R x C, same dtypes);
+ * the result is a host blob byte-identical to ep_encode_cpu's for the same
+ * inputs and parameters (nthreads is ignored), and *stats (nullable) equal to
+ * its statistics.  Unlike the decode entry points it allocates device scratch
+ * (about 10 bytes per weight for the values, fields and rANS words) and frees
+ * it before returning, and it synchronises hip_stream: on return the blob is
+ * complete.  Errors: as ep_encode_cpu, plus EP_ERR_HIP (device allocation or
+ * launch failure) and EP_ERR_UNSUPPORTED (R >= 2^31). */
+int ep_encode_gpu(const void* d_w, int w_dtype, int64_t rows, int64_t cols,
+                  const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats,
+                  void* hip_stream);
 void ep_blob_free(ep_blob* blob);
 
 /* ---- inspection ---------------------------------------------------------- */

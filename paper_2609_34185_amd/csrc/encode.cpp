@@ -25,6 +25,7 @@
 
 #include "../../include/entropack.h"
 #include "common.h"
+#include "encode_gpu.h"
 #include "encode_math.h"
 
 namespace ep {
@@ -257,6 +258,12 @@ std::vector<int64_t> pick_rows(int64_t R, int64_t C, int64_t nominal_vectors) {
   return idx;
 }
 
+#define EP_TRY_G(call)          \
+  do {                          \
+    int rcg_ = (call);          \
+    if (rcg_ != EP_OK) return rcg_; \
+  } while (0)
+
 // ---- backends -----------------------------------------------------------
 // The search, refit, table and serialisation logic below is shared; a
 // backend supplies the bulk work on its own device:
@@ -434,6 +441,78 @@ struct CpuBackend {
       }
     });
     return EP_OK;
+  }
+};
+
+// Bulk passes on the GPU (encode_gpu.hip); extents come back from the
+// quantisation pass, counts only when every field table fits `cap` (the
+// search discards the counts otherwise).
+struct GpuBackend {
+  genc::Ctx* c = nullptr;
+  int64_t R = 0;
+  std::vector<float> delta;
+  std::vector<double> mu;
+  ~GpuBackend() { genc::close(c); }
+
+  int prep(int) {
+    delta.resize((size_t)R);
+    mu.resize((size_t)R);
+    return genc::prep(c, delta.data(), mu.data());
+  }
+
+  int quantize(const std::vector<int64_t>* rows, double s, Model& md, int64_t cap, double* num,
+               double* den) {
+    int32_t lohi[2 * kTables];
+    EP_TRY_G(genc::quantize(c, rows ? rows->data() : nullptr, rows ? (int64_t)rows->size() : R, s, lohi));
+    md = Model();
+    int32_t lo[kTables], A[kTables];
+    for (int i = 0; i < kTables; i++) {
+      int32_t l = i ? lohi[2 * i] : 0, h = i ? lohi[2 * i + 1] : 1;
+      Table& tb = md.t[i];
+      tb.lo = h >= l ? l : 0;
+      tb.A = h >= l ? (int32_t)((int64_t)h - l + 1) : 0;
+      lo[i] = tb.lo;
+      A[i] = tb.A;
+    }
+    if (md.max_field_alphabet() <= cap) {
+      uint64_t cells = 0;
+      for (int i = 0; i < kTables; i++) cells += (uint64_t)A[i];
+      std::vector<uint64_t> n(cells);
+      EP_TRY_G(genc::count(c, rows != nullptr, lo, A, n.data()));
+      uint64_t at = 0;
+      for (int i = 0; i < kTables; i++) {
+        Table& tb = md.t[i];
+        tb.n.assign(n.begin() + at, n.begin() + at + tb.A);
+        tb.f.assign((size_t)tb.A, 0);
+        at += tb.A;
+      }
+    }
+    if (num) EP_TRY_G(genc::refit(c, num, den));
+    return EP_OK;
+  }
+
+  int rans(const Model& full, int b, uint32_t V, uint64_t tiles, std::vector<uint32_t>& states,
+           std::vector<uint64_t>& words) {
+    int32_t lo[kTables], A[kTables];
+    std::vector<uint32_t> f;
+    for (int i = 0; i < kTables; i++) {
+      lo[i] = full.t[i].lo;
+      A[i] = full.t[i].A;
+      f.insert(f.end(), full.t[i].f.begin(), full.t[i].f.end());
+    }
+    states.assign(tiles * kLanes, 0);
+    words.assign(tiles, 0);
+    return genc::rans(c, b, V, tiles, lo, A, f.data(), states.data(), words.data());
+  }
+
+  int payload(uint8_t* dst, const std::vector<uint32_t>& offs) {
+    const uint64_t tiles = offs.size() - 1;
+    return genc::payload(c, offs.data(), tiles, offs[tiles], dst);
+  }
+
+  int errors(const std::vector<float>& sigma, int rdt, int, std::vector<double>& acc) {
+    acc.assign((size_t)R * 4, 0.0);
+    return genc::errors(c, sigma.data(), rdt, acc.data());
   }
 };
 
@@ -649,6 +728,19 @@ int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
   }
 }
 
+int encode_gpu(const void* d_w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
+               ep_blob* out, ep_encode_stats* stats, void* stream) {
+  EP_TRY(check_args(d_w, w_dtype, R, C, prm, out));
+  try {
+    GpuBackend E;
+    E.R = R;
+    EP_TRY(genc::open(&E.c, d_w, w_dtype, R, C, prm->container, stream));
+    return encode_impl(E, w_dtype, R, C, prm, out, stats);
+  } catch (const std::bad_alloc&) {
+    return fail(EP_ERR_NOMEM, "ep_encode_gpu: out of host memory");
+  }
+}
+
 }  // namespace ep
 
 extern "C" {
@@ -671,6 +763,12 @@ void ep_encode_params_default(ep_encode_params* p) {
 int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
                   const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats) {
   return ep::encode_cpu(w, w_dtype, rows, cols, params, out, stats);
+}
+
+int ep_encode_gpu(const void* d_w, int w_dtype, int64_t rows, int64_t cols,
+                  const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats,
+                  void* hip_stream) {
+  return ep::encode_gpu(d_w, w_dtype, rows, cols, params, out, stats, hip_stream);
 }
 
 void ep_blob_free(ep_blob* blob) {

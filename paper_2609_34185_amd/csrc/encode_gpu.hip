@@ -1,0 +1,558 @@
+// GPU encoder passes on gfx950 (declared in encode_gpu.h).
+//
+// The bulk of encoding runs here: input conversion and the container route
+// (App. A.6, B.1), the row RMS (Section 3.2), nearest-E8 quantisation and the
+// field map of every vector at a trial or final scale (Section 3.2, eqs. d8,
+// parity), per-table extents and counts (Section 3.3), the refit sums
+// (eq. scale_fit), the 32-state interleaved rANS encode of every tile (eq.
+// rans_encode, App. C.3) and the per-row error sums of the statistics.  The
+// per-value arithmetic is the CPU encoder's own (encode_math.h) compiled for
+// the device, and every sum that rounds is accumulated in the CPU encoder's
+// element order, so the blob is byte-identical to the CPU encoder's.
+//
+// Mapping: element-wise passes take one thread per vector (or a workgroup
+// per row for the conversion); passes whose double sums must follow element
+// order (row RMS, refit, errors) take one thread per row; counts go through a
+// workgroup histogram in LDS when all tables fit (else straight to memory);
+// the rANS encode runs two tiles per wave, one per half, each lane one state,
+// words placed by a 32-lane ballot in the order the decoder consumes them.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "../../include/entropack.h"
+#include "common.h"
+#include "encode_gpu.h"
+#include "encode_math.h"
+
+namespace ep {
+namespace genc {
+namespace {
+
+constexpr int kTablesN = 17;
+constexpr uint32_t kLanesN = 32;
+constexpr uint32_t kLdsBins = 36864;   // histogram in LDS when all tables fit (144 KiB)
+
+__device__ __forceinline__ float load_input(const void* w, int dt, int64_t i) {
+  if (dt == EP_FP32) return static_cast<const float*>(w)[i];
+  const uint16_t h = static_cast<const uint16_t*>(w)[i];
+  if (dt == EP_FP16) return (float)__builtin_bit_cast(_Float16, h);
+  return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+// One workgroup per row: input -> coded values (container route), delta_r.
+__global__ __launch_bounds__(256) void k_prep_rows(const void* w, int dt, int64_t C, int cont,
+                                                   float* x, float* delta, int* bad) {
+  __shared__ double s_amax[256];
+  __shared__ int s_bad;
+  const int64_t r = blockIdx.x, base = r * C;
+  const int t = threadIdx.x;
+  if (t == 0) s_bad = 0;
+  __syncthreads();
+  double amax = 0;
+  int nb = 0;
+  for (int64_t j = t; j < C; j += 256) {
+    const float v = load_input(w, dt, base + j);
+    if (!__builtin_isfinite(v)) nb = 1;
+    const double a = __builtin_fabs((double)v);
+    if (a > amax) amax = a;
+    if (!cont) x[base + j] = v;
+  }
+  if (nb) s_bad = 1;
+  s_amax[t] = amax;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (t < h && s_amax[t + h] > s_amax[t]) s_amax[t] = s_amax[t + h];
+    __syncthreads();
+  }
+  if (t == 0 && s_bad) atomicOr(bad, 1);
+  if (!cont) return;
+  amax = s_amax[0];
+  const float d = amax > 0 ? (float)(amax / (cont == EP_CONT_FP8_ROW ? 448.0 : 127.0)) : 1.0f;
+  if (t == 0) delta[r] = d;
+  for (int64_t j = t; j < C; j += 256) {
+    const double q = (double)load_input(w, dt, base + j) / (double)d;
+    double cv = cont == EP_CONT_FP8_ROW ? em::to_e4m3(q) : __builtin_rint(q);
+    if (cont == EP_CONT_INT8_ROW) cv = cv > 127.0 ? 127.0 : (cv < -127.0 ? -127.0 : cv);
+    x[base + j] = (float)cv;
+  }
+}
+
+// One thread per row: mu_r = max(sqrt(sum x^2 / C), eta), summed in element order.
+__global__ void k_prep_mu(const float* x, int64_t R, int64_t C, double* mu) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const float* xr = x + r * C;
+  double ss = 0;
+  for (int64_t j = 0; j < C; j++) ss += (double)xr[j] * (double)xr[j];
+  const double m = __builtin_sqrt(ss / (double)C);
+  mu[r] = m > em::kEta ? m : em::kEta;
+}
+
+// One thread per vector: fields at scale s, table extents.
+__global__ __launch_bounds__(256) void k_quantize(const float* x, const double* mu,
+                                                  const int64_t* rows, int64_t nrows, int64_t cvec,
+                                                  int64_t C, double s, int32_t* fl, int32_t* lohi) {
+  __shared__ int32_t s_lo[16], s_hi[16];
+  const int t = threadIdx.x;
+  if (t < 16) {
+    s_lo[t] = INT_MAX;
+    s_hi[t] = INT_MIN;
+  }
+  __syncthreads();
+  const int64_t id = (int64_t)blockIdx.x * 256 + t;
+  if (id < nrows * cvec) {
+    const int64_t k = id / cvec, jv = id - k * cvec;
+    const int64_t r = rows ? rows[k] : k;
+    const float4* xv = reinterpret_cast<const float4*>(x + r * C + 8 * jv);
+    const float4 a = xv[0], b = xv[1];
+    const float xs[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    const double m = mu[r];
+    double y[8];
+    for (int j = 0; j < 8; j++) y[j] = ((double)xs[j] / m) / s;
+    int32_t p2[8], f[9];
+    em::e8_point(y, p2);
+    em::split_fields(p2, f);
+    int32_t* o = fl + 9 * id;
+    for (int i = 0; i < 9; i++) o[i] = f[i];
+    for (int i = 1; i <= 8; i++) {
+      const int ti = em::table_index(i, f[0]) - 1;
+      atomicMin(&s_lo[ti], f[i]);
+      atomicMax(&s_hi[ti], f[i]);
+    }
+  }
+  __syncthreads();
+  if (t < 16 && s_lo[t] <= s_hi[t]) {
+    atomicMin(&lohi[2 * (t + 1)], s_lo[t]);
+    atomicMax(&lohi[2 * (t + 1) + 1], s_hi[t]);
+  }
+}
+
+struct TableDesc {
+  int32_t lo[kTablesN];
+  uint32_t base[kTablesN];
+};
+
+__device__ __forceinline__ uint32_t bin_of(const TableDesc& td, const int32_t* q, int i) {
+  if (i == 0) return (uint32_t)q[0];
+  const int ti = em::table_index(i, q[0]);
+  return td.base[ti] + (uint32_t)(q[i] - td.lo[ti]);
+}
+
+// Counts with a workgroup histogram in LDS (cells <= kLdsBins).
+__global__ __launch_bounds__(256) void k_count_lds(const int32_t* fl, int64_t nv, TableDesc td,
+                                                   uint32_t cells, uint32_t* counts) {
+  extern __shared__ uint32_t h[];
+  for (uint32_t i = threadIdx.x; i < cells; i += 256) h[i] = 0;
+  __syncthreads();
+  for (int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x; id < nv; id += (int64_t)gridDim.x * 256) {
+    const int32_t* q = fl + 9 * id;
+    for (int i = 0; i < 9; i++) atomicAdd(&h[bin_of(td, q, i)], 1u);
+  }
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < cells; i += 256)
+    if (h[i]) atomicAdd(&counts[i], h[i]);
+}
+
+// Counts straight into memory (tables too wide for LDS).
+__global__ __launch_bounds__(256) void k_count_mem(const int32_t* fl, int64_t nv, TableDesc td,
+                                                   uint32_t* counts) {
+  for (int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x; id < nv; id += (int64_t)gridDim.x * 256) {
+    const int32_t* q = fl + 9 * id;
+    for (int i = 0; i < 9; i++) atomicAdd(&counts[bin_of(td, q, i)], 1u);
+  }
+}
+
+// One thread per row: refit sums in element order.
+__global__ void k_refit(const float* x, const int32_t* fl, int64_t R, int64_t cvec, double* num,
+                        double* den) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const float* xr = x + r * cvec * 8;
+  double sn = 0, sd = 0;
+  for (int64_t jv = 0; jv < cvec; jv++) {
+    int32_t p2[8];
+    em::join_fields(fl + 9 * (r * cvec + jv), p2);
+    for (int j = 0; j < 8; j++) {
+      const double pj = p2[j] / 2.0;
+      sn += (double)xr[8 * jv + j] * pj;
+      sd += pj * pj;
+    }
+  }
+  num[r] = sn;
+  den[r] = sd;
+}
+
+// Two tiles per wave (one per half), lane = state.  Steps run backwards
+// (last vector's last field first); within a step the words pushed by the
+// renormalising lanes go, in descending lane order, to the end of the tile's
+// scratch row moving towards its start, so the row ends with the tile's
+// stream in the decoder's (step ascending, lane ascending) order.
+__global__ __launch_bounds__(64) void k_rans(const int32_t* fl, uint64_t nvec, uint32_t V,
+                                             uint32_t rounds_max, uint64_t tiles, TableDesc td,
+                                             const uint2* tab, int b, uint32_t* states,
+                                             uint32_t* cnt, uint16_t* scratch, uint32_t cap) {
+  const uint32_t lane = threadIdx.x, half = lane >> 5, l = lane & 31;
+  const uint64_t t = 2ull * blockIdx.x + half;
+  const bool tile_ok = t < tiles;
+  const uint64_t v0 = t * V;
+  const uint64_t nv = tile_ok ? (nvec - v0 < V ? nvec - v0 : V) : 0;
+  const uint32_t M = 1u << b;
+  uint16_t* out = scratch + t * cap + cap - 1;
+  uint32_t st = 1u << 15, pos = 0;
+  for (uint32_t step = 9 * rounds_max; step-- > 0;) {
+    const uint32_t k = step / 9, fi = step - 9 * k;
+    const uint64_t li = l + kLanesN * (uint64_t)k;
+    const bool active = li < nv;
+    uint32_t f = 1, F = 0;
+    if (active) {
+      const int32_t* q = fl + 9 * (v0 + li);
+      const uint2 e = tab[bin_of(td, q, (int)fi)];
+      f = e.x;
+      F = e.y;
+    }
+    uint32_t xs = st;
+    const bool push = active && (uint64_t)xs >= ((uint64_t)f << (31 - b));
+    const uint64_t mask = __ballot(push);
+    const uint32_t m = (uint32_t)(mask >> (32 * half));
+    if (push) {
+      const uint32_t idx = pos + (uint32_t)__popcll((uint64_t)m >> (l + 1));
+      out[-(int64_t)idx] = (uint16_t)(xs & 0xFFFF);
+      xs >>= 16;
+    }
+    pos += (uint32_t)__popc(m);
+    if (active) st = (xs / f) * M + xs % f + F;
+  }
+  if (tile_ok) {
+    states[t * kLanesN + l] = st;
+    if (l == 0) cnt[t] = pos;
+  }
+}
+
+// One workgroup per tile: the tile's words from the end of its scratch row to
+// the payload at its offset.
+__global__ __launch_bounds__(256) void k_gather(const uint16_t* scratch, uint32_t cap,
+                                                const uint32_t* cnt, const uint32_t* offs,
+                                                uint16_t* payload) {
+  const uint64_t t = blockIdx.x;
+  const uint32_t n = cnt[t];
+  const uint16_t* src = scratch + t * cap + cap - n;
+  uint16_t* dst = payload + offs[t];
+  for (uint32_t i = threadIdx.x; i < n; i += 256) dst[i] = src[i];
+}
+
+// One thread per row: error sums in element order.
+__global__ void k_errors(const void* w, int dt, const float* x, const int32_t* fl,
+                         const float* sigma, const float* delta, int rdt, int cont, int64_t R,
+                         int64_t cvec, double* acc) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const int64_t C = cvec * 8;
+  double ec = 0, rc = 0, eo = 0, ro = 0;
+  for (int64_t jv = 0; jv < cvec; jv++) {
+    int32_t two[8];
+    em::join_fields(fl + 9 * (r * cvec + jv), two);
+    for (int j = 0; j < 8; j++) {
+      const double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
+      const double v = rdt == EP_BF16 ? em::to_bf16(y) : rdt == EP_FP16 ? em::to_fp16(y)
+                     : rdt == EP_FP8_E4M3 ? em::to_e4m3(y) : rdt == EP_INT8 ? em::int8_snap(y) : y;
+      const double xc = x[r * C + 8 * jv + j];
+      ec += (v - xc) * (v - xc);
+      rc += xc * xc;
+      const double wo = (double)load_input(w, dt, r * C + 8 * jv + j);
+      const double vo = cont ? v * (double)delta[r] : v;
+      eo += (vo - wo) * (vo - wo);
+      ro += wo * wo;
+    }
+  }
+  acc[4 * r] = ec;
+  acc[4 * r + 1] = rc;
+  acc[4 * r + 2] = eo;
+  acc[4 * r + 3] = ro;
+}
+
+unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+struct Ctx {
+  const void* w = nullptr;
+  int dt = 0, cont = 0;
+  int64_t R = 0, C = 0, cvec = 0;
+  hipStream_t st = nullptr;
+  std::vector<void*> owned;
+  float* x = nullptr;
+  float* delta = nullptr;
+  double* mu = nullptr;
+  int* bad = nullptr;
+  int64_t* rows = nullptr;
+  int32_t* sfl = nullptr;
+  int64_t sfl_vectors = 0, sample_vectors = 0;
+  int32_t* fl = nullptr;
+  int32_t* lohi = nullptr;
+  uint16_t* words = nullptr;   // rANS output rows (cap words per tile), rans() -> payload()
+  uint32_t* words_n = nullptr;
+  uint32_t cap = 0;
+
+  template <class T>
+  int alloc(T** p, uint64_t count, const char* what) {
+    void* q = nullptr;
+    if (hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(EP_ERR_HIP, what);
+    }
+    owned.push_back(q);
+    *p = static_cast<T*>(q);
+    return EP_OK;
+  }
+  void release(void* p) {
+    for (auto& q : owned)
+      if (q == p) {
+        (void)hipFree(q);
+        q = nullptr;
+      }
+  }
+  int sync(const char* what) {
+    if (hipStreamSynchronize(st) != hipSuccess || hipGetLastError() != hipSuccess)
+      return fail(EP_ERR_HIP, what);
+    return EP_OK;
+  }
+  int to_host(void* dst, const void* src, uint64_t bytes, const char* what) {
+    if (bytes && hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return fail(EP_ERR_HIP, what);
+    return sync(what);
+  }
+  int to_dev(void* dst, const void* src, uint64_t bytes, const char* what) {
+    if (bytes && hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st) != hipSuccess)
+      return fail(EP_ERR_HIP, what);
+    return EP_OK;
+  }
+};
+
+#define EP_GTRY(call)             \
+  do {                            \
+    int rc_ = (call);             \
+    if (rc_ != EP_OK) return rc_; \
+  } while (0)
+#define EP_LAUNCHED(what) \
+  if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, what)
+
+int open(Ctx** out, const void* d_w, int dt, int64_t R, int64_t C, int container, void* stream) {
+  *out = nullptr;
+  if (R >= (int64_t(1) << 31)) return fail(EP_ERR_UNSUPPORTED, "ep_encode_gpu: more than 2^31 rows");
+  Ctx* c = new Ctx;
+  c->w = d_w;
+  c->dt = dt;
+  c->cont = container;
+  c->R = R;
+  c->C = C;
+  c->cvec = C / 8;
+  c->st = static_cast<hipStream_t>(stream);
+  const uint64_t N = (uint64_t)R * (uint64_t)C;
+  int rc = EP_OK;
+  if ((rc = c->alloc(&c->x, N, "ep_encode_gpu: device allocation (values)")) != EP_OK ||
+      (rc = c->alloc(&c->delta, R, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->mu, R, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->bad, 1, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->rows, R, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->fl, N / 8 * 9, "ep_encode_gpu: device allocation (fields)")) != EP_OK ||
+      (rc = c->alloc(&c->lohi, 2 * kTablesN, "ep_encode_gpu: device allocation")) != EP_OK) {
+    close(c);
+    return rc;
+  }
+  *out = c;
+  return EP_OK;
+}
+
+void close(Ctx* c) {
+  if (!c) return;
+  if (c->st) (void)hipStreamSynchronize(c->st);
+  for (void* q : c->owned)
+    if (q) (void)hipFree(q);
+  delete c;
+}
+
+int prep(Ctx* c, float* delta, double* mu) {
+  const int zero = 0;
+  EP_GTRY(c->to_dev(c->bad, &zero, sizeof(int), "ep_encode_gpu: copy"));
+  if (hipMemsetAsync(c->delta, 0, 4 * (size_t)c->R, c->st) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_encode_gpu: clear");
+  hipLaunchKernelGGL(k_prep_rows, dim3((unsigned)c->R), dim3(256), 0, c->st, c->w, c->dt, c->C,
+                     c->cont, c->x, c->delta, c->bad);
+  EP_LAUNCHED("ep_encode_gpu: launch (prep)");
+  hipLaunchKernelGGL(k_prep_mu, dim3(blocks_for(c->R, 64)), dim3(64), 0, c->st, c->x, c->R, c->C,
+                     c->mu);
+  EP_LAUNCHED("ep_encode_gpu: launch (row rms)");
+  int bad = 0;
+  EP_GTRY(c->to_host(&bad, c->bad, sizeof(int), "ep_encode_gpu: prep"));
+  if (bad) return fail(EP_ERR_ARG, "ep_encode: non-finite input value");
+  EP_GTRY(c->to_host(delta, c->delta, 4 * (uint64_t)c->R, "ep_encode_gpu: prep"));
+  return c->to_host(mu, c->mu, 8 * (uint64_t)c->R, "ep_encode_gpu: prep");
+}
+
+int quantize(Ctx* c, const int64_t* rows, int64_t nrows, double s, int32_t* lohi) {
+  int32_t* dst = c->fl;
+  const int64_t nv = nrows * c->cvec;
+  if (rows) {
+    if (nv > c->sfl_vectors) {
+      if (c->sfl) c->release(c->sfl);
+      c->sfl = nullptr;
+      EP_GTRY(c->alloc(&c->sfl, (uint64_t)nv * 9, "ep_encode_gpu: device allocation (sample)"));
+      c->sfl_vectors = nv;
+    }
+    dst = c->sfl;
+    c->sample_vectors = nv;
+    EP_GTRY(c->to_dev(c->rows, rows, 8 * (uint64_t)nrows, "ep_encode_gpu: copy (rows)"));
+  }
+  int32_t init[2 * kTablesN];
+  for (int i = 0; i < kTablesN; i++) {
+    init[2 * i] = INT_MAX;
+    init[2 * i + 1] = INT_MIN;
+  }
+  EP_GTRY(c->to_dev(c->lohi, init, sizeof(init), "ep_encode_gpu: copy"));
+  hipLaunchKernelGGL(k_quantize, dim3(blocks_for(nv, 256)), dim3(256), 0, c->st, c->x, c->mu,
+                     rows ? c->rows : nullptr, nrows, c->cvec, c->C, s, dst, c->lohi);
+  EP_LAUNCHED("ep_encode_gpu: launch (quantize)");
+  return c->to_host(lohi, c->lohi, sizeof(init), "ep_encode_gpu: quantize");
+}
+
+namespace {
+TableDesc desc_of(const int32_t* lo, const int32_t* A, uint32_t* cells) {
+  TableDesc td;
+  uint32_t base = 0;
+  for (int i = 0; i < kTablesN; i++) {
+    td.lo[i] = lo[i];
+    td.base[i] = base;
+    base += (uint32_t)A[i];
+  }
+  *cells = base;
+  return td;
+}
+}  // namespace
+
+int count(Ctx* c, bool sample, const int32_t* lo, const int32_t* A, uint64_t* n) {
+  uint32_t cells = 0;
+  const TableDesc td = desc_of(lo, A, &cells);
+  const int32_t* src = sample ? c->sfl : c->fl;
+  const int64_t nv = sample ? c->sample_vectors : c->R * c->cvec;
+  uint32_t* d = nullptr;
+  EP_GTRY(c->alloc(&d, cells, "ep_encode_gpu: device allocation (counts)"));
+  int rc = EP_OK;
+  if (hipMemsetAsync(d, 0, 4ull * cells, c->st) != hipSuccess) rc = fail(EP_ERR_HIP, "ep_encode_gpu: clear");
+  const unsigned grid = nv > 0 ? (unsigned)std::min<int64_t>(256, (nv + 255) / 256) : 0;
+  if (rc == EP_OK && grid) {
+    if (cells <= kLdsBins) {
+      if (hipFuncSetAttribute((const void*)k_count_lds, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)(4 * kLdsBins)) != hipSuccess)
+        rc = fail(EP_ERR_HIP, "ep_encode_gpu: LDS limit");
+      else
+        hipLaunchKernelGGL(k_count_lds, dim3(grid), dim3(256), 4 * cells, c->st, src, nv, td, cells, d);
+    } else {
+      hipLaunchKernelGGL(k_count_mem, dim3(grid), dim3(256), 0, c->st, src, nv, td, d);
+    }
+    if (rc == EP_OK && hipGetLastError() != hipSuccess) rc = fail(EP_ERR_HIP, "ep_encode_gpu: launch (count)");
+  }
+  std::vector<uint32_t> h(cells);
+  if (rc == EP_OK) rc = c->to_host(h.data(), d, 4ull * cells, "ep_encode_gpu: count");
+  c->release(d);
+  if (rc != EP_OK) return rc;
+  for (uint32_t i = 0; i < cells; i++) n[i] = h[i];
+  return EP_OK;
+}
+
+int refit(Ctx* c, double* num, double* den) {
+  double *dn = nullptr, *dd = nullptr;
+  EP_GTRY(c->alloc(&dn, c->R, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->alloc(&dd, c->R, "ep_encode_gpu: device allocation"));
+  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, 64)), dim3(64), 0, c->st, c->x, c->fl, c->R,
+                     c->cvec, dn, dd);
+  EP_LAUNCHED("ep_encode_gpu: launch (refit)");
+  EP_GTRY(c->to_host(num, dn, 8 * (uint64_t)c->R, "ep_encode_gpu: refit"));
+  EP_GTRY(c->to_host(den, dd, 8 * (uint64_t)c->R, "ep_encode_gpu: refit"));
+  c->release(dn);
+  c->release(dd);
+  return EP_OK;
+}
+
+int rans(Ctx* c, int b, uint32_t V, uint64_t tiles, const int32_t* lo, const int32_t* A,
+         const uint32_t* f, uint32_t* states, uint64_t* words) {
+  uint32_t cells = 0;
+  const TableDesc td = desc_of(lo, A, &cells);
+  std::vector<uint2> tab(cells);
+  for (int i = 0; i < kTablesN; i++) {
+    uint32_t F = 0;
+    for (int32_t z = 0; z < A[i]; z++) {
+      tab[td.base[i] + z] = make_uint2(f[td.base[i] + z], F);
+      F += f[td.base[i] + z];
+    }
+  }
+  const uint32_t rounds_max = (V + kLanesN - 1) / kLanesN;
+  const uint64_t cap = 9ull * rounds_max * kLanesN;
+  if (cap > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_encode_gpu: tile too large");
+  uint2* dtab = nullptr;
+  uint32_t *dst = nullptr, *dcnt = nullptr;
+  uint16_t* scr = nullptr;
+  EP_GTRY(c->alloc(&dtab, cells, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->alloc(&dst, tiles * kLanesN, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->alloc(&dcnt, tiles, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->alloc(&scr, tiles * cap, "ep_encode_gpu: device allocation (rANS words)"));
+  EP_GTRY(c->to_dev(dtab, tab.data(), 8ull * cells, "ep_encode_gpu: copy (tables)"));
+  hipLaunchKernelGGL(k_rans, dim3((unsigned)((tiles + 1) / 2)), dim3(64), 0, c->st, c->fl,
+                     (uint64_t)(c->R * c->cvec), V, rounds_max, tiles, td, dtab, b, dst, dcnt, scr,
+                     (uint32_t)cap);
+  EP_LAUNCHED("ep_encode_gpu: launch (rANS)");
+  std::vector<uint32_t> cnt(tiles);
+  EP_GTRY(c->to_host(states, dst, 4 * tiles * kLanesN, "ep_encode_gpu: rANS"));
+  EP_GTRY(c->to_host(cnt.data(), dcnt, 4 * tiles, "ep_encode_gpu: rANS"));
+  for (uint64_t t = 0; t < tiles; t++) words[t] = cnt[t];
+  c->release(dtab);
+  c->release(dst);
+  c->words = scr;
+  c->words_n = dcnt;
+  c->cap = (uint32_t)cap;
+  return EP_OK;
+}
+
+int payload(Ctx* c, const uint32_t* offs, uint64_t tiles, uint64_t total_words, uint8_t* dst) {
+  if (!c->words) return fail(EP_ERR_ARG, "ep_encode_gpu: payload before rans");
+  uint32_t* doffs = nullptr;
+  uint16_t* dpay = nullptr;
+  EP_GTRY(c->alloc(&doffs, tiles + 1, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->alloc(&dpay, total_words, "ep_encode_gpu: device allocation (payload)"));
+  EP_GTRY(c->to_dev(doffs, offs, 4 * (tiles + 1), "ep_encode_gpu: copy (offsets)"));
+  if (tiles) {
+    hipLaunchKernelGGL(k_gather, dim3((unsigned)tiles), dim3(256), 0, c->st, c->words, c->cap,
+                       c->words_n, doffs, dpay);
+    EP_LAUNCHED("ep_encode_gpu: launch (payload)");
+  }
+  EP_GTRY(c->to_host(dst, dpay, 2 * total_words, "ep_encode_gpu: payload"));
+  c->release(doffs);
+  c->release(dpay);
+  c->release(c->words);
+  c->release(c->words_n);
+  c->words = nullptr;
+  c->words_n = nullptr;
+  return EP_OK;
+}
+
+int errors(Ctx* c, const float* sigma, int rdt, double* acc) {
+  float* ds = nullptr;
+  double* da = nullptr;
+  EP_GTRY(c->alloc(&ds, c->R, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->alloc(&da, 4 * (uint64_t)c->R, "ep_encode_gpu: device allocation"));
+  EP_GTRY(c->to_dev(ds, sigma, 4 * (uint64_t)c->R, "ep_encode_gpu: copy (scales)"));
+  hipLaunchKernelGGL(k_errors, dim3(blocks_for(c->R, 64)), dim3(64), 0, c->st, c->w, c->dt, c->x,
+                     c->fl, ds, c->delta, rdt, c->cont, c->R, c->cvec, da);
+  EP_LAUNCHED("ep_encode_gpu: launch (errors)");
+  EP_GTRY(c->to_host(acc, da, 32 * (uint64_t)c->R, "ep_encode_gpu: errors"));
+  c->release(ds);
+  c->release(da);
+  return EP_OK;
+}
+
+}  // namespace genc
+}  // namespace ep

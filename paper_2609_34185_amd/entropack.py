@@ -96,6 +96,8 @@ def lib():
         L.ep_encode_params_default.restype = None
         L.ep_encode_cpu.argtypes = [vp, C.c_int, i64, i64, C.POINTER(EncodeParams),
                                     C.POINTER(Blob), C.POINTER(EncodeStats)]
+        L.ep_encode_gpu.argtypes = [vp, C.c_int, i64, i64, C.POINTER(EncodeParams),
+                                    C.POINTER(Blob), C.POINTER(EncodeStats), vp]
         L.ep_blob_free.argtypes = [C.POINTER(Blob)]
         L.ep_blob_free.restype = None
         L.ep_blob_info.argtypes = [vp, u64, C.POINTER(TensorInfo)]
@@ -113,7 +115,7 @@ def lib():
     return _lib
 
 
-EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_blob_free", "ep_blob_info",
+EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_encode_gpu", "ep_blob_free", "ep_blob_info",
            "ep_decode_tiles", "ep_decode_layers_workspace", "ep_decode_layers",
            "ep_stack_workspace", "ep_stack_prepare", "ep_stack_decode", "ep_gemm_i8_nt",
            "ep_last_error"]
@@ -144,6 +146,20 @@ def encode(w: np.ndarray, target_bpp: float, dtype: int | None = None, **kw):
     st = EncodeStats()
     _check(lib().ep_encode_cpu(w.ctypes.data_as(C.c_void_p), dtype, w.shape[0], w.shape[1],
                                C.byref(p), C.byref(out), C.byref(st)), "ep_encode_cpu")
+    blob = np.ctypeslib.as_array(out.data, shape=(out.size,)).copy()
+    lib().ep_blob_free(C.byref(out))
+    return blob, {k: getattr(st, k) for k, _ in EncodeStats._fields_}
+
+
+def encode_gpu(d_w: int, rows: int, cols: int, target_bpp: float, dtype: int = BF16,
+               stream: int = 0, **kw):
+    """Encode an R x C device matrix (pointer d_w: BF16/FP16 bits or FP32) with the GPU
+    encoder.  Returns (blob as a uint8 numpy array, stats dict), as encode()."""
+    p = default_params(target_bpp, **kw)
+    out = Blob()
+    st = EncodeStats()
+    _check(lib().ep_encode_gpu(d_w, dtype, rows, cols, C.byref(p), C.byref(out), C.byref(st),
+                               stream or None), "ep_encode_gpu")
     blob = np.ctypeslib.as_array(out.data, shape=(out.size,)).copy()
     lib().ep_blob_free(C.byref(out))
     return blob, {k: getattr(st, k) for k, _ in EncodeStats._fields_}
