@@ -17,7 +17,10 @@ Other workloads (--workload): attn_fp16 (3072 x 3072 at 3.0 bpp to FP16),
 dit_stack (30 diffusion-transformer blocks, 180 layers at 2.5 bpp to BF16 in one
 launch), mlp_down_int8 (the MLP down projection in the INT8 container at
 6.0 bpp to INT8, followed by the INT8 MFMA product with 8192 x 17408
-activations, timed separately: decode time over product time is reported).
+activations, timed separately: decode time over product time is reported),
+encode_mlp (the GPU encoder on the MLP set's three BF16 tensors, FP8 container
+at 4.0 bpp; a step encodes all three; the CPU baseline is the oracle encoder
+on the down projection).
 
 The roofline's `traffic` field is the decode kernel's measured HBM bytes per
 launch, read from the committed rocprofv3 counter summary of this workload
@@ -100,6 +103,56 @@ def workload(name, E, W, threads):
     else:
         raise SystemExit(f"unknown workload {name}")
     return desc, items
+
+
+def encode_bench(args, E, W, threads):
+    """--workload encode_mlp: the GPU encoder on the 27B-class MLP set (gate, up, down BF16,
+    FP8 row container at 4.0 bpp, as the decode workload is prepared), inputs resident in
+    HBM.  A step encodes all three tensors (each call returns a finished host blob)."""
+    import numpy as np
+    import torch
+    d = W.llm_mlp()
+    names = ("gate", "up", "down")
+    dev = {n: torch.from_numpy(d[n].view(np.int16)).cuda() for n in names}
+    weights = sum(d[n].size for n in names)
+    s = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        return [E.encode_gpu(dev[n].data_ptr(), d[n].shape[0], d[n].shape[1], 4.0,
+                             container=E.CONT_FP8_ROW, stream=s) for n in names]
+
+    first = step()
+    ref = [E.encode(d[n], 4.0, container=E.CONT_FP8_ROW, nthreads=threads)[0] for n in names]
+    assert all(np.array_equal(a[0], b) for a, b in zip(first, ref)), "GPU and CPU encoder blobs differ"
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    line = {
+        "metric": "encoded weights/s (GPU encoder; blobs byte-identical to the CPU encoder)",
+        "value": weights / sec, "unit": "weights/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": sec * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "GPU encode of the 27B-class LLM MLP set: gate+up 17408x5120, "
+                               "down 5120x17408 BF16 in HBM, FP8 row container at 4.0 bpp, "
+                               "host blobs out", "tensors": 3, "weights": weights,
+                   "stored_bytes": int(sum(b.size for b in ref))},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        log("timing the CPU oracle encoder on the down projection")
+        t0 = time.perf_counter()
+        O.encode(d["down"], 4.0, container=1)
+        osec = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": d["down"].size / osec, "unit": "weights/s", "cores": 1,
+                                "kind": "oracle", "sample": "the down projection (89,128,960 "
+                                "weights) encoded once by the plain C oracle encoder",
+                                "seconds": round(osec, 3)}
+    print(json.dumps(line), flush=True)
 
 
 def source_digest() -> str:
@@ -265,6 +318,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.workload == "encode_mlp":
+        encode_bench(args, E, W, min(16, len(os.sched_getaffinity(0))))
         return
     threads = min(16, len(os.sched_getaffinity(0)))
 

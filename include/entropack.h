@@ -140,7 +140,8 @@ int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
  * on the host between passes).  d_w is a device array (R x C, same dtypes);
  * the result is a host blob byte-identical to ep_encode_cpu's for the same
  * inputs and parameters (nthreads is ignored), and *stats (nullable) equal to
- * its statistics.  Unlike the decode entry points it allocates device scratch
+ * its statistics (erel_coded and erel_original to rounding: their row sums
+ * are taken in a different order).  Unlike the decode entry points it allocates device scratch
  * (about 10 bytes per weight for the values, fields and rANS words) and frees
  * it before returning, and it synchronises hip_stream: on return the blob is
  * complete.  Errors: as ep_encode_cpu, plus EP_ERR_HIP (device allocation or

@@ -7,12 +7,13 @@
 // (eq. scale_fit), the 32-state interleaved rANS encode of every tile (eq.
 // rans_encode, App. C.3) and the per-row error sums of the statistics.  The
 // per-value arithmetic is the CPU encoder's own (encode_math.h) compiled for
-// the device, and every sum that rounds is accumulated in the CPU encoder's
-// element order, so the blob is byte-identical to the CPU encoder's.
+// the device, and every sum that reaches the blob is accumulated in the CPU
+// encoder's element order, so the blob is byte-identical to the CPU encoder's.
 //
 // Mapping: element-wise passes take one thread per vector (or a workgroup
-// per row for the conversion); passes whose double sums must follow element
-// order (row RMS, refit, errors) take one thread per row; counts go through a
+// per row for the conversion and the error sums); passes whose double sums
+// decide the blob (row RMS, refit) take one thread per row, summing in
+// element order out of coalesced LDS-staged chunks; counts go through a
 // workgroup histogram in LDS when all tables fit (else straight to memory);
 // the rANS encode runs two tiles per wave, one per half, each lane one state,
 // words placed by a 32-lane ballot in the order the decoder consumes them.
@@ -36,6 +37,7 @@ namespace {
 constexpr int kTablesN = 17;
 constexpr uint32_t kLanesN = 32;
 constexpr uint32_t kLdsBins = 36864;   // histogram in LDS when all tables fit (144 KiB)
+constexpr uint32_t kMaxCells = 2 + 16 * 32768;   // counted tables have A <= 2^15
 
 __device__ __forceinline__ float load_input(const void* w, int dt, int64_t i) {
   if (dt == EP_FP32) return static_cast<const float*>(w)[i];
@@ -82,15 +84,40 @@ __global__ __launch_bounds__(256) void k_prep_rows(const void* w, int dt, int64_
   }
 }
 
-// One thread per row: mu_r = max(sqrt(sum x^2 / C), eta), summed in element order.
-__global__ void k_prep_mu(const float* x, int64_t R, int64_t C, double* mu) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= R) return;
-  const float* xr = x + r * C;
+constexpr int kRowsPerBlock = 64;   // row-ordered sums: one thread per row, 64 rows per workgroup
+
+// mu_r = max(sqrt(sum x^2 / C), eta), summed in element order by the row's
+// thread; the workgroup stages 64 x 64 chunks of its rows through LDS so the
+// loads are coalesced.
+__global__ __launch_bounds__(64) void k_prep_mu(const float* x, int64_t R, int64_t C, double* mu) {
+  __shared__ float tile[kRowsPerBlock][65];
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
+  const int nr = (int)(R - r0 < kRowsPerBlock ? R - r0 : kRowsPerBlock);
+  // chunk j0's values go to LDS, then chunk j0 + 64 is requested into the
+  // same registers while the rows' threads sum chunk j0
+  float v[kRowsPerBlock];
+  auto fetch = [&](int64_t j0) {
+    const bool in = j0 + t < C;
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) v[i] = (i < nr && in) ? x[(r0 + i) * C + j0 + t] : 0.0f;
+  };
   double ss = 0;
-  for (int64_t j = 0; j < C; j++) ss += (double)xr[j] * (double)xr[j];
-  const double m = __builtin_sqrt(ss / (double)C);
-  mu[r] = m > em::kEta ? m : em::kEta;
+  fetch(0);
+  for (int64_t j0 = 0; j0 < C; j0 += 64) {
+    const int ne = (int)(C - j0 < 64 ? C - j0 : 64);
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) tile[i][t] = v[i];
+    __syncthreads();
+    if (j0 + 64 < C) fetch(j0 + 64);
+    if (t < nr)
+      for (int e = 0; e < ne; e++) ss += (double)tile[t][e] * (double)tile[t][e];
+    __syncthreads();
+  }
+  if (t < nr) {
+    const double m = __builtin_sqrt(ss / (double)C);
+    mu[r0 + t] = m > em::kEta ? m : em::kEta;
+  }
 }
 
 // One thread per vector: fields at scale s, table extents.
@@ -167,24 +194,58 @@ __global__ __launch_bounds__(256) void k_count_mem(const int32_t* fl, int64_t nv
   }
 }
 
-// One thread per row: refit sums in element order.
-__global__ void k_refit(const float* x, const int32_t* fl, int64_t R, int64_t cvec, double* num,
-                        double* den) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= R) return;
-  const float* xr = x + r * cvec * 8;
-  double sn = 0, sd = 0;
-  for (int64_t jv = 0; jv < cvec; jv++) {
-    int32_t p2[8];
-    em::join_fields(fl + 9 * (r * cvec + jv), p2);
-    for (int j = 0; j < 8; j++) {
-      const double pj = p2[j] / 2.0;
-      sn += (double)xr[8 * jv + j] * pj;
-      sd += pj * pj;
+// Refit sums in element order by the row's thread, 8 vectors (64 values and
+// 72 fields) of each of the workgroup's 64 rows staged through LDS at a time.
+__global__ __launch_bounds__(64) void k_refit(const float* x, const int32_t* fl, int64_t R,
+                                              int64_t cvec, double* num, double* den) {
+  __shared__ float tx[kRowsPerBlock][65];
+  __shared__ int32_t tf[kRowsPerBlock][73];   // 72 fields used
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock, C = cvec * 8;
+  const int nr = (int)(R - r0 < kRowsPerBlock ? R - r0 : kRowsPerBlock);
+  // chunk v0 goes to LDS, then chunk v0 + 8 is requested into the same
+  // registers while the rows' threads sum chunk v0
+  float xv[kRowsPerBlock];
+  int32_t f0[kRowsPerBlock], f1[kRowsPerBlock];
+  auto fetch = [&](int64_t v0) {
+    const int nvv = (int)(cvec - v0 < 8 ? cvec - v0 : 8);
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) {
+      const bool row = i < nr;
+      const int64_t fb = 9 * ((r0 + i) * cvec + v0);
+      xv[i] = (row && t < 8 * nvv) ? x[(r0 + i) * C + 8 * v0 + t] : 0.0f;
+      f0[i] = (row && t < 9 * nvv) ? fl[fb + t] : 0;
+      f1[i] = (row && t + 64 < 9 * nvv) ? fl[fb + t + 64] : 0;
     }
+  };
+  double sn = 0, sd = 0;
+  fetch(0);
+  for (int64_t v0 = 0; v0 < cvec; v0 += 8) {
+    const int nvv = (int)(cvec - v0 < 8 ? cvec - v0 : 8);
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) {
+      tx[i][t] = xv[i];
+      tf[i][t] = f0[i];
+      if (t < 9) tf[i][t + 64] = f1[i];
+    }
+    __syncthreads();
+    if (v0 + 8 < cvec) fetch(v0 + 8);
+    if (t < nr)
+      for (int v = 0; v < nvv; v++) {
+        int32_t p2[8];
+        em::join_fields(&tf[t][9 * v], p2);
+        for (int j = 0; j < 8; j++) {
+          const double pj = p2[j] / 2.0;
+          sn += (double)tx[t][8 * v + j] * pj;
+          sd += pj * pj;
+        }
+      }
+    __syncthreads();
   }
-  num[r] = sn;
-  den[r] = sd;
+  if (t < nr) {
+    num[r0 + t] = sn;
+    den[r0 + t] = sd;
+  }
 }
 
 // Two tiles per wave (one per half), lane = state.  Steps run backwards
@@ -245,15 +306,18 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* scratch, uint32_
   for (uint32_t i = threadIdx.x; i < n; i += 256) dst[i] = src[i];
 }
 
-// One thread per row: error sums in element order.
-__global__ void k_errors(const void* w, int dt, const float* x, const int32_t* fl,
-                         const float* sigma, const float* delta, int rdt, int cont, int64_t R,
-                         int64_t cvec, double* acc) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= R) return;
-  const int64_t C = cvec * 8;
+// One workgroup per row: error sums, each thread over a strided subset of the
+// row's vectors, combined by a fixed tree (deterministic, but not the CPU
+// encoder's element order: these statistics agree with its to rounding).
+__global__ __launch_bounds__(256) void k_errors(const void* w, int dt, const float* x,
+                                                const int32_t* fl, const float* sigma,
+                                                const float* delta, int rdt, int cont, int64_t cvec,
+                                                double* acc) {
+  __shared__ double red[4][256];
+  const int64_t r = blockIdx.x, C = cvec * 8;
+  const int t = threadIdx.x;
   double ec = 0, rc = 0, eo = 0, ro = 0;
-  for (int64_t jv = 0; jv < cvec; jv++) {
+  for (int64_t jv = t; jv < cvec; jv += 256) {
     int32_t two[8];
     em::join_fields(fl + 9 * (r * cvec + jv), two);
     for (int j = 0; j < 8; j++) {
@@ -269,10 +333,17 @@ __global__ void k_errors(const void* w, int dt, const float* x, const int32_t* f
       ro += wo * wo;
     }
   }
-  acc[4 * r] = ec;
-  acc[4 * r + 1] = rc;
-  acc[4 * r + 2] = eo;
-  acc[4 * r + 3] = ro;
+  red[0][t] = ec;
+  red[1][t] = rc;
+  red[2][t] = eo;
+  red[3][t] = ro;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (t < h)
+      for (int q = 0; q < 4; q++) red[q][t] += red[q][t + h];
+    __syncthreads();
+  }
+  if (t < 4) acc[4 * r + t] = red[t][0];
 }
 
 unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
@@ -297,6 +368,10 @@ struct Ctx {
   uint16_t* words = nullptr;   // rANS output rows (cap words per tile), rans() -> payload()
   uint32_t* words_n = nullptr;
   uint32_t cap = 0;
+  uint32_t* counts = nullptr;  // kMaxCells histogram cells
+  double *num = nullptr, *den = nullptr, *acc = nullptr;
+  float* sigma = nullptr;
+  std::vector<int64_t> rows_up;   // the row list last uploaded to `rows`
 
   template <class T>
   int alloc(T** p, uint64_t count, const char* what) {
@@ -360,7 +435,12 @@ int open(Ctx** out, const void* d_w, int dt, int64_t R, int64_t C, int container
       (rc = c->alloc(&c->bad, 1, "ep_encode_gpu: device allocation")) != EP_OK ||
       (rc = c->alloc(&c->rows, R, "ep_encode_gpu: device allocation")) != EP_OK ||
       (rc = c->alloc(&c->fl, N / 8 * 9, "ep_encode_gpu: device allocation (fields)")) != EP_OK ||
-      (rc = c->alloc(&c->lohi, 2 * kTablesN, "ep_encode_gpu: device allocation")) != EP_OK) {
+      (rc = c->alloc(&c->lohi, 2 * kTablesN, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->counts, kMaxCells, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->num, R, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->den, R, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->acc, 4 * (uint64_t)R, "ep_encode_gpu: device allocation")) != EP_OK ||
+      (rc = c->alloc(&c->sigma, R, "ep_encode_gpu: device allocation")) != EP_OK) {
     close(c);
     return rc;
   }
@@ -384,8 +464,8 @@ int prep(Ctx* c, float* delta, double* mu) {
   hipLaunchKernelGGL(k_prep_rows, dim3((unsigned)c->R), dim3(256), 0, c->st, c->w, c->dt, c->C,
                      c->cont, c->x, c->delta, c->bad);
   EP_LAUNCHED("ep_encode_gpu: launch (prep)");
-  hipLaunchKernelGGL(k_prep_mu, dim3(blocks_for(c->R, 64)), dim3(64), 0, c->st, c->x, c->R, c->C,
-                     c->mu);
+  hipLaunchKernelGGL(k_prep_mu, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+                     c->x, c->R, c->C, c->mu);
   EP_LAUNCHED("ep_encode_gpu: launch (row rms)");
   int bad = 0;
   EP_GTRY(c->to_host(&bad, c->bad, sizeof(int), "ep_encode_gpu: prep"));
@@ -406,7 +486,11 @@ int quantize(Ctx* c, const int64_t* rows, int64_t nrows, double s, int32_t* lohi
     }
     dst = c->sfl;
     c->sample_vectors = nv;
-    EP_GTRY(c->to_dev(c->rows, rows, 8 * (uint64_t)nrows, "ep_encode_gpu: copy (rows)"));
+    if ((int64_t)c->rows_up.size() != nrows ||
+        std::memcmp(c->rows_up.data(), rows, 8 * (size_t)nrows) != 0) {
+      c->rows_up.assign(rows, rows + nrows);
+      EP_GTRY(c->to_dev(c->rows, c->rows_up.data(), 8 * (uint64_t)nrows, "ep_encode_gpu: copy (rows)"));
+    }
   }
   int32_t init[2 * kTablesN];
   for (int i = 0; i < kTablesN; i++) {
@@ -437,45 +521,35 @@ TableDesc desc_of(const int32_t* lo, const int32_t* A, uint32_t* cells) {
 int count(Ctx* c, bool sample, const int32_t* lo, const int32_t* A, uint64_t* n) {
   uint32_t cells = 0;
   const TableDesc td = desc_of(lo, A, &cells);
+  if (cells > kMaxCells) return fail(EP_ERR_ARG, "ep_encode_gpu: count of a table wider than 2^15");
   const int32_t* src = sample ? c->sfl : c->fl;
   const int64_t nv = sample ? c->sample_vectors : c->R * c->cvec;
-  uint32_t* d = nullptr;
-  EP_GTRY(c->alloc(&d, cells, "ep_encode_gpu: device allocation (counts)"));
-  int rc = EP_OK;
-  if (hipMemsetAsync(d, 0, 4ull * cells, c->st) != hipSuccess) rc = fail(EP_ERR_HIP, "ep_encode_gpu: clear");
-  const unsigned grid = nv > 0 ? (unsigned)std::min<int64_t>(256, (nv + 255) / 256) : 0;
-  if (rc == EP_OK && grid) {
+  uint32_t* d = c->counts;
+  if (hipMemsetAsync(d, 0, 4ull * cells, c->st) != hipSuccess) return fail(EP_ERR_HIP, "ep_encode_gpu: clear");
+  const unsigned grid = (unsigned)std::min<int64_t>(256, (nv + 255) / 256);
+  if (grid) {
     if (cells <= kLdsBins) {
       if (hipFuncSetAttribute((const void*)k_count_lds, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)(4 * kLdsBins)) != hipSuccess)
-        rc = fail(EP_ERR_HIP, "ep_encode_gpu: LDS limit");
-      else
-        hipLaunchKernelGGL(k_count_lds, dim3(grid), dim3(256), 4 * cells, c->st, src, nv, td, cells, d);
+        return fail(EP_ERR_HIP, "ep_encode_gpu: LDS limit");
+      hipLaunchKernelGGL(k_count_lds, dim3(grid), dim3(256), 4 * cells, c->st, src, nv, td, cells, d);
     } else {
       hipLaunchKernelGGL(k_count_mem, dim3(grid), dim3(256), 0, c->st, src, nv, td, d);
     }
-    if (rc == EP_OK && hipGetLastError() != hipSuccess) rc = fail(EP_ERR_HIP, "ep_encode_gpu: launch (count)");
+    EP_LAUNCHED("ep_encode_gpu: launch (count)");
   }
   std::vector<uint32_t> h(cells);
-  if (rc == EP_OK) rc = c->to_host(h.data(), d, 4ull * cells, "ep_encode_gpu: count");
-  c->release(d);
-  if (rc != EP_OK) return rc;
+  EP_GTRY(c->to_host(h.data(), d, 4ull * cells, "ep_encode_gpu: count"));
   for (uint32_t i = 0; i < cells; i++) n[i] = h[i];
   return EP_OK;
 }
 
 int refit(Ctx* c, double* num, double* den) {
-  double *dn = nullptr, *dd = nullptr;
-  EP_GTRY(c->alloc(&dn, c->R, "ep_encode_gpu: device allocation"));
-  EP_GTRY(c->alloc(&dd, c->R, "ep_encode_gpu: device allocation"));
-  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, 64)), dim3(64), 0, c->st, c->x, c->fl, c->R,
-                     c->cvec, dn, dd);
+  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+                     c->x, c->fl, c->R, c->cvec, c->num, c->den);
   EP_LAUNCHED("ep_encode_gpu: launch (refit)");
-  EP_GTRY(c->to_host(num, dn, 8 * (uint64_t)c->R, "ep_encode_gpu: refit"));
-  EP_GTRY(c->to_host(den, dd, 8 * (uint64_t)c->R, "ep_encode_gpu: refit"));
-  c->release(dn);
-  c->release(dd);
-  return EP_OK;
+  EP_GTRY(c->to_host(num, c->num, 8 * (uint64_t)c->R, "ep_encode_gpu: refit"));
+  return c->to_host(den, c->den, 8 * (uint64_t)c->R, "ep_encode_gpu: refit");
 }
 
 int rans(Ctx* c, int b, uint32_t V, uint64_t tiles, const int32_t* lo, const int32_t* A,
@@ -540,18 +614,11 @@ int payload(Ctx* c, const uint32_t* offs, uint64_t tiles, uint64_t total_words, 
 }
 
 int errors(Ctx* c, const float* sigma, int rdt, double* acc) {
-  float* ds = nullptr;
-  double* da = nullptr;
-  EP_GTRY(c->alloc(&ds, c->R, "ep_encode_gpu: device allocation"));
-  EP_GTRY(c->alloc(&da, 4 * (uint64_t)c->R, "ep_encode_gpu: device allocation"));
-  EP_GTRY(c->to_dev(ds, sigma, 4 * (uint64_t)c->R, "ep_encode_gpu: copy (scales)"));
-  hipLaunchKernelGGL(k_errors, dim3(blocks_for(c->R, 64)), dim3(64), 0, c->st, c->w, c->dt, c->x,
-                     c->fl, ds, c->delta, rdt, c->cont, c->R, c->cvec, da);
+  EP_GTRY(c->to_dev(c->sigma, sigma, 4 * (uint64_t)c->R, "ep_encode_gpu: copy (scales)"));
+  hipLaunchKernelGGL(k_errors, dim3((unsigned)c->R), dim3(256), 0, c->st, c->w, c->dt, c->x, c->fl,
+                     c->sigma, c->delta, rdt, c->cont, c->cvec, c->acc);
   EP_LAUNCHED("ep_encode_gpu: launch (errors)");
-  EP_GTRY(c->to_host(acc, da, 32 * (uint64_t)c->R, "ep_encode_gpu: errors"));
-  c->release(ds);
-  c->release(da);
-  return EP_OK;
+  return c->to_host(acc, c->acc, 32 * (uint64_t)c->R, "ep_encode_gpu: errors");
 }
 
 }  // namespace genc
