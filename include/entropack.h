@@ -97,6 +97,9 @@ typedef struct {
   int64_t sample_vectors;   /* nominal sample size in 8-vectors (App. C.1: 2^18) */
   double state_credit_bits; /* bits credited per terminal state in eq. estimate (8) */
   int32_t nthreads;         /* worker threads, 0 = hardware concurrency */
+  int32_t rdo_candidates;   /* K of the per-row rate-distortion refinement (Section 3.5,
+                               App. C.2); <= 1 = off (default); at most 64 */
+  int32_t rdo_sweeps;       /* T allocation sweeps of that refinement; 0 = off (default) */
   int32_t reserved;
 } ep_encode_params;
 
@@ -121,6 +124,8 @@ typedef struct {
   uint32_t sample_rows;
   uint32_t escalations;     /* precision increases */
   uint32_t coarsenings;     /* coarsening steps after b = 15 */
+  uint32_t rdo_rows_moved;  /* rows the refinement moved off the baseline scale */
+  uint32_t reserved;
 } ep_encode_stats;
 
 /* Default parameters of the paper (App. C.1) with V = 512 and 8 credited bits. */
@@ -128,7 +133,8 @@ void ep_encode_params_default(ep_encode_params* p);
 
 /* Encode W (R x C row-major; w_dtype EP_BF16 / EP_FP16 bit patterns or EP_FP32)
  * at p->target_bpp (Section 3.1 objective; Alg. rate selection in 3.4; refit
- * 3.5; rANS 3.6).  On success out->data holds the blob (caller frees with
+ * 3.5; optional per-row refinement, Section 3.5 and App. C.2, when
+ * rdo_candidates > 1 and rdo_sweeps > 0; rANS 3.6).  On success out->data holds the blob (caller frees with
  * ep_blob_free) and *stats (nullable) is filled.  The output is independent of
  * nthreads.  Errors: EP_ERR_ARG (C % 8 != 0, R or C <= 0, non-finite input,
  * target <= 0, bad parameters), EP_ERR_NOMEM. */
@@ -145,7 +151,8 @@ int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
  * (about 10 bytes per weight for the values, fields and rANS words) and frees
  * it before returning, and it synchronises hip_stream: on return the blob is
  * complete.  Errors: as ep_encode_cpu, plus EP_ERR_HIP (device allocation or
- * launch failure) and EP_ERR_UNSUPPORTED (R >= 2^31). */
+ * launch failure) and EP_ERR_UNSUPPORTED (R >= 2^31, or the per-row
+ * refinement requested: it runs in ep_encode_cpu only). */
 int ep_encode_gpu(const void* d_w, int w_dtype, int64_t rows, int64_t cols,
                   const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats,
                   void* hip_stream);

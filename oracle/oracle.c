@@ -30,6 +30,11 @@
  *   - container routes: delta_r = fp32(amax_r/448) (FP8 e4m3fn) or
  *     fp32(amax_r/127) (INT8, symmetric), amax 0 gives delta 1, the quotient
  *     W/delta is formed in FP64 and rounded once into the container.
+ *   - per-row refinement (optional): candidate ratios are log-midpoints of
+ *     the widest gaps of [0.70, 1.45] (the ends are not candidates);
+ *     D_{r,k} uses the stored FP32 row scale in coded units; candidates join
+ *     only while every joined table range fits 2^b; the lambda bracket starts
+ *     at 2^-20 sum D / sum R; argmin ties go to the earlier candidate.
  *
  * Parity status of every function is stated in its comment; pins live in the
  * CPU tests.
@@ -69,13 +74,16 @@ typedef struct {
                              * the equation prints 16; a state started at 2^15 retains
                              * log2(x/2^15) bits, 8 on average, and 8 is the default
                              * reading (16 stays selectable). */
+  int32_t rdo_candidates;   /* K of the per-row refinement [3.5, App. C.2]; <= 1: off */
+  int32_t rdo_sweeps;       /* T allocation sweeps; 0: off */
 } ora_params;
 
 /* indices into the stats array filled by ora_encode */
 enum {
   ST_SCALE = 0, ST_B, ST_RHAT_SUB, ST_R_STORED, ST_BYTES, ST_PAYLOAD_BITS, ST_CCE_FULL,
   ST_N_TILES, ST_MAX_A, ST_EREL_CODED, ST_EREL_ORIG, ST_MEAN_STATE_BITS,
-  ST_TABLE_BYTES, ST_SAMPLE_ROWS, ST_ESCALATIONS, ST_COARSENINGS, ST_N_STATS = 32
+  ST_TABLE_BYTES, ST_SAMPLE_ROWS, ST_ESCALATIONS, ST_COARSENINGS, ST_RDO_ROWS_MOVED,
+  ST_RDO_BUDGET_BYTES, ST_RDO_LAMBDA, ST_N_STATS = 32
 };
 
 /* ========================================================================= */
@@ -607,6 +615,295 @@ static void symbol_of(const int32_t* f9, int i, const table_t* T, int* t, int32_
   }
 }
 
+/* ========================================================================= */
+/* Per-row rate-distortion refinement [3.5, eqs. rdo_rate, rdo_budget,        */
+/* rdo_choice; App. C.2, Alg. rdo].                                           */
+/* ========================================================================= */
+
+/* Candidate ratios: rho_0 = 1, then each further ratio is the log-midpoint of
+ * the widest gap (first on ties) between consecutive points of {0.70, the
+ * ratios so far, 1.45}, so the sets are nested in K.  Reading: the range ends
+ * bound the gaps and are not candidates themselves. */
+int ora_rdo_ratios(int K, double* rho) {
+  if (K < 1 || K > 64) return O_ERR_ARG;
+  double pts[66];
+  int n = 3;
+  pts[0] = log(0.70);
+  pts[1] = 0.0;
+  pts[2] = log(1.45);
+  rho[0] = 1.0;
+  for (int k = 1; k < K; k++) {
+    int g = 0;
+    for (int i = 1; i + 1 < n; i++)
+      if (pts[i + 1] - pts[i] > pts[g + 1] - pts[g]) g = i;
+    double mid = 0.5 * (pts[g] + pts[g + 1]);
+    for (int i = n; i > g + 1; i--) pts[i] = pts[i - 1];
+    pts[g + 1] = mid;
+    n++;
+    rho[k] = exp(mid);
+  }
+  return O_OK;
+}
+
+/* kappa_lambda(r): the first candidate minimising D + lambda R over the admitted ones. */
+static void rdo_choose(int64_t R, int K, const unsigned char* adm, const double* D,
+                       const double* Rt, double lambda, int* sel) {
+  for (int64_t r = 0; r < R; r++) {
+    int best = 0;
+    double bv = D[r * K] + lambda * Rt[r * K];
+    for (int k = 1; k < K; k++) {
+      if (!adm[k]) continue;
+      double v = D[r * K + k] + lambda * Rt[r * K + k];
+      if (v < bv) {
+        bv = v;
+        best = k;
+      }
+    }
+    sel[r] = best;
+  }
+}
+
+/* L(lambda) = sum_r R_{r, kappa_lambda(r)} (rows in order). */
+static double rdo_length(int64_t R, int K, const double* Rt, const int* sel) {
+  double L = 0;
+  for (int64_t r = 0; r < R; r++) L += Rt[r * K + sel[r]];
+  return L;
+}
+
+/* Estimated stored bytes of a field set: its b-bit tables and eq. estimate. */
+static int rdo_est_bytes(const int32_t* fields, int64_t nvec, int b, uint32_t V, double kappa,
+                         int64_t R, int cont, double* bytes) {
+  table_t T[ORA_NTAB];
+  memset(T, 0, sizeof T);
+  int rc = tables_count(fields, nvec, T);
+  if (!rc) rc = tables_normalize(T, b);
+  if (!rc)
+    *bytes = estimate_bits(tables_code_length(T, b), n_tiles_of((uint64_t)nvec, V), kappa, T,
+                           (uint64_t)R, cont) / 8.0;
+  tables_free(T);
+  return rc;
+}
+
+/* Refines the baseline (fields, 2p, sigma at scale s and precision b) row by
+ * row.  Each candidate k quantises every row at rho_k s and refits its row
+ * scales (eq. scale_fit, fallback rho_k s mu_r); D_{r,k} is the squared error
+ * sum_j (x_rj - sigma_{r,k} p_rj)^2 with the stored FP32 sigma (coded units, no
+ * dtype snap).  Readings where the paper is silent: a candidate is admitted
+ * (in candidate order) only if every table's index range, joined with those
+ * of the candidates already admitted, stays within 2^b, so that any row
+ * mixture can be coded at b; the +1/2 smoothing runs over those joined ranges;
+ * the lambda bracket starts at 2^-20 sum_r D_{r,0} / sum_r R_{r,0} (2^-20 if
+ * that is 0) and doubles while L > R_budget; ties in the argmin go to the
+ * earlier candidate.  B and B_mix are eq. estimate on the full tensor with
+ * the b-bit tables of the baseline and of the current mixture.  On return the
+ * rows' fields, 2p and sigma are those of their selected candidates. */
+static int rdo_refine(const float* x, const double* mu, int64_t R, int64_t C, double s, int b,
+                      uint32_t V, double kappa, int cont, int K, int sweeps, int32_t* fields,
+                      int32_t* two_p, float* sigma, double* st) {
+  const int64_t cvec = C / 8, nvec = R * cvec, N = R * C;
+  double rho[64];
+  int rc = ora_rdo_ratios(K, rho);
+  if (rc) return rc;
+  int32_t** cf = (int32_t**)calloc((size_t)K, sizeof(int32_t*));
+  int32_t** cp = (int32_t**)calloc((size_t)K, sizeof(int32_t*));
+  float* csig = (float*)malloc((size_t)(R * K) * sizeof(float));
+  double* D = (double*)malloc((size_t)(R * K) * sizeof(double));
+  double* Rt = (double*)malloc((size_t)(R * K) * sizeof(double));
+  int* sel = (int*)calloc((size_t)R, sizeof(int));
+  int* cand = (int*)malloc((size_t)R * sizeof(int));
+  int64_t* all = (int64_t*)malloc((size_t)R * sizeof(int64_t));
+  int32_t* mix = (int32_t*)malloc((size_t)nvec * 9 * sizeof(int32_t));
+  unsigned char adm[64] = {0};
+  double* lq[ORA_NTAB];
+  memset(lq, 0, sizeof lq);
+  if (!cf || !cp || !csig || !D || !Rt || !sel || !cand || !all || !mix) {
+    rc = O_ERR_NOMEM;
+    goto out;
+  }
+  for (int64_t r = 0; r < R; r++) all[r] = r;
+
+  /* candidates: fields, 2p, refit scales, distortions */
+  for (int k = 0; k < K; k++) {
+    cf[k] = (int32_t*)malloc((size_t)nvec * 9 * sizeof(int32_t));
+    cp[k] = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+    if (!cf[k] || !cp[k]) {
+      rc = O_ERR_NOMEM;
+      goto out;
+    }
+    const double sk = rho[k] * s;
+    quantize_rows(x, mu, C, all, R, sk, cf[k], cp[k]);
+    for (int64_t r = 0; r < R; r++) {
+      double num = 0, den = 0;
+      for (int64_t j = 0; j < C; j++) {
+        double p = cp[k][r * C + j] / 2.0;
+        num += (double)x[r * C + j] * p;
+        den += p * p;
+      }
+      double sg = den > 0 ? (num / den < ORA_ETA ? ORA_ETA : num / den) : sk * mu[r];
+      float sgf = (float)sg;
+      double d = 0;
+      for (int64_t j = 0; j < C; j++) {
+        double e = (double)x[r * C + j] - (double)sgf * (cp[k][r * C + j] / 2.0);
+        d += e * e;
+      }
+      csig[r * K + k] = sgf;
+      D[r * K + k] = d;
+    }
+  }
+
+  /* admission and the joined index ranges */
+  int32_t ulo[ORA_NTAB], uhi[ORA_NTAB];
+  for (int t = 0; t < ORA_NTAB; t++) {
+    ulo[t] = INT32_MAX;
+    uhi[t] = INT32_MIN;
+  }
+  ulo[0] = 0;
+  uhi[0] = 1;
+  for (int k = 0; k < K; k++) {
+    int32_t lo[ORA_NTAB], hi[ORA_NTAB];
+    memcpy(lo, ulo, sizeof lo);
+    memcpy(hi, uhi, sizeof hi);
+    for (int64_t v = 0; v < nvec; v++) {
+      const int32_t* f9 = cf[k] + 9 * v;
+      for (int i = 1; i <= 8; i++) {
+        int t = table_of(i, f9[0]);
+        if (f9[i] < lo[t]) lo[t] = f9[i];
+        if (f9[i] > hi[t]) hi[t] = f9[i];
+      }
+    }
+    int fits = 1;
+    for (int t = 1; t < ORA_NTAB; t++)
+      if (hi[t] >= lo[t] && (int64_t)hi[t] - lo[t] + 1 > (1 << b)) fits = 0;
+    if (k == 0 || fits) {
+      adm[k] = 1;
+      memcpy(ulo, lo, sizeof lo);
+      memcpy(uhi, hi, sizeof hi);
+    }
+  }
+
+  /* baseline budget B */
+  double B = 0, Bmix = 0;
+  rc = rdo_est_bytes(cf[0], nvec, b, V, kappa, R, cont, &B);
+  if (rc) goto out;
+  st[ST_RDO_BUDGET_BYTES] = B;
+
+  for (int sw = 0; sw < sweeps; sw++) {
+    /* the current mixture */
+    for (int64_t r = 0; r < R; r++)
+      memcpy(mix + 9 * r * cvec, cf[sel[r]] + 9 * r * cvec, (size_t)cvec * 9 * sizeof(int32_t));
+    /* shared model: counts of the selection plus 1/2 over the joined ranges */
+    for (int t = 0; t < ORA_NTAB; t++) {
+      free(lq[t]);
+      lq[t] = NULL;
+      if (uhi[t] < ulo[t]) continue;
+      int64_t A = (int64_t)uhi[t] - ulo[t] + 1;
+      double* n = (double*)calloc((size_t)A, sizeof(double));
+      lq[t] = (double*)malloc((size_t)A * sizeof(double));
+      if (!n || !lq[t]) {
+        free(n);
+        rc = O_ERR_NOMEM;
+        goto out;
+      }
+      double tot = 0;
+      for (int64_t v = 0; v < nvec; v++) {
+        const int32_t* f9 = mix + 9 * v;
+        if (t == 0) {
+          n[f9[0]] += 1;
+          tot += 1;
+        } else if ((t - 1) / 8 == f9[0]) {
+          n[f9[1 + (t - 1) % 8] - ulo[t]] += 1;
+          tot += 1;
+        }
+      }
+      for (int64_t z = 0; z < A; z++) lq[t][z] = -log2((n[z] + 0.5) / (tot + 0.5 * (double)A));
+      free(n);
+    }
+    /* R_{r,k} [eq. rdo_rate] */
+    for (int k = 0; k < K; k++) {
+      if (!adm[k]) continue;
+      for (int64_t r = 0; r < R; r++) {
+        double acc = 0;
+        for (int64_t jv = 0; jv < cvec; jv++) {
+          const int32_t* f9 = cf[k] + 9 * (r * cvec + jv);
+          acc += lq[0][f9[0]];
+          for (int i = 1; i <= 8; i++) {
+            int t = table_of(i, f9[0]);
+            acc += lq[t][f9[i] - ulo[t]];
+          }
+        }
+        Rt[r * K + k] = acc;
+      }
+    }
+    rc = rdo_est_bytes(mix, nvec, b, V, kappa, R, cont, &Bmix);
+    if (rc) goto out;
+    /* R_budget [eq. rdo_budget] */
+    double budget = rdo_length(R, K, Rt, sel) + 8.0 * (B - Bmix);
+    /* allocation [eq. rdo_choice] */
+    rdo_choose(R, K, adm, D, Rt, 0.0, cand);
+    double lambda = 0;
+    if (rdo_length(R, K, Rt, cand) > budget) {
+      int* tmp = (int*)malloc((size_t)R * sizeof(int));
+      if (!tmp) {
+        rc = O_ERR_NOMEM;
+        goto out;
+      }
+      double sd = 0, sr = 0;
+      for (int64_t r = 0; r < R; r++) {
+        sd += D[r * K];
+        sr += Rt[r * K];
+      }
+      double lo = 0, hi = (sd > 0 && sr > 0) ? ldexp(sd / sr, -20) : ldexp(1.0, -20);
+      for (int it = 0; it < 2000; it++) {
+        rdo_choose(R, K, adm, D, Rt, hi, tmp);
+        if (rdo_length(R, K, Rt, tmp) <= budget) break;
+        hi *= 2.0;
+      }
+      for (int j = 0; j < 20; j++) {
+        double lam = lo == 0 ? hi / 2.0 : sqrt(lo * hi);
+        rdo_choose(R, K, adm, D, Rt, lam, tmp);
+        if (rdo_length(R, K, Rt, tmp) > budget) {
+          lo = lam;
+        } else {
+          hi = lam;
+          memcpy(cand, tmp, (size_t)R * sizeof(int));
+          lambda = lam;
+        }
+      }
+      free(tmp);
+    }
+    memcpy(sel, cand, (size_t)R * sizeof(int));
+    st[ST_RDO_LAMBDA] = lambda;
+  }
+
+  /* the selected rows */
+  int64_t moved = 0;
+  for (int64_t r = 0; r < R; r++) {
+    int k = sel[r];
+    moved += k != 0;
+    memcpy(fields + 9 * r * cvec, cf[k] + 9 * r * cvec, (size_t)cvec * 9 * sizeof(int32_t));
+    memcpy(two_p + r * C, cp[k] + r * C, (size_t)C * sizeof(int32_t));
+    sigma[r] = csig[r * K + k];
+  }
+  st[ST_RDO_ROWS_MOVED] = (double)moved;
+
+out:
+  if (cf)
+    for (int k = 0; k < K; k++) free(cf[k]);
+  if (cp)
+    for (int k = 0; k < K; k++) free(cp[k]);
+  free(cf);
+  free(cp);
+  free(csig);
+  free(D);
+  free(Rt);
+  free(sel);
+  free(cand);
+  free(all);
+  free(mix);
+  for (int t = 0; t < ORA_NTAB; t++) free(lq[t]);
+  return rc;
+}
+
 int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params* prm,
                uint8_t** out_blob, uint64_t* out_size, double* stats) {
   if (!w || !prm || !out_blob || !out_size || R <= 0 || C <= 0 || C % 8) return O_ERR_ARG;
@@ -614,6 +911,7 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
   if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0) return O_ERR_ARG;
   if (prm->container < 0 || prm->container > 2) return O_ERR_ARG;
   if (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) return O_ERR_ARG;
+  if (prm->rdo_candidates > 64 || prm->rdo_sweeps < 0) return O_ERR_ARG;
   if ((R * C) / 8 > 0xFFFFFFFFll || R > 0xFFFFFFFFll || C > 0xFFFFFFFFll) return O_ERR_ARG;
 
   const int64_t N = R * C, nvec = N / 8, cvec = C / 8;
@@ -726,6 +1024,17 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
       sg = s * mu[r];
     }
     sigma[r] = (float)sg;
+  }
+
+  /* optional per-row refinement [3.5; App. C.2]; the tables follow the new fields */
+  if (prm->rdo_candidates > 1 && prm->rdo_sweeps > 0) {
+    rc = rdo_refine(x, mu, R, C, s, b, V, prm->state_credit_bits, cont, prm->rdo_candidates,
+                    prm->rdo_sweeps, fields, two_p, sigma, st);
+    if (rc) goto done;
+    tables_free(T);
+    rc = tables_count(fields, nvec, T);
+    if (!rc) rc = tables_normalize(T, b);
+    if (rc) goto done;
   }
 
   /* tiled interleaved rANS [3.6, eq. rans_encode; App. C.3] */

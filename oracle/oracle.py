@@ -22,7 +22,7 @@ OK, ERR_ARG, ERR_FORMAT, ERR_UNSUPPORTED, ERR_NOMEM, ERR_CORRUPT = 0, -1, -2, -3
 
 STATS = ["scale", "b", "rhat_sub", "r_stored", "bytes", "payload_bits", "cce_full", "n_tiles",
          "max_A", "erel_coded", "erel_orig", "mean_state_bits", "table_bytes", "sample_rows",
-         "escalations", "coarsenings"]
+         "escalations", "coarsenings", "rdo_rows_moved", "rdo_budget_bytes", "rdo_lambda"]
 
 OUT_ITEMSIZE = {BF16: 2, FP16: 2, FP32: 4, FP8: 1, INT8: 1, COORD2: 4}
 OUT_NPTYPE = {BF16: np.uint16, FP16: np.uint16, FP32: np.float32, FP8: np.uint8, INT8: np.int8,
@@ -33,14 +33,16 @@ class Params(C.Structure):
     _fields_ = [("target_bpp", C.c_double), ("tile_vectors", C.c_int32),
                 ("prob_bits", C.c_int32), ("search_steps", C.c_int32),
                 ("container", C.c_int32), ("scale_lo", C.c_double), ("scale_hi", C.c_double),
-                ("sample_vectors", C.c_int64), ("state_credit_bits", C.c_double)]
+                ("sample_vectors", C.c_int64), ("state_credit_bits", C.c_double),
+                ("rdo_candidates", C.c_int32), ("rdo_sweeps", C.c_int32)]
 
 
 def params(target_bpp, tile_vectors=512, prob_bits=0, search_steps=12, container=0,
-           scale_lo=1e-3, scale_hi=8.0, sample_vectors=1 << 18, state_credit_bits=8.0):
+           scale_lo=1e-3, scale_hi=8.0, sample_vectors=1 << 18, state_credit_bits=8.0,
+           rdo_candidates=0, rdo_sweeps=0):
     return Params(float(target_bpp), int(tile_vectors), int(prob_bits), int(search_steps),
                   int(container), float(scale_lo), float(scale_hi), int(sample_vectors),
-                  float(state_credit_bits))
+                  float(state_credit_bits), int(rdo_candidates), int(rdo_sweeps))
 
 
 def build(force: bool = True) -> str:
@@ -78,6 +80,7 @@ def lib():
         L.ora_values.argtypes = [p, i64, C.c_int, p]
         L.ora_quantize.argtypes = [p, C.c_int, i64, i64, C.c_int, dbl, p, p, p]
         L.ora_sample_rows.argtypes = [i64, i64, i64, p]
+        L.ora_rdo_ratios.argtypes = [C.c_int, p]
         L.ora_sample_rows.restype = i64
         L.ora_estimate.argtypes = [p, i64, i64, i32, i32, dbl, i32, p]
         _lib = L
@@ -228,6 +231,13 @@ def quantize(w: np.ndarray, s: float, container: int = 0, dtype=None):
     _chk(lib().ora_quantize(_ptr(w), _dtype_code(w, dtype), R, Cc, container, float(s), _ptr(tp),
                             _ptr(xv), _ptr(mu)), "ora_quantize")
     return tp, xv, mu
+
+
+def rdo_ratios(K: int) -> np.ndarray:
+    """Candidate scale ratios of the per-row refinement (Section 3.5), in candidate order."""
+    out = np.zeros(K, dtype=np.float64)
+    _chk(lib().ora_rdo_ratios(K, _ptr(out)), "ora_rdo_ratios")
+    return out
 
 
 def sample_rows(R: int, Cc: int, sample_vectors: int = 1 << 18) -> np.ndarray:

@@ -403,6 +403,229 @@ struct CpuBackend {
     return EP_OK;
   }
 
+  // Per-row rate-distortion refinement (Section 3.5, eqs. rdo_rate, rdo_budget,
+  // rdo_choice; App. C.2, Alg. rdo) of the full field set at baseline (s, b):
+  // candidates at rho_k s (rho_0 = 1, then log-midpoints of the widest gap of
+  // {0.70, ratios so far, 1.45}), each row refit; D_{r,k} the squared error
+  // with the stored FP32 scale; a candidate joins only if every table's index
+  // range, joined with those already admitted, stays within 2^b; the shared
+  // model adds 1/2 to each count over those joined ranges; B and B_mix are
+  // eq. estimate with the b-bit tables of the baseline and of the mixture; the
+  // lambda bracket starts at 2^-20 sum D / sum R and doubles.  Every sum runs in
+  // the order of the oracle's definition; rows are independent.  On return fl
+  // and sigma hold the selected candidates' fields and scales.
+  int rdo(double s, int b, uint32_t V, double kappa, int cont, int K, int sweeps,
+          std::vector<float>& sigma, uint32_t& moved) {
+    const int64_t nvec = R * cvec;
+    if (K > 64) return fail(EP_ERR_ARG, "ep_encode: at most 64 refinement candidates");
+    std::vector<double> rho((size_t)K);
+    {
+      std::vector<double> pts = {std::log(0.70), 0.0, std::log(1.45)};
+      rho[0] = 1.0;
+      for (int k = 1; k < K; k++) {
+        size_t g = 0;
+        for (size_t i = 1; i + 1 < pts.size(); i++)
+          if (pts[i + 1] - pts[i] > pts[g + 1] - pts[g]) g = i;
+        double mid = 0.5 * (pts[g] + pts[g + 1]);
+        pts.insert(pts.begin() + (long)g + 1, mid);
+        rho[k] = std::exp(mid);
+      }
+    }
+    std::vector<std::vector<int32_t>> cf((size_t)K);
+    std::vector<float> csig((size_t)(R * K));
+    std::vector<double> D((size_t)(R * K)), Rt((size_t)(R * K), 0.0);
+    for (int k = 0; k < K; k++) {
+      const double sk = rho[k] * s;
+      cf[k].resize((size_t)nvec * 9);
+      int32_t* f9 = cf[k].data();
+      parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
+        for (int64_t r = rb; r < re; r++) {
+          const float* xr = x.data() + r * C;
+          double num = 0, den = 0;
+          for (int64_t jv = 0; jv < cvec; jv++) {
+            double y[8];
+            int32_t p2[8];
+            for (int j = 0; j < 8; j++) y[j] = ((double)xr[8 * jv + j] / mu[r]) / sk;
+            em::e8_point(y, p2);
+            em::split_fields(p2, f9 + 9 * (r * cvec + jv));
+            for (int j = 0; j < 8; j++) {
+              double pj = p2[j] / 2.0;
+              num += (double)xr[8 * jv + j] * pj;
+              den += pj * pj;
+            }
+          }
+          double sg = den > 0 ? (num / den < kEta ? kEta : num / den) : sk * mu[r];
+          float sgf = (float)sg;
+          double d = 0;
+          for (int64_t jv = 0; jv < cvec; jv++) {
+            int32_t p2[8];
+            em::join_fields(f9 + 9 * (r * cvec + jv), p2);
+            for (int j = 0; j < 8; j++) {
+              double e = (double)xr[8 * jv + j] - (double)sgf * (p2[j] / 2.0);
+              d += e * e;
+            }
+          }
+          csig[r * K + k] = sgf;
+          D[r * K + k] = d;
+        }
+      });
+    }
+
+    // admission and the joined ranges
+    std::vector<char> adm((size_t)K, 0);
+    int32_t ulo[kTables], uhi[kTables];
+    for (int t = 0; t < kTables; t++) {
+      ulo[t] = std::numeric_limits<int32_t>::max();
+      uhi[t] = std::numeric_limits<int32_t>::min();
+    }
+    ulo[0] = 0;
+    uhi[0] = 1;
+    for (int k = 0; k < K; k++) {
+      int32_t lo[kTables], hi[kTables];
+      std::copy(ulo, ulo + kTables, lo);
+      std::copy(uhi, uhi + kTables, hi);
+      const int32_t* f9 = cf[k].data();
+      for (int64_t v = 0; v < nvec; v++) {
+        const int32_t* q = f9 + 9 * v;
+        for (int i = 1; i <= 8; i++) {
+          int t = table_index(i, q[0]);
+          lo[t] = std::min(lo[t], q[i]);
+          hi[t] = std::max(hi[t], q[i]);
+        }
+      }
+      bool fits = true;
+      for (int t = 1; t < kTables; t++)
+        if (hi[t] >= lo[t] && (int64_t)hi[t] - lo[t] + 1 > (1 << b)) fits = false;
+      if (k == 0 || fits) {
+        adm[k] = 1;
+        std::copy(lo, lo + kTables, ulo);
+        std::copy(hi, hi + kTables, uhi);
+      }
+    }
+
+    const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
+    auto est_bytes = [&](const int32_t* f9) {
+      Model md;
+      count_fields(f9, nvec, T, md);
+      for (auto& tb : md.t) quantize_freqs(tb, b);
+      return estimated_bits(model_bits(md, b), tiles, kappa, md, (uint64_t)R, cont) / 8.0;
+    };
+    auto choose = [&](double lambda, std::vector<int>& out) {
+      for (int64_t r = 0; r < R; r++) {
+        int best = 0;
+        double bv = D[r * K] + lambda * Rt[r * K];
+        for (int k = 1; k < K; k++) {
+          if (!adm[k]) continue;
+          double v = D[r * K + k] + lambda * Rt[r * K + k];
+          if (v < bv) {
+            bv = v;
+            best = k;
+          }
+        }
+        out[r] = best;
+      }
+    };
+    auto length = [&](const std::vector<int>& sel) {
+      double L = 0;
+      for (int64_t r = 0; r < R; r++) L += Rt[r * K + sel[r]];
+      return L;
+    };
+
+    const double B = est_bytes(cf[0].data());
+    std::vector<int> sel((size_t)R, 0), cand((size_t)R), tmp((size_t)R);
+    std::vector<int32_t> mix((size_t)nvec * 9);
+    std::vector<std::vector<double>> lq(kTables);
+    for (int sw = 0; sw < sweeps; sw++) {
+      for (int64_t r = 0; r < R; r++)
+        std::copy(cf[sel[r]].begin() + 9 * r * cvec, cf[sel[r]].begin() + 9 * (r + 1) * cvec,
+                  mix.begin() + 9 * r * cvec);
+      // shared model: counts of the selection plus 1/2 over the joined ranges
+      std::vector<std::vector<double>> n(kTables);
+      double tot[kTables] = {0};
+      for (int t = 0; t < kTables; t++)
+        if (uhi[t] >= ulo[t]) n[t].assign((size_t)((int64_t)uhi[t] - ulo[t] + 1), 0.0);
+      for (int64_t v = 0; v < nvec; v++) {
+        const int32_t* q = mix.data() + 9 * v;
+        n[0][q[0]] += 1;
+        tot[0] += 1;
+        for (int i = 1; i <= 8; i++) {
+          int t = table_index(i, q[0]);
+          n[t][q[i] - ulo[t]] += 1;
+          tot[t] += 1;
+        }
+      }
+      for (int t = 0; t < kTables; t++) {
+        lq[t].assign(n[t].size(), 0.0);
+        const double A = (double)n[t].size();
+        for (size_t z = 0; z < n[t].size(); z++)
+          lq[t][z] = -std::log2((n[t][z] + 0.5) / (tot[t] + 0.5 * A));
+      }
+      // R_{r,k} (eq. rdo_rate)
+      for (int k = 0; k < K; k++) {
+        if (!adm[k]) continue;
+        const int32_t* f9 = cf[k].data();
+        parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
+          for (int64_t r = rb; r < re; r++) {
+            double acc = 0;
+            for (int64_t jv = 0; jv < cvec; jv++) {
+              const int32_t* q = f9 + 9 * (r * cvec + jv);
+              acc += lq[0][q[0]];
+              for (int i = 1; i <= 8; i++) {
+                int t = table_index(i, q[0]);
+                acc += lq[t][q[i] - ulo[t]];
+              }
+            }
+            Rt[r * K + k] = acc;
+          }
+        });
+      }
+      const double Bmix = est_bytes(mix.data());
+      const double budget = length(sel) + 8.0 * (B - Bmix);   // eq. rdo_budget
+      choose(0.0, cand);                                       // eq. rdo_choice
+      if (length(cand) > budget) {
+        double sd = 0, sr = 0;
+        for (int64_t r = 0; r < R; r++) {
+          sd += D[r * K];
+          sr += Rt[r * K];
+        }
+        double lo = 0, hi = (sd > 0 && sr > 0) ? std::ldexp(sd / sr, -20) : std::ldexp(1.0, -20);
+        for (int it = 0; it < 2000; it++) {
+          choose(hi, tmp);
+          if (length(tmp) <= budget) break;
+          hi *= 2.0;
+        }
+        for (int j = 0; j < 20; j++) {
+          double lam = lo == 0 ? hi / 2.0 : std::sqrt(lo * hi);
+          choose(lam, tmp);
+          if (length(tmp) > budget) {
+            lo = lam;
+          } else {
+            hi = lam;
+            cand = tmp;
+          }
+        }
+      }
+      sel = cand;
+    }
+
+    moved = 0;
+    for (int64_t r = 0; r < R; r++) {
+      const int k = sel[r];
+      moved += k != 0;
+      std::copy(cf[k].begin() + 9 * r * cvec, cf[k].begin() + 9 * (r + 1) * cvec,
+                fl.begin() + 9 * r * cvec);
+      sigma[r] = csig[r * K + k];
+    }
+    return EP_OK;
+  }
+
+  int recount(Model& md, int b) {
+    md = Model();
+    count_fields(fl.data(), R * cvec, T, md);
+    for (auto& tb : md.t) quantize_freqs(tb, b);
+    return EP_OK;
+  }
+
   int payload(uint8_t* dst, const std::vector<uint32_t>& offs) {
     parallel_for((int64_t)tile_words.size(), T, [&](int64_t tb, int64_t te, int) {
       for (int64_t t = tb; t < te; t++)
@@ -505,6 +728,11 @@ struct GpuBackend {
     return genc::rans(c, b, V, tiles, lo, A, f.data(), states.data(), words.data());
   }
 
+  int rdo(double, int, uint32_t, double, int, int, int, std::vector<float>&, uint32_t&) {
+    return fail(EP_ERR_UNSUPPORTED, "ep_encode_gpu: the per-row refinement runs in ep_encode_cpu only");
+  }
+  int recount(Model&, int) { return EP_ERR_UNSUPPORTED; }
+
   int payload(uint8_t* dst, const std::vector<uint32_t>& offs) {
     const uint64_t tiles = offs.size() - 1;
     return genc::payload(c, offs.data(), tiles, offs[tiles], dst);
@@ -527,7 +755,8 @@ int check_args(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
   if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0 ||
       prm->container < 0 || prm->container > 2 || !(prm->scale_lo > 0) ||
       !(prm->scale_hi > prm->scale_lo) || prm->sample_vectors < 1 ||
-      (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)))
+      (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) ||
+      prm->rdo_candidates > 64 || prm->rdo_sweeps < 0)
     return fail(EP_ERR_ARG, "ep_encode: invalid parameters");
   if (R > 0xFFFFFFFFll || C > 0xFFFFFFFFll || (R * C) / 8 > 0xFFFFFFFFll)
     return fail(EP_ERR_ARG, "ep_encode: tensor too large");
@@ -607,6 +836,14 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
       sg = s * E.mu[r];
     }
     sigma[r] = (float)sg;
+  }
+
+  // optional per-row refinement (Section 3.5; App. C.2); the tables follow the new fields
+  uint32_t moved = 0;
+  if (prm->rdo_candidates > 1 && prm->rdo_sweeps > 0) {
+    EP_TRY(E.rdo(s, b, V, prm->state_credit_bits, cont, prm->rdo_candidates, prm->rdo_sweeps,
+                 sigma, moved));
+    EP_TRY(E.recount(full, b));
   }
 
   // interleaved rANS per tile (eq. rans_encode; App. C.3)
@@ -702,6 +939,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
     stats->sample_rows = (uint32_t)srows.size();
     stats->escalations = escal;
     stats->coarsenings = coarse;
+    stats->rdo_rows_moved = moved;
   }
   out->data = blob;
   out->size = L.total;

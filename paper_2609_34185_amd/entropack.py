@@ -30,7 +30,8 @@ class EncodeParams(C.Structure):
                 ("prob_bits", C.c_int32), ("search_steps", C.c_int32),
                 ("container", C.c_int32), ("scale_lo", C.c_double), ("scale_hi", C.c_double),
                 ("sample_vectors", C.c_int64), ("state_credit_bits", C.c_double),
-                ("nthreads", C.c_int32), ("reserved", C.c_int32)]
+                ("nthreads", C.c_int32), ("rdo_candidates", C.c_int32),
+                ("rdo_sweeps", C.c_int32), ("reserved", C.c_int32)]
 
 
 class EncodeStats(C.Structure):
@@ -41,7 +42,8 @@ class EncodeStats(C.Structure):
                 ("payload_bits", C.c_uint64), ("prob_bits", C.c_uint32),
                 ("n_tiles", C.c_uint32), ("max_alphabet", C.c_uint32),
                 ("sample_rows", C.c_uint32), ("escalations", C.c_uint32),
-                ("coarsenings", C.c_uint32)]
+                ("coarsenings", C.c_uint32), ("rdo_rows_moved", C.c_uint32),
+                ("reserved", C.c_uint32)]
 
 
 class Blob(C.Structure):

@@ -41,6 +41,12 @@ CASES = [
     ("high_rate", lambda: W.ragged_tensor(5, 64, 1024), 9.0, {}),
     ("b9", lambda: W.ragged_tensor(6, 64, 256), 2.0, dict(prob_bits=9)),
     ("literal_credit", lambda: W.ragged_tensor(7, 96, 512), 3.0, dict(state_credit_bits=16.0)),
+    ("rdo_k5", lambda: W.ragged_tensor(3, 96, 512), 3.0, dict(rdo_candidates=5, rdo_sweeps=1)),
+    ("rdo_k9_t2", lambda: W.attention_projection()[:300], 3.0, dict(rdo_candidates=9, rdo_sweeps=2)),
+    ("rdo_fp8", lambda: W.ragged_tensor(4, 128, 512, scale=0.05), 4.0,
+     dict(container=1, rdo_candidates=5, rdo_sweeps=1)),
+    ("rdo_int8_ragged", lambda: W.ragged_tensor(5, 77, 136), 6.0,
+     dict(container=2, tile_vectors=45, rdo_candidates=4, rdo_sweeps=3)),
 ]
 
 
@@ -51,6 +57,7 @@ def test_encoder_matches_oracle_bytes(E, oracle, name, gen, target, kw):
     b_pr, s_pr = E.encode(w, target, **kw)
     assert np.array_equal(b_pr, b_or)
     assert s_pr["scale"] == s_or["scale"] and s_pr["prob_bits"] == s_or["b"]
+    assert s_pr["rdo_rows_moved"] == s_or["rdo_rows_moved"]
 
 
 def test_encoder_escalation_matches_oracle(E, oracle):

@@ -137,6 +137,13 @@ def test_gpu_encoder_rejects_bad_input(E):
     assert e.value.code == E.ERR_ARG
 
 
+def test_gpu_encoder_refuses_the_row_refinement(E):
+    """The per-row refinement runs in the CPU encoder only; the GPU encoder says so."""
+    with pytest.raises(E.EntroPackError) as e:
+        gpu_encode(E, W.ragged_tensor(3, 32, 256), 3.0, rdo_candidates=5, rdo_sweeps=1)
+    assert e.value.code == E.ERR_UNSUPPORTED
+
+
 def test_gpu_encoder_full_size_attention(E, oracle):
     w = W.attention_projection()
     say("  encode 3072 x 3072 at 3.0 (oracle, then GPU)")
