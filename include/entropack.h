@@ -232,7 +232,7 @@ typedef struct {
   void* d_workspace;         /* device descriptor list (caller-owned memory) */
   int32_t n_layers;
   uint32_t path;             /* decode path shared by all layers */
-  uint32_t total_tasks;      /* 8-tile tasks over all layers */
+  uint32_t total_tasks;      /* 4-tile tasks over all layers */
   uint32_t lds_bytes;        /* LDS of the launch */
   uint32_t reserved[4];
 } ep_stack;

@@ -1392,38 +1392,29 @@ __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
 // encoder starts from for targets up to 7 bpp; otherwise the generic loop
 // takes the task as two four-tile halves.
 constexpr int kChains = 2;                 // chains of the generic loop
-constexpr uint32_t kTilesPerTask = 8;
+// A task is one pass of a wave: two chains of two tiles.  (Small layer lists
+// then spread over more waves, which shortens the serial chain each wave runs.)
+constexpr uint32_t kTilesPerTask = 4;
 static_assert(kChains == 2, "the generic loop and the search steady state advance two chains");
-static_assert(kTilesPerTask == 4 * kChains, "task granularity: two four-tile passes");
+static_assert(kTilesPerTask == 2 * kChains, "task granularity: one four-tile pass");
 
 template <int PATH, int B>
 __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                        uint32_t ring_area, uint32_t task, int32_t* status) {
   const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
   const uint32_t nvec = L.rows * L.cvec;
-  const bool full8 = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
-                     (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
-  if (full8 && L.pay_bytes < kFastOob && (PATH == kPathSearch || B == 11)) {
+  const bool full = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
+                    (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
+  if (full && L.pay_bytes < kFastOob && (PATH == kPathSearch || B == 11)) {
     if constexpr (PATH != kPathSearch && B == 11) {
-      if (lut_task_any<B, PATH == kPathWide>(L, lb, ring_area, t0, status)) {
-        lut_task_any<B, PATH == kPathWide>(L, lb, ring_area, t0 + 4, status);
-        return;
-      }
+      if (lut_task_any<B, PATH == kPathWide>(L, lb, ring_area, t0, status)) return;
     } else if constexpr (PATH == kPathSearch) {
-      if (decode_task_fast_any<PATH, B>(L, lb, ring_area, 2 * task, status)) {
-        decode_task_fast_any<PATH, B>(L, lb, ring_area, 2 * task + 1, status);
-        return;
-      }
+      if (decode_task_fast_any<PATH, B>(L, lb, ring_area, task, status)) return;
     }
   }
-  // generic loop: halves of four tiles (decode_task's task unit)
-  for (uint32_t h = 0; h < 2; h++) {
-    const uint32_t s0 = t0 + 4 * h;
-    if (s0 >= L.tile_end) break;
-    const bool full = (L.V % 32 == 0) && s0 + 4 <= L.tile_end && (uint64_t)(s0 + 4) * L.V <= nvec;
-    if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, 2 * task + h, status);
-    else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, 2 * task + h, status);
-  }
+  // generic loop
+  if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, task, status);
+  else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, task, status);
 }
 
 template <int PATH>

@@ -266,7 +266,7 @@ def test_prepared_stack_decodes_like_the_oracle(E, oracle, mlp_fp8_blobs):
     d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream().cuda_stream
     st = E.stack_prepare(layers, d_ws.data_ptr(), ws, stream)
-    assert st.n_layers == 3 and st.path == 1 and st.total_tasks == 65280 // 8
+    assert st.n_layers == 3 and st.path == 1 and st.total_tasks == 65280 // 4
     refs = {n: oracle.decode(mlp_fp8_blobs[n], oracle.FP8) for n in names}
     for rep in range(2):
         for n in names:
