@@ -142,13 +142,12 @@ __device__ __forceinline__ Hot make_hot(const LayerDev& L) {
 // ---- output snapping (eq. recon) --------------------------------------------
 __device__ __forceinline__ float sat(float y, float m) { return __builtin_amdgcn_fmed3f(y, -m, m); }
 
+// Two FP32 values to a BF16 pair (round to nearest even), converted where it
+// stands: left to itself the compiler keeps the eight FP32 values of a vector
+// alive until its store, which costs a scratch spill in the steady state.
 __device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
-  typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-  typedef float f2 __attribute__((ext_vector_type(2)));
-  f2 v = {a, b};
-  bf2 h = __builtin_convertvector(v, bf2);
   uint32_t r;
-  __builtin_memcpy(&r, &h, 4);
+  asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
   return r;
 }
 
