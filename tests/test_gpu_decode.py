@@ -327,3 +327,51 @@ def test_config4_stack_two_blocks_one_launch(E, oracle):
         refs = list(ex.map(lambda b: oracle.decode(b, oracle.BF16)[0], blobs))
     for (name, _), o, r in zip(layers_np, outs, refs):
         assert np.array_equal(gpu_bits(o), r), name
+
+
+def test_config4_full_stack_sampled_tiles(E, oracle):
+    """The full diffusion-transformer configuration as the benchmark runs it: 30 blocks (180
+    layers, 4.13e9 weights) at 2.5 bpp, one prepared-stack launch to BF16.  The oracle decodes
+    sampled tiles of every layer (first, last and three drawn at random) one by one; each
+    must equal the GPU's output over that tile's weights.  Blobs come from the library's CPU
+    encoder, whose bytes equal the oracle encoder's (checked here on one layer, and on the
+    encoder parity set in the CPU tests)."""
+    blobs, names = [], []
+    with ThreadPoolExecutor(8) as ex:   # blocks drawn ahead while earlier ones encode
+        drawn = list(ex.map(W.dit_block, range(30)))
+    for blk, block in enumerate(drawn):
+        for name, w in block:
+            b, _ = E.encode(w, 2.5)
+            if blk == 0 and name.endswith(".q"):
+                assert np.array_equal(b, oracle.encode(w, 2.5)[0])
+            blobs.append(b)
+            names.append(name)
+        drawn[blk] = None
+        if blk % 5 == 4:
+            say(f"  encoded {blk + 1} blocks")
+    infos = [E.blob_info(b) for b in blobs]
+    dev = [E.to_device(b) for b in blobs]
+    outs = [torch.empty((i.rows, i.cols), dtype=torch.bfloat16, device="cuda") for i in infos]
+    for o in outs:
+        o.view(torch.int16).fill_(0x7FC1)   # NaN pattern: any tile left unwritten fails
+    layers = [(i, d.data_ptr(), o.data_ptr(), 0, E.BF16) for i, d, o in zip(infos, dev, outs)]
+    ws = E.stack_workspace(len(layers))
+    d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    st = E.stack_prepare(layers, d_ws.data_ptr(), ws, stream)
+    assert st.n_layers == 180 and st.total_tasks == 1008000 // 4
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    say("  ep_stack_decode over 180 layers")
+    E.stack_decode(st, status.data_ptr(), stream)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    rng = np.random.default_rng(44)
+    for name, blob, info, o in zip(names, blobs, infos, outs):
+        picks = sorted({0, info.n_tiles - 1, *rng.choice(info.n_tiles, 3, replace=False).tolist()})
+        flat = o.view(torch.int16).view(-1)
+        for t in picks:
+            ref, _ = oracle.decode(blob, oracle.BF16, t, t + 1)
+            a, b = t * 4096, min((t + 1) * 4096, info.rows * info.cols)
+            got = flat[a:b].cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, ref.reshape(-1)[a:b]), (name, t)
+    say("  sampled tiles of all 180 layers equal the oracle")
