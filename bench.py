@@ -288,9 +288,32 @@ def cpu_baseline(items, threads):
     with ThreadPoolExecutor(threads) as ex:
         list(ex.map(run, jobs))
     sec = time.perf_counter() - t
+    # one thread on a bounded sample: the first tensor's first 2048 tiles
+    label, blob, dt = items[0]
+    h = O.header(blob)
+    t1 = min(2048, h["n_tiles"])
+    out, dq = outs[0]
+    t = time.perf_counter()
+    O.decode(blob, ocode[dt], 0, t1, out=out, dequant=dq)
+    sec1 = time.perf_counter() - t
+    w1 = min(t1 * h["V"] * 8, h["rows"] * h["cols"])
     return {"value": weights / sec, "unit": "weights/s", "cores": threads, "kind": "oracle",
             "sample": f"all {len(items)} tensors ({weights} weights) decoded once by the plain C "
-                      f"oracle, tiles split over {threads} threads", "seconds": round(sec, 3)}
+                      f"oracle, tiles split over {threads} threads", "seconds": round(sec, 3),
+            "cpu": cpu_model(),
+            "single_thread": {"value": w1 / sec1, "unit": "weights/s", "cores": 1,
+                              "sample": f"{label}: tiles [0, {t1}) ({w1} weights)",
+                              "seconds": round(sec1, 3)}}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
