@@ -296,20 +296,36 @@ __device__ __forceinline__ void build_lut_table(const LayerDev& L, uint32_t* lut
   const uint32_t A = L.tab_A[t], base = L.tab_base[t];
   const uint32_t u0 = j * per;
   uint32_t* row = lut + t * M;
+  // Lane j owns slots u0 .. u0 + per - 1 but writes them starting at offset
+  // j mod per and wrapping, so that at each store the wave's lanes hit
+  // different banks (in order, every lane would hit the same bank: runs of
+  // per = 32 slots are 128 bytes apart).  Both starting symbols are found
+  // before the loop, so the wrap is a select, not a divergent search.
+  const uint32_t i0 = (uint32_t)j & (per - 1);
   if (A == 0) {
-    for (uint32_t u = u0; u < u0 + per; u++) row[u] = 0;
+    for (uint32_t k = 0; k < per; k++) row[u0 + ((i0 + k) & (per - 1))] = 0;
     return;
   }
-  // largest s with F_s <= u0
-  uint32_t s = 0, n = A;
-  while (n > 1) {
-    uint32_t h = n >> 1;
-    if ((cum[base + s + h] & 0xFFFF) <= u0) s += h;
+  // largest s with F_s <= u, for u = u0 + i0 and u = u0 (the two searches
+  // advance together, their reads in flight at once)
+  uint32_t s_mid = 0, s_start = 0;
+  for (uint32_t n = A; n > 1;) {
+    const uint32_t h = n >> 1;
+    const uint32_t c_mid = cum[base + s_mid + h], c_start = cum[base + s_start + h];
+    if ((c_mid & 0xFFFF) <= u0 + i0) s_mid += h;
+    if ((c_start & 0xFFFF) <= u0) s_start += h;
     n -= h;
   }
   const int field = (t & 7) + 1;
-  uint32_t e = cum[base + s];
-  for (uint32_t u = u0; u < u0 + per; u++) {
+  const uint32_t e_mid = cum[base + s_mid], e_start = cum[base + s_start];
+  uint32_t s = s_mid, e = e_mid;
+  for (uint32_t k = 0; k < per; k++) {
+    const uint32_t i = (i0 + k) & (per - 1);
+    const uint32_t u = u0 + i;
+    if (i == 0) {   // wrapped to the start of the run
+      s = s_start;
+      e = e_start;
+    }
     while (s + 1 < A && (e & 0xFFFF) + (e >> 16) <= u) e = cum[base + ++s];
     uint32_t F = e & 0xFFFF, f = e >> 16;
     const int32_t v = (int32_t)s + L.tab_min[t];
@@ -1385,11 +1401,10 @@ __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
   }
 }
 
-// A wave task is eight tiles.  When all eight are full (V vectors each, V a
-// multiple of 32) every path decodes them in two four-tile steady-state passes
-// (two chains each) -- the slot-table paths at b = 11, the precision the
-// encoder starts from for targets up to 7 bpp; otherwise the generic loop
-// takes the task as two four-tile halves.
+// A wave task is four tiles (two chains of two).  When all four are full (V
+// vectors each, V a multiple of 32) the slot-table paths at b = 11 (the
+// precision the encoder starts from for targets up to 7 bpp) and the search
+// path decode them in a steady-state pass; otherwise the generic loop does.
 constexpr int kChains = 2;                 // chains of the generic loop
 // A task is one pass of a wave: two chains of two tiles.  (Small layer lists
 // then spread over more waves, which shortens the serial chain each wave runs.)
