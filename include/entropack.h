@@ -151,8 +151,8 @@ int ep_encode_cpu(const void* w, int w_dtype, int64_t rows, int64_t cols,
  * (about 10 bytes per weight for the values, fields and rANS words) and frees
  * it before returning, and it synchronises hip_stream: on return the blob is
  * complete.  Errors: as ep_encode_cpu, plus EP_ERR_HIP (device allocation or
- * launch failure) and EP_ERR_UNSUPPORTED (R >= 2^31, or the per-row
- * refinement requested: it runs in ep_encode_cpu only). */
+ * launch failure) and EP_ERR_UNSUPPORTED (R >= 2^31).  The per-row refinement
+ * holds rdo_candidates field sets on the device (4.5 bytes per weight each). */
 int ep_encode_gpu(const void* d_w, int w_dtype, int64_t rows, int64_t cols,
                   const ep_encode_params* params, ep_blob* out, ep_encode_stats* stats,
                   void* hip_stream);

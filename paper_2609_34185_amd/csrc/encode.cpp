@@ -13,6 +13,7 @@
 // (counts) and tiles (rANS); every reduction that involves rounding runs in a
 // fixed order, so the blob does not depend on the thread count.
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -403,228 +404,130 @@ struct CpuBackend {
     return EP_OK;
   }
 
-  // Per-row rate-distortion refinement (Section 3.5, eqs. rdo_rate, rdo_budget,
-  // rdo_choice; App. C.2, Alg. rdo) of the full field set at baseline (s, b):
-  // candidates at rho_k s (rho_0 = 1, then log-midpoints of the widest gap of
-  // {0.70, ratios so far, 1.45}), each row refit; D_{r,k} the squared error
-  // with the stored FP32 scale; a candidate joins only if every table's index
-  // range, joined with those already admitted, stays within 2^b; the shared
-  // model adds 1/2 to each count over those joined ranges; B and B_mix are
-  // eq. estimate with the b-bit tables of the baseline and of the mixture; the
-  // lambda bracket starts at 2^-20 sum D / sum R and doubles.  Every sum runs in
-  // the order of the oracle's definition; rows are independent.  On return fl
-  // and sigma hold the selected candidates' fields and scales.
-  int rdo(double s, int b, uint32_t V, double kappa, int cont, int K, int sweeps,
-          std::vector<float>& sigma, uint32_t& moved) {
-    const int64_t nvec = R * cvec;
-    if (K > 64) return fail(EP_ERR_ARG, "ep_encode: at most 64 refinement candidates");
-    std::vector<double> rho((size_t)K);
-    {
-      std::vector<double> pts = {std::log(0.70), 0.0, std::log(1.45)};
-      rho[0] = 1.0;
-      for (int k = 1; k < K; k++) {
-        size_t g = 0;
-        for (size_t i = 1; i + 1 < pts.size(); i++)
-          if (pts[i + 1] - pts[i] > pts[g + 1] - pts[g]) g = i;
-        double mid = 0.5 * (pts[g] + pts[g + 1]);
-        pts.insert(pts.begin() + (long)g + 1, mid);
-        rho[k] = std::exp(mid);
-      }
-    }
-    std::vector<std::vector<int32_t>> cf((size_t)K);
-    std::vector<float> csig((size_t)(R * K));
-    std::vector<double> D((size_t)(R * K)), Rt((size_t)(R * K), 0.0);
-    for (int k = 0; k < K; k++) {
-      const double sk = rho[k] * s;
-      cf[k].resize((size_t)nvec * 9);
-      int32_t* f9 = cf[k].data();
-      parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
-        for (int64_t r = rb; r < re; r++) {
-          const float* xr = x.data() + r * C;
-          double num = 0, den = 0;
-          for (int64_t jv = 0; jv < cvec; jv++) {
-            double y[8];
-            int32_t p2[8];
-            for (int j = 0; j < 8; j++) y[j] = ((double)xr[8 * jv + j] / mu[r]) / sk;
-            em::e8_point(y, p2);
-            em::split_fields(p2, f9 + 9 * (r * cvec + jv));
-            for (int j = 0; j < 8; j++) {
-              double pj = p2[j] / 2.0;
-              num += (double)xr[8 * jv + j] * pj;
-              den += pj * pj;
-            }
-          }
-          double sg = den > 0 ? (num / den < kEta ? kEta : num / den) : sk * mu[r];
-          float sgf = (float)sg;
-          double d = 0;
-          for (int64_t jv = 0; jv < cvec; jv++) {
-            int32_t p2[8];
-            em::join_fields(f9 + 9 * (r * cvec + jv), p2);
-            for (int j = 0; j < 8; j++) {
-              double e = (double)xr[8 * jv + j] - (double)sgf * (p2[j] / 2.0);
-              d += e * e;
-            }
-          }
-          csig[r * K + k] = sgf;
-          D[r * K + k] = d;
-        }
-      });
-    }
+  // ---- per-row refinement primitives (the algorithm is rdo_run below) ----
+  std::vector<std::vector<int32_t>> cf;   // candidate field sets
 
-    // admission and the joined ranges
-    std::vector<char> adm((size_t)K, 0);
-    int32_t ulo[kTables], uhi[kTables];
+  int rdo_alloc(int K) {
+    cf.assign((size_t)K, {});
+    return EP_OK;
+  }
+  // candidate k <- every row's fields at scale sk; extents; refit sums in element order
+  int rdo_quantize(int k, double sk, int32_t* lo, int32_t* hi, double* num, double* den) {
+    cf[k].resize((size_t)(R * cvec) * 9);
+    int32_t* f9 = cf[k].data();
+    parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
+      for (int64_t r = rb; r < re; r++) {
+        const float* xr = x.data() + r * C;
+        double sn = 0, sd = 0;
+        for (int64_t jv = 0; jv < cvec; jv++) {
+          double y[8];
+          int32_t p2[8];
+          for (int j = 0; j < 8; j++) y[j] = ((double)xr[8 * jv + j] / mu[r]) / sk;
+          em::e8_point(y, p2);
+          em::split_fields(p2, f9 + 9 * (r * cvec + jv));
+          for (int j = 0; j < 8; j++) {
+            double pj = p2[j] / 2.0;
+            sn += (double)xr[8 * jv + j] * pj;
+            sd += pj * pj;
+          }
+        }
+        num[r] = sn;
+        den[r] = sd;
+      }
+    });
+    extents(f9, lo, hi);
+    return EP_OK;
+  }
+  void extents(const int32_t* f9, int32_t* lo, int32_t* hi) const {
     for (int t = 0; t < kTables; t++) {
-      ulo[t] = std::numeric_limits<int32_t>::max();
-      uhi[t] = std::numeric_limits<int32_t>::min();
+      lo[t] = std::numeric_limits<int32_t>::max();
+      hi[t] = std::numeric_limits<int32_t>::min();
     }
-    ulo[0] = 0;
-    uhi[0] = 1;
-    for (int k = 0; k < K; k++) {
-      int32_t lo[kTables], hi[kTables];
-      std::copy(ulo, ulo + kTables, lo);
-      std::copy(uhi, uhi + kTables, hi);
-      const int32_t* f9 = cf[k].data();
-      for (int64_t v = 0; v < nvec; v++) {
-        const int32_t* q = f9 + 9 * v;
-        for (int i = 1; i <= 8; i++) {
-          int t = table_index(i, q[0]);
-          lo[t] = std::min(lo[t], q[i]);
-          hi[t] = std::max(hi[t], q[i]);
-        }
-      }
-      bool fits = true;
-      for (int t = 1; t < kTables; t++)
-        if (hi[t] >= lo[t] && (int64_t)hi[t] - lo[t] + 1 > (1 << b)) fits = false;
-      if (k == 0 || fits) {
-        adm[k] = 1;
-        std::copy(lo, lo + kTables, ulo);
-        std::copy(hi, hi + kTables, uhi);
+    for (int64_t v = 0; v < R * cvec; v++) {
+      const int32_t* q = f9 + 9 * v;
+      for (int i = 1; i <= 8; i++) {
+        int t = table_index(i, q[0]);
+        lo[t] = std::min(lo[t], q[i]);
+        hi[t] = std::max(hi[t], q[i]);
       }
     }
-
-    const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
-    auto est_bytes = [&](const int32_t* f9) {
-      Model md;
-      count_fields(f9, nvec, T, md);
-      for (auto& tb : md.t) quantize_freqs(tb, b);
-      return estimated_bits(model_bits(md, b), tiles, kappa, md, (uint64_t)R, cont) / 8.0;
-    };
-    auto choose = [&](double lambda, std::vector<int>& out) {
-      for (int64_t r = 0; r < R; r++) {
-        int best = 0;
-        double bv = D[r * K] + lambda * Rt[r * K];
-        for (int k = 1; k < K; k++) {
-          if (!adm[k]) continue;
-          double v = D[r * K + k] + lambda * Rt[r * K + k];
-          if (v < bv) {
-            bv = v;
-            best = k;
+  }
+  // D_r = sum_j (x_rj - sigma_r p_rj)^2 of candidate k, in element order
+  int rdo_distortion(int k, const float* sig, double* D) {
+    const int32_t* f9 = cf[k].data();
+    parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
+      for (int64_t r = rb; r < re; r++) {
+        const float* xr = x.data() + r * C;
+        double d = 0;
+        for (int64_t jv = 0; jv < cvec; jv++) {
+          int32_t p2[8];
+          em::join_fields(f9 + 9 * (r * cvec + jv), p2);
+          for (int j = 0; j < 8; j++) {
+            double e = (double)xr[8 * jv + j] - (double)sig[r] * (p2[j] / 2.0);
+            d += e * e;
           }
         }
-        out[r] = best;
+        D[r] = d;
       }
-    };
-    auto length = [&](const std::vector<int>& sel) {
-      double L = 0;
-      for (int64_t r = 0; r < R; r++) L += Rt[r * K + sel[r]];
-      return L;
-    };
-
-    const double B = est_bytes(cf[0].data());
-    std::vector<int> sel((size_t)R, 0), cand((size_t)R), tmp((size_t)R);
-    std::vector<int32_t> mix((size_t)nvec * 9);
-    std::vector<std::vector<double>> lq(kTables);
-    for (int sw = 0; sw < sweeps; sw++) {
-      for (int64_t r = 0; r < R; r++)
-        std::copy(cf[sel[r]].begin() + 9 * r * cvec, cf[sel[r]].begin() + 9 * (r + 1) * cvec,
-                  mix.begin() + 9 * r * cvec);
-      // shared model: counts of the selection plus 1/2 over the joined ranges
-      std::vector<std::vector<double>> n(kTables);
-      double tot[kTables] = {0};
-      for (int t = 0; t < kTables; t++)
-        if (uhi[t] >= ulo[t]) n[t].assign((size_t)((int64_t)uhi[t] - ulo[t] + 1), 0.0);
-      for (int64_t v = 0; v < nvec; v++) {
-        const int32_t* q = mix.data() + 9 * v;
-        n[0][q[0]] += 1;
-        tot[0] += 1;
-        for (int i = 1; i <= 8; i++) {
-          int t = table_index(i, q[0]);
-          n[t][q[i] - ulo[t]] += 1;
-          tot[t] += 1;
-        }
-      }
-      for (int t = 0; t < kTables; t++) {
-        lq[t].assign(n[t].size(), 0.0);
-        const double A = (double)n[t].size();
-        for (size_t z = 0; z < n[t].size(); z++)
-          lq[t][z] = -std::log2((n[t][z] + 0.5) / (tot[t] + 0.5 * A));
-      }
-      // R_{r,k} (eq. rdo_rate)
-      for (int k = 0; k < K; k++) {
-        if (!adm[k]) continue;
-        const int32_t* f9 = cf[k].data();
-        parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
-          for (int64_t r = rb; r < re; r++) {
-            double acc = 0;
-            for (int64_t jv = 0; jv < cvec; jv++) {
-              const int32_t* q = f9 + 9 * (r * cvec + jv);
-              acc += lq[0][q[0]];
-              for (int i = 1; i <= 8; i++) {
-                int t = table_index(i, q[0]);
-                acc += lq[t][q[i] - ulo[t]];
-              }
-            }
-            Rt[r * K + k] = acc;
-          }
-        });
-      }
-      const double Bmix = est_bytes(mix.data());
-      const double budget = length(sel) + 8.0 * (B - Bmix);   // eq. rdo_budget
-      choose(0.0, cand);                                       // eq. rdo_choice
-      if (length(cand) > budget) {
-        double sd = 0, sr = 0;
-        for (int64_t r = 0; r < R; r++) {
-          sd += D[r * K];
-          sr += Rt[r * K];
-        }
-        double lo = 0, hi = (sd > 0 && sr > 0) ? std::ldexp(sd / sr, -20) : std::ldexp(1.0, -20);
-        for (int it = 0; it < 2000; it++) {
-          choose(hi, tmp);
-          if (length(tmp) <= budget) break;
-          hi *= 2.0;
-        }
-        for (int j = 0; j < 20; j++) {
-          double lam = lo == 0 ? hi / 2.0 : std::sqrt(lo * hi);
-          choose(lam, tmp);
-          if (length(tmp) > budget) {
-            lo = lam;
-          } else {
-            hi = lam;
-            cand = tmp;
-          }
-        }
-      }
-      sel = cand;
+    });
+    return EP_OK;
+  }
+  // R_r of candidate k: sum of lq over the row's symbols in symbol order
+  int rdo_rate(int k, const double* lq, const int32_t* lo, const int32_t* A, double* Rt) {
+    uint64_t base[kTables];
+    uint64_t at = 0;
+    for (int t = 0; t < kTables; t++) {
+      base[t] = at;
+      at += (uint64_t)A[t];
     }
-
-    moved = 0;
-    for (int64_t r = 0; r < R; r++) {
-      const int k = sel[r];
-      moved += k != 0;
-      std::copy(cf[k].begin() + 9 * r * cvec, cf[k].begin() + 9 * (r + 1) * cvec,
+    const int32_t* f9 = cf[k].data();
+    parallel_for(R, T, [&](int64_t rb, int64_t re, int) {
+      for (int64_t r = rb; r < re; r++) {
+        double acc = 0;
+        for (int64_t jv = 0; jv < cvec; jv++) {
+          const int32_t* q = f9 + 9 * (r * cvec + jv);
+          acc += lq[q[0]];
+          for (int i = 1; i <= 8; i++) {
+            int t = table_index(i, q[0]);
+            acc += lq[base[t] + (uint64_t)(q[i] - lo[t])];
+          }
+        }
+        Rt[r] = acc;
+      }
+    });
+    return EP_OK;
+  }
+  // the full field set <- row r of candidate sel[r]; its extents
+  int rdo_select(const int32_t* sel, int32_t* lo, int32_t* hi) {
+    fl.resize((size_t)(R * cvec) * 9);
+    for (int64_t r = 0; r < R; r++)
+      std::copy(cf[sel[r]].begin() + 9 * r * cvec, cf[sel[r]].begin() + 9 * (r + 1) * cvec,
                 fl.begin() + 9 * r * cvec);
-      sigma[r] = csig[r * K + k];
+    extents(fl.data(), lo, hi);
+    return EP_OK;
+  }
+  // counts of candidate k, or of the full set for k < 0 (layout as the GPU backend's)
+  int rdo_counts(int k, const int32_t* lo, const int32_t* A, uint64_t* n) {
+    const int32_t* f9 = k < 0 ? fl.data() : cf[k].data();
+    uint64_t base[kTables];
+    uint64_t at = 0;
+    for (int t = 0; t < kTables; t++) {
+      base[t] = at;
+      at += (uint64_t)A[t];
+    }
+    std::fill(n, n + at, 0);
+    for (int64_t v = 0; v < R * cvec; v++) {
+      const int32_t* q = f9 + 9 * v;
+      n[q[0]]++;
+      for (int i = 1; i <= 8; i++) {
+        int t = table_index(i, q[0]);
+        n[base[t] + (uint64_t)(q[i] - lo[t])]++;
+      }
     }
     return EP_OK;
   }
 
-  int recount(Model& md, int b) {
-    md = Model();
-    count_fields(fl.data(), R * cvec, T, md);
-    for (auto& tb : md.t) quantize_freqs(tb, b);
-    return EP_OK;
-  }
+
 
   int payload(uint8_t* dst, const std::vector<uint32_t>& offs) {
     parallel_for((int64_t)tile_words.size(), T, [&](int64_t tb, int64_t te, int) {
@@ -728,10 +631,33 @@ struct GpuBackend {
     return genc::rans(c, b, V, tiles, lo, A, f.data(), states.data(), words.data());
   }
 
-  int rdo(double, int, uint32_t, double, int, int, int, std::vector<float>&, uint32_t&) {
-    return fail(EP_ERR_UNSUPPORTED, "ep_encode_gpu: the per-row refinement runs in ep_encode_cpu only");
+  // ---- per-row refinement primitives (device passes; see CpuBackend) ----
+  int rdo_alloc(int K) { return genc::cand_alloc(c, K); }
+  int rdo_quantize(int k, double sk, int32_t* lo, int32_t* hi, double* num, double* den) {
+    int32_t lohi[2 * kTables];
+    EP_TRY_G(genc::cand_quantize(c, k, sk, lohi));
+    for (int t = 0; t < kTables; t++) {
+      lo[t] = t ? lohi[2 * t] : std::numeric_limits<int32_t>::max();
+      hi[t] = t ? lohi[2 * t + 1] : std::numeric_limits<int32_t>::min();
+    }
+    return genc::cand_refit(c, k, num, den);
   }
-  int recount(Model&, int) { return EP_ERR_UNSUPPORTED; }
+  int rdo_distortion(int k, const float* sig, double* D) { return genc::cand_distortion(c, k, sig, D); }
+  int rdo_rate(int k, const double* lq, const int32_t* lo, const int32_t* A, double* Rt) {
+    return genc::cand_rate(c, k, lq, lo, A, Rt);
+  }
+  int rdo_select(const int32_t* sel, int32_t* lo, int32_t* hi) {
+    int32_t lohi[2 * kTables];
+    EP_TRY_G(genc::cand_select(c, sel, lohi));
+    for (int t = 0; t < kTables; t++) {
+      lo[t] = t ? lohi[2 * t] : std::numeric_limits<int32_t>::max();
+      hi[t] = t ? lohi[2 * t + 1] : std::numeric_limits<int32_t>::min();
+    }
+    return EP_OK;
+  }
+  int rdo_counts(int k, const int32_t* lo, const int32_t* A, uint64_t* n) {
+    return genc::cand_count(c, k, lo, A, n);
+  }
 
   int payload(uint8_t* dst, const std::vector<uint32_t>& offs) {
     const uint64_t tiles = offs.size() - 1;
@@ -743,6 +669,206 @@ struct GpuBackend {
     return genc::errors(c, sigma.data(), rdt, acc.data());
   }
 };
+
+// Per-row rate-distortion refinement (Section 3.5, eqs. rdo_rate, rdo_budget,
+// rdo_choice; App. C.2, Alg. rdo) of the full field set at baseline (s, b),
+// over a backend's bulk passes: candidates at rho_k s (rho_0 = 1, then
+// log-midpoints of the widest gap of {0.70, ratios so far, 1.45}), each row
+// refit; D_{r,k} the squared error with the stored FP32 scale; a candidate
+// joins only if every table's index range, joined with those already
+// admitted, stays within 2^b; the shared model adds 1/2 to each count over
+// those joined ranges; B and B_mix are eq. estimate with the b-bit tables of
+// the baseline and of the mixture; the lambda bracket starts at
+// 2^-20 sum D / sum R and doubles.  Every sum runs in the order of the oracle's
+// definition.  On return the backend's full field set, `full` (b-bit) and
+// sigma are those of the selected candidates.
+template <class BK>
+int rdo_run(BK& E, int64_t R, int64_t cvec, const std::vector<double>& mu, double s, int b,
+            uint32_t V, double kappa, int cont, int K, int sweeps, std::vector<float>& sigma,
+            Model& full, uint32_t& moved) {
+  if (K > 64) return fail(EP_ERR_ARG, "ep_encode: at most 64 refinement candidates");
+  const int64_t nvec = R * cvec;
+  std::vector<double> rho((size_t)K);
+  {
+    std::vector<double> pts = {std::log(0.70), 0.0, std::log(1.45)};
+    rho[0] = 1.0;
+    for (int k = 1; k < K; k++) {
+      size_t g = 0;
+      for (size_t i = 1; i + 1 < pts.size(); i++)
+        if (pts[i + 1] - pts[i] > pts[g + 1] - pts[g]) g = i;
+      double mid = 0.5 * (pts[g] + pts[g + 1]);
+      pts.insert(pts.begin() + (long)g + 1, mid);
+      rho[k] = std::exp(mid);
+    }
+  }
+  EP_TRY_G(E.rdo_alloc(K));
+  std::vector<float> csig((size_t)(R * K)), sk_sig((size_t)R);
+  std::vector<double> D((size_t)(R * K)), Rt((size_t)(R * K), 0.0), col((size_t)R);
+  std::vector<double> num((size_t)R), den((size_t)R);
+  std::vector<std::array<int32_t, kTables>> clo((size_t)K), chi((size_t)K);
+  for (int k = 0; k < K; k++) {
+    const double sk = rho[k] * s;
+    EP_TRY_G(E.rdo_quantize(k, sk, clo[k].data(), chi[k].data(), num.data(), den.data()));
+    for (int64_t r = 0; r < R; r++) {
+      double sg = den[r] > 0 ? (num[r] / den[r] < kEta ? kEta : num[r] / den[r]) : sk * mu[r];
+      sk_sig[r] = (float)sg;
+      csig[r * K + k] = sk_sig[r];
+    }
+    EP_TRY_G(E.rdo_distortion(k, sk_sig.data(), col.data()));
+    for (int64_t r = 0; r < R; r++) D[r * K + k] = col[r];
+  }
+
+  // admission and the joined ranges
+  std::vector<char> adm((size_t)K, 0);
+  int32_t ulo[kTables], uhi[kTables];
+  for (int t = 0; t < kTables; t++) {
+    ulo[t] = std::numeric_limits<int32_t>::max();
+    uhi[t] = std::numeric_limits<int32_t>::min();
+  }
+  ulo[0] = 0;
+  uhi[0] = 1;
+  for (int k = 0; k < K; k++) {
+    int32_t lo[kTables], hi[kTables];
+    bool fits = true;
+    for (int t = 0; t < kTables; t++) {
+      lo[t] = std::min(ulo[t], clo[k][t]);
+      hi[t] = std::max(uhi[t], chi[k][t]);
+      if (t && hi[t] >= lo[t] && (int64_t)hi[t] - lo[t] + 1 > (1 << b)) fits = false;
+    }
+    if (k == 0 || fits) {
+      adm[k] = 1;
+      std::copy(lo, lo + kTables, ulo);
+      std::copy(hi, hi + kTables, uhi);
+    }
+  }
+
+  const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
+  // b-bit model of a field set with extents lo/hi (table 0: [0, 1])
+  auto model_of = [&](int k, const int32_t* lo, const int32_t* hi, Model& md) {
+    int32_t mlo[kTables], mA[kTables];
+    uint64_t cells = 0;
+    for (int t = 0; t < kTables; t++) {
+      const int32_t l = t ? lo[t] : 0, h = t ? hi[t] : 1;
+      mlo[t] = h >= l ? l : 0;
+      mA[t] = h >= l ? (int32_t)((int64_t)h - l + 1) : 0;
+      cells += (uint64_t)mA[t];
+    }
+    std::vector<uint64_t> n(cells);
+    const int rc = E.rdo_counts(k, mlo, mA, n.data());
+    if (rc != EP_OK) return rc;
+    md = Model();
+    uint64_t at = 0;
+    for (int t = 0; t < kTables; t++) {
+      Table& tb = md.t[t];
+      tb.lo = mlo[t];
+      tb.A = mA[t];
+      tb.n.assign(n.begin() + (long)at, n.begin() + (long)(at + mA[t]));
+      tb.f.assign((size_t)mA[t], 0);
+      at += (uint64_t)mA[t];
+    }
+    return (int)EP_OK;
+  };
+  auto est_bytes = [&](Model& md) {
+    for (auto& tb : md.t) quantize_freqs(tb, b);
+    return estimated_bits(model_bits(md, b), tiles, kappa, md, (uint64_t)R, cont) / 8.0;
+  };
+  auto choose = [&](double lambda, std::vector<int32_t>& out) {
+    for (int64_t r = 0; r < R; r++) {
+      int best = 0;
+      double bv = D[r * K] + lambda * Rt[r * K];
+      for (int k = 1; k < K; k++) {
+        if (!adm[k]) continue;
+        double v = D[r * K + k] + lambda * Rt[r * K + k];
+        if (v < bv) {
+          bv = v;
+          best = k;
+        }
+      }
+      out[r] = best;
+    }
+  };
+  auto length = [&](const std::vector<int32_t>& sel) {
+    double L = 0;
+    for (int64_t r = 0; r < R; r++) L += Rt[r * K + sel[r]];
+    return L;
+  };
+
+  Model md;
+  EP_TRY_G(model_of(0, clo[0].data(), chi[0].data(), md));
+  const double B = est_bytes(md);
+  std::vector<int32_t> sel((size_t)R, 0), cand((size_t)R), tmp((size_t)R);
+  int32_t ulo_t[kTables], uA[kTables];
+  uint64_t ucells = 0;
+  for (int t = 0; t < kTables; t++) {
+    ulo_t[t] = uhi[t] >= ulo[t] ? ulo[t] : 0;
+    uA[t] = uhi[t] >= ulo[t] ? (int32_t)((int64_t)uhi[t] - ulo[t] + 1) : 0;
+    ucells += (uint64_t)uA[t];
+  }
+  std::vector<double> lq(ucells);
+  for (int sw = 0; sw < sweeps; sw++) {
+    int32_t mlo[kTables], mhi[kTables];
+    EP_TRY_G(E.rdo_select(sel.data(), mlo, mhi));
+    EP_TRY_G(model_of(-1, mlo, mhi, md));
+    // shared model: counts of the selection plus 1/2 over the joined ranges
+    uint64_t at = 0;
+    for (int t = 0; t < kTables; t++) {
+      double tot = 0;
+      for (int32_t z = 0; z < md.t[t].A; z++) tot += (double)md.t[t].n[z];
+      const double A = (double)uA[t];
+      for (int32_t z = 0; z < uA[t]; z++) {
+        const int32_t v = ulo_t[t] + z;
+        const int32_t mz = v - md.t[t].lo;
+        const double n = (mz >= 0 && mz < md.t[t].A) ? (double)md.t[t].n[mz] : 0.0;
+        lq[at + z] = -std::log2((n + 0.5) / (tot + 0.5 * A));
+      }
+      at += (uint64_t)uA[t];
+    }
+    // R_{r,k} (eq. rdo_rate)
+    for (int k = 0; k < K; k++) {
+      if (!adm[k]) continue;
+      EP_TRY_G(E.rdo_rate(k, lq.data(), ulo_t, uA, col.data()));
+      for (int64_t r = 0; r < R; r++) Rt[r * K + k] = col[r];
+    }
+    const double Bmix = est_bytes(md);
+    const double budget = length(sel) + 8.0 * (B - Bmix);   // eq. rdo_budget
+    choose(0.0, cand);                                       // eq. rdo_choice
+    if (length(cand) > budget) {
+      double sd = 0, sr = 0;
+      for (int64_t r = 0; r < R; r++) {
+        sd += D[r * K];
+        sr += Rt[r * K];
+      }
+      double lo = 0, hi = (sd > 0 && sr > 0) ? std::ldexp(sd / sr, -20) : std::ldexp(1.0, -20);
+      for (int it = 0; it < 2000; it++) {
+        choose(hi, tmp);
+        if (length(tmp) <= budget) break;
+        hi *= 2.0;
+      }
+      for (int j = 0; j < 20; j++) {
+        double lam = lo == 0 ? hi / 2.0 : std::sqrt(lo * hi);
+        choose(lam, tmp);
+        if (length(tmp) > budget) {
+          lo = lam;
+        } else {
+          hi = lam;
+          cand = tmp;
+        }
+      }
+    }
+    sel = cand;
+  }
+
+  moved = 0;
+  for (int64_t r = 0; r < R; r++) {
+    moved += sel[r] != 0;
+    sigma[r] = csig[r * K + sel[r]];
+  }
+  int32_t flo[kTables], fhi[kTables];
+  EP_TRY_G(E.rdo_select(sel.data(), flo, fhi));
+  EP_TRY_G(model_of(-1, flo, fhi, full));
+  for (auto& tb : full.t) quantize_freqs(tb, b);
+  return EP_OK;
+}
 
 int check_args(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
                ep_blob* out) {
@@ -763,11 +889,6 @@ int check_args(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
   return EP_OK;
 }
 
-#define EP_TRY(call)          \
-  do {                        \
-    int rc_ = (call);         \
-    if (rc_ != EP_OK) return rc_; \
-  } while (0)
 
 template <class BK>
 int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
@@ -777,7 +898,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
   const uint32_t V = (uint32_t)prm->tile_vectors;
 
   // input values, container route, row RMS (Section 3.2; App. A.6, B.1)
-  EP_TRY(E.prep(cont));
+  EP_TRY_G(E.prep(cont));
 
   // scale search on a fixed row sample (Alg. rate selection; App. C.1)
   std::vector<int64_t> srows = pick_rows(R, C, prm->sample_vectors);
@@ -798,7 +919,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
     for (int it = 0; it < prm->search_steps; it++) {
       s = std::sqrt(lo * hi);
       Model sm;
-      EP_TRY(E.quantize(sample_all ? nullptr : &srows, s, sm, 1 << b, nullptr, nullptr));
+      EP_TRY_G(E.quantize(sample_all ? nullptr : &srows, s, sm, 1 << b, nullptr, nullptr));
       if (sm.max_field_alphabet() > (1 << b)) {
         rhat = std::numeric_limits<double>::infinity();
       } else {
@@ -810,7 +931,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
       else hi = s;
     }
     s = std::sqrt(lo * hi);
-    EP_TRY(E.quantize(nullptr, s, full, 1 << b, num.data(), den.data()));
+    EP_TRY_G(E.quantize(nullptr, s, full, 1 << b, num.data(), den.data()));
     fits = full.max_field_alphabet() <= (1 << b);
     if (!fits) escal++;
   }
@@ -819,7 +940,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
     b = 15;
     while (full.max_field_alphabet() > (1 << b)) {
       s = 1.05 * s * (double)full.max_field_alphabet() / (double)(1 << b);
-      EP_TRY(E.quantize(nullptr, s, full, 1 << b, num.data(), den.data()));
+      EP_TRY_G(E.quantize(nullptr, s, full, 1 << b, num.data(), den.data()));
       coarse++;
     }
   }
@@ -841,16 +962,15 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
   // optional per-row refinement (Section 3.5; App. C.2); the tables follow the new fields
   uint32_t moved = 0;
   if (prm->rdo_candidates > 1 && prm->rdo_sweeps > 0) {
-    EP_TRY(E.rdo(s, b, V, prm->state_credit_bits, cont, prm->rdo_candidates, prm->rdo_sweeps,
-                 sigma, moved));
-    EP_TRY(E.recount(full, b));
+    EP_TRY_G(rdo_run(E, R, C / 8, E.mu, s, b, V, prm->state_credit_bits, cont, prm->rdo_candidates,
+                   prm->rdo_sweeps, sigma, full, moved));
   }
 
   // interleaved rANS per tile (eq. rans_encode; App. C.3)
   const uint64_t tiles = ((uint64_t)nvec + V - 1) / V;
   std::vector<uint32_t> states;
   std::vector<uint64_t> tw;
-  EP_TRY(E.rans(full, b, V, tiles, states, tw));
+  EP_TRY_G(E.rans(full, b, V, tiles, states, tw));
   uint64_t words = 0;
   std::vector<uint32_t> offs(tiles + 1);
   for (uint64_t t = 0; t < tiles; t++) {
@@ -950,7 +1070,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
 
 int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
                ep_blob* out, ep_encode_stats* stats) {
-  EP_TRY(check_args(w, w_dtype, R, C, prm, out));
+  EP_TRY_G(check_args(w, w_dtype, R, C, prm, out));
   try {
     CpuBackend E;
     E.w = w;
@@ -968,11 +1088,11 @@ int encode_cpu(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
 
 int encode_gpu(const void* d_w, int w_dtype, int64_t R, int64_t C, const ep_encode_params* prm,
                ep_blob* out, ep_encode_stats* stats, void* stream) {
-  EP_TRY(check_args(d_w, w_dtype, R, C, prm, out));
+  EP_TRY_G(check_args(d_w, w_dtype, R, C, prm, out));
   try {
     GpuBackend E;
     E.R = R;
-    EP_TRY(genc::open(&E.c, d_w, w_dtype, R, C, prm->container, stream));
+    EP_TRY_G(genc::open(&E.c, d_w, w_dtype, R, C, prm->container, stream));
     return encode_impl(E, w_dtype, R, C, prm, out, stats);
   } catch (const std::bad_alloc&) {
     return fail(EP_ERR_NOMEM, "ep_encode_gpu: out of host memory");

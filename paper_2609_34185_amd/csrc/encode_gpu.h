@@ -50,5 +50,22 @@ int payload(Ctx* ctx, const uint32_t* offs, uint64_t tiles, uint64_t total_words
 // values, then against the input (decoded weights snapped to rdt).
 int errors(Ctx* ctx, const float* sigma, int rdt, double* acc);
 
+// Per-row refinement (Section 3.5, App. C.2): K candidate field sets of the
+// whole tensor held on the device.
+int cand_alloc(Ctx* ctx, int K);
+// Candidate k <- every row's fields at scale s; extents as quantize().
+int cand_quantize(Ctx* ctx, int k, double s, int32_t* lohi);
+// Refit sums of candidate k (as refit()).
+int cand_refit(Ctx* ctx, int k, double* num, double* den);
+// D_r = sum_j (x_rj - sigma_r p_rj)^2 of candidate k in element order (sigma: R FP32).
+int cand_distortion(Ctx* ctx, int k, const float* sigma, double* D);
+// R_r of candidate k: the sum, in symbol order (per vector: coset, fields 1..8),
+// of lq at each symbol's cell (table layout lo, A as count()).
+int cand_rate(Ctx* ctx, int k, const double* lq, const int32_t* lo, const int32_t* A, double* Rt);
+// The full field set <- row r of candidate sel[r]; extents of the result.
+int cand_select(Ctx* ctx, const int32_t* sel, int32_t* lohi);
+// Counts of candidate k, or of the full field set for k < 0 (as count()).
+int cand_count(Ctx* ctx, int k, const int32_t* lo, const int32_t* A, uint64_t* n);
+
 }  // namespace genc
 }  // namespace ep

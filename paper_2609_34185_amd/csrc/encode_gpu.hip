@@ -346,6 +346,116 @@ __global__ __launch_bounds__(256) void k_errors(const void* w, int dt, const flo
   if (t < 4) acc[4 * r + t] = red[t][0];
 }
 
+// Per-row refinement, candidate k: D_r = sum_j (x_rj - sigma_r p_rj)^2 in
+// element order (one thread per row, chunks staged through LDS as in k_refit).
+__global__ __launch_bounds__(64) void k_dist(const float* x, const int32_t* fl, const float* sigma,
+                                             int64_t R, int64_t cvec, double* D) {
+  __shared__ float tx[kRowsPerBlock][65];
+  __shared__ int32_t tf[kRowsPerBlock][73];
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock, C = cvec * 8;
+  const int nr = (int)(R - r0 < kRowsPerBlock ? R - r0 : kRowsPerBlock);
+  const double sg = t < nr ? (double)sigma[r0 + t] : 0.0;
+  double d = 0;
+  for (int64_t v0 = 0; v0 < cvec; v0 += 8) {
+    const int nvv = (int)(cvec - v0 < 8 ? cvec - v0 : 8);
+    float xv[kRowsPerBlock];
+    int32_t f0[kRowsPerBlock], f1[kRowsPerBlock];
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) {
+      const bool row = i < nr;
+      const int64_t fb = 9 * ((r0 + i) * cvec + v0);
+      xv[i] = (row && t < 8 * nvv) ? x[(r0 + i) * C + 8 * v0 + t] : 0.0f;
+      f0[i] = (row && t < 9 * nvv) ? fl[fb + t] : 0;
+      f1[i] = (row && t + 64 < 9 * nvv) ? fl[fb + t + 64] : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) {
+      tx[i][t] = xv[i];
+      tf[i][t] = f0[i];
+      if (t < 9) tf[i][t + 64] = f1[i];
+    }
+    __syncthreads();
+    if (t < nr)
+      for (int v = 0; v < nvv; v++) {
+        int32_t p2[8];
+        em::join_fields(&tf[t][9 * v], p2);
+        for (int j = 0; j < 8; j++) {
+          const double e = (double)tx[t][8 * v + j] - sg * (p2[j] / 2.0);
+          d += e * e;
+        }
+      }
+    __syncthreads();
+  }
+  if (t < nr) D[r0 + t] = d;
+}
+
+// Per-row refinement, candidate k: R_r = sum over the row's symbols (coset,
+// then fields 1..8 of each vector, vectors in order) of lq[base_t + v - lo_t].
+__global__ __launch_bounds__(64) void k_rate(const int32_t* fl, const double* lq, TableDesc td,
+                                             int64_t R, int64_t cvec, double* Rt) {
+  __shared__ int32_t tf[kRowsPerBlock][73];
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
+  const int nr = (int)(R - r0 < kRowsPerBlock ? R - r0 : kRowsPerBlock);
+  double acc = 0;
+  for (int64_t v0 = 0; v0 < cvec; v0 += 8) {
+    const int nvv = (int)(cvec - v0 < 8 ? cvec - v0 : 8);
+    int32_t f0[kRowsPerBlock], f1[kRowsPerBlock];
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) {
+      const bool row = i < nr;
+      const int64_t fb = 9 * ((r0 + i) * cvec + v0);
+      f0[i] = (row && t < 9 * nvv) ? fl[fb + t] : 0;
+      f1[i] = (row && t + 64 < 9 * nvv) ? fl[fb + t + 64] : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < kRowsPerBlock; i++) {
+      tf[i][t] = f0[i];
+      if (t < 9) tf[i][t + 64] = f1[i];
+    }
+    __syncthreads();
+    if (t < nr)
+      for (int v = 0; v < nvv; v++) {
+        const int32_t* q = &tf[t][9 * v];
+        acc += lq[bin_of(td, q, 0)];
+        for (int i = 1; i <= 8; i++) acc += lq[bin_of(td, q, i)];
+      }
+    __syncthreads();
+  }
+  if (t < nr) Rt[r0 + t] = acc;
+}
+
+// The full field set <- row r of candidate sel[r], with the result's table extents.
+__global__ __launch_bounds__(256) void k_select(const int32_t* cand, uint64_t cand_stride,
+                                                const int32_t* sel, int64_t nvec, int64_t cvec,
+                                                int32_t* fl, int32_t* lohi) {
+  __shared__ int32_t s_lo[16], s_hi[16];
+  const int t = threadIdx.x;
+  if (t < 16) {
+    s_lo[t] = INT_MAX;
+    s_hi[t] = INT_MIN;
+  }
+  __syncthreads();
+  const int64_t id = (int64_t)blockIdx.x * 256 + t;
+  if (id < nvec) {
+    const int32_t* q = cand + (uint64_t)sel[id / cvec] * cand_stride + 9 * id;
+    int32_t f[9];
+    for (int i = 0; i < 9; i++) f[i] = q[i];
+    for (int i = 0; i < 9; i++) fl[9 * id + i] = f[i];
+    for (int i = 1; i <= 8; i++) {
+      const int ti = em::table_index(i, f[0]) - 1;
+      atomicMin(&s_lo[ti], f[i]);
+      atomicMax(&s_hi[ti], f[i]);
+    }
+  }
+  __syncthreads();
+  if (t < 16 && s_lo[t] <= s_hi[t]) {
+    atomicMin(&lohi[2 * (t + 1)], s_lo[t]);
+    atomicMax(&lohi[2 * (t + 1) + 1], s_hi[t]);
+  }
+}
+
 unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
@@ -372,6 +482,12 @@ struct Ctx {
   double *num = nullptr, *den = nullptr, *acc = nullptr;
   float* sigma = nullptr;
   std::vector<int64_t> rows_up;   // the row list last uploaded to `rows`
+  int32_t* cand = nullptr;        // K candidate field sets of the per-row refinement
+  int cand_k = 0;
+  int32_t* sel = nullptr;
+  float* csig = nullptr;
+  double* lq = nullptr;
+  uint32_t lq_cells = 0;
 
   template <class T>
   int alloc(T** p, uint64_t count, const char* what) {
@@ -518,12 +634,11 @@ TableDesc desc_of(const int32_t* lo, const int32_t* A, uint32_t* cells) {
 }
 }  // namespace
 
-int count(Ctx* c, bool sample, const int32_t* lo, const int32_t* A, uint64_t* n) {
+namespace {
+int count_on(Ctx* c, const int32_t* src, int64_t nv, const int32_t* lo, const int32_t* A, uint64_t* n) {
   uint32_t cells = 0;
   const TableDesc td = desc_of(lo, A, &cells);
   if (cells > kMaxCells) return fail(EP_ERR_ARG, "ep_encode_gpu: count of a table wider than 2^15");
-  const int32_t* src = sample ? c->sfl : c->fl;
-  const int64_t nv = sample ? c->sample_vectors : c->R * c->cvec;
   uint32_t* d = c->counts;
   if (hipMemsetAsync(d, 0, 4ull * cells, c->st) != hipSuccess) return fail(EP_ERR_HIP, "ep_encode_gpu: clear");
   const unsigned grid = (unsigned)std::min<int64_t>(256, (nv + 255) / 256);
@@ -542,6 +657,11 @@ int count(Ctx* c, bool sample, const int32_t* lo, const int32_t* A, uint64_t* n)
   EP_GTRY(c->to_host(h.data(), d, 4ull * cells, "ep_encode_gpu: count"));
   for (uint32_t i = 0; i < cells; i++) n[i] = h[i];
   return EP_OK;
+}
+}  // namespace
+
+int count(Ctx* c, bool sample, const int32_t* lo, const int32_t* A, uint64_t* n) {
+  return count_on(c, sample ? c->sfl : c->fl, sample ? c->sample_vectors : c->R * c->cvec, lo, A, n);
 }
 
 int refit(Ctx* c, double* num, double* den) {
@@ -619,6 +739,86 @@ int errors(Ctx* c, const float* sigma, int rdt, double* acc) {
                      c->sigma, c->delta, rdt, c->cont, c->cvec, c->acc);
   EP_LAUNCHED("ep_encode_gpu: launch (errors)");
   return c->to_host(acc, c->acc, 32 * (uint64_t)c->R, "ep_encode_gpu: errors");
+}
+
+// ---- per-row refinement ----------------------------------------------------
+namespace {
+int32_t* cand_ptr(Ctx* c, int k) { return c->cand + (uint64_t)k * (uint64_t)(c->R * c->cvec) * 9; }
+void init_lohi(int32_t* init) {
+  for (int i = 0; i < kTablesN; i++) {
+    init[2 * i] = INT_MAX;
+    init[2 * i + 1] = INT_MIN;
+  }
+}
+}  // namespace
+
+int cand_alloc(Ctx* c, int K) {
+  if (c->cand) return fail(EP_ERR_ARG, "ep_encode_gpu: candidates already allocated");
+  const uint64_t nvec = (uint64_t)(c->R * c->cvec);
+  EP_GTRY(c->alloc(&c->cand, nvec * 9 * (uint64_t)K, "ep_encode_gpu: device allocation (candidates)"));
+  EP_GTRY(c->alloc(&c->sel, (uint64_t)c->R, "ep_encode_gpu: device allocation"));
+  c->cand_k = K;
+  return EP_OK;
+}
+
+int cand_quantize(Ctx* c, int k, double s, int32_t* lohi) {
+  if (k < 0 || k >= c->cand_k) return fail(EP_ERR_ARG, "ep_encode_gpu: candidate index");
+  int32_t init[2 * kTablesN];
+  init_lohi(init);
+  EP_GTRY(c->to_dev(c->lohi, init, sizeof(init), "ep_encode_gpu: copy"));
+  const int64_t nv = c->R * c->cvec;
+  hipLaunchKernelGGL(k_quantize, dim3(blocks_for(nv, 256)), dim3(256), 0, c->st, c->x, c->mu,
+                     nullptr, c->R, c->cvec, c->C, s, cand_ptr(c, k), c->lohi);
+  EP_LAUNCHED("ep_encode_gpu: launch (candidate quantize)");
+  return c->to_host(lohi, c->lohi, sizeof(init), "ep_encode_gpu: candidate quantize");
+}
+
+int cand_refit(Ctx* c, int k, double* num, double* den) {
+  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+                     c->x, cand_ptr(c, k), c->R, c->cvec, c->num, c->den);
+  EP_LAUNCHED("ep_encode_gpu: launch (candidate refit)");
+  EP_GTRY(c->to_host(num, c->num, 8 * (uint64_t)c->R, "ep_encode_gpu: candidate refit"));
+  return c->to_host(den, c->den, 8 * (uint64_t)c->R, "ep_encode_gpu: candidate refit");
+}
+
+int cand_distortion(Ctx* c, int k, const float* sigma, double* D) {
+  EP_GTRY(c->to_dev(c->sigma, sigma, 4 * (uint64_t)c->R, "ep_encode_gpu: copy (scales)"));
+  hipLaunchKernelGGL(k_dist, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+                     c->x, cand_ptr(c, k), c->sigma, c->R, c->cvec, c->num);
+  EP_LAUNCHED("ep_encode_gpu: launch (distortion)");
+  return c->to_host(D, c->num, 8 * (uint64_t)c->R, "ep_encode_gpu: distortion");
+}
+
+int cand_rate(Ctx* c, int k, const double* lq, const int32_t* lo, const int32_t* A, double* Rt) {
+  uint32_t cells = 0;
+  const TableDesc td = desc_of(lo, A, &cells);
+  if (cells > c->lq_cells) {
+    if (c->lq) c->release(c->lq);
+    c->lq = nullptr;
+    EP_GTRY(c->alloc(&c->lq, cells, "ep_encode_gpu: device allocation"));
+    c->lq_cells = cells;
+  }
+  EP_GTRY(c->to_dev(c->lq, lq, 8ull * cells, "ep_encode_gpu: copy (model)"));
+  hipLaunchKernelGGL(k_rate, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+                     cand_ptr(c, k), c->lq, td, c->R, c->cvec, c->num);
+  EP_LAUNCHED("ep_encode_gpu: launch (rate)");
+  return c->to_host(Rt, c->num, 8 * (uint64_t)c->R, "ep_encode_gpu: rate");
+}
+
+int cand_select(Ctx* c, const int32_t* sel, int32_t* lohi) {
+  int32_t init[2 * kTablesN];
+  init_lohi(init);
+  EP_GTRY(c->to_dev(c->lohi, init, sizeof(init), "ep_encode_gpu: copy"));
+  EP_GTRY(c->to_dev(c->sel, sel, 4 * (uint64_t)c->R, "ep_encode_gpu: copy (selection)"));
+  const int64_t nv = c->R * c->cvec;
+  hipLaunchKernelGGL(k_select, dim3(blocks_for(nv, 256)), dim3(256), 0, c->st, c->cand,
+                     (uint64_t)nv * 9, c->sel, nv, c->cvec, c->fl, c->lohi);
+  EP_LAUNCHED("ep_encode_gpu: launch (select)");
+  return c->to_host(lohi, c->lohi, sizeof(init), "ep_encode_gpu: select");
+}
+
+int cand_count(Ctx* c, int k, const int32_t* lo, const int32_t* A, uint64_t* n) {
+  return count_on(c, k < 0 ? c->fl : cand_ptr(c, k), c->R * c->cvec, lo, A, n);
 }
 
 }  // namespace genc

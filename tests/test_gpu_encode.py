@@ -137,11 +137,24 @@ def test_gpu_encoder_rejects_bad_input(E):
     assert e.value.code == E.ERR_ARG
 
 
-def test_gpu_encoder_refuses_the_row_refinement(E):
-    """The per-row refinement runs in the CPU encoder only; the GPU encoder says so."""
-    with pytest.raises(E.EntroPackError) as e:
-        gpu_encode(E, W.ragged_tensor(3, 32, 256), 3.0, rdo_candidates=5, rdo_sweeps=1)
-    assert e.value.code == E.ERR_UNSUPPORTED
+RDO_CASES = [
+    ("rdo_k5", lambda: W.ragged_tensor(3, 96, 512), 3.0, dict(rdo_candidates=5, rdo_sweeps=1)),
+    ("rdo_k9_t2", lambda: W.attention_projection()[:300], 3.0, dict(rdo_candidates=9, rdo_sweeps=2)),
+    ("rdo_fp8", lambda: W.ragged_tensor(4, 128, 512, scale=0.05), 4.0,
+     dict(container=1, rdo_candidates=5, rdo_sweeps=1)),
+    ("rdo_int8_ragged", lambda: W.ragged_tensor(5, 77, 136), 6.0,
+     dict(container=2, tile_vectors=45, rdo_candidates=4, rdo_sweeps=3)),
+]
+
+
+@pytest.mark.parametrize("name,gen,target,kw", RDO_CASES, ids=[c[0] for c in RDO_CASES])
+def test_gpu_encoder_row_refinement_matches_oracle_bytes(E, oracle, name, gen, target, kw):
+    """The per-row refinement (Section 3.5, App. C.2) with its candidate passes on the GPU."""
+    w = gen()
+    b_or, s_or = oracle.encode(w, target, **kw)
+    b_gpu, s_gpu = gpu_encode(E, w, target, **kw)
+    assert np.array_equal(b_gpu, b_or)
+    assert s_gpu["rdo_rows_moved"] == s_or["rdo_rows_moved"]
 
 
 def test_gpu_encoder_full_size_attention(E, oracle):
