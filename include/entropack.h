@@ -199,6 +199,25 @@ int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtyp
                     float* d_dequant, uint32_t tile_begin, uint32_t tile_end, int32_t* d_status,
                     void* hip_stream);
 
+/* Fused decode and small-batch product (the decode of Section 3.7 feeding an
+ * INT8 matrix product directly, the fusion the paper's conclusion leaves to
+ * future work, on the INT8 route of Appendix B.1):
+ *   Y[t][r] = sum_j X[t][j] * W'[r][j]   for t < m, r < R,
+ * where W' is the tensor's INT8 container matrix exactly as ep_decode_tiles
+ * writes it with EP_INT8 (the weights are delta_r * W'), X is m x C int8
+ * row-major and Y m x R int32 row-major, exact (no rounding, no overflow:
+ * C <= 131071).  W' is never written to memory: every decoded vector goes
+ * straight into dot products with the m rows of X.  Y is overwritten (cleared
+ * on hip_stream first); d_dequant (nullable) receives delta_r for every row.
+ * All pointers are device memory owned by the caller; X 8-byte aligned.
+ * Asynchronous on hip_stream, no allocation, one clear and one kernel launch.
+ * d_status as for ep_decode_tiles.  Meant for few rows of X (decode-time
+ * serving); for large batches decode once and call ep_gemm_i8_nt.
+ * Errors: EP_ERR_ARG (null pointers, m outside 1..8), EP_ERR_UNSUPPORTED (not
+ * the INT8 row container, C > 131071), EP_ERR_HIP. */
+int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int m,
+                        int32_t* d_y, float* d_dequant, int32_t* d_status, void* hip_stream);
+
 /* One layer of a stack decode. */
 typedef struct {
   ep_tensor_info info;       /* from ep_blob_info on the host copy */

@@ -45,6 +45,11 @@ constexpr int kWaveSize = 64;
 constexpr int kWavesPerGroup = 16;
 constexpr int kThreads = kWaveSize * kWavesPerGroup;
 constexpr uint32_t kStateLow = 1u << 15;
+// Internal output mode of the fused product (never a public dtype code): the
+// decoded INT8 container values are multiplied into a small int8 batch X and
+// summed into Y (int32) instead of being stored.
+constexpr int kOutDotI8 = 0x200;
+constexpr uint32_t kDotMaxTokens = 8;
 
 // Index of the calling wave in its workgroup, as a wave-uniform (scalar) value.
 __device__ __forceinline__ uint32_t wave_id() {
@@ -79,6 +84,8 @@ struct LayerDev {
   int32_t tab_min[16];
   uint32_t tab_A[16];
   uint32_t tab_base[16];          // prefix of tab_A (search path)
+  const int8_t* x;                // fused product: X (m x cols, row-major), Y in `out`
+  uint32_t m;
 };
 
 // The scalars the decode loop needs, read once per layer segment and forced
@@ -93,6 +100,8 @@ struct Hot {
   uint32_t meta, bucket;          // search path: u32 index of the metadata, u16 index of the buckets
   uint32_t bucket_shift, bucket_n1; // search path: b - k and 2^k + 1
   uint32_t off_sigma, off_delta, off_states, off_offsets, off_payload;
+  const int8_t* x;
+  uint32_t m, cols;
 };
 
 __device__ __forceinline__ uint32_t uni(uint32_t v) {
@@ -136,6 +145,9 @@ __device__ __forceinline__ Hot make_hot(const LayerDev& L) {
   H.off_states = uni((uint32_t)L.off_states);
   H.off_offsets = uni((uint32_t)L.off_offsets);
   H.off_payload = uni((uint32_t)L.off_payload);
+  H.x = uni_ptr(L.x);
+  H.m = uni(L.m);
+  H.cols = uni(L.cols);
   return H;
 }
 
@@ -221,8 +233,48 @@ __device__ __forceinline__ void store_vec(void* out, uint32_t v, const int32_t* 
   }
 }
 
+__device__ __forceinline__ uint32_t row_of(const Hot& L, uint32_t v);
+
+// *p += v as a global-memory atomic (never a flat one: flat instructions also
+// count against lgkmcnt, which the decode steps' LDS waits rely on).
+__device__ __forceinline__ void add_i32(EP_GLOBAL int32_t* p, int32_t v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#else
+  (void)p;
+  (void)v;
+#endif
+}
+
+// Fused product, one vector at a time: the eight INT8 weights (w0: elements
+// 0-3, w1: 4-7, one byte each) of vector v times the same eight columns of
+// every row t of X, added to Y[t][row] (int32, exact).
+__device__ __forceinline__ void dot_add(const Hot& L, uint32_t w0, uint32_t w1, uint32_t v,
+                                        uint32_t r) {
+  const uint32_t col8 = 8 * (v - r * L.cvec);
+  const EP_GLOBAL int8_t* xp = gptr<const int8_t>(L.x) + col8;
+  EP_GLOBAL int32_t* y = gptr<int32_t>(L.out) + r;
+  for (uint32_t t = 0; t < L.m; t++) {
+    const u32x2 xv = *reinterpret_cast<const EP_GLOBAL u32x2*>(xp + (uint64_t)t * L.cols);
+    const int d = __builtin_amdgcn_sdot4((int)w1, (int)xv.y, __builtin_amdgcn_sdot4((int)w0, (int)xv.x, 0, false), false);
+    add_i32(y + (uint64_t)t * L.rows, d);
+  }
+}
+
+__device__ __forceinline__ void dot_vec(const Hot& L, uint32_t v, const int32_t* p2, float half_sigma) {
+  float y[8];
+#pragma unroll
+  for (int j = 0; j < 8; j++) y[j] = half_sigma * (float)p2[j];
+  dot_add(L, int8_quad(y[0], y[1], y[2], y[3]), int8_quad(y[4], y[5], y[6], y[7]), v, row_of(L, v));
+}
+
+template <bool DOT = false>
 __device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int32_t* p2,
                                              float half_sigma) {
+  if constexpr (DOT) {
+    dot_vec(L, v, p2, half_sigma);
+    return;
+  }
   switch (L.out_dtype) {
     case EP_BF16:
       if (L.saturate) store_vec<EP_BF16, true>(L.out, v, p2, half_sigma);
@@ -506,7 +558,7 @@ __device__ __forceinline__ uint32_t row_of(const Hot& L, uint32_t v) {
   return (q + ((v - q) >> 1)) >> L.div_shift;
 }
 
-template <int PATH, int B, int NC, bool FULL>
+template <int PATH, int B, int NC, bool FULL, bool DOT = false>
 __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, uint8_t* lds,
                             uint32_t ring_area, uint32_t task, int32_t* status) {
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
@@ -591,7 +643,7 @@ __device__ __forceinline__ void decode_task(const Hot& L, const uint32_t* tab, u
           acc += d[j][i];
         }
         p2[7] = d[j][8] | (acc & 2);
-        store_vector(L, v[j], p2, 0.5f * sg[j]);
+        store_vector<DOT>(L, v[j], p2, 0.5f * sg[j]);
       }
     }
   }
@@ -847,7 +899,8 @@ __device__ __forceinline__ void decode_task_fast(const Hot& L, uint8_t* lds, uin
         acc += d[j][i];
       }
       p2[7] = d[j][8] | (acc & 2);
-      store_vec<DT, SAT>(L.out, v0[j] + l + 32 * k, p2, 0.5f * sg[j]);
+      if constexpr (DT == kOutDotI8) dot_vec(L, v0[j] + l + 32 * k, p2, 0.5f * sg[j]);
+      else store_vec<DT, SAT>(L.out, v0[j] + l + 32 * k, p2, 0.5f * sg[j]);
       // next vector of this lane: 32 vectors further
       if (wide) {
         col[j] += 32;
@@ -1165,11 +1218,36 @@ constexpr uint32_t vec_bytes() {
   return DT == EP_FP8_E4M3 || DT == EP_INT8 ? 8u : (DT == EP_BF16 || DT == EP_FP16) ? 16u : 32u;
 }
 
+// Sum of v over the 32 lanes of each half-wave, valid in lanes 0 and 32 (the
+// lanes that add it to Y).  DPP moves and lane reads only, no LDS instruction:
+// the LDS waits inside the decode steps count on their own reads alone.
+// Every lane of the wave must be active.
+__device__ __forceinline__ int32_t half_sum(int32_t v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);    // lane i ^ 1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);    // lane i ^ 2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);   // the other quad of 8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);   // the other 8 of 16
+  const int32_t a = __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16);
+  const int32_t b = __builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48);
+  return (threadIdx.x & 32) ? b : a;
+}
+
 // The steady-state task of the slot-table path: four full tiles t0 .. t0 + 3
 // (two chains).  TWO: every lane's vectors v, v + 32, ... of a tile lie in at
 // most two rows (C/8 >= V - 32), so each lane holds both row scales and
 // switches at round kc; otherwise the row scale is loaded every round.
-template <int B, int DT, bool SAT, bool TWO, bool WIDE>
+//
+// Fused product (DT = kOutDotI8): each round's eight INT8 weights go straight
+// into two dot4 instructions per row of X.  With TWO (the caller guarantees
+// C/8 >= V here, so a tile spans at most rows r0 and r0 + 1) each lane keeps
+// MT int32 sums per chain: at the start of the round where a lane's vectors
+// pass into row r0 + 1 its sums so far are summed over its half-wave and
+// added to Y[t][r0], and at the end of the task the remaining sums go to r0
+// or r0 + 1.  Columns 0-3 of X for a round are requested at its start and
+// used once the vector's first four weights are known (after field 4), when
+// columns 4-7 are requested, used at the end of the round.
+// Without TWO every vector is added to Y on its own.
+template <int B, int DT, bool SAT, bool TWO, bool WIDE, int MT = 1>
 __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ring_area, uint32_t t0,
                                          int32_t* status) {
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
@@ -1207,6 +1285,23 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
       sb[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r + 4, 0, 0));
     }
   }
+  constexpr bool DOT = DT == kOutDotI8;
+  constexpr bool ACC = DOT && TWO;
+  int32_t dacc[2][MT];
+  uint32_t r0[2], kd[2], colb[2];
+  __amdgpu_buffer_rsrc_t xrsrc;
+  if constexpr (ACC) {
+    xrsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(L.x), (short)0,
+                                              (int)(L.m * L.cols), 0x00020000);
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      r0[j] = row_of(L, (t0 + 2 * j + half) * L.V);   // first row of the lane's tile
+      kd[j] = row_of(L, vb[j]) == r0[j] ? kc[j] : 0u;   // first round in row r0 + 1
+      colb[j] = vb[j] - r0[j] * L.cvec;
+#pragma unroll
+      for (int t = 0; t < MT; t++) dacc[j][t] = 0;
+    }
+  }
   FastChain F0, F1;
   u32x2 pend0, pend1, pendB0, pendB1;
 #pragma unroll
@@ -1238,6 +1333,27 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
       else sg[j] = __uint_as_float(
           __builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row_of(L, vb[j] + 32 * k), 0, 0));
     }
+    uint32_t xo[2], xq[2][MT];
+    if constexpr (ACC) {
+      EP_GLOBAL int32_t* y = gptr<int32_t>(L.out);
+#pragma unroll
+      for (int j = 0; j < 2; j++) {
+        // lanes whose vectors pass into row r0 + 1 this round: their sums so far belong to r0
+        const bool dep = k == kd[j];
+        if (__builtin_expect(__ballot(dep) != 0, 0)) {
+#pragma unroll
+          for (int t = 0; t < MT; t++) {
+            const int32_t sum = half_sum(dep ? dacc[j][t] : 0);
+            if (l == 0 && (uint32_t)t < L.m && sum != 0) add_i32(y + (uint64_t)t * L.rows + r0[j], sum);
+            if (dep) dacc[j][t] = 0;
+          }
+        }
+        xo[j] = 8 * (colb[j] + 32 * k - (k >= kd[j] ? L.cvec : 0u));
+        // columns 0-3 of the vector now, 4-7 once the first four weights are known
+#pragma unroll
+        for (int t = 0; t < MT; t++) xq[j][t] = __builtin_amdgcn_raw_buffer_load_b32(xrsrc, xo[j], t * L.cols, 0);
+      }
+    }
     uint32_t cb[2], e0, e1;
     float y0, y1;
     QAcc acc[2];
@@ -1251,13 +1367,54 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
   q_take<DT, I, WIDE>(acc[1], e1, y1, cb[1] >> (B + 5));
     EP_FIELD(1) EP_FIELD(2)
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
-    EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
+    EP_FIELD(3) EP_FIELD(4)
+    if constexpr (ACC) {
+#pragma unroll
+      for (int j = 0; j < 2; j++) {
+#pragma unroll
+        for (int t = 0; t < MT; t++) {
+          dacc[j][t] = __builtin_amdgcn_sdot4((int)acc[j].w[0], (int)xq[j][t], dacc[j][t], false);
+          xq[j][t] = __builtin_amdgcn_raw_buffer_load_b32(xrsrc, xo[j] + 4, t * L.cols, 0);
+        }
+      }
+    }
+    EP_FIELD(5)
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
 #undef EP_FIELD
-    q_put<DT>(obase, voff[0], acc[0]);
-    q_put<DT>(obase, voff[1], acc[1]);
-    obase += 32 * VB;
+    if constexpr (ACC) {
+#pragma unroll
+      for (int j = 0; j < 2; j++)
+#pragma unroll
+        for (int t = 0; t < MT; t++)
+          dacc[j][t] = __builtin_amdgcn_sdot4((int)acc[j].w[1], (int)xq[j][t], dacc[j][t], false);
+    } else if constexpr (DOT) {
+#pragma unroll
+      for (int j = 0; j < 2; j++) {
+        const uint32_t v = vb[j] + 32 * k;
+        dot_add(L, acc[j].w[0], acc[j].w[1], v, row_of(L, v));
+      }
+    } else {
+      q_put<DT>(obase, voff[0], acc[0]);
+      q_put<DT>(obase, voff[1], acc[1]);
+      obase += 32 * VB;
+    }
+  }
+  if constexpr (ACC) {
+    EP_GLOBAL int32_t* y = gptr<int32_t>(L.out);
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const bool moved = rounds > kd[j];   // the lane's last vector lies in row r0 + 1
+#pragma unroll
+      for (int t = 0; t < MT; t++) {
+        const int32_t s0 = half_sum(moved ? 0 : dacc[j][t]);
+        const int32_t s1 = half_sum(moved ? dacc[j][t] : 0);
+        if (l == 0 && (uint32_t)t < L.m) {
+          if (s0 != 0) add_i32(y + (uint64_t)t * L.rows + r0[j], s0);
+          if (s1 != 0) add_i32(y + (uint64_t)t * L.rows + r0[j] + 1, s1);
+        }
+      }
+    }
   }
 
   uint32_t err = 0;
@@ -1281,16 +1438,31 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
 template <int B, int DT, bool SAT, bool WIDE>
 __device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                               uint32_t t0, int32_t* status) {
-  if (L.cvec + 32 >= L.V) lut_task<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
-  else lut_task<B, DT, SAT, false, WIDE>(L, lds, ring_area, t0, status);
+  if constexpr (DT == kOutDotI8) {
+    if (L.cvec >= L.V) {
+      if (L.m <= 1) lut_task<B, DT, false, true, WIDE, 1>(L, lds, ring_area, t0, status);
+      else if (L.m <= 2) lut_task<B, DT, false, true, WIDE, 2>(L, lds, ring_area, t0, status);
+      else if (L.m <= 4) lut_task<B, DT, false, true, WIDE, 4>(L, lds, ring_area, t0, status);
+      else lut_task<B, DT, false, true, WIDE, kDotMaxTokens>(L, lds, ring_area, t0, status);
+    } else {
+      lut_task<B, DT, false, false, WIDE>(L, lds, ring_area, t0, status);
+    }
+  } else {
+    if (L.cvec + 32 >= L.V) lut_task<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
+    else lut_task<B, DT, SAT, false, WIDE>(L, lds, ring_area, t0, status);
+  }
 }
 
 // Output-type dispatch of a full four-tile slot-table task (narrow or wide
 // entries).  Returns false for the combinations the steady state does not
 // cover (they take the generic loop).
-template <int B, bool WIDE>
+template <int B, bool WIDE, bool DOT = false>
 __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                              uint32_t t0, int32_t* status) {
+  if constexpr (DOT) {
+    lut_task_rows<B, kOutDotI8, false, WIDE>(L, lds, ring_area, t0, status);
+    return true;
+  }
   switch (L.out_dtype) {
     case EP_BF16:
       if (L.saturate) lut_task_rows<B, EP_BF16, true, WIDE>(L, lds, ring_area, t0, status);
@@ -1313,9 +1485,13 @@ __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_
 
 // Output-type dispatch of a full search-path task (four tiles, two chains).  Returns
 // false for the combinations the steady state does not cover (they take the generic loop).
-template <int PATH, int B>
+template <int PATH, int B, bool DOT = false>
 __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                                      uint32_t task, int32_t* status) {
+  if constexpr (DOT) {
+    decode_task_fast<PATH, B, kOutDotI8, false>(L, lds, ring_area, task, status);
+    return true;
+  }
   switch (L.out_dtype) {
     case EP_BF16:
       if (L.saturate) return false;
@@ -1412,7 +1588,7 @@ constexpr uint32_t kTilesPerTask = 4;
 static_assert(kChains == 2, "the generic loop and the search steady state advance two chains");
 static_assert(kTilesPerTask == 2 * kChains, "task granularity: one four-tile pass");
 
-template <int PATH, int B>
+template <int PATH, int B, bool DOT>
 __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                        uint32_t ring_area, uint32_t task, int32_t* status) {
   const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
@@ -1421,28 +1597,29 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
                     (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
   if (full && L.pay_bytes < kFastOob && (PATH == kPathSearch || B == 11)) {
     if constexpr (PATH != kPathSearch && B == 11) {
-      if (lut_task_any<B, PATH == kPathWide>(L, lb, ring_area, t0, status)) return;
+      if (lut_task_any<B, PATH == kPathWide, DOT>(L, lb, ring_area, t0, status)) return;
     } else if constexpr (PATH == kPathSearch) {
-      if (decode_task_fast_any<PATH, B>(L, lb, ring_area, task, status)) return;
+      if (decode_task_fast_any<PATH, B, DOT>(L, lb, ring_area, task, status)) return;
     }
   }
   // generic loop
-  if (full) decode_task<PATH, B, kChains, true>(L, tab, lb, ring_area, task, status);
-  else decode_task<PATH, B, kChains, false>(L, tab, lb, ring_area, task, status);
+  if (full) decode_task<PATH, B, kChains, true, DOT>(L, tab, lb, ring_area, task, status);
+  else decode_task<PATH, B, kChains, false, DOT>(L, tab, lb, ring_area, task, status);
 }
 
-template <int PATH>
+template <int PATH, bool DOT>
 __device__ __forceinline__ void dispatch_task(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                               uint32_t ring_area, uint32_t task, int32_t* status) {
-  if (PATH == kPathSearch) task_b<PATH, 0>(L, tab, lb, ring_area, task, status);
-  else if (L.b == 11) task_b<PATH, 11>(L, tab, lb, ring_area, task, status);
-  else if (L.b == 10) task_b<PATH, 10>(L, tab, lb, ring_area, task, status);
-  else task_b<PATH, 9>(L, tab, lb, ring_area, task, status);
+  if (PATH == kPathSearch) task_b<PATH, 0, DOT>(L, tab, lb, ring_area, task, status);
+  else if (L.b == 11) task_b<PATH, 11, DOT>(L, tab, lb, ring_area, task, status);
+  else if (L.b == 10) task_b<PATH, 10, DOT>(L, tab, lb, ring_area, task, status);
+  else task_b<PATH, 9, DOT>(L, tab, lb, ring_area, task, status);
 }
 
 // Decode global tasks [t_begin, t_end) of a layer list: per layer segment the
 // workgroup builds that layer's tables, then its waves take tasks in turn.
-template <int PATH>
+// DOT: the fused product (every layer's output mode is kOutDotI8).
+template <int PATH, bool DOT = false>
 __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers, uint32_t total,
                            uint32_t per_group, int32_t* status) {
   extern __shared__ uint32_t lds[];
@@ -1464,7 +1641,7 @@ __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers,
     const Hot H = make_hot(L);
     uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
     for (uint32_t task = seg + wave; task < seg_end; task += kWavesPerGroup)
-      dispatch_task<PATH>(H, lds, lb, ring_area, task - first, status);
+      dispatch_task<PATH, DOT>(H, lds, lb, ring_area, task - first, status);
     seg = seg_end;
   }
 }
@@ -1490,6 +1667,22 @@ __global__ __launch_bounds__(kThreads) void decode_args_kernel(const LayerList l
   const LayerDev* layers = list.L;
 #endif
   run_layers<PATH>(layers, n_layers, total, per_group, status);
+}
+
+// The fused decode and product, in kernels of its own: its steady state needs
+// more registers than the decode's, and sharing a kernel would give every
+// decode launch its scratch allocation.
+template <int PATH>
+__global__ __launch_bounds__(kThreads) void decode_dot_kernel(const LayerList list, int n_layers,
+                                                              uint32_t total, uint32_t per_group,
+                                                              int32_t* status) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  (void)list;
+  const LayerDev* layers = (const LayerDev*)__builtin_amdgcn_kernarg_segment_ptr();
+#else
+  const LayerDev* layers = list.L;
+#endif
+  run_layers<PATH, true>(layers, n_layers, total, per_group, status);
 }
 
 template <int PATH>
@@ -1620,7 +1813,9 @@ int set_lds_limit(size_t bytes) {
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   hipError_t e2 = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_ws_kernel<PATH>),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  return (e1 == hipSuccess && e2 == hipSuccess) ? EP_OK : EP_ERR_HIP;
+  hipError_t e3 = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_dot_kernel<PATH>),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  return (e1 == hipSuccess && e2 == hipSuccess && e3 == hipSuccess) ? EP_OK : EP_ERR_HIP;
 }
 
 // Grid of a launch over `total` tasks: G workgroups of `per` consecutive tasks.
@@ -1658,8 +1853,9 @@ int launch_list(uint32_t path, const LayerDev* dl, int n, uint32_t total, uint32
 // else from d_ws (copied there first on the same stream).
 int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total, uint32_t lds,
                   void* d_ws, uint64_t ws_bytes, int32_t* d_status, hipStream_t s,
-                  const char* who) {
+                  const char* who, bool dot = false) {
   const int n = (int)D.size();
+  if (dot && n > kArgLayers) return fail(EP_ERR_ARG, (std::string(who) + ": too many layers").c_str());
   if (n > kArgLayers) {
     if (!d_ws || ws_bytes < sizeof(LayerDev) * (uint64_t)n)
       return fail(EP_ERR_ARG, "ep_decode_layers: workspace too small");
@@ -1674,7 +1870,13 @@ int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total,
     LayerList list;
     std::memset(&list, 0, sizeof list);
     for (int i = 0; i < n; i++) list.L[i] = D[i];
-    if (path == kPathLut)
+    if (dot && path == kPathLut)
+      hipLaunchKernelGGL(decode_dot_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else if (dot && path == kPathWide)
+      hipLaunchKernelGGL(decode_dot_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else if (dot)
+      hipLaunchKernelGGL(decode_dot_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else if (path == kPathLut)
       hipLaunchKernelGGL(decode_args_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
     else if (path == kPathWide)
       hipLaunchKernelGGL(decode_args_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
@@ -1694,6 +1896,32 @@ int decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtype, 
   if (D[0].n_tasks == 0) return EP_OK;
   return launch_layers(info->path, D, D[0].n_tasks, lds_bytes(info->path, *info), nullptr, 0,
                        d_status, static_cast<hipStream_t>(stream), "ep_decode_tiles");
+}
+
+// Fused decode and small-batch product: the INT8 container values of every
+// tile, multiplied into X as they are decoded (see lut_task).
+int decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int m,
+                     int32_t* d_y, float* d_dequant, int32_t* d_status, void* stream) {
+  if (!info) return fail(EP_ERR_ARG, "ep_decode_matmul_i8: null info");
+  if (info->container != EP_CONT_INT8_ROW)
+    return fail(EP_ERR_UNSUPPORTED, "ep_decode_matmul_i8: the tensor is not in the INT8 row container");
+  if (m < 1 || m > (int)kDotMaxTokens) return fail(EP_ERR_ARG, "ep_decode_matmul_i8: m must be 1 .. 8");
+  if (!d_x || !d_y) return fail(EP_ERR_ARG, "ep_decode_matmul_i8: null X or Y");
+  if (info->cols > 131071)
+    return fail(EP_ERR_UNSUPPORTED, "ep_decode_matmul_i8: rows longer than 131071 weights may overflow int32");
+  std::vector<LayerDev> D(1);
+  int rc = fill_layer(*info, d_blob, EP_INT8, d_y, d_dequant, 0, info->n_tiles, D[0]);
+  if (rc) return rc;
+  D[0].out_dtype = kOutDotI8;
+  D[0].saturate = 0;
+  D[0].x = d_x;
+  D[0].m = (uint32_t)m;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (hipMemsetAsync(d_y, 0, sizeof(int32_t) * (size_t)m * info->rows, s) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_matmul_i8: clearing Y failed");
+  if (D[0].n_tasks == 0) return EP_OK;
+  return launch_layers(info->path, D, D[0].n_tasks, lds_bytes(info->path, *info), nullptr, 0,
+                       d_status, s, "ep_decode_matmul_i8", true);
 }
 
 uint64_t decode_layers_workspace(int n) {
@@ -1783,6 +2011,11 @@ int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtyp
                     void* hip_stream) {
   return ep::decode_tiles(info, d_blob, out_dtype, d_out, d_dequant, tile_begin, tile_end,
                           d_status, hip_stream);
+}
+
+int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int m,
+                        int32_t* d_y, float* d_dequant, int32_t* d_status, void* hip_stream) {
+  return ep::decode_matmul_i8(info, d_blob, d_x, m, d_y, d_dequant, d_status, hip_stream);
 }
 
 uint64_t ep_decode_layers_workspace(int n) { return ep::decode_layers_workspace(n); }

@@ -112,6 +112,7 @@ def lib():
         L.ep_stack_prepare.argtypes = [C.POINTER(Layer), C.c_int, vp, u64, C.POINTER(Stack), vp]
         L.ep_stack_decode.argtypes = [C.POINTER(Stack), vp, vp]
         L.ep_gemm_i8_nt.argtypes = [vp, vp, vp, i64, i64, i64, vp]
+        L.ep_decode_matmul_i8.argtypes = [C.POINTER(TensorInfo), vp, vp, C.c_int, vp, vp, vp, vp]
         L.ep_last_error.restype = C.c_char_p
         _lib = L
     return _lib
@@ -120,6 +121,7 @@ def lib():
 EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_encode_gpu", "ep_blob_free", "ep_blob_info",
            "ep_decode_tiles", "ep_decode_layers_workspace", "ep_decode_layers",
            "ep_stack_workspace", "ep_stack_prepare", "ep_stack_decode", "ep_gemm_i8_nt",
+           "ep_decode_matmul_i8",
            "ep_last_error"]
 
 
@@ -226,6 +228,13 @@ def stack_decode(st: Stack, d_status: int = 0, stream: int = 0):
 
 def gemm_i8_nt(d_a: int, d_b: int, d_y: int, m: int, n: int, k: int, stream: int = 0):
     _check(lib().ep_gemm_i8_nt(d_a, d_b, d_y, m, n, k, stream or None), "ep_gemm_i8_nt")
+
+
+def decode_matmul_i8(info: TensorInfo, d_blob: int, d_x: int, m: int, d_y: int, d_dequant: int = 0,
+                     d_status: int = 0, stream: int = 0):
+    """Y (m x R int32) = X (m x C int8) times the decoded INT8 container matrix, transposed."""
+    _check(lib().ep_decode_matmul_i8(C.byref(info), d_blob, d_x, m, d_y, d_dequant or None,
+                                     d_status or None, stream or None), "ep_decode_matmul_i8")
 
 
 # ---- torch conveniences (device memory and streams only) ------------------------

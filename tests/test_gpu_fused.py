@@ -1,0 +1,126 @@
+"""GPU parity of the fused decode and small-batch product (ep_decode_matmul_i8).
+
+Y = X W'^T, with W' the INT8 container matrix of a blob and X a few int8 rows,
+must equal the oracle's product of the oracle-decoded W' exactly, on every
+element: the steady state with per-lane sums for 1, 2, 4 and 8 rows of X (rows
+at least a tile long, tiles crossing rows), rows shorter than a tile (every
+vector added on its own), ragged tiles (the generic loop), b = 12 (the search
+path), the full-size 27B-class MLP down projection at 6.0 bpp, and the delta
+output.  The call overwrites Y, so a second call into the same buffer must
+give the same result.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2609_34185_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+@pytest.fixture(scope="module")
+def E():
+    from paper_2609_34185_amd import entropack
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    entropack.lib()
+    return entropack
+
+
+def activations(seed: int, m: int, cols: int) -> np.ndarray:
+    return np.random.default_rng(seed).integers(-127, 128, (m, cols), dtype=np.int8)
+
+
+def fused(E, blob: np.ndarray, x: np.ndarray, twice: bool = False):
+    """(Y, delta, status) of the fused product on the GPU."""
+    info = E.blob_info(blob)
+    d_blob = torch.from_numpy(blob).cuda()
+    d_x = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    m = x.shape[0]
+    y = torch.full((m, info.rows), 7, dtype=torch.int32, device="cuda")
+    dq = torch.zeros(info.rows, dtype=torch.float32, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    for _ in range(2 if twice else 1):
+        E.decode_matmul_i8(info, d_blob.data_ptr(), d_x.data_ptr(), m, y.data_ptr(), dq.data_ptr(),
+                           st.data_ptr(), s)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), dq.cpu().numpy(), int(st.item())
+
+
+def reference(oracle, blob: np.ndarray, x: np.ndarray):
+    w, dq = oracle.decode(blob, oracle.INT8)
+    return oracle.gemm_i8_nt(x, w), dq
+
+
+CASES = [
+    # name, generator, target, encode kwargs, rows of X
+    ("long_rows_m1", lambda: W.ragged_tensor(11, 96, 8 * 1000, scale=0.05), 6.0, {}, 1),
+    ("long_rows_m2", lambda: W.ragged_tensor(12, 80, 8 * 1100, scale=0.05), 6.0, {}, 2),
+    ("long_rows_m3", lambda: W.ragged_tensor(13, 64, 8 * 640, scale=0.05), 4.0, {}, 3),
+    ("long_rows_m4", lambda: W.ragged_tensor(14, 72, 8 * 777, scale=0.05), 6.0, {}, 4),
+    ("long_rows_m8", lambda: W.ragged_tensor(15, 70, 8 * 1024, scale=0.05), 6.0, {}, 8),
+    ("row_just_short_of_a_tile_m5", lambda: W.ragged_tensor(16, 64, 8 * 500, scale=0.05), 6.0, {}, 5),
+    ("short_rows_m4", lambda: W.ragged_tensor(17, 300, 512, scale=0.05), 6.0, {}, 4),
+    ("ragged_tiles_m2", lambda: W.ragged_tensor(18, 37, 136, scale=0.05), 6.0, dict(tile_vectors=45), 2),
+    ("ragged_tiles_m7", lambda: W.ragged_tensor(19, 41, 8 * 333, scale=0.05), 5.0, dict(tile_vectors=96), 7),
+    ("b12_search_m3", lambda: W.ragged_tensor(20, 64, 8 * 600, scale=0.05), 6.0, dict(prob_bits=12), 3),
+    ("one_vector_m1", lambda: W.ragged_tensor(21, 1, 8, scale=0.05), 6.0, {}, 1),
+]
+
+
+@pytest.mark.parametrize("name,gen,target,kw,m", CASES, ids=[c[0] for c in CASES])
+def test_fused_product_matches_oracle(E, oracle, name, gen, target, kw, m):
+    w = gen()
+    say(f"  fused {name}: {w.shape} at {target}, m = {m}")
+    blob, _ = oracle.encode(w, target, container=oracle.CONT_INT8, **kw)
+    x = activations(len(name), m, w.shape[1])
+    y_ref, dq_ref = reference(oracle, blob, x)
+    y, dq, st = fused(E, blob, x, twice=True)
+    assert st == 0
+    assert np.array_equal(y, y_ref)
+    assert np.array_equal(dq, dq_ref)
+
+
+def test_fused_product_config5_down(E, oracle):
+    """The INT8-container MLP down projection (5120 x 17408, 6.0 bpp) times the first
+    rows of the 8192 x 17408 activations, every element of Y."""
+    say("  fused cfg5: encoding the down projection (INT8 container, 6.0 bpp)")
+    w = W.llm_mlp(["down"])["down"]
+    blob, _ = E.encode(w, 6.0, container=E.CONT_INT8_ROW)
+    act = W.llm_activations()
+    w_ref, dq_ref = oracle.decode(blob, oracle.INT8)
+    for m in (1, 4, 8):
+        x = act[:m]
+        say(f"  fused cfg5: m = {m}")
+        y, dq, st = fused(E, blob, x)
+        assert st == 0
+        assert np.array_equal(y, oracle.gemm_i8_nt(x, w_ref))
+        assert np.array_equal(dq, dq_ref)
+
+
+def test_fused_product_rejects_bad_arguments(E, oracle):
+    w = W.ragged_tensor(22, 32, 256, scale=0.05)
+    blob_int8, _ = oracle.encode(w, 6.0, container=oracle.CONT_INT8)
+    blob_fp8, _ = oracle.encode(w, 6.0, container=oracle.CONT_FP8)
+    x = activations(1, 9, 256)
+    d_x = torch.from_numpy(x).cuda()
+    y = torch.zeros((9, 32), dtype=torch.int32, device="cuda")
+    lib = E.lib()
+    for blob, m, code in ((blob_fp8, 1, E.ERR_UNSUPPORTED), (blob_int8, 0, E.ERR_ARG),
+                          (blob_int8, 9, E.ERR_ARG)):
+        info = E.blob_info(blob)
+        d_blob = torch.from_numpy(blob).cuda()
+        rc = lib.ep_decode_matmul_i8(E.C.byref(info), d_blob.data_ptr(), d_x.data_ptr(), m,
+                                     y.data_ptr(), None, None, None)
+        assert rc == code
+    info = E.blob_info(blob_int8)
+    d_blob = torch.from_numpy(blob_int8).cuda()
+    assert lib.ep_decode_matmul_i8(E.C.byref(info), d_blob.data_ptr(), None, 1, y.data_ptr(),
+                                   None, None, None) == E.ERR_ARG
