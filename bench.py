@@ -20,7 +20,10 @@ launch), mlp_down_int8 (the MLP down projection in the INT8 container at
 activations, timed separately: decode time over product time is reported),
 encode_mlp (the GPU encoder on the MLP set's three BF16 tensors, FP8 container
 at 4.0 bpp; a step encodes all three; the CPU baseline is the oracle encoder
-on the down projection).
+on the down projection), fused_down_m1 / _m2 / _m4 / _m8 (the fused decode and
+small-batch product ep_decode_matmul_i8: the INT8-container down projection
+times the first 1, 2, 4 or 8 rows of the activations, one launch per step;
+algorithmic bytes = compressed blob + X read, Y and dequant written).
 
 The roofline's `traffic` field is the decode kernel's measured HBM bytes per
 launch, read from the committed rocprofv3 counter summary of this workload
@@ -152,6 +155,78 @@ def encode_bench(args, E, W, threads):
                                 "kind": "oracle", "sample": "the down projection (89,128,960 "
                                 "weights) encoded once by the plain C oracle encoder",
                                 "seconds": round(osec, 3)}
+    print(json.dumps(line), flush=True)
+
+
+def fused_bench(args, E, W, threads, m):
+    """--workload fused_down_m<m>: Y = X W'^T for the INT8-container MLP down projection
+    (5120 x 17408 at 6.0 bpp) and the first m rows of the 8192 x 17408 activations, W' never
+    written.  The first result is checked against the product of the GPU-decoded W'."""
+    import numpy as np
+    import torch
+    w = W.llm_mlp(["down"])["down"]
+    blob, _ = E.encode(w, 6.0, container=E.CONT_INT8_ROW, nthreads=threads)
+    info = E.blob_info(blob)
+    x_host = np.ascontiguousarray(W.llm_activations()[:m])
+    d_blob = E.to_device(blob, torch.device("cuda", 0))
+    x = torch.from_numpy(x_host).cuda()
+    y = torch.empty((m, info.rows), dtype=torch.int32, device="cuda")
+    dq = torch.empty(info.rows, dtype=torch.float32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        E.decode_matmul_i8(info, d_blob.data_ptr(), x.data_ptr(), m, y.data_ptr(), dq.data_ptr(),
+                           status.data_ptr(), stream.cuda_stream)
+
+    step()
+    wd, _, _ = E.decode(blob, E.INT8, d_blob=d_blob, info=info)
+    ref = x_host.astype(np.int64) @ wd.cpu().numpy().astype(np.int64).T
+    torch.cuda.synchronize()
+    assert np.array_equal(y.cpu().numpy(), ref), "fused product differs from decode-then-multiply"
+    t0 = time.perf_counter()
+    for _ in range(args.warmup):
+        step()
+    settle = 0
+    while time.perf_counter() - t0 < SETTLE_S:
+        for _ in range(10):
+            step()
+        settle += 10
+        torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(args.steps):
+        step()
+    b.record(stream)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+    ms = a.elapsed_time(b) / args.steps
+    weights = info.rows * info.cols
+    algo = blob.size + m * info.cols + 4 * m * info.rows + 4 * info.rows
+    gbps = algo / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "fused decode + product: decoded weights/s and achieved HBM GB/s (% roofline)",
+        "value": weights / (ms * 1e-3), "unit": "weights/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "i32", "data": "synthetic",
+        "config": {"workload": f"fused decode and product: MLP down 5120x17408 in the INT8 row "
+                               f"container at 6.0 bpp times X = {m} x 17408 int8 rows, Y int32 "
+                               f"exact, decoded weights never written", "rows_x": m,
+                   "weights": weights, "bytes_per_step": algo, "settle_steps": settle},
+        "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": gbps / HBM_PEAK_GBPS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        log("timing the CPU oracle: decode, then the product")
+        t = time.perf_counter()
+        wo, _ = O.decode(blob, O.INT8)
+        O.gemm_i8_nt(x_host, wo)
+        osec = time.perf_counter() - t
+        line["cpu_baseline"] = {"value": weights / osec, "unit": "weights/s", "cores": 1,
+                                "kind": "oracle", "sample": f"the whole down projection decoded by "
+                                f"the plain C oracle, then its exact product with the {m} rows",
+                                "seconds": round(osec, 3), "cpu": cpu_model()}
     print(json.dumps(line), flush=True)
 
 
@@ -344,6 +419,10 @@ def main():
         return
     if args.workload == "encode_mlp":
         encode_bench(args, E, W, min(16, len(os.sched_getaffinity(0))))
+        return
+    if args.workload.startswith("fused_down_m"):
+        m = int(args.workload[len("fused_down_m"):])
+        fused_bench(args, E, W, min(16, len(os.sched_getaffinity(0))), m)
         return
     threads = min(16, len(os.sched_getaffinity(0)))
 
