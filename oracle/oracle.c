@@ -27,9 +27,11 @@
  *   - rANS renormalisation threshold f*2^(31-b), states start at 2^15, words
  *     are consumed in (step ascending, lane ascending) order;
  *   - tile-local vector i belongs to lane i mod 32;
- *   - container routes: delta_r = fp32(amax_r/448) (FP8 e4m3fn) or
- *     fp32(amax_r/127) (INT8, symmetric), amax 0 gives delta 1, the quotient
- *     W/delta is formed in FP64 and rounded once into the container.
+ *   - container routes: delta_r = fp32(amax_r/448) (FP8 e4m3fn),
+ *     fp32(amax_r/57344) (FP8 e5m2) or fp32(amax_r/127) (INT8, symmetric),
+ *     amax 0 gives delta 1, the quotient W/delta is formed in FP64 and rounded
+ *     once into the container (the per-row FP8 scaling of Sec. 5.6's dtype
+ *     table, read for both FP8 formats).
  *   - per-row refinement (optional): candidate ratios are log-midpoints of
  *     the widest gaps of [0.70, 1.45] (the ends are not candidates);
  *     D_{r,k} uses the stored FP32 row scale in coded units; candidates join
@@ -57,8 +59,8 @@
 #define ORA_HEADER_BYTES 48u
 
 /* dtype codes (inputs: 1..3; outputs: 1..5, 100) */
-enum { O_BF16 = 1, O_FP16 = 2, O_FP32 = 3, O_FP8 = 4, O_INT8 = 5, O_COORD2 = 100 };
-enum { O_CONT_DIRECT = 0, O_CONT_FP8 = 1, O_CONT_INT8 = 2 };
+enum { O_BF16 = 1, O_FP16 = 2, O_FP32 = 3, O_FP8 = 4, O_INT8 = 5, O_FP8E5 = 6, O_COORD2 = 100 };
+enum { O_CONT_DIRECT = 0, O_CONT_FP8 = 1, O_CONT_INT8 = 2, O_CONT_FP8E5 = 3 };
 enum { O_OK = 0, O_ERR_ARG = -1, O_ERR_FORMAT = -2, O_ERR_UNSUPPORTED = -3,
        O_ERR_NOMEM = -4, O_ERR_CORRUPT = -6 };
 
@@ -113,6 +115,9 @@ static const double BF16_MAX = 3.38953138925153547590470800371487866880e+38; /* 
 static double snap_bf16(double y) { return snap_binary(y, 7, -126, BF16_MAX); }
 static double snap_fp16(double y) { return snap_binary(y, 10, -14, 65504.0); }
 static double snap_e4m3(double y) { return snap_binary(y, 3, -6, 448.0); }
+/* FP8 e5m2: 2 mantissa bits, normals from 2^-14, largest finite 57344; saturated
+ * like the other types (the format's infinities are never produced). */
+static double snap_e5m2(double y) { return snap_binary(y, 2, -14, 57344.0); }
 
 static uint16_t bf16_bits(double r) { /* r already a bf16 value: exact as float */
   float f = (float)r;
@@ -145,6 +150,18 @@ static uint8_t e4m3_bits(double r) { /* r already an e4m3fn value, |r| <= 448 */
   return (uint8_t)(s | ((uint8_t)(e + 7) << 3) | mant);
 }
 
+static uint8_t e5m2_bits(double r) { /* r already an e5m2 value, |r| <= 57344 */
+  uint8_t s = (r < 0 || (r == 0 && signbit(r))) ? 0x80 : 0;
+  double a = fabs(r);
+  if (a == 0) return s;
+  if (a < ldexp(1.0, -14)) return (uint8_t)(s | (uint8_t)(a / ldexp(1.0, -16)));
+  int e;
+  frexp(a, &e);
+  e -= 1;
+  uint8_t mant = (uint8_t)((a / ldexp(1.0, e) - 1.0) * 4.0);
+  return (uint8_t)(s | ((uint8_t)(e + 15) << 2) | mant);
+}
+
 static double bf16_value(uint16_t h) {
   uint32_t u = (uint32_t)h << 16;
   float f;
@@ -170,6 +187,15 @@ static double e4m3_value(uint8_t b) {
   return s ? -v : v;
 }
 
+static double e5m2_value(uint8_t b) {
+  int s = b >> 7, e = (b >> 2) & 31, m = b & 3;
+  double v;
+  if (e == 31) v = m ? NAN : INFINITY;
+  else if (e == 0) v = ldexp((double)m, -16);
+  else v = ldexp(1.0 + m / 4.0, e - 15);
+  return s ? -v : v;
+}
+
 /* Test hook: snap doubles to an output dtype and write its bit patterns.
  * INT8 is clamp(RNE(y), -128, 127).  Pinned against torch CPU casts. */
 int ora_snap(const double* y, int64_t n, int dtype, void* out) {
@@ -180,6 +206,7 @@ int ora_snap(const double* y, int64_t n, int dtype, void* out) {
       case O_FP16: ((uint16_t*)out)[i] = fp16_bits(snap_fp16(v)); break;
       case O_FP32: ((float*)out)[i] = (float)v; break;
       case O_FP8: ((uint8_t*)out)[i] = e4m3_bits(snap_e4m3(v)); break;
+      case O_FP8E5: ((uint8_t*)out)[i] = e5m2_bits(snap_e5m2(v)); break;
       case O_INT8: {
         double r = nearbyint(v);
         if (r > 127) r = 127;
@@ -502,7 +529,7 @@ static int prepare_values(const void* w, int dtype, int64_t R, int64_t C, int co
       if (fabs(v) > amax) amax = fabs(v);
     }
     if (container == O_CONT_DIRECT) continue;
-    double qmax = container == O_CONT_FP8 ? 448.0 : 127.0;
+    double qmax = container == O_CONT_FP8 ? 448.0 : container == O_CONT_FP8E5 ? 57344.0 : 127.0;
     float d = amax > 0 ? (float)(amax / qmax) : 1.0f;
     delta[r] = d;
     for (int64_t j = 0; j < C; j++) {
@@ -510,6 +537,8 @@ static int prepare_values(const void* w, int dtype, int64_t R, int64_t C, int co
       double cv;
       if (container == O_CONT_FP8) {
         cv = snap_e4m3(q);
+      } else if (container == O_CONT_FP8E5) {
+        cv = snap_e5m2(q);
       } else {
         cv = nearbyint(q);
         if (cv > 127) cv = 127;
@@ -909,7 +938,7 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
   if (!w || !prm || !out_blob || !out_size || R <= 0 || C <= 0 || C % 8) return O_ERR_ARG;
   if (dtype != O_BF16 && dtype != O_FP16 && dtype != O_FP32) return O_ERR_ARG;
   if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0) return O_ERR_ARG;
-  if (prm->container < 0 || prm->container > 2) return O_ERR_ARG;
+  if (prm->container < 0 || prm->container > 3) return O_ERR_ARG;
   if (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) return O_ERR_ARG;
   if (prm->rdo_candidates > 64 || prm->rdo_sweeps < 0) return O_ERR_ARG;
   if ((R * C) / 8 > 0xFFFFFFFFll || R > 0xFFFFFFFFll || C > 0xFFFFFFFFll) return O_ERR_ARG;
@@ -1151,7 +1180,7 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
     /* statistics */
     double cce_full = tables_code_length(T, b);
     double err_c = 0, ref_c = 0, err_o = 0, ref_o = 0;
-    int rdt = cont == O_CONT_FP8 ? O_FP8 : cont == O_CONT_INT8 ? O_INT8 : dtype;
+    int rdt = cont == O_CONT_FP8 ? O_FP8 : cont == O_CONT_FP8E5 ? O_FP8E5 : cont == O_CONT_INT8 ? O_INT8 : dtype;
     for (int64_t r = 0; r < R; r++) {
       for (int64_t j = 0; j < C; j++) {
         double y = (double)(float)((double)sigma[r] * (two_p[r * C + j] / 2.0));
@@ -1160,6 +1189,7 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
           case O_BF16: wh = snap_bf16(y); break;
           case O_FP16: wh = snap_fp16(y); break;
           case O_FP8: wh = snap_e4m3(y); break;
+          case O_FP8E5: wh = snap_e5m2(y); break;
           case O_INT8: {
             wh = nearbyint(y);
             if (wh > 127) wh = 127;
@@ -1290,7 +1320,7 @@ static int parse_blob(const uint8_t* blob, uint64_t n, blobview* bv, table_t* T)
   bv->n_words = get32(blob + 36);
   bv->total = get64(blob + 40);
   if (bv->total != n || bv->R == 0 || bv->C == 0 || bv->C % 8 || bv->b < 9 || bv->b > 15 ||
-      bv->V == 0 || bv->container > 2)
+      bv->V == 0 || bv->container > 3)
     return O_ERR_FORMAT;
   uint64_t nvec = (uint64_t)bv->R * bv->C / 8;
   if (bv->n_tiles != n_tiles_of(nvec, bv->V)) return O_ERR_FORMAT;
@@ -1381,6 +1411,7 @@ static void write_output(void* out, int dtype, uint64_t e, float y) {
     case O_FP16: ((uint16_t*)out)[e] = fp16_bits(snap_fp16(v)); break;
     case O_FP32: ((float*)out)[e] = y; break;
     case O_FP8: ((uint8_t*)out)[e] = e4m3_bits(snap_e4m3(v)); break;
+    case O_FP8E5: ((uint8_t*)out)[e] = e5m2_bits(snap_e5m2(v)); break;
     case O_INT8: {
       double r = nearbyint(v);
       if (r > 127) r = 127;
@@ -1408,7 +1439,7 @@ int ora_decode(const uint8_t* blob, uint64_t n, int out_dtype, void* out, float*
   int rc = parse_blob(blob, n, &bv, T);
   if (rc) goto out;
   if (out_dtype != O_BF16 && out_dtype != O_FP16 && out_dtype != O_FP32 && out_dtype != O_FP8 &&
-      out_dtype != O_INT8 && out_dtype != O_COORD2) {
+      out_dtype != O_FP8E5 && out_dtype != O_INT8 && out_dtype != O_COORD2) {
     rc = O_ERR_ARG;
     goto out;
   }
@@ -1527,7 +1558,7 @@ int ora_estimate(const int32_t* fields, int64_t nvec, int64_t rows, int32_t b, i
 }
 
 /* Test hook: values of output bit patterns (BF16, FP16, FP32, FP8 e4m3fn,
- * INT8, or 2p as int32) as doubles. */
+ * FP8 e5m2, INT8, or 2p as int32) as doubles. */
 int ora_values(const void* bits, int64_t n, int dtype, double* out) {
   for (int64_t i = 0; i < n; i++) {
     switch (dtype) {
@@ -1535,6 +1566,7 @@ int ora_values(const void* bits, int64_t n, int dtype, double* out) {
       case O_FP16: out[i] = fp16_value(((const uint16_t*)bits)[i]); break;
       case O_FP32: out[i] = ((const float*)bits)[i]; break;
       case O_FP8: out[i] = e4m3_value(((const uint8_t*)bits)[i]); break;
+      case O_FP8E5: out[i] = e5m2_value(((const uint8_t*)bits)[i]); break;
       case O_INT8: out[i] = ((const int8_t*)bits)[i]; break;
       case O_COORD2: out[i] = ((const int32_t*)bits)[i] / 2.0; break;
       default: return O_ERR_ARG;

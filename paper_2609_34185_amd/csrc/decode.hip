@@ -181,6 +181,13 @@ __device__ __forceinline__ uint32_t fp8_quad(float a, float b, float c, float d)
   return (uint32_t)w;
 }
 
+// The same for OCP e5m2 (v_cvt_pk_bf8_f32: round to nearest even).
+__device__ __forceinline__ uint32_t e5m2_quad(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_bf8_f32(a, b, (int)__float_as_uint(a), false);
+  w = __builtin_amdgcn_cvt_pk_bf8_f32(c, d, w, true);
+  return (uint32_t)w;
+}
+
 __device__ __forceinline__ uint32_t int8_quad(float a, float b, float c, float d) {
   int ia = (int)__builtin_rintf(sat(a, 128.0f)), ib = (int)__builtin_rintf(sat(b, 128.0f));
   int ic = (int)__builtin_rintf(sat(c, 128.0f)), id = (int)__builtin_rintf(sat(d, 128.0f));
@@ -222,6 +229,12 @@ __device__ __forceinline__ void store_vec(void* out, uint32_t v, const int32_t* 
 #pragma unroll
       for (int j = 0; j < 8; j++) y[j] = sat(y[j], 448.0f);
     const u32x2 o = {fp8_quad(y[0], y[1], y[2], y[3]), fp8_quad(y[4], y[5], y[6], y[7])};
+    gptr<u32x2>(out)[v] = o;
+  } else if constexpr (DT == EP_FP8_E5M2) {
+    if constexpr (SAT)
+#pragma unroll
+      for (int j = 0; j < 8; j++) y[j] = sat(y[j], 57344.0f);
+    const u32x2 o = {e5m2_quad(y[0], y[1], y[2], y[3]), e5m2_quad(y[4], y[5], y[6], y[7])};
     gptr<u32x2>(out)[v] = o;
   } else if constexpr (DT == EP_INT8) {
     const u32x2 o = {int8_quad(y[0], y[1], y[2], y[3]), int8_quad(y[4], y[5], y[6], y[7])};
@@ -288,6 +301,10 @@ __device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int
     case EP_FP8_E4M3:
       if (L.saturate) store_vec<EP_FP8_E4M3, true>(L.out, v, p2, half_sigma);
       else store_vec<EP_FP8_E4M3, false>(L.out, v, p2, half_sigma);
+      break;
+    case EP_FP8_E5M2:
+      if (L.saturate) store_vec<EP_FP8_E5M2, true>(L.out, v, p2, half_sigma);
+      else store_vec<EP_FP8_E5M2, false>(L.out, v, p2, half_sigma);
       break;
     case EP_INT8: store_vec<EP_INT8, false>(L.out, v, p2, half_sigma); break;
     default: store_vec<EP_COORD2_I32, false>(L.out, v, p2, half_sigma); break;
@@ -1191,6 +1208,9 @@ __device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float y, uint32_t c)
       // the low half is written first; its high half is overwritten by the next pair
       a.w[p / 2] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(
           y0, y1, (int)(p & 1 ? a.w[p / 2] : __float_as_uint(y0)), (p & 1) != 0);
+    } else if constexpr (DT == EP_FP8_E5M2) {
+      a.w[p / 2] = (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(
+          y0, y1, (int)(p & 1 ? a.w[p / 2] : __float_as_uint(y0)), (p & 1) != 0);
     } else {  // EP_INT8
       const uint32_t h = int8_pair(y0, y1);
       a.w[p / 2] = p & 1 ? (a.w[p / 2] | (h << 16)) : h;
@@ -1203,7 +1223,7 @@ template <int DT>
 __device__ __forceinline__ void q_put(EP_GLOBAL uint8_t* base, uint32_t off, const QAcc& a) {
   if constexpr (DT == EP_BF16 || DT == EP_FP16) {
     *reinterpret_cast<EP_GLOBAL u32x4*>(base + off) = u32x4{a.w[0], a.w[1], a.w[2], a.w[3]};
-  } else if constexpr (DT == EP_FP8_E4M3 || DT == EP_INT8) {
+  } else if constexpr (DT == EP_FP8_E4M3 || DT == EP_FP8_E5M2 || DT == EP_INT8) {
     *reinterpret_cast<EP_GLOBAL u32x2*>(base + off) = u32x2{a.w[0], a.w[1]};
   } else {
     EP_GLOBAL u32x4* o = reinterpret_cast<EP_GLOBAL u32x4*>(base + off);
@@ -1215,7 +1235,8 @@ __device__ __forceinline__ void q_put(EP_GLOBAL uint8_t* base, uint32_t off, con
 // Bytes of one 8-weight vector in output type DT.
 template <int DT>
 constexpr uint32_t vec_bytes() {
-  return DT == EP_FP8_E4M3 || DT == EP_INT8 ? 8u : (DT == EP_BF16 || DT == EP_FP16) ? 16u : 32u;
+  return DT == EP_FP8_E4M3 || DT == EP_FP8_E5M2 || DT == EP_INT8 ? 8u
+         : (DT == EP_BF16 || DT == EP_FP16) ? 16u : 32u;
 }
 
 // Sum of v over the 32 lanes of each half-wave, valid in lanes 0 and 32 (the
@@ -1262,7 +1283,8 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
   // weights formed in the steps: none for the doubled-coordinate output,
   // clamped to the type's finite range when SAT
   constexpr int YM = DT == EP_COORD2_I32 ? 0 : SAT ? 2 : 1;
-  const float ymax = DT == EP_FP8_E4M3 ? 448.0f : DT == EP_FP16 ? 65504.0f : 3.38953139e38f;
+  const float ymax = DT == EP_FP8_E4M3 ? 448.0f : DT == EP_FP8_E5M2 ? 57344.0f
+                     : DT == EP_FP16 ? 65504.0f : 3.38953139e38f;
 
   const uint32_t vrb0 = ring_area + wave * 2 * kFastChainBytes + half * kFastRingBytes;
   const uint32_t vrb1 = vrb0 + kFastChainBytes;
@@ -1476,6 +1498,10 @@ __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_
       if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true, WIDE>(L, lds, ring_area, t0, status);
       else lut_task_rows<B, EP_FP8_E4M3, false, WIDE>(L, lds, ring_area, t0, status);
       return true;
+    case EP_FP8_E5M2:
+      if (L.saturate) lut_task_rows<B, EP_FP8_E5M2, true, WIDE>(L, lds, ring_area, t0, status);
+      else lut_task_rows<B, EP_FP8_E5M2, false, WIDE>(L, lds, ring_area, t0, status);
+      return true;
     case EP_INT8: lut_task_rows<B, EP_INT8, false, WIDE>(L, lds, ring_area, t0, status); return true;
     case EP_FP32: lut_task_rows<B, EP_FP32, false, WIDE>(L, lds, ring_area, t0, status); return true;
     case EP_COORD2_I32: lut_task_rows<B, EP_COORD2_I32, false, WIDE>(L, lds, ring_area, t0, status); return true;
@@ -1504,6 +1530,10 @@ __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds,
     case EP_FP8_E4M3:
       if (L.saturate) decode_task_fast<PATH, B, EP_FP8_E4M3, true>(L, lds, ring_area, task, status);
       else decode_task_fast<PATH, B, EP_FP8_E4M3, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_FP8_E5M2:
+      if (L.saturate) decode_task_fast<PATH, B, EP_FP8_E5M2, true>(L, lds, ring_area, task, status);
+      else decode_task_fast<PATH, B, EP_FP8_E5M2, false>(L, lds, ring_area, task, status);
       return true;
     case EP_INT8:
       decode_task_fast<PATH, B, EP_INT8, false>(L, lds, ring_area, task, status);
@@ -1726,13 +1756,14 @@ float dtype_max(int dt) {
     case EP_BF16: return 3.38953139e38f;
     case EP_FP16: return 65504.0f;
     case EP_FP8_E4M3: return 448.0f;
+    case EP_FP8_E5M2: return 57344.0f;
     default: return 3.4e38f;
   }
 }
 
 bool valid_out_dtype(int dt) {
-  return dt == EP_BF16 || dt == EP_FP16 || dt == EP_FP32 || dt == EP_FP8_E4M3 || dt == EP_INT8 ||
-         dt == EP_COORD2_I32;
+  return dt == EP_BF16 || dt == EP_FP16 || dt == EP_FP32 || dt == EP_FP8_E4M3 || dt == EP_FP8_E5M2 ||
+         dt == EP_INT8 || dt == EP_COORD2_I32;
 }
 
 int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void* d_out,

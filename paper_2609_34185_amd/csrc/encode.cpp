@@ -302,13 +302,11 @@ struct CpuBackend {
           amax = std::max(amax, std::fabs((double)v));
         }
         if (cont) {
-          float d = amax > 0 ? (float)(amax / (cont == EP_CONT_FP8_ROW ? 448.0 : 127.0)) : 1.0f;
+          float d = amax > 0 ? (float)(amax / em::container_max(cont)) : 1.0f;
           delta[r] = d;
           for (int64_t j = 0; j < C; j++) {
             double q = (double)xr[j] / (double)d;
-            double cv = cont == EP_CONT_FP8_ROW ? to_e4m3(q) : std::nearbyint(q);
-            if (cont == EP_CONT_INT8_ROW) cv = std::min(127.0, std::max(-127.0, cv));
-            xr[j] = (float)cv;
+            xr[j] = (float)em::container_snap(cont, q);
           }
         }
         double ss = 0;
@@ -549,8 +547,7 @@ struct CpuBackend {
           em::join_fields(fl.data() + 9 * (r * cvec + jv), two);
           for (int j = 0; j < 8; j++) {
             double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
-            double v = rdt == EP_BF16 ? to_bf16(y) : rdt == EP_FP16 ? to_fp16(y)
-                     : rdt == EP_FP8_E4M3 ? to_e4m3(y) : rdt == EP_INT8 ? int8_snap(y) : y;
+            double v = em::snap_out(rdt, y);
             double xc = x[r * C + 8 * jv + j];
             ec += (v - xc) * (v - xc);
             rc += xc * xc;
@@ -879,7 +876,7 @@ int check_args(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
   if (w_dtype != EP_BF16 && w_dtype != EP_FP16 && w_dtype != EP_FP32)
     return fail(EP_ERR_ARG, "ep_encode: input dtype must be BF16, FP16 or FP32");
   if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0 ||
-      prm->container < 0 || prm->container > 2 || !(prm->scale_lo > 0) ||
+      prm->container < 0 || prm->container > 3 || !(prm->scale_lo > 0) ||
       !(prm->scale_hi > prm->scale_lo) || prm->sample_vectors < 1 ||
       (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) ||
       prm->rdo_candidates > 64 || prm->rdo_sweeps < 0)
@@ -1024,7 +1021,7 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
 
   if (stats) {
     // reconstruction error in the dtype of the coded values
-    int rdt = cont == EP_CONT_FP8_ROW ? EP_FP8_E4M3 : cont == EP_CONT_INT8_ROW ? EP_INT8 : w_dtype;
+    int rdt = em::container_dtype(cont, w_dtype);
     std::vector<double> acc;
     rc = E.errors(sigma, rdt, cont, acc);
     if (rc != EP_OK) {

@@ -74,13 +74,11 @@ __global__ __launch_bounds__(256) void k_prep_rows(const void* w, int dt, int64_
   if (t == 0 && s_bad) atomicOr(bad, 1);
   if (!cont) return;
   amax = s_amax[0];
-  const float d = amax > 0 ? (float)(amax / (cont == EP_CONT_FP8_ROW ? 448.0 : 127.0)) : 1.0f;
+  const float d = amax > 0 ? (float)(amax / em::container_max(cont)) : 1.0f;
   if (t == 0) delta[r] = d;
   for (int64_t j = t; j < C; j += 256) {
     const double q = (double)load_input(w, dt, base + j) / (double)d;
-    double cv = cont == EP_CONT_FP8_ROW ? em::to_e4m3(q) : __builtin_rint(q);
-    if (cont == EP_CONT_INT8_ROW) cv = cv > 127.0 ? 127.0 : (cv < -127.0 ? -127.0 : cv);
-    x[base + j] = (float)cv;
+    x[base + j] = (float)em::container_snap(cont, q);
   }
 }
 
@@ -322,8 +320,7 @@ __global__ __launch_bounds__(256) void k_errors(const void* w, int dt, const flo
     em::join_fields(fl + 9 * (r * cvec + jv), two);
     for (int j = 0; j < 8; j++) {
       const double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
-      const double v = rdt == EP_BF16 ? em::to_bf16(y) : rdt == EP_FP16 ? em::to_fp16(y)
-                     : rdt == EP_FP8_E4M3 ? em::to_e4m3(y) : rdt == EP_INT8 ? em::int8_snap(y) : y;
+      const double v = em::snap_out(rdt, y);
       const double xc = x[r * C + 8 * jv + j];
       ec += (v - xc) * (v - xc);
       rc += xc * xc;

@@ -6,6 +6,8 @@
 #include <cmath>
 #include <cstdint>
 
+#include "../../include/entropack.h"
+
 #if defined(__HIPCC__)
 #define EP_HD __host__ __device__
 #else
@@ -31,12 +33,36 @@ EP_HD inline double round_to_format(double v, int frac, int emin, double vmax) {
 }
 
 EP_HD inline double to_e4m3(double v) { return round_to_format(v, 3, -6, 448.0); }
+EP_HD inline double to_e5m2(double v) { return round_to_format(v, 2, -14, 57344.0); }
+
+// Largest magnitude of a row container (delta_r = amax_r / qmax) and the
+// rounding of a quotient W / delta_r into it.
+EP_HD inline double container_max(int cont) {
+  return cont == EP_CONT_FP8_ROW ? 448.0 : cont == EP_CONT_FP8E5M2_ROW ? 57344.0 : 127.0;
+}
+EP_HD inline double container_snap(int cont, double q) {
+  if (cont == EP_CONT_FP8_ROW) return to_e4m3(q);
+  if (cont == EP_CONT_FP8E5M2_ROW) return to_e5m2(q);
+  const double r = std::nearbyint(q);
+  return r > 127.0 ? 127.0 : (r < -127.0 ? -127.0 : r);
+}
+// Output type in which a container's values are reconstructed.
+EP_HD inline int container_dtype(int cont, int direct) {
+  return cont == EP_CONT_FP8_ROW ? EP_FP8_E4M3 : cont == EP_CONT_FP8E5M2_ROW ? EP_FP8_E5M2
+         : cont == EP_CONT_INT8_ROW ? EP_INT8 : direct;
+}
 EP_HD inline double to_bf16(double v) { return round_to_format(v, 7, -126, 3.3895313892515355e38); }
 EP_HD inline double to_fp16(double v) { return round_to_format(v, 10, -14, 65504.0); }
 
 EP_HD inline double int8_snap(double v) {
   double r = std::nearbyint(v);
   return r > 127 ? 127 : (r < -128 ? -128 : r);
+}
+
+// y snapped to output type dt (FP32 and others: y itself).
+EP_HD inline double snap_out(int dt, double y) {
+  return dt == EP_BF16 ? to_bf16(y) : dt == EP_FP16 ? to_fp16(y) : dt == EP_FP8_E4M3 ? to_e4m3(y)
+         : dt == EP_FP8_E5M2 ? to_e5m2(y) : dt == EP_INT8 ? int8_snap(y) : y;
 }
 
 // Nearest point of D8: coordinate rounding (ties to even), then, if the sum is

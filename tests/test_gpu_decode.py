@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-DTYPES = ["COORD2", "BF16", "FP16", "FP32", "FP8", "INT8"]
+DTYPES = ["COORD2", "BF16", "FP16", "FP32", "FP8", "INT8", "E5M2"]
 
 
 def say(*a):
@@ -35,7 +35,8 @@ def E():
 def codes(E, oracle, name):
     return {"COORD2": (E.COORD2_I32, oracle.COORD2), "BF16": (E.BF16, oracle.BF16),
             "FP16": (E.FP16, oracle.FP16), "FP32": (E.FP32, oracle.FP32),
-            "FP8": (E.FP8_E4M3, oracle.FP8), "INT8": (E.INT8, oracle.INT8)}[name]
+            "FP8": (E.FP8_E4M3, oracle.FP8), "INT8": (E.INT8, oracle.INT8),
+            "E5M2": (E.FP8_E5M2, oracle.FP8E5)}[name]
 
 
 def gpu_bits(t):
@@ -43,7 +44,7 @@ def gpu_bits(t):
     t = t.cpu()
     if t.dtype in (torch.bfloat16, torch.float16):
         return t.view(torch.int16).numpy().view(np.uint16)
-    if t.dtype == torch.float8_e4m3fn:
+    if t.dtype in (torch.float8_e4m3fn, torch.float8_e5m2):
         return t.view(torch.uint8).numpy()
     return t.numpy()
 
@@ -195,7 +196,23 @@ def test_saturation(E, oracle):
     w = (rng.standard_normal((32, 256)) * 3e4).astype(np.float32)
     w[0, :8] = 1e5
     blob, st = oracle.encode(w, 5.0)
-    check_blob(E, oracle, blob, dtypes=["FP16", "FP8", "INT8", "BF16"], tag="sat")
+    check_blob(E, oracle, blob, dtypes=["FP16", "FP8", "INT8", "BF16", "E5M2"], tag="sat")
+    w[1, :8] = 9e4   # beyond e5m2's 57344
+    blob, st = oracle.encode(w, 5.0)
+    check_blob(E, oracle, blob, dtypes=["E5M2"], tag="sat e5m2")
+
+
+@pytest.mark.parametrize("shape,target,kw", [
+    ((96, 8 * 1000), 4.0, {}),                        # full tasks, slot-table steady state
+    ((64, 8 * 640), 7.0, {}),                         # larger coordinates
+    ((37, 136), 4.0, dict(tile_vectors=45)),          # ragged tiles: the generic loop
+    ((64, 8 * 600), 6.0, dict(prob_bits=12)),         # the bucketed-search path
+])
+def test_fp8_e5m2_container(E, oracle, shape, target, kw):
+    """The FP8 e5m2 row container (the paper's dtype table) decoded to e5m2 with its row scales."""
+    w = W.ragged_tensor(31, *shape, scale=0.05)
+    blob, _ = oracle.encode(w, target, container=oracle.CONT_FP8E5, **kw)
+    check_blob(E, oracle, blob, dtypes=["E5M2", "COORD2", "FP32"], tag="e5m2 container")
 
 
 def test_corrupt_payload_sets_status_without_fault(E, oracle):

@@ -262,6 +262,56 @@ def test_conversions_match_torch_casts(oracle):
     assert i8.tolist() == [127, 127, -128, -128, 2, -2, 4]
 
 
+def test_e5m2_conversion_matches_torch_casts(oracle):
+    """FP8 e5m2 (2 mantissa bits, normals from 2^-14, subnormal quantum 2^-16, largest finite
+    57344): round to nearest even on in-range values, saturation beyond, values of the bit
+    patterns, all against torch's CPU float8_e5m2."""
+    rng = np.random.default_rng(23)
+    y = np.concatenate([
+        rng.standard_normal(20000) * 10.0 ** rng.uniform(-8, 4.6, 20000),
+        np.arange(-400, 400) * 0.125,                         # ties at several exponents
+        np.ldexp(np.arange(1, 48, dtype=np.float64), -17),    # subnormals and their ties
+        np.array([0.0, -0.0, 57344.0, -57344.0, 49152.0, 2.0 ** -14, 2.0 ** -16]),
+    ]).astype(np.float32).astype(np.float64)
+    inr = np.abs(y) <= 57344
+    t = torch.from_numpy(y[inr]).float()
+    f8 = oracle.snap(y[inr], oracle.FP8E5)
+    assert np.array_equal(f8, t.to(torch.float8_e5m2).view(torch.uint8).numpy())
+    vals = oracle.values(f8, oracle.FP8E5)
+    assert np.array_equal(vals, t.to(torch.float8_e5m2).to(torch.float64).numpy())
+    big = np.array([1e6, -1e6, 57345.0, 61439.0, 61440.0, -7e4])
+    assert oracle.values(oracle.snap(big, oracle.FP8E5), oracle.FP8E5).tolist() == [57344, -57344] + [57344] * 3 + [-57344]
+
+
+def test_e5m2_container_route(oracle):
+    """The FP8 e5m2 row container: delta_r = fp32(amax_r / 57344), coded values are the
+    e5m2 roundings of W / delta_r, the decode to e5m2 reproduces them and delta exactly."""
+    w = W.ragged_tensor(9, 48, 256, scale=0.05)
+    blob, st = oracle.encode(w, 4.0, container=oracle.CONT_FP8E5)
+    assert oracle.header(blob)["container"] == oracle.CONT_FP8E5
+    tp, xv, _ = oracle.quantize(w, st["scale"], container=oracle.CONT_FP8E5)
+    wf = W.bf16_bits_to_f32(w).astype(np.float64)
+    delta = (np.abs(wf).max(axis=1) / 57344.0).astype(np.float32)
+    x64 = xv.astype(np.float64)
+    back = torch.from_numpy(x64).to(torch.float8_e5m2).to(torch.float64).numpy()
+    assert np.array_equal(back, x64)
+    q = wf / delta[:, None]
+    ref = torch.from_numpy(q).to(torch.float8_e5m2).to(torch.float64).numpy()
+    diff = x64 != ref
+    assert diff.mean() < 0.01
+    assert np.all(np.abs(x64 - q)[diff] < np.abs(ref - q)[diff])
+    out, dq = oracle.decode(blob, oracle.FP8E5)
+    assert np.array_equal(dq, delta)
+    two_p, _ = oracle.decode(blob, oracle.COORD2)
+    assert np.array_equal(two_p, tp)
+    # the decoded codes are the e5m2 roundings of fp32(sigma_r * p)
+    h = oracle.header(blob)
+    off = 48 + h["table_bytes"]
+    sig = np.frombuffer(blob[off:off + 4 * h["rows"]].tobytes(), dtype=np.float32).astype(np.float64)
+    y = (sig[:, None] * (two_p / 2.0)).astype(np.float32).astype(np.float64)
+    assert np.array_equal(out, oracle.snap(y.ravel(), oracle.FP8E5).reshape(out.shape))
+
+
 def test_high_resolution_rate_law_loosely(oracle):
     """Sanity only (parity unpinned for E_rel on synthetic data): at high rate the error of a
     unit-Gaussian source falls by about 2x per extra bit per weight [eq. high_resolution]."""
