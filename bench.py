@@ -23,7 +23,10 @@ at 4.0 bpp; a step encodes all three; the CPU baseline is the oracle encoder
 on the down projection), fused_down_m1 / _m2 / _m4 / _m8 (the fused decode and
 small-batch product ep_decode_matmul_i8: the INT8-container down projection
 times the first 1, 2, 4 or 8 rows of the activations, one launch per step;
-algorithmic bytes = compressed blob + X read, Y and dequant written).
+algorithmic bytes = compressed blob + X read, Y and dequant written),
+tile_sweep (the paper's reference-layer shape 10240 x 3840 at 4.0 bpp to BF16,
+encoded and decoded at tile sizes of 128 to 3640 vectors: stored rate, tile
+count and decode time per size; value is the 512-vector point).
 
 The roofline's `traffic` field is the decode kernel's measured HBM bytes per
 launch, read from the committed rocprofv3 counter summary of this workload
@@ -230,6 +233,65 @@ def fused_bench(args, E, W, threads, m):
     print(json.dumps(line), flush=True)
 
 
+SWEEP_V = (128, 256, 512, 1024, 1820, 2048, 3640)
+
+
+def tile_sweep(args, E, W, threads):
+    """--workload tile_sweep: one layer of the reference shape (10240 x 3840, the DiT stack's
+    first MLP input projection) at 4.0 bpp, decoded to BF16, for several tile sizes V (the
+    paper's 4096, 8192, 16384 and 32768 symbols per tile are V = 455, 910, 1820, 3640)."""
+    import torch
+    w = dict(W.dit_block(0))["blocks.0.mlp_in"]
+    weights = w.size
+    rows = []
+    for V in SWEEP_V:
+        blob, st = E.encode(w, 4.0, tile_vectors=V, nthreads=threads)
+        info = E.blob_info(blob)
+        d_blob = E.to_device(blob)
+        out = torch.empty((info.rows, info.cols), dtype=torch.bfloat16, device="cuda")
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        s = torch.cuda.current_stream()
+
+        def step():
+            E.decode_tiles(info, d_blob.data_ptr(), E.BF16, out.data_ptr(), 0, 0, info.n_tiles,
+                           status.data_ptr(), s.cuda_stream)
+
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < SETTLE_S:
+            for _ in range(10):
+                step()
+            torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(args.steps):
+            step()
+        b.record(s)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0, "decode reported a corrupt stream"
+        ms = a.elapsed_time(b) / args.steps
+        steady = V % 32 == 0
+        rows.append({"V": V, "symbols_per_tile": 9 * V, "tiles": info.n_tiles,
+                     "stored_bpp": round(8.0 * blob.size / weights, 4),
+                     "erel_pct": round(100.0 * st["erel_coded"], 3), "ms": ms,
+                     "weights_per_s": weights / (ms * 1e-3),
+                     "gbps": (blob.size + 2 * weights) / (ms * 1e-3) / 1e9,
+                     "steady_state": steady})
+        log(f"V={V}: {rows[-1]['stored_bpp']} bpp, E_rel {rows[-1]['erel_pct']} %, {ms * 1e3:.1f} us")
+    ref = [r for r in rows if r["V"] == 512][0]
+    line = {
+        "metric": "decoded weights/s per tile size (reference layer)", "value": ref["weights_per_s"],
+        "unit": "weights/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ref["ms"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u32", "data": "synthetic",
+        "config": {"workload": "tile-size sweep: 10240x3840 BF16 (Student-t rows) at 4.0 bpp, "
+                               "decoded to BF16, one tensor per launch", "weights": weights,
+                   "sweep": rows},
+        "roofline": {"bound": "hbm", "achieved": ref["gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": ref["gbps"] / HBM_PEAK_GBPS, "traffic": None},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def source_digest() -> str:
     with open(DECODE_SRC, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
@@ -419,6 +481,9 @@ def main():
         return
     if args.workload == "encode_mlp":
         encode_bench(args, E, W, min(16, len(os.sched_getaffinity(0))))
+        return
+    if args.workload == "tile_sweep":
+        tile_sweep(args, E, W, min(16, len(os.sched_getaffinity(0))))
         return
     if args.workload.startswith("fused_down_m"):
         m = int(args.workload[len("fused_down_m"):])
