@@ -278,3 +278,59 @@ def gemm_i8_nt(a: np.ndarray, b: np.ndarray, rows=None) -> np.ndarray:
         rc = L.ora_gemm_i8_nt(_ptr(a), _ptr(b), _ptr(y), m, n, k, _ptr(r), r.size)
     _chk(rc, "gemm_i8_nt")
     return y
+
+
+def _table_bits(values: np.ndarray, b: int):
+    """(code length in bits, serialized bytes, alphabet) of one table built from `values`:
+    counts over [min, max], frequencies normalised to 2^b, min:i32 + A:u32 + f:u16[A]."""
+    if values.size == 0:
+        return 0.0, 8, 0
+    lo, hi = int(values.min()), int(values.max())
+    counts = np.bincount(values - lo, minlength=hi - lo + 1).astype(np.uint64)
+    A = counts.size
+    if A > (1 << b):
+        return float("inf"), 8 + 2 * A, A
+    f = normalize(counts, b)
+    return code_length(counts, f, b), 8 + 2 * A, A
+
+
+def coding_ablation(blob: np.ndarray) -> dict:
+    """Stored bits of a blob's own lattice points under the three coding models of the
+    entropy-model ablation (App. D.2, Table coding; eqs. cond, parity, conditioning_gain):
+      'entropack': coset table + one table per (field, coset), fields (c, z1..z7, m);
+      'pooled':    coset table + one table per field for both cosets (no conditioning);
+      'direct_z8': as 'entropack' with z8 = 2m + pi coded in place of m (no parity reduction).
+    Every variant keeps the points, row scales, tiles and precision b, and builds its tables
+    from its own fields.  Payload: the exact code length of the fields under the variant's
+    b-bit tables (eq. length); the stored size is the blob's own size plus each variant's
+    difference in code length and in serialized table bytes from the blob's model (so the
+    per-tile state and padding overheads, common to all three, are the blob's own)."""
+    h = header(blob)
+    b = h["b"]
+    two_p, _ = decode(blob, COORD2)
+    f9 = fields(two_p)
+    c = f9[:, 0]
+    z8 = (two_p.reshape(-1, 8)[:, 7] - c) // 2
+    out = {}
+    for name in ("entropack", "pooled", "direct_z8"):
+        bits, tbytes = _table_bits(c, b)[:2]
+        for i in range(1, 9):
+            col = z8 if (name == "direct_z8" and i == 8) else f9[:, i]
+            if name == "pooled":
+                parts = [col]
+            else:
+                parts = [col[c == 0], col[c == 1]]
+            for p in parts:
+                cl, tb, _ = _table_bits(p, b)
+                bits += cl
+                tbytes += tb
+        out[name] = (bits, tbytes)
+    base_bits, base_tbytes = out["entropack"]
+    n = h["rows"] * h["cols"]
+    res = {"b": b, "weights": n, "stored_bits": {}, "code_bits": {}}
+    for name, (bits, tbytes) in out.items():
+        stored = 8.0 * h["total_bytes"] + (bits - base_bits) + 8.0 * (tbytes - base_tbytes)
+        res["stored_bits"][name] = stored
+        res["code_bits"][name] = bits
+        res[name + "_bpp"] = stored / n
+    return res
