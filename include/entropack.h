@@ -71,6 +71,7 @@ enum ep_dtype {
   EP_FP8_E4M3 = 4,         /* OCP e4m3fn, nearest even incl. subnormals, saturating at +-448 */
   EP_INT8 = 5,             /* clamp(round-half-even(y), -128, 127) */
   EP_FP8_E5M2 = 6,         /* OCP e5m2, nearest even incl. subnormals, saturating at +-57344 */
+  EP_UINT8 = 7,            /* clamp(round-half-even(y), 0, 255) */
   EP_COORD2_I32 = 100      /* debug: the doubled lattice coordinates 2p as int32 */
 };
 
@@ -78,7 +79,10 @@ enum ep_container {
   EP_CONT_DIRECT = 0,      /* the input values are coded directly */
   EP_CONT_FP8_ROW = 1,     /* row-scaled FP8 e4m3fn container (Appendix A.6, B.1) */
   EP_CONT_INT8_ROW = 2,    /* row-scaled symmetric INT8 container (Appendix B.1) */
-  EP_CONT_FP8E5M2_ROW = 3  /* row-scaled FP8 e5m2 container (the dtype table of Sec. 5.6) */
+  EP_CONT_FP8E5M2_ROW = 3, /* row-scaled FP8 e5m2 container (the dtype table of Sec. 5.6) */
+  EP_CONT_UINT8_TENSOR = 4 /* UINT8 with one scale per tensor and offset 128 (same table):
+                              codes clamp(RNE(W/delta), -127, 127) + 128, delta = amax/127,
+                              stored for every row; weights are delta * (value - 128) */
 };
 
 /* Bits of *d_status set by the decode kernels (OR-ed; the caller zeroes it). */

@@ -31,7 +31,10 @@
  *     fp32(amax_r/57344) (FP8 e5m2) or fp32(amax_r/127) (INT8, symmetric),
  *     amax 0 gives delta 1, the quotient W/delta is formed in FP64 and rounded
  *     once into the container (the per-row FP8 scaling of Sec. 5.6's dtype
- *     table, read for both FP8 formats).
+ *     table, read for both FP8 formats); the UINT8 container of that table
+ *     takes one scale for the whole tensor, delta = fp32(amax/127), and codes
+ *     clamp(RNE(W/delta), -127, 127) + 128; its errors are measured with the
+ *     offset 128 removed.
  *   - per-row refinement (optional): candidate ratios are log-midpoints of
  *     the widest gaps of [0.70, 1.45] (the ends are not candidates);
  *     D_{r,k} uses the stored FP32 row scale in coded units; candidates join
@@ -59,8 +62,10 @@
 #define ORA_HEADER_BYTES 48u
 
 /* dtype codes (inputs: 1..3; outputs: 1..5, 100) */
-enum { O_BF16 = 1, O_FP16 = 2, O_FP32 = 3, O_FP8 = 4, O_INT8 = 5, O_FP8E5 = 6, O_COORD2 = 100 };
-enum { O_CONT_DIRECT = 0, O_CONT_FP8 = 1, O_CONT_INT8 = 2, O_CONT_FP8E5 = 3 };
+enum { O_BF16 = 1, O_FP16 = 2, O_FP32 = 3, O_FP8 = 4, O_INT8 = 5, O_FP8E5 = 6, O_UINT8 = 7,
+       O_COORD2 = 100 };
+enum { O_CONT_DIRECT = 0, O_CONT_FP8 = 1, O_CONT_INT8 = 2, O_CONT_FP8E5 = 3, O_CONT_UINT8 = 4 };
+#define UINT8_OFFSET 128.0
 enum { O_OK = 0, O_ERR_ARG = -1, O_ERR_FORMAT = -2, O_ERR_UNSUPPORTED = -3,
        O_ERR_NOMEM = -4, O_ERR_CORRUPT = -6 };
 
@@ -207,6 +212,11 @@ int ora_snap(const double* y, int64_t n, int dtype, void* out) {
       case O_FP32: ((float*)out)[i] = (float)v; break;
       case O_FP8: ((uint8_t*)out)[i] = e4m3_bits(snap_e4m3(v)); break;
       case O_FP8E5: ((uint8_t*)out)[i] = e5m2_bits(snap_e5m2(v)); break;
+      case O_UINT8: {
+        double r = nearbyint(v);
+        ((uint8_t*)out)[i] = (uint8_t)(r > 255 ? 255 : (r < 0 ? 0 : r));
+        break;
+      }
       case O_INT8: {
         double r = nearbyint(v);
         if (r > 127) r = 127;
@@ -520,6 +530,14 @@ static double input_value(const void* w, int dtype, int64_t i) {
  * error for non-finite input. */
 static int prepare_values(const void* w, int dtype, int64_t R, int64_t C, int container,
                           float* x, float* delta) {
+  double tmax = 0; /* whole-tensor amax (UINT8 container) */
+  if (container == O_CONT_UINT8) {
+    for (int64_t i = 0; i < R * C; i++) {
+      double v = (double)(float)input_value(w, dtype, i);
+      if (!isfinite(v)) return O_ERR_ARG;
+      if (fabs(v) > tmax) tmax = fabs(v);
+    }
+  }
   for (int64_t r = 0; r < R; r++) {
     double amax = 0;
     for (int64_t j = 0; j < C; j++) {
@@ -530,6 +548,7 @@ static int prepare_values(const void* w, int dtype, int64_t R, int64_t C, int co
     }
     if (container == O_CONT_DIRECT) continue;
     double qmax = container == O_CONT_FP8 ? 448.0 : container == O_CONT_FP8E5 ? 57344.0 : 127.0;
+    if (container == O_CONT_UINT8) amax = tmax;
     float d = amax > 0 ? (float)(amax / qmax) : 1.0f;
     delta[r] = d;
     for (int64_t j = 0; j < C; j++) {
@@ -543,6 +562,7 @@ static int prepare_values(const void* w, int dtype, int64_t R, int64_t C, int co
         cv = nearbyint(q);
         if (cv > 127) cv = 127;
         if (cv < -127) cv = -127;
+        if (container == O_CONT_UINT8) cv += UINT8_OFFSET;
       }
       x[r * C + j] = (float)cv;
     }
@@ -938,7 +958,7 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
   if (!w || !prm || !out_blob || !out_size || R <= 0 || C <= 0 || C % 8) return O_ERR_ARG;
   if (dtype != O_BF16 && dtype != O_FP16 && dtype != O_FP32) return O_ERR_ARG;
   if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0) return O_ERR_ARG;
-  if (prm->container < 0 || prm->container > 3) return O_ERR_ARG;
+  if (prm->container < 0 || prm->container > 4) return O_ERR_ARG;
   if (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) return O_ERR_ARG;
   if (prm->rdo_candidates > 64 || prm->rdo_sweeps < 0) return O_ERR_ARG;
   if ((R * C) / 8 > 0xFFFFFFFFll || R > 0xFFFFFFFFll || C > 0xFFFFFFFFll) return O_ERR_ARG;
@@ -1180,7 +1200,9 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
     /* statistics */
     double cce_full = tables_code_length(T, b);
     double err_c = 0, ref_c = 0, err_o = 0, ref_o = 0;
-    int rdt = cont == O_CONT_FP8 ? O_FP8 : cont == O_CONT_FP8E5 ? O_FP8E5 : cont == O_CONT_INT8 ? O_INT8 : dtype;
+    int rdt = cont == O_CONT_FP8 ? O_FP8 : cont == O_CONT_FP8E5 ? O_FP8E5 : cont == O_CONT_INT8 ? O_INT8
+              : cont == O_CONT_UINT8 ? O_UINT8 : dtype;
+    double off = cont == O_CONT_UINT8 ? UINT8_OFFSET : 0.0;
     for (int64_t r = 0; r < R; r++) {
       for (int64_t j = 0; j < C; j++) {
         double y = (double)(float)((double)sigma[r] * (two_p[r * C + j] / 2.0));
@@ -1196,13 +1218,19 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
             if (wh < -128) wh = -128;
             break;
           }
+          case O_UINT8: {
+            wh = nearbyint(y);
+            if (wh > 255) wh = 255;
+            if (wh < 0) wh = 0;
+            break;
+          }
           default: wh = y;
         }
         double xc = x[r * C + j];
         err_c += (wh - xc) * (wh - xc);
-        ref_c += xc * xc;
+        ref_c += (xc - off) * (xc - off);
         double wo = (double)(float)input_value(w, dtype, r * C + j);
-        double who = cont ? wh * (double)delta[r] : wh;
+        double who = cont ? (wh - off) * (double)delta[r] : wh;
         err_o += (who - wo) * (who - wo);
         ref_o += wo * wo;
       }
@@ -1320,7 +1348,7 @@ static int parse_blob(const uint8_t* blob, uint64_t n, blobview* bv, table_t* T)
   bv->n_words = get32(blob + 36);
   bv->total = get64(blob + 40);
   if (bv->total != n || bv->R == 0 || bv->C == 0 || bv->C % 8 || bv->b < 9 || bv->b > 15 ||
-      bv->V == 0 || bv->container > 3)
+      bv->V == 0 || bv->container > 4)
     return O_ERR_FORMAT;
   uint64_t nvec = (uint64_t)bv->R * bv->C / 8;
   if (bv->n_tiles != n_tiles_of(nvec, bv->V)) return O_ERR_FORMAT;
@@ -1412,6 +1440,11 @@ static void write_output(void* out, int dtype, uint64_t e, float y) {
     case O_FP32: ((float*)out)[e] = y; break;
     case O_FP8: ((uint8_t*)out)[e] = e4m3_bits(snap_e4m3(v)); break;
     case O_FP8E5: ((uint8_t*)out)[e] = e5m2_bits(snap_e5m2(v)); break;
+    case O_UINT8: {
+      double r = nearbyint(v);
+      ((uint8_t*)out)[e] = (uint8_t)(r > 255 ? 255 : (r < 0 ? 0 : r));
+      break;
+    }
     case O_INT8: {
       double r = nearbyint(v);
       if (r > 127) r = 127;
@@ -1439,7 +1472,7 @@ int ora_decode(const uint8_t* blob, uint64_t n, int out_dtype, void* out, float*
   int rc = parse_blob(blob, n, &bv, T);
   if (rc) goto out;
   if (out_dtype != O_BF16 && out_dtype != O_FP16 && out_dtype != O_FP32 && out_dtype != O_FP8 &&
-      out_dtype != O_FP8E5 && out_dtype != O_INT8 && out_dtype != O_COORD2) {
+      out_dtype != O_FP8E5 && out_dtype != O_UINT8 && out_dtype != O_INT8 && out_dtype != O_COORD2) {
     rc = O_ERR_ARG;
     goto out;
   }
@@ -1568,6 +1601,7 @@ int ora_values(const void* bits, int64_t n, int dtype, double* out) {
       case O_FP8: out[i] = e4m3_value(((const uint8_t*)bits)[i]); break;
       case O_FP8E5: out[i] = e5m2_value(((const uint8_t*)bits)[i]); break;
       case O_INT8: out[i] = ((const int8_t*)bits)[i]; break;
+      case O_UINT8: out[i] = ((const uint8_t*)bits)[i]; break;
       case O_COORD2: out[i] = ((const int32_t*)bits)[i] / 2.0; break;
       default: return O_ERR_ARG;
     }

@@ -16,16 +16,16 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
-BF16, FP16, FP32, FP8, INT8, FP8E5, COORD2 = 1, 2, 3, 4, 5, 6, 100
-CONT_DIRECT, CONT_FP8, CONT_INT8, CONT_FP8E5 = 0, 1, 2, 3
+BF16, FP16, FP32, FP8, INT8, FP8E5, UINT8, COORD2 = 1, 2, 3, 4, 5, 6, 7, 100
+CONT_DIRECT, CONT_FP8, CONT_INT8, CONT_FP8E5, CONT_UINT8 = 0, 1, 2, 3, 4
 OK, ERR_ARG, ERR_FORMAT, ERR_UNSUPPORTED, ERR_NOMEM, ERR_CORRUPT = 0, -1, -2, -3, -4, -6
 
 STATS = ["scale", "b", "rhat_sub", "r_stored", "bytes", "payload_bits", "cce_full", "n_tiles",
          "max_A", "erel_coded", "erel_orig", "mean_state_bits", "table_bytes", "sample_rows",
          "escalations", "coarsenings", "rdo_rows_moved", "rdo_budget_bytes", "rdo_lambda"]
 
-OUT_ITEMSIZE = {BF16: 2, FP16: 2, FP32: 4, FP8: 1, INT8: 1, FP8E5: 1, COORD2: 4}
-OUT_NPTYPE = {BF16: np.uint16, FP16: np.uint16, FP32: np.float32, FP8: np.uint8, INT8: np.int8, FP8E5: np.uint8,
+OUT_ITEMSIZE = {BF16: 2, FP16: 2, FP32: 4, FP8: 1, INT8: 1, FP8E5: 1, UINT8: 1, COORD2: 4}
+OUT_NPTYPE = {BF16: np.uint16, FP16: np.uint16, FP32: np.float32, FP8: np.uint8, INT8: np.int8, FP8E5: np.uint8, UINT8: np.uint8,
               COORD2: np.int32}
 
 

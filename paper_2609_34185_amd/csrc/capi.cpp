@@ -51,7 +51,7 @@ int blob_info(const void* host_blob, uint64_t n, ep_tensor_info* info) {
   if (I.total_bytes != n) return fail(EP_ERR_FORMAT, "ep_blob_info: size field differs from blob size");
   if (!I.rows || !I.cols || I.cols % 8) return fail(EP_ERR_FORMAT, "ep_blob_info: bad shape");
   if (I.prob_bits < 9 || I.prob_bits > 15) return fail(EP_ERR_FORMAT, "ep_blob_info: b outside 9..15");
-  if (!I.tile_vectors || I.container > 3) return fail(EP_ERR_FORMAT, "ep_blob_info: bad tile size or container");
+  if (!I.tile_vectors || I.container > 4) return fail(EP_ERR_FORMAT, "ep_blob_info: bad tile size or container");
   const uint64_t nvec = (uint64_t)I.rows * I.cols / 8;
   if (nvec > 0xFFFFFFFFull) return fail(EP_ERR_FORMAT, "ep_blob_info: tensor too large");
   if ((uint64_t)I.n_tiles != (nvec + I.tile_vectors - 1) / I.tile_vectors)

@@ -188,6 +188,14 @@ __device__ __forceinline__ uint32_t e5m2_quad(float a, float b, float c, float d
   return (uint32_t)w;
 }
 
+__device__ __forceinline__ uint32_t uint8_quad(float a, float b, float c, float d) {
+  const int ia = (int)__builtin_rintf(__builtin_amdgcn_fmed3f(a, 0.0f, 255.0f));
+  const int ib = (int)__builtin_rintf(__builtin_amdgcn_fmed3f(b, 0.0f, 255.0f));
+  const int ic = (int)__builtin_rintf(__builtin_amdgcn_fmed3f(c, 0.0f, 255.0f));
+  const int id = (int)__builtin_rintf(__builtin_amdgcn_fmed3f(d, 0.0f, 255.0f));
+  return (uint32_t)ia | ((uint32_t)ib << 8) | ((uint32_t)ic << 16) | ((uint32_t)id << 24);
+}
+
 __device__ __forceinline__ uint32_t int8_quad(float a, float b, float c, float d) {
   int ia = (int)__builtin_rintf(sat(a, 128.0f)), ib = (int)__builtin_rintf(sat(b, 128.0f));
   int ic = (int)__builtin_rintf(sat(c, 128.0f)), id = (int)__builtin_rintf(sat(d, 128.0f));
@@ -238,6 +246,9 @@ __device__ __forceinline__ void store_vec(void* out, uint32_t v, const int32_t* 
     gptr<u32x2>(out)[v] = o;
   } else if constexpr (DT == EP_INT8) {
     const u32x2 o = {int8_quad(y[0], y[1], y[2], y[3]), int8_quad(y[4], y[5], y[6], y[7])};
+    gptr<u32x2>(out)[v] = o;
+  } else if constexpr (DT == EP_UINT8) {
+    const u32x2 o = {uint8_quad(y[0], y[1], y[2], y[3]), uint8_quad(y[4], y[5], y[6], y[7])};
     gptr<u32x2>(out)[v] = o;
   } else {  // EP_COORD2_I32
     EP_GLOBAL u32x4* o = gptr<u32x4>(out) + 2ull * v;
@@ -307,6 +318,7 @@ __device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int
       else store_vec<EP_FP8_E5M2, false>(L.out, v, p2, half_sigma);
       break;
     case EP_INT8: store_vec<EP_INT8, false>(L.out, v, p2, half_sigma); break;
+    case EP_UINT8: store_vec<EP_UINT8, false>(L.out, v, p2, half_sigma); break;
     default: store_vec<EP_COORD2_I32, false>(L.out, v, p2, half_sigma); break;
   }
 }
@@ -1176,6 +1188,14 @@ __device__ __forceinline__ uint32_t int8_pair(float a, float b) {
   return r & 0xFFFFu;
 }
 
+// The same with saturation to [0, 255] (unsigned bytes).
+__device__ __forceinline__ uint32_t uint8_pair(float a, float b) {
+  const int ia = (int)__builtin_rintf(a), ib = (int)__builtin_rintf(b);
+  uint32_t r;
+  asm("v_ashr_pk_u8_i32 %0, %1, %2, 0" : "=v"(r) : "v"(ia), "v"(ib));
+  return r & 0xFFFFu;
+}
+
 // Fold field FIELD's entry e and weight y (computed in the step, see
 // field_step2) into the chain's accumulator; c is the coset bit.
 template <int DT, int FIELD, bool WIDE>
@@ -1211,6 +1231,9 @@ __device__ __forceinline__ void q_take(QAcc& a, uint32_t e, float y, uint32_t c)
     } else if constexpr (DT == EP_FP8_E5M2) {
       a.w[p / 2] = (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(
           y0, y1, (int)(p & 1 ? a.w[p / 2] : __float_as_uint(y0)), (p & 1) != 0);
+    } else if constexpr (DT == EP_UINT8) {
+      const uint32_t h = uint8_pair(y0, y1);
+      a.w[p / 2] = p & 1 ? (a.w[p / 2] | (h << 16)) : h;
     } else {  // EP_INT8
       const uint32_t h = int8_pair(y0, y1);
       a.w[p / 2] = p & 1 ? (a.w[p / 2] | (h << 16)) : h;
@@ -1223,7 +1246,7 @@ template <int DT>
 __device__ __forceinline__ void q_put(EP_GLOBAL uint8_t* base, uint32_t off, const QAcc& a) {
   if constexpr (DT == EP_BF16 || DT == EP_FP16) {
     *reinterpret_cast<EP_GLOBAL u32x4*>(base + off) = u32x4{a.w[0], a.w[1], a.w[2], a.w[3]};
-  } else if constexpr (DT == EP_FP8_E4M3 || DT == EP_FP8_E5M2 || DT == EP_INT8) {
+  } else if constexpr (DT == EP_FP8_E4M3 || DT == EP_FP8_E5M2 || DT == EP_INT8 || DT == EP_UINT8) {
     *reinterpret_cast<EP_GLOBAL u32x2*>(base + off) = u32x2{a.w[0], a.w[1]};
   } else {
     EP_GLOBAL u32x4* o = reinterpret_cast<EP_GLOBAL u32x4*>(base + off);
@@ -1235,7 +1258,7 @@ __device__ __forceinline__ void q_put(EP_GLOBAL uint8_t* base, uint32_t off, con
 // Bytes of one 8-weight vector in output type DT.
 template <int DT>
 constexpr uint32_t vec_bytes() {
-  return DT == EP_FP8_E4M3 || DT == EP_FP8_E5M2 || DT == EP_INT8 ? 8u
+  return DT == EP_FP8_E4M3 || DT == EP_FP8_E5M2 || DT == EP_INT8 || DT == EP_UINT8 ? 8u
          : (DT == EP_BF16 || DT == EP_FP16) ? 16u : 32u;
 }
 
@@ -1503,6 +1526,7 @@ __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_
       else lut_task_rows<B, EP_FP8_E5M2, false, WIDE>(L, lds, ring_area, t0, status);
       return true;
     case EP_INT8: lut_task_rows<B, EP_INT8, false, WIDE>(L, lds, ring_area, t0, status); return true;
+    case EP_UINT8: lut_task_rows<B, EP_UINT8, false, WIDE>(L, lds, ring_area, t0, status); return true;
     case EP_FP32: lut_task_rows<B, EP_FP32, false, WIDE>(L, lds, ring_area, t0, status); return true;
     case EP_COORD2_I32: lut_task_rows<B, EP_COORD2_I32, false, WIDE>(L, lds, ring_area, t0, status); return true;
     default: return false;
@@ -1537,6 +1561,9 @@ __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds,
       return true;
     case EP_INT8:
       decode_task_fast<PATH, B, EP_INT8, false>(L, lds, ring_area, task, status);
+      return true;
+    case EP_UINT8:
+      decode_task_fast<PATH, B, EP_UINT8, false>(L, lds, ring_area, task, status);
       return true;
     case EP_FP32:
       decode_task_fast<PATH, B, EP_FP32, false>(L, lds, ring_area, task, status);
@@ -1763,7 +1790,7 @@ float dtype_max(int dt) {
 
 bool valid_out_dtype(int dt) {
   return dt == EP_BF16 || dt == EP_FP16 || dt == EP_FP32 || dt == EP_FP8_E4M3 || dt == EP_FP8_E5M2 ||
-         dt == EP_INT8 || dt == EP_COORD2_I32;
+         dt == EP_INT8 || dt == EP_UINT8 || dt == EP_COORD2_I32;
 }
 
 int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void* d_out,

@@ -291,6 +291,7 @@ struct CpuBackend {
     delta.assign((size_t)R, 0.0f);
     mu.resize((size_t)R);
     std::vector<char> bad((size_t)R, 0);
+    std::vector<double> am((size_t)R, 0.0);
     parallel_for(R, T, [&](int64_t b, int64_t e, int) {
       for (int64_t r = b; r < e; r++) {
         double amax = 0;
@@ -301,6 +302,15 @@ struct CpuBackend {
           xr[j] = v;
           amax = std::max(amax, std::fabs((double)v));
         }
+        am[r] = amax;
+      }
+    });
+    double tmax = 0;   // one scale for the whole tensor (unsigned container)
+    for (double a : am) tmax = std::max(tmax, a);
+    parallel_for(R, T, [&](int64_t b, int64_t e, int) {
+      for (int64_t r = b; r < e; r++) {
+        const double amax = cont == EP_CONT_UINT8_TENSOR ? tmax : am[r];
+        float* xr = x.data() + r * C;
         if (cont) {
           float d = amax > 0 ? (float)(amax / em::container_max(cont)) : 1.0f;
           delta[r] = d;
@@ -549,10 +559,11 @@ struct CpuBackend {
             double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
             double v = em::snap_out(rdt, y);
             double xc = x[r * C + 8 * jv + j];
+            const double off = em::container_offset(cont);
             ec += (v - xc) * (v - xc);
-            rc += xc * xc;
+            rc += (xc - off) * (xc - off);
             double wo = (double)(float)input_at(w, dt, r * C + 8 * jv + j);
-            double vo = cont ? v * (double)delta[r] : v;
+            double vo = cont ? (v - off) * (double)delta[r] : v;
             eo += (vo - wo) * (vo - wo);
             ro += wo * wo;
           }
@@ -876,7 +887,7 @@ int check_args(const void* w, int w_dtype, int64_t R, int64_t C, const ep_encode
   if (w_dtype != EP_BF16 && w_dtype != EP_FP16 && w_dtype != EP_FP32)
     return fail(EP_ERR_ARG, "ep_encode: input dtype must be BF16, FP16 or FP32");
   if (!(prm->target_bpp > 0) || prm->tile_vectors < 1 || prm->search_steps < 0 ||
-      prm->container < 0 || prm->container > 3 || !(prm->scale_lo > 0) ||
+      prm->container < 0 || prm->container > 4 || !(prm->scale_lo > 0) ||
       !(prm->scale_hi > prm->scale_lo) || prm->sample_vectors < 1 ||
       (prm->prob_bits && (prm->prob_bits < 9 || prm->prob_bits > 15)) ||
       prm->rdo_candidates > 64 || prm->rdo_sweeps < 0)

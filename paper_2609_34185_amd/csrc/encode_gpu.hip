@@ -47,8 +47,11 @@ __device__ __forceinline__ float load_input(const void* w, int dt, int64_t i) {
 }
 
 // One workgroup per row: input -> coded values (container route), delta_r.
+// The unsigned container scales the whole tensor at once: its first pass
+// (tmax < 0) only writes each row's amax into delta, the second quantises
+// with tmax, the largest of them.
 __global__ __launch_bounds__(256) void k_prep_rows(const void* w, int dt, int64_t C, int cont,
-                                                   float* x, float* delta, int* bad) {
+                                                   double tmax, float* x, float* delta, int* bad) {
   __shared__ double s_amax[256];
   __shared__ int s_bad;
   const int64_t r = blockIdx.x, base = r * C;
@@ -74,6 +77,13 @@ __global__ __launch_bounds__(256) void k_prep_rows(const void* w, int dt, int64_
   if (t == 0 && s_bad) atomicOr(bad, 1);
   if (!cont) return;
   amax = s_amax[0];
+  if (cont == EP_CONT_UINT8_TENSOR) {
+    if (tmax < 0) {
+      if (t == 0) delta[r] = (float)amax;   // exact: amax is an FP32 value
+      return;
+    }
+    amax = tmax;
+  }
   const float d = amax > 0 ? (float)(amax / em::container_max(cont)) : 1.0f;
   if (t == 0) delta[r] = d;
   for (int64_t j = t; j < C; j += 256) {
@@ -322,10 +332,11 @@ __global__ __launch_bounds__(256) void k_errors(const void* w, int dt, const flo
       const double y = (double)(float)((double)sigma[r] * (two[j] / 2.0));
       const double v = em::snap_out(rdt, y);
       const double xc = x[r * C + 8 * jv + j];
+      const double off = em::container_offset(cont);
       ec += (v - xc) * (v - xc);
-      rc += xc * xc;
+      rc += (xc - off) * (xc - off);
       const double wo = (double)load_input(w, dt, r * C + 8 * jv + j);
-      const double vo = cont ? v * (double)delta[r] : v;
+      const double vo = cont ? (v - off) * (double)delta[r] : v;
       eo += (vo - wo) * (vo - wo);
       ro += wo * wo;
     }
@@ -574,8 +585,18 @@ int prep(Ctx* c, float* delta, double* mu) {
   EP_GTRY(c->to_dev(c->bad, &zero, sizeof(int), "ep_encode_gpu: copy"));
   if (hipMemsetAsync(c->delta, 0, 4 * (size_t)c->R, c->st) != hipSuccess)
     return fail(EP_ERR_HIP, "ep_encode_gpu: clear");
+  double tmax = -1.0;
+  if (c->cont == EP_CONT_UINT8_TENSOR) {
+    hipLaunchKernelGGL(k_prep_rows, dim3((unsigned)c->R), dim3(256), 0, c->st, c->w, c->dt, c->C,
+                       c->cont, -1.0, c->x, c->delta, c->bad);
+    EP_LAUNCHED("ep_encode_gpu: launch (row amax)");
+    std::vector<float> am((size_t)c->R);
+    EP_GTRY(c->to_host(am.data(), c->delta, 4 * (uint64_t)c->R, "ep_encode_gpu: prep"));
+    tmax = 0.0;
+    for (float a : am) tmax = a > tmax ? (double)a : tmax;
+  }
   hipLaunchKernelGGL(k_prep_rows, dim3((unsigned)c->R), dim3(256), 0, c->st, c->w, c->dt, c->C,
-                     c->cont, c->x, c->delta, c->bad);
+                     c->cont, tmax, c->x, c->delta, c->bad);
   EP_LAUNCHED("ep_encode_gpu: launch (prep)");
   hipLaunchKernelGGL(k_prep_mu, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
                      c->x, c->R, c->C, c->mu);

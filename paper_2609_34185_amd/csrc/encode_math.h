@@ -44,12 +44,14 @@ EP_HD inline double container_snap(int cont, double q) {
   if (cont == EP_CONT_FP8_ROW) return to_e4m3(q);
   if (cont == EP_CONT_FP8E5M2_ROW) return to_e5m2(q);
   const double r = std::nearbyint(q);
-  return r > 127.0 ? 127.0 : (r < -127.0 ? -127.0 : r);
+  return (r > 127.0 ? 127.0 : (r < -127.0 ? -127.0 : r)) + (cont == EP_CONT_UINT8_TENSOR ? 128.0 : 0.0);
 }
+// Offset of a container's values (the unsigned container's 128; 0 otherwise).
+EP_HD inline double container_offset(int cont) { return cont == EP_CONT_UINT8_TENSOR ? 128.0 : 0.0; }
 // Output type in which a container's values are reconstructed.
 EP_HD inline int container_dtype(int cont, int direct) {
   return cont == EP_CONT_FP8_ROW ? EP_FP8_E4M3 : cont == EP_CONT_FP8E5M2_ROW ? EP_FP8_E5M2
-         : cont == EP_CONT_INT8_ROW ? EP_INT8 : direct;
+         : cont == EP_CONT_INT8_ROW ? EP_INT8 : cont == EP_CONT_UINT8_TENSOR ? EP_UINT8 : direct;
 }
 EP_HD inline double to_bf16(double v) { return round_to_format(v, 7, -126, 3.3895313892515355e38); }
 EP_HD inline double to_fp16(double v) { return round_to_format(v, 10, -14, 65504.0); }
@@ -61,6 +63,10 @@ EP_HD inline double int8_snap(double v) {
 
 // y snapped to output type dt (FP32 and others: y itself).
 EP_HD inline double snap_out(int dt, double y) {
+  if (dt == EP_UINT8) {
+    const double r = std::nearbyint(y);
+    return r > 255 ? 255 : (r < 0 ? 0 : r);
+  }
   return dt == EP_BF16 ? to_bf16(y) : dt == EP_FP16 ? to_fp16(y) : dt == EP_FP8_E4M3 ? to_e4m3(y)
          : dt == EP_FP8_E5M2 ? to_e5m2(y) : dt == EP_INT8 ? int8_snap(y) : y;
 }

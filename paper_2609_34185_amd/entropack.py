@@ -18,11 +18,11 @@ LIB_PATH = os.path.join(HERE, "libentropack.so")
 
 # ---- constants (mirror include/entropack.h) -------------------------------------
 OK, ERR_ARG, ERR_FORMAT, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP, ERR_CORRUPT = 0, -1, -2, -3, -4, -5, -6
-BF16, FP16, FP32, FP8_E4M3, INT8, FP8_E5M2, COORD2_I32 = 1, 2, 3, 4, 5, 6, 100
-CONT_DIRECT, CONT_FP8_ROW, CONT_INT8_ROW, CONT_FP8E5M2_ROW = 0, 1, 2, 3
+BF16, FP16, FP32, FP8_E4M3, INT8, FP8_E5M2, UINT8, COORD2_I32 = 1, 2, 3, 4, 5, 6, 7, 100
+CONT_DIRECT, CONT_FP8_ROW, CONT_INT8_ROW, CONT_FP8E5M2_ROW, CONT_UINT8_TENSOR = 0, 1, 2, 3, 4
 STATUS_PAYLOAD_OVERRUN, STATUS_BAD_FINAL_STATE, STATUS_BAD_END_OFFSET = 1, 2, 4
 
-ITEMSIZE = {BF16: 2, FP16: 2, FP32: 4, FP8_E4M3: 1, INT8: 1, FP8_E5M2: 1, COORD2_I32: 4}
+ITEMSIZE = {BF16: 2, FP16: 2, FP32: 4, FP8_E4M3: 1, INT8: 1, FP8_E5M2: 1, UINT8: 1, COORD2_I32: 4}
 
 
 class EncodeParams(C.Structure):
@@ -249,7 +249,7 @@ TORCH_DTYPE = {}
 def torch_dtype(code: int):
     t = _torch()
     return {BF16: t.bfloat16, FP16: t.float16, FP32: t.float32, FP8_E4M3: t.float8_e4m3fn,
-            INT8: t.int8, FP8_E5M2: t.float8_e5m2, COORD2_I32: t.int32}[code]
+            INT8: t.int8, FP8_E5M2: t.float8_e5m2, UINT8: t.uint8, COORD2_I32: t.int32}[code]
 
 
 def to_device(blob: np.ndarray, device="cuda"):

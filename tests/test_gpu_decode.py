@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-DTYPES = ["COORD2", "BF16", "FP16", "FP32", "FP8", "INT8", "E5M2"]
+DTYPES = ["COORD2", "BF16", "FP16", "FP32", "FP8", "INT8", "E5M2", "UINT8"]
 
 
 def say(*a):
@@ -36,7 +36,7 @@ def codes(E, oracle, name):
     return {"COORD2": (E.COORD2_I32, oracle.COORD2), "BF16": (E.BF16, oracle.BF16),
             "FP16": (E.FP16, oracle.FP16), "FP32": (E.FP32, oracle.FP32),
             "FP8": (E.FP8_E4M3, oracle.FP8), "INT8": (E.INT8, oracle.INT8),
-            "E5M2": (E.FP8_E5M2, oracle.FP8E5)}[name]
+            "E5M2": (E.FP8_E5M2, oracle.FP8E5), "UINT8": (E.UINT8, oracle.UINT8)}[name]
 
 
 def gpu_bits(t):
@@ -208,11 +208,14 @@ def test_saturation(E, oracle):
     ((37, 136), 4.0, dict(tile_vectors=45)),          # ragged tiles: the generic loop
     ((64, 8 * 600), 6.0, dict(prob_bits=12)),         # the bucketed-search path
 ])
-def test_fp8_e5m2_container(E, oracle, shape, target, kw):
-    """The FP8 e5m2 row container (the paper's dtype table) decoded to e5m2 with its row scales."""
+def test_fp8_e5m2_and_uint8_containers(E, oracle, shape, target, kw):
+    """The FP8 e5m2 row container and the UINT8 tensor container (the paper's dtype table),
+    decoded to their types with their scales."""
     w = W.ragged_tensor(31, *shape, scale=0.05)
     blob, _ = oracle.encode(w, target, container=oracle.CONT_FP8E5, **kw)
     check_blob(E, oracle, blob, dtypes=["E5M2", "COORD2", "FP32"], tag="e5m2 container")
+    blob, _ = oracle.encode(w, target, container=oracle.CONT_UINT8, **kw)
+    check_blob(E, oracle, blob, dtypes=["UINT8", "COORD2"], tag="uint8 container")
 
 
 def test_corrupt_payload_sets_status_without_fault(E, oracle):

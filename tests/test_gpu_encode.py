@@ -64,6 +64,7 @@ CASES = [
     ("fp8_container", lambda: W.ragged_tensor(3, 128, 512, scale=0.05), 4.0, dict(container=1)),
     ("int8_container", lambda: W.ragged_tensor(4, 128, 512, scale=0.05), 6.0, dict(container=2)),
     ("fp8e5m2_container", lambda: W.ragged_tensor(23, 96, 512, scale=0.05), 4.0, dict(container=3)),
+    ("uint8_container", lambda: W.ragged_tensor(24, 80, 520, scale=0.05), 4.0, dict(container=4)),
     ("high_rate", lambda: W.ragged_tensor(5, 64, 1024), 9.0, {}),
     ("b9", lambda: W.ragged_tensor(6, 64, 256), 2.0, dict(prob_bits=9)),
     ("literal_credit", lambda: W.ragged_tensor(7, 96, 512), 3.0, dict(state_credit_bits=16.0)),

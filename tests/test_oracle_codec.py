@@ -312,6 +312,32 @@ def test_e5m2_container_route(oracle):
     assert np.array_equal(out, oracle.snap(y.ravel(), oracle.FP8E5).reshape(out.shape))
 
 
+def test_uint8_snap_and_container_route(oracle):
+    """UINT8 output is clamp(RNE(y), 0, 255).  The unsigned container of the dtype table takes
+    one scale for the tensor, delta = fp32(amax / 127), codes clamp(RNE(W / delta), -127, 127)
+    + 128, and measures its error with the offset removed."""
+    y = np.array([-3.0, -0.5, 0.5, 1.5, 2.5, 127.5, 254.5, 255.4, 255.6, 300.0])
+    assert oracle.snap(y, oracle.UINT8).tolist() == [0, 0, 0, 2, 2, 128, 254, 255, 255, 255]
+    w = W.ragged_tensor(9, 48, 256, scale=0.05)
+    blob, st = oracle.encode(w, 4.0, container=oracle.CONT_UINT8)
+    tp, xv, _ = oracle.quantize(w, st["scale"], container=oracle.CONT_UINT8)
+    wf = W.bf16_bits_to_f32(w).astype(np.float64)
+    delta = np.float32(np.abs(wf).max() / 127.0)
+    assert np.array_equal(xv, np.clip(np.rint(wf / np.float64(delta)), -127, 127) + 128)
+    out, dq = oracle.decode(blob, oracle.UINT8)
+    assert np.all(dq == delta)
+    two_p, _ = oracle.decode(blob, oracle.COORD2)
+    assert np.array_equal(two_p, tp)
+    h = oracle.header(blob)
+    off = 48 + h["table_bytes"]
+    sig = np.frombuffer(blob[off:off + 4 * h["rows"]].tobytes(), dtype=np.float32).astype(np.float64)
+    yv = (sig[:, None] * (two_p / 2.0)).astype(np.float32).astype(np.float64)
+    assert np.array_equal(out, np.clip(np.rint(yv), 0, 255).astype(np.uint8))
+    e = out.astype(np.float64) - xv
+    assert st["erel_coded"] == pytest.approx(np.sqrt((e ** 2).sum() / ((xv - 128.0) ** 2).sum()), rel=1e-9)
+    assert 0.02 < st["erel_coded"] < 0.3
+
+
 def test_high_resolution_rate_law_loosely(oracle):
     """Sanity only (parity unpinned for E_rel on synthetic data): at high rate the error of a
     unit-Gaussian source falls by about 2x per extra bit per weight [eq. high_resolution]."""
