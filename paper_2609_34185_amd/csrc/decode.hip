@@ -327,6 +327,12 @@ __device__ __forceinline__ void store_vector(const Hot& L, uint32_t v, const int
 // Prefix sums of the 16 field tables' frequencies: put(t, s, F_s, f_s) for every
 // symbol s of table t, and end(t, M) once per table with the total (= 2^b).
 // Wave w scans table w (and w + kWavesPerGroup ... when fewer waves exist).
+// The frequencies of up to kScanAhead chunks of 64 symbols are requested
+// together before any of them is scanned, so a table of a few hundred symbols
+// waits for memory once rather than once per chunk (every workgroup builds its
+// tables at the same moment, when loads are slowest).  Lanes past the end read
+// the table's last entry (in bounds) and use 0.
+constexpr int kScanAhead = 4;
 template <class Put, class End>
 __device__ __forceinline__ void scan_tables(const LayerDev& L, Put put, End end) {
   const int lane = threadIdx.x & 63, wave = (int)wave_id();
@@ -334,17 +340,28 @@ __device__ __forceinline__ void scan_tables(const LayerDev& L, Put put, End end)
     const EP_GLOBAL uint16_t* f = gptr<const uint16_t>(L.blob + L.tab_off[t]);
     const uint32_t A = L.tab_A[t];
     uint32_t running = 0;
-    for (uint32_t s0 = 0; s0 < A; s0 += kWaveSize) {
-      uint32_t s = s0 + lane;
-      uint32_t fs = s < A ? f[s] : 0u;
-      uint32_t incl = fs;
+    for (uint32_t g0 = 0; g0 < A; g0 += kScanAhead * kWaveSize) {
+      uint32_t fa[kScanAhead];
 #pragma unroll
-      for (int d = 1; d < kWaveSize; d <<= 1) {
-        uint32_t o = __shfl_up(incl, d, kWaveSize);
-        if (lane >= d) incl += o;
+      for (int k = 0; k < kScanAhead; k++) {
+        const uint32_t s = g0 + k * kWaveSize + lane;
+        const uint32_t v = f[s < A ? s : A - 1];
+        fa[k] = s < A ? v : 0u;
       }
-      if (s < A) put(t, s, running + incl - fs, fs);
-      running += __shfl(incl, kWaveSize - 1, kWaveSize);
+#pragma unroll
+      for (int k = 0; k < kScanAhead; k++) {
+        const uint32_t s0 = g0 + k * kWaveSize;
+        if (s0 >= A) break;
+        const uint32_t s = s0 + lane, fs = fa[k];
+        uint32_t incl = fs;
+#pragma unroll
+        for (int d = 1; d < kWaveSize; d <<= 1) {
+          uint32_t o = __shfl_up(incl, d, kWaveSize);
+          if (lane >= d) incl += o;
+        }
+        if (s < A) put(t, s, running + incl - fs, fs);
+        running += __shfl(incl, kWaveSize - 1, kWaveSize);
+      }
     }
     if (lane == 0) end(t, running);
   }
