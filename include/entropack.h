@@ -79,7 +79,7 @@ enum ep_container {
   EP_CONT_DIRECT = 0,      /* the input values are coded directly */
   EP_CONT_FP8_ROW = 1,     /* row-scaled FP8 e4m3fn container (Appendix A.6, B.1) */
   EP_CONT_INT8_ROW = 2,    /* row-scaled symmetric INT8 container (Appendix B.1) */
-  EP_CONT_FP8E5M2_ROW = 3, /* row-scaled FP8 e5m2 container (the dtype table of Sec. 5.6) */
+  EP_CONT_FP8E5M2_ROW = 3, /* row-scaled FP8 e5m2 container (the dtype table of App. A.6) */
   EP_CONT_UINT8_TENSOR = 4 /* UINT8 with one scale per tensor and offset 128 (same table):
                               codes clamp(RNE(W/delta), -127, 127) + 128, delta = amax/127,
                               stored for every row; weights are delta * (value - 128) */

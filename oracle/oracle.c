@@ -30,7 +30,7 @@
  *   - container routes: delta_r = fp32(amax_r/448) (FP8 e4m3fn),
  *     fp32(amax_r/57344) (FP8 e5m2) or fp32(amax_r/127) (INT8, symmetric),
  *     amax 0 gives delta 1, the quotient W/delta is formed in FP64 and rounded
- *     once into the container (the per-row FP8 scaling of Sec. 5.6's dtype
+ *     once into the container (the per-row FP8 scaling of App. A.6's dtype
  *     table, read for both FP8 formats); the UINT8 container of that table
  *     takes one scale for the whole tensor, delta = fp32(amax/127), and codes
  *     clamp(RNE(W/delta), -127, 127) + 128; its errors are measured with the

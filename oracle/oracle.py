@@ -296,7 +296,7 @@ def _table_bits(values: np.ndarray, b: int):
 
 def coding_ablation(blob: np.ndarray) -> dict:
     """Stored bits of a blob's own lattice points under the three coding models of the
-    entropy-model ablation (App. D.2, Table coding; eqs. cond, parity, conditioning_gain):
+    entropy-model ablation (App. A.3, Table coding; eqs. cond, parity, conditioning_gain):
       'entropack': coset table + one table per (field, coset), fields (c, z1..z7, m);
       'pooled':    coset table + one table per field for both cosets (no conditioning);
       'direct_z8': as 'entropack' with z8 = 2m + pi coded in place of m (no parity reduction).

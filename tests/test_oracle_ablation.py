@@ -1,4 +1,4 @@
-"""CPU pins of the coding ablation (App. D.2, Table coding; eqs. cond, parity,
+"""CPU pins of the coding ablation (App. A.3, Table coding; eqs. cond, parity,
 conditioning_gain): the same lattice points coded with 17 coset-conditioned
 tables (the method), 9 pooled tables, or z8 in place of m.
 
