@@ -284,7 +284,8 @@ int ep_stack_decode(const ep_stack* stack, int32_t* d_status, void* hip_stream);
  * accumulation: the product of decoded INT8 weights (B) with INT8
  * activations, as in the compressed-storage INT8 route of the paper's
  * Appendix B.1.  All pointers are device memory owned by the caller; A and B
- * 16-byte aligned.  Requires M, N > 0, K > 0, K % 16 == 0 and K <= 2^24.
+ * 16-byte aligned.  Requires M, N > 0, K > 0, K % 16 == 0 and K <= 131071 (each
+ * product is at most 2^14 in magnitude, so every int32 sum is exact).
  * Asynchronous on hip_stream.  Errors: EP_ERR_ARG, EP_ERR_HIP. */
 int ep_gemm_i8_nt(const int8_t* d_a, const int8_t* d_b, int32_t* d_y, int64_t m, int64_t n,
                   int64_t k, void* hip_stream);

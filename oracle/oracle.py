@@ -14,7 +14,8 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "oracle.c")
-LIB = os.path.join(HERE, "liboracle.so")
+# ORACLE_LIB names another build of the same source (the sanitizer run of the CPU pins)
+LIB = os.environ.get("ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 
 BF16, FP16, FP32, FP8, INT8, FP8E5, UINT8, COORD2 = 1, 2, 3, 4, 5, 6, 7, 100
 CONT_DIRECT, CONT_FP8, CONT_INT8, CONT_FP8E5, CONT_UINT8 = 0, 1, 2, 3, 4
@@ -46,6 +47,8 @@ def params(target_bpp, tile_vectors=512, prob_bits=0, search_steps=12, container
 
 
 def build(force: bool = True) -> str:
+    if os.environ.get("ORACLE_LIB"):
+        return LIB
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-shared", "-fPIC", SRC,

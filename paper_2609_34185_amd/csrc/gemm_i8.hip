@@ -299,8 +299,9 @@ extern "C" int ep_gemm_i8_nt(const int8_t* d_a, const int8_t* d_b, int32_t* d_y,
     return ep::fail(EP_ERR_ARG, "ep_gemm_i8_nt: need m, n, k > 0 and k % 16 == 0");
   if ((reinterpret_cast<uintptr_t>(d_a) | reinterpret_cast<uintptr_t>(d_b)) & 15)
     return ep::fail(EP_ERR_ARG, "ep_gemm_i8_nt: operands must be 16-byte aligned");
-  if (k > (int64_t(1) << 24))
-    return ep::fail(EP_ERR_ARG, "ep_gemm_i8_nt: k above 2^24 may overflow int32 sums");
+  // |a * b| <= 128 * 128 = 2^14, so a K-term sum stays below 2^31 for K <= 131071
+  if (k > 131071)
+    return ep::fail(EP_ERR_ARG, "ep_gemm_i8_nt: k above 131071 may overflow the int32 sums");
   if (m * k >= (int64_t)ep::kOutside || n * k >= (int64_t)ep::kOutside)
     return ep::fail(EP_ERR_ARG, "ep_gemm_i8_nt: an operand above 2^31 bytes");
   int dev = 0, cus = 0;

@@ -146,3 +146,17 @@ def test_blob_info_refuses_malformed(E, oracle):
     b = blob.copy()   # non-finite row scale
     b[info.off_sigma: info.off_sigma + 4].view(np.float32)[0] = np.inf
     assert refused(b)
+
+
+def test_gemm_rejects_sums_that_could_overflow_int32(E):
+    """|a * b| <= 2^14 for int8 operands, so K-term sums are exact in int32 only for
+    K <= 131071; longer K, misaligned operands and bad shapes are refused on the host,
+    before any device call (the pointers below are never dereferenced)."""
+    a, b, y = 1 << 20, 2 << 20, 3 << 20
+    for m, n, k in [(16, 16, 131072), (16, 16, 1 << 24), (16, 16, 24), (0, 16, 64), (16, 16, 0)]:
+        with pytest.raises(E.EntroPackError) as ei:
+            E.gemm_i8_nt(a, b, y, m, n, k)
+        assert ei.value.code == E.ERR_ARG
+    with pytest.raises(E.EntroPackError) as ei:
+        E.gemm_i8_nt(a + 8, b, y, 16, 16, 64)
+    assert ei.value.code == E.ERR_ARG
