@@ -175,7 +175,12 @@ typedef struct {
   int32_t coord2_min;        /* smallest doubled coordinate value any table can produce */
   int32_t coord2_max;        /* largest one */
   float max_abs_weight;      /* upper bound of |fp32(sigma_r * p)| over the tensor */
-  uint32_t path;             /* decode kernel family chosen for this tensor (internal) */
+  uint32_t path;             /* decode kernel family chosen for this tensor: 1 narrow slot
+                                table, 3 wide slot table, 2 bucketed search (all in LDS), 4
+                                global tables (frequencies read from the blob in global
+                                memory, App. C.3), the first that holds the tables; every
+                                valid blob has one.  A caller may name another path that
+                                holds the tables (any such path decodes the same bits). */
   uint32_t sum_alphabet;     /* sum of the field tables' index ranges */
   uint32_t table_off[16];    /* byte offset of field table 1 + 8c + (i-1) in the blob */
   int32_t table_min[16];     /* its min value */
@@ -199,8 +204,8 @@ int ep_blob_info(const void* host_blob, uint64_t n, ep_tensor_info* info);
  * whose first vector lies in a decoded tile.  d_status (nullable, device
  * int32, zeroed by the caller) receives ep_status_bits for corrupt streams;
  * the kernels never read or write outside the blob's tile windows and the
- * output.  Errors (host side, before launch): EP_ERR_ARG, EP_ERR_UNSUPPORTED,
- * EP_ERR_HIP. */
+ * output.  Errors (host side, before launch): EP_ERR_ARG (also for an info whose
+ * path cannot hold the tensor's tables), EP_ERR_UNSUPPORTED, EP_ERR_HIP. */
 int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtype, void* d_out,
                     float* d_dequant, uint32_t tile_begin, uint32_t tile_end, int32_t* d_status,
                     void* hip_stream);
@@ -243,8 +248,9 @@ uint64_t ep_decode_layers_workspace(int n);
  * ep_decode_layers_workspace(n) bytes, device memory owned by the caller) by
  * one hipMemcpyAsync on the same stream, which has read the host list by the
  * time it returns; d_workspace must stay untouched until the launch completes.
- * All layers must select the same decode path (ep_tensor_info.path).  The
- * layers array is host memory and is not retained.  Errors: as
+ * Layers may take different decode paths (ep_tensor_info.path): each
+ * workgroup builds the tables of the layer it works on in that layer's form.
+ * The layers array is host memory and is not retained.  Errors: as
  * ep_decode_tiles, and EP_ERR_ARG for a missing or short workspace. */
 int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      int32_t* d_status, void* hip_stream);
@@ -256,7 +262,7 @@ int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t 
 typedef struct {
   void* d_workspace;         /* device descriptor list (caller-owned memory) */
   int32_t n_layers;
-  uint32_t path;             /* decode path shared by all layers */
+  uint32_t path;             /* decode path shared by all layers, or 15 for a list of several */
   uint32_t total_tasks;      /* 4-tile tasks over all layers */
   uint32_t lds_bytes;        /* LDS of the launch */
   uint32_t reserved[4];

@@ -24,7 +24,9 @@
 //               f - 1 (bits 0-10), u - F (bits 11-21) and z as a signed
 //               10-bit field (bits 22-31); one more add per symbol;
 //   kPathSearch per-symbol cumulative table (F | f << 16) searched with a
-//               fixed-trip binary search -- any b, alphabets up to the LDS size.
+//               fixed-trip binary search -- any b, alphabets up to the LDS size;
+//   kPathGlobal every G-th cumulative value in LDS, the frequencies themselves
+//               read from the blob in global memory -- any valid table.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -86,6 +88,8 @@ struct LayerDev {
   uint32_t tab_base[16];          // prefix of tab_A (search path)
   const int8_t* x;                // fused product: X (m x cols, row-major), Y in `out`
   uint32_t m;
+  uint32_t path;                  // decode path of the layer (DecodePath)
+  uint32_t g_bits, g_meta;        // global-table path: log2 G, byte offset of its metadata
 };
 
 // The scalars the decode loop needs, read once per layer segment and forced
@@ -102,6 +106,8 @@ struct Hot {
   uint32_t off_sigma, off_delta, off_states, off_offsets, off_payload;
   const int8_t* x;
   uint32_t m, cols;
+  uint32_t g_bits, g_meta;        // global-table path: log2 G, u32 index of the metadata
+  uint32_t tab_bytes;             // end of the tables section (bounds of their loads)
 };
 
 __device__ __forceinline__ uint32_t uni(uint32_t v) {
@@ -148,6 +154,9 @@ __device__ __forceinline__ Hot make_hot(const LayerDev& L) {
   H.x = uni_ptr(L.x);
   H.m = uni(L.m);
   H.cols = uni(L.cols);
+  H.g_bits = uni(L.g_bits);
+  H.g_meta = uni(L.g_meta / 4);
+  H.tab_bytes = uni((uint32_t)L.off_sigma);
   return H;
 }
 
@@ -575,6 +584,44 @@ __device__ __forceinline__ void decode_field(const Hot& L, const uint32_t* lds, 
     const uint32_t g = x >> B;
     x = __umul24(e & 0x7FFu, g) + g + ((e >> 11) & 0x7FFu);   // (f - 1) g + g + (u - F)
     dval = 2 * ((int32_t)e >> 22) + (int32_t)c;
+  } else if (PATH == kPathGlobal) {
+    // Coarse search: C_j = F_{jG} of table t in LDS (C_0 = 0 <= u), the largest j
+    // with C_j <= u, then a scan of the block's frequencies f_{jG} .. f_{jG+G-1},
+    // two per dword, from the blob's table in global memory.  The block holds the
+    // symbol (its successor's C exceeds u, or it is the last block, whose
+    // frequencies run up to 2^b), so the scan ends inside it.
+    const uint16_t* cum = reinterpret_cast<const uint16_t*>(lds);
+    const uint32_t u = x & ((1u << L.b) - 1);
+    const uint32_t t = 8 * c + (uint32_t)(field - 1);
+    const uint32_t base = lds[L.g_meta + t], n = lds[L.g_meta + 32 + t];
+    uint32_t lo = 0, hi = n ? n - 1 : 0;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) >> 1;
+      if (cum[base + mid] <= u) lo = mid;
+      else hi = mid - 1;
+    }
+    uint32_t F = cum[base + lo], s = lo << L.g_bits, f = 0;
+    const __amdgpu_buffer_rsrc_t trsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(L.blob), (short)0, (int)L.tab_bytes, 0x00020000);
+    const uint32_t off = lds[L.g_meta + 48 + t] + 2 * s;
+    for (uint32_t k = 0; k < (1u << L.g_bits); k += 2) {
+      const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(trsrc, off + 2 * k, 0, 0);
+      const uint32_t f0 = w & 0xFFFFu, f1 = w >> 16;
+      if (u < F + f0) {
+        f = f0;
+        s += k;
+        break;
+      }
+      F += f0;
+      if (u < F + f1) {
+        f = f1;
+        s += k + 1;
+        break;
+      }
+      F += f1;
+    }
+    x = __umul24(f, x >> L.b) + u - F;
+    dval = doubled_value((int32_t)s + (int32_t)lds[L.g_meta + 16 + t], field, c);
   } else {
     // Bucketed search: the bucket j of u (its top k bits) bounds the symbol to
     // [bk[j], bk[j + 1]]; a binary search on the u16 cumulative table narrows
@@ -1597,6 +1644,7 @@ __device__ __forceinline__ bool decode_task_fast_any(const Hot& L, uint8_t* lds,
 // after the search tables (search path).
 template <int PATH>
 __device__ __forceinline__ uint32_t ring_offset(const LayerDev& L) {
+  if (PATH == kPathGlobal) return (L.g_meta + 4 * 64 + 511) & ~511u;   // GlobalLayout::total
   return PATH != kPathSearch ? (64u << L.b) : search_layout(L.b, L.sum_A).total;
 }
 
@@ -1627,9 +1675,37 @@ __device__ __forceinline__ void build_search(const LayerDev& L, uint32_t* lds) {
   }
 }
 
+// Global-table path: C_j = F_{jG} of every table (u16, table t's entries from the
+// sum of ceil(A_t' / G) over t' < t) and the metadata (GlobalLayout).
+__device__ __forceinline__ uint32_t global_base(const LayerDev& L, uint32_t t) {
+  uint32_t acc = 0;
+  for (uint32_t i = 0; i < t; i++) acc += (L.tab_A[i] + (1u << L.g_bits) - 1) >> L.g_bits;
+  return acc;
+}
+
+__device__ __forceinline__ void build_global(const LayerDev& L, uint32_t* lds) {
+  uint16_t* cum = reinterpret_cast<uint16_t*>(lds);
+  const uint32_t g = L.g_bits, G = 1u << g;
+  scan_tables(
+      L,
+      [&](int t, uint32_t s, uint32_t F, uint32_t) {
+        if ((s & (G - 1)) == 0) cum[global_base(L, (uint32_t)t) + (s >> g)] = (uint16_t)F;
+      },
+      [](int, uint32_t) {});
+  if (threadIdx.x < 64) {
+    const uint32_t t = threadIdx.x & 15, q = threadIdx.x >> 4;
+    lds[L.g_meta / 4 + threadIdx.x] = q == 0 ? global_base(L, t)
+                                      : q == 1 ? (uint32_t)L.tab_min[t]
+                                      : q == 2 ? (L.tab_A[t] + G - 1) >> g
+                                               : L.tab_off[t];
+  }
+}
+
 template <int PATH>
 __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
-  if (PATH != kPathSearch && L.sum_A <= kRingBytes / 4) {
+  if (PATH == kPathGlobal) {
+    build_global(L, lds);
+  } else if (PATH != kPathSearch && L.sum_A <= kRingBytes / 4) {
     uint32_t* cum = lds + (16u << L.b);   // scratch inside the ring area
     build_cumulative(L, cum);
     __syncthreads();
@@ -1684,11 +1760,33 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
 template <int PATH, bool DOT>
 __device__ __forceinline__ void dispatch_task(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                               uint32_t ring_area, uint32_t task, int32_t* status) {
-  if (PATH == kPathSearch) task_b<PATH, 0, DOT>(L, tab, lb, ring_area, task, status);
+  if (PATH == kPathSearch || PATH == kPathGlobal) task_b<PATH, 0, DOT>(L, tab, lb, ring_area, task, status);
   else if (L.b == 11) task_b<PATH, 11, DOT>(L, tab, lb, ring_area, task, status);
   else if (L.b == 10) task_b<PATH, 10, DOT>(L, tab, lb, ring_area, task, status);
   else task_b<PATH, 9, DOT>(L, tab, lb, ring_area, task, status);
 }
+
+// Decode global tasks [t_begin, t_end) of a layer list: per layer segment the
+// workgroup builds that layer's tables, then its waves take tasks in turn.
+// DOT: the fused product (every layer's output mode is kOutDotI8).
+// One layer segment of a workgroup: build the layer's tables, then the waves
+// take tasks [seg, seg_end) in turn.
+template <int PATH, bool DOT>
+__device__ __forceinline__ void run_segment(const LayerDev& L, uint32_t* lds, uint32_t seg,
+                                            uint32_t seg_end, int32_t* status) {
+  build_tables<PATH>(L, lds);
+  __syncthreads();
+  const uint32_t ring_area = uni(ring_offset<PATH>(L));
+  const uint32_t first = uni(L.task_begin);
+  const Hot H = make_hot(L);
+  uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
+  for (uint32_t task = seg + wave_id(); task < seg_end; task += kWavesPerGroup)
+    dispatch_task<PATH, DOT>(H, lds, lb, ring_area, task - first, status);
+}
+
+// A layer list whose layers take different decode paths: each segment runs
+// the kernel family of its own layer (the path is uniform over the workgroup).
+constexpr int kPathMixed = 15;
 
 // Decode global tasks [t_begin, t_end) of a layer list: per layer segment the
 // workgroup builds that layer's tables, then its waves take tasks in turn.
@@ -1700,7 +1798,6 @@ __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers,
   const uint32_t t_begin = blockIdx.x * per_group;
   const uint32_t t_end = min(total, t_begin + per_group);
   if (t_begin >= t_end) return;
-  const uint32_t wave = wave_id();
   int li = 0;
   while (li + 1 < n_layers && layers[li + 1].task_begin <= t_begin) li++;
   for (uint32_t seg = t_begin; seg < t_end && li < n_layers; li++) {
@@ -1708,14 +1805,16 @@ __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers,
     const uint32_t seg_end = min(t_end, L.task_begin + L.n_tasks);
     if (seg_end <= seg) continue;
     __syncthreads();
-    build_tables<PATH>(L, lds);
-    __syncthreads();
-    const uint32_t ring_area = uni(ring_offset<PATH>(L));
-    const uint32_t first = uni(L.task_begin);
-    const Hot H = make_hot(L);
-    uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
-    for (uint32_t task = seg + wave; task < seg_end; task += kWavesPerGroup)
-      dispatch_task<PATH, DOT>(H, lds, lb, ring_area, task - first, status);
+    if constexpr (PATH == kPathMixed) {
+      switch (uni(L.path)) {
+        case kPathLut: run_segment<kPathLut, DOT>(L, lds, seg, seg_end, status); break;
+        case kPathWide: run_segment<kPathWide, DOT>(L, lds, seg, seg_end, status); break;
+        case kPathSearch: run_segment<kPathSearch, DOT>(L, lds, seg, seg_end, status); break;
+        default: run_segment<kPathGlobal, DOT>(L, lds, seg, seg_end, status); break;
+      }
+    } else {
+      run_segment<PATH, DOT>(L, lds, seg, seg_end, status);
+    }
     seg = seg_end;
   }
 }
@@ -1791,6 +1890,7 @@ DeviceProps device_props() {
 }
 
 uint32_t lds_bytes(uint32_t path, const ep_tensor_info& I) {
+  if (path == kPathGlobal) return global_layout(I.table_A).total + kRingBytes;
   if (path != kPathSearch) return (64u << I.prob_bits) + kRingBytes;
   return search_layout(I.prob_bits, I.sum_alphabet).total + kRingBytes;
 }
@@ -1817,9 +1917,15 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
   if (t0 > t1 || t1 > I.n_tiles) return fail(EP_ERR_ARG, "decode: tile range outside the tensor");
   if (!I.rows || !I.cols || I.cols % 8 || I.prob_bits < 9 || I.prob_bits > 15 || !I.tile_vectors)
     return fail(EP_ERR_ARG, "decode: tensor info not filled by ep_blob_info");
-  if (I.path == kPathNone)
-    return fail(EP_ERR_UNSUPPORTED, "decode: the frequency tables do not fit a decode path of this build");
+  if (!path_fits(I.path, I))
+    return fail(EP_ERR_ARG, "decode: the tensor's tables do not fit the decode path in its info");
   std::memset(&D, 0, sizeof D);
+  D.path = I.path;
+  if (I.path == kPathGlobal) {
+    const GlobalLayout G = global_layout(I.table_A);
+    D.g_bits = G.g_bits;
+    D.g_meta = G.meta;
+  }
   D.blob = static_cast<const uint8_t*>(d_blob);
   D.out = d_out;
   D.dequant = d_dequant;
@@ -1875,7 +1981,9 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
 // is a long serial chain of symbol rounds, so a lightly loaded CU finishes it
 // sooner.
 uint32_t groups_for(uint32_t path, uint32_t lds, uint32_t tasks, const DeviceProps& P) {
-  uint32_t per_cu = path != kPathSearch ? 1u : (uint32_t)std::max<size_t>(1, std::min<size_t>(2, 160 * 1024 / std::max<uint32_t>(lds, 1)));
+  uint32_t per_cu = path == kPathLut || path == kPathWide || path == kPathMixed
+                        ? 1u
+                        : (uint32_t)std::max<size_t>(1, std::min<size_t>(2, 160 * 1024 / std::max<uint32_t>(lds, 1)));
   uint32_t g = (uint32_t)P.cus * per_cu;
   return std::max(1u, std::min(g, tasks));
 }
@@ -1888,9 +1996,16 @@ int set_lds_limit(size_t bytes) {
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   hipError_t e2 = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_ws_kernel<PATH>),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  hipError_t e3 = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_dot_kernel<PATH>),
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  hipError_t e3 = hipSuccess;
+  if constexpr (PATH != kPathMixed)
+    e3 = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_dot_kernel<PATH>),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   return (e1 == hipSuccess && e2 == hipSuccess && e3 == hipSuccess) ? EP_OK : EP_ERR_HIP;
+}
+
+bool valid_launch_path(uint32_t path) {
+  return path == kPathLut || path == kPathWide || path == kPathSearch || path == kPathGlobal ||
+         path == (uint32_t)kPathMixed;
 }
 
 // Grid of a launch over `total` tasks: G workgroups of `per` consecutive tasks.
@@ -1903,7 +2018,9 @@ int launch_geometry(uint32_t path, uint32_t total, uint32_t lds, uint32_t& G, ui
   G = (total + per - 1) / per;
   int rc = path == kPathLut ? set_lds_limit<kPathLut>(lds)
            : path == kPathWide ? set_lds_limit<kPathWide>(lds)
-                               : set_lds_limit<kPathSearch>(lds);
+           : path == kPathSearch ? set_lds_limit<kPathSearch>(lds)
+           : path == kPathGlobal ? set_lds_limit<kPathGlobal>(lds)
+                                 : set_lds_limit<kPathMixed>(lds);
   if (rc) return fail(EP_ERR_HIP, "decode: cannot raise the kernel's LDS limit");
   return EP_OK;
 }
@@ -1918,8 +2035,12 @@ int launch_list(uint32_t path, const LayerDev* dl, int n, uint32_t total, uint32
     hipLaunchKernelGGL(decode_ws_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
   else if (path == kPathWide)
     hipLaunchKernelGGL(decode_ws_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
-  else
+  else if (path == kPathSearch)
     hipLaunchKernelGGL(decode_ws_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
+  else if (path == kPathGlobal)
+    hipLaunchKernelGGL(decode_ws_kernel<kPathGlobal>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
+  else
+    hipLaunchKernelGGL(decode_ws_kernel<kPathMixed>, dim3(G), dim3(kThreads), lds, s, dl, n, total, per, d_status);
   if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (std::string(who) + ": launch failed").c_str());
   return EP_OK;
 }
@@ -1949,14 +2070,20 @@ int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total,
       hipLaunchKernelGGL(decode_dot_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
     else if (dot && path == kPathWide)
       hipLaunchKernelGGL(decode_dot_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
-    else if (dot)
+    else if (dot && path == kPathSearch)
       hipLaunchKernelGGL(decode_dot_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else if (dot)
+      hipLaunchKernelGGL(decode_dot_kernel<kPathGlobal>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
     else if (path == kPathLut)
       hipLaunchKernelGGL(decode_args_kernel<kPathLut>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
     else if (path == kPathWide)
       hipLaunchKernelGGL(decode_args_kernel<kPathWide>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
-    else
+    else if (path == kPathSearch)
       hipLaunchKernelGGL(decode_args_kernel<kPathSearch>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else if (path == kPathGlobal)
+      hipLaunchKernelGGL(decode_args_kernel<kPathGlobal>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
+    else
+      hipLaunchKernelGGL(decode_args_kernel<kPathMixed>, dim3(G), dim3(kThreads), lds, s, list, n, total, per, d_status);
   }
   if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (std::string(who) + ": launch failed").c_str());
   return EP_OK;
@@ -2015,14 +2142,13 @@ int describe_layers(const ep_layer* layers, int n, const char* who, std::vector<
   uint64_t tasks = 0;
   for (int i = 0; i < n; i++) {
     const ep_layer& Lr = layers[i];
-    if (Lr.info.path != path)
-      return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": layers need different decode paths").c_str());
+    if (Lr.info.path != layers[0].info.path) path = kPathMixed;   // one kernel for every family
     int rc = fill_layer(Lr.info, Lr.d_blob, Lr.out_dtype, Lr.d_out, Lr.d_dequant, 0,
                         Lr.info.n_tiles, D[i]);
     if (rc) return rc;
     D[i].task_begin = (uint32_t)tasks;
     tasks += D[i].n_tasks;
-    lds = std::max(lds, lds_bytes(path, Lr.info));
+    lds = std::max(lds, lds_bytes(Lr.info.path, Lr.info));
   }
   if (tasks > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": too many tiles").c_str());
   total = (uint32_t)tasks;
@@ -2070,8 +2196,7 @@ int stack_decode(const ep_stack* st, int32_t* d_status, void* stream) {
   if (!st || st->n_layers < 0 || (st->n_layers > 0 && !st->d_workspace))
     return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
   if (st->total_tasks == 0) return EP_OK;
-  if (st->path != kPathLut && st->path != kPathSearch && st->path != kPathWide)
-    return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
+  if (!valid_launch_path(st->path)) return fail(EP_ERR_ARG, "ep_stack_decode: stack not prepared");
   return launch_list(st->path, static_cast<const LayerDev*>(st->d_workspace), st->n_layers,
                      st->total_tasks, st->lds_bytes, d_status, static_cast<hipStream_t>(stream),
                      "ep_stack_decode");

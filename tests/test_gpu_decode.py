@@ -49,8 +49,13 @@ def gpu_bits(t):
     return t.numpy()
 
 
-def check_blob(E, oracle, blob, dtypes=DTYPES, tag=""):
+def check_blob(E, oracle, blob, dtypes=DTYPES, tag="", path=None):
+    """Decode `blob` on the GPU to every type in `dtypes` and compare with the oracle bit for
+    bit.  `path` forces a decode path other than the one ep_blob_info chose (any path that can
+    hold the tables must give the same result)."""
     info = E.blob_info(blob)
+    if path is not None:
+        info.path = path
     d_blob = E.to_device(blob)
     for name in dtypes:
         ecode, ocode = codes(E, oracle, name)
@@ -94,14 +99,26 @@ def test_every_probability_precision(E, oracle, b):
     check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"b{b}")
 
 
+def search_fits(b, sum_A):
+    """Whether the bucketed-search tables (u16 cumulative values, 2^k + 1 bucket bounds per
+    table for some k in min(b, 11) .. 8, metadata) fit the 128 KiB the payload rings leave."""
+    cum = (2 * (sum_A + 16) + 3) & ~3
+    for k in range(min(b, 11), 7, -1):
+        meta = (cum + 2 * 16 * ((1 << k) + 1) + 3) & ~3
+        if ((meta + 128 + 511) & ~511) <= 128 * 1024:
+            return sum_A <= 0xFFFF0
+    return False
+
+
 def expected_path(info):
     """The decode path rule: narrow slot entries while every doubled coordinate lies in
-    [-256, 255], wide ones up to [-1024, 1023] (both for b <= 11), else bucketed search."""
+    [-256, 255], wide ones up to [-1024, 1023] (both for b <= 11), else bucketed search when
+    its tables fit the LDS, else the global-table path."""
     if info.prob_bits <= 11 and -256 <= info.coord2_min and info.coord2_max <= 255:
         return 1
     if info.prob_bits <= 11 and -1024 <= info.coord2_min and info.coord2_max <= 1023:
         return 3
-    return 2
+    return 2 if search_fits(info.prob_bits, info.sum_alphabet) else 4
 
 
 @pytest.mark.parametrize("target", [6.0, 8.0, 10.0])
@@ -131,23 +148,67 @@ def test_wide_slot_entries(E, oracle, b):
         check_blob(E, oracle, blob, tag=f"wide{b}")
 
 
-def test_escalated_precision_blobs(E, oracle):
-    """Blobs whose precision was escalated (b > 11) or whose scale was coarsened at b = 15
-    either decode exactly or are refused with EP_ERR_UNSUPPORTED before any launch."""
+def escalated_blobs(oracle):
+    """Two blobs of App. C.1's precision escalation, from a tensor whose sampled rows miss
+    large values in the other rows: at 10 bpp the alphabet escalates b to 13 (bucketed search
+    in LDS); at 14 bpp it exceeds 2^15 and the scale is coarsened at b = 15 (sum of the table
+    ranges 77,519, largest 31,209: beyond any LDS table, the global-table path)."""
     R, Cc = 40, 65536
     rng = np.random.default_rng(12)
     w = (rng.standard_normal((R, Cc)) * 1e-3).astype(np.float32)
     outside = [r for r in range(R) if r not in set(oracle.sample_rows(R, Cc).tolist())]
+    out = []
     for val, target in ((0.02, 10.0), (0.5, 14.0)):
         w[outside, 5] = val
         blob, st = oracle.encode(w, target, prob_bits=11)
-        info = E.blob_info(blob)
-        say(f"    target {target}: b={info.prob_bits} sum_A={info.sum_alphabet} path={info.path}")
-        if info.path:
-            check_blob(E, oracle, blob, dtypes=["COORD2"], tag=f"esc{target}")
-        else:
-            with pytest.raises(RuntimeError, match="decode path"):
-                E.decode(blob, E.COORD2_I32, info=info)
+        out.append((blob, st))
+    return out
+
+
+def test_escalated_precision_blobs(E, oracle):
+    """Every valid blob decodes on the GPU, bit-exact: the escalated one (b = 13) from LDS
+    search tables, the coarsened one (b = 15, tables too large for LDS) through the
+    global-table path, whose frequencies stay in the blob in global memory."""
+    (b13, s13), (b15, s15) = escalated_blobs(oracle)
+    assert s13["b"] == 13 and s13["coarsenings"] == 0
+    assert s15["b"] == 15 and s15["coarsenings"] >= 1
+    i13, i15 = E.blob_info(b13), E.blob_info(b15)
+    say(f"    b=13 sum_A={i13.sum_alphabet} path={i13.path}; b=15 sum_A={i15.sum_alphabet} path={i15.path}")
+    assert i13.path == expected_path(i13) == 2
+    assert i15.path == expected_path(i15) == 4 and i15.sum_alphabet == 77519
+    check_blob(E, oracle, b13, dtypes=["COORD2", "BF16"], tag="esc b13")
+    check_blob(E, oracle, b15, dtypes=["COORD2", "BF16", "FP32", "FP16"], tag="coarsened b15")
+
+
+@pytest.mark.parametrize("case", ["cfg1", "ragged45", "c8", "fp8c", "int8c", "b9", "b15", "wide", "V1"])
+def test_global_table_path_on_any_blob(E, oracle, case):
+    """The global-table path holds any valid table, so forcing it on blobs that would take
+    another path must give the same bits: every output type, ragged tiles, containers with
+    their scales, b from 9 to 15 and wide coordinates."""
+    gen = {
+        "cfg1": lambda: oracle.encode(W.single_linear(), 4.0, prob_bits=12),
+        "ragged45": lambda: oracle.encode(W.ragged_tensor(1, 37, 136), 3.3, tile_vectors=45),
+        "c8": lambda: oracle.encode(W.ragged_tensor(2, 300, 8), 4.0, tile_vectors=33),
+        "fp8c": lambda: oracle.encode(W.ragged_tensor(3, 128, 512, scale=0.05), 4.0, container=1),
+        "int8c": lambda: oracle.encode(W.ragged_tensor(4, 128, 512, scale=0.05), 6.0, container=2),
+        "b9": lambda: oracle.encode(W.ragged_tensor(6, 64, 256), 2.0, prob_bits=9),
+        "b15": lambda: oracle.encode(W.ragged_tensor(7, 64, 1024), 9.0, prob_bits=15),
+        "wide": lambda: oracle.encode(W.attention_projection()[:256, :2048], 8.0),
+        "V1": lambda: oracle.encode(W.ragged_tensor(8, 1, 4096), 3.0, tile_vectors=1),
+    }[case]
+    blob, _ = gen()
+    check_blob(E, oracle, blob, tag=f"global {case}", path=4)
+
+
+def test_decode_refuses_a_path_that_cannot_hold_the_tables(E, oracle):
+    """A caller-edited info naming a slot-table path for tables it cannot hold is refused on
+    the host with EP_ERR_ARG, before any launch."""
+    (b13, _), _ = escalated_blobs(oracle)
+    info = E.blob_info(b13)
+    info.path = 1
+    with pytest.raises(E.EntroPackError) as ei:
+        E.decode(b13, E.COORD2_I32, info=info)
+    assert ei.value.code == E.ERR_ARG
 
 
 @pytest.mark.parametrize("shape,V", [((1, 8), 512), ((3, 24), 32), ((7, 400), 45),
@@ -323,6 +384,62 @@ def test_config5_down_int8_container(E, oracle, mlp):
     assert info.path == 3   # coordinates beyond a signed byte: wide slot entries
 
 
+def test_mixed_path_stack_in_one_launch(E, oracle, mlp, mlp_fp8_blobs):
+    """Layers whose tables take different decode paths decode in one launch: the config-3
+    FP8 set (narrow slot tables), the config-5 INT8-container down projection (wide slot
+    tables), the two escalated blobs (LDS search tables; the global-table path) and three
+    ragged layers (the generic loop), through ep_decode_layers (nine layers: descriptors in the
+    workspace) and through a prepared stack decoded twice."""
+    b5, _ = oracle.encode(mlp["down"], 6.0, container=oracle.CONT_INT8)
+    (b13, _), (b15, _) = escalated_blobs(oracle)
+    items = [(mlp_fp8_blobs[n], "FP8") for n in ("gate", "up", "down")]
+    items += [(b5, "INT8"), (b13, "BF16"), (b15, "BF16")]
+    for seed, shape, V in ((1, (37, 136), 45), (2, (300, 8), 33), (5, (65, 1000), 77)):
+        items.append((oracle.encode(W.ragged_tensor(seed, *shape), 3.0, tile_vectors=V)[0], "FP16"))
+    infos = [E.blob_info(b) for b, _ in items]
+    assert [i.path for i in infos[:6]] == [1, 1, 1, 3, 2, 4]
+    dev = [E.to_device(b) for b, _ in items]
+    outs = [torch.empty((i.rows, i.cols), dtype=E.torch_dtype(codes(E, oracle, dt)[0]), device="cuda")
+            for i, (_, dt) in zip(infos, items)]
+    dqs = [torch.zeros(i.rows, dtype=torch.float32, device="cuda") if i.container else None for i in infos]
+    layers = [(i, d.data_ptr(), o.data_ptr(), q.data_ptr() if q is not None else 0, codes(E, oracle, dt)[0])
+              for i, d, o, q, (_, dt) in zip(infos, dev, outs, dqs, items)]
+    with ThreadPoolExecutor(8) as ex:
+        refs = list(ex.map(lambda it: oracle.decode(it[0], codes(E, oracle, it[1])[1]), items))
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def check(tag):
+        for k, (o, q, (ref, ref_dq)) in enumerate(zip(outs, dqs, refs)):
+            assert np.array_equal(gpu_bits(o), ref), (tag, k, infos[k].path)
+            if q is not None:
+                assert np.array_equal(q.cpu().numpy(), ref_dq), (tag, k)
+
+    def clear():
+        for o in outs:
+            o.view(torch.uint8).fill_(0x55)
+
+    clear()
+    ws = E.decode_layers_workspace(len(layers))
+    d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    say("  ep_decode_layers over 9 layers on 5 decode paths")
+    E.decode_layers(layers, d_ws.data_ptr(), ws, st.data_ptr(), stream)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    check("decode_layers")
+    sws = E.stack_workspace(len(layers))
+    d_sws = torch.zeros(sws, dtype=torch.uint8, device="cuda")
+    stk = E.stack_prepare(layers, d_sws.data_ptr(), sws, stream)
+    for rep in range(2):
+        clear()
+        st.zero_()
+        say(f"  mixed prepared stack, launch {rep}")
+        E.stack_decode(stk, st.data_ptr(), stream)
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0
+        check(f"stack {rep}")
+
+
 def test_config4_stack_two_blocks_one_launch(E, oracle):
     """Two diffusion-transformer blocks (12 layers at full layer shapes) in one
     ep_decode_layers launch; more than 8 layers use the workspace descriptor list."""
@@ -373,7 +490,7 @@ def test_config4_full_stack_sampled_tiles(E, oracle):
     dev = [E.to_device(b) for b in blobs]
     outs = [torch.empty((i.rows, i.cols), dtype=torch.bfloat16, device="cuda") for i in infos]
     for o in outs:
-        o.view(torch.int16).fill_(0x7FC1)   # NaN pattern: any tile left unwritten fails
+        o.view(torch.int16).fill_(0x7FC1)   # NaN pattern, which a decode never writes
     layers = [(i, d.data_ptr(), o.data_ptr(), 0, E.BF16) for i, d, o in zip(infos, dev, outs)]
     ws = E.stack_workspace(len(layers))
     d_ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
@@ -385,6 +502,9 @@ def test_config4_full_stack_sampled_tiles(E, oracle):
     E.stack_decode(st, status.data_ptr(), stream)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
+    # every weight of every layer was written: no sentinel left anywhere
+    for name, o in zip(names, outs):
+        assert not bool((o.view(torch.int16) == 0x7FC1).any()), name
     rng = np.random.default_rng(44)
     for name, blob, info, o in zip(names, blobs, infos, outs):
         picks = sorted({0, info.n_tiles - 1, *rng.choice(info.n_tiles, 3, replace=False).tolist()})
