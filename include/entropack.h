@@ -255,6 +255,18 @@ uint64_t ep_decode_layers_workspace(int n);
 int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      int32_t* d_status, void* hip_stream);
 
+/* The same decode as ep_decode_layers for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument and no allocation of any kind.  The layer
+ * descriptors are copied (one hipMemcpyAsync on hip_stream, which has read the host
+ * list when it returns) into a static device array of the library, 512 descriptors
+ * in size, that each device keeps until the process ends; n above 512 is refused
+ * with EP_ERR_ARG.  Every call on a device shares that array: calls that overlap on
+ * one device (several streams, several host threads) race and must be serialised by
+ * the caller; consecutive calls on one stream are ordered.  Errors: as
+ * ep_decode_layers, and EP_ERR_HIP when the array's address cannot be found. */
+int ep_decode_layers_noalloc(const ep_layer* layers, int n, int32_t* d_status, void* hip_stream);
+
 /* ---- prepared stacks ------------------------------------------------------ */
 /* A layer list whose device descriptors were written once by ep_stack_prepare,
  * so that every later decode of the same blobs into the same outputs (one per

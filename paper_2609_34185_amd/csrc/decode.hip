@@ -2166,6 +2166,54 @@ int decode_layers(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, 
                        static_cast<hipStream_t>(stream), "ep_decode_layers");
 }
 
+// ---- decode without any allocation: the descriptor list in a static device array ----
+// For callers that cannot allocate device memory.  The descriptors that
+// ep_decode_layers copies into the caller's workspace go to `scratch`, a
+// file-scope device array that every device running this library holds until
+// the process ends.  Host code never names the array as a pointer: its device
+// address on each device is looked up once with hipGetSymbolAddress and kept.
+constexpr int kNoAllocMaxLayers = 512;
+constexpr size_t kScratchBytes = (size_t)kNoAllocMaxLayers * sizeof(LayerDev);
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device (looked up on first use
+// per device), or an error.
+int scratch_address(void** out) {
+  static std::mutex mu;
+  static std::vector<void*> addr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return fail(EP_ERR_HIP, "ep_decode_layers_noalloc: no HIP device");
+  std::lock_guard<std::mutex> g(mu);
+  if ((int)addr.size() <= dev) addr.resize((size_t)dev + 1, nullptr);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+      return fail(EP_ERR_HIP, "ep_decode_layers_noalloc: cannot find the static descriptor array");
+    addr[dev] = ptr;
+  }
+  *out = addr[dev];
+  return EP_OK;
+}
+
+int decode_layers_noalloc(const ep_layer* layers, int n, int32_t* d_status, void* stream) {
+  if (n > kNoAllocMaxLayers)
+    return fail(EP_ERR_ARG, "ep_decode_layers_noalloc: more than 512 layers (the static descriptor array's size)");
+  std::vector<LayerDev> D;
+  uint32_t path = 0, total = 0, lds = 0;
+  int rc = describe_layers(layers, n, "ep_decode_layers_noalloc", D, path, total, lds);
+  if (rc) return rc;
+  if (total == 0) return EP_OK;
+  void* ptr = nullptr;
+  rc = scratch_address(&ptr);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the previous call's descriptors are simply overwritten (every entry used is written here)
+  if (hipMemcpyAsync(ptr, D.data(), sizeof(LayerDev) * D.size(), hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_layers_noalloc: descriptor copy failed");
+  return launch_list(path, static_cast<const LayerDev*>(ptr), n, total, lds, d_status, s,
+                     "ep_decode_layers_noalloc");
+}
+
 uint64_t stack_workspace(int n) { return n > 0 ? (uint64_t)n * sizeof(LayerDev) : 0; }
 
 int stack_prepare(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, ep_stack* st,
@@ -2223,6 +2271,10 @@ uint64_t ep_decode_layers_workspace(int n) { return ep::decode_layers_workspace(
 int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      int32_t* d_status, void* hip_stream) {
   return ep::decode_layers(layers, n, d_workspace, ws_bytes, d_status, hip_stream);
+}
+
+int ep_decode_layers_noalloc(const ep_layer* layers, int n, int32_t* d_status, void* hip_stream) {
+  return ep::decode_layers_noalloc(layers, n, d_status, hip_stream);
 }
 
 uint64_t ep_stack_workspace(int n) { return ep::stack_workspace(n); }

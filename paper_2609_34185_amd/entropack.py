@@ -107,6 +107,7 @@ def lib():
         L.ep_decode_layers_workspace.argtypes = [C.c_int]
         L.ep_decode_layers_workspace.restype = u64
         L.ep_decode_layers.argtypes = [C.POINTER(Layer), C.c_int, vp, u64, vp, vp]
+        L.ep_decode_layers_noalloc.argtypes = [C.POINTER(Layer), C.c_int, vp, vp]
         L.ep_stack_workspace.argtypes = [C.c_int]
         L.ep_stack_workspace.restype = u64
         L.ep_stack_prepare.argtypes = [C.POINTER(Layer), C.c_int, vp, u64, C.POINTER(Stack), vp]
@@ -120,6 +121,7 @@ def lib():
 
 EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_encode_gpu", "ep_blob_free", "ep_blob_info",
            "ep_decode_tiles", "ep_decode_layers_workspace", "ep_decode_layers",
+           "ep_decode_layers_noalloc",
            "ep_stack_workspace", "ep_stack_prepare", "ep_stack_decode", "ep_gemm_i8_nt",
            "ep_decode_matmul_i8",
            "ep_last_error"]
@@ -207,6 +209,14 @@ def decode_layers(layers, d_ws: int, ws_bytes: int, d_status: int = 0, stream: i
     arr = _layer_array(layers)
     _check(lib().ep_decode_layers(arr, len(layers), d_ws, ws_bytes, d_status or None,
                                   stream or None), "ep_decode_layers")
+
+
+def decode_layers_noalloc(layers, d_status: int = 0, stream: int = 0):
+    """As decode_layers, with the descriptors in the library's static device array (no
+    workspace, no allocation; at most 512 layers)."""
+    arr = _layer_array(layers)
+    _check(lib().ep_decode_layers_noalloc(arr, len(layers), d_status or None, stream or None),
+           "ep_decode_layers_noalloc")
 
 
 def stack_workspace(n: int) -> int:
