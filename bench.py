@@ -36,6 +36,10 @@ SALU and LDS utilisation from the committed SQ counter summary.  Both are null
 when their summary is absent or was taken from a different decode kernel
 source than the one built.
 
+Parity gate: before anything is timed, the CPU-baseline leg decodes the same blobs with the
+oracle, and one GPU step's output (every weight, and the dequant scales) must equal it bit for
+bit, or the run stops (config.parity_gate records the check; --no-cpu-baseline skips both).
+
 Timing: the W warm-up steps are followed, untimed, by further steps until
 SETTLE_S seconds have passed since the warm-up began (config.settle_steps
 says how many), because a GPU fresh from idle runs its first milliseconds at
@@ -399,7 +403,8 @@ def cold_cache_ms(step, reps=15):
 
 
 def cpu_baseline(items, threads):
-    """The oracle decoder on the same blobs, tiles split over `threads` host threads."""
+    """The oracle decoder on the same blobs, tiles split over `threads` host threads.  Returns
+    (the timing record, the oracle's outputs [(weights, dequant or None)] for the parity gate)."""
     import numpy as np
     from oracle import oracle as O
     ocode = {1: O.BF16, 2: O.FP16, 3: O.FP32, 4: O.FP8, 5: O.INT8}
@@ -434,13 +439,35 @@ def cpu_baseline(items, threads):
     O.decode(blob, ocode[dt], 0, t1, out=out, dequant=dq)
     sec1 = time.perf_counter() - t
     w1 = min(t1 * h["V"] * 8, h["rows"] * h["cols"])
-    return {"value": weights / sec, "unit": "weights/s", "cores": threads, "kind": "oracle",
-            "sample": f"all {len(items)} tensors ({weights} weights) decoded once by the plain C "
-                      f"oracle, tiles split over {threads} threads", "seconds": round(sec, 3),
-            "cpu": cpu_model(),
-            "single_thread": {"value": w1 / sec1, "unit": "weights/s", "cores": 1,
-                              "sample": f"{label}: tiles [0, {t1}) ({w1} weights)",
-                              "seconds": round(sec1, 3)}}
+    # the single-thread run rewrote the first tiles of the first tensor with the same values
+    rec = {"value": weights / sec, "unit": "weights/s", "cores": threads, "kind": "oracle",
+           "host_cores": len(os.sched_getaffinity(0)),
+           "sample": f"all {len(items)} tensors ({weights} weights) decoded once by the plain C "
+                     f"oracle, tiles split over {threads} threads (the box's CPU share of "
+                     f"{len(os.sched_getaffinity(0))} visible cores)", "seconds": round(sec, 3),
+           "cpu": cpu_model(),
+           "single_thread": {"value": w1 / sec1, "unit": "weights/s", "cores": 1,
+                             "sample": f"{label}: tiles [0, {t1}) ({w1} weights)",
+                             "seconds": round(sec1, 3)}}
+    return rec, [(out, dq if O.header(blob)["container"] else None)
+                 for (out, dq), (_, blob, _) in zip(outs, items)]
+
+
+def parity_gate(keep, refs, torch):
+    """Bit-exact comparison of every decoded weight (and dequant scale) of one GPU step with the
+    oracle's decode of the same blobs, before anything is timed."""
+    import numpy as np
+    n = 0
+    for k, (ref, ref_dq) in enumerate(refs):
+        out, dq = keep[3 * k + 1], keep[3 * k + 2]
+        got = out.view(torch.uint8 if out.element_size() == 1 else
+                       torch.int16 if out.element_size() == 2 else torch.int32).cpu().numpy()
+        if not np.array_equal(got.reshape(ref.shape), ref.view(got.dtype)):   # bit patterns
+            raise SystemExit(f"parity gate: tensor {k} differs from the oracle's decode")
+        if ref_dq is not None and not np.array_equal(dq.cpu().numpy(), ref_dq):
+            raise SystemExit(f"parity gate: dequant scales of tensor {k} differ from the oracle's")
+        n += ref.size
+    return {"tensors": len(refs), "weights": n, "bit_exact": True}
 
 
 def cpu_model() -> str:
@@ -517,6 +544,20 @@ def main():
     def step():
         E.stack_decode(stack, status.data_ptr(), stream.cuda_stream)
 
+    # the CPU-baseline leg runs first: the oracle's outputs are the parity gate's reference
+    cpu = refs = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle decoder")
+        cpu, refs = cpu_baseline(items, threads)
+    step()
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+    gate = None
+    if refs is not None:
+        log("parity gate: every decoded weight against the oracle")
+        gate = parity_gate(keep, refs, torch)
+        del refs
+
     t0 = time.perf_counter()
     for _ in range(args.warmup):
         step()
@@ -574,9 +615,9 @@ def main():
     line["counters"] = measured_counters(args.workload)
     if gemm is not None:
         line["config"]["gemm"] = gemm
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle decoder")
-        line["cpu_baseline"] = cpu_baseline(items, threads)
+    line["config"]["parity_gate"] = gate
+    if cpu is not None:
+        line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
 
 
