@@ -268,9 +268,11 @@ int ep_decode_layers(const ep_layer* layers, int n, void* d_workspace, uint64_t 
 int ep_decode_layers_noalloc(const ep_layer* layers, int n, int32_t* d_status, void* hip_stream);
 
 /* ---- prepared stacks ------------------------------------------------------ */
-/* A layer list whose device descriptors were written once by ep_stack_prepare,
- * so that every later decode of the same blobs into the same outputs (one per
- * forward pass of a compressed model) is a single kernel launch with no copy. */
+/* A layer list whose device descriptors and decode tables were written once by
+ * ep_stack_prepare, so that every later decode of the same blobs into the same
+ * outputs (one per forward pass of a compressed model) is a single kernel launch
+ * with no copy: its workgroups load each layer's prepared tables instead of
+ * rebuilding them from the blob. */
 typedef struct {
   void* d_workspace;         /* device descriptor list (caller-owned memory) */
   int32_t n_layers;
@@ -280,13 +282,16 @@ typedef struct {
   uint32_t reserved[4];
 } ep_stack;
 
-/* Device bytes ep_stack_prepare needs for n layers. */
+/* Device bytes ep_stack_prepare needs for n layers: the descriptors and one
+ * 128 KiB decode-table image per layer. */
 uint64_t ep_stack_workspace(int n);
 
-/* Validate n layers (as for ep_decode_layers), write their descriptors into
- * d_workspace (>= ep_stack_workspace(n) bytes, device memory owned by the
- * caller, which must outlive every ep_stack_decode of this stack) and fill
- * *stack.  Synchronous: returns after the copy on hip_stream has completed.
+/* Validate n layers (as for ep_decode_layers), write their descriptors and build
+ * their decode tables into d_workspace (>= ep_stack_workspace(n) bytes, device
+ * memory owned by the caller, which must outlive every ep_stack_decode of this
+ * stack; the blobs must stay unchanged too) and fill *stack.  Synchronous:
+ * returns after the copy and the table-building launch on hip_stream have
+ * completed.
  * Errors: as ep_decode_layers, EP_ERR_ARG for a null stack or short workspace. */
 int ep_stack_prepare(const ep_layer* layers, int n, void* d_workspace, uint64_t ws_bytes,
                      ep_stack* stack, void* hip_stream);

@@ -90,6 +90,8 @@ struct LayerDev {
   uint32_t m;
   uint32_t path;                  // decode path of the layer (DecodePath)
   uint32_t g_bits, g_meta;        // global-table path: log2 G, byte offset of its metadata
+  const uint8_t* tables;          // prepared stacks: the layer's decode tables as built in LDS
+                                  // (ring_offset bytes), copied in instead of rebuilt; or null
 };
 
 // The scalars the decode loop needs, read once per layer segment and forced
@@ -1769,12 +1771,37 @@ __device__ __forceinline__ void dispatch_task(const Hot& L, const uint32_t* tab,
 // Decode global tasks [t_begin, t_end) of a layer list: per layer segment the
 // workgroup builds that layer's tables, then its waves take tasks in turn.
 // DOT: the fused product (every layer's output mode is kOutDotI8).
-// One layer segment of a workgroup: build the layer's tables, then the waves
-// take tasks [seg, seg_end) in turn.
+// Prepared stacks: copy the layer's decode tables, built once by the stack's
+// preparation, from global memory into LDS (16 bytes per thread and load, eight
+// loads in flight before the first write).
+template <int PATH>
+__device__ __forceinline__ void load_tables(const LayerDev& L, uint32_t* lds) {
+  const uint32_t n16 = ring_offset<PATH>(L) / 16;
+  const EP_GLOBAL u32x4* src = gptr<const u32x4>(L.tables);
+  u32x4* dst = reinterpret_cast<u32x4*>(lds);
+  constexpr uint32_t kUnroll = 8;
+  for (uint32_t i0 = threadIdx.x; i0 < n16; i0 += kUnroll * kThreads) {
+    u32x4 v[kUnroll];
+#pragma unroll
+    for (uint32_t k = 0; k < kUnroll; k++) {
+      const uint32_t i = i0 + k * kThreads;
+      if (i < n16) v[k] = src[i];
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < kUnroll; k++) {
+      const uint32_t i = i0 + k * kThreads;
+      if (i < n16) dst[i] = v[k];
+    }
+  }
+}
+
+// One layer segment of a workgroup: build (or copy) the layer's tables, then
+// the waves take tasks [seg, seg_end) in turn.
 template <int PATH, bool DOT>
 __device__ __forceinline__ void run_segment(const LayerDev& L, uint32_t* lds, uint32_t seg,
                                             uint32_t seg_end, int32_t* status) {
-  build_tables<PATH>(L, lds);
+  if (L.tables) load_tables<PATH>(L, lds);
+  else build_tables<PATH>(L, lds);
   __syncthreads();
   const uint32_t ring_area = uni(ring_offset<PATH>(L));
   const uint32_t first = uni(L.task_begin);
@@ -1864,6 +1891,29 @@ __global__ __launch_bounds__(kThreads) void decode_ws_kernel(const LayerDev* __r
                                                              uint32_t total, uint32_t per_group,
                                                              int32_t* status) {
   run_layers<PATH>(layers, n_layers, total, per_group, status);
+}
+
+// Prepared stacks: workgroup i builds layer i's decode tables in LDS, exactly as
+// a decode launch would, and writes them to the layer's table image.
+template <int PATH>
+__device__ __forceinline__ void build_and_store(const LayerDev& L, uint32_t* lds) {
+  build_tables<PATH>(L, lds);
+  __syncthreads();
+  const uint32_t n16 = ring_offset<PATH>(L) / 16;
+  EP_GLOBAL u32x4* dst = gptr<u32x4>(L.tables);
+  const u32x4* src = reinterpret_cast<const u32x4*>(lds);
+  for (uint32_t i = threadIdx.x; i < n16; i += kThreads) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(kThreads) void stack_tables_kernel(const LayerDev* __restrict__ layers) {
+  extern __shared__ uint32_t lds[];
+  const LayerDev& L = layers[blockIdx.x];
+  switch (uni(L.path)) {
+    case kPathLut: build_and_store<kPathLut>(L, lds); break;
+    case kPathWide: build_and_store<kPathWide>(L, lds); break;
+    case kPathSearch: build_and_store<kPathSearch>(L, lds); break;
+    default: build_and_store<kPathGlobal>(L, lds); break;
+  }
 }
 
 // ---- host side ---------------------------------------------------------------------
@@ -2214,7 +2264,13 @@ int decode_layers_noalloc(const ep_layer* layers, int n, int32_t* d_status, void
                      "ep_decode_layers_noalloc");
 }
 
-uint64_t stack_workspace(int n) { return n > 0 ? (uint64_t)n * sizeof(LayerDev) : 0; }
+// Workspace of a prepared stack: the n descriptors, then one table image per layer
+// (every path's tables fit 128 KiB).
+constexpr uint64_t kTableImageBytes = 128 * 1024;
+uint64_t stack_tables_offset(int n) { return ((uint64_t)n * sizeof(LayerDev) + 255) & ~255ull; }
+uint64_t stack_workspace(int n) {
+  return n > 0 ? stack_tables_offset(n) + (uint64_t)n * kTableImageBytes : 0;
+}
 
 int stack_prepare(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, ep_stack* st,
                   void* stream) {
@@ -2227,10 +2283,23 @@ int stack_prepare(const ep_layer* layers, int n, void* d_ws, uint64_t ws_bytes, 
   if (n > 0) {
     if (!d_ws || ws_bytes < stack_workspace(n))
       return fail(EP_ERR_ARG, "ep_stack_prepare: workspace too small");
+    uint8_t* images = static_cast<uint8_t*>(d_ws) + stack_tables_offset(n);
+    uint32_t build_lds = 0;
+    for (int i = 0; i < n; i++) {
+      D[i].tables = images + (uint64_t)i * kTableImageBytes;
+      build_lds = std::max(build_lds, lds_bytes(layers[i].info.path, layers[i].info));
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (hipMemcpyAsync(d_ws, D.data(), sizeof(LayerDev) * D.size(), hipMemcpyHostToDevice, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (hipMemcpyAsync(d_ws, D.data(), sizeof(LayerDev) * D.size(), hipMemcpyHostToDevice, s) != hipSuccess)
       return fail(EP_ERR_HIP, "ep_stack_prepare: descriptor copy failed");
+    // the tables are built once here; every ep_stack_decode copies them into LDS
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&stack_tables_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)build_lds) != hipSuccess)
+      return fail(EP_ERR_HIP, "ep_stack_prepare: cannot raise the table kernel's LDS limit");
+    hipLaunchKernelGGL(stack_tables_kernel, dim3((unsigned)n), dim3(kThreads), build_lds, s,
+                       static_cast<const LayerDev*>(d_ws));
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+      return fail(EP_ERR_HIP, "ep_stack_prepare: building the decode tables failed");
   }
   st->d_workspace = d_ws;
   st->n_layers = n;
