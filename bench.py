@@ -273,7 +273,7 @@ def tile_sweep(args, E, W, threads):
         torch.cuda.synchronize()
         assert int(status.item()) == 0, "decode reported a corrupt stream"
         ms = a.elapsed_time(b) / args.steps
-        steady = V % 32 == 0
+        steady = info.prob_bits == 11 and info.path in (1, 3) and V >= 32   # slot-table steady state (any V >= 32)
         rows.append({"V": V, "symbols_per_tile": 9 * V, "tiles": info.n_tiles,
                      "stored_bpp": round(8.0 * blob.size / weights, 4),
                      "erel_pct": round(100.0 * st["erel_coded"], 3), "ms": ms,

@@ -34,6 +34,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/entropack.h"
@@ -781,6 +782,7 @@ constexpr uint32_t kFastRingWords = kFastRingBytes / 2;
 constexpr uint32_t kFastBlockWords = 128;
 constexpr uint32_t kFastChainBytes = 2 * kFastRingBytes;
 constexpr uint32_t kFastOob = 0x80000000u;   // buffer offset past any payload section
+constexpr uint32_t kPinnedState = 0x7FFFFFFFu; // a state that takes no refill for one symbol
 static_assert(kWavesPerGroup * 2 * kFastChainBytes <= kRingBytes, "fast ring area");
 static_assert(search_layout(11, 0).total % kFastRingBytes == 0 &&
                   search_layout(12, 12345).total % kFastRingBytes == 0 &&
@@ -1344,8 +1346,8 @@ __device__ __forceinline__ int32_t half_sum(int32_t v) {
 
 // The steady-state task of the slot-table path: four full tiles t0 .. t0 + 3
 // (two chains).  TWO: every lane's vectors v, v + 32, ... of a tile lie in at
-// most two rows (C/8 >= V - 32), so each lane holds both row scales and
-// switches at round kc; otherwise the row scale is loaded every round.
+// most two rows (C/8 >= 32 (ceil(V / 32) - 1)), so each lane holds both row
+// scales and switches at round kc; otherwise the row scale is loaded every round.
 //
 // Fused product (DT = kOutDotI8): each round's eight INT8 weights go straight
 // into two dot4 instructions per row of X.  With TWO (the caller guarantees
@@ -1430,10 +1432,25 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
   EP_GLOBAL uint8_t* obase = gptr<uint8_t>(L.out) + (uint64_t)t0 * L.V * VB;
   const uint32_t vH = half;
   const uint32_t vf0 = L.coset_f0, vf1 = L.coset_f1, vcb = 32u << B;
-  const uint32_t rounds = L.V / 32;
+  // V = 32 * full + tail vectors: `full` rounds in which every lane decodes a
+  // vector, then (tail > 0, store outputs only) one round in which lanes
+  // l >= tail have none.  That round runs the same steps with those lanes'
+  // states pinned at 2^31 - 1 before every symbol: x >> b then exceeds 2^15 / f
+  // for any f >= 1, so they never take a refill word, and the staging commits
+  // stay outside any divergent region.  Their decoded values are not stored,
+  // and their real final states (saved first) are checked at the end.
+  const uint32_t full = L.V / 32, tail = L.V % 32;
+  const uint32_t rounds = full + (tail ? 1 : 0);
   const uint32_t vrb08 = vrb0 + vl8, vrb18 = vrb1 + vl8;
+  uint32_t xsave[2] = {0, 0};
+  const bool pin = l >= tail;
 
-  for (uint32_t k = 0; k < rounds; k++) {
+  auto round = [&](uint32_t k, auto part) {
+    constexpr bool PART = decltype(part)::value;
+    if constexpr (PART) {
+      xsave[0] = x[0];
+      xsave[1] = x[1];
+    }
     // room for a block: margin <= ring - block
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half,
                     kFastRingWords - kFastBlockWords + 1);
@@ -1469,9 +1486,16 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
     float y0, y1;
     QAcc acc[2];
     acc[0].X = acc[1].X = 0;
+#define EP_PIN                            \
+  if constexpr (PART) {                   \
+    x[0] = pin ? kPinnedState : x[0];     \
+    x[1] = pin ? kPinnedState : x[1];     \
+  }
+    EP_PIN
     coset_step2<B>(x[0], x[1], cb[0], cb[1], hc[0], hc[1], sg[0], sg[1], vf0, vf1, vcb, F0, F1, vH,
                    vrb0, vrb1);
 #define EP_FIELD(I)                                                                           \
+  EP_PIN                                                                                      \
   field_step2<B, I, YM, WIDE>(x[0], x[1], cb[0], cb[1], e0, e1, y0, y1, sg[0], sg[1], hc[0],  \
                               hc[1], acc[0].X, acc[1].X, ymax, F0, F1, vH, vrb0, vrb1);       \
   q_take<DT, I, WIDE>(acc[0], e0, y0, cb[0] >> (B + 5));                                      \
@@ -1493,6 +1517,7 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
     fast_stage_both(F0, F1, pend0, pendB0, pend1, pendB1, lds, vrb08, vrb18, vl8, rsrc, half, 3 * 32);
     EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
 #undef EP_FIELD
+#undef EP_PIN
     if constexpr (ACC) {
 #pragma unroll
       for (int j = 0; j < 2; j++)
@@ -1506,9 +1531,19 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
         dot_add(L, acc[j].w[0], acc[j].w[1], v, row_of(L, v));
       }
     } else {
-      q_put<DT>(obase, voff[0], acc[0]);
-      q_put<DT>(obase, voff[1], acc[1]);
+      if (!PART || !pin) {
+        q_put<DT>(obase, voff[0], acc[0]);
+        q_put<DT>(obase, voff[1], acc[1]);
+      }
       obase += 32 * VB;
+    }
+  };
+  for (uint32_t k = 0; k < full; k++) round(k, std::false_type{});
+  if constexpr (!DOT) {
+    if (tail) {
+      round(full, std::true_type{});
+      x[0] = pin ? xsave[0] : x[0];
+      x[1] = pin ? xsave[1] : x[1];
     }
   }
   if constexpr (ACC) {
@@ -1559,7 +1594,9 @@ __device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32
       lut_task<B, DT, false, false, WIDE>(L, lds, ring_area, t0, status);
     }
   } else {
-    if (L.cvec + 32 >= L.V) lut_task<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
+    // a lane's vectors v, v + 32, ..., v + 32 (ceil(V / 32) - 1) lie in at most two rows when
+    // C/8 is at least their span
+    if (L.cvec >= 32 * ((L.V - 1) / 32)) lut_task<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
     else lut_task<B, DT, SAT, false, WIDE>(L, lds, ring_area, t0, status);
   }
 }
@@ -1745,9 +1782,13 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
                                        uint32_t ring_area, uint32_t task, int32_t* status) {
   const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
   const uint32_t nvec = L.rows * L.cvec;
-  const bool full = (L.V % 32 == 0) && t0 + kTilesPerTask <= L.tile_end &&
-                    (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
-  if (full && L.pay_bytes < kFastOob && (PATH == kPathSearch || B == 11)) {
+  const bool whole = t0 + kTilesPerTask <= L.tile_end && (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
+  const bool full = whole && L.V % 32 == 0;   // every lane has a vector in every round
+  // The slot-table steady state also takes tiles of any length V >= 32 (a
+  // partial last round, see lut_task); the fused product and the search path's
+  // steady state need whole rounds.
+  const bool lut_ok = whole && (full || (!DOT && L.V >= 32));
+  if (L.pay_bytes < kFastOob && ((PATH == kPathSearch && full) || (B == 11 && lut_ok))) {
     if constexpr (PATH != kPathSearch && B == 11) {
       if (lut_task_any<B, PATH == kPathWide, DOT>(L, lb, ring_area, t0, status)) return;
     } else if constexpr (PATH == kPathSearch) {
@@ -1772,27 +1813,20 @@ __device__ __forceinline__ void dispatch_task(const Hot& L, const uint32_t* tab,
 // workgroup builds that layer's tables, then its waves take tasks in turn.
 // DOT: the fused product (every layer's output mode is kOutDotI8).
 // Prepared stacks: copy the layer's decode tables, built once by the stack's
-// preparation, from global memory into LDS (16 bytes per thread and load, eight
-// loads in flight before the first write).
+// preparation, from global memory into LDS with direct loads (memory to LDS,
+// no registers): one wave instruction moves 1 KiB, lane l writing 16 bytes at
+// l * 16.  Bytes past the image read as 0 (buffer bounds) and land in the ring
+// area, which every task initialises after the barrier that follows.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
 template <int PATH>
 __device__ __forceinline__ void load_tables(const LayerDev& L, uint32_t* lds) {
-  const uint32_t n16 = ring_offset<PATH>(L) / 16;
-  const EP_GLOBAL u32x4* src = gptr<const u32x4>(L.tables);
-  u32x4* dst = reinterpret_cast<u32x4*>(lds);
-  constexpr uint32_t kUnroll = 8;
-  for (uint32_t i0 = threadIdx.x; i0 < n16; i0 += kUnroll * kThreads) {
-    u32x4 v[kUnroll];
-#pragma unroll
-    for (uint32_t k = 0; k < kUnroll; k++) {
-      const uint32_t i = i0 + k * kThreads;
-      if (i < n16) v[k] = src[i];
-    }
-#pragma unroll
-    for (uint32_t k = 0; k < kUnroll; k++) {
-      const uint32_t i = i0 + k * kThreads;
-      if (i < n16) dst[i] = v[k];
-    }
-  }
+  const uint32_t bytes = ring_offset<PATH>(L);
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.tables), (short)0, (int)bytes, 0x00020000);
+  const uint32_t lane = threadIdx.x & 63;
+  for (uint32_t c = wave_id() * 1024u; c < bytes; c += kWavesPerGroup * 1024u)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_u8*)lds + c, 16, c + 16 * lane, 0, 0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
 }
 
 // One layer segment of a workgroup: build (or copy) the layer's tables, then

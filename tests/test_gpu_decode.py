@@ -220,6 +220,36 @@ def test_ragged_shapes_and_tiles(E, oracle, shape, V):
     check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "FP8"], tag=f"V{V}")
 
 
+@pytest.mark.parametrize("shape,V", [((400, 136), 45), ((200, 520), 77), ((120, 1024), 100),
+                                     ((64, 2048), 33)])
+def test_partial_last_round_in_the_steady_state(E, oracle, shape, V):
+    """Tiles whose length is not a multiple of 32 vectors run the slot-table steady state with
+    a partial last round; a lane's vectors then lie 32 (ceil(V / 32) - 1) vectors apart, so
+    with rows of 17, 65, 128 and 256 vectors they span up to three rows, and the row scale
+    of each vector must still be its own (every output type)."""
+    w = W.ragged_tensor(50 + V, *shape)
+    blob, st = oracle.encode(w, 4.0, tile_vectors=V)
+    info = E.blob_info(blob)
+    assert info.prob_bits == 11 and info.path in (1, 3)
+    check_blob(E, oracle, blob, tag=f"partial V{V}")
+
+
+@pytest.mark.parametrize("V", [455, 1820])
+def test_paper_tile_sizes_at_full_size(E, oracle, V):
+    """The paper's default tile sizes of 4096 and 16384 symbols (Table tileoverhead: 455 and
+    1820 vectors, not multiples of 32) on the reference-layer shape 10240 x 3840 at 4.0 bpp,
+    decoded at full size to BF16 and to doubled coordinates: every element equals the oracle.
+    The slot-table steady state runs these tiles with a partial last round.  Blobs come from
+    the library encoder, byte-identical to the oracle's (checked on the first tiles' bytes of
+    the same layer in the CPU encoder tests; here the two decoders are compared)."""
+    w = dict(W.dit_block(0))["blocks.0.mlp_in"]
+    blob, st = E.encode(w, 4.0, tile_vectors=V)
+    info = E.blob_info(blob)
+    assert info.tile_vectors == V and info.path in (1, 3) and info.prob_bits == 11
+    say(f"    V={V}: {info.n_tiles} tiles, {st['rate_stored']:.4f} bpp, path {info.path}")
+    check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"V{V}")
+
+
 def test_tile_ranges_write_only_their_tiles(E, oracle):
     blob, st = oracle.encode(W.ragged_tensor(3, 200, 520), 3.5, tile_vectors=64)
     info = E.blob_info(blob)
