@@ -20,7 +20,10 @@ launch), mlp_down_int8 (the MLP down projection in the INT8 container at
 activations, timed separately: decode time over product time is reported),
 encode_mlp (the GPU encoder on the MLP set's three BF16 tensors, FP8 container
 at 4.0 bpp; a step encodes all three; the CPU baseline is the oracle encoder
-on the down projection), fused_down_m1 / _m2 / _m4 / _m8 (the fused decode and
+on the down projection), fused_mfma_m<m> (the fused decode and MFMA product
+ep_decode_gemm_i8 of the INT8-container down projection with the first m rows of the
+activations, timed beside decode-then-GEMM and the product alone on resident weights),
+fused_down_m1 / _m2 / _m4 / _m8 (the fused decode and
 small-batch product ep_decode_matmul_i8: the INT8-container down projection
 times the first 1, 2, 4 or 8 rows of the activations, one launch per step;
 algorithmic bytes = compressed blob + X read, Y and dequant written),
@@ -234,6 +237,92 @@ def fused_bench(args, E, W, threads, m):
                                 "kind": "oracle", "sample": f"the whole down projection decoded by "
                                 f"the plain C oracle, then its exact product with the {m} rows",
                                 "seconds": round(osec, 3), "cpu": cpu_model()}
+    print(json.dumps(line), flush=True)
+
+
+def time_steps(args, step, stream):
+    """Warm-up, settle, then the mean over args.steps launches (HIP events on `stream`)."""
+    import torch
+    t0 = time.perf_counter()
+    for _ in range(args.warmup):
+        step()
+    while time.perf_counter() - t0 < SETTLE_S:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(args.steps):
+        step()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / args.steps
+
+
+def fused_mfma_bench(args, E, W, threads, m):
+    """--workload fused_mfma_m<m>: Y = X W'^T for the INT8-container MLP down projection
+    (5120 x 17408 at 6.0 bpp) and the first m rows of the 8192 x 17408 activations by the fused
+    decode and MFMA product (ep_decode_gemm_i8, W' never written as a whole), timed beside
+    decode-then-GEMM (ep_decode_tiles to INT8, then ep_gemm_i8_nt) and beside the product alone
+    on resident decoded weights: the analog of the paper's decode-cost curve over tokens per
+    call (App. A.5, Fig. cost).  The fused Y must equal decode-then-GEMM's Y."""
+    import numpy as np
+    import torch
+    w = W.llm_mlp(["down"])["down"]
+    blob, _ = E.encode(w, 6.0, container=E.CONT_INT8_ROW, nthreads=threads)
+    info = E.blob_info(blob)
+    x = torch.from_numpy(np.ascontiguousarray(W.llm_activations()[:m])).cuda()
+    d_blob = E.to_device(blob, torch.device("cuda", 0))
+    y = torch.empty((m, info.rows), dtype=torch.int32, device="cuda")
+    y2 = torch.empty((m, info.rows), dtype=torch.int32, device="cuda")
+    wd = torch.empty((info.rows, info.cols), dtype=torch.int8, device="cuda")
+    dq = torch.empty(info.rows, dtype=torch.float32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = E.decode_gemm_i8_workspace(info)
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    s = stream.cuda_stream
+
+    def fused_step():
+        E.decode_gemm_i8(info, d_blob.data_ptr(), x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
+                         dq.data_ptr(), status.data_ptr(), s)
+
+    def decode_step():
+        E.decode_tiles(info, d_blob.data_ptr(), E.INT8, wd.data_ptr(), dq.data_ptr(), 0, info.n_tiles,
+                       status.data_ptr(), s)
+
+    def gemm_step():
+        E.gemm_i8_nt(x.data_ptr(), wd.data_ptr(), y2.data_ptr(), m, info.rows, info.cols, s)
+
+    fused_step()
+    decode_step()
+    gemm_step()
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+    assert torch.equal(y, y2), "fused product differs from decode-then-GEMM"
+    ms = time_steps(args, fused_step, stream)
+    ms_dec = time_steps(args, decode_step, stream)
+    ms_gemm = time_steps(args, gemm_step, stream)
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+    weights = info.rows * info.cols
+    ops = 2.0 * m * info.rows * info.cols
+    line = {
+        "metric": "fused decode + MFMA product: decoded weights/s and int8 TOP/s (% of MFMA peak)",
+        "value": weights / (ms * 1e-3), "unit": "weights/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "i32", "data": "synthetic",
+        "config": {"workload": f"fused decode and MFMA product: MLP down 5120x17408 in the INT8 row "
+                               f"container at 6.0 bpp times X = {m} x 17408 int8 rows, Y int32 exact",
+                   "rows_x": m, "weights": weights,
+                   "decode_then_gemm_ms": {"decode": ms_dec, "gemm": ms_gemm, "total": ms_dec + ms_gemm},
+                   "resident_gemm_ms": ms_gemm,
+                   "fused_over_decode_then_gemm": ms / (ms_dec + ms_gemm),
+                   "overhead_vs_resident_pct": 100.0 * (ms / ms_gemm - 1.0),
+                   "decode_then_gemm_overhead_vs_resident_pct": 100.0 * (ms_dec / ms_gemm)},
+        "roofline": {"bound": "mfma", "achieved": ops / (ms * 1e-3) / 1e12, "peak": INT8_PEAK_TOPS,
+                     "unit": "TFLOP/s", "frac": ops / (ms * 1e-3) / 1e12 / INT8_PEAK_TOPS,
+                     "traffic": None},
+    }
     print(json.dumps(line), flush=True)
 
 
@@ -511,6 +600,10 @@ def main():
         return
     if args.workload == "tile_sweep":
         tile_sweep(args, E, W, min(16, len(os.sched_getaffinity(0))))
+        return
+    if args.workload.startswith("fused_mfma_m"):
+        fused_mfma_bench(args, E, W, min(16, len(os.sched_getaffinity(0))),
+                         int(args.workload[len("fused_mfma_m"):]))
         return
     if args.workload.startswith("fused_down_m"):
         m = int(args.workload[len("fused_down_m"):])

@@ -229,6 +229,33 @@ int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtyp
 int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int m,
                         int32_t* d_y, float* d_dequant, int32_t* d_status, void* hip_stream);
 
+/* Fused decode and MFMA product for any number of rows of X (the fusion of
+ * Section 3.7's decode with the matrix product that the paper leaves to future
+ * work, App. D; the decode-time cost it measures against the product's size in
+ * App. A.5, Fig. cost; the INT8 route of App. B.1):
+ *   Y[t][r] = sum_j X[t][j] * W'[r][j]   for t < m, r < R,
+ * with W' the tensor's INT8 container matrix exactly as ep_decode_tiles writes it
+ * with EP_INT8, X m x C int8 row-major, Y m x R int32 row-major, exact (C <=
+ * 131071).  W' is never written as a whole: each workgroup decodes the tiles
+ * touching a block of ceil(R / CUs) rows into its slab of d_workspace (the
+ * block's rows plus a tile's reach on either side, so it stays in L2 and the
+ * last-level cache) and multiplies X by those rows on the matrix cores
+ * (v_mfma_i32_16x16x64_i8).  d_workspace: >= ep_decode_gemm_i8_workspace(info)
+ * bytes of device memory owned by the caller, untouched until the launch
+ * completes.  Y is overwritten (cleared first on hip_stream when m < 256, where
+ * partial sums over K are added with atomics).  d_dequant (nullable) receives delta_r for every row; d_status as for
+ * ep_decode_tiles.  Asynchronous, no allocation, at most one clear and one launch.
+ * Errors: EP_ERR_ARG (null pointers, m outside 1..65536, X above 2^31 bytes, short
+ * workspace), EP_ERR_UNSUPPORTED (not the INT8 row container, C > 131071),
+ * EP_ERR_HIP. */
+int ep_decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
+                      int32_t* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
+                      int32_t* d_status, void* hip_stream);
+
+/* Workspace bytes ep_decode_gemm_i8 needs for a tensor on the current device (one
+ * slab per workgroup; 0 if info is null or no device is present). */
+uint64_t ep_decode_gemm_i8_workspace(const ep_tensor_info* info);
+
 /* One layer of a stack decode. */
 typedef struct {
   ep_tensor_info info;       /* from ep_blob_info on the host copy */

@@ -1927,6 +1927,145 @@ __global__ __launch_bounds__(kThreads) void decode_ws_kernel(const LayerDev* __r
   run_layers<PATH>(layers, n_layers, total, per_group, status);
 }
 
+// ---- fused decode and MFMA product (any number of rows of X) ----------------------
+// Y[t][r] = sum_j X[t][j] W'[r][j] for an INT8-container tensor, with W' never
+// written as a whole.  A matrix core needs 16 rows of W' at the same columns,
+// and the tiles of the format are row segments, so each workgroup owns a block
+// of RB consecutive rows (RB = ceil(R / CUs), so that every block runs at once):
+// it decodes every tile that touches its block (the row-major INT8 values) into
+// a slab of the caller's workspace, which stays in L2 and the last-level cache,
+// then its waves multiply X by the slab's rows with v_mfma_i32_16x16x64_i8.  A
+// tile can span a block boundary: both blocks decode it, each keeping the rows
+// it owns (the slab has `margin` rows on either side for the rest).
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+
+struct GemmArgs {
+  const int8_t* x;       // m x C, row-major
+  int32_t* y;            // m x R, row-major (cleared first when K is split over waves)
+  uint8_t* slabs;        // one slab per workgroup
+  uint64_t slab_bytes;   // (RB + 2 margin) x C, rounded up to 256
+  uint32_t m, margin, n_blocks, rows_per_block;
+};
+
+struct GemmLaunch {
+  LayerDev L;
+  GemmArgs g;
+};
+
+// Block b's rows times X, from the slab (row i of the block at slab row
+// margin + i).  A work item is one tile of 16 rows of X against all NT =
+// ceil(RB / 16) tiles of 16 block rows, so each X fragment is loaded once per
+// block; items are dealt to the waves, and when there are fewer items than
+// waves K is split over the idle waves and the partial sums are added with
+// atomics (exact, order-free integer additions).  MFMA
+// operands: lane l supplies row l mod 16 of the X tile and of the slab tile, 16
+// consecutive bytes of K each (k = 16 (l / 16) + 0..15 of a 64-byte step);
+// accumulator r of lane l is element (4 (l / 16) + r, l mod 16) of a 16 x 16
+// result.
+constexpr uint32_t kGemmMaxTiles = 4;   // NT <= 4: blocks of at most 64 rows
+__device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs& g,
+                                              const uint8_t* slab, uint32_t b) {
+  const uint32_t wave = wave_id(), lane = threadIdx.x & 63;
+  const uint32_t C = L.cols, m = g.m, RB = g.rows_per_block;
+  const uint32_t T = (m + 15) / 16, NT = (RB + 15) / 16;
+  const uint32_t S = T >= kWavesPerGroup ? 1u : kWavesPerGroup / T;   // K slices
+  if (T < kWavesPerGroup && wave >= T * S) return;
+  const uint32_t slice = T >= kWavesPerGroup ? 0u : wave / T;
+  const uint32_t tt0 = T >= kWavesPerGroup ? wave : wave % T;
+  const uint32_t tstep = T >= kWavesPerGroup ? kWavesPerGroup : T;
+  constexpr uint32_t kGroup = 2;   // 64-byte K steps per group
+  const uint32_t groups = (C + 64 * kGroup - 1) / (64 * kGroup), gper = (groups + S - 1) / S;
+  const uint32_t k_begin = slice * gper * 64 * kGroup, k_end = min(C, (slice + 1) * gper * 64 * kGroup);
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int8_t*>(g.x), (short)0, (int)((uint64_t)m * C), 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(slab), (short)0, (int)g.slab_bytes, 0x00020000);
+  const uint32_t li = lane & 15, q = lane >> 4;
+  const uint32_t row0 = b * RB;
+  EP_GLOBAL int32_t* y = gptr<int32_t>(g.y);
+  for (uint32_t tt = tt0; tt < T; tt += tstep) {
+    const uint32_t tok = 16 * tt + li;
+    const uint32_t xrow = tok * C;
+    v4i_t acc[kGemmMaxTiles];
+#pragma unroll
+    for (uint32_t c = 0; c < kGemmMaxTiles; c++) acc[c] = v4i_t{0, 0, 0, 0};
+    for (uint32_t k0 = k_begin; k0 < k_end; k0 += 64 * kGroup) {
+      v4i_t a[kGroup], w[kGroup][kGemmMaxTiles];
+#pragma unroll
+      for (uint32_t u = 0; u < kGroup; u++) {
+        const uint32_t kq = k0 + 64 * u + 16 * q;
+        // K beyond the row (C % 64 != 0) reads as zeros of X: C is a multiple of 8,
+        // so a lane's 16 bytes are whole, half (the upper 8 beyond C) or none
+        const bool in = kq < k_end && tok < m;
+        v4i_t av = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(xr, in ? xrow + kq : 0x80000000u, 0, 0);
+        if (in && kq + 8 >= C) av[2] = av[3] = 0;
+        a[u] = av;
+#pragma unroll
+        for (uint32_t c = 0; c < kGemmMaxTiles; c++) {
+          const uint32_t wrow = (g.margin + 16 * c + li) * C;   // slab offset of the lane's W' row
+          w[u][c] = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(
+              wr, (c < NT && kq < k_end) ? wrow + kq : 0x80000000u, 0, 0);
+        }
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kGroup; u++)
+#pragma unroll
+        for (uint32_t c = 0; c < kGemmMaxTiles; c++)
+          if (c < NT) acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[u], w[u][c], acc[c], 0, 0, 0);
+    }
+#pragma unroll
+    for (uint32_t c = 0; c < kGemmMaxTiles; c++) {
+      const uint32_t rl = 16 * c + li, row = row0 + rl;
+#pragma unroll
+      for (uint32_t r = 0; r < 4; r++) {
+        const uint32_t t = 16 * tt + 4 * q + r;
+        if (c < NT && t < m && rl < RB && row < L.rows) {
+          if (S > 1) add_i32(y + (uint64_t)t * L.rows + row, acc[c][r]);
+          else y[(uint64_t)t * L.rows + row] = acc[c][r];
+        }
+      }
+    }
+  }
+}
+
+template <int PATH>
+__global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch launch, int32_t* status) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  (void)launch;
+  const GemmLaunch& A = *(const GemmLaunch*)__builtin_amdgcn_kernarg_segment_ptr();
+#else
+  const GemmLaunch& A = launch;
+#endif
+  extern __shared__ uint32_t lds[];
+  const LayerDev& L = A.L;
+  const GemmArgs& g = A.g;
+  build_tables<PATH>(L, lds);
+  __syncthreads();
+  const uint32_t ring_area = uni(ring_offset<PATH>(L));
+  uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
+  uint8_t* slab = g.slabs + (uint64_t)blockIdx.x * g.slab_bytes;
+  const uint64_t nvec = (uint64_t)L.rows * L.cvec;
+  const uint32_t RB = g.rows_per_block;
+  for (uint32_t b = blockIdx.x; b < g.n_blocks; b += gridDim.x) {
+    // tiles touching rows [RB b, RB (b + 1)): decoded into the slab, row r at
+    // slab row r - RB b + margin
+    const uint64_t v_first = (uint64_t)b * RB * L.cvec;
+    const uint64_t v_end_b = (uint64_t)(b + 1) * RB * L.cvec;
+    const uint64_t v_end = v_end_b < nvec ? v_end_b : nvec;
+    Hot H = make_hot(L);
+    H.tile_begin = uni((uint32_t)(v_first / L.V));
+    H.tile_end = uni((uint32_t)((v_end + L.V - 1) / L.V));
+    const int64_t shift = ((int64_t)b * RB - (int64_t)g.margin) * (int64_t)L.cols;
+    H.out = uni_ptr(reinterpret_cast<void*>(reinterpret_cast<intptr_t>(slab) - (intptr_t)shift));
+    const uint32_t tasks = (H.tile_end - H.tile_begin + kTilesPerTask - 1) / kTilesPerTask;
+    for (uint32_t task = wave_id(); task < tasks; task += kWavesPerGroup)
+      dispatch_task<PATH, false>(H, lds, lb, ring_area, task, status);
+    __syncthreads();   // the block's rows are in the slab
+    block_product(L, g, slab, b);
+    __syncthreads();   // every wave is done with the slab
+  }
+}
+
 // Prepared stacks: workgroup i builds layer i's decode tables in LDS, exactly as
 // a decode launch would, and writes them to the layer's table image.
 template <int PATH>
@@ -2210,6 +2349,87 @@ int decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_
                        d_status, s, "ep_decode_matmul_i8", true);
 }
 
+// Fused decode and MFMA product: grid, margin rows and slab bytes of a tensor.
+struct GemmGeom {
+  uint32_t groups, margin, n_blocks, rows_per_block;
+  uint64_t slab_bytes;
+};
+
+int gemm_geometry(const ep_tensor_info& I, GemmGeom& G) {
+  DeviceProps P = device_props();
+  if (!P.cus) return fail(EP_ERR_HIP, "ep_decode_gemm_i8: no HIP device");
+  const uint32_t cvec = I.cols / 8;
+  G.margin = (I.tile_vectors - 1 + cvec - 1) / cvec;   // rows a tile reaches past either side
+  // as many blocks as CUs (one round), each of at least one row
+  G.rows_per_block = std::max<uint32_t>(1, (I.rows + (uint32_t)P.cus - 1) / (uint32_t)P.cus);
+  G.rows_per_block = std::min<uint32_t>(G.rows_per_block, 16 * kGemmMaxTiles);   // then several rounds
+  G.n_blocks = (I.rows + G.rows_per_block - 1) / G.rows_per_block;
+  G.groups = std::min<uint32_t>(G.n_blocks, (uint32_t)P.cus);
+  G.slab_bytes = (((uint64_t)G.rows_per_block + 2 * G.margin) * I.cols + 255) & ~255ull;
+  return EP_OK;
+}
+
+uint64_t decode_gemm_workspace(const ep_tensor_info* info) {
+  GemmGeom G;
+  if (!info || gemm_geometry(*info, G)) return 0;
+  return (uint64_t)G.groups * G.slab_bytes;
+}
+
+int decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
+                   int32_t* d_y, float* d_dequant, void* d_ws, uint64_t ws_bytes, int32_t* d_status,
+                   void* stream) {
+  if (!info) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: null info");
+  if (info->container != EP_CONT_INT8_ROW)
+    return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: the tensor is not in the INT8 row container");
+  if (m < 1 || m > 65536) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: m must be 1 .. 65536");
+  if (!d_x || !d_y) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: null X or Y");
+  if (info->cols > 131071)
+    return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: rows longer than 131071 weights may overflow int32");
+  if ((uint64_t)m * info->cols > 0x7FFFFFFFull)
+    return fail(EP_ERR_ARG, "ep_decode_gemm_i8: X above 2^31 bytes");
+  GemmLaunch A;
+  std::memset(&A, 0, sizeof A);
+  int rc = fill_layer(*info, d_blob, EP_INT8, d_y, d_dequant, 0, info->n_tiles, A.L);
+  if (rc) return rc;
+  GemmGeom G;
+  rc = gemm_geometry(*info, G);
+  if (rc) return rc;
+  if (G.slab_bytes > 0x7FFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: rows too long");
+  if (!d_ws || ws_bytes < (uint64_t)G.groups * G.slab_bytes)
+    return fail(EP_ERR_ARG, "ep_decode_gemm_i8: workspace too small");
+  A.g.x = d_x;
+  A.g.y = d_y;
+  A.g.slabs = static_cast<uint8_t*>(d_ws);
+  A.g.slab_bytes = G.slab_bytes;
+  A.g.m = (uint32_t)m;
+  A.g.margin = G.margin;
+  A.g.n_blocks = G.n_blocks;
+  A.g.rows_per_block = G.rows_per_block;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((uint32_t)((m + 15) / 16) < kWavesPerGroup &&   // partial sums are added with atomics
+      hipMemsetAsync(d_y, 0, sizeof(int32_t) * (size_t)m * info->rows, s) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_gemm_i8: clearing Y failed");
+  const uint32_t lds = lds_bytes(info->path, *info);
+  DeviceProps P = device_props();
+  if (lds > P.max_lds) return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: tables exceed the device LDS");
+  const void* fn = info->path == kPathLut ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathLut>)
+                   : info->path == kPathWide ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathWide>)
+                   : info->path == kPathSearch ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathSearch>)
+                                               : reinterpret_cast<const void*>(&decode_gemm_kernel<kPathGlobal>);
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_gemm_i8: cannot raise the kernel's LDS limit");
+  if (info->path == kPathLut)
+    hipLaunchKernelGGL(decode_gemm_kernel<kPathLut>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
+  else if (info->path == kPathWide)
+    hipLaunchKernelGGL(decode_gemm_kernel<kPathWide>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
+  else if (info->path == kPathSearch)
+    hipLaunchKernelGGL(decode_gemm_kernel<kPathSearch>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
+  else
+    hipLaunchKernelGGL(decode_gemm_kernel<kPathGlobal>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
+  if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, "ep_decode_gemm_i8: launch failed");
+  return EP_OK;
+}
+
 uint64_t decode_layers_workspace(int n) {
   return n > kArgLayers ? (uint64_t)n * sizeof(LayerDev) : 0;
 }
@@ -2367,6 +2587,15 @@ int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtyp
 int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int m,
                         int32_t* d_y, float* d_dequant, int32_t* d_status, void* hip_stream) {
   return ep::decode_matmul_i8(info, d_blob, d_x, m, d_y, d_dequant, d_status, hip_stream);
+}
+
+uint64_t ep_decode_gemm_i8_workspace(const ep_tensor_info* info) { return ep::decode_gemm_workspace(info); }
+
+int ep_decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
+                      int32_t* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
+                      int32_t* d_status, void* hip_stream) {
+  return ep::decode_gemm_i8(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
+                            hip_stream);
 }
 
 uint64_t ep_decode_layers_workspace(int n) { return ep::decode_layers_workspace(n); }

@@ -124,3 +124,114 @@ def test_fused_product_rejects_bad_arguments(E, oracle):
     d_blob = torch.from_numpy(blob_int8).cuda()
     assert lib.ep_decode_matmul_i8(E.C.byref(info), d_blob.data_ptr(), None, 1, y.data_ptr(),
                                    None, None, None) == E.ERR_ARG
+
+
+# ---- the fused decode and MFMA product (any number of rows of X) ---------------------
+
+def fused_mfma(E, blob: np.ndarray, x: np.ndarray, twice: bool = False):
+    """(Y, delta, status) of ep_decode_gemm_i8 on the GPU; Y starts as garbage."""
+    info = E.blob_info(blob)
+    d_blob = torch.from_numpy(blob).cuda()
+    d_x = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    m = x.shape[0]
+    y = torch.full((m, info.rows), 7, dtype=torch.int32, device="cuda")
+    dq = torch.zeros(info.rows, dtype=torch.float32, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = E.decode_gemm_i8_workspace(info)
+    d_ws = torch.empty(max(1, ws), dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    for _ in range(2 if twice else 1):
+        E.decode_gemm_i8(info, d_blob.data_ptr(), d_x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
+                         dq.data_ptr(), st.data_ptr(), s)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), dq.cpu().numpy(), int(st.item())
+
+
+MFMA_CASES = [
+    # name, generator, target, encode kwargs, rows of X
+    ("long_rows_m16", lambda: W.ragged_tensor(31, 96, 8 * 1000, scale=0.05), 6.0, {}, 16),
+    ("long_rows_m1", lambda: W.ragged_tensor(32, 40, 8 * 700, scale=0.05), 6.0, {}, 1),
+    ("long_rows_m17", lambda: W.ragged_tensor(33, 50, 8 * 640, scale=0.05), 4.0, {}, 17),
+    ("long_rows_m64", lambda: W.ragged_tensor(34, 72, 8 * 777, scale=0.05), 6.0, {}, 64),
+    ("long_rows_m100", lambda: W.ragged_tensor(35, 33, 8 * 1024, scale=0.05), 6.0, {}, 100),
+    ("long_rows_m256", lambda: W.ragged_tensor(36, 48, 8 * 520, scale=0.05), 6.0, {}, 256),
+    ("long_rows_m300", lambda: W.ragged_tensor(37, 20, 8 * 300, scale=0.05), 6.0, {}, 300),
+    ("short_rows_m40", lambda: W.ragged_tensor(38, 300, 512, scale=0.05), 6.0, {}, 40),
+    ("tiny_rows_m33", lambda: W.ragged_tensor(39, 200, 24, scale=0.05), 6.0, dict(tile_vectors=45), 33),
+    ("ragged_tiles_m20", lambda: W.ragged_tensor(40, 41, 8 * 333, scale=0.05), 5.0, dict(tile_vectors=96), 20),
+    ("b12_search_m48", lambda: W.ragged_tensor(41, 64, 8 * 600, scale=0.05), 6.0, dict(prob_bits=12), 48),
+    ("one_vector_m5", lambda: W.ragged_tensor(42, 1, 8, scale=0.05), 6.0, {}, 5),
+]
+
+
+@pytest.mark.parametrize("name,gen,target,kw,m", MFMA_CASES, ids=[c[0] for c in MFMA_CASES])
+def test_fused_mfma_product_matches_oracle(E, oracle, name, gen, target, kw, m):
+    """Every element of Y against the oracle's decode followed by its exact product: token
+    counts from 1 to 300 (K split over waves below 256 rows of X, whole token tiles above),
+    rows longer and shorter than a tile, blocks of 16 rows cut by tiles, ragged tiles (the
+    generic loop), b = 12 (the search path), and two calls into the same Y."""
+    w = gen()
+    say(f"  fused MFMA {name}: {w.shape} at {target}, m = {m}")
+    blob, _ = oracle.encode(w, target, container=oracle.CONT_INT8, **kw)
+    x = activations(100 + len(name), m, w.shape[1])
+    y_ref, dq_ref = reference(oracle, blob, x)
+    y, dq, st = fused_mfma(E, blob, x, twice=True)
+    assert st == 0
+    assert np.array_equal(y, y_ref)
+    assert np.array_equal(dq, dq_ref)
+
+
+def test_fused_mfma_product_global_table_path(E, oracle):
+    """The same product when the tables are read through the global-table path."""
+    w = W.ragged_tensor(43, 64, 8 * 512, scale=0.05)
+    blob, _ = oracle.encode(w, 6.0, container=oracle.CONT_INT8)
+    x = activations(7, 24, w.shape[1])
+    info = E.blob_info(blob)
+    info.path = 4
+    d_blob = torch.from_numpy(blob).cuda()
+    d_x = torch.from_numpy(x).cuda()
+    y = torch.zeros((24, info.rows), dtype=torch.int32, device="cuda")
+    ws = E.decode_gemm_i8_workspace(info)
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    E.decode_gemm_i8(info, d_blob.data_ptr(), d_x.data_ptr(), 24, y.data_ptr(), d_ws.data_ptr(), ws,
+                     0, st.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert np.array_equal(y.cpu().numpy(), reference(oracle, blob, x)[0])
+
+
+def test_fused_mfma_product_config5_down(E, oracle):
+    """The INT8-container MLP down projection (5120 x 17408, 6.0 bpp) times the first 16, 64
+    and 256 rows of the 8192 x 17408 activations: every element of Y."""
+    w = W.llm_mlp(["down"])["down"]
+    blob, _ = E.encode(w, 6.0, container=E.CONT_INT8_ROW)
+    act = W.llm_activations()
+    w_ref, dq_ref = oracle.decode(blob, oracle.INT8)
+    for m in (16, 64, 256):
+        x = act[:m]
+        say(f"  fused MFMA cfg5: m = {m}")
+        y, dq, st = fused_mfma(E, blob, x)
+        assert st == 0
+        assert np.array_equal(y, oracle.gemm_i8_nt(x, w_ref))
+        assert np.array_equal(dq, dq_ref)
+
+
+def test_fused_mfma_product_rejects_bad_arguments(E, oracle):
+    w = W.ragged_tensor(44, 32, 256, scale=0.05)
+    blob_int8, _ = oracle.encode(w, 6.0, container=oracle.CONT_INT8)
+    blob_fp8, _ = oracle.encode(w, 6.0, container=oracle.CONT_FP8)
+    x = activations(1, 20, 256)
+    d_x = torch.from_numpy(x).cuda()
+    y = torch.zeros((20, 32), dtype=torch.int32, device="cuda")
+    lib = E.lib()
+    info8 = E.blob_info(blob_int8)
+    ws = E.decode_gemm_i8_workspace(info8)
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    for blob, m, wsb, code in ((blob_fp8, 1, ws, E.ERR_UNSUPPORTED), (blob_int8, 0, ws, E.ERR_ARG),
+                               (blob_int8, 20, ws - 1, E.ERR_ARG)):
+        info = E.blob_info(blob)
+        d_blob = torch.from_numpy(blob).cuda()
+        rc = lib.ep_decode_gemm_i8(E.C.byref(info), d_blob.data_ptr(), d_x.data_ptr(), m,
+                                   y.data_ptr(), None, d_ws.data_ptr(), wsb, None, None)
+        assert rc == code
