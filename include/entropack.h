@@ -219,11 +219,14 @@ int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtyp
  * row-major and Y m x R int32 row-major, exact (no rounding, no overflow:
  * C <= 131071).  W' is never written to memory: every decoded vector goes
  * straight into dot products with the m rows of X.  Y is overwritten (cleared
- * on hip_stream first); d_dequant (nullable) receives delta_r for every row.
+ * on hip_stream first by a small fill kernel, not a memset node, so the call
+ * can be captured in a graph); d_dequant (nullable) receives delta_r for every
+ * row.
  * All pointers are device memory owned by the caller; X 8-byte aligned.
  * Asynchronous on hip_stream, no allocation, one clear and one kernel launch.
  * d_status as for ep_decode_tiles.  Meant for few rows of X (decode-time
- * serving); for large batches decode once and call ep_gemm_i8_nt.
+ * serving; it beats decode-then-GEMM up to about 4 rows); for more rows
+ * decode once and call ep_gemm_i8_nt.
  * Errors: EP_ERR_ARG (null pointers, m outside 1..8), EP_ERR_UNSUPPORTED (not
  * the INT8 row container, C > 131071), EP_ERR_HIP. */
 int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int m,
@@ -242,8 +245,8 @@ int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const in
  * last-level cache) and multiplies X by those rows on the matrix cores
  * (v_mfma_i32_16x16x64_i8).  d_workspace: >= ep_decode_gemm_i8_workspace(info)
  * bytes of device memory owned by the caller, untouched until the launch
- * completes.  Y is overwritten (cleared first on hip_stream when m < 256, where
- * partial sums over K are added with atomics).  d_dequant (nullable) receives delta_r for every row; d_status as for
+ * completes.  Y is overwritten (cleared first on hip_stream by a small fill
+ * kernel when m < 256, where partial sums over K are added with atomics).  d_dequant (nullable) receives delta_r for every row; d_status as for
  * ep_decode_tiles.  Asynchronous, no allocation, at most one clear and one launch.
  * Errors: EP_ERR_ARG (null pointers, m outside 1..65536, X above 2^31 bytes, short
  * workspace), EP_ERR_UNSUPPORTED (not the INT8 row container, C > 131071),
@@ -336,7 +339,12 @@ int ep_stack_decode(const ep_stack* stack, int32_t* d_status, void* hip_stream);
  * Appendix B.1.  All pointers are device memory owned by the caller; A and B
  * 16-byte aligned.  Requires M, N > 0, K > 0, K % 16 == 0 and K <= 131071 (each
  * product is at most 2^14 in magnitude, so every int32 sum is exact).
- * Asynchronous on hip_stream.  Errors: EP_ERR_ARG, EP_ERR_HIP. */
+ * Y is overwritten whatever it held.  A launch of few 256 x 256 tiles (at
+ * most half as many as CUs, e.g. few rows of A) splits K over several
+ * workgroups per tile: a small fill kernel clears Y first and the partial
+ * sums are added with atomics (exact, order-independent); calls that overlap
+ * on the same Y then race.  Asynchronous on hip_stream, no allocation, no
+ * memset node (graph capture is safe).  Errors: EP_ERR_ARG, EP_ERR_HIP. */
 int ep_gemm_i8_nt(const int8_t* d_a, const int8_t* d_b, int32_t* d_y, int64_t m, int64_t n,
                   int64_t k, void* hip_stream);
 

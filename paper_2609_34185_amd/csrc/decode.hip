@@ -2089,7 +2089,22 @@ __global__ __launch_bounds__(kThreads) void stack_tables_kernel(const LayerDev* 
   }
 }
 
+// Clears Y before the launches that add partial sums to it.  A kernel rather
+// than hipMemsetAsync, so that a caller may capture the call in a graph.
+__global__ void zero_i32_kernel(int32_t* __restrict__ y, int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    gptr<int32_t>(y)[i] = 0;
+}
+
 // ---- host side ---------------------------------------------------------------------
+bool clear_i32(int32_t* y, int64_t count, hipStream_t s) {
+  if (count <= 0) return true;
+  const unsigned blocks = (unsigned)std::min<int64_t>((count + 255) / 256, 4096);
+  hipLaunchKernelGGL(zero_i32_kernel, dim3(blocks), dim3(256), 0, s, y, count);
+  return hipGetLastError() == hipSuccess;
+}
+
 struct DeviceProps {
   int cus = 0;
   size_t max_lds = 0;
@@ -2342,7 +2357,7 @@ int decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_
   D[0].x = d_x;
   D[0].m = (uint32_t)m;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (hipMemsetAsync(d_y, 0, sizeof(int32_t) * (size_t)m * info->rows, s) != hipSuccess)
+  if (!clear_i32(d_y, (int64_t)m * info->rows, s))
     return fail(EP_ERR_HIP, "ep_decode_matmul_i8: clearing Y failed");
   if (D[0].n_tasks == 0) return EP_OK;
   return launch_layers(info->path, D, D[0].n_tasks, lds_bytes(info->path, *info), nullptr, 0,
@@ -2407,7 +2422,7 @@ int decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t*
   A.g.rows_per_block = G.rows_per_block;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if ((uint32_t)((m + 15) / 16) < kWavesPerGroup &&   // partial sums are added with atomics
-      hipMemsetAsync(d_y, 0, sizeof(int32_t) * (size_t)m * info->rows, s) != hipSuccess)
+      !clear_i32(d_y, (int64_t)m * info->rows, s))
     return fail(EP_ERR_HIP, "ep_decode_gemm_i8: clearing Y failed");
   const uint32_t lds = lds_bytes(info->path, *info);
   DeviceProps P = device_props();

@@ -6,20 +6,23 @@
 // Y; each wave owns 128 x 128 = 4 x 4 blocks of v_mfma_i32_32x32x32_i8 (256
 // accumulator registers), which reads 8 KiB of LDS operands (eight 16-byte
 // fragments per lane) per 32-byte K chunk for 16 MFMAs.  One workgroup per
-// CU, one wave per SIMD.  K is walked in steps of 64 bytes (two chunks).
+// CU, one wave per SIMD.  K is walked in steps of 128 bytes (four chunks).
 //
 // Operands reach LDS by direct loads (buffer_load ... lds: memory to LDS
-// without passing through registers) into four rotating stage buffers, three
-// steps ahead.  Per step s (buffer s mod 4 holds step s):
-//   half A: MFMAs of chunk 0 (fragments already in registers); meanwhile
-//           step s + 3 is requested into the buffer step s - 1 used and the
-//           chunk-1 fragments of step s are read;
+// without passing through registers), one wave instruction per 8 rows x 128
+// bytes, so that eight lanes cover one whole 128-byte line of a row.  (With
+// 64-byte row pieces each line is requested twice, in consecutive steps, and
+// a CU's stream of direct loads runs at about 60 % of the rate it reaches
+// with whole lines.)  Two stage buffers of 64 KiB alternate.  Per step s
+// (buffer s mod 2 holds step s, and step s + 1 is in flight):
+//   chunks 1..3: the MFMAs of chunk c - 1 while the fragments of chunk c are
+//           read;
 //   barrier (this wave's loads of step s + 1 landed, its LDS reads returned);
-//   half B: MFMAs of chunk 1; meanwhile the chunk-0 fragments of step s + 1
-//           are read.
-// The single barrier sits between two MFMA halves whose operands are already
-// in registers, so the matrix pipe does not wait on LDS latency, and it
-// orders every wave's last read of a buffer before the next load into it.
+//   then step s + 2 is requested into buffer s mod 2, which every wave has
+//   finished reading, and the MFMAs of chunk 3 run while the chunk-0
+//   fragments of step s + 1 are read.
+// A step's loads thus have a whole step of MFMAs to land.  The single barrier
+// sits between two MFMA groups whose operands are already in registers.
 // Direct loads are bounded buffer loads: out-of-range chunks land as zeros.
 //
 // Tile order: workgroups are dealt to the 8 XCDs round-robin, so the
@@ -29,11 +32,13 @@
 // would occupy at most half of the CUs, its tiles are issued as twice as many
 // 256 x 128 halves instead, so that round takes about half as long.
 //
-// LDS rows are 64 bytes (four 16-byte chunks) without padding; the chunk j of
-// row r is stored at position j ^ swz(r), with swz a fixed 16-entry table over
-// r mod 16 chosen so that neither the direct loads (16 rows x 64 bytes per
-// wave instruction) nor the fragment reads (32 consecutive rows at one chunk)
-// put two lanes of an LDS cycle on the same bank, for 32 or 64 banks.
+// LDS rows are 128 bytes (eight 16-byte chunks) without padding; the chunk j
+// of row r is stored at position j ^ swz(r), swz(r) = (r mod 8) ^ ((r / 8)
+// mod 2).  Any 8 consecutive rows then hold one chunk in 8 different 16-byte
+// bank groups (32 banks), and any 16 consecutive rows in 16 different groups
+// of a 256-byte bank row (64 banks), so the fragment reads (32 consecutive
+// rows at one chunk) are free of bank conflicts; the direct loads write 1 KiB
+// contiguously.
 //
 // MFMA operand layout (32x32x32, int8): lane l supplies row (l mod 32) of the
 // A block and column (l mod 32) of the B block, 16 consecutive k bytes each,
@@ -42,7 +47,9 @@
 // (8 (r / 4) + 4 (l / 32) + r mod 4, l mod 32) of the 32 x 32 block.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
+#include <type_traits>
 
 #include "../../include/entropack.h"
 #include "common.h"
@@ -53,57 +60,70 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int kTileM = 256, kTileK = 64;
+constexpr int kTileM = 256, kTileK = 128;
 constexpr int kWaveM = 128;                         // per wave: 4 x (TN / 64) blocks of 32 x 32
 constexpr int kBlocksM = kWaveM / 32;
 constexpr int kGemmThreads = 256;
 constexpr int kRowBytes = kTileK;                   // no padding: chunks are swizzled
-constexpr int kABytes = kTileM * kRowBytes;
-constexpr uint32_t kSwizzle = 0x63c99e34u;          // swz(r) = bits [2 (r mod 16), +2)
 
 #define EP_GLOBAL __attribute__((address_space(1)))
 
 constexpr uint32_t kOutside = 0x80000000u;   // operands are limited to 2^31 bytes
 
-__device__ __forceinline__ uint32_t swz(uint32_t r) { return (kSwizzle >> (2 * (r & 15))) & 3; }
+__device__ __forceinline__ uint32_t swz(uint32_t r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
-// Per-thread part of the direct (global -> LDS) load of one K step of the
-// stage: the stage is 16 KiB of A rows then TN / 16 KiB of B rows, cut into
-// 1 KiB segments of 16 rows; one wave instruction fills one segment, lane l
-// writing the 16 bytes at l * 16, i.e. slot (l mod 4) of row l / 4 of the
-// segment, so the lane loads chunk (l mod 4) ^ swz(row) of that row.  Wave w
-// fills segments w + 4 q.
+// Per-thread part of the direct (global -> LDS) loads of one K step: an
+// operand's 128-byte pieces of 256 (A) or TN (B) rows go to one 32 KiB slot,
+// cut into 1 KiB segments of 8 rows; one wave instruction fills one segment,
+// lane l writing the 16 bytes at l * 16, i.e. slot (l mod 8) of row l / 8 of
+// the segment, so the lane loads chunk (l mod 8) ^ swz(row) of that row.
+// Wave w fills segments w + 4 q.
 template <int TN>
-struct StageLoader {
-  static constexpr int kSegs = (kTileM + TN) / 16 / 4;   // per wave
-  uint32_t row_off[kSegs];   // byte offset of the row start in its operand, or kOutside
-  uint32_t chunk;            // byte offset of the lane's chunk within a 64-byte K step
+struct PanelLoader {
+  static constexpr int kSegsA = kTileM / 32, kSegsB = TN / 32;   // per wave
+  uint32_t a_off[kSegsA], b_off[kSegsB];   // byte offset of the row start, or kOutside
+  uint32_t chunk;            // byte offset of the lane's chunk within a 128-byte K step
   uint32_t seg0;             // LDS offset of the wave's first segment
 
   __device__ __forceinline__ void init(int64_t m, int64_t n, int64_t k, int64_t m0, int64_t n0,
                                        int wave, int lane) {
-    const uint32_t r = (uint32_t)lane >> 2;   // row within the segment = row mod 16
-    chunk = 16 * (((uint32_t)lane & 3) ^ swz(r));
+    const uint32_t r = (uint32_t)lane >> 3;   // row within the segment
+    // slot row 8 (wave + 4 q) + r: its value mod 16 is 8 (wave mod 2) + r for every q
+    chunk = 16 * (((uint32_t)lane & 7) ^ swz(8 * ((uint32_t)wave & 1) + r));
     seg0 = 1024 * wave;
 #pragma unroll
-    for (int q = 0; q < kSegs; q++) {
-      const int64_t row = 16 * (wave + 4 * q) + r;   // stage row
-      const bool is_a = q < kTileM / 64;
-      const int64_t g = is_a ? m0 + row : n0 + row - kTileM;
-      row_off[q] = g < (is_a ? m : n) ? (uint32_t)(g * k) : kOutside;
+    for (int q = 0; q < kSegsA; q++) {
+      const int64_t g = m0 + 8 * (wave + 4 * q) + r;
+      a_off[q] = g < m ? (uint32_t)(g * k) : kOutside;
+    }
+#pragma unroll
+    for (int q = 0; q < kSegsB; q++) {
+      const int64_t g = n0 + 8 * (wave + 4 * q) + r;
+      b_off[q] = g < n ? (uint32_t)(g * k) : kOutside;
     }
   }
-  __device__ __forceinline__ void fetch(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                        int64_t k, int64_t k0, lds_u8* stage) const {
+  // segments [Q0, Q1) of the step at K offset k0 into `slot`; bytes at or past
+  // k_end land as zeros
+  template <int Q0, int Q1, int NQ>
+  __device__ __forceinline__ static void fetch(const uint32_t (&off)[NQ], uint32_t chunk, uint32_t seg0,
+                                               __amdgpu_buffer_rsrc_t rsrc, int64_t k_end, int64_t k0,
+                                               lds_u8* slot) {
     const int64_t kk = k0 + chunk;
 #pragma unroll
-    for (int q = 0; q < kSegs; q++) {
-      const uint32_t off = (kk < k && row_off[q] != kOutside) ? row_off[q] + (uint32_t)kk : kOutside;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(q < kTileM / 64 ? ra : rb, stage + seg0 + 4096 * q, 16,
-                                               off, 0, 0, 0);
+    for (int q = Q0; q < Q1; q++) {
+      const uint32_t o = (kk < k_end && off[q] != kOutside) ? off[q] + (uint32_t)kk : kOutside;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, slot + seg0 + 4096 * q, 16, o, 0, 0, 0);
     }
+  }
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void fetch_a(__amdgpu_buffer_rsrc_t ra, int64_t k_end, int64_t k0, lds_u8* slot) const {
+    fetch<Q0, Q1>(a_off, chunk, seg0, ra, k_end, k0, slot);
+  }
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void fetch_b(__amdgpu_buffer_rsrc_t rb, int64_t k_end, int64_t k0, lds_u8* slot) const {
+    fetch<Q0, Q1>(b_off, chunk, seg0, rb, k_end, k0, slot);
   }
 };
 
@@ -142,27 +162,39 @@ __device__ __forceinline__ void tile_of(uint32_t idx, uint32_t tm, uint32_t tn, 
 }
 
 constexpr int kTileN = 256;
-constexpr int kStages = 4;   // LDS stage buffers: loads run kStages - 1 steps ahead
-constexpr int stage_bytes(int tn) { return kABytes + tn * kRowBytes; }   // A tile then B tile
+constexpr int kSlots = 5;                          // LDS ring of operand panels
+constexpr int kSlotBytes = kTileM * kRowBytes;     // 32 KiB: one operand's rows for one K step
+constexpr int kChunks = kTileK / 32;               // 32-byte MFMA K chunks per step
 
-// Y[m0 .. m0 + 256, n0 .. n0 + TN) over all of K; a wave owns 128 x TN / 2.
-template <int TN>
+// Y[m0 .. m0 + 256, n0 .. n0 + TN), summed over K in [k_lo, k_hi) (k_lo a
+// multiple of the 128-byte step); a wave owns 128 x TN / 2.  With ADD the
+// sums are added to Y by atomics (a K range of a split tile), else stored.
+//
+// The ring: slot j mod 5 holds the j-th panel of the sequence A(0), B(0),
+// A(1), B(1), ... (A(t), B(t): the operands' rows for K step t).  Iteration t
+// reads A(t), B(t) and loads B(t + 1), A(t + 2) into the slots of A(t - 1),
+// B(t - 1), which the barrier ending iteration t - 1 released.  Its barrier
+// waits for B(t + 1) (A(t + 1) is older) and lets A(t + 2) stay in flight.
+// Each of the four sections of an iteration runs the MFMAs of one chunk,
+// with the fragment reads of the next chunk and a quarter of the loads
+// between them, so the loads are spread thinly over the whole step: issued
+// in bursts they stall the wave (its SIMD has no other wave to feed the
+// matrix pipe) while the CU's load path drains.
+template <int TN, bool ADD>
 __device__ __forceinline__ void tile_product(const int8_t* a, const int8_t* b, int32_t* y, int64_t m,
                                              int64_t n, int64_t k, int64_t m0, int64_t n0,
-                                             lds_u8* lds) {
+                                             int64_t k_lo, int64_t k_hi, lds_u8* lds) {
   constexpr int kWaveN = TN / 2, kBlocksN = kWaveN / 32;
-  constexpr int kStageBytes = stage_bytes(TN);
   constexpr int kFrags = kBlocksM + kBlocksN, kMfmas = kBlocksM * kBlocksN;
-  constexpr int kSegs = StageLoader<TN>::kSegs;
-  static_assert(kWaveN % 32 == 0 && TN % 64 == 0, "tile width");
-  // half A puts the direct loads behind the first MFMAs and the fragment
-  // reads, kPer at a time, behind the rest
-  static_assert(kSegs < kMfmas && kFrags <= kMfmas, "schedule");
-  constexpr int kPer = (kFrags + kMfmas - kSegs - 1) / (kMfmas - kSegs);
+  using Loader = PanelLoader<TN>;
+  constexpr int kSegsA = Loader::kSegsA, kSegsB = Loader::kSegsB;
+  static_assert(kWaveN % 32 == 0 && TN % 64 == 0 && TN <= kTileM, "tile width");
+  static_assert(kFrags < kMfmas && kSegsB % 2 == 0 && kSegsA % 2 == 0, "schedule");
+  static_assert(kChunks == 4, "an iteration walks four chunks");
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wm = wave >> 1, wn = wave & 1;   // wave's 128 x TN / 2 block of the tile
-  const int64_t steps = (k + kTileK - 1) / kTileK;
+  const int64_t steps = (k_hi - k_lo + kTileK - 1) / kTileK;
 
   v16i acc[kBlocksM][kBlocksN];
 #pragma unroll
@@ -174,26 +206,24 @@ __device__ __forceinline__ void tile_product(const int8_t* a, const int8_t* b, i
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a), (short)0, (int)(m * k), 0x00020000);
   const __amdgpu_buffer_rsrc_t rb =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(b), (short)0, (int)(n * k), 0x00020000);
-  StageLoader<TN> ld;
+  Loader ld;
   ld.init(m, n, k, m0, n0, wave, lane);
 
-  // fragment addresses: row (l mod 32) of each block, chunk (l / 32) of the
-  // 32-byte K chunk, swizzled (row mod 16 = l mod 16 for every block)
+  // fragment addresses: row (l mod 32) of each block, 16-byte chunk 2 c + l / 32
+  // for the 32-byte K chunk c, swizzled (row mod 16 = l mod 16 for every block)
   const uint32_t fr = lane & 31, fh = lane >> 5, fs = swz(lane & 15);
-  const uint32_t fa[2] = {(kWaveM * wm + fr) * kRowBytes + 16 * (fh ^ fs),
-                          (kWaveM * wm + fr) * kRowBytes + 16 * ((2 + fh) ^ fs)};
-  const uint32_t fb[2] = {kABytes + (kWaveN * wn + fr) * kRowBytes + 16 * (fh ^ fs),
-                          kABytes + (kWaveN * wn + fr) * kRowBytes + 16 * ((2 + fh) ^ fs)};
+  const uint32_t fa = (kWaveM * wm + fr) * kRowBytes, fb = (kWaveN * wn + fr) * kRowBytes;
 
-  v4i xa0[kBlocksM], xb0[kBlocksN], xa1[kBlocksM], xb1[kBlocksN];   // chunk-0 / chunk-1 fragments
+  v4i xa0[kBlocksM], xb0[kBlocksN], xa1[kBlocksM], xb1[kBlocksN];   // fragments of two chunks
 
-  auto read_frags = [&](const lds_u8* buf, int kc, v4i* xa, v4i* xb) {
+  auto read_frags = [&](const lds_u8* pa, const lds_u8* pb, int c, v4i* xa, v4i* xb) {
+    const uint32_t o = 16 * ((2 * c + fh) ^ fs);
 #pragma unroll
     for (int i = 0; i < kBlocksM; i++)
-      xa[i] = *reinterpret_cast<const __attribute__((address_space(3))) v4i*>(buf + fa[kc] + 32 * kRowBytes * i);
+      xa[i] = *reinterpret_cast<const __attribute__((address_space(3))) v4i*>(pa + fa + o + 32 * kRowBytes * i);
 #pragma unroll
     for (int j = 0; j < kBlocksN; j++)
-      xb[j] = *reinterpret_cast<const __attribute__((address_space(3))) v4i*>(buf + fb[kc] + 32 * kRowBytes * j);
+      xb[j] = *reinterpret_cast<const __attribute__((address_space(3))) v4i*>(pb + fb + o + 32 * kRowBytes * j);
   };
   auto mfmas = [&](const v4i* xa, const v4i* xb) {
 #pragma unroll
@@ -202,52 +232,63 @@ __device__ __forceinline__ void tile_product(const int8_t* a, const int8_t* b, i
       for (int j = 0; j < kBlocksN; j++)
         acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xa[i], xb[j], acc[i][j], 0, 0, 0);
   };
-  // One step: `cur` holds step s, `nxt` step s + 1 (in flight), `fut` (read
-  // during step s - 1, released by its barrier) receives step s + kStages - 1.
-  auto step = [&](const lds_u8* cur, const lds_u8* nxt, lds_u8* fut, int64_t s) {
-    ld.fetch(ra, rb, k, (s + kStages - 1) * kTileK, fut);
-    read_frags(cur, 1, xa1, xb1);
-    mfmas(xa0, xb0);
+  // one section's order: an MFMA, then a fragment read, until the reads are
+  // out; then an MFMA and its share of the section's L loads.  The reads come
+  // first in program order too: the compiler keeps LDS reads and direct loads
+  // in the order written.
+  auto section = [&](auto loads) {
+    constexpr int L = decltype(loads)::value;
+    constexpr int kPer = (L + kMfmas - kFrags - 1) / (kMfmas - kFrags);
 #pragma unroll
-    for (int r = 0; r < kSegs; r++) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    for (int r = 0; r < kMfmas; r++) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-#pragma unroll
-    for (int r = 0; r < kMfmas - kSegs; r++) {
-      __builtin_amdgcn_sched_group_barrier(0x100, kPer, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-    // every wave's part of step s + 1 has landed, every read of step s is done
-    stage_barrier<(kStages - 2) * kSegs>();
-    read_frags(nxt, 0, xa0, xb0);
-    mfmas(xa1, xb1);
-#pragma unroll
-    for (int r = 0; r < kFrags; r++) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (r < kFrags) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      else if ((r - kFrags) * kPer < L) __builtin_amdgcn_sched_group_barrier(0x020, kPer, 0);
     }
   };
+  using HalfB = std::integral_constant<int, kSegsB / 2>;
+  using HalfA = std::integral_constant<int, kSegsA / 2>;
 
-  lds_u8* const b0 = lds;
-  lds_u8* const b1 = lds + kStageBytes;
-  lds_u8* const b2 = lds + 2 * kStageBytes;
-  lds_u8* const b3 = lds + 3 * kStageBytes;
-  ld.fetch(ra, rb, k, 0, b0);
-  ld.fetch(ra, rb, k, kTileK, b1);
-  ld.fetch(ra, rb, k, 2 * kTileK, b2);
-  stage_barrier<(kStages - 2) * kSegs>();
-  read_frags(b0, 0, xa0, xb0);
+  auto slot = [&](uint32_t j) { return lds + kSlotBytes * (j < kSlots ? j : j - kSlots); };
+  ld.template fetch_a<0, kSegsA>(ra, k_hi, k_lo, slot(0));
+  ld.template fetch_b<0, kSegsB>(rb, k_hi, k_lo, slot(1));
+  ld.template fetch_a<0, kSegsA>(ra, k_hi, k_lo + kTileK, slot(2));
+  stage_barrier<kSegsA>();
+#pragma unroll
+  for (int i = 0; i < kBlocksM; i++) xa1[i] = v4i{};
+#pragma unroll
+  for (int j = 0; j < kBlocksN; j++) xb1[j] = v4i{};
 
-  // Four steps per trip, the buffers rotating; steps past the end (up to
-  // three in the last trip) are zero tiles and add nothing.
-  static_assert(kStages == 4, "the trip below rotates four buffers");
-  for (int64_t s = 0; s < steps; s += 4) {
-    step(b0, b1, b3, s);
-    step(b1, b2, b0, s + 1);
-    step(b2, b3, b1, s + 2);
-    step(b3, b0, b2, s + 3);
+  uint32_t j0 = 0;   // slot of A(t)
+  for (int64_t s = 0; s < steps; s++) {
+    const lds_u8* const pa = slot(j0);
+    const lds_u8* const pb = slot(j0 + 1);
+    lds_u8* const qb = slot(j0 + 3);   // B(s + 1)
+    lds_u8* const qa = slot(j0 + 4);   // A(s + 2)
+    const int64_t kb = k_lo + (s + 1) * kTileK, ka = k_lo + (s + 2) * kTileK;
+    // chunk 3 of step s - 1 (zeros before the first step) while chunk 0 is read
+    read_frags(pa, pb, 0, xa0, xb0);
+    ld.template fetch_b<0, kSegsB / 2>(rb, k_hi, kb, qb);
+    mfmas(xa1, xb1);
+    section(HalfB{});
+    read_frags(pa, pb, 1, xa1, xb1);
+    ld.template fetch_b<kSegsB / 2, kSegsB>(rb, k_hi, kb, qb);
+    mfmas(xa0, xb0);
+    section(HalfB{});
+    read_frags(pa, pb, 2, xa0, xb0);
+    ld.template fetch_a<0, kSegsA / 2>(ra, k_hi, ka, qa);
+    mfmas(xa1, xb1);
+    section(HalfA{});
+    read_frags(pa, pb, 3, xa1, xb1);
+    ld.template fetch_a<kSegsA / 2, kSegsA>(ra, k_hi, ka, qa);
+    mfmas(xa0, xb0);
+    section(HalfA{});
+    // B(s + 1) has landed for this wave and every read of A(s), B(s) is done;
+    // then for every wave
+    stage_barrier<kSegsA>();
+    j0 = j0 + 2 < kSlots ? j0 + 2 : j0 + 2 - kSlots;
   }
+  mfmas(xa1, xb1);                 // chunk 3 of the last step
   __builtin_amdgcn_s_waitcnt(0);   // direct loads still in flight land before the wave ends
 
   const int half = lane >> 5;
@@ -259,7 +300,11 @@ __device__ __forceinline__ void tile_product(const int8_t* a, const int8_t* b, i
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const int64_t row = m0 + kWaveM * wm + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (row < m && col < n) ((EP_GLOBAL int32_t*)y)[row * n + col] = acc[i][j][r];
+        if (row < m && col < n) {
+          EP_GLOBAL int32_t* const p = (EP_GLOBAL int32_t*)y + row * n + col;
+          if (ADD) __hip_atomic_fetch_add(p, acc[i][j][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          else *p = acc[i][j][r];
+        }
       }
     }
 }
@@ -267,26 +312,50 @@ __device__ __forceinline__ void tile_product(const int8_t* a, const int8_t* b, i
 // Workgroups [0, full) take whole 256 x 256 tiles; when the last round of
 // whole tiles would fill at most half the CUs, its `split` tiles are instead
 // taken as 2 * split half-width (256 x 128) tiles by workgroups [full, ..),
-// so that round lasts about half as long.
+// so that round lasts about half as long.  With parts > 1 (a launch of few
+// tiles) each of those units is taken by `parts` workgroups, each summing a
+// range of `part_steps` K steps into Y with atomics (Y cleared before).
+template <bool ADD>
+__device__ __forceinline__ void gemm_unit(const int8_t* a, const int8_t* b, int32_t* y, int64_t m,
+                                          int64_t n, int64_t k, uint32_t tm, uint32_t tn,
+                                          uint32_t full, uint32_t split, uint32_t id, int64_t k_lo,
+                                          int64_t k_hi, lds_u8* lds) {
+  uint32_t ti, tj;
+  if (id < full) {
+    tile_of(xcd_spread(id, full), tm, tn, ti, tj);
+    tile_product<kTileN, ADD>(a, b, y, m, n, k, (int64_t)ti * kTileM, (int64_t)tj * kTileN, k_lo,
+                              k_hi, lds);
+  } else {
+    const uint32_t u = xcd_spread(id - full, 2 * split);
+    tile_of(full + u / 2, tm, tn, ti, tj);
+    tile_product<kTileN / 2, ADD>(a, b, y, m, n, k, (int64_t)ti * kTileM,
+                                  (int64_t)tj * kTileN + (kTileN / 2) * (u & 1), k_lo, k_hi, lds);
+  }
+}
+
 __global__ __launch_bounds__(kGemmThreads) void gemm_i8_nt_kernel(const int8_t* __restrict__ a,
                                                                   const int8_t* __restrict__ b,
                                                                   int32_t* __restrict__ y,
                                                                   int64_t m, int64_t n, int64_t k,
                                                                   uint32_t tm, uint32_t tn,
-                                                                  uint32_t full, uint32_t split) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds_mem[kStages * stage_bytes(kTileN)];
+                                                                  uint32_t full, uint32_t split,
+                                                                  uint32_t parts, uint32_t part_steps) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_mem[kSlots * kSlotBytes];
   lds_u8* const lds = (lds_u8*)lds_mem;
-  const uint32_t id = blockIdx.x;
-  uint32_t ti, tj;
-  if (id < full) {
-    tile_of(xcd_spread(id, full), tm, tn, ti, tj);
-    tile_product<kTileN>(a, b, y, m, n, k, (int64_t)ti * kTileM, (int64_t)tj * kTileN, lds);
+  if (parts == 1) {
+    gemm_unit<false>(a, b, y, m, n, k, tm, tn, full, split, blockIdx.x, 0, k, lds);
   } else {
-    const uint32_t u = xcd_spread(id - full, 2 * split);
-    tile_of(full + u / 2, tm, tn, ti, tj);
-    tile_product<kTileN / 2>(a, b, y, m, n, k, (int64_t)ti * kTileM,
-                             (int64_t)tj * kTileN + (kTileN / 2) * (u & 1), lds);
+    const uint32_t unit = blockIdx.x / parts, part = blockIdx.x % parts;
+    const int64_t k_lo = (int64_t)part * part_steps * kTileK;
+    const int64_t k_hi = k_lo + (int64_t)part_steps * kTileK < k ? k_lo + (int64_t)part_steps * kTileK : k;
+    if (k_lo < k_hi) gemm_unit<true>(a, b, y, m, n, k, tm, tn, full, split, unit, k_lo, k_hi, lds);
   }
+}
+
+__global__ void zero_i32_kernel(int32_t* __restrict__ y, int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    ((EP_GLOBAL int32_t*)y)[i] = 0;
 }
 
 }  // namespace
@@ -312,9 +381,21 @@ extern "C" int ep_gemm_i8_nt(const int8_t* d_a, const int8_t* d_b, int32_t* d_y,
   const int64_t tiles = tm * tn, last = tiles % cus;
   if (tiles + last > 0x7FFFFFFF) return ep::fail(EP_ERR_ARG, "ep_gemm_i8_nt: matrix too large");
   const int64_t split = (last > 0 && 2 * last <= cus) ? last : 0;   // one workgroup per CU
-  hipLaunchKernelGGL(ep::gemm_i8_nt_kernel, dim3((unsigned)(tiles + split)), dim3(ep::kGemmThreads), 0,
-                     static_cast<hipStream_t>(hip_stream), d_a, d_b, d_y, m, n, k, (uint32_t)tm,
-                     (uint32_t)tn, (uint32_t)(tiles - split), (uint32_t)split);
+  // A launch of at most half as many units (whole or half tiles) as CUs splits
+  // K over `parts` workgroups per unit, at least four 128-byte steps each.
+  const int64_t units = tiles + split, steps = (k + ep::kTileK - 1) / ep::kTileK;
+  int64_t parts = 1;
+  if (2 * units <= cus) parts = std::max<int64_t>(1, std::min<int64_t>(cus / units, steps / 4));
+  const int64_t part_steps = (steps + parts - 1) / parts;
+  const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  if (parts > 1) {
+    const int64_t count = m * n;
+    const unsigned blocks = (unsigned)std::min<int64_t>((count + 255) / 256, 4096);
+    hipLaunchKernelGGL(ep::zero_i32_kernel, dim3(blocks), dim3(256), 0, stream, d_y, count);
+  }
+  hipLaunchKernelGGL(ep::gemm_i8_nt_kernel, dim3((unsigned)(units * parts)), dim3(ep::kGemmThreads), 0,
+                     stream, d_a, d_b, d_y, m, n, k, (uint32_t)tm, (uint32_t)tn,
+                     (uint32_t)(tiles - split), (uint32_t)split, (uint32_t)parts, (uint32_t)part_steps);
   if (hipGetLastError() != hipSuccess) return ep::fail(EP_ERR_HIP, "ep_gemm_i8_nt: launch failed");
   return EP_OK;
 }

@@ -41,11 +41,19 @@ def gemm_gpu(E, a: np.ndarray, b: np.ndarray) -> np.ndarray:
 
 
 @pytest.mark.parametrize("m,n,k", [(128, 128, 64), (200, 130, 208), (1, 1, 16), (257, 129, 1024),
-                                   (512, 384, 4096), (4300, 4000, 80), (4096, 2560, 48)])
+                                   (512, 384, 4096), (4300, 4000, 80), (4096, 2560, 48),
+                                   (300, 520, 1168), (2304, 2560, 1168), (2048, 1280, 1936),
+                                   (16, 5120, 17408)])
 def test_gemm_matches_oracle_everywhere(E, oracle, m, n, k):
-    """Every element.  On a 256-CU device the launch takes the small shapes as half-width
-    tiles only, 4300 x 4000 as 256 whole tiles plus 16 tiles split in halves (ragged in
-    m, n and k), and 4096 x 2560 as whole tiles only."""
+    """Every element, with Y filled with -1 beforehand.  On a 256-CU device the launch
+    takes 4300 x 4000 as 256 whole tiles plus 16 tiles split in halves (ragged in m, n and
+    k), 4096 x 2560 as whole tiles only, and 2304 x 2560 as whole tiles plus halves.  K
+    walks in 128-byte steps through a ring of five operand slots; k = 1168 (10 steps, the
+    last partial) wraps it twice.  Launches of at most 128 units (whole or half tiles)
+    split K over several workgroups per unit, whose partial sums meet in Y by atomics after
+    a clear: 257 x 129 (2 parts), 512 x 384 (8), 300 x 520 (2), 2048 x 1280 (3 parts of 6,
+    6 and 4 steps) and the MLP down projection's shape against 16 rows of activations
+    (6 parts of 23 and 21 steps)."""
     rng = np.random.default_rng([11, m, n, k])
     a = rng.integers(-128, 128, (m, k), dtype=np.int8)
     b = rng.integers(-128, 128, (n, k), dtype=np.int8)
