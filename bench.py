@@ -262,10 +262,13 @@ def time_steps(args, step, stream):
 def fused_mfma_bench(args, E, W, threads, m):
     """--workload fused_mfma_m<m>: Y = X W'^T for the INT8-container MLP down projection
     (5120 x 17408 at 6.0 bpp) and the first m rows of the 8192 x 17408 activations by the fused
-    decode and MFMA product (ep_decode_gemm_i8, W' never written as a whole), timed beside
-    decode-then-GEMM (ep_decode_tiles to INT8, then ep_gemm_i8_nt) and beside the product alone
-    on resident decoded weights: the analog of the paper's decode-cost curve over tokens per
-    call (App. A.5, Fig. cost).  The fused Y must equal decode-then-GEMM's Y."""
+    decode and MFMA product (ep_decode_gemm_i8_prepared on a workspace whose tables
+    ep_decode_gemm_i8_prepare built once; W' never written as a whole), timed beside
+    decode-then-GEMM (a prepared one-layer stack decoded to INT8 by ep_stack_decode, then
+    ep_gemm_i8_nt) and beside the product alone on resident decoded weights: the analog of the
+    paper's decode-cost curve over tokens per call (App. A.5, Fig. cost).  The variants that
+    build their tables at every call (ep_decode_gemm_i8, ep_decode_tiles) are timed too.  The
+    fused Y must equal decode-then-GEMM's Y."""
     import numpy as np
     import torch
     w = W.llm_mlp(["down"])["down"]
@@ -282,26 +285,42 @@ def fused_mfma_bench(args, E, W, threads, m):
     d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     s = stream.cuda_stream
+    E.decode_gemm_i8_prepare(info, d_blob.data_ptr(), d_ws.data_ptr(), ws, s)
+    sws = E.stack_workspace(1)
+    d_sws = torch.empty(sws, dtype=torch.uint8, device="cuda")
+    stack = E.stack_prepare([(info, d_blob.data_ptr(), wd.data_ptr(), dq.data_ptr(), E.INT8)],
+                            d_sws.data_ptr(), sws, s)
 
     def fused_step():
+        E.decode_gemm_i8_prepared(info, d_blob.data_ptr(), x.data_ptr(), m, y.data_ptr(),
+                                  d_ws.data_ptr(), ws, dq.data_ptr(), status.data_ptr(), s)
+
+    def fused_built_step():
         E.decode_gemm_i8(info, d_blob.data_ptr(), x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
                          dq.data_ptr(), status.data_ptr(), s)
 
     def decode_step():
+        E.stack_decode(stack, status.data_ptr(), s)
+
+    def decode_tiles_step():
         E.decode_tiles(info, d_blob.data_ptr(), E.INT8, wd.data_ptr(), dq.data_ptr(), 0, info.n_tiles,
                        status.data_ptr(), s)
 
     def gemm_step():
         E.gemm_i8_nt(x.data_ptr(), wd.data_ptr(), y2.data_ptr(), m, info.rows, info.cols, s)
 
-    fused_step()
-    decode_step()
-    gemm_step()
+    for f in (fused_step, decode_step, gemm_step):
+        f()
     torch.cuda.synchronize()
     assert int(status.item()) == 0, "decode reported a corrupt stream"
     assert torch.equal(y, y2), "fused product differs from decode-then-GEMM"
+    fused_built_step()
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2), "fused product (tables built) differs from decode-then-GEMM"
     ms = time_steps(args, fused_step, stream)
+    ms_built = time_steps(args, fused_built_step, stream)
     ms_dec = time_steps(args, decode_step, stream)
+    ms_tiles = time_steps(args, decode_tiles_step, stream)
     ms_gemm = time_steps(args, gemm_step, stream)
     assert int(status.item()) == 0, "decode reported a corrupt stream"
     weights = info.rows * info.cols
@@ -315,6 +334,8 @@ def fused_mfma_bench(args, E, W, threads, m):
                                f"container at 6.0 bpp times X = {m} x 17408 int8 rows, Y int32 exact",
                    "rows_x": m, "weights": weights,
                    "decode_then_gemm_ms": {"decode": ms_dec, "gemm": ms_gemm, "total": ms_dec + ms_gemm},
+                   "tables_built_every_call_ms": {"fused": ms_built, "decode": ms_tiles,
+                                                  "decode_then_gemm": ms_tiles + ms_gemm},
                    "resident_gemm_ms": ms_gemm,
                    "fused_over_decode_then_gemm": ms / (ms_dec + ms_gemm),
                    "overhead_vs_resident_pct": 100.0 * (ms / ms_gemm - 1.0),

@@ -255,9 +255,32 @@ int ep_decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8
                       int32_t* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
                       int32_t* d_status, void* hip_stream);
 
-/* Workspace bytes ep_decode_gemm_i8 needs for a tensor on the current device (one
- * slab per workgroup; 0 if info is null or no device is present). */
+/* Workspace bytes ep_decode_gemm_i8 and ep_decode_gemm_i8_prepared need for a
+ * tensor on the current device: a 128 KiB area for the prepared decode tables, a
+ * layer descriptor, then one slab per workgroup (0 if info is null or no device
+ * is present). */
 uint64_t ep_decode_gemm_i8_workspace(const ep_tensor_info* info);
+
+/* Build the tensor's decode tables (the stage model of Section 3.7, the same
+ * tables every workgroup of ep_decode_gemm_i8 builds in LDS) once, into the
+ * table area of d_workspace, for later ep_decode_gemm_i8_prepared calls: the
+ * serving case, where one weight is multiplied by new rows of X at every step.
+ * d_workspace: >= ep_decode_gemm_i8_workspace(info) bytes of device memory
+ * owned by the caller.  Synchronous: returns after the descriptor copy and the
+ * table-building launch on hip_stream have completed.
+ * Errors: as ep_decode_gemm_i8 (EP_ERR_ARG for a short workspace). */
+int ep_decode_gemm_i8_prepare(const ep_tensor_info* info, const void* d_blob, void* d_workspace,
+                              uint64_t ws_bytes, void* hip_stream);
+
+/* ep_decode_gemm_i8 on a workspace that ep_decode_gemm_i8_prepare filled for this
+ * same blob (d_blob unchanged since, workspace not used for another tensor in
+ * between): every workgroup copies the prepared tables into LDS instead of
+ * building them.  Same arguments, results and errors as ep_decode_gemm_i8; a
+ * workspace prepared for another blob gives undefined values in Y (reads and
+ * writes stay within the blob, X, Y, d_dequant and the workspace). */
+int ep_decode_gemm_i8_prepared(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x,
+                               int64_t m, int32_t* d_y, float* d_dequant, void* d_workspace,
+                               uint64_t ws_bytes, int32_t* d_status, void* hip_stream);
 
 /* One layer of a stack decode. */
 typedef struct {

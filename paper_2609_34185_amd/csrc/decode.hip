@@ -1952,30 +1952,34 @@ struct GemmLaunch {
   GemmArgs g;
 };
 
-// Block b's rows times X, from the slab (row i of the block at slab row
-// margin + i).  A work item is one tile of 16 rows of X against all NT =
-// ceil(RB / 16) tiles of 16 block rows, so each X fragment is loaded once per
-// block; items are dealt to the waves, and when there are fewer items than
-// waves K is split over the idle waves and the partial sums are added with
-// atomics (exact, order-free integer additions).  MFMA
+// The product of one block: a work item is one tile of 16 rows of X against
+// all NT = ceil(RB / 16) tiles of 16 block rows, so each X fragment is loaded
+// once per block; items are dealt to the waves, and when there are fewer items
+// than waves K is split over the idle waves and the partial sums are added
+// with atomics (exact, order-free integer additions).  NT is a template
+// argument so that no load is issued for a tile the block does not have.  MFMA
 // operands: lane l supplies row l mod 16 of the X tile and of the slab tile, 16
 // consecutive bytes of K each (k = 16 (l / 16) + 0..15 of a 64-byte step);
 // accumulator r of lane l is element (4 (l / 16) + r, l mod 16) of a 16 x 16
 // result.
 constexpr uint32_t kGemmMaxTiles = 4;   // NT <= 4: blocks of at most 64 rows
-__device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs& g,
-                                              const uint8_t* slab, uint32_t b) {
+template <uint32_t NT>
+__device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmArgs& g,
+                                                 const uint8_t* slab, uint32_t b) {
   const uint32_t wave = wave_id(), lane = threadIdx.x & 63;
   const uint32_t C = L.cols, m = g.m, RB = g.rows_per_block;
-  const uint32_t T = (m + 15) / 16, NT = (RB + 15) / 16;
+  const uint32_t T = (m + 15) / 16;
   const uint32_t S = T >= kWavesPerGroup ? 1u : kWavesPerGroup / T;   // K slices
   if (T < kWavesPerGroup && wave >= T * S) return;
   const uint32_t slice = T >= kWavesPerGroup ? 0u : wave / T;
   const uint32_t tt0 = T >= kWavesPerGroup ? wave : wave % T;
   const uint32_t tstep = T >= kWavesPerGroup ? kWavesPerGroup : T;
-  constexpr uint32_t kGroup = 2;   // 64-byte K steps per group
-  const uint32_t groups = (C + 64 * kGroup - 1) / (64 * kGroup), gper = (groups + S - 1) / S;
-  const uint32_t k_begin = slice * gper * 64 * kGroup, k_end = min(C, (slice + 1) * gper * 64 * kGroup);
+  // 64-byte K steps per group: two groups' fragments stay within the
+  // registers the decode leaves (2 (1 + NT) kGroup fragments of 4 VGPRs)
+  constexpr uint32_t kGroup = NT <= 2 ? 2 : 1;
+  // slices are cut at 128-byte boundaries whatever the group
+  const uint32_t groups = (C + 127) / 128, gper = (groups + S - 1) / S;
+  const uint32_t k_begin = slice * gper * 128, k_end = min(C, (slice + 1) * gper * 128);
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<int8_t*>(g.x), (short)0, (int)((uint64_t)m * C), 0x00020000);
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
@@ -1983,14 +1987,19 @@ __device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs&
   const uint32_t li = lane & 15, q = lane >> 4;
   const uint32_t row0 = b * RB;
   EP_GLOBAL int32_t* y = gptr<int32_t>(g.y);
+  // one group's fragments: X and the NT slab tiles for kGroup 64-byte K steps
+  struct Frags {
+    v4i_t a[kGroup], w[kGroup][NT];
+  };
   for (uint32_t tt = tt0; tt < T; tt += tstep) {
     const uint32_t tok = 16 * tt + li;
     const uint32_t xrow = tok * C;
-    v4i_t acc[kGemmMaxTiles];
+    v4i_t acc[NT];
 #pragma unroll
-    for (uint32_t c = 0; c < kGemmMaxTiles; c++) acc[c] = v4i_t{0, 0, 0, 0};
-    for (uint32_t k0 = k_begin; k0 < k_end; k0 += 64 * kGroup) {
-      v4i_t a[kGroup], w[kGroup][kGemmMaxTiles];
+    for (uint32_t c = 0; c < NT; c++) acc[c] = v4i_t{0, 0, 0, 0};
+    // bytes at or past k_end read as zeros (bounded buffer loads), so the
+    // prefetch past the slice's end and a partial last group add nothing
+    auto load = [&](uint32_t k0, Frags& f) {
 #pragma unroll
       for (uint32_t u = 0; u < kGroup; u++) {
         const uint32_t kq = k0 + 64 * u + 16 * q;
@@ -1999,32 +2008,57 @@ __device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs&
         const bool in = kq < k_end && tok < m;
         v4i_t av = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(xr, in ? xrow + kq : 0x80000000u, 0, 0);
         if (in && kq + 8 >= C) av[2] = av[3] = 0;
-        a[u] = av;
+        f.a[u] = av;
 #pragma unroll
-        for (uint32_t c = 0; c < kGemmMaxTiles; c++) {
+        for (uint32_t c = 0; c < NT; c++) {
           const uint32_t wrow = (g.margin + 16 * c + li) * C;   // slab offset of the lane's W' row
-          w[u][c] = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(
-              wr, (c < NT && kq < k_end) ? wrow + kq : 0x80000000u, 0, 0);
+          f.w[u][c] = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(
+              wr, kq < k_end ? wrow + kq : 0x80000000u, 0, 0);
         }
       }
+    };
+    auto mma = [&](const Frags& f) {
 #pragma unroll
       for (uint32_t u = 0; u < kGroup; u++)
 #pragma unroll
-        for (uint32_t c = 0; c < kGemmMaxTiles; c++)
-          if (c < NT) acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[u], w[u][c], acc[c], 0, 0, 0);
+        for (uint32_t c = 0; c < NT; c++)
+          acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(f.a[u], f.w[u][c], acc[c], 0, 0, 0);
+    };
+    // two groups in flight: the next group's loads are issued before this
+    // group's MFMAs wait for their operands
+    Frags f0, f1;
+    load(k_begin, f0);
+    for (uint32_t k0 = k_begin; k0 < k_end; k0 += 2 * 64 * kGroup) {
+      load(k0 + 64 * kGroup, f1);
+      mma(f0);
+      if (k0 + 64 * kGroup >= k_end) break;
+      load(k0 + 2 * 64 * kGroup, f0);
+      mma(f1);
     }
 #pragma unroll
-    for (uint32_t c = 0; c < kGemmMaxTiles; c++) {
+    for (uint32_t c = 0; c < NT; c++) {
       const uint32_t rl = 16 * c + li, row = row0 + rl;
 #pragma unroll
       for (uint32_t r = 0; r < 4; r++) {
         const uint32_t t = 16 * tt + 4 * q + r;
-        if (c < NT && t < m && rl < RB && row < L.rows) {
+        if (t < m && rl < RB && row < L.rows) {
           if (S > 1) add_i32(y + (uint64_t)t * L.rows + row, acc[c][r]);
           else y[(uint64_t)t * L.rows + row] = acc[c][r];
         }
       }
     }
+  }
+}
+
+// Block b's rows times X, from the slab (row i of the block at slab row
+// margin + i), for NT = ceil(RB / 16) tiles of 16 block rows.
+__device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs& g,
+                                              const uint8_t* slab, uint32_t b) {
+  switch (uni((g.rows_per_block + 15) / 16)) {
+    case 1: block_product_nt<1>(L, g, slab, b); break;
+    case 2: block_product_nt<2>(L, g, slab, b); break;
+    case 3: block_product_nt<3>(L, g, slab, b); break;
+    default: block_product_nt<4>(L, g, slab, b); break;
   }
 }
 
@@ -2039,7 +2073,8 @@ __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch 
   extern __shared__ uint32_t lds[];
   const LayerDev& L = A.L;
   const GemmArgs& g = A.g;
-  build_tables<PATH>(L, lds);
+  if (L.tables) load_tables<PATH>(L, lds);   // prepared by ep_decode_gemm_i8_prepare
+  else build_tables<PATH>(L, lds);
   __syncthreads();
   const uint32_t ring_area = uni(ring_offset<PATH>(L));
   uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
@@ -2047,14 +2082,17 @@ __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch 
   const uint64_t nvec = (uint64_t)L.rows * L.cvec;
   const uint32_t RB = g.rows_per_block;
   for (uint32_t b = blockIdx.x; b < g.n_blocks; b += gridDim.x) {
-    // tiles touching rows [RB b, RB (b + 1)): decoded into the slab, row r at
-    // slab row r - RB b + margin
+    // tiles touching rows [RB b, RB (b + 1)), widened to whole tasks (task
+    // boundaries at multiples of kTilesPerTask tiles, so that every task but
+    // the tensor's last runs the steady state): decoded into the slab, row r
+    // at slab row r - RB b + margin
     const uint64_t v_first = (uint64_t)b * RB * L.cvec;
     const uint64_t v_end_b = (uint64_t)(b + 1) * RB * L.cvec;
     const uint64_t v_end = v_end_b < nvec ? v_end_b : nvec;
     Hot H = make_hot(L);
-    H.tile_begin = uni((uint32_t)(v_first / L.V));
-    H.tile_end = uni((uint32_t)((v_end + L.V - 1) / L.V));
+    const uint32_t t_end = (uint32_t)((v_end + L.V - 1) / L.V);
+    H.tile_begin = uni((uint32_t)(v_first / L.V) / kTilesPerTask * kTilesPerTask);
+    H.tile_end = uni(min(L.tile_end, (t_end + kTilesPerTask - 1) / kTilesPerTask * kTilesPerTask));
     const int64_t shift = ((int64_t)b * RB - (int64_t)g.margin) * (int64_t)L.cols;
     H.out = uni_ptr(reinterpret_cast<void*>(reinterpret_cast<intptr_t>(slab) - (intptr_t)shift));
     const uint32_t tasks = (H.tile_end - H.tile_begin + kTilesPerTask - 1) / kTilesPerTask;
@@ -2365,6 +2403,15 @@ int decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_
 }
 
 // Fused decode and MFMA product: grid, margin rows and slab bytes of a tensor.
+// A layer's decode tables as built in LDS (ring_offset bytes, at most this).
+constexpr uint64_t kTableImageBytes = 128 * 1024;
+
+// Workspace of the fused MFMA product: the table image that
+// ep_decode_gemm_i8_prepare writes, the layer descriptor the table kernel
+// reads, then one slab per workgroup.
+constexpr uint64_t kGemmDescOffset = kTableImageBytes;
+constexpr uint64_t kGemmSlabsOffset = kGemmDescOffset + ((sizeof(LayerDev) + 255) & ~255ull);
+
 struct GemmGeom {
   uint32_t groups, margin, n_blocks, rows_per_block;
   uint64_t slab_bytes;
@@ -2374,7 +2421,9 @@ int gemm_geometry(const ep_tensor_info& I, GemmGeom& G) {
   DeviceProps P = device_props();
   if (!P.cus) return fail(EP_ERR_HIP, "ep_decode_gemm_i8: no HIP device");
   const uint32_t cvec = I.cols / 8;
-  G.margin = (I.tile_vectors - 1 + cvec - 1) / cvec;   // rows a tile reaches past either side
+  // rows a block's tiles reach past either side: its tile range is widened to
+  // whole tasks of kTilesPerTask tiles
+  G.margin = (kTilesPerTask * I.tile_vectors - 1 + cvec - 1) / cvec;
   // as many blocks as CUs (one round), each of at least one row
   G.rows_per_block = std::max<uint32_t>(1, (I.rows + (uint32_t)P.cus - 1) / (uint32_t)P.cus);
   G.rows_per_block = std::min<uint32_t>(G.rows_per_block, 16 * kGemmMaxTiles);   // then several rounds
@@ -2387,34 +2436,70 @@ int gemm_geometry(const ep_tensor_info& I, GemmGeom& G) {
 uint64_t decode_gemm_workspace(const ep_tensor_info* info) {
   GemmGeom G;
   if (!info || gemm_geometry(*info, G)) return 0;
-  return (uint64_t)G.groups * G.slab_bytes;
+  return kGemmSlabsOffset + (uint64_t)G.groups * G.slab_bytes;
 }
 
-int decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
-                   int32_t* d_y, float* d_dequant, void* d_ws, uint64_t ws_bytes, int32_t* d_status,
-                   void* stream) {
-  if (!info) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: null info");
+// Checks shared by the fused product's entry points.
+int gemm_checks(const ep_tensor_info* info, const char* who) {
+  if (!info) return fail(EP_ERR_ARG, who);
   if (info->container != EP_CONT_INT8_ROW)
     return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: the tensor is not in the INT8 row container");
-  if (m < 1 || m > 65536) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: m must be 1 .. 65536");
-  if (!d_x || !d_y) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: null X or Y");
   if (info->cols > 131071)
     return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: rows longer than 131071 weights may overflow int32");
+  return EP_OK;
+}
+
+int decode_gemm_prepare(const ep_tensor_info* info, const void* d_blob, void* d_ws, uint64_t ws_bytes,
+                        void* stream) {
+  int rc = gemm_checks(info, "ep_decode_gemm_i8_prepare: null info");
+  if (rc) return rc;
+  if (!d_ws || ws_bytes < decode_gemm_workspace(info))
+    return fail(EP_ERR_ARG, "ep_decode_gemm_i8_prepare: workspace too small");
+  LayerDev D;
+  // the output pointer is never used by the table build
+  rc = fill_layer(*info, d_blob, EP_INT8, d_ws, nullptr, 0, info->n_tiles, D);
+  if (rc) return rc;
+  uint8_t* ws = static_cast<uint8_t*>(d_ws);
+  D.tables = ws;
+  const uint32_t lds = lds_bytes(info->path, *info);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (hipMemcpyAsync(ws + kGemmDescOffset, &D, sizeof D, hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_gemm_i8_prepare: descriptor copy failed");
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(&stack_tables_kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_gemm_i8_prepare: cannot raise the table kernel's LDS limit");
+  hipLaunchKernelGGL(stack_tables_kernel, dim3(1), dim3(kThreads), lds, s,
+                     reinterpret_cast<const LayerDev*>(ws + kGemmDescOffset));
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+    return fail(EP_ERR_HIP, "ep_decode_gemm_i8_prepare: building the decode tables failed");
+  return EP_OK;
+}
+
+// prepared: the workspace holds this tensor's tables (ep_decode_gemm_i8_prepare)
+int decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
+                   int32_t* d_y, float* d_dequant, void* d_ws, uint64_t ws_bytes, int32_t* d_status,
+                   void* stream, bool prepared) {
+  int rc = gemm_checks(info, "ep_decode_gemm_i8: null info");
+  if (rc) return rc;
+  if (m < 1 || m > 65536) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: m must be 1 .. 65536");
+  if (!d_x || !d_y) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: null X or Y");
   if ((uint64_t)m * info->cols > 0x7FFFFFFFull)
     return fail(EP_ERR_ARG, "ep_decode_gemm_i8: X above 2^31 bytes");
   GemmLaunch A;
   std::memset(&A, 0, sizeof A);
-  int rc = fill_layer(*info, d_blob, EP_INT8, d_y, d_dequant, 0, info->n_tiles, A.L);
+  rc = fill_layer(*info, d_blob, EP_INT8, d_y, d_dequant, 0, info->n_tiles, A.L);
   if (rc) return rc;
   GemmGeom G;
   rc = gemm_geometry(*info, G);
   if (rc) return rc;
   if (G.slab_bytes > 0x7FFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: rows too long");
-  if (!d_ws || ws_bytes < (uint64_t)G.groups * G.slab_bytes)
+  if (!d_ws || ws_bytes < decode_gemm_workspace(info))
     return fail(EP_ERR_ARG, "ep_decode_gemm_i8: workspace too small");
+  uint8_t* ws = static_cast<uint8_t*>(d_ws);
+  A.L.tables = prepared ? ws : nullptr;
   A.g.x = d_x;
   A.g.y = d_y;
-  A.g.slabs = static_cast<uint8_t*>(d_ws);
+  A.g.slabs = ws + kGemmSlabsOffset;
   A.g.slab_bytes = G.slab_bytes;
   A.g.m = (uint32_t)m;
   A.g.margin = G.margin;
@@ -2535,7 +2620,6 @@ int decode_layers_noalloc(const ep_layer* layers, int n, int32_t* d_status, void
 
 // Workspace of a prepared stack: the n descriptors, then one table image per layer
 // (every path's tables fit 128 KiB).
-constexpr uint64_t kTableImageBytes = 128 * 1024;
 uint64_t stack_tables_offset(int n) { return ((uint64_t)n * sizeof(LayerDev) + 255) & ~255ull; }
 uint64_t stack_workspace(int n) {
   return n > 0 ? stack_tables_offset(n) + (uint64_t)n * kTableImageBytes : 0;
@@ -2606,11 +2690,23 @@ int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const in
 
 uint64_t ep_decode_gemm_i8_workspace(const ep_tensor_info* info) { return ep::decode_gemm_workspace(info); }
 
+int ep_decode_gemm_i8_prepare(const ep_tensor_info* info, const void* d_blob, void* d_workspace,
+                              uint64_t ws_bytes, void* hip_stream) {
+  return ep::decode_gemm_prepare(info, d_blob, d_workspace, ws_bytes, hip_stream);
+}
+
+int ep_decode_gemm_i8_prepared(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x,
+                               int64_t m, int32_t* d_y, float* d_dequant, void* d_workspace,
+                               uint64_t ws_bytes, int32_t* d_status, void* hip_stream) {
+  return ep::decode_gemm_i8(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
+                            hip_stream, true);
+}
+
 int ep_decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
                       int32_t* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
                       int32_t* d_status, void* hip_stream) {
   return ep::decode_gemm_i8(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
-                            hip_stream);
+                            hip_stream, false);
 }
 
 uint64_t ep_decode_layers_workspace(int n) { return ep::decode_layers_workspace(n); }

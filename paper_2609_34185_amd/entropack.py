@@ -115,6 +115,9 @@ def lib():
         L.ep_gemm_i8_nt.argtypes = [vp, vp, vp, i64, i64, i64, vp]
         L.ep_decode_matmul_i8.argtypes = [C.POINTER(TensorInfo), vp, vp, C.c_int, vp, vp, vp, vp]
         L.ep_decode_gemm_i8.argtypes = [C.POINTER(TensorInfo), vp, vp, i64, vp, vp, vp, u64, vp, vp]
+        L.ep_decode_gemm_i8_prepared.argtypes = [C.POINTER(TensorInfo), vp, vp, i64, vp, vp, vp, u64,
+                                                 vp, vp]
+        L.ep_decode_gemm_i8_prepare.argtypes = [C.POINTER(TensorInfo), vp, vp, u64, vp]
         L.ep_decode_gemm_i8_workspace.argtypes = [C.POINTER(TensorInfo)]
         L.ep_decode_gemm_i8_workspace.restype = u64
         L.ep_last_error.restype = C.c_char_p
@@ -127,6 +130,7 @@ EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_encode_gpu", "ep_blo
            "ep_decode_layers_noalloc",
            "ep_stack_workspace", "ep_stack_prepare", "ep_stack_decode", "ep_gemm_i8_nt",
            "ep_decode_matmul_i8", "ep_decode_gemm_i8", "ep_decode_gemm_i8_workspace",
+           "ep_decode_gemm_i8_prepare", "ep_decode_gemm_i8_prepared",
            "ep_last_error"]
 
 
@@ -260,6 +264,20 @@ def decode_gemm_i8(info: TensorInfo, d_blob: int, d_x: int, m: int, d_y: int, d_
     on the matrix cores, for any m (the fused decode and MFMA product)."""
     _check(lib().ep_decode_gemm_i8(C.byref(info), d_blob, d_x, m, d_y, d_dequant or None, d_ws,
                                    ws_bytes, d_status or None, stream or None), "ep_decode_gemm_i8")
+
+
+def decode_gemm_i8_prepare(info: TensorInfo, d_blob: int, d_ws: int, ws_bytes: int, stream: int = 0):
+    """Build the tensor's decode tables once into the workspace (synchronous)."""
+    _check(lib().ep_decode_gemm_i8_prepare(C.byref(info), d_blob, d_ws, ws_bytes, stream or None),
+           "ep_decode_gemm_i8_prepare")
+
+
+def decode_gemm_i8_prepared(info: TensorInfo, d_blob: int, d_x: int, m: int, d_y: int, d_ws: int,
+                            ws_bytes: int, d_dequant: int = 0, d_status: int = 0, stream: int = 0):
+    """decode_gemm_i8 on a workspace that decode_gemm_i8_prepare filled for this blob."""
+    _check(lib().ep_decode_gemm_i8_prepared(C.byref(info), d_blob, d_x, m, d_y, d_dequant or None,
+                                            d_ws, ws_bytes, d_status or None, stream or None),
+           "ep_decode_gemm_i8_prepared")
 
 
 # ---- torch conveniences (device memory and streams only) ------------------------

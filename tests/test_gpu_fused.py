@@ -128,9 +128,14 @@ def test_fused_product_rejects_bad_arguments(E, oracle):
 
 # ---- the fused decode and MFMA product (any number of rows of X) ---------------------
 
-def fused_mfma(E, blob: np.ndarray, x: np.ndarray, twice: bool = False):
-    """(Y, delta, status) of ep_decode_gemm_i8 on the GPU; Y starts as garbage."""
+def fused_mfma(E, blob: np.ndarray, x: np.ndarray, twice: bool = False, prepared: bool = False,
+               path: int = 0):
+    """(Y, delta, status) of ep_decode_gemm_i8 on the GPU; Y starts as garbage.  With
+    `prepared`, ep_decode_gemm_i8_prepare first builds the tables into the workspace and
+    ep_decode_gemm_i8_prepared runs on it."""
     info = E.blob_info(blob)
+    if path:
+        info.path = path
     d_blob = torch.from_numpy(blob).cuda()
     d_x = torch.from_numpy(np.ascontiguousarray(x)).cuda()
     m = x.shape[0]
@@ -138,11 +143,15 @@ def fused_mfma(E, blob: np.ndarray, x: np.ndarray, twice: bool = False):
     dq = torch.zeros(info.rows, dtype=torch.float32, device="cuda")
     st = torch.zeros(1, dtype=torch.int32, device="cuda")
     ws = E.decode_gemm_i8_workspace(info)
-    d_ws = torch.empty(max(1, ws), dtype=torch.uint8, device="cuda")
+    d_ws = torch.full((max(1, ws),), 0xA5, dtype=torch.uint8, device="cuda")
     s = torch.cuda.current_stream().cuda_stream
+    run = E.decode_gemm_i8
+    if prepared:
+        E.decode_gemm_i8_prepare(info, d_blob.data_ptr(), d_ws.data_ptr(), ws, s)
+        run = E.decode_gemm_i8_prepared
     for _ in range(2 if twice else 1):
-        E.decode_gemm_i8(info, d_blob.data_ptr(), d_x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
-                         dq.data_ptr(), st.data_ptr(), s)
+        run(info, d_blob.data_ptr(), d_x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
+            dq.data_ptr(), st.data_ptr(), s)
     torch.cuda.synchronize()
     return y.cpu().numpy(), dq.cpu().numpy(), int(st.item())
 
@@ -164,54 +173,49 @@ MFMA_CASES = [
 ]
 
 
+@pytest.mark.parametrize("prepared", [False, True], ids=["tables_built", "tables_prepared"])
 @pytest.mark.parametrize("name,gen,target,kw,m", MFMA_CASES, ids=[c[0] for c in MFMA_CASES])
-def test_fused_mfma_product_matches_oracle(E, oracle, name, gen, target, kw, m):
+def test_fused_mfma_product_matches_oracle(E, oracle, name, gen, target, kw, m, prepared):
     """Every element of Y against the oracle's decode followed by its exact product: token
     counts from 1 to 300 (K split over waves below 256 rows of X, whole token tiles above),
     rows longer and shorter than a tile, blocks of 16 rows cut by tiles, ragged tiles (the
-    generic loop), b = 12 (the search path), and two calls into the same Y."""
+    generic loop), b = 12 (the search path), and two calls into the same Y; with the tables
+    built in every workgroup and copied from a prepared workspace."""
     w = gen()
-    say(f"  fused MFMA {name}: {w.shape} at {target}, m = {m}")
+    say(f"  fused MFMA {name}: {w.shape} at {target}, m = {m}, prepared = {prepared}")
     blob, _ = oracle.encode(w, target, container=oracle.CONT_INT8, **kw)
     x = activations(100 + len(name), m, w.shape[1])
     y_ref, dq_ref = reference(oracle, blob, x)
-    y, dq, st = fused_mfma(E, blob, x, twice=True)
+    y, dq, st = fused_mfma(E, blob, x, twice=True, prepared=prepared)
     assert st == 0
     assert np.array_equal(y, y_ref)
     assert np.array_equal(dq, dq_ref)
 
 
-def test_fused_mfma_product_global_table_path(E, oracle):
+@pytest.mark.parametrize("prepared", [False, True], ids=["tables_built", "tables_prepared"])
+def test_fused_mfma_product_global_table_path(E, oracle, prepared):
     """The same product when the tables are read through the global-table path."""
     w = W.ragged_tensor(43, 64, 8 * 512, scale=0.05)
     blob, _ = oracle.encode(w, 6.0, container=oracle.CONT_INT8)
     x = activations(7, 24, w.shape[1])
-    info = E.blob_info(blob)
-    info.path = 4
-    d_blob = torch.from_numpy(blob).cuda()
-    d_x = torch.from_numpy(x).cuda()
-    y = torch.zeros((24, info.rows), dtype=torch.int32, device="cuda")
-    ws = E.decode_gemm_i8_workspace(info)
-    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
-    st = torch.zeros(1, dtype=torch.int32, device="cuda")
-    E.decode_gemm_i8(info, d_blob.data_ptr(), d_x.data_ptr(), 24, y.data_ptr(), d_ws.data_ptr(), ws,
-                     0, st.data_ptr(), torch.cuda.current_stream().cuda_stream)
-    torch.cuda.synchronize()
-    assert int(st.item()) == 0
-    assert np.array_equal(y.cpu().numpy(), reference(oracle, blob, x)[0])
+    y_ref, dq_ref = reference(oracle, blob, x)
+    y, dq, st = fused_mfma(E, blob, x, prepared=prepared, path=4)
+    assert st == 0
+    assert np.array_equal(y, y_ref)
+    assert np.array_equal(dq, dq_ref)
 
 
 def test_fused_mfma_product_config5_down(E, oracle):
-    """The INT8-container MLP down projection (5120 x 17408, 6.0 bpp) times the first 16, 64
+    """The INT8-container MLP down projection (5120 x 17408, 6.0 bpp) times the first 1, 16, 64
     and 256 rows of the 8192 x 17408 activations: every element of Y."""
     w = W.llm_mlp(["down"])["down"]
     blob, _ = E.encode(w, 6.0, container=E.CONT_INT8_ROW)
     act = W.llm_activations()
     w_ref, dq_ref = oracle.decode(blob, oracle.INT8)
-    for m in (16, 64, 256):
+    for m, prepared in ((1, True), (16, False), (16, True), (64, True), (256, False)):
         x = act[:m]
-        say(f"  fused MFMA cfg5: m = {m}")
-        y, dq, st = fused_mfma(E, blob, x)
+        say(f"  fused MFMA cfg5: m = {m}, prepared = {prepared}")
+        y, dq, st = fused_mfma(E, blob, x, prepared=prepared)
         assert st == 0
         assert np.array_equal(y, oracle.gemm_i8_nt(x, w_ref))
         assert np.array_equal(dq, dq_ref)
@@ -235,3 +239,10 @@ def test_fused_mfma_product_rejects_bad_arguments(E, oracle):
         rc = lib.ep_decode_gemm_i8(E.C.byref(info), d_blob.data_ptr(), d_x.data_ptr(), m,
                                    y.data_ptr(), None, d_ws.data_ptr(), wsb, None, None)
         assert rc == code
+        rc = lib.ep_decode_gemm_i8_prepared(E.C.byref(info), d_blob.data_ptr(), d_x.data_ptr(), m,
+                                            y.data_ptr(), None, d_ws.data_ptr(), wsb, None, None)
+        assert rc == code
+        if m:
+            rc = lib.ep_decode_gemm_i8_prepare(E.C.byref(info), d_blob.data_ptr(), d_ws.data_ptr(),
+                                               wsb, None)
+            assert rc == code

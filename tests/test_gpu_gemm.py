@@ -81,7 +81,8 @@ def test_gemm_rejects_bad_arguments(E):
 
 def test_config5_decode_then_gemm(E, oracle):
     """Decode the INT8-container down projection on the GPU, multiply by the activations on
-    MFMA, and compare sampled rows with the oracle's product of the oracle-decoded weights."""
+    MFMA, and compare sampled rows with the oracle's product of the oracle-decoded weights,
+    then every element with an independent library GEMM."""
     say("  cfg5: generating and encoding the down projection (INT8 container, 6.0 bpp)")
     w = W.llm_mlp(["down"])["down"]
     blob, _ = E.encode(w, 6.0, container=E.CONT_INT8_ROW)
@@ -105,3 +106,10 @@ def test_config5_decode_then_gemm(E, oracle):
     ref = oracle.gemm_i8_nt(act, ref_w, rows=rows)
     got = y[torch.from_numpy(rows).cuda()].cpu().numpy()
     assert np.array_equal(got, ref)
+    # every element against an independent GEMM (the vendor library behind torch._int_mm,
+    # used only as a checker here): int32 sums of int8 products are exact in both
+    if hasattr(torch, "_int_mm"):
+        say("  cfg5: all of Y against torch._int_mm")
+        ind = torch._int_mm(d_act, out.view(torch.int8).t())
+        torch.cuda.synchronize()
+        assert torch.equal(ind, y)
