@@ -197,6 +197,13 @@ typedef struct {
 int ep_blob_info(const void* host_blob, uint64_t n, ep_tensor_info* info);
 
 /* ---- GPU decode ---------------------------------------------------------- */
+/* Work mapping (every decode entry point): a wave decodes four tiles at a time
+ * (two interleaved rANS chains, each over two tiles).  A launch with fewer than
+ * 2048 such tasks whose layers all take the same slot-table path at b = 11 runs
+ * two-tile tasks instead (one chain per wave): small layers then spread over
+ * twice as many waves.  The environment variable EP_SMALL_TASK_LIMIT, read at
+ * each call, replaces the 2048 (0: always four-tile tasks).  The outputs do
+ * not depend on the choice. */
 /* Decode tiles [tile_begin, tile_end) of one tensor (Section 3.7: eq.
  * rans_decode, eq. point_inverse, eq. recon).  d_out receives R x C
  * elements of out_dtype (row-major); only the elements of the given tiles are

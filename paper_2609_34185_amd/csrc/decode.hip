@@ -30,6 +30,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstdint>
 #include <cstring>
 #include <mutex>
@@ -90,6 +91,7 @@ struct LayerDev {
   const int8_t* x;                // fused product: X (m x cols, row-major), Y in `out`
   uint32_t m;
   uint32_t path;                  // decode path of the layer (DecodePath)
+  uint32_t tpt;                   // tiles per task: 4 (two chains per wave) or 2 (one chain)
   uint32_t g_bits, g_meta;        // global-table path: log2 G, byte offset of its metadata
   const uint8_t* tables;          // prepared stacks: the layer's decode tables as built in LDS
                                   // (ring_offset bytes), copied in instead of rebuilt; or null
@@ -111,6 +113,7 @@ struct Hot {
   uint32_t m, cols;
   uint32_t g_bits, g_meta;        // global-table path: log2 G, u32 index of the metadata
   uint32_t tab_bytes;             // end of the tables section (bounds of their loads)
+  uint32_t tpt;                   // tiles per task (LayerDev::tpt)
 };
 
 __device__ __forceinline__ uint32_t uni(uint32_t v) {
@@ -160,6 +163,7 @@ __device__ __forceinline__ Hot make_hot(const LayerDev& L) {
   H.g_bits = uni(L.g_bits);
   H.g_meta = uni(L.g_meta / 4);
   H.tab_bytes = uni((uint32_t)L.off_sigma);
+  H.tpt = uni(L.tpt);
   return H;
 }
 
@@ -1222,6 +1226,118 @@ __device__ __forceinline__ void coset_step2(uint32_t& x0, uint32_t& x1, uint32_t
       : EP_STEP_CLOBBERS);
 }
 
+// ---- one chain per wave (small launches) ----------------------------------------
+// The same steps for a wave that advances a single chain (two tiles, one per
+// half): each step's instructions are chain 0's of the two-chain steps.  A
+// wave alone on its SIMD issues about one instruction per four cycles, so a
+// launch with too few tasks to put several waves on every SIMD finishes
+// sooner when each wave issues half the instructions per symbol and there are
+// twice as many waves.
+#define EP_REFILL_ONE_W(WORK)                                               \
+  "v_cmp_gt_u32_e32 vcc, 0x8000, %[x0]\n\t"                                 \
+  "s_bcnt1_i32_b32 %[c0lo], vcc_lo\n\t"                                    \
+  "v_mbcnt_lo_u32_b32 %[t0], vcc_lo, 0\n\t"                                 \
+  "s_bcnt1_i32_b32 %[c0hi], vcc_hi\n\t"                                    \
+  "v_mbcnt_hi_u32_b32 %[t0], vcc_hi, %[t0]\n\t"                             \
+  "s_sub_u32 %[d0], %[D0], %[c0lo]\n\t"                                    \
+  "v_mad_i32_i24 %[t0], %[vH], %[d0], %[t0]\n\t"                            \
+  "v_add_lshl_u32 %[t0], %[t0], %[SA0], 1\n\t"                              \
+  "v_and_or_b32 %[t0], %[t0], %[rmask], %[vrb0]\n\t"                        \
+  "ds_read_u16 %[w0], %[t0]\n\t"                                            \
+  "s_add_u32 %[SA0], %[SA0], %[c0lo]\n\t"                                  \
+  "s_setprio 0\n\t"                                                        \
+  "s_add_u32 %[D0], %[d0], %[c0hi]\n\t"                                  \
+  WORK                                                                     \
+  "s_and_saveexec_b64 %[ex], vcc\n\t"                                       \
+  "s_waitcnt lgkmcnt(0)\n\t"                                                \
+  "v_lshl_or_b32 %[x0], %[x0], 16, %[w0]\n\t"                               \
+  "s_mov_b64 exec, %[ex]\n\t"
+
+#define EP_STEP1_OUTS                                                                    \
+  [x0] "+v"(x0), [SA0] "+s"(F0.OA), [D0] "+s"(F0.D), [u0] "=&v"(u0), [g0] "=&v"(g0),   \
+      [t0] "=&v"(t0), [w0] "=&v"(w0), [c0lo] "=&s"(c0lo), [c0hi] "=&s"(c0hi),           \
+      [d0] "=&s"(dd0), [ex] "=&s"(ex)
+
+#define EP_STEP1_TEMPS                                                                   \
+  uint32_t u0, g0, t0, w0, c0lo, c0hi, dd0;                                              \
+  uint64_t ex
+
+#define EP_STEP1_INS                                                                     \
+  [vH] "v"(vH), [vrb0] "v"(vrb0), [rmask] "s"(kFastRingBytes - 1), [mk] "i"((1 << B) - 1), \
+      [b] "i"(B)
+
+#define EP_STEP1_CLOBBERS "vcc", "scc", "exec", "memory"
+
+#define EP_Y_CVT1                                                                     \
+  "v_cvt_f32_i32_sdwa %[y0], sext(%[e0]) dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3\n\t" \
+  "v_fma_f32 %[y0], %[sg0], %[y0], %[hc0]\n\t"
+#define EP_Y_CVT1_WIDE                                                                \
+  "v_ashrrev_i32 %[y0], 22, %[e0]\n\t"                                                \
+  "v_cvt_f32_i32_e32 %[y0], %[y0]\n\t"                                                \
+  "v_fma_f32 %[y0], %[sg0], %[y0], %[hc0]\n\t"
+#define EP_Y_SAT1 "v_med3_f32 %[y0], %[y0], %[nm], %[m]\n\t"
+#define EP_Y_PAR1 "v_and_or_b32 %[e0], %[X0], %[bit], %[e0]\n\t"
+
+#define EP_FIELD1_ASM(DEC0, WORK)                                                        \
+  asm volatile(                                                                          \
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"                                                \
+      "v_lshl_add_u32 %[u0], %[u0], 2, %[cb0]\n\t"                                       \
+      "ds_read_b32 %[e0], %[u0] offset:%[off]\n\t"                                       \
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"                                             \
+      "s_waitcnt lgkmcnt(0)\n\t"                                                         \
+      "s_setprio 2\n\t"                                                                  \
+      DEC0                                                                               \
+      EP_REFILL_ONE_W(WORK)                                                              \
+      : EP_STEP1_OUTS, [e0] "=&v"(e0), [y0] "=&v"(y0)                                    \
+      : [cb0] "v"(cb0), [off] "i"((FIELD - 1) * (4 << B)), [sg0] "v"(sg0), [hc0] "v"(hc0), \
+        [m] "s"(m), [nm] "v"(-m), [X0] "v"(X0), [bit] "s"(zbit), EP_STEP1_INS            \
+      : EP_STEP1_CLOBBERS)
+
+// Field symbol of the single chain (see field_step2).
+template <int B, int FIELD, int YM, bool WIDE>
+__device__ __forceinline__ void field_step1(uint32_t& x0, uint32_t cb0, uint32_t& e0, float& y0,
+                                            float sg0, float hc0, uint32_t X0, float m, FastChain& F0,
+                                            uint32_t vH, uint32_t vrb0) {
+  EP_STEP1_TEMPS;
+  const uint32_t zbit = 1u << (WIDE ? 22 : 24);   // low bit of the entry's z
+  if constexpr (WIDE) {
+    if constexpr (YM == 0) EP_FIELD1_ASM(EP_DEC_WIDE(0), "");
+    else if constexpr (FIELD == 8 && YM == 1) EP_FIELD1_ASM(EP_DEC_WIDE(0), EP_Y_PAR1 EP_Y_CVT1_WIDE);
+    else if constexpr (FIELD == 8) EP_FIELD1_ASM(EP_DEC_WIDE(0), EP_Y_PAR1 EP_Y_CVT1_WIDE EP_Y_SAT1);
+    else if constexpr (YM == 1) EP_FIELD1_ASM(EP_DEC_WIDE(0), EP_Y_CVT1_WIDE);
+    else EP_FIELD1_ASM(EP_DEC_WIDE(0), EP_Y_CVT1_WIDE EP_Y_SAT1);
+  } else {
+    if constexpr (YM == 0) EP_FIELD1_ASM(EP_DEC(0), "");
+    else if constexpr (FIELD == 8 && YM == 1) EP_FIELD1_ASM(EP_DEC(0), EP_Y_PAR1 EP_Y_CVT1);
+    else if constexpr (FIELD == 8) EP_FIELD1_ASM(EP_DEC(0), EP_Y_PAR1 EP_Y_CVT1 EP_Y_SAT1);
+    else if constexpr (YM == 1) EP_FIELD1_ASM(EP_DEC(0), EP_Y_CVT1);
+    else EP_FIELD1_ASM(EP_DEC(0), EP_Y_CVT1 EP_Y_SAT1);
+  }
+}
+
+// Coset symbol of the single chain (see coset_step2).
+template <int B>
+__device__ __forceinline__ void coset_step1(uint32_t& x0, uint32_t& cb0, float& hc0, float sg0,
+                                            uint32_t vf0, uint32_t vf1, uint32_t vcb, FastChain& F0,
+                                            uint32_t vH, uint32_t vrb0) {
+  EP_STEP1_TEMPS;
+  asm volatile(
+      "v_and_b32 %[u0], %[mk], %[x0]\n\t"
+      "v_lshrrev_b32 %[g0], %[b], %[x0]\n\t"
+      "v_cmp_le_u32_e32 vcc, %[vf0], %[u0]\n\t"
+      "v_cndmask_b32_e32 %[w0], %[vf0], %[vf1], vcc\n\t"
+      "v_cndmask_b32_e32 %[t0], 0, %[vf0], vcc\n\t"
+      "v_cndmask_b32_e32 %[cb0], 0, %[vcb], vcc\n\t"
+      "v_mad_u32_u24 %[x0], %[w0], %[g0], %[u0]\n\t"
+      "v_mul_f32_e32 %[w0], 0.5, %[sg0]\n\t"
+      "v_cndmask_b32_e32 %[hc0], 0, %[w0], vcc\n\t"
+      "v_sub_u32_e32 %[x0], %[x0], %[t0]\n\t"
+      EP_REFILL_ONE_W("")
+      : EP_STEP1_OUTS, [cb0] "=&v"(cb0), [hc0] "=&v"(hc0)
+      : [vf0] "v"(vf0), [vf1] "v"(vf1), [vcb] "v"(vcb), [sg0] "v"(sg0), EP_STEP1_INS
+      : EP_STEP1_CLOBBERS);
+}
+
 __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
   uint32_t r;
   asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "v"(c));
@@ -1581,10 +1697,123 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
   if (err && status) atomicOr(status, (int32_t)err);
 }
 
-template <int B, int DT, bool SAT, bool WIDE>
+// The slot-table steady state with one chain: a task of two tiles, t0 in
+// lanes 0-31 and t0 + 1 in lanes 32-63, for launches with too few four-tile
+// tasks to fill the SIMDs (see field_step1).  Decoded outputs only (no fused
+// product).  The structure is lut_task's with the second chain removed.
+template <int B, int DT, bool SAT, bool TWO, bool WIDE>
+__device__ __forceinline__ void lut_task1(const Hot& L, uint8_t* lds, uint32_t ring_area, uint32_t t0,
+                                          int32_t* status) {
+  static_assert(DT != kOutDotI8, "one-chain tasks decode only");
+  const uint32_t lane = threadIdx.x & 63, wave = wave_id();
+  const uint32_t half = lane >> 5, l = lane & 31;
+  const EP_GLOBAL uint32_t* states = gptr<const uint32_t>(L.blob + L.off_states);
+  const EP_GLOBAL uint32_t* offs = gptr<const uint32_t>(L.blob + L.off_offsets);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_payload), (short)0, (int)L.pay_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(L.blob + L.off_sigma), (short)0, (int)(4 * L.rows), 0x00020000);
+  constexpr uint32_t VB = vec_bytes<DT>();
+  constexpr int YM = DT == EP_COORD2_I32 ? 0 : SAT ? 2 : 1;
+  const float ymax = DT == EP_FP8_E4M3 ? 448.0f : DT == EP_FP8_E5M2 ? 57344.0f
+                     : DT == EP_FP16 ? 65504.0f : 3.38953139e38f;
+
+  // the wave's first ring (the two-chain layout's chain 0)
+  const uint32_t vrb0 = ring_area + wave * 2 * kFastChainBytes + half * kFastRingBytes;
+  const uint32_t vl8 = 8 * l;
+  uint32_t o[3];
+#pragma unroll
+  for (int i = 0; i < 3; i++) o[i] = offs[t0 + i];
+  const uint32_t tile = t0 + half;
+  uint32_t x = states[(uint64_t)tile * 32 + l];
+  const uint32_t vb = tile * L.V + l;
+  const uint32_t voff = (half * L.V + l) * VB;
+  uint32_t kc = 0;
+  float sa = 0.0f, sb = 0.0f;
+  if constexpr (TWO) {
+    const uint32_t r = row_of(L, vb);
+    kc = ((r + 1) * L.cvec - vb + 31) >> 5;
+    sa = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r, 0, 0));
+    sb = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r + 4, 0, 0));
+  }
+  FastChain F0;
+  u32x2 pend0, pendB0;
+#pragma unroll
+  for (int i = 0; i < 3; i++) o[i] = uni(o[i]);
+  const u32x4 fill0 = fast_start(F0, pend0, rsrc, half, l, o[0], o[1], o[1], o[2]);
+  __builtin_amdgcn_s_waitcnt(0);
+  *reinterpret_cast<u32x4*>(lds + vrb0 + 16 * l) = fill0;
+  pendB0 = pend0;   // pend0 serves lanes 0-31, pendB0 lanes 32-63
+
+  EP_GLOBAL uint8_t* obase = gptr<uint8_t>(L.out) + (uint64_t)t0 * L.V * VB;
+  const uint32_t vH = half;
+  const uint32_t vf0 = L.coset_f0, vf1 = L.coset_f1, vcb = 32u << B;
+  // full rounds, then a partial one with the states of lanes past the tile
+  // pinned (see lut_task)
+  const uint32_t full = L.V / 32, tail = L.V % 32;
+  const uint32_t vrb08 = vrb0 + vl8;
+  uint32_t xsave = 0;
+  const bool pin = l >= tail;
+
+  auto round = [&](uint32_t k, auto part) {
+    constexpr bool PART = decltype(part)::value;
+    if constexpr (PART) xsave = x;
+    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, kFastRingWords - kFastBlockWords + 1);
+    float sg;
+    if constexpr (TWO) sg = k < kc ? sa : sb;
+    else sg = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row_of(L, vb + 32 * k), 0, 0));
+    uint32_t cb, e0;
+    float y0, hc;
+    QAcc acc;
+    acc.X = 0;
+#define EP_PIN1                       \
+  if constexpr (PART) x = pin ? kPinnedState : x;
+    EP_PIN1
+    coset_step1<B>(x, cb, hc, sg, vf0, vf1, vcb, F0, vH, vrb0);
+#define EP_FIELD(I)                                                                        \
+  EP_PIN1                                                                                  \
+  field_step1<B, I, YM, WIDE>(x, cb, e0, y0, sg, hc, acc.X, ymax, F0, vH, vrb0);           \
+  q_take<DT, I, WIDE>(acc, e0, y0, cb >> (B + 5));
+    EP_FIELD(1) EP_FIELD(2)
+    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
+    EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
+    fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
+    EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
+#undef EP_FIELD
+#undef EP_PIN1
+    if (!PART || !pin) q_put<DT>(obase, voff, acc);
+    obase += 32 * VB;
+  };
+  for (uint32_t k = 0; k < full; k++) round(k, std::false_type{});
+  if (tail) {
+    round(full, std::true_type{});
+    x = pin ? xsave : x;
+  }
+
+  uint32_t err = 0;
+  if (x != kStateLow) err |= EP_STATUS_BAD_FINAL_STATE;
+  const uint32_t P = half ? F0.OA + F0.D : F0.OA, E = half ? F0.EB : F0.EA;
+  if (l == 0 && P != E) err |= P > E ? EP_STATUS_PAYLOAD_OVERRUN : EP_STATUS_BAD_END_OFFSET;
+  if (L.container && L.dequant) {
+    const EP_GLOBAL float* delta = gptr<const float>(L.blob + L.off_delta);
+    const uint32_t v0 = tile * L.V;
+    const uint32_t r_first = (v0 + L.cvec - 1) / L.cvec;
+    const uint32_t r_last = (v0 + L.V - 1) / L.cvec;
+    for (uint32_t r = r_first + l; r <= r_last; r += 32) gptr<float>(L.dequant)[r] = delta[r];
+  }
+  if (err && status) atomicOr(status, (int32_t)err);
+}
+
+// NCH: chains per wave (2: a four-tile task, 1: a two-tile task).
+template <int B, int DT, bool SAT, bool WIDE, int NCH = 2>
 __device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                               uint32_t t0, int32_t* status) {
-  if constexpr (DT == kOutDotI8) {
+  static_assert(NCH == 2 || DT == EP_BF16 || DT == EP_FP16 || DT == EP_FP8_E4M3 || DT == EP_INT8,
+                "one-chain tasks cover the common output types");
+  if constexpr (NCH == 1) {
+    if (L.cvec >= 32 * ((L.V - 1) / 32)) lut_task1<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
+    else lut_task1<B, DT, SAT, false, WIDE>(L, lds, ring_area, t0, status);
+  } else if constexpr (DT == kOutDotI8) {
     if (L.cvec >= L.V) {
       if (L.m <= 1) lut_task<B, DT, false, true, WIDE, 1>(L, lds, ring_area, t0, status);
       else if (L.m <= 2) lut_task<B, DT, false, true, WIDE, 2>(L, lds, ring_area, t0, status);
@@ -1601,38 +1830,61 @@ __device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32
   }
 }
 
-// Output-type dispatch of a full four-tile slot-table task (narrow or wide
-// entries).  Returns false for the combinations the steady state does not
-// cover (they take the generic loop).
-template <int B, bool WIDE, bool DOT = false>
+// Output-type dispatch of a full slot-table task (narrow or wide entries;
+// four tiles, or two with NCH = 1).  Returns false for the combinations the
+// steady state does not cover (they take the generic loop).
+template <int B, bool WIDE, bool DOT = false, int NCH = 2>
 __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                              uint32_t t0, int32_t* status) {
   if constexpr (DOT) {
+    static_assert(NCH == 2, "the fused product runs four-tile tasks");
     lut_task_rows<B, kOutDotI8, false, WIDE>(L, lds, ring_area, t0, status);
     return true;
   }
-  switch (L.out_dtype) {
-    case EP_BF16:
-      if (L.saturate) lut_task_rows<B, EP_BF16, true, WIDE>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_BF16, false, WIDE>(L, lds, ring_area, t0, status);
-      return true;
-    case EP_FP16:
-      if (L.saturate) lut_task_rows<B, EP_FP16, true, WIDE>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_FP16, false, WIDE>(L, lds, ring_area, t0, status);
-      return true;
-    case EP_FP8_E4M3:
-      if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true, WIDE>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_FP8_E4M3, false, WIDE>(L, lds, ring_area, t0, status);
-      return true;
-    case EP_FP8_E5M2:
-      if (L.saturate) lut_task_rows<B, EP_FP8_E5M2, true, WIDE>(L, lds, ring_area, t0, status);
-      else lut_task_rows<B, EP_FP8_E5M2, false, WIDE>(L, lds, ring_area, t0, status);
-      return true;
-    case EP_INT8: lut_task_rows<B, EP_INT8, false, WIDE>(L, lds, ring_area, t0, status); return true;
-    case EP_UINT8: lut_task_rows<B, EP_UINT8, false, WIDE>(L, lds, ring_area, t0, status); return true;
-    case EP_FP32: lut_task_rows<B, EP_FP32, false, WIDE>(L, lds, ring_area, t0, status); return true;
-    case EP_COORD2_I32: lut_task_rows<B, EP_COORD2_I32, false, WIDE>(L, lds, ring_area, t0, status); return true;
-    default: return false;
+  if constexpr (NCH == 1) {
+    // the output types small layers are decoded to; the rest take the generic loop
+    switch (L.out_dtype) {
+      case EP_BF16:
+        if (L.saturate) lut_task_rows<B, EP_BF16, true, WIDE, 1>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_BF16, false, WIDE, 1>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_FP16:
+        if (L.saturate) lut_task_rows<B, EP_FP16, true, WIDE, 1>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_FP16, false, WIDE, 1>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_FP8_E4M3:
+        if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true, WIDE, 1>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_FP8_E4M3, false, WIDE, 1>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_INT8: lut_task_rows<B, EP_INT8, false, WIDE, 1>(L, lds, ring_area, t0, status); return true;
+      default: return false;
+    }
+  } else {
+    switch (L.out_dtype) {
+      case EP_BF16:
+        if (L.saturate) lut_task_rows<B, EP_BF16, true, WIDE, NCH>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_BF16, false, WIDE, NCH>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_FP16:
+        if (L.saturate) lut_task_rows<B, EP_FP16, true, WIDE, NCH>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_FP16, false, WIDE, NCH>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_FP8_E4M3:
+        if (L.saturate) lut_task_rows<B, EP_FP8_E4M3, true, WIDE, NCH>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_FP8_E4M3, false, WIDE, NCH>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_FP8_E5M2:
+        if (L.saturate) lut_task_rows<B, EP_FP8_E5M2, true, WIDE, NCH>(L, lds, ring_area, t0, status);
+        else lut_task_rows<B, EP_FP8_E5M2, false, WIDE, NCH>(L, lds, ring_area, t0, status);
+        return true;
+      case EP_INT8: lut_task_rows<B, EP_INT8, false, WIDE, NCH>(L, lds, ring_area, t0, status); return true;
+      case EP_UINT8: lut_task_rows<B, EP_UINT8, false, WIDE, NCH>(L, lds, ring_area, t0, status); return true;
+      case EP_FP32: lut_task_rows<B, EP_FP32, false, WIDE, NCH>(L, lds, ring_area, t0, status); return true;
+      case EP_COORD2_I32:
+        lut_task_rows<B, EP_COORD2_I32, false, WIDE, NCH>(L, lds, ring_area, t0, status);
+        return true;
+      default: return false;
+    }
   }
 }
 
@@ -1777,11 +2029,25 @@ constexpr uint32_t kTilesPerTask = 4;
 static_assert(kChains == 2, "the generic loop and the search steady state advance two chains");
 static_assert(kTilesPerTask == 2 * kChains, "task granularity: one four-tile pass");
 
-template <int PATH, int B, bool DOT>
+// SMALL: the kernel may run two-tile tasks (see use_small_tasks).
+template <int PATH, int B, bool DOT, bool SMALL>
 __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                        uint32_t ring_area, uint32_t task, int32_t* status) {
-  const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
   const uint32_t nvec = L.rows * L.cvec;
+  if constexpr (SMALL && !DOT && (PATH == kPathLut || PATH == kPathWide) && B == 11) {
+    if (L.tpt == 2) {
+      // two-tile tasks, one chain per wave
+      const uint32_t t0 = L.tile_begin + 2 * task;
+      const bool whole = t0 + 2 <= L.tile_end && (uint64_t)(t0 + 2) * L.V <= nvec;
+      if (whole && L.V >= 32 && L.pay_bytes < kFastOob &&
+          lut_task_any<B, PATH == kPathWide, false, 1>(L, lb, ring_area, t0, status))
+        return;
+      if (whole && L.V % 32 == 0) decode_task<PATH, B, 1, true, DOT>(L, tab, lb, ring_area, task, status);
+      else decode_task<PATH, B, 1, false, DOT>(L, tab, lb, ring_area, task, status);
+      return;
+    }
+  }
+  const uint32_t t0 = L.tile_begin + kTilesPerTask * task;
   const bool whole = t0 + kTilesPerTask <= L.tile_end && (uint64_t)(t0 + kTilesPerTask) * L.V <= nvec;
   const bool full = whole && L.V % 32 == 0;   // every lane has a vector in every round
   // The slot-table steady state also takes tiles of any length V >= 32 (a
@@ -1800,13 +2066,13 @@ __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_
   else decode_task<PATH, B, kChains, false, DOT>(L, tab, lb, ring_area, task, status);
 }
 
-template <int PATH, bool DOT>
+template <int PATH, bool DOT, bool SMALL = false>
 __device__ __forceinline__ void dispatch_task(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                               uint32_t ring_area, uint32_t task, int32_t* status) {
-  if (PATH == kPathSearch || PATH == kPathGlobal) task_b<PATH, 0, DOT>(L, tab, lb, ring_area, task, status);
-  else if (L.b == 11) task_b<PATH, 11, DOT>(L, tab, lb, ring_area, task, status);
-  else if (L.b == 10) task_b<PATH, 10, DOT>(L, tab, lb, ring_area, task, status);
-  else task_b<PATH, 9, DOT>(L, tab, lb, ring_area, task, status);
+  if (PATH == kPathSearch || PATH == kPathGlobal) task_b<PATH, 0, DOT, SMALL>(L, tab, lb, ring_area, task, status);
+  else if (L.b == 11) task_b<PATH, 11, DOT, SMALL>(L, tab, lb, ring_area, task, status);
+  else if (L.b == 10) task_b<PATH, 10, DOT, SMALL>(L, tab, lb, ring_area, task, status);
+  else task_b<PATH, 9, DOT, SMALL>(L, tab, lb, ring_area, task, status);
 }
 
 // Decode global tasks [t_begin, t_end) of a layer list: per layer segment the
@@ -1831,7 +2097,7 @@ __device__ __forceinline__ void load_tables(const LayerDev& L, uint32_t* lds) {
 
 // One layer segment of a workgroup: build (or copy) the layer's tables, then
 // the waves take tasks [seg, seg_end) in turn.
-template <int PATH, bool DOT>
+template <int PATH, bool DOT, bool SMALL = false>
 __device__ __forceinline__ void run_segment(const LayerDev& L, uint32_t* lds, uint32_t seg,
                                             uint32_t seg_end, int32_t* status) {
   if (L.tables) load_tables<PATH>(L, lds);
@@ -1842,7 +2108,7 @@ __device__ __forceinline__ void run_segment(const LayerDev& L, uint32_t* lds, ui
   const Hot H = make_hot(L);
   uint8_t* lb = reinterpret_cast<uint8_t*>(lds);
   for (uint32_t task = seg + wave_id(); task < seg_end; task += kWavesPerGroup)
-    dispatch_task<PATH, DOT>(H, lds, lb, ring_area, task - first, status);
+    dispatch_task<PATH, DOT, SMALL>(H, lds, lb, ring_area, task - first, status);
 }
 
 // A layer list whose layers take different decode paths: each segment runs
@@ -1874,7 +2140,8 @@ __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers,
         default: run_segment<kPathGlobal, DOT>(L, lds, seg, seg_end, status); break;
       }
     } else {
-      run_segment<PATH, DOT>(L, lds, seg, seg_end, status);
+      // the mixed-path kernel never runs two-tile tasks (use_small_tasks)
+      run_segment<PATH, DOT, !DOT>(L, lds, seg, seg_end, status);
     }
     seg = seg_end;
   }
@@ -2214,6 +2481,7 @@ int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void*
   D.container = I.container;
   D.tile_begin = t0;
   D.tile_end = t1;
+  D.tpt = kTilesPerTask;
   D.n_tasks = (t1 - t0 + kTilesPerTask - 1) / kTilesPerTask;
   D.out_dtype = (uint32_t)out_dtype;
   D.saturate = I.max_abs_weight >= dtype_max(out_dtype) ? 1u : 0u;
@@ -2365,14 +2633,47 @@ int launch_layers(uint32_t path, const std::vector<LayerDev>& D, uint32_t total,
   return EP_OK;
 }
 
+// A launch of fewer four-tile tasks than this runs two-tile tasks (one chain
+// per wave) when every layer takes the same slot-table path at b = 11: twice
+// as many waves, each issuing half the instructions per symbol (see
+// field_step1).  The environment variable EP_SMALL_TASK_LIMIT overrides the
+// limit (0: always four-tile tasks).
+constexpr uint32_t kSmallLaunchTasks = 2048;
+
+uint32_t small_task_limit() {
+  const char* e = std::getenv("EP_SMALL_TASK_LIMIT");
+  if (!e || !*e) return kSmallLaunchTasks;
+  char* end = nullptr;
+  const unsigned long v = std::strtoul(e, &end, 10);
+  return (end && *end == 0 && v <= 0xFFFFFFFFul) ? (uint32_t)v : kSmallLaunchTasks;
+}
+
+void use_small_tasks(std::vector<LayerDev>& D, uint32_t& total) {
+  if (total == 0 || total >= small_task_limit()) return;
+  for (const LayerDev& d : D)
+    if ((d.path != kPathLut && d.path != kPathWide) || d.path != D[0].path || d.out_dtype == kOutDotI8 ||
+        d.b != 11)
+      return;
+  uint32_t tasks = 0;
+  for (LayerDev& d : D) {
+    d.tpt = 2;
+    d.n_tasks = (d.tile_end - d.tile_begin + 1) / 2;
+    d.task_begin = tasks;
+    tasks += d.n_tasks;
+  }
+  total = tasks;
+}
+
 int decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtype, void* d_out,
                  float* d_dequant, uint32_t t0, uint32_t t1, int32_t* d_status, void* stream) {
   if (!info) return fail(EP_ERR_ARG, "ep_decode_tiles: null info");
   std::vector<LayerDev> D(1);
   int rc = fill_layer(*info, d_blob, out_dtype, d_out, d_dequant, t0, t1, D[0]);
   if (rc) return rc;
-  if (D[0].n_tasks == 0) return EP_OK;
-  return launch_layers(info->path, D, D[0].n_tasks, lds_bytes(info->path, *info), nullptr, 0,
+  uint32_t total = D[0].n_tasks;
+  use_small_tasks(D, total);
+  if (total == 0) return EP_OK;
+  return launch_layers(info->path, D, total, lds_bytes(info->path, *info), nullptr, 0,
                        d_status, static_cast<hipStream_t>(stream), "ep_decode_tiles");
 }
 
@@ -2556,6 +2857,7 @@ int describe_layers(const ep_layer* layers, int n, const char* who, std::vector<
   }
   if (tasks > 0xFFFFFFFFull) return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": too many tiles").c_str());
   total = (uint32_t)tasks;
+  use_small_tasks(D, total);
   return EP_OK;
 }
 

@@ -32,6 +32,31 @@ def E():
     return entropack
 
 
+# Launches of few four-tile tasks run two-tile tasks (one chain per wave) unless
+# EP_SMALL_TASK_LIMIT says otherwise; the small-size tests below run both ways.
+TASKS = ["one_chain", "two_chain"]
+
+
+class task_mode:
+    """Context: "two_chain" sets EP_SMALL_TASK_LIMIT=0 (always four-tile tasks)."""
+
+    def __init__(self, mode):
+        self.mode = mode
+
+    def __enter__(self):
+        self.old = os.environ.get("EP_SMALL_TASK_LIMIT")
+        if self.mode == "two_chain":
+            os.environ["EP_SMALL_TASK_LIMIT"] = "0"
+        else:
+            os.environ.pop("EP_SMALL_TASK_LIMIT", None)
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("EP_SMALL_TASK_LIMIT", None)
+        else:
+            os.environ["EP_SMALL_TASK_LIMIT"] = self.old
+
+
 def codes(E, oracle, name):
     return {"COORD2": (E.COORD2_I32, oracle.COORD2), "BF16": (E.BF16, oracle.BF16),
             "FP16": (E.FP16, oracle.FP16), "FP32": (E.FP32, oracle.FP32),
@@ -81,15 +106,20 @@ def test_config1_all_dtypes_search_path(E, oracle):
     assert info.path == 2
 
 
-def test_config1_all_dtypes_lut_path(E, oracle):
+@pytest.mark.parametrize("tasks", TASKS)
+def test_config1_all_dtypes_lut_path(E, oracle, tasks):
     blob, st = oracle.encode(W.single_linear(), 4.0, prob_bits=11)
-    info = check_blob(E, oracle, blob, tag="cfg1-b11")
+    with task_mode(tasks):
+        info = check_blob(E, oracle, blob, tag=f"cfg1-b11 {tasks}")
     assert info.path == 1
 
 
-def test_config2_fp16_bf16(E, oracle):
+@pytest.mark.parametrize("tasks", TASKS)
+def test_config2_fp16_bf16(E, oracle, tasks):
     blob, st = oracle.encode(W.attention_projection(), 3.0)
-    check_blob(E, oracle, blob, dtypes=["COORD2", "FP16", "BF16"], tag="cfg2")
+    with task_mode(tasks):
+        check_blob(E, oracle, blob, dtypes=["COORD2", "FP16", "BF16", "FP8", "INT8"],
+                   tag=f"cfg2 {tasks}")
 
 
 @pytest.mark.parametrize("b", [9, 10, 11, 12, 13, 14, 15])
@@ -145,7 +175,9 @@ def test_wide_slot_entries(E, oracle, b):
         info = E.blob_info(blob)
         say(f"    {rows}x{cols} b={info.prob_bits} coord2 [{info.coord2_min}, {info.coord2_max}]")
         assert info.path == 3, (info.prob_bits, info.coord2_min, info.coord2_max)
-        check_blob(E, oracle, blob, tag=f"wide{b}")
+        for tasks in TASKS if b == 11 else TASKS[:1]:
+            with task_mode(tasks):
+                check_blob(E, oracle, blob, tag=f"wide{b} {tasks}")
 
 
 def escalated_blobs(oracle):
@@ -211,18 +243,23 @@ def test_decode_refuses_a_path_that_cannot_hold_the_tables(E, oracle):
     assert ei.value.code == E.ERR_ARG
 
 
+@pytest.mark.parametrize("tasks", TASKS)
 @pytest.mark.parametrize("shape,V", [((1, 8), 512), ((3, 24), 32), ((7, 400), 45),
                                      ((33, 264), 512), ((130, 72), 100), ((300, 8), 33),
-                                     ((65, 1000), 77), ((1, 4096), 1)])
-def test_ragged_shapes_and_tiles(E, oracle, shape, V):
+                                     ((65, 1000), 77), ((1, 4096), 1), ((5, 1024), 64)])
+def test_ragged_shapes_and_tiles(E, oracle, shape, V, tasks):
+    """Tensors of one tile to a few hundred, ragged last tiles and odd tile counts (a two-tile
+    task with one tile, a four-tile task with one to three)."""
     w = W.ragged_tensor(8, *shape)
     blob, st = oracle.encode(w, 3.0, tile_vectors=V)
-    check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "FP8"], tag=f"V{V}")
+    with task_mode(tasks):
+        check_blob(E, oracle, blob, dtypes=["COORD2", "BF16", "FP8"], tag=f"V{V} {tasks}")
 
 
+@pytest.mark.parametrize("tasks", TASKS)
 @pytest.mark.parametrize("shape,V", [((400, 136), 45), ((200, 520), 77), ((120, 1024), 100),
                                      ((64, 2048), 33)])
-def test_partial_last_round_in_the_steady_state(E, oracle, shape, V):
+def test_partial_last_round_in_the_steady_state(E, oracle, shape, V, tasks):
     """Tiles whose length is not a multiple of 32 vectors run the slot-table steady state with
     a partial last round; a lane's vectors then lie 32 (ceil(V / 32) - 1) vectors apart, so
     with rows of 17, 65, 128 and 256 vectors they span up to three rows, and the row scale
@@ -231,11 +268,13 @@ def test_partial_last_round_in_the_steady_state(E, oracle, shape, V):
     blob, st = oracle.encode(w, 4.0, tile_vectors=V)
     info = E.blob_info(blob)
     assert info.prob_bits == 11 and info.path in (1, 3)
-    check_blob(E, oracle, blob, tag=f"partial V{V}")
+    with task_mode(tasks):
+        check_blob(E, oracle, blob, tag=f"partial V{V} {tasks}")
 
 
+@pytest.mark.parametrize("tasks", TASKS)
 @pytest.mark.parametrize("V", [455, 1820])
-def test_paper_tile_sizes_at_full_size(E, oracle, V):
+def test_paper_tile_sizes_at_full_size(E, oracle, V, tasks):
     """The paper's default tile sizes of 4096 and 16384 symbols (Table tileoverhead: 455 and
     1820 vectors, not multiples of 32) on the reference-layer shape 10240 x 3840 at 4.0 bpp,
     decoded at full size to BF16 and to doubled coordinates: every element equals the oracle.
@@ -247,7 +286,8 @@ def test_paper_tile_sizes_at_full_size(E, oracle, V):
     info = E.blob_info(blob)
     assert info.tile_vectors == V and info.path in (1, 3) and info.prob_bits == 11
     say(f"    V={V}: {info.n_tiles} tiles, {st['rate_stored']:.4f} bpp, path {info.path}")
-    check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"V{V}")
+    with task_mode(tasks):
+        check_blob(E, oracle, blob, dtypes=["COORD2", "BF16"], tag=f"V{V} {tasks}")
 
 
 def test_tile_ranges_write_only_their_tiles(E, oracle):
@@ -282,15 +322,18 @@ def test_degenerate_tensors(E, oracle):
     check_blob(E, oracle, blob, dtypes=["COORD2", "FP16"], tag="const")
 
 
-def test_saturation(E, oracle):
+@pytest.mark.parametrize("tasks", TASKS)
+def test_saturation(E, oracle, tasks):
     rng = np.random.default_rng(4)
     w = (rng.standard_normal((32, 256)) * 3e4).astype(np.float32)
     w[0, :8] = 1e5
     blob, st = oracle.encode(w, 5.0)
-    check_blob(E, oracle, blob, dtypes=["FP16", "FP8", "INT8", "BF16", "E5M2"], tag="sat")
+    with task_mode(tasks):
+        check_blob(E, oracle, blob, dtypes=["FP16", "FP8", "INT8", "BF16", "E5M2"], tag=f"sat {tasks}")
     w[1, :8] = 9e4   # beyond e5m2's 57344
     blob, st = oracle.encode(w, 5.0)
-    check_blob(E, oracle, blob, dtypes=["E5M2"], tag="sat e5m2")
+    with task_mode(tasks):
+        check_blob(E, oracle, blob, dtypes=["E5M2"], tag=f"sat e5m2 {tasks}")
 
 
 @pytest.mark.parametrize("shape,target,kw", [
