@@ -10,6 +10,7 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
@@ -30,19 +31,22 @@ def _run(cmd):
 
 
 def build(verbose: bool = True) -> str:
+    """Compile every source (concurrently: decode.hip alone takes minutes) and link."""
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
+    jobs = []
     for src in HOST_SRC:
         obj = os.path.join(BUILD, src + ".o")
-        _run(["g++", *COMMON, "-pthread", "-Wall", "-c", os.path.join(CSRC, src), "-o", obj])
-        objs.append(obj)
+        jobs.append((["g++", *COMMON, "-pthread", "-Wall", "-c", os.path.join(CSRC, src), "-o", obj], obj))
     for src in HIP_SRC:
         path = os.path.join(CSRC, src)
         if not os.path.exists(path):
             continue
         obj = os.path.join(BUILD, src + ".o")
-        _run([HIPCC, *COMMON, *HIP_FLAGS, "-c", path, "-o", obj])
-        objs.append(obj)
+        jobs.append(([HIPCC, *COMMON, *HIP_FLAGS, "-c", path, "-o", obj], obj))
+    with ThreadPoolExecutor(max_workers=len(jobs)) as pool:
+        for f in [pool.submit(_run, cmd) for cmd, _ in jobs]:
+            f.result()
+    objs = [obj for _, obj in jobs]
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", *objs, "-o", tmp])
     os.replace(tmp, LIB)
