@@ -70,7 +70,10 @@ METRIC = "decoded weights/s and achieved HBM GB/s (% roofline), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
 SETTLE_S = 0.3
 INT8_PEAK_TOPS = 5000.0   # dense MFMA int8, MI355X
-DECODE_SRC = os.path.join(ROOT, "paper_2609_34185_amd", "csrc", "decode.hip")
+# the decode kernels' sources: their device code, then the file that instantiates
+# the kernels bench.py times
+DECODE_SRCS = [os.path.join(ROOT, "paper_2609_34185_amd", "csrc", n)
+               for n in ("decode_kernels.h", "decode.hip")]
 COPY_BYTES = 1 << 30
 
 
@@ -407,8 +410,12 @@ def tile_sweep(args, E, W, threads):
 
 
 def source_digest() -> str:
-    with open(DECODE_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """sha256 of the decode kernels' sources, in DECODE_SRCS order."""
+    h = hashlib.sha256()
+    for path in DECODE_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def profile_summary(name: str):
