@@ -303,6 +303,12 @@ int decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_
   D[0].saturate = 0;
   D[0].x = d_x;
   D[0].m = (uint32_t)m;
+  // More than four rows of X: two-tile tasks with one chain per wave, whose
+  // eight running sums per lane fit the registers (with two chains they spill).
+  if (m > 4 && (D[0].path == kPathLut || D[0].path == kPathWide) && D[0].b == 11) {
+    D[0].tpt = 2;
+    D[0].n_tasks = (D[0].tile_end - D[0].tile_begin + 1) / 2;
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (!clear_i32(d_y, (int64_t)m * info->rows, s))
     return fail(EP_ERR_HIP, "ep_decode_matmul_i8: clearing Y failed");

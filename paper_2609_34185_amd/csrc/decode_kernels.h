@@ -1703,12 +1703,14 @@ __device__ __forceinline__ void lut_task(const Hot& L, uint8_t* lds, uint32_t ri
 
 // The slot-table steady state with one chain: a task of two tiles, t0 in
 // lanes 0-31 and t0 + 1 in lanes 32-63, for launches with too few four-tile
-// tasks to fill the SIMDs (see field_step1).  Decoded outputs only (no fused
-// product).  The structure is lut_task's with the second chain removed.
-template <int B, int DT, bool SAT, bool TWO, bool WIDE>
+// tasks to fill the SIMDs (see field_step1), and for the fused product with
+// more than four rows of X, whose sums then fit the registers.  The structure
+// is lut_task's with the second chain removed.
+template <int B, int DT, bool SAT, bool TWO, bool WIDE, int MT = 1>
 __device__ __forceinline__ void lut_task1(const Hot& L, uint8_t* lds, uint32_t ring_area, uint32_t t0,
                                           int32_t* status) {
-  static_assert(DT != kOutDotI8, "one-chain tasks decode only");
+  constexpr bool DOT = DT == kOutDotI8;
+  static_assert(!DOT || TWO, "the fused product runs the steady state on rows of at least a tile");
   const uint32_t lane = threadIdx.x & 63, wave = wave_id();
   const uint32_t half = lane >> 5, l = lane & 31;
   const EP_GLOBAL uint32_t* states = gptr<const uint32_t>(L.blob + L.off_states);
@@ -1740,6 +1742,18 @@ __device__ __forceinline__ void lut_task1(const Hot& L, uint8_t* lds, uint32_t r
     sa = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r, 0, 0));
     sb = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * r + 4, 0, 0));
   }
+  int32_t dacc[MT];
+  uint32_t r0 = 0, kd = 0, colb = 0;
+  __amdgpu_buffer_rsrc_t xrsrc;
+  if constexpr (DOT) {
+    xrsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(L.x), (short)0,
+                                              (int)(L.m * L.cols), 0x00020000);
+    r0 = row_of(L, tile * L.V);                 // first row of the lane's tile
+    kd = row_of(L, vb) == r0 ? kc : 0u;         // first round in row r0 + 1
+    colb = vb - r0 * L.cvec;
+#pragma unroll
+    for (int t = 0; t < MT; t++) dacc[t] = 0;
+  }
   FastChain F0;
   u32x2 pend0, pendB0;
 #pragma unroll
@@ -1766,6 +1780,24 @@ __device__ __forceinline__ void lut_task1(const Hot& L, uint8_t* lds, uint32_t r
     float sg;
     if constexpr (TWO) sg = k < kc ? sa : sb;
     else sg = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srsrc, 4 * row_of(L, vb + 32 * k), 0, 0));
+    uint32_t xo = 0, xq[MT];
+    if constexpr (DOT) {
+      EP_GLOBAL int32_t* y = gptr<int32_t>(L.out);
+      // lanes whose vectors pass into row r0 + 1 this round: their sums so far belong to r0
+      const bool dep = k == kd;
+      if (__builtin_expect(__ballot(dep) != 0, 0)) {
+#pragma unroll
+        for (int t = 0; t < MT; t++) {
+          const int32_t sum = half_sum(dep ? dacc[t] : 0);
+          if (l == 0 && (uint32_t)t < L.m && sum != 0) add_i32(y + (uint64_t)t * L.rows + r0, sum);
+          if (dep) dacc[t] = 0;
+        }
+      }
+      xo = 8 * (colb + 32 * k - (k >= kd ? L.cvec : 0u));
+      // columns 0-3 of the vector now, 4-7 once the first four weights are known
+#pragma unroll
+      for (int t = 0; t < MT; t++) xq[t] = __builtin_amdgcn_raw_buffer_load_b32(xrsrc, xo, t * L.cols, 0);
+    }
     uint32_t cb, e0;
     float y0, hc;
     QAcc acc;
@@ -1780,18 +1812,46 @@ __device__ __forceinline__ void lut_task1(const Hot& L, uint8_t* lds, uint32_t r
   q_take<DT, I, WIDE>(acc, e0, y0, cb >> (B + 5));
     EP_FIELD(1) EP_FIELD(2)
     fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
-    EP_FIELD(3) EP_FIELD(4) EP_FIELD(5)
+    EP_FIELD(3) EP_FIELD(4)
+    if constexpr (DOT) {
+#pragma unroll
+      for (int t = 0; t < MT; t++) {
+        dacc[t] = __builtin_amdgcn_sdot4((int)acc.w[0], (int)xq[t], dacc[t], false);
+        xq[t] = __builtin_amdgcn_raw_buffer_load_b32(xrsrc, xo + 4, t * L.cols, 0);
+      }
+    }
+    EP_FIELD(5)
     fast_stage(F0, pend0, pendB0, lds, vrb08, vl8, rsrc, half, 3 * 32);
     EP_FIELD(6) EP_FIELD(7) EP_FIELD(8)
 #undef EP_FIELD
 #undef EP_PIN1
-    if (!PART || !pin) q_put<DT>(obase, voff, acc);
-    obase += 32 * VB;
+    if constexpr (DOT) {
+#pragma unroll
+      for (int t = 0; t < MT; t++)
+        dacc[t] = __builtin_amdgcn_sdot4((int)acc.w[1], (int)xq[t], dacc[t], false);
+    } else {
+      if (!PART || !pin) q_put<DT>(obase, voff, acc);
+      obase += 32 * VB;
+    }
   };
   for (uint32_t k = 0; k < full; k++) round(k, std::false_type{});
-  if (tail) {
-    round(full, std::true_type{});
-    x = pin ? xsave : x;
+  if constexpr (!DOT) {
+    if (tail) {
+      round(full, std::true_type{});
+      x = pin ? xsave : x;
+    }
+  } else {
+    EP_GLOBAL int32_t* y = gptr<int32_t>(L.out);
+    const bool moved = full > kd;   // the lane's last vector lies in row r0 + 1
+#pragma unroll
+    for (int t = 0; t < MT; t++) {
+      const int32_t s0 = half_sum(moved ? 0 : dacc[t]);
+      const int32_t s1 = half_sum(moved ? dacc[t] : 0);
+      if (l == 0 && (uint32_t)t < L.m) {
+        if (s0 != 0) add_i32(y + (uint64_t)t * L.rows + r0, s0);
+        if (s1 != 0) add_i32(y + (uint64_t)t * L.rows + r0 + 1, s1);
+      }
+    }
   }
 
   uint32_t err = 0;
@@ -1812,17 +1872,22 @@ __device__ __forceinline__ void lut_task1(const Hot& L, uint8_t* lds, uint32_t r
 template <int B, int DT, bool SAT, bool WIDE, int NCH = 2>
 __device__ __forceinline__ void lut_task_rows(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                               uint32_t t0, int32_t* status) {
-  static_assert(NCH == 2 || DT == EP_BF16 || DT == EP_FP16 || DT == EP_FP8_E4M3 || DT == EP_INT8,
+  static_assert(NCH == 2 || DT == EP_BF16 || DT == EP_FP16 || DT == EP_FP8_E4M3 || DT == EP_INT8 ||
+                    DT == kOutDotI8,
                 "one-chain tasks cover the common output types");
-  if constexpr (NCH == 1) {
+  if constexpr (NCH == 1 && DT == kOutDotI8) {
+    // more than four rows of X (the only product that runs one chain); rows
+    // of at least a tile (lut_task_any checks)
+    lut_task1<B, DT, false, true, WIDE, kDotMaxTokens>(L, lds, ring_area, t0, status);
+  } else if constexpr (NCH == 1) {
     if (L.cvec >= 32 * ((L.V - 1) / 32)) lut_task1<B, DT, SAT, true, WIDE>(L, lds, ring_area, t0, status);
     else lut_task1<B, DT, SAT, false, WIDE>(L, lds, ring_area, t0, status);
   } else if constexpr (DT == kOutDotI8) {
+    // up to four rows of X (more take one chain per wave, lut_task_any)
     if (L.cvec >= L.V) {
       if (L.m <= 1) lut_task<B, DT, false, true, WIDE, 1>(L, lds, ring_area, t0, status);
       else if (L.m <= 2) lut_task<B, DT, false, true, WIDE, 2>(L, lds, ring_area, t0, status);
-      else if (L.m <= 4) lut_task<B, DT, false, true, WIDE, 4>(L, lds, ring_area, t0, status);
-      else lut_task<B, DT, false, true, WIDE, kDotMaxTokens>(L, lds, ring_area, t0, status);
+      else lut_task<B, DT, false, true, WIDE, 4>(L, lds, ring_area, t0, status);
     } else {
       lut_task<B, DT, false, false, WIDE>(L, lds, ring_area, t0, status);
     }
@@ -1841,8 +1906,10 @@ template <int B, bool WIDE, bool DOT = false, int NCH = 2>
 __device__ __forceinline__ bool lut_task_any(const Hot& L, uint8_t* lds, uint32_t ring_area,
                                              uint32_t t0, int32_t* status) {
   if constexpr (DOT) {
-    static_assert(NCH == 2, "the fused product runs four-tile tasks");
-    lut_task_rows<B, kOutDotI8, false, WIDE>(L, lds, ring_area, t0, status);
+    if (NCH == 1 && L.cvec < L.V) return false;   // the generic loop adds vector by vector
+    // two chains hold the sums of at most four rows of X in registers
+    if (NCH == 2 && L.m > 4) return false;
+    lut_task_rows<B, kOutDotI8, false, WIDE, NCH>(L, lds, ring_area, t0, status);
     return true;
   }
   if constexpr (NCH == 1) {
@@ -2038,13 +2105,13 @@ template <int PATH, int B, bool DOT, bool SMALL>
 __device__ __forceinline__ void task_b(const Hot& L, const uint32_t* tab, uint8_t* lb,
                                        uint32_t ring_area, uint32_t task, int32_t* status) {
   const uint32_t nvec = L.rows * L.cvec;
-  if constexpr (SMALL && !DOT && (PATH == kPathLut || PATH == kPathWide) && B == 11) {
+  if constexpr (SMALL && (PATH == kPathLut || PATH == kPathWide) && B == 11) {
     if (L.tpt == 2) {
-      // two-tile tasks, one chain per wave
+      // two-tile tasks, one chain per wave (the fused product needs whole rounds)
       const uint32_t t0 = L.tile_begin + 2 * task;
       const bool whole = t0 + 2 <= L.tile_end && (uint64_t)(t0 + 2) * L.V <= nvec;
-      if (whole && L.V >= 32 && L.pay_bytes < kFastOob &&
-          lut_task_any<B, PATH == kPathWide, false, 1>(L, lb, ring_area, t0, status))
+      if (whole && L.V >= 32 && (!DOT || L.V % 32 == 0) && L.pay_bytes < kFastOob &&
+          lut_task_any<B, PATH == kPathWide, DOT, 1>(L, lb, ring_area, t0, status))
         return;
       if (whole && L.V % 32 == 0) decode_task<PATH, B, 1, true, DOT>(L, tab, lb, ring_area, task, status);
       else decode_task<PATH, B, 1, false, DOT>(L, tab, lb, ring_area, task, status);
@@ -2145,7 +2212,7 @@ __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers,
       }
     } else {
       // the mixed-path kernel never runs two-tile tasks (use_small_tasks)
-      run_segment<PATH, DOT, !DOT>(L, lds, seg, seg_end, status);
+      run_segment<PATH, DOT, true>(L, lds, seg, seg_end, status);
     }
     seg = seg_end;
   }
