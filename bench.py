@@ -23,6 +23,9 @@ at 4.0 bpp; a step encodes all three; the CPU baseline is the oracle encoder
 on the down projection), fused_mfma_m<m> (the fused decode and MFMA product
 ep_decode_gemm_i8 of the INT8-container down projection with the first m rows of the
 activations, timed beside decode-then-GEMM and the product alone on resident weights),
+fused_bf16_m<m> (the fused decode and BF16 MFMA product ep_decode_gemm_bf16 of the
+diffusion-transformer MLP input projection 10240 x 3840 at 2.5 bpp with m rows of bf16
+activations, timed beside a BF16 decode followed by the library BF16 GEMM),
 fused_down_m1 / _m2 / _m4 / _m8 (the fused decode and
 small-batch product ep_decode_matmul_i8: the INT8-container down projection
 times the first 1, 2, 4 or 8 rows of the activations, one launch per step;
@@ -70,6 +73,7 @@ METRIC = "decoded weights/s and achieved HBM GB/s (% roofline), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
 SETTLE_S = 0.3
 INT8_PEAK_TOPS = 5000.0   # dense MFMA int8, MI355X
+BF16_PEAK_TFLOPS = 2500.0   # dense MFMA bf16, MI355X
 # the decode kernels' sources: their device code, then the file that instantiates
 # the kernels bench.py times
 DECODE_SRCS = [os.path.join(ROOT, "paper_2609_34185_amd", "csrc", n)
@@ -345,6 +349,76 @@ def fused_mfma_bench(args, E, W, threads, m):
                    "decode_then_gemm_overhead_vs_resident_pct": 100.0 * (ms_dec / ms_gemm)},
         "roofline": {"bound": "mfma", "achieved": ops / (ms * 1e-3) / 1e12, "peak": INT8_PEAK_TOPS,
                      "unit": "TFLOP/s", "frac": ops / (ms * 1e-3) / 1e12 / INT8_PEAK_TOPS,
+                     "traffic": None},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def fused_bf16_bench(args, E, W, threads, m):
+    """--workload fused_bf16_m<m>: Y = X W'^T (fp32) for the diffusion-transformer MLP input
+    projection (10240 x 3840 Student-t rows at 2.5 bpp, the paper's reference-layer shape) and
+    m rows of bf16 activations by the fused decode and BF16 MFMA product
+    (ep_decode_gemm_bf16_prepared, tables prepared once; W' never written as a whole), timed
+    beside decode-then-GEMM (a prepared one-layer stack decoded to BF16 by ep_stack_decode,
+    then torch's BF16 GEMM, used only as the comparison) and beside that GEMM alone on the
+    resident decoded weights.  The fused Y is checked against the fp32 product of the decoded
+    weights before anything is timed."""
+    import numpy as np
+    import torch
+    w = dict(W.dit_block(0))["blocks.0.mlp_in"]
+    blob, _ = E.encode(w, 2.5, nthreads=threads)
+    info = E.blob_info(blob)
+    rng = np.random.default_rng(7)
+    x = torch.from_numpy(rng.standard_normal((m, info.cols)).astype(np.float32)).cuda().to(torch.bfloat16)
+    d_blob = E.to_device(blob, torch.device("cuda", 0))
+    y = torch.empty((m, info.rows), dtype=torch.float32, device="cuda")
+    wd = torch.empty((info.rows, info.cols), dtype=torch.bfloat16, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = E.decode_gemm_bf16_workspace(info)
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    s = stream.cuda_stream
+    E.decode_gemm_bf16_prepare(info, d_blob.data_ptr(), d_ws.data_ptr(), ws, s)
+    sws = E.stack_workspace(1)
+    d_sws = torch.empty(sws, dtype=torch.uint8, device="cuda")
+    stack = E.stack_prepare([(info, d_blob.data_ptr(), wd.data_ptr(), 0, E.BF16)], d_sws.data_ptr(), sws, s)
+
+    def fused_step():
+        E.decode_gemm_bf16_prepared(info, d_blob.data_ptr(), x.data_ptr(), m, y.data_ptr(),
+                                    d_ws.data_ptr(), ws, 0, status.data_ptr(), s)
+
+    def decode_step():
+        E.stack_decode(stack, status.data_ptr(), s)
+
+    def gemm_step():
+        torch.nn.functional.linear(x, wd)   # a 2-D product (no batched GEMM)
+
+    fused_step()
+    decode_step()
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+    ref = x.float() @ wd.float().t().contiguous()
+    torch.cuda.synchronize()
+    assert torch.allclose(y, ref, rtol=1e-3, atol=1e-3 * float(ref.abs().max())), \
+        "fused BF16 product differs from the product of the decoded weights"
+    ms = time_steps(args, fused_step, stream)
+    ms_dec = time_steps(args, decode_step, stream)
+    ms_gemm = time_steps(args, gemm_step, stream)
+    assert int(status.item()) == 0, "decode reported a corrupt stream"
+    weights = info.rows * info.cols
+    flops = 2.0 * m * info.rows * info.cols
+    line = {
+        "metric": "fused decode + BF16 MFMA product: decoded weights/s and TFLOP/s (% of MFMA peak)",
+        "value": weights / (ms * 1e-3), "unit": "weights/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"fused decode and BF16 MFMA product: DiT MLP input projection 10240x3840 "
+                               f"at 2.5 bpp times X = {m} x 3840 bf16 rows, Y fp32",
+                   "rows_x": m, "weights": weights,
+                   "decode_then_gemm_ms": {"decode": ms_dec, "gemm": ms_gemm, "total": ms_dec + ms_gemm},
+                   "fused_over_decode_then_gemm": ms / (ms_dec + ms_gemm)},
+        "roofline": {"bound": "mfma", "achieved": flops / (ms * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": flops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
                      "traffic": None},
     }
     print(json.dumps(line), flush=True)
@@ -628,6 +702,10 @@ def main():
         return
     if args.workload == "tile_sweep":
         tile_sweep(args, E, W, min(16, len(os.sched_getaffinity(0))))
+        return
+    if args.workload.startswith("fused_bf16_m"):
+        fused_bf16_bench(args, E, W, min(16, len(os.sched_getaffinity(0))),
+                         int(args.workload[len("fused_bf16_m"):]))
         return
     if args.workload.startswith("fused_mfma_m"):
         fused_mfma_bench(args, E, W, min(16, len(os.sched_getaffinity(0))),

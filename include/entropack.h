@@ -289,6 +289,39 @@ int ep_decode_gemm_i8_prepared(const ep_tensor_info* info, const void* d_blob, c
                                int64_t m, int32_t* d_y, float* d_dequant, void* d_workspace,
                                uint64_t ws_bytes, int32_t* d_status, void* hip_stream);
 
+/* The same fused decode and MFMA product with BF16 operands, for any blob:
+ *   Y[t][r] = sum_j X[t][j] * W'[r][j]   for t < m, r < R,
+ * with W' the tensor exactly as ep_decode_tiles writes it with EP_BF16 (for
+ * containers: the container values, the weights being delta_r * W'), X m x C
+ * bf16 row-major (d_x), Y m x R fp32 row-major (d_y).  Each workgroup decodes
+ * its block's tiles to bf16 in its slab and multiplies on the matrix cores
+ * (v_mfma_f32_16x16x32_bf16); every product of two bf16 values is exact in
+ * fp32 and the sums are fp32, so |Y - X W'^T| <= (C + s + 2) 2^-24 sum_j
+ * |X[t][j] W'[r][j]| with s <= 16 partial sums per element (K is split over
+ * waves when m < 256, and those partial sums are added with float atomics, so
+ * the last bits of Y may differ from call to call).  d_workspace: >=
+ * ep_decode_gemm_bf16_workspace(info) bytes.  Y is overwritten (cleared first
+ * when m < 256).  d_dequant, d_status as for ep_decode_gemm_i8.  Asynchronous,
+ * no allocation, at most one clear and one launch.
+ * Errors: EP_ERR_ARG (null pointers, m outside 1..65536, X above 2^31 bytes,
+ * short workspace), EP_ERR_UNSUPPORTED, EP_ERR_HIP. */
+int ep_decode_gemm_bf16(const ep_tensor_info* info, const void* d_blob, const void* d_x, int64_t m,
+                        float* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
+                        int32_t* d_status, void* hip_stream);
+
+/* Workspace bytes of ep_decode_gemm_bf16 (slabs hold bf16 rows; 0 if info is
+ * null or no device is present). */
+uint64_t ep_decode_gemm_bf16_workspace(const ep_tensor_info* info);
+
+/* ep_decode_gemm_i8_prepare and ep_decode_gemm_i8_prepared for the BF16
+ * product: the tables are built once into the workspace's table area, then
+ * every ep_decode_gemm_bf16_prepared call copies them (same contract). */
+int ep_decode_gemm_bf16_prepare(const ep_tensor_info* info, const void* d_blob, void* d_workspace,
+                                uint64_t ws_bytes, void* hip_stream);
+int ep_decode_gemm_bf16_prepared(const ep_tensor_info* info, const void* d_blob, const void* d_x,
+                                 int64_t m, float* d_y, float* d_dequant, void* d_workspace,
+                                 uint64_t ws_bytes, int32_t* d_status, void* hip_stream);
+
 /* One layer of a stack decode. */
 typedef struct {
   ep_tensor_info info;       /* from ep_blob_info on the host copy */

@@ -317,7 +317,6 @@ int decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const int8_
                        d_status, s, "ep_decode_matmul_i8", true);
 }
 
-// Fused decode and MFMA product: grid, margin rows and slab bytes of a tensor.
 // A layer's decode tables as built in LDS (ring_offset bytes, at most this).
 constexpr uint64_t kTableImageBytes = 128 * 1024;
 
@@ -327,14 +326,16 @@ constexpr uint64_t kTableImageBytes = 128 * 1024;
 constexpr uint64_t kGemmDescOffset = kTableImageBytes;
 constexpr uint64_t kGemmSlabsOffset = kGemmDescOffset + ((sizeof(LayerDev) + 255) & ~255ull);
 
+// Fused decode and MFMA product: grid, margin rows and slab bytes of a tensor
+// (elem: bytes per decoded weight, 1 for the INT8 product, 2 for the BF16 one).
 struct GemmGeom {
   uint32_t groups, margin, n_blocks, rows_per_block;
   uint64_t slab_bytes;
 };
 
-int gemm_geometry(const ep_tensor_info& I, GemmGeom& G) {
+int gemm_geometry(const ep_tensor_info& I, uint32_t elem, GemmGeom& G) {
   DeviceProps P = device_props();
-  if (!P.cus) return fail(EP_ERR_HIP, "ep_decode_gemm_i8: no HIP device");
+  if (!P.cus) return fail(EP_ERR_HIP, "ep_decode_gemm: no HIP device");
   const uint32_t cvec = I.cols / 8;
   // rows a block's tiles reach past either side: its tile range is widened to
   // whole tasks of kTilesPerTask tiles
@@ -344,72 +345,100 @@ int gemm_geometry(const ep_tensor_info& I, GemmGeom& G) {
   G.rows_per_block = std::min<uint32_t>(G.rows_per_block, 16 * kGemmMaxTiles);   // then several rounds
   G.n_blocks = (I.rows + G.rows_per_block - 1) / G.rows_per_block;
   G.groups = std::min<uint32_t>(G.n_blocks, (uint32_t)P.cus);
-  G.slab_bytes = (((uint64_t)G.rows_per_block + 2 * G.margin) * I.cols + 255) & ~255ull;
+  G.slab_bytes = (((uint64_t)G.rows_per_block + 2 * G.margin) * I.cols * elem + 255) & ~255ull;
   return EP_OK;
 }
 
-uint64_t decode_gemm_workspace(const ep_tensor_info* info) {
+uint64_t decode_gemm_workspace(const ep_tensor_info* info, uint32_t elem) {
   GemmGeom G;
-  if (!info || gemm_geometry(*info, G)) return 0;
+  if (!info || gemm_geometry(*info, elem, G)) return 0;
   return kGemmSlabsOffset + (uint64_t)G.groups * G.slab_bytes;
 }
 
-// Checks shared by the fused product's entry points.
-int gemm_checks(const ep_tensor_info* info, const char* who) {
-  if (!info) return fail(EP_ERR_ARG, who);
+// Checks shared by the fused products' entry points.  The INT8 product takes
+// the INT8 row container's values (exact int32 sums need C <= 131071); the
+// BF16 one takes the bf16 decode of any blob.
+int gemm_checks(const ep_tensor_info* info, bool bf, const char* who) {
+  if (!info) return fail(EP_ERR_ARG, (std::string(who) + ": null info").c_str());
+  if (bf) return EP_OK;
   if (info->container != EP_CONT_INT8_ROW)
-    return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: the tensor is not in the INT8 row container");
+    return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": the tensor is not in the INT8 row container").c_str());
   if (info->cols > 131071)
-    return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: rows longer than 131071 weights may overflow int32");
+    return fail(EP_ERR_UNSUPPORTED, (std::string(who) + ": rows longer than 131071 weights may overflow int32").c_str());
   return EP_OK;
 }
 
+// Build the tensor's decode tables into the table area at the start of the
+// workspace (the same area for both products).
 int decode_gemm_prepare(const ep_tensor_info* info, const void* d_blob, void* d_ws, uint64_t ws_bytes,
-                        void* stream) {
-  int rc = gemm_checks(info, "ep_decode_gemm_i8_prepare: null info");
+                        void* stream, bool bf, const char* who) {
+  int rc = gemm_checks(info, bf, who);
   if (rc) return rc;
-  if (!d_ws || ws_bytes < decode_gemm_workspace(info))
-    return fail(EP_ERR_ARG, "ep_decode_gemm_i8_prepare: workspace too small");
+  if (!d_ws || ws_bytes < decode_gemm_workspace(info, bf ? 2 : 1))
+    return fail(EP_ERR_ARG, (std::string(who) + ": workspace too small").c_str());
   LayerDev D;
   // the output pointer is never used by the table build
-  rc = fill_layer(*info, d_blob, EP_INT8, d_ws, nullptr, 0, info->n_tiles, D);
+  rc = fill_layer(*info, d_blob, bf ? EP_BF16 : EP_INT8, d_ws, nullptr, 0, info->n_tiles, D);
   if (rc) return rc;
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   D.tables = ws;
   const uint32_t lds = lds_bytes(info->path, *info);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (hipMemcpyAsync(ws + kGemmDescOffset, &D, sizeof D, hipMemcpyHostToDevice, s) != hipSuccess)
-    return fail(EP_ERR_HIP, "ep_decode_gemm_i8_prepare: descriptor copy failed");
+    return fail(EP_ERR_HIP, (std::string(who) + ": descriptor copy failed").c_str());
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(&stack_tables_kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-    return fail(EP_ERR_HIP, "ep_decode_gemm_i8_prepare: cannot raise the table kernel's LDS limit");
+    return fail(EP_ERR_HIP, (std::string(who) + ": cannot raise the table kernel's LDS limit").c_str());
   hipLaunchKernelGGL(stack_tables_kernel, dim3(1), dim3(kThreads), lds, s,
                      reinterpret_cast<const LayerDev*>(ws + kGemmDescOffset));
   if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
-    return fail(EP_ERR_HIP, "ep_decode_gemm_i8_prepare: building the decode tables failed");
+    return fail(EP_ERR_HIP, (std::string(who) + ": building the decode tables failed").c_str());
   return EP_OK;
 }
 
-// prepared: the workspace holds this tensor's tables (ep_decode_gemm_i8_prepare)
-int decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
-                   int32_t* d_y, float* d_dequant, void* d_ws, uint64_t ws_bytes, int32_t* d_status,
-                   void* stream, bool prepared) {
-  int rc = gemm_checks(info, "ep_decode_gemm_i8: null info");
+template <bool BF>
+const void* gemm_kernel_fn(uint32_t path) {
+  return path == kPathLut ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathLut, BF>)
+         : path == kPathWide ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathWide, BF>)
+         : path == kPathSearch ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathSearch, BF>)
+                               : reinterpret_cast<const void*>(&decode_gemm_kernel<kPathGlobal, BF>);
+}
+
+template <bool BF>
+void launch_gemm(uint32_t path, uint32_t groups, uint32_t lds, hipStream_t s, const GemmLaunch& A,
+                 int32_t* st) {
+  if (path == kPathLut)
+    hipLaunchKernelGGL((decode_gemm_kernel<kPathLut, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
+  else if (path == kPathWide)
+    hipLaunchKernelGGL((decode_gemm_kernel<kPathWide, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
+  else if (path == kPathSearch)
+    hipLaunchKernelGGL((decode_gemm_kernel<kPathSearch, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
+  else
+    hipLaunchKernelGGL((decode_gemm_kernel<kPathGlobal, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
+}
+
+// The fused decode and MFMA product: INT8 (bf = false: int8 X, int32 Y, the
+// INT8 container's values) or BF16 (bf16 X, fp32 Y, the bf16 decode).
+// prepared: the workspace holds this tensor's tables (decode_gemm_prepare).
+int decode_gemm(const ep_tensor_info* info, const void* d_blob, const void* d_x, int64_t m, void* d_y,
+                float* d_dequant, void* d_ws, uint64_t ws_bytes, int32_t* d_status, void* stream,
+                bool prepared, bool bf, const char* who) {
+  int rc = gemm_checks(info, bf, who);
   if (rc) return rc;
-  if (m < 1 || m > 65536) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: m must be 1 .. 65536");
-  if (!d_x || !d_y) return fail(EP_ERR_ARG, "ep_decode_gemm_i8: null X or Y");
-  if ((uint64_t)m * info->cols > 0x7FFFFFFFull)
-    return fail(EP_ERR_ARG, "ep_decode_gemm_i8: X above 2^31 bytes");
+  const std::string w(who);
+  const uint32_t elem = bf ? 2 : 1;
+  if (m < 1 || m > 65536) return fail(EP_ERR_ARG, (w + ": m must be 1 .. 65536").c_str());
+  if (!d_x || !d_y) return fail(EP_ERR_ARG, (w + ": null X or Y").c_str());
+  if ((uint64_t)m * info->cols * elem > 0x7FFFFFFFull) return fail(EP_ERR_ARG, (w + ": X above 2^31 bytes").c_str());
   GemmLaunch A;
   std::memset(&A, 0, sizeof A);
-  rc = fill_layer(*info, d_blob, EP_INT8, d_y, d_dequant, 0, info->n_tiles, A.L);
+  rc = fill_layer(*info, d_blob, bf ? EP_BF16 : EP_INT8, d_y, d_dequant, 0, info->n_tiles, A.L);
   if (rc) return rc;
   GemmGeom G;
-  rc = gemm_geometry(*info, G);
+  rc = gemm_geometry(*info, elem, G);
   if (rc) return rc;
-  if (G.slab_bytes > 0x7FFFFFFFull) return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: rows too long");
-  if (!d_ws || ws_bytes < decode_gemm_workspace(info))
-    return fail(EP_ERR_ARG, "ep_decode_gemm_i8: workspace too small");
+  if (G.slab_bytes > 0x7FFFFFFFull) return fail(EP_ERR_UNSUPPORTED, (w + ": rows too long").c_str());
+  if (!d_ws || ws_bytes < decode_gemm_workspace(info, elem)) return fail(EP_ERR_ARG, (w + ": workspace too small").c_str());
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   A.L.tables = prepared ? ws : nullptr;
   A.g.x = d_x;
@@ -421,27 +450,19 @@ int decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t*
   A.g.n_blocks = G.n_blocks;
   A.g.rows_per_block = G.rows_per_block;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((uint32_t)((m + 15) / 16) < kWavesPerGroup &&   // partial sums are added with atomics
-      !clear_i32(d_y, (int64_t)m * info->rows, s))
-    return fail(EP_ERR_HIP, "ep_decode_gemm_i8: clearing Y failed");
+  // partial sums are added with atomics (0 is also +0.0f for the BF16 product)
+  if ((uint32_t)((m + 15) / 16) < kWavesPerGroup &&
+      !clear_i32(static_cast<int32_t*>(d_y), (int64_t)m * info->rows, s))
+    return fail(EP_ERR_HIP, (w + ": clearing Y failed").c_str());
   const uint32_t lds = lds_bytes(info->path, *info);
   DeviceProps P = device_props();
-  if (lds > P.max_lds) return fail(EP_ERR_UNSUPPORTED, "ep_decode_gemm_i8: tables exceed the device LDS");
-  const void* fn = info->path == kPathLut ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathLut>)
-                   : info->path == kPathWide ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathWide>)
-                   : info->path == kPathSearch ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathSearch>)
-                                               : reinterpret_cast<const void*>(&decode_gemm_kernel<kPathGlobal>);
+  if (lds > P.max_lds) return fail(EP_ERR_UNSUPPORTED, (w + ": tables exceed the device LDS").c_str());
+  const void* fn = bf ? gemm_kernel_fn<true>(info->path) : gemm_kernel_fn<false>(info->path);
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-    return fail(EP_ERR_HIP, "ep_decode_gemm_i8: cannot raise the kernel's LDS limit");
-  if (info->path == kPathLut)
-    hipLaunchKernelGGL(decode_gemm_kernel<kPathLut>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
-  else if (info->path == kPathWide)
-    hipLaunchKernelGGL(decode_gemm_kernel<kPathWide>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
-  else if (info->path == kPathSearch)
-    hipLaunchKernelGGL(decode_gemm_kernel<kPathSearch>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
-  else
-    hipLaunchKernelGGL(decode_gemm_kernel<kPathGlobal>, dim3(G.groups), dim3(kThreads), lds, s, A, d_status);
-  if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, "ep_decode_gemm_i8: launch failed");
+    return fail(EP_ERR_HIP, (w + ": cannot raise the kernel's LDS limit").c_str());
+  if (bf) launch_gemm<true>(info->path, G.groups, lds, s, A, d_status);
+  else launch_gemm<false>(info->path, G.groups, lds, s, A, d_status);
+  if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (w + ": launch failed").c_str());
   return EP_OK;
 }
 
@@ -604,25 +625,48 @@ int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const in
   return ep::decode_matmul_i8(info, d_blob, d_x, m, d_y, d_dequant, d_status, hip_stream);
 }
 
-uint64_t ep_decode_gemm_i8_workspace(const ep_tensor_info* info) { return ep::decode_gemm_workspace(info); }
+uint64_t ep_decode_gemm_i8_workspace(const ep_tensor_info* info) { return ep::decode_gemm_workspace(info, 1); }
 
 int ep_decode_gemm_i8_prepare(const ep_tensor_info* info, const void* d_blob, void* d_workspace,
                               uint64_t ws_bytes, void* hip_stream) {
-  return ep::decode_gemm_prepare(info, d_blob, d_workspace, ws_bytes, hip_stream);
+  return ep::decode_gemm_prepare(info, d_blob, d_workspace, ws_bytes, hip_stream, false,
+                                 "ep_decode_gemm_i8_prepare");
 }
 
 int ep_decode_gemm_i8_prepared(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x,
                                int64_t m, int32_t* d_y, float* d_dequant, void* d_workspace,
                                uint64_t ws_bytes, int32_t* d_status, void* hip_stream) {
-  return ep::decode_gemm_i8(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
-                            hip_stream, true);
+  return ep::decode_gemm(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
+                         hip_stream, true, false, "ep_decode_gemm_i8_prepared");
 }
 
 int ep_decode_gemm_i8(const ep_tensor_info* info, const void* d_blob, const int8_t* d_x, int64_t m,
                       int32_t* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
                       int32_t* d_status, void* hip_stream) {
-  return ep::decode_gemm_i8(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
-                            hip_stream, false);
+  return ep::decode_gemm(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
+                         hip_stream, false, false, "ep_decode_gemm_i8");
+}
+
+uint64_t ep_decode_gemm_bf16_workspace(const ep_tensor_info* info) { return ep::decode_gemm_workspace(info, 2); }
+
+int ep_decode_gemm_bf16_prepare(const ep_tensor_info* info, const void* d_blob, void* d_workspace,
+                                uint64_t ws_bytes, void* hip_stream) {
+  return ep::decode_gemm_prepare(info, d_blob, d_workspace, ws_bytes, hip_stream, true,
+                                 "ep_decode_gemm_bf16_prepare");
+}
+
+int ep_decode_gemm_bf16(const ep_tensor_info* info, const void* d_blob, const void* d_x, int64_t m,
+                        float* d_y, float* d_dequant, void* d_workspace, uint64_t ws_bytes,
+                        int32_t* d_status, void* hip_stream) {
+  return ep::decode_gemm(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
+                         hip_stream, false, true, "ep_decode_gemm_bf16");
+}
+
+int ep_decode_gemm_bf16_prepared(const ep_tensor_info* info, const void* d_blob, const void* d_x,
+                                 int64_t m, float* d_y, float* d_dequant, void* d_workspace,
+                                 uint64_t ws_bytes, int32_t* d_status, void* hip_stream) {
+  return ep::decode_gemm(info, d_blob, d_x, m, d_y, d_dequant, d_workspace, ws_bytes, d_status,
+                         hip_stream, true, true, "ep_decode_gemm_bf16_prepared");
 }
 
 uint64_t ep_decode_layers_workspace(int n) { return ep::decode_layers_workspace(n); }

@@ -3,7 +3,7 @@
 // and most kernels), decode_args.hip and decode_mixed.hip, which instantiate
 // the remaining kernels, so that the three compile concurrently.
 //
-// One wavefront (64 lanes) decodes two tiles at once: lanes 0-31 hold the 32
+// A chain is one wavefront (64 lanes) over two tiles: lanes 0-31 hold the 32
 // interleaved rANS states of the first tile, lanes 32-63 those of the second.
 // Each lane decodes whole 8-vectors: the coset symbol with the two-entry coset
 // table, then the eight fields with the tables selected by that coset
@@ -12,11 +12,12 @@
 // vector's ninth symbol is known the lane inverts the field map
 // (eq. point_inverse), multiplies by the FP32 row scale and snaps to the
 // output dtype (eq. recon), and stores the eight weights; no symbol tensor is
-// ever written.
+// ever written.  A wave interleaves two chains (a four-tile task), or runs one
+// (a two-tile task) in launches with too few four-tile tasks to fill the SIMDs.
 //
-// Workgroups are persistent: each takes a contiguous range of two-tile tasks,
-// builds the decode tables of the layer it is working on in LDS, and its 16
-// waves walk the range.  Two table families exist:
+// Workgroups are persistent: each takes a contiguous range of tasks, builds
+// (or copies in) the decode tables of the layer it is working on in LDS, and
+// its 16 waves walk the range.  Four table layouts exist:
 //   kPathLut    packed slot table, one LDS read per symbol: for table
 //               (field i, coset c) and slot u in [0, 2^b) the 32-bit entry
 //               holds f (bits 0-11), u - F (bits 12-22) and, as a signed
@@ -2094,8 +2095,8 @@ __device__ __forceinline__ void build_tables(const LayerDev& L, uint32_t* lds) {
 // precision the encoder starts from for targets up to 7 bpp) and the search
 // path decode them in a steady-state pass; otherwise the generic loop does.
 constexpr int kChains = 2;                 // chains of the generic loop
-// A task is one pass of a wave: two chains of two tiles.  (Small layer lists
-// then spread over more waves, which shortens the serial chain each wave runs.)
+// A task is one pass of a wave: two chains of two tiles, or in a launch with
+// few tasks (LayerDev::tpt = 2) one chain of two tiles.
 constexpr uint32_t kTilesPerTask = 4;
 static_assert(kChains == 2, "the generic loop and the search steady state advance two chains");
 static_assert(kTilesPerTask == 2 * kChains, "task granularity: one four-tile pass");
@@ -2211,7 +2212,8 @@ __device__ __forceinline__ void run_layers(const LayerDev* layers, int n_layers,
         default: run_segment<kPathGlobal, DOT>(L, lds, seg, seg_end, status); break;
       }
     } else {
-      // the mixed-path kernel never runs two-tile tasks (use_small_tasks)
+      // a single-path kernel may run two-tile tasks; the mixed-path kernel
+      // (above) never does (use_small_tasks)
       run_segment<PATH, DOT, true>(L, lds, seg, seg_end, status);
     }
     seg = seg_end;
@@ -2276,10 +2278,12 @@ __global__ __launch_bounds__(kThreads) void decode_ws_kernel(const LayerDev* __r
 // tile can span a block boundary: both blocks decode it, each keeping the rows
 // it owns (the slab has `margin` rows on either side for the rest).
 typedef int v4i_t __attribute__((ext_vector_type(4)));
+typedef float v4f_t __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf_t __attribute__((ext_vector_type(8)));
 
 struct GemmArgs {
-  const int8_t* x;       // m x C, row-major
-  int32_t* y;            // m x R, row-major (cleared first when K is split over waves)
+  const void* x;         // m x C, row-major: int8, or bf16 for the BF16 product
+  void* y;               // m x R, row-major: int32, or fp32 (cleared first when K is split over waves)
   uint8_t* slabs;        // one slab per workgroup
   uint64_t slab_bytes;   // (RB + 2 margin) x C, rounded up to 256
   uint32_t m, margin, n_blocks, rows_per_block;
@@ -2301,11 +2305,16 @@ struct GemmLaunch {
 // accumulator r of lane l is element (4 (l / 16) + r, l mod 16) of a 16 x 16
 // result.
 constexpr uint32_t kGemmMaxTiles = 4;   // NT <= 4: blocks of at most 64 rows
-template <uint32_t NT>
+//
+// BF: the BF16 product (bf16 X and slab, v_mfma_f32_16x16x32_bf16, fp32 Y).
+// A lane's 16 bytes of a 64-byte K step are then 8 bf16 elements, the same
+// bytes as 16 int8 ones, so the addressing below is in bytes for both; the
+// sums are fp32 and K slices add them with float atomics.
+template <uint32_t NT, bool BF>
 __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmArgs& g,
                                                  const uint8_t* slab, uint32_t b) {
   const uint32_t wave = wave_id(), lane = threadIdx.x & 63;
-  const uint32_t C = L.cols, m = g.m, RB = g.rows_per_block;
+  const uint32_t C = L.cols * (BF ? 2 : 1), m = g.m, RB = g.rows_per_block;   // C: row bytes
   const uint32_t T = (m + 15) / 16;
   const uint32_t S = T >= kWavesPerGroup ? 1u : kWavesPerGroup / T;   // K slices
   if (T < kWavesPerGroup && wave >= T * S) return;
@@ -2319,12 +2328,14 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
   const uint32_t groups = (C + 127) / 128, gper = (groups + S - 1) / S;
   const uint32_t k_begin = slice * gper * 128, k_end = min(C, (slice + 1) * gper * 128);
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<int8_t*>(g.x), (short)0, (int)((uint64_t)m * C), 0x00020000);
+      const_cast<void*>(g.x), (short)0, (int)((uint64_t)m * C), 0x00020000);
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(slab), (short)0, (int)g.slab_bytes, 0x00020000);
   const uint32_t li = lane & 15, q = lane >> 4;
   const uint32_t row0 = b * RB;
-  EP_GLOBAL int32_t* y = gptr<int32_t>(g.y);
+  using Acc = typename std::conditional<BF, v4f_t, v4i_t>::type;
+  using Out = typename std::conditional<BF, float, int32_t>::type;
+  EP_GLOBAL Out* y = gptr<Out>(g.y);
   // one group's fragments: X and the NT slab tiles for kGroup 64-byte K steps
   struct Frags {
     v4i_t a[kGroup], w[kGroup][NT];
@@ -2332,17 +2343,17 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
   for (uint32_t tt = tt0; tt < T; tt += tstep) {
     const uint32_t tok = 16 * tt + li;
     const uint32_t xrow = tok * C;
-    v4i_t acc[NT];
+    Acc acc[NT];
 #pragma unroll
-    for (uint32_t c = 0; c < NT; c++) acc[c] = v4i_t{0, 0, 0, 0};
+    for (uint32_t c = 0; c < NT; c++) acc[c] = Acc{0, 0, 0, 0};
     // bytes at or past k_end read as zeros (bounded buffer loads), so the
     // prefetch past the slice's end and a partial last group add nothing
     auto load = [&](uint32_t k0, Frags& f) {
 #pragma unroll
       for (uint32_t u = 0; u < kGroup; u++) {
         const uint32_t kq = k0 + 64 * u + 16 * q;
-        // K beyond the row (C % 64 != 0) reads as zeros of X: C is a multiple of 8,
-        // so a lane's 16 bytes are whole, half (the upper 8 beyond C) or none
+        // K beyond the row (C % 64 != 0) reads as zeros of X: C is a multiple of 8
+        // bytes, so a lane's 16 bytes are whole, half (the upper 8 beyond C) or none
         const bool in = kq < k_end && tok < m;
         v4i_t av = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(xr, in ? xrow + kq : 0x80000000u, 0, 0);
         if (in && kq + 8 >= C) av[2] = av[3] = 0;
@@ -2359,8 +2370,14 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
 #pragma unroll
       for (uint32_t u = 0; u < kGroup; u++)
 #pragma unroll
-        for (uint32_t c = 0; c < NT; c++)
-          acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(f.a[u], f.w[u][c], acc[c], 0, 0, 0);
+        for (uint32_t c = 0; c < NT; c++) {
+          if constexpr (BF)
+            acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf_t, f.a[u]),
+                                                             __builtin_bit_cast(v8bf_t, f.w[u][c]), acc[c], 0,
+                                                             0, 0);
+          else
+            acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(f.a[u], f.w[u][c], acc[c], 0, 0, 0);
+        }
     };
     // two groups in flight: the next group's loads are issued before this
     // group's MFMAs wait for their operands
@@ -2380,8 +2397,15 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
       for (uint32_t r = 0; r < 4; r++) {
         const uint32_t t = 16 * tt + 4 * q + r;
         if (t < m && rl < RB && row < L.rows) {
-          if (S > 1) add_i32(y + (uint64_t)t * L.rows + row, acc[c][r]);
-          else y[(uint64_t)t * L.rows + row] = acc[c][r];
+          if (S > 1) {
+            if constexpr (BF)
+              __hip_atomic_fetch_add(y + (uint64_t)t * L.rows + row, acc[c][r], __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+            else
+              add_i32(y + (uint64_t)t * L.rows + row, acc[c][r]);
+          } else {
+            y[(uint64_t)t * L.rows + row] = acc[c][r];
+          }
         }
       }
     }
@@ -2390,17 +2414,19 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
 
 // Block b's rows times X, from the slab (row i of the block at slab row
 // margin + i), for NT = ceil(RB / 16) tiles of 16 block rows.
+template <bool BF>
 __device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs& g,
                                               const uint8_t* slab, uint32_t b) {
   switch (uni((g.rows_per_block + 15) / 16)) {
-    case 1: block_product_nt<1>(L, g, slab, b); break;
-    case 2: block_product_nt<2>(L, g, slab, b); break;
-    case 3: block_product_nt<3>(L, g, slab, b); break;
-    default: block_product_nt<4>(L, g, slab, b); break;
+    case 1: block_product_nt<1, BF>(L, g, slab, b); break;
+    case 2: block_product_nt<2, BF>(L, g, slab, b); break;
+    case 3: block_product_nt<3, BF>(L, g, slab, b); break;
+    default: block_product_nt<4, BF>(L, g, slab, b); break;
   }
 }
 
-template <int PATH>
+// BF: the BF16 product (the slab holds the bf16 decode of the tiles).
+template <int PATH, bool BF>
 __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch launch, int32_t* status) {
 #if defined(__HIP_DEVICE_COMPILE__)
   (void)launch;
@@ -2411,7 +2437,7 @@ __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch 
   extern __shared__ uint32_t lds[];
   const LayerDev& L = A.L;
   const GemmArgs& g = A.g;
-  if (L.tables) load_tables<PATH>(L, lds);   // prepared by ep_decode_gemm_i8_prepare
+  if (L.tables) load_tables<PATH>(L, lds);   // prepared by ep_decode_gemm_prepare
   else build_tables<PATH>(L, lds);
   __syncthreads();
   const uint32_t ring_area = uni(ring_offset<PATH>(L));
@@ -2431,13 +2457,13 @@ __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch 
     const uint32_t t_end = (uint32_t)((v_end + L.V - 1) / L.V);
     H.tile_begin = uni((uint32_t)(v_first / L.V) / kTilesPerTask * kTilesPerTask);
     H.tile_end = uni(min(L.tile_end, (t_end + kTilesPerTask - 1) / kTilesPerTask * kTilesPerTask));
-    const int64_t shift = ((int64_t)b * RB - (int64_t)g.margin) * (int64_t)L.cols;
+    const int64_t shift = ((int64_t)b * RB - (int64_t)g.margin) * (int64_t)L.cols * (BF ? 2 : 1);
     H.out = uni_ptr(reinterpret_cast<void*>(reinterpret_cast<intptr_t>(slab) - (intptr_t)shift));
     const uint32_t tasks = (H.tile_end - H.tile_begin + kTilesPerTask - 1) / kTilesPerTask;
     for (uint32_t task = wave_id(); task < tasks; task += kWavesPerGroup)
       dispatch_task<PATH, false>(H, lds, lb, ring_area, task, status);
     __syncthreads();   // the block's rows are in the slab
-    block_product(L, g, slab, b);
+    block_product<BF>(L, g, slab, b);
     __syncthreads();   // every wave is done with the slab
   }
 }

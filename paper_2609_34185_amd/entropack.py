@@ -118,6 +118,12 @@ def lib():
         L.ep_decode_gemm_i8_prepared.argtypes = [C.POINTER(TensorInfo), vp, vp, i64, vp, vp, vp, u64,
                                                  vp, vp]
         L.ep_decode_gemm_i8_prepare.argtypes = [C.POINTER(TensorInfo), vp, vp, u64, vp]
+        L.ep_decode_gemm_bf16.argtypes = [C.POINTER(TensorInfo), vp, vp, i64, vp, vp, vp, u64, vp, vp]
+        L.ep_decode_gemm_bf16_prepared.argtypes = [C.POINTER(TensorInfo), vp, vp, i64, vp, vp, vp, u64,
+                                                   vp, vp]
+        L.ep_decode_gemm_bf16_prepare.argtypes = [C.POINTER(TensorInfo), vp, vp, u64, vp]
+        L.ep_decode_gemm_bf16_workspace.argtypes = [C.POINTER(TensorInfo)]
+        L.ep_decode_gemm_bf16_workspace.restype = u64
         L.ep_decode_gemm_i8_workspace.argtypes = [C.POINTER(TensorInfo)]
         L.ep_decode_gemm_i8_workspace.restype = u64
         L.ep_last_error.restype = C.c_char_p
@@ -131,6 +137,8 @@ EXPORTS = ["ep_encode_params_default", "ep_encode_cpu", "ep_encode_gpu", "ep_blo
            "ep_stack_workspace", "ep_stack_prepare", "ep_stack_decode", "ep_gemm_i8_nt",
            "ep_decode_matmul_i8", "ep_decode_gemm_i8", "ep_decode_gemm_i8_workspace",
            "ep_decode_gemm_i8_prepare", "ep_decode_gemm_i8_prepared",
+           "ep_decode_gemm_bf16", "ep_decode_gemm_bf16_workspace", "ep_decode_gemm_bf16_prepare",
+           "ep_decode_gemm_bf16_prepared",
            "ep_last_error"]
 
 
@@ -278,6 +286,32 @@ def decode_gemm_i8_prepared(info: TensorInfo, d_blob: int, d_x: int, m: int, d_y
     _check(lib().ep_decode_gemm_i8_prepared(C.byref(info), d_blob, d_x, m, d_y, d_dequant or None,
                                             d_ws, ws_bytes, d_status or None, stream or None),
            "ep_decode_gemm_i8_prepared")
+
+
+def decode_gemm_bf16_workspace(info: TensorInfo) -> int:
+    return int(lib().ep_decode_gemm_bf16_workspace(C.byref(info)))
+
+
+def decode_gemm_bf16(info: TensorInfo, d_blob: int, d_x: int, m: int, d_y: int, d_ws: int,
+                     ws_bytes: int, d_dequant: int = 0, d_status: int = 0, stream: int = 0):
+    """Y (m x R fp32) = X (m x C bf16) times the tensor's bf16 decode, transposed, on the
+    matrix cores, for any m (the fused decode and BF16 MFMA product)."""
+    _check(lib().ep_decode_gemm_bf16(C.byref(info), d_blob, d_x, m, d_y, d_dequant or None, d_ws,
+                                     ws_bytes, d_status or None, stream or None), "ep_decode_gemm_bf16")
+
+
+def decode_gemm_bf16_prepare(info: TensorInfo, d_blob: int, d_ws: int, ws_bytes: int, stream: int = 0):
+    """Build the tensor's decode tables once into the workspace (synchronous)."""
+    _check(lib().ep_decode_gemm_bf16_prepare(C.byref(info), d_blob, d_ws, ws_bytes, stream or None),
+           "ep_decode_gemm_bf16_prepare")
+
+
+def decode_gemm_bf16_prepared(info: TensorInfo, d_blob: int, d_x: int, m: int, d_y: int, d_ws: int,
+                              ws_bytes: int, d_dequant: int = 0, d_status: int = 0, stream: int = 0):
+    """decode_gemm_bf16 on a workspace that decode_gemm_bf16_prepare filled for this blob."""
+    _check(lib().ep_decode_gemm_bf16_prepared(C.byref(info), d_blob, d_x, m, d_y, d_dequant or None,
+                                              d_ws, ws_bytes, d_status or None, stream or None),
+           "ep_decode_gemm_bf16_prepared")
 
 
 # ---- torch conveniences (device memory and streams only) ------------------------

@@ -246,3 +246,136 @@ def test_fused_mfma_product_rejects_bad_arguments(E, oracle):
             rc = lib.ep_decode_gemm_i8_prepare(E.C.byref(info), d_blob.data_ptr(), d_ws.data_ptr(),
                                                wsb, None)
             assert rc == code
+
+
+# ---- the fused decode and BF16 MFMA product --------------------------------------
+def bf16_bits(f: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (nearest even) and return the bits."""
+    u = np.ascontiguousarray(f, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def bf16_values(bits: np.ndarray) -> np.ndarray:
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def bf16_activations(seed: int, m: int, cols: int) -> np.ndarray:
+    return bf16_bits(np.random.default_rng(seed).standard_normal((m, cols)).astype(np.float32))
+
+
+def fused_bf16(E, blob: np.ndarray, xbits: np.ndarray, prepared: bool = False, twice: bool = False):
+    """(Y fp32, delta, status) of ep_decode_gemm_bf16 on the GPU; Y starts as garbage."""
+    info = E.blob_info(blob)
+    d_blob = torch.from_numpy(blob).cuda()
+    d_x = torch.from_numpy(np.ascontiguousarray(xbits).view(np.int16)).cuda()
+    m = xbits.shape[0]
+    y = torch.full((m, info.rows), 7.0, dtype=torch.float32, device="cuda")
+    dq = torch.zeros(info.rows, dtype=torch.float32, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = E.decode_gemm_bf16_workspace(info)
+    d_ws = torch.full((max(1, ws),), 0xA5, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    run = E.decode_gemm_bf16
+    if prepared:
+        E.decode_gemm_bf16_prepare(info, d_blob.data_ptr(), d_ws.data_ptr(), ws, s)
+        run = E.decode_gemm_bf16_prepared
+    for _ in range(2 if twice else 1):
+        run(info, d_blob.data_ptr(), d_x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
+            dq.data_ptr(), st.data_ptr(), s)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), dq.cpu().numpy(), int(st.item())
+
+
+def check_bf16_product(oracle, blob: np.ndarray, xbits: np.ndarray, y: np.ndarray):
+    """Y against the exact product of the oracle's bf16 decode, within the fp32 summation
+    bound: every product of two bf16 values is exact in fp32, and at most C + 16 + 2
+    roundings of 2^-24 relative size fall on any partial sum, so
+    |Y - X W'^T| <= (C + 18) 2^-24 sum_j |X[t][j] W'[r][j]|."""
+    wbits, _ = oracle.decode(blob, oracle.BF16)
+    w = bf16_values(wbits)
+    x = bf16_values(xbits)
+    exact = x @ w.T
+    bound = (x.shape[1] + 18) * 2.0 ** -24 * (np.abs(x) @ np.abs(w).T)
+    err = np.abs(y.astype(np.float64) - exact)
+    worst = np.argmax(err - bound)
+    assert (err <= bound).all(), (f"{int((err > bound).sum())} elements beyond the bound; worst "
+                                  f"{np.unravel_index(worst, err.shape)}: err {err.flat[worst]:.3e} "
+                                  f"bound {bound.flat[worst]:.3e}")
+    # the bound is a small fraction of Y's typical size, so a wrong row, column or scale
+    # (errors of that size) cannot hide within it
+    assert np.median(bound) < 0.05 * np.sqrt(np.mean(exact ** 2))
+
+
+BF16_CASES = [
+    # name, generator, target, encode kwargs, rows of X
+    ("direct_long_rows_m16", lambda: W.ragged_tensor(61, 96, 8 * 1000), 4.0, {}, 16),
+    ("direct_m1", lambda: W.ragged_tensor(62, 40, 8 * 700), 3.0, {}, 1),
+    ("direct_m17_short_rows", lambda: W.ragged_tensor(63, 300, 512), 4.0, {}, 17),
+    ("direct_m64_ragged_tiles", lambda: W.ragged_tensor(64, 41, 8 * 333), 5.0, dict(tile_vectors=96), 64),
+    ("direct_m300", lambda: W.ragged_tensor(65, 20, 8 * 300), 4.0, {}, 300),
+    ("direct_b12_search_m20", lambda: W.ragged_tensor(66, 64, 8 * 600), 4.0, dict(prob_bits=12), 20),
+    ("int8_container_m16", lambda: W.ragged_tensor(67, 64, 8 * 777, scale=0.05), 6.0,
+     dict(container="INT8"), 16),
+    ("fp8_container_m33", lambda: W.ragged_tensor(68, 50, 8 * 640, scale=0.05), 4.0,
+     dict(container="FP8"), 33),
+]
+
+
+@pytest.mark.parametrize("prepared", [False, True], ids=["tables_built", "tables_prepared"])
+@pytest.mark.parametrize("name,gen,target,kw,m", BF16_CASES, ids=[c[0] for c in BF16_CASES])
+def test_fused_bf16_product_matches_oracle(E, oracle, name, gen, target, kw, m, prepared):
+    """Every element of Y within the fp32 summation bound of the exact product of the oracle's
+    bf16 decode: direct blobs and both containers, rows longer and shorter than a tile,
+    ragged tiles, the search path, 1 to 300 rows of X (K split over waves below 256 rows), two
+    calls into the same Y, and the tables built in every workgroup or prepared."""
+    w = gen()
+    kw = dict(kw)
+    if kw.get("container") == "INT8":
+        kw["container"] = oracle.CONT_INT8
+    elif kw.get("container") == "FP8":
+        kw["container"] = oracle.CONT_FP8
+    say(f"  fused BF16 {name}: {w.shape} at {target}, m = {m}, prepared = {prepared}")
+    blob, _ = oracle.encode(w, target, **kw)
+    xbits = bf16_activations(200 + len(name), m, w.shape[1])
+    y, dq, st = fused_bf16(E, blob, xbits, prepared=prepared, twice=True)
+    assert st == 0
+    check_bf16_product(oracle, blob, xbits, y)
+    if E.blob_info(blob).container:
+        assert np.array_equal(dq, oracle.decode(blob, oracle.BF16)[1])
+
+
+def test_fused_bf16_product_dit_layer(E, oracle):
+    """The diffusion-transformer MLP input projection (10240 x 3840 at 2.5 bpp, the paper's
+    reference-layer shape) times 16 and 64 rows of bf16 activations: every element within
+    the bound."""
+    w = dict(W.dit_block(0))["blocks.0.mlp_in"]
+    blob, _ = E.encode(w, 2.5)
+    for m, prepared in ((16, False), (64, True)):
+        say(f"  fused BF16 DiT mlp_in: m = {m}, prepared = {prepared}")
+        xbits = bf16_activations(300 + m, m, w.shape[1])
+        y, _, st = fused_bf16(E, blob, xbits, prepared=prepared)
+        assert st == 0
+        check_bf16_product(oracle, blob, xbits, y)
+
+
+def test_fused_bf16_product_rejects_bad_arguments(E, oracle):
+    w = W.ragged_tensor(69, 32, 256)
+    blob, _ = oracle.encode(w, 4.0)
+    info = E.blob_info(blob)
+    d_blob = torch.from_numpy(blob).cuda()
+    x = torch.zeros((20, 256), dtype=torch.int16, device="cuda")
+    y = torch.zeros((20, 32), dtype=torch.float32, device="cuda")
+    ws = E.decode_gemm_bf16_workspace(info)
+    assert ws > E.decode_gemm_i8_workspace(info)   # bf16 slabs are twice the size
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    lib = E.lib()
+    for m, wsb in ((0, ws), (70000, ws), (20, ws - 1)):
+        for fn in (lib.ep_decode_gemm_bf16, lib.ep_decode_gemm_bf16_prepared):
+            rc = fn(E.C.byref(info), d_blob.data_ptr(), x.data_ptr(), m, y.data_ptr(), None,
+                    d_ws.data_ptr(), wsb, None, None)
+            assert rc == E.ERR_ARG
+    assert lib.ep_decode_gemm_bf16_prepare(E.C.byref(info), d_blob.data_ptr(), d_ws.data_ptr(), ws - 1,
+                                           None) == E.ERR_ARG
+    # the INT8 product refuses a tensor outside the INT8 container; the BF16 one takes it
+    assert lib.ep_decode_gemm_i8(E.C.byref(info), d_blob.data_ptr(), x.data_ptr(), 20, y.data_ptr(),
+                                 None, d_ws.data_ptr(), ws, None, None) == E.ERR_UNSUPPORTED
