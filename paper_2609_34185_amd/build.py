@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libentropack.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 HOST_SRC = ["encode.cpp", "capi.cpp"]
-HIP_SRC = ["decode.hip", "decode_args.hip", "decode_mixed.hip", "gemm_i8.hip", "encode_gpu.hip"]
+HIP_SRC = ["decode.hip", "decode_args.hip", "decode_mixed.hip", "decode_gemm.hip", "gemm_i8.hip", "encode_gpu.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off"]
 HIP_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-munsafe-fp-atomics"]

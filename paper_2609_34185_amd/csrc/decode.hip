@@ -396,27 +396,6 @@ int decode_gemm_prepare(const ep_tensor_info* info, const void* d_blob, void* d_
   return EP_OK;
 }
 
-template <bool BF>
-const void* gemm_kernel_fn(uint32_t path) {
-  return path == kPathLut ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathLut, BF>)
-         : path == kPathWide ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathWide, BF>)
-         : path == kPathSearch ? reinterpret_cast<const void*>(&decode_gemm_kernel<kPathSearch, BF>)
-                               : reinterpret_cast<const void*>(&decode_gemm_kernel<kPathGlobal, BF>);
-}
-
-template <bool BF>
-void launch_gemm(uint32_t path, uint32_t groups, uint32_t lds, hipStream_t s, const GemmLaunch& A,
-                 int32_t* st) {
-  if (path == kPathLut)
-    hipLaunchKernelGGL((decode_gemm_kernel<kPathLut, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
-  else if (path == kPathWide)
-    hipLaunchKernelGGL((decode_gemm_kernel<kPathWide, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
-  else if (path == kPathSearch)
-    hipLaunchKernelGGL((decode_gemm_kernel<kPathSearch, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
-  else
-    hipLaunchKernelGGL((decode_gemm_kernel<kPathGlobal, BF>), dim3(groups), dim3(kThreads), lds, s, A, st);
-}
-
 // The fused decode and MFMA product: INT8 (bf = false: int8 X, int32 Y, the
 // INT8 container's values) or BF16 (bf16 X, fp32 Y, the bf16 decode).
 // prepared: the workspace holds this tensor's tables (decode_gemm_prepare).
@@ -451,17 +430,16 @@ int decode_gemm(const ep_tensor_info* info, const void* d_blob, const void* d_x,
   A.g.rows_per_block = G.rows_per_block;
   hipStream_t s = static_cast<hipStream_t>(stream);
   // partial sums are added with atomics (0 is also +0.0f for the BF16 product)
-  if ((uint32_t)((m + 15) / 16) < kWavesPerGroup &&
+  if (gemm_splits_k((G.rows_per_block + 15) / 16, (uint32_t)((m + 15) / 16)) &&
       !clear_i32(static_cast<int32_t*>(d_y), (int64_t)m * info->rows, s))
     return fail(EP_ERR_HIP, (w + ": clearing Y failed").c_str());
   const uint32_t lds = lds_bytes(info->path, *info);
   DeviceProps P = device_props();
   if (lds > P.max_lds) return fail(EP_ERR_UNSUPPORTED, (w + ": tables exceed the device LDS").c_str());
-  const void* fn = bf ? gemm_kernel_fn<true>(info->path) : gemm_kernel_fn<false>(info->path);
-  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+  const bool wide = gemm_wide((uint32_t)((m + 15) / 16));
+  if (set_gemm_lds_limit(info->path, bf, wide, lds) != hipSuccess)
     return fail(EP_ERR_HIP, (w + ": cannot raise the kernel's LDS limit").c_str());
-  if (bf) launch_gemm<true>(info->path, G.groups, lds, s, A, d_status);
-  else launch_gemm<false>(info->path, G.groups, lds, s, A, d_status);
+  launch_gemm(info->path, bf, wide, &A, G.groups, lds, d_status, s);
   if (hipGetLastError() != hipSuccess) return fail(EP_ERR_HIP, (w + ": launch failed").c_str());
   return EP_OK;
 }

@@ -1,7 +1,8 @@
 // Device side of the fused decode (Section 3.7): tables, steady states,
 // generic loop and the kernel templates.  Included by decode.hip (host code
-// and most kernels), decode_args.hip and decode_mixed.hip, which instantiate
-// the remaining kernels, so that the three compile concurrently.
+// and most kernels), decode_args.hip, decode_mixed.hip and decode_gemm.hip,
+// which instantiate the remaining kernels, so that the four compile
+// concurrently.
 //
 // A chain is one wavefront (64 lanes) over two tiles: lanes 0-31 hold the 32
 // interleaved rANS states of the first tile, lanes 32-63 those of the second.
@@ -2294,36 +2295,36 @@ struct GemmLaunch {
   GemmArgs g;
 };
 
-// The product of one block: a work item is one tile of 16 rows of X against
+// The product of one block: a work item is XT tiles of 16 rows of X against
 // all NT = ceil(RB / 16) tiles of 16 block rows, so each X fragment is loaded
-// once per block; items are dealt to the waves, and when there are fewer items
-// than waves K is split over the idle waves and the partial sums are added
-// with atomics (exact, order-free integer additions).  NT is a template
-// argument so that no load is issued for a tile the block does not have.  MFMA
-// operands: lane l supplies row l mod 16 of the X tile and of the slab tile, 16
-// consecutive bytes of K each (k = 16 (l / 16) + 0..15 of a 64-byte step);
-// accumulator r of lane l is element (4 (l / 16) + r, l mod 16) of a 16 x 16
-// result.
+// once per block and each slab fragment once per item; items are dealt to the
+// waves, and when there are fewer items than waves K is split over the idle
+// waves and the partial sums are added with atomics (exact, order-free integer
+// additions).  NT and XT are template arguments so that no load is issued for
+// a tile the block does not have.  MFMA operands: lane l supplies row l mod 16
+// of an X tile and of a slab tile, 16 consecutive bytes of K each
+// (k = 16 (l / 16) + 0..15 of a 64-byte step); accumulator r of lane l is
+// element (4 (l / 16) + r, l mod 16) of a 16 x 16 result.
 constexpr uint32_t kGemmMaxTiles = 4;   // NT <= 4: blocks of at most 64 rows
 //
 // BF: the BF16 product (bf16 X and slab, v_mfma_f32_16x16x32_bf16, fp32 Y).
 // A lane's 16 bytes of a 64-byte K step are then 8 bf16 elements, the same
 // bytes as 16 int8 ones, so the addressing below is in bytes for both; the
 // sums are fp32 and K slices add them with float atomics.
-template <uint32_t NT, bool BF>
+template <uint32_t NT, uint32_t XT, bool BF>
 __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmArgs& g,
                                                  const uint8_t* slab, uint32_t b) {
   const uint32_t wave = wave_id(), lane = threadIdx.x & 63;
   const uint32_t C = L.cols * (BF ? 2 : 1), m = g.m, RB = g.rows_per_block;   // C: row bytes
-  const uint32_t T = (m + 15) / 16;
-  const uint32_t S = T >= kWavesPerGroup ? 1u : kWavesPerGroup / T;   // K slices
-  if (T < kWavesPerGroup && wave >= T * S) return;
-  const uint32_t slice = T >= kWavesPerGroup ? 0u : wave / T;
-  const uint32_t tt0 = T >= kWavesPerGroup ? wave : wave % T;
-  const uint32_t tstep = T >= kWavesPerGroup ? kWavesPerGroup : T;
+  const uint32_t T = (m + 15) / 16, I = (T + XT - 1) / XT;   // X tiles, items
+  const uint32_t S = I >= kWavesPerGroup ? 1u : kWavesPerGroup / I;   // K slices
+  if (I < kWavesPerGroup && wave >= I * S) return;
+  const uint32_t slice = I >= kWavesPerGroup ? 0u : wave / I;
+  const uint32_t it0 = I >= kWavesPerGroup ? wave : wave % I;
+  const uint32_t istep = I >= kWavesPerGroup ? kWavesPerGroup : I;
   // 64-byte K steps per group: two groups' fragments stay within the
-  // registers the decode leaves (2 (1 + NT) kGroup fragments of 4 VGPRs)
-  constexpr uint32_t kGroup = NT <= 2 ? 2 : 1;
+  // registers the decode leaves (2 (XT + NT) kGroup fragments of 4 VGPRs)
+  constexpr uint32_t kGroup = XT + NT <= 3 ? 2 : 1;
   // slices are cut at 128-byte boundaries whatever the group
   const uint32_t groups = (C + 127) / 128, gper = (groups + S - 1) / S;
   const uint32_t k_begin = slice * gper * 128, k_end = min(C, (slice + 1) * gper * 128);
@@ -2336,28 +2337,33 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
   using Acc = typename std::conditional<BF, v4f_t, v4i_t>::type;
   using Out = typename std::conditional<BF, float, int32_t>::type;
   EP_GLOBAL Out* y = gptr<Out>(g.y);
-  // one group's fragments: X and the NT slab tiles for kGroup 64-byte K steps
+  // one group's fragments: XT X tiles and the NT slab tiles for kGroup 64-byte K steps
   struct Frags {
-    v4i_t a[kGroup], w[kGroup][NT];
+    v4i_t a[kGroup][XT], w[kGroup][NT];
   };
-  for (uint32_t tt = tt0; tt < T; tt += tstep) {
-    const uint32_t tok = 16 * tt + li;
-    const uint32_t xrow = tok * C;
-    Acc acc[NT];
+  for (uint32_t it = it0; it < I; it += istep) {
+    Acc acc[XT][NT];
 #pragma unroll
-    for (uint32_t c = 0; c < NT; c++) acc[c] = Acc{0, 0, 0, 0};
+    for (uint32_t x = 0; x < XT; x++)
+#pragma unroll
+      for (uint32_t c = 0; c < NT; c++) acc[x][c] = Acc{0, 0, 0, 0};
     // bytes at or past k_end read as zeros (bounded buffer loads), so the
-    // prefetch past the slice's end and a partial last group add nothing
+    // prefetch past the slice's end and a partial last group add nothing; so
+    // do the rows of X past m (a last item with fewer than XT tiles)
     auto load = [&](uint32_t k0, Frags& f) {
 #pragma unroll
       for (uint32_t u = 0; u < kGroup; u++) {
         const uint32_t kq = k0 + 64 * u + 16 * q;
-        // K beyond the row (C % 64 != 0) reads as zeros of X: C is a multiple of 8
-        // bytes, so a lane's 16 bytes are whole, half (the upper 8 beyond C) or none
-        const bool in = kq < k_end && tok < m;
-        v4i_t av = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(xr, in ? xrow + kq : 0x80000000u, 0, 0);
-        if (in && kq + 8 >= C) av[2] = av[3] = 0;
-        f.a[u] = av;
+#pragma unroll
+        for (uint32_t x = 0; x < XT; x++) {
+          const uint32_t tok = 16 * (XT * it + x) + li;
+          // K beyond the row (C % 64 != 0) reads as zeros of X: C is a multiple of 8
+          // bytes, so a lane's 16 bytes are whole, half (the upper 8 beyond C) or none
+          const bool in = kq < k_end && tok < m;
+          v4i_t av = (v4i_t)__builtin_amdgcn_raw_buffer_load_b128(xr, in ? tok * C + kq : 0x80000000u, 0, 0);
+          if (in && kq + 8 >= C) av[2] = av[3] = 0;
+          f.a[u][x] = av;
+        }
 #pragma unroll
         for (uint32_t c = 0; c < NT; c++) {
           const uint32_t wrow = (g.margin + 16 * c + li) * C;   // slab offset of the lane's W' row
@@ -2370,14 +2376,16 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
 #pragma unroll
       for (uint32_t u = 0; u < kGroup; u++)
 #pragma unroll
-        for (uint32_t c = 0; c < NT; c++) {
-          if constexpr (BF)
-            acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf_t, f.a[u]),
-                                                             __builtin_bit_cast(v8bf_t, f.w[u][c]), acc[c], 0,
-                                                             0, 0);
-          else
-            acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(f.a[u], f.w[u][c], acc[c], 0, 0, 0);
-        }
+        for (uint32_t x = 0; x < XT; x++)
+#pragma unroll
+          for (uint32_t c = 0; c < NT; c++) {
+            if constexpr (BF)
+              acc[x][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(v8bf_t, f.a[u][x]), __builtin_bit_cast(v8bf_t, f.w[u][c]), acc[x][c],
+                  0, 0, 0);
+            else
+              acc[x][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(f.a[u][x], f.w[u][c], acc[x][c], 0, 0, 0);
+          }
     };
     // two groups in flight: the next group's loads are issued before this
     // group's MFMAs wait for their operands
@@ -2391,42 +2399,67 @@ __device__ __forceinline__ void block_product_nt(const LayerDev& L, const GemmAr
       mma(f1);
     }
 #pragma unroll
-    for (uint32_t c = 0; c < NT; c++) {
-      const uint32_t rl = 16 * c + li, row = row0 + rl;
+    for (uint32_t x = 0; x < XT; x++)
 #pragma unroll
-      for (uint32_t r = 0; r < 4; r++) {
-        const uint32_t t = 16 * tt + 4 * q + r;
-        if (t < m && rl < RB && row < L.rows) {
-          if (S > 1) {
-            if constexpr (BF)
-              __hip_atomic_fetch_add(y + (uint64_t)t * L.rows + row, acc[c][r], __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
-            else
-              add_i32(y + (uint64_t)t * L.rows + row, acc[c][r]);
-          } else {
-            y[(uint64_t)t * L.rows + row] = acc[c][r];
+      for (uint32_t c = 0; c < NT; c++) {
+        const uint32_t rl = 16 * c + li, row = row0 + rl;
+#pragma unroll
+        for (uint32_t r = 0; r < 4; r++) {
+          const uint32_t t = 16 * (XT * it + x) + 4 * q + r;
+          if (t < m && rl < RB && row < L.rows) {
+            if (S > 1) {
+              if constexpr (BF)
+                __hip_atomic_fetch_add(y + (uint64_t)t * L.rows + row, acc[x][c][r], __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+              else
+                add_i32(y + (uint64_t)t * L.rows + row, acc[x][c][r]);
+            } else {
+              y[(uint64_t)t * L.rows + row] = acc[x][c][r];
+            }
           }
         }
       }
-    }
   }
+}
+
+// Whether a product of T tiles of X (16 rows each) takes the kernels whose work
+// items hold several X tiles: more than 32 rows of X.
+__host__ __device__ inline bool gemm_wide(uint32_t t) { return t > 2; }
+
+// X tiles per work item of a block's product, for NT slab tiles and T tiles of
+// X: one in the kernels for up to 32 rows of X; above, four when the block has
+// a single slab tile, two when it has two or three.  2 kGroup (XT + NT)
+// fragments and XT NT accumulators of 4 VGPRs each (at most 64 registers)
+// then fit in what the decode leaves.  Every item reads the block's slab once,
+// so fewer items read it fewer times.
+__host__ __device__ constexpr uint32_t gemm_x_tiles(uint32_t nt, bool wide) {
+  return !wide || nt > 3 ? 1u : nt == 1 ? 4u : 2u;
+}
+
+// Whether the product splits K over waves, adding partial sums to Y with
+// atomics (Y must then start at zero): fewer work items than waves.
+__host__ __device__ inline bool gemm_splits_k(uint32_t nt, uint32_t t) {
+  const uint32_t xt = gemm_x_tiles(nt, gemm_wide(t));
+  return (t + xt - 1) / xt < (uint32_t)kWavesPerGroup;
 }
 
 // Block b's rows times X, from the slab (row i of the block at slab row
-// margin + i), for NT = ceil(RB / 16) tiles of 16 block rows.
-template <bool BF>
+// margin + i), for NT = ceil(RB / 16) tiles of 16 block rows.  WIDE: more
+// than 32 rows of X.
+template <bool BF, bool WIDE>
 __device__ __forceinline__ void block_product(const LayerDev& L, const GemmArgs& g,
                                               const uint8_t* slab, uint32_t b) {
   switch (uni((g.rows_per_block + 15) / 16)) {
-    case 1: block_product_nt<1, BF>(L, g, slab, b); break;
-    case 2: block_product_nt<2, BF>(L, g, slab, b); break;
-    case 3: block_product_nt<3, BF>(L, g, slab, b); break;
-    default: block_product_nt<4, BF>(L, g, slab, b); break;
+    case 1: block_product_nt<1, gemm_x_tiles(1, WIDE), BF>(L, g, slab, b); break;
+    case 2: block_product_nt<2, gemm_x_tiles(2, WIDE), BF>(L, g, slab, b); break;
+    case 3: block_product_nt<3, gemm_x_tiles(3, WIDE), BF>(L, g, slab, b); break;
+    default: block_product_nt<4, gemm_x_tiles(4, WIDE), BF>(L, g, slab, b); break;
   }
 }
 
-// BF: the BF16 product (the slab holds the bf16 decode of the tiles).
-template <int PATH, bool BF>
+// BF: the BF16 product (the slab holds the bf16 decode of the tiles).  WIDE:
+// more than 32 rows of X.  Instantiated in decode_gemm.hip.
+template <int PATH, bool BF, bool WIDE>
 __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch launch, int32_t* status) {
 #if defined(__HIP_DEVICE_COMPILE__)
   (void)launch;
@@ -2463,7 +2496,7 @@ __global__ __launch_bounds__(kThreads) void decode_gemm_kernel(const GemmLaunch 
     for (uint32_t task = wave_id(); task < tasks; task += kWavesPerGroup)
       dispatch_task<PATH, false>(H, lds, lb, ring_area, task, status);
     __syncthreads();   // the block's rows are in the slab
-    block_product<BF>(L, g, slab, b);
+    block_product<BF, WIDE>(L, g, slab, b);
     __syncthreads();   // every wave is done with the slab
   }
 }

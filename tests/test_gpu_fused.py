@@ -170,6 +170,10 @@ MFMA_CASES = [
     ("ragged_tiles_m20", lambda: W.ragged_tensor(40, 41, 8 * 333, scale=0.05), 5.0, dict(tile_vectors=96), 20),
     ("b12_search_m48", lambda: W.ragged_tensor(41, 64, 8 * 600, scale=0.05), 6.0, dict(prob_bits=12), 48),
     ("one_vector_m5", lambda: W.ragged_tensor(42, 1, 8, scale=0.05), 6.0, {}, 5),
+    # 40-row blocks (three slab tiles); 64-row blocks (four) in two rounds of workgroups
+    ("blocks_of_40_rows_m40", lambda: W.ragged_tensor(45, 10240, 64, scale=0.05), 6.0, {}, 40),
+    ("two_rounds_m7", lambda: W.ragged_tensor(46, 16640, 64, scale=0.05), 6.0, {}, 7),
+    ("two_rounds_m72", lambda: W.ragged_tensor(47, 16640, 64, scale=0.05), 6.0, {}, 72),
 ]
 
 
@@ -178,9 +182,11 @@ MFMA_CASES = [
 def test_fused_mfma_product_matches_oracle(E, oracle, name, gen, target, kw, m, prepared):
     """Every element of Y against the oracle's decode followed by its exact product: token
     counts from 1 to 300 (K split over waves below 256 rows of X, whole token tiles above),
-    rows longer and shorter than a tile, blocks of 16 rows cut by tiles, ragged tiles (the
-    generic loop), b = 12 (the search path), and two calls into the same Y; with the tables
-    built in every workgroup and copied from a prepared workspace."""
+    rows longer and shorter than a tile, blocks of 16 rows cut by tiles, blocks of 40 and 64
+    rows (three and four slab tiles against one, two or more X tiles per work item), the
+    64-row blocks in two rounds of workgroups, ragged tiles (the generic loop), b = 12 (the
+    search path), and two calls into the same Y; with the tables built in every workgroup and
+    copied from a prepared workspace."""
     w = gen()
     say(f"  fused MFMA {name}: {w.shape} at {target}, m = {m}, prepared = {prepared}")
     blob, _ = oracle.encode(w, target, container=oracle.CONT_INT8, **kw)
@@ -318,6 +324,7 @@ BF16_CASES = [
      dict(container="INT8"), 16),
     ("fp8_container_m33", lambda: W.ragged_tensor(68, 50, 8 * 640, scale=0.05), 4.0,
      dict(container="FP8"), 33),
+    ("direct_two_rounds_m40", lambda: W.ragged_tensor(69, 16640, 64), 4.0, {}, 40),
 ]
 
 
