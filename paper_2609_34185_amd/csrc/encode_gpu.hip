@@ -23,6 +23,8 @@
 #include <climits>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
+#include <thread>
 #include <vector>
 
 #include "../../include/entropack.h"
@@ -466,6 +468,42 @@ __global__ __launch_bounds__(256) void k_select(const int32_t* cand, uint64_t ca
 
 unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
+// Two pinned host buffers through which large device-to-host copies are
+// staged: a copy into pageable memory runs at a few GB/s, while a pinned one
+// runs at the link's rate and, chunk by chunk, overlaps the host copy of the
+// previous chunk into place.  Allocated on first use and kept until the
+// process ends; one copy uses them at a time.
+constexpr uint64_t kStageBytes = 8ull << 20;
+struct Stage {
+  std::mutex mu;
+  void* buf[2] = {nullptr, nullptr};
+  bool tried = false;
+};
+Stage& stage() {
+  static Stage* s = new Stage;   // never destroyed: no HIP call at exit
+  return *s;
+}
+
+// Touch every page of a large, freshly allocated host range from several
+// threads before it is copied into: the page faults of first use, taken one
+// at a time by a single copying thread, cost more than the copy itself.
+void prefault(uint8_t* d, uint64_t n) {
+  const unsigned T = std::min(8u, std::max(1u, std::thread::hardware_concurrency()));
+  if (n < (8ull << 20) || T < 2) return;
+  const uint64_t part = (n / T + 4095) & ~4095ull;
+  std::vector<std::thread> th;
+  for (unsigned t = 0; t < T; t++) {
+    const uint64_t lo = t * part, hi = std::min(n, lo + part);
+    if (lo >= hi) break;
+    th.emplace_back([d, lo, hi] {
+      volatile uint8_t* v = d;
+      for (uint64_t i = lo; i < hi; i += 4096) v[i] = 0;
+      v[hi - 1] = 0;
+    });
+  }
+  for (auto& x : th) x.join();
+}
+
 }  // namespace
 
 struct Ctx {
@@ -524,6 +562,41 @@ struct Ctx {
     if (bytes && hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, st) != hipSuccess)
       return fail(EP_ERR_HIP, what);
     return sync(what);
+  }
+  // The same copy staged through the pinned buffers (chunks of kStageBytes):
+  // the transfer of chunk i runs while chunk i - 1 is copied into place, and
+  // the destination's pages are mapped first.  Without the pinned buffers
+  // (their allocation failed), a plain copy.
+  int to_host_staged(void* dst, const void* src, uint64_t bytes, const char* what) {
+    Stage& S = stage();
+    std::lock_guard<std::mutex> lock(S.mu);
+    if (!S.tried) {
+      S.tried = true;
+      for (void*& b : S.buf)
+        if (hipHostMalloc(&b, kStageBytes, hipHostMallocDefault) != hipSuccess) {
+          (void)hipGetLastError();
+          b = nullptr;
+        }
+    }
+    if (!S.buf[0] || !S.buf[1]) return to_host(dst, src, bytes, what);
+    uint8_t* d = static_cast<uint8_t*>(dst);
+    const uint8_t* g = static_cast<const uint8_t*>(src);
+    prefault(d, bytes);
+    uint64_t prev_off = 0, prev_n = 0;
+    int prev_b = 0;
+    for (uint64_t off = 0, i = 0; off < bytes || prev_n; i++) {
+      const uint64_t n = off < bytes ? std::min(kStageBytes, bytes - off) : 0;
+      const int b = (int)(i & 1);
+      if (n && hipMemcpyAsync(S.buf[b], g + off, n, hipMemcpyDeviceToHost, st) != hipSuccess)
+        return fail(EP_ERR_HIP, what);
+      if (prev_n) std::memcpy(d + prev_off, S.buf[prev_b], prev_n);
+      if (n && sync(what) != EP_OK) return EP_ERR_HIP;
+      prev_off = off;
+      prev_n = n;
+      prev_b = b;
+      off += n;
+    }
+    return EP_OK;
   }
   int to_dev(void* dst, const void* src, uint64_t bytes, const char* what) {
     if (bytes && hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st) != hipSuccess)
@@ -741,7 +814,7 @@ int payload(Ctx* c, const uint32_t* offs, uint64_t tiles, uint64_t total_words, 
                        c->words_n, doffs, dpay);
     EP_LAUNCHED("ep_encode_gpu: launch (payload)");
   }
-  EP_GTRY(c->to_host(dst, dpay, 2 * total_words, "ep_encode_gpu: payload"));
+  EP_GTRY(c->to_host_staged(dst, dpay, 2 * total_words, "ep_encode_gpu: payload"));
   c->release(doffs);
   c->release(dpay);
   c->release(c->words);
