@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import ctypes as C
 import os
+import weakref
 
 import numpy as np
 
@@ -156,9 +157,23 @@ def default_params(target_bpp: float, **kw) -> EncodeParams:
     return p
 
 
+def _blob_array(out: Blob) -> np.ndarray:
+    """The blob the library allocated, as a uint8 numpy array over the same memory (no
+    copy); ep_blob_free releases it once no array refers to that memory any more."""
+    addr = C.cast(out.data, C.c_void_p).value
+    buf = (C.c_uint8 * out.size).from_address(addr)
+    weakref.finalize(buf, _free_blob, addr, out.size)
+    return np.frombuffer(buf, dtype=np.uint8)
+
+
+def _free_blob(addr: int, size: int) -> None:
+    b = Blob(C.cast(addr, C.POINTER(C.c_uint8)), size)
+    lib().ep_blob_free(C.byref(b))
+
+
 def encode(w: np.ndarray, target_bpp: float, dtype: int | None = None, **kw):
     """Encode an R x C matrix (uint16 BF16 bits, or float32; FP16 bits with dtype=FP16).
-    Returns (blob as a uint8 numpy array, stats dict)."""
+    Returns (blob as a uint8 numpy array over the library's memory, no copy; stats dict)."""
     w = np.ascontiguousarray(w)
     if dtype is None:
         dtype = FP32 if w.dtype == np.float32 else BF16
@@ -167,9 +182,7 @@ def encode(w: np.ndarray, target_bpp: float, dtype: int | None = None, **kw):
     st = EncodeStats()
     _check(lib().ep_encode_cpu(w.ctypes.data_as(C.c_void_p), dtype, w.shape[0], w.shape[1],
                                C.byref(p), C.byref(out), C.byref(st)), "ep_encode_cpu")
-    blob = np.ctypeslib.as_array(out.data, shape=(out.size,)).copy()
-    lib().ep_blob_free(C.byref(out))
-    return blob, {k: getattr(st, k) for k, _ in EncodeStats._fields_}
+    return _blob_array(out), {k: getattr(st, k) for k, _ in EncodeStats._fields_}
 
 
 def encode_gpu(d_w: int, rows: int, cols: int, target_bpp: float, dtype: int = BF16,
@@ -181,9 +194,7 @@ def encode_gpu(d_w: int, rows: int, cols: int, target_bpp: float, dtype: int = B
     st = EncodeStats()
     _check(lib().ep_encode_gpu(d_w, dtype, rows, cols, C.byref(p), C.byref(out), C.byref(st),
                                stream or None), "ep_encode_gpu")
-    blob = np.ctypeslib.as_array(out.data, shape=(out.size,)).copy()
-    lib().ep_blob_free(C.byref(out))
-    return blob, {k: getattr(st, k) for k, _ in EncodeStats._fields_}
+    return _blob_array(out), {k: getattr(st, k) for k, _ in EncodeStats._fields_}
 
 
 def blob_info(blob: np.ndarray) -> TensorInfo:
