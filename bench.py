@@ -681,7 +681,7 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the decode shards by tile range with no exchange; see the design notes)",
               file=sys.stderr)
         sys.exit(2)

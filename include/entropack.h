@@ -58,7 +58,7 @@ enum ep_status {
   EP_OK = 0,
   EP_ERR_ARG = -1,         /* invalid argument (shape, pointer, range, dtype) */
   EP_ERR_FORMAT = -2,      /* blob fails validation */
-  EP_ERR_UNSUPPORTED = -3, /* valid request this build does not handle */
+  EP_ERR_UNSUPPORTED = -3, /* valid request the library does not handle */
   EP_ERR_NOMEM = -4,       /* host allocation failed (encoder only) */
   EP_ERR_HIP = -5,         /* a HIP runtime call failed (launch error) */
   EP_ERR_CORRUPT = -6      /* decoded stream inconsistent (terminal state/offset) */
