@@ -1046,11 +1046,12 @@ int encode_impl(BK& E, int w_dtype, int64_t R, int64_t C, const ep_encode_params
       eo += acc[4 * r + 2];
       ro += acc[4 * r + 3];
     }
+    // sum over a tile's lanes of log2(x / 2^15), as the log of the product: each
+    // factor lies in [1, 2^16), so 32 of them stay below 2^512
     for (uint64_t t = 0; t < tiles; t++) {
-      double a = 0;
-      for (uint32_t l = 0; l < kLanes; l++)
-        a += std::log2((double)states[t * kLanes + l] / (double)kStateLow);
-      sb += a;
+      double prod = 1.0;
+      for (uint32_t l = 0; l < kLanes; l++) prod *= (double)states[t * kLanes + l] / (double)kStateLow;
+      sb += std::log2(prod);
     }
     stats->scale = s;
     stats->rate_estimate_sample = rhat;

@@ -27,6 +27,8 @@
 #include <thread>
 #include <vector>
 
+#include <sys/mman.h>
+
 #include "../../include/entropack.h"
 #include "common.h"
 #include "encode_gpu.h"
@@ -486,10 +488,15 @@ Stage& stage() {
 
 // Touch every page of a large, freshly allocated host range from several
 // threads before it is copied into: the page faults of first use, taken one
-// at a time by a single copying thread, cost more than the copy itself.
+// at a time by a single copying thread, cost more than the copy itself.  The
+// range's whole 2 MiB pages are offered to the kernel as huge pages first
+// (where transparent huge pages are enabled, one fault then maps 2 MiB).
 void prefault(uint8_t* d, uint64_t n) {
   const unsigned T = std::min(8u, std::max(1u, std::thread::hardware_concurrency()));
   if (n < (8ull << 20) || T < 2) return;
+  constexpr uintptr_t kHuge = 2ull << 20;
+  const uintptr_t lo = ((uintptr_t)d + kHuge - 1) & ~(kHuge - 1), hi = ((uintptr_t)d + n) & ~(kHuge - 1);
+  if (hi > lo) (void)madvise(reinterpret_cast<void*>(lo), hi - lo, MADV_HUGEPAGE);
   const uint64_t part = (n / T + 4095) & ~4095ull;
   std::vector<std::thread> th;
   for (unsigned t = 0; t < T; t++) {
