@@ -97,29 +97,40 @@ __global__ __launch_bounds__(256) void k_prep_rows(const void* w, int dt, int64_
 }
 
 constexpr int kRowsPerBlock = 64;   // row-ordered sums: one thread per row, 64 rows per workgroup
+constexpr int kFetchThreads = 256;  // threads of a workgroup of k_prep_mu and k_refit (rows' threads first)
 
 // mu_r = max(sqrt(sum x^2 / C), eta), summed in element order by the row's
-// thread; the workgroup stages 64 x 64 chunks of its rows through LDS so the
-// loads are coalesced.
-__global__ __launch_bounds__(64) void k_prep_mu(const float* x, int64_t R, int64_t C, double* mu) {
+// thread (the first wave); the four waves of the workgroup stage 64 x 64
+// chunks of its rows through LDS with 16-byte loads, the next chunk's loads in
+// flight while the rows' threads sum the current one.
+__global__ __launch_bounds__(kFetchThreads) void k_prep_mu(const float* x, int64_t R, int64_t C, double* mu) {
   __shared__ float tile[kRowsPerBlock][65];
   const int t = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
   const int nr = (int)(R - r0 < kRowsPerBlock ? R - r0 : kRowsPerBlock);
-  // chunk j0's values go to LDS, then chunk j0 + 64 is requested into the
-  // same registers while the rows' threads sum chunk j0
-  float v[kRowsPerBlock];
+  // a chunk is 64 rows x 16 groups of 4 values; this thread moves groups t + 256 k
+  float4 v[4];
   auto fetch = [&](int64_t j0) {
-    const bool in = j0 + t < C;
 #pragma unroll
-    for (int i = 0; i < kRowsPerBlock; i++) v[i] = (i < nr && in) ? x[(r0 + i) * C + j0 + t] : 0.0f;
+    for (int k = 0; k < 4; k++) {
+      const int i = t + kFetchThreads * k, row = i >> 4, g = i & 15;
+      const bool in = row < nr && j0 + 4 * g < C;   // C % 8 == 0: groups are whole
+      v[k] = in ? *reinterpret_cast<const float4*>(x + (r0 + row) * C + j0 + 4 * g)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   };
   double ss = 0;
   fetch(0);
   for (int64_t j0 = 0; j0 < C; j0 += 64) {
     const int ne = (int)(C - j0 < 64 ? C - j0 : 64);
 #pragma unroll
-    for (int i = 0; i < kRowsPerBlock; i++) tile[i][t] = v[i];
+    for (int k = 0; k < 4; k++) {
+      const int i = t + kFetchThreads * k, row = i >> 4, g = i & 15;
+      tile[row][4 * g] = v[k].x;
+      tile[row][4 * g + 1] = v[k].y;
+      tile[row][4 * g + 2] = v[k].z;
+      tile[row][4 * g + 3] = v[k].w;
+    }
     __syncthreads();
     if (j0 + 64 < C) fetch(j0 + 64);
     if (t < nr)
@@ -206,28 +217,36 @@ __global__ __launch_bounds__(256) void k_count_mem(const int32_t* fl, int64_t nv
   }
 }
 
-// Refit sums in element order by the row's thread, 8 vectors (64 values and
-// 72 fields) of each of the workgroup's 64 rows staged through LDS at a time.
-__global__ __launch_bounds__(64) void k_refit(const float* x, const int32_t* fl, int64_t R,
-                                              int64_t cvec, double* num, double* den) {
+// Refit sums in element order by the row's thread (the first wave), 8 vectors
+// (64 values and 72 fields) of each of the workgroup's 64 rows staged through
+// LDS at a time by its four waves: values in 16-byte groups, fields one by
+// one; the next chunk's loads are in flight while the rows' threads sum the
+// current one.
+__global__ __launch_bounds__(kFetchThreads) void k_refit(const float* x, const int32_t* fl, int64_t R,
+                                                         int64_t cvec, double* num, double* den) {
   __shared__ float tx[kRowsPerBlock][65];
   __shared__ int32_t tf[kRowsPerBlock][73];   // 72 fields used
   const int t = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock, C = cvec * 8;
   const int nr = (int)(R - r0 < kRowsPerBlock ? R - r0 : kRowsPerBlock);
-  // chunk v0 goes to LDS, then chunk v0 + 8 is requested into the same
-  // registers while the rows' threads sum chunk v0
-  float xv[kRowsPerBlock];
-  int32_t f0[kRowsPerBlock], f1[kRowsPerBlock];
+  // values: 64 rows x 16 groups of 4, groups t + 256 k; fields: 64 rows x 72,
+  // fields t + 256 k
+  constexpr int kF = kRowsPerBlock * 72 / kFetchThreads;   // 18
+  float4 xv[4];
+  int32_t fv[kF];
   auto fetch = [&](int64_t v0) {
     const int nvv = (int)(cvec - v0 < 8 ? cvec - v0 : 8);
 #pragma unroll
-    for (int i = 0; i < kRowsPerBlock; i++) {
-      const bool row = i < nr;
-      const int64_t fb = 9 * ((r0 + i) * cvec + v0);
-      xv[i] = (row && t < 8 * nvv) ? x[(r0 + i) * C + 8 * v0 + t] : 0.0f;
-      f0[i] = (row && t < 9 * nvv) ? fl[fb + t] : 0;
-      f1[i] = (row && t + 64 < 9 * nvv) ? fl[fb + t + 64] : 0;
+    for (int k = 0; k < 4; k++) {
+      const int i = t + kFetchThreads * k, row = i >> 4, g = i & 15;
+      const bool in = row < nr && 4 * g < 8 * nvv;
+      xv[k] = in ? *reinterpret_cast<const float4*>(x + (r0 + row) * C + 8 * v0 + 4 * g)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int k = 0; k < kF; k++) {
+      const int i = t + kFetchThreads * k, row = i / 72, c = i % 72;
+      fv[k] = (row < nr && c < 9 * nvv) ? fl[9 * ((r0 + row) * cvec + v0) + c] : 0;
     }
   };
   double sn = 0, sd = 0;
@@ -235,10 +254,17 @@ __global__ __launch_bounds__(64) void k_refit(const float* x, const int32_t* fl,
   for (int64_t v0 = 0; v0 < cvec; v0 += 8) {
     const int nvv = (int)(cvec - v0 < 8 ? cvec - v0 : 8);
 #pragma unroll
-    for (int i = 0; i < kRowsPerBlock; i++) {
-      tx[i][t] = xv[i];
-      tf[i][t] = f0[i];
-      if (t < 9) tf[i][t + 64] = f1[i];
+    for (int k = 0; k < 4; k++) {
+      const int i = t + kFetchThreads * k, row = i >> 4, g = i & 15;
+      tx[row][4 * g] = xv[k].x;
+      tx[row][4 * g + 1] = xv[k].y;
+      tx[row][4 * g + 2] = xv[k].z;
+      tx[row][4 * g + 3] = xv[k].w;
+    }
+#pragma unroll
+    for (int k = 0; k < kF; k++) {
+      const int i = t + kFetchThreads * k;
+      tf[i / 72][i % 72] = fv[k];
     }
     __syncthreads();
     if (v0 + 8 < cvec) fetch(v0 + 8);
@@ -359,7 +385,8 @@ __global__ __launch_bounds__(256) void k_errors(const void* w, int dt, const flo
 }
 
 // Per-row refinement, candidate k: D_r = sum_j (x_rj - sigma_r p_rj)^2 in
-// element order (one thread per row, chunks staged through LDS as in k_refit).
+// element order (one thread per row, which also loads the 64 x 8-vector chunks
+// that the workgroup stages through LDS).
 __global__ __launch_bounds__(64) void k_dist(const float* x, const int32_t* fl, const float* sigma,
                                              int64_t R, int64_t cvec, double* D) {
   __shared__ float tx[kRowsPerBlock][65];
@@ -678,7 +705,7 @@ int prep(Ctx* c, float* delta, double* mu) {
   hipLaunchKernelGGL(k_prep_rows, dim3((unsigned)c->R), dim3(256), 0, c->st, c->w, c->dt, c->C,
                      c->cont, tmax, c->x, c->delta, c->bad);
   EP_LAUNCHED("ep_encode_gpu: launch (prep)");
-  hipLaunchKernelGGL(k_prep_mu, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+  hipLaunchKernelGGL(k_prep_mu, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kFetchThreads), 0, c->st,
                      c->x, c->R, c->C, c->mu);
   EP_LAUNCHED("ep_encode_gpu: launch (row rms)");
   int bad = 0;
@@ -763,7 +790,7 @@ int count(Ctx* c, bool sample, const int32_t* lo, const int32_t* A, uint64_t* n)
 }
 
 int refit(Ctx* c, double* num, double* den) {
-  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kFetchThreads), 0, c->st,
                      c->x, c->fl, c->R, c->cvec, c->num, c->den);
   EP_LAUNCHED("ep_encode_gpu: launch (refit)");
   EP_GTRY(c->to_host(num, c->num, 8 * (uint64_t)c->R, "ep_encode_gpu: refit"));
@@ -872,7 +899,7 @@ int cand_quantize(Ctx* c, int k, double s, int32_t* lohi) {
 }
 
 int cand_refit(Ctx* c, int k, double* num, double* den) {
-  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kRowsPerBlock), 0, c->st,
+  hipLaunchKernelGGL(k_refit, dim3(blocks_for(c->R, kRowsPerBlock)), dim3(kFetchThreads), 0, c->st,
                      c->x, cand_ptr(c, k), c->R, c->cvec, c->num, c->den);
   EP_LAUNCHED("ep_encode_gpu: launch (candidate refit)");
   EP_GTRY(c->to_host(num, c->num, 8 * (uint64_t)c->R, "ep_encode_gpu: candidate refit"));
