@@ -593,6 +593,26 @@ def cold_cache_ms(step, reps=15):
     return {"min": times[0], "median": times[len(times) // 2], "reps": reps}
 
 
+def copy_bandwidth(reps=10):
+    """Achieved bandwidth of a plain 1 GiB device-to-device copy (bytes read plus bytes
+    written per second, HIP events): the practical ceiling a streaming kernel is held against
+    beside the 8 TB/s nominal figure."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    s = torch.cuda.current_stream()
+    for _ in range(3):
+        dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record(s)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    return 2 * COPY_BYTES / (ms * 1e-3) / 1e9
+
+
 def cpu_baseline(items, threads):
     """The oracle decoder on the same blobs, tiles split over `threads` host threads.  Returns
     (the timing record, the oracle's outputs [(weights, dequant or None)] for the parity gate)."""
@@ -783,6 +803,7 @@ def main():
     assert int(status.item()) == 0, "decode reported a corrupt stream"
 
     cold = cold_cache_ms(step)
+    copy_gbps = copy_bandwidth()
     gemm = None
     if args.workload == "mlp_down_int8":
         log("timing the INT8 product of the decoded weights")
@@ -807,7 +828,8 @@ def main():
         "data": "synthetic",
         "config": dict(desc, weights=weights, stored_bpp=round(stored_bpp, 4),
                        bytes_per_step=algo_bytes, wall_s=round(wall, 4), settle_steps=settle,
-                       cold_cache_ms=cold),
+                       cold_cache_ms=cold, measured_copy_gbps=round(copy_gbps, 1),
+                       frac_of_measured_copy=round(gbps / copy_gbps, 4)),
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gbps / HBM_PEAK_GBPS, "traffic": traffic},
     }
