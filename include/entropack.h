@@ -207,8 +207,9 @@ int ep_blob_info(const void* host_blob, uint64_t n, ep_tensor_info* info);
 /* Decode tiles [tile_begin, tile_end) of one tensor (Section 3.7: eq.
  * rans_decode, eq. point_inverse, eq. recon).  d_out receives R x C
  * elements of out_dtype (row-major); only the elements of the given tiles are
- * written.  For containers, d_dequant (nullable) receives delta_r for each row
- * whose first vector lies in a decoded tile.  d_status (nullable, device
+ * written.  For containers, d_dequant (R floats, required; ignored for other
+ * tensors) receives delta_r for each row whose first vector lies in a decoded
+ * tile.  d_status (nullable, device
  * int32, zeroed by the caller) receives ep_status_bits for corrupt streams;
  * the kernels never read or write outside the blob's tile windows and the
  * output.  Errors (host side, before launch): EP_ERR_ARG (also for an info whose
@@ -227,8 +228,8 @@ int ep_decode_tiles(const ep_tensor_info* info, const void* d_blob, int out_dtyp
  * C <= 131071).  W' is never written to memory: every decoded vector goes
  * straight into dot products with the m rows of X.  Y is overwritten (cleared
  * on hip_stream first by a small fill kernel, not a memset node, so the call
- * can be captured in a graph); d_dequant (nullable) receives delta_r for every
- * row.
+ * can be captured in a graph); d_dequant (R floats, required) receives delta_r
+ * for every row.
  * All pointers are device memory owned by the caller; X 8-byte aligned.
  * Asynchronous on hip_stream, no allocation, one clear and one kernel launch.
  * d_status as for ep_decode_tiles.  Meant for few rows of X (decode-time
@@ -253,8 +254,10 @@ int ep_decode_matmul_i8(const ep_tensor_info* info, const void* d_blob, const in
  * (v_mfma_i32_16x16x64_i8).  d_workspace: >= ep_decode_gemm_i8_workspace(info)
  * bytes of device memory owned by the caller, untouched until the launch
  * completes.  Y is overwritten (cleared first on hip_stream by a small fill
- * kernel when m < 256, where partial sums over K are added with atomics).  d_dequant (nullable) receives delta_r for every row; d_status as for
- * ep_decode_tiles.  Asynchronous, no allocation, at most one clear and one launch.
+ * kernel whenever partial sums over K are added with atomics: at fewer rows of
+ * X than 16 work items need, 256 to 976 rows by the block's height).
+ * d_dequant (R floats, required) receives delta_r for every row; d_status as
+ * for ep_decode_tiles.  Asynchronous, no allocation, at most one clear and one launch.
  * Errors: EP_ERR_ARG (null pointers, m outside 1..65536, X above 2^31 bytes, short
  * workspace), EP_ERR_UNSUPPORTED (not the INT8 row container, C > 131071),
  * EP_ERR_HIP. */
@@ -298,10 +301,12 @@ int ep_decode_gemm_i8_prepared(const ep_tensor_info* info, const void* d_blob, c
  * (v_mfma_f32_16x16x32_bf16); every product of two bf16 values is exact in
  * fp32 and the sums are fp32, so |Y - X W'^T| <= (C + s + 2) 2^-24 sum_j
  * |X[t][j] W'[r][j]| with s <= 16 partial sums per element (K is split over
- * waves when m < 256, and those partial sums are added with float atomics, so
- * the last bits of Y may differ from call to call).  d_workspace: >=
- * ep_decode_gemm_bf16_workspace(info) bytes.  Y is overwritten (cleared first
- * when m < 256).  d_dequant, d_status as for ep_decode_gemm_i8.  Asynchronous,
+ * waves at small m, as for the INT8 product, and those partial sums are added
+ * with float atomics, so the last bits of Y may differ from call to call).
+ * d_workspace: >= ep_decode_gemm_bf16_workspace(info) bytes.  Y is
+ * overwritten (cleared first when K is split).  d_status as for
+ * ep_decode_gemm_i8; d_dequant (R floats) receives delta_r for container
+ * tensors (required for them, ignored otherwise).  Asynchronous,
  * no allocation, at most one clear and one launch.
  * Errors: EP_ERR_ARG (null pointers, m outside 1..65536, X above 2^31 bytes,
  * short workspace), EP_ERR_UNSUPPORTED, EP_ERR_HIP. */
@@ -327,7 +332,7 @@ typedef struct {
   ep_tensor_info info;       /* from ep_blob_info on the host copy */
   const void* d_blob;
   void* d_out;
-  float* d_dequant;          /* nullable */
+  float* d_dequant;          /* R floats, required for container tensors, else ignored */
   int32_t out_dtype;
   int32_t reserved;
 } ep_layer;

@@ -66,9 +66,12 @@ bool valid_out_dtype(int dt) {
          dt == EP_INT8 || dt == EP_UINT8 || dt == EP_COORD2_I32;
 }
 
+// tables_only: the descriptor only serves a table build (no output, no dequant).
 int fill_layer(const ep_tensor_info& I, const void* d_blob, int out_dtype, void* d_out,
-               float* d_dequant, uint32_t t0, uint32_t t1, LayerDev& D) {
+               float* d_dequant, uint32_t t0, uint32_t t1, LayerDev& D, bool tables_only = false) {
   if (!d_blob || !d_out) return fail(EP_ERR_ARG, "decode: null device pointer");
+  if (I.container && !d_dequant && !tables_only)
+    return fail(EP_ERR_ARG, "decode: a container tensor needs d_dequant (its row scales)");
   if (!valid_out_dtype(out_dtype)) return fail(EP_ERR_ARG, "decode: unknown output dtype");
   if (t0 > t1 || t1 > I.n_tiles) return fail(EP_ERR_ARG, "decode: tile range outside the tensor");
   if (!I.rows || !I.cols || I.cols % 8 || I.prob_bits < 9 || I.prob_bits > 15 || !I.tile_vectors)
@@ -378,7 +381,7 @@ int decode_gemm_prepare(const ep_tensor_info* info, const void* d_blob, void* d_
     return fail(EP_ERR_ARG, (std::string(who) + ": workspace too small").c_str());
   LayerDev D;
   // the output pointer is never used by the table build
-  rc = fill_layer(*info, d_blob, bf ? EP_BF16 : EP_INT8, d_ws, nullptr, 0, info->n_tiles, D);
+  rc = fill_layer(*info, d_blob, bf ? EP_BF16 : EP_INT8, d_ws, nullptr, 0, info->n_tiles, D, true);
   if (rc) return rc;
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   D.tables = ws;

@@ -160,3 +160,21 @@ def test_gemm_rejects_sums_that_could_overflow_int32(E):
     with pytest.raises(E.EntroPackError) as ei:
         E.gemm_i8_nt(a + 8, b, y, 16, 16, 64)
     assert ei.value.code == E.ERR_ARG
+
+
+def test_container_decodes_require_dequant(E, oracle):
+    """A container tensor's weights are delta_r times the decoded values, so every decode
+    entry point refuses a null d_dequant for it, on the host, before any device call (the
+    device pointers below are never dereferenced); a direct tensor needs none."""
+    w = W.ragged_tensor(90, 16, 64, scale=0.05)
+    cont, _ = oracle.encode(w, 6.0, container=oracle.CONT_INT8)
+    info = E.blob_info(cont)
+    assert info.container
+    blob, out, x, ws = 1 << 20, 2 << 20, 3 << 20, 4 << 20
+    lib = E.lib()
+    assert lib.ep_decode_tiles(E.C.byref(info), blob, E.INT8, out, None, 0, info.n_tiles,
+                               None, None) == E.ERR_ARG
+    assert lib.ep_decode_matmul_i8(E.C.byref(info), blob, x, 1, out, None, None, None) == E.ERR_ARG
+    layer = E.Layer(info, blob, out, None, E.INT8, 0)
+    assert lib.ep_decode_layers(E.C.byref(layer), 1, None, 0, None, None) == E.ERR_ARG
+    assert b"dequant" in lib.ep_last_error()
