@@ -664,6 +664,80 @@ static void symbol_of(const int32_t* f9, int i, const table_t* T, int* t, int32_
   }
 }
 
+/* Tiled interleaved rANS [3.6, eq. rans_encode; App. C.3] of nvec vectors'
+ * fields under tables T (frequencies normalised to 2^b).  Per tile the 32
+ * lanes' states start at L; the symbols are pushed last to first (vector
+ * by vector from the tile's end, field 8 down to the coset, lane 31 down to
+ * 0), each renormalising 16 bits at a time; the tile's words are then
+ * reversed into the decoder's order.  The words are appended to pay;
+ * states[tile][lane] and offsets[0 .. n_tiles] (both nullable) receive the
+ * final states and the tiles' word offsets, *state_bits the sum of
+ * log2(x / L) over the final states. */
+static int rans_tiles(const int32_t* fields, uint64_t nvec, uint32_t V, int b, const table_t* T,
+                      uint32_t* states, uint32_t* offsets, wordbuf* pay, double* state_bits) {
+  const uint64_t n_tiles = n_tiles_of(nvec, V);
+  const uint32_t M = 1u << b;
+  uint32_t* cumul[ORA_NTAB];
+  memset(cumul, 0, sizeof cumul);
+  int rc = O_OK;
+  for (int t = 0; t < ORA_NTAB; t++) {
+    cumul[t] = (uint32_t*)calloc((size_t)T[t].A + 1, sizeof(uint32_t));
+    if (!cumul[t]) {
+      rc = O_ERR_NOMEM;
+      goto out;
+    }
+    for (int32_t z = 0; z < T[t].A; z++) cumul[t][z + 1] = cumul[t][z] + T[t].f[z];
+  }
+  double sb = 0;
+  if (offsets) offsets[0] = 0;
+  for (uint64_t tile = 0; tile < n_tiles; tile++) {
+    uint64_t v0 = tile * V;
+    uint64_t nv = nvec - v0 < V ? nvec - v0 : V;
+    uint64_t steps = 9 * ((nv + ORA_J - 1) / ORA_J);
+    uint32_t xs[ORA_J];
+    for (uint32_t l = 0; l < ORA_J; l++) xs[l] = ORA_L;
+    uint64_t start = pay->n;
+    for (uint64_t step = steps; step-- > 0;) {
+      uint64_t k = step / 9;
+      int i = (int)(step % 9);
+      for (uint32_t l = ORA_J; l-- > 0;) {
+        uint64_t li = l + ORA_J * k;
+        if (li >= nv) continue;
+        int t;
+        int32_t idx;
+        symbol_of(fields + 9 * (v0 + li), i, T, &t, &idx);
+        uint32_t f = T[t].f[idx], F = cumul[t][idx];
+        uint64_t xx = xs[l];
+        if (xx >= ((uint64_t)f << (31 - b))) {
+          rc = wb_push(pay, (uint16_t)(xx & 0xFFFF));
+          if (rc) goto out;
+          xx >>= 16;
+        }
+        xx = (xx / f) * M + (xx % f) + F;
+        xs[l] = (uint32_t)xx;
+      }
+    }
+    for (uint64_t a = start, z = pay->n - 1; pay->n && a < z; a++, z--) { /* emitted backwards */
+      uint16_t tmp = pay->w[a];
+      pay->w[a] = pay->w[z];
+      pay->w[z] = tmp;
+    }
+    if (pay->n > 0xFFFFFFFFull) {
+      rc = O_ERR_UNSUPPORTED;
+      goto out;
+    }
+    for (uint32_t l = 0; l < ORA_J; l++) {
+      if (states) states[tile * ORA_J + l] = xs[l];
+      sb += log2((double)xs[l] / (double)ORA_L);
+    }
+    if (offsets) offsets[tile + 1] = (uint32_t)pay->n;
+  }
+  *state_bits = sb;
+out:
+  for (int t = 0; t < ORA_NTAB; t++) free(cumul[t]);
+  return rc;
+}
+
 /* ========================================================================= */
 /* Per-row rate-distortion refinement [3.5, eqs. rdo_rate, rdo_budget,        */
 /* rdo_choice; App. C.2, Alg. rdo].                                           */
@@ -1088,68 +1162,15 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
 
   /* tiled interleaved rANS [3.6, eq. rans_encode; App. C.3] */
   const uint64_t n_tiles = n_tiles_of((uint64_t)nvec, V);
-  const uint32_t M = 1u << b;
   states = (uint32_t*)malloc(n_tiles * ORA_J * sizeof(uint32_t));
   offsets = (uint32_t*)malloc((n_tiles + 1) * sizeof(uint32_t));
-  uint32_t* cumul[ORA_NTAB];
-  memset(cumul, 0, sizeof cumul);
   if (!states || !offsets) {
     rc = O_ERR_NOMEM;
     goto done;
   }
-  for (int t = 0; t < ORA_NTAB; t++) {
-    cumul[t] = (uint32_t*)calloc((size_t)T[t].A + 1, sizeof(uint32_t));
-    if (!cumul[t]) {
-      rc = O_ERR_NOMEM;
-      for (int u = 0; u < t; u++) free(cumul[u]);
-      goto done;
-    }
-    for (int32_t z = 0; z < T[t].A; z++) cumul[t][z + 1] = cumul[t][z] + T[t].f[z];
-  }
   double state_bits = 0;
-  offsets[0] = 0;
-  for (uint64_t tile = 0; tile < n_tiles; tile++) {
-    uint64_t v0 = tile * V;
-    uint64_t nv = (uint64_t)nvec - v0 < V ? (uint64_t)nvec - v0 : V;
-    uint64_t steps = 9 * ((nv + ORA_J - 1) / ORA_J);
-    uint32_t xs[ORA_J];
-    for (uint32_t l = 0; l < ORA_J; l++) xs[l] = ORA_L;
-    uint64_t start = pay.n;
-    for (uint64_t step = steps; step-- > 0;) {
-      uint64_t k = step / 9;
-      int i = (int)(step % 9);
-      for (uint32_t l = ORA_J; l-- > 0;) {
-        uint64_t li = l + ORA_J * k;
-        if (li >= nv) continue;
-        int t;
-        int32_t idx;
-        symbol_of(fields + 9 * (v0 + li), i, T, &t, &idx);
-        uint32_t f = T[t].f[idx], F = cumul[t][idx];
-        uint64_t xx = xs[l];
-        if (xx >= ((uint64_t)f << (31 - b))) {
-          rc = wb_push(&pay, (uint16_t)(xx & 0xFFFF));
-          if (rc) goto done_cumul;
-          xx >>= 16;
-        }
-        xx = (xx / f) * M + (xx % f) + F;
-        xs[l] = (uint32_t)xx;
-      }
-    }
-    for (uint64_t a = start, z = pay.n - 1; pay.n && a < z; a++, z--) { /* emitted backwards */
-      uint16_t tmp = pay.w[a];
-      pay.w[a] = pay.w[z];
-      pay.w[z] = tmp;
-    }
-    if (pay.n > 0xFFFFFFFFull) {
-      rc = O_ERR_UNSUPPORTED;
-      goto done_cumul;
-    }
-    for (uint32_t l = 0; l < ORA_J; l++) {
-      states[tile * ORA_J + l] = xs[l];
-      state_bits += log2((double)xs[l] / (double)ORA_L);
-    }
-    offsets[tile + 1] = (uint32_t)pay.n;
-  }
+  rc = rans_tiles(fields, (uint64_t)nvec, V, b, T, states, offsets, &pay, &state_bits);
+  if (rc) goto done;
 
   /* serialise */
   {
@@ -1164,7 +1185,7 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
     blob = (uint8_t*)calloc((size_t)total, 1);
     if (!blob) {
       rc = O_ERR_NOMEM;
-      goto done_cumul;
+      goto done;
     }
     put32(blob + 0, ORA_MAGIC);
     put32(blob + 4, ORA_VERSION);
@@ -1257,8 +1278,6 @@ int ora_encode(const void* w, int dtype, int64_t R, int64_t C, const ora_params*
     blob = NULL;
   }
 
-done_cumul:
-  for (int t = 0; t < ORA_NTAB; t++) free(cumul[t]);
 done:
   free(x);
   free(delta);
@@ -1279,6 +1298,53 @@ done:
 }
 
 void ora_blob_free(uint8_t* blob) { free(blob); }
+
+/* Payload words of the tiled interleaved rANS coding (rans_tiles) of nvec
+ * vectors' fields under 17 given tables, for the coding ablation's
+ * re-encoding of a tensor's points under another table layout (App. A.3).
+ * Table t covers tA[t] values from tmin[t]; its normalised frequencies (summing
+ * to 2^b) are freqs[o_t .. o_t + tA[t]), the tables' frequencies stored one
+ * after another (o_t = tA[0] + ... + tA[t - 1]).  Every coset field must be 0
+ * or 1 and every symbol must fall in its table's range with a non-zero
+ * frequency (O_ERR_ARG otherwise).  *state_bits (nullable) receives the sum of
+ * log2(x / L) over the tiles' final states. */
+int ora_rans_words(const int32_t* fields, int64_t nvec, int32_t V, int32_t b, const int32_t* tmin,
+                   const int32_t* tA, const uint32_t* freqs, uint64_t* words, double* state_bits) {
+  if (!fields || nvec < 0 || V < 1 || b < 9 || b > 15 || !tmin || !tA || !freqs || !words)
+    return O_ERR_ARG;
+  table_t T[ORA_NTAB];
+  memset(T, 0, sizeof T);
+  uint64_t off = 0;
+  for (int t = 0; t < ORA_NTAB; t++) {
+    if (tA[t] < 0 || tA[t] > (1 << b)) return O_ERR_ARG;
+    T[t].min = tmin[t];
+    T[t].A = tA[t];
+    T[t].f = (uint32_t*)(freqs + off);
+    off += (uint64_t)tA[t];
+    uint64_t sum = 0;
+    for (int32_t z = 0; z < tA[t]; z++) sum += T[t].f[z];
+    if (tA[t] && sum != (1ull << b)) return O_ERR_ARG;
+  }
+  for (int64_t v = 0; v < nvec; v++) {
+    const int32_t* f9 = fields + 9 * v;
+    if (f9[0] < 0 || f9[0] > 1) return O_ERR_ARG;
+    for (int i = 0; i < 9; i++) {
+      int t;
+      int32_t idx;
+      symbol_of(f9, i, T, &t, &idx);
+      if (idx < 0 || idx >= T[t].A || T[t].f[idx] == 0) return O_ERR_ARG;
+    }
+  }
+  wordbuf pay = {0};
+  double sb = 0;
+  int rc = rans_tiles(fields, (uint64_t)nvec, (uint32_t)V, b, T, NULL, NULL, &pay, &sb);
+  if (!rc) {
+    *words = pay.n;
+    if (state_bits) *state_bits = sb;
+  }
+  free(pay.w);
+  return rc;
+}
 
 /* Test hook: 2p of every vector at a given scale s, with the same input
  * conversion, container route and row normalisation as the encoder. */

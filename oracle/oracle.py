@@ -79,6 +79,7 @@ def lib():
         L.ora_normalize.argtypes = [p, i32, i32, p]
         L.ora_code_length.argtypes = [p, p, i32, i32]
         L.ora_code_length.restype = dbl
+        L.ora_rans_words.argtypes = [p, i64, i32, i32, p, p, p, p, p]
         L.ora_snap.argtypes = [p, i64, C.c_int, p]
         L.ora_values.argtypes = [p, i64, C.c_int, p]
         L.ora_quantize.argtypes = [p, C.c_int, i64, i64, C.c_int, dbl, p, p, p]
@@ -283,57 +284,80 @@ def gemm_i8_nt(a: np.ndarray, b: np.ndarray, rows=None) -> np.ndarray:
     return y
 
 
-def _table_bits(values: np.ndarray, b: int):
-    """(code length in bits, serialized bytes, alphabet) of one table built from `values`:
-    counts over [min, max], frequencies normalised to 2^b, min:i32 + A:u32 + f:u16[A]."""
+def _table(values: np.ndarray, b: int):
+    """One table built from `values` (Section 3.3): (min, A, counts over [min, max],
+    frequencies normalised to 2^b, or None when the range exceeds 2^b)."""
     if values.size == 0:
-        return 0.0, 8, 0
+        return 0, 0, np.zeros(0, np.uint64), np.zeros(0, np.uint32)
     lo, hi = int(values.min()), int(values.max())
     counts = np.bincount(values - lo, minlength=hi - lo + 1).astype(np.uint64)
-    A = counts.size
-    if A > (1 << b):
-        return float("inf"), 8 + 2 * A, A
-    f = normalize(counts, b)
-    return code_length(counts, f, b), 8 + 2 * A, A
+    if counts.size > (1 << b):
+        return lo, counts.size, counts, None
+    return lo, counts.size, counts, normalize(counts, b)
+
+
+def rans_words(f9: np.ndarray, V: int, b: int, tmin, tA, freqs) -> int:
+    """Payload words of the tiled interleaved rANS coding of the fields f9 (nvec x 9) with
+    17 tables (Section 3.6): table 0 for the coset, 1 + 8 c + (i - 1) for field i under
+    coset c, covering tA[t] values from tmin[t] with normalised frequencies freqs[t]."""
+    f = np.ascontiguousarray(f9, dtype=np.int32)
+    lo = np.ascontiguousarray(tmin, dtype=np.int32)
+    A = np.ascontiguousarray(tA, dtype=np.int32)
+    fr = np.concatenate([np.asarray(x, dtype=np.uint32) for x in freqs] + [np.zeros(1, np.uint32)])
+    words = np.zeros(1, dtype=np.uint64)
+    _chk(lib().ora_rans_words(_ptr(f), f.shape[0], V, b, _ptr(lo), _ptr(A), _ptr(fr),
+                              _ptr(words), None), "ora_rans_words")
+    return int(words[0])
 
 
 def coding_ablation(blob: np.ndarray) -> dict:
-    """Stored bits of a blob's own lattice points under the three coding models of the
-    entropy-model ablation (App. A.3, Table coding; eqs. cond, parity, conditioning_gain):
+    """Stored size of a blob's own lattice points re-encoded under the three coding models of
+    the entropy-model ablation (App. A.3, Table coding; eqs. cond, parity, conditioning_gain):
       'entropack': coset table + one table per (field, coset), fields (c, z1..z7, m);
       'pooled':    coset table + one table per field for both cosets (no conditioning);
       'direct_z8': as 'entropack' with z8 = 2m + pi coded in place of m (no parity reduction).
-    Every variant keeps the points, row scales, tiles and precision b, and builds its tables
-    from its own fields.  Payload: the exact code length of the fields under the variant's
-    b-bit tables (eq. length); the stored size is the blob's own size plus each variant's
-    difference in code length and in serialized table bytes from the blob's model (so the
-    per-tile state and padding overheads, common to all three, are the blob's own)."""
+    Every variant keeps the points, row scales, tiles and precision b, builds its tables from
+    its own fields (counts normalised to 2^b), and re-runs the tiled rANS encoder on its
+    symbols.  Its stored size is the blob layout's (header, serialized tables, scales, states,
+    offsets, payload) with its own tables and payload; the pooled model stores 9 tables, the
+    others 17.  code_bits is each model's ideal code length C_CE under its tables (eq. length)."""
     h = header(blob)
-    b = h["b"]
+    b, V, R = h["b"], h["V"], h["rows"]
     two_p, _ = decode(blob, COORD2)
     f9 = fields(two_p)
     c = f9[:, 0]
     z8 = (two_p.reshape(-1, 8)[:, 7] - c) // 2
-    out = {}
-    for name in ("entropack", "pooled", "direct_z8"):
-        bits, tbytes = _table_bits(c, b)[:2]
-        for i in range(1, 9):
-            col = z8 if (name == "direct_z8" and i == 8) else f9[:, i]
-            if name == "pooled":
-                parts = [col]
-            else:
-                parts = [col[c == 0], col[c == 1]]
-            for p in parts:
-                cl, tb, _ = _table_bits(p, b)
-                bits += cl
-                tbytes += tb
-        out[name] = (bits, tbytes)
-    base_bits, base_tbytes = out["entropack"]
     n = h["rows"] * h["cols"]
-    res = {"b": b, "weights": n, "stored_bits": {}, "code_bits": {}}
-    for name, (bits, tbytes) in out.items():
-        stored = 8.0 * h["total_bytes"] + (bits - base_bits) + 8.0 * (tbytes - base_tbytes)
+    fixed = (48 + 4 * R + (4 * R if h["container"] else 0) + 128 * h["n_tiles"]
+             + 4 * (h["n_tiles"] + 1))
+    cn = np.array([(c == 0).sum(), (c == 1).sum()], dtype=np.uint64)
+    cf = normalize(cn, b)
+    res = {"b": b, "weights": n, "stored_bits": {}, "code_bits": {}, "payload_words": {}}
+    for name in ("entropack", "pooled", "direct_z8"):
+        g = f9.copy()
+        if name == "direct_z8":
+            g[:, 8] = z8
+        tmin, tA = [0] * 17, [0] * 17
+        freqs = [np.zeros(0, np.uint32)] * 17
+        tA[0], freqs[0] = 2, cf
+        bits = code_length(cn, cf, b)
+        tbytes = 4                                  # the coset pair f0, f1
+        for i in range(1, 9):
+            parts = [(None, g[:, i])] if name == "pooled" else [(k, g[c == k, i]) for k in (0, 1)]
+            for k, vals in parts:
+                lo, A, cnt, fr = _table(vals, b)
+                if fr is None:
+                    raise ValueError(f"{name}: field {i} spans {A} values, more than 2^{b}")
+                if cnt.size:
+                    bits += code_length(cnt, fr, b)
+                tbytes += 8 + (2 * A + 3) // 4 * 4
+                for kk in ((0, 1) if k is None else (k,)):
+                    t = 1 + 8 * kk + (i - 1)
+                    tmin[t], tA[t], freqs[t] = lo, A, fr
+        words = rans_words(g, V, b, tmin, tA, freqs)
+        stored = 8.0 * (fixed + tbytes + (2 * words + 3) // 4 * 4)
         res["stored_bits"][name] = stored
         res["code_bits"][name] = bits
+        res["payload_words"][name] = words
         res[name + "_bpp"] = stored / n
     return res

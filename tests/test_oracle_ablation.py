@@ -1,10 +1,15 @@
 """CPU pins of the coding ablation (App. A.3, Table coding; eqs. cond, parity,
-conditioning_gain): the same lattice points coded with 17 coset-conditioned
+conditioning_gain): the same lattice points re-encoded with 17 coset-conditioned
 tables (the method), 9 pooled tables, or z8 in place of m.
 
 What fixes the results:
+  - re-encoding the blob's own points under the method's tables reproduces the
+    blob: the same payload word count and the same stored size, byte for byte;
   - the baseline's code length equals the encoder's own C_CE of the blob (an
     independent computation in C from the stored tables);
+  - every variant's actual payload lies in the window that eq. (length) and the
+    terminal states fix: above C_CE less 16 bits per state, at most C_CE plus
+    the coder's small rounding loss;
   - with exact empirical probabilities, pooled minus conditioned ideal cost is
     the sum of the fields' mutual information with the coset
     (eq. conditioning_gain), computed here from the joint distribution;
@@ -59,6 +64,24 @@ def test_baseline_code_length_is_the_encoders(oracle, case):
     r = oracle.coding_ablation(blob)
     assert r["code_bits"]["entropack"] == pytest.approx(st["cce_full"], rel=1e-12)
     assert r["entropack_bpp"] == pytest.approx(st["r_stored"], rel=1e-12)
+
+
+def test_baseline_re_encoding_reproduces_the_blob(oracle, case):
+    blob, _, _, _ = case
+    h = oracle.header(blob)
+    r = oracle.coding_ablation(blob)
+    assert r["payload_words"]["entropack"] == h["payload_words"]
+    assert r["stored_bits"]["entropack"] == 8 * h["total_bytes"]
+
+
+def test_variant_payloads_lie_in_the_code_length_window(oracle, case):
+    blob, _, _, _ = case
+    h = oracle.header(blob)
+    r = oracle.coding_ablation(blob)
+    slack = 16 * 32 * h["n_tiles"]   # at most 16 bits in each terminal state
+    for name in ("entropack", "pooled", "direct_z8"):
+        bits = 16 * r["payload_words"][name]
+        assert r["code_bits"][name] - slack < bits <= r["code_bits"][name] * 1.005, name
 
 
 def test_conditioning_gain_identity(oracle, case):
