@@ -7,7 +7,7 @@ encoder's parity set (tile sizes that leave partial tiles and odd tile
 counts, both containers, b = 9, high rate, the literal state credit, FP16 and
 FP32 input), the escalation path, degenerate inputs, and two full-size
 tensors (the 3072 x 3072 attention projection, and the 27B-class MLP down
-projection in the FP8 row container).
+projection in the FP8 row container, also encoded by two host threads at once).
 """
 import sys
 
@@ -168,10 +168,44 @@ def test_gpu_encoder_full_size_attention(E, oracle):
     same_stats(s_gpu, s_or)
 
 
-def test_gpu_encoder_full_size_mlp_down_fp8(E, oracle):
+@pytest.fixture(scope="module")
+def mlp_down_fp8(oracle):
     w = W.llm_mlp(["down"])["down"]
-    say(f"  encode MLP down {w.shape} in the FP8 row container at 4.0 (oracle, then GPU)")
+    say(f"  oracle encode of MLP down {w.shape} in the FP8 row container at 4.0")
     b_or, s_or = oracle.encode(w, 4.0, container=1)
+    return w, b_or, s_or
+
+
+def test_gpu_encoder_full_size_mlp_down_fp8(E, mlp_down_fp8):
+    w, b_or, s_or = mlp_down_fp8
     b_gpu, s_gpu = gpu_encode(E, w, 4.0, container=1)
     assert np.array_equal(b_gpu, b_or)
     same_stats(s_gpu, s_or)
+
+
+def test_gpu_encoder_concurrent_calls(E, mlp_down_fp8):
+    """Two host threads encode the same tensor at once, each on its own stream; their
+    payload copies (45 MB, several staging chunks) take the library's pinned staging buffers
+    in turn.  Both blobs equal the oracle's."""
+    import threading
+    w, b_or, _ = mlp_down_fp8
+    d, dt = to_device(w, E)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    out, errs = [None, None], []
+
+    def run(i):
+        try:
+            out[i] = E.encode_gpu(d.data_ptr(), w.shape[0], w.shape[1], 4.0, dtype=dt,
+                                  stream=streams[i].cuda_stream, container=1)[0]
+        except Exception as e:   # re-raised below, in the test's thread
+            errs.append(e)
+
+    threads = [threading.Thread(target=run, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errs, errs
+    for b in out:
+        assert np.array_equal(b, b_or)
