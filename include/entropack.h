@@ -10,8 +10,14 @@
  *   - validation/inspection of an encoded blob on the host (ep_blob_info),
  *   - fused GPU decode on gfx950: rANS symbol decode with the coset-conditional
  *     tables, field inverse, row rescale and dtype snap, with no intermediate
- *     symbol tensor (ep_decode_tiles, ep_decode_layers; Section 3.7),
- *   - an INT8 MFMA matrix product for decode-then-GEMM (ep_gemm_i8_nt).
+ *     symbol tensor (ep_decode_tiles, ep_decode_layers; Section 3.7), for
+ *     prepared layer stacks (ep_stack_prepare, ep_stack_decode) and for
+ *     callers that cannot allocate (ep_decode_layers_noalloc),
+ *   - an INT8 MFMA matrix product for decode-then-GEMM (ep_gemm_i8_nt),
+ *   - decode fused with the matrix product, the decoded weights never written
+ *     as a whole (ep_decode_matmul_i8 for a few int8 rows of X;
+ *     ep_decode_gemm_i8 and ep_decode_gemm_bf16 on the matrix cores for any
+ *     number of rows; App. D).
  *
  * Conventions shared by every entry point:
  *   - Return value: EP_OK (0) or a negative ep_status.  ep_last_error() gives a
@@ -21,8 +27,11 @@
  *     current HIP device; all other pointers are host pointers.
  *   - GPU calls are asynchronous on the given hipStream_t (passed as void*,
  *     NULL = default stream).  They allocate no device memory and never
- *     synchronise; the caller owns every buffer.  The one exception is the
- *     GPU encoder (ep_encode_gpu), which returns a finished host blob.
+ *     synchronise; the caller owns every buffer.  The exceptions are the GPU
+ *     encoder (ep_encode_gpu), which allocates its work buffers and returns a
+ *     finished host blob, and the preparation calls (ep_stack_prepare,
+ *     ep_decode_gemm_i8_prepare, ep_decode_gemm_bf16_prepare), which return
+ *     once their table build on the stream has completed.
  *   - Outputs must not alias the blob or each other.
  *
  * Stored representation (all little-endian; every section starts on a 4-byte
