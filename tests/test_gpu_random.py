@@ -95,3 +95,116 @@ def test_random_configuration(E, oracle, i):
                                  f"gpu {got[r, c]} oracle {ref[r, c]}")
         if info.container:
             assert np.array_equal(dq.cpu().numpy(), ref_dq), name
+
+
+N_LISTS = 10
+
+
+def draw_layer(rng):
+    rows = int(rng.integers(1, 161))
+    cols = 8 * int(rng.integers(1, 121))
+    w = W.draw_tensor(rng, rows, cols, body=str(rng.choice(["gauss", "t5"])),
+                      log_mu=float(rng.uniform(-5, -1)), log_sigma=float(rng.uniform(0, 0.6)))
+    kw = dict(tile_vectors=int(rng.choice([7, 32, 100, 512])), container=int(rng.integers(0, 5)))
+    pb = int(rng.choice([0, 0, 9, 12]))
+    if pb:
+        kw["prob_bits"] = pb
+    return w, float(rng.uniform(1.5, 7.5)), kw, str(rng.choice(OUT))
+
+
+@pytest.mark.parametrize("i", range(N_LISTS))
+def test_random_layer_list(E, oracle, i):
+    """A list of 1 to 12 random layers (paths, containers and output types mixed) decoded in
+    one launch: by ep_decode_layers (descriptors by value up to 8 layers, in the workspace
+    above) and by a prepared stack; every layer against the oracle."""
+    rng = np.random.default_rng([8, i])
+    n = int(rng.integers(1, 13))
+    drawn = [draw_layer(rng) for _ in range(n)]
+    blobs = [oracle.encode(w, t, **kw)[0] for w, t, kw, _ in drawn]
+    infos = [E.blob_info(b) for b in blobs]
+    say(f"  list {i}: {n} layers, paths {[x.path for x in infos]}, "
+        f"outputs {[d[3] for d in drawn]}")
+    dev = [E.to_device(b) for b in blobs]
+    for how in ("layers", "stack"):
+        outs, dqs, layers = [], [], []
+        for (w, _, _, name), info, d in zip(drawn, infos, dev):
+            code = codes(E, oracle, name)[0]
+            o = torch.empty((info.rows, info.cols), dtype=E.torch_dtype(code), device="cuda")
+            q = torch.zeros(info.rows, dtype=torch.float32, device="cuda") if info.container else None
+            outs.append(o)
+            dqs.append(q)
+            layers.append((info, d.data_ptr(), o.data_ptr(), q.data_ptr() if q is not None else 0, code))
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        s = torch.cuda.current_stream().cuda_stream
+        if how == "layers":
+            ws = E.decode_layers_workspace(n)
+            d_ws = torch.empty(max(1, ws), dtype=torch.uint8, device="cuda")
+            E.decode_layers(layers, d_ws.data_ptr(), ws, status.data_ptr(), s)
+        else:
+            ws = E.stack_workspace(n)
+            d_ws = torch.empty(max(1, ws), dtype=torch.uint8, device="cuda")
+            st = E.stack_prepare(layers, d_ws.data_ptr(), ws, s)
+            E.stack_decode(st, status.data_ptr(), s)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0, how
+        for k, ((_, _, _, name), blob, info, o, q) in enumerate(zip(drawn, blobs, infos, outs, dqs)):
+            ref, ref_dq = oracle.decode(blob, codes(E, oracle, name)[1])
+            assert np.array_equal(gpu_bits(o), ref), (how, k, name)
+            if info.container:
+                assert np.array_equal(q.cpu().numpy(), ref_dq), (how, k)
+
+
+N_FUSED = 10
+
+
+@pytest.mark.parametrize("i", range(N_FUSED))
+def test_random_fused_products(E, oracle, i):
+    """The fused decode and MFMA products on random tensors and rows of X: the INT8 product
+    (INT8 row container) exact against the oracle's decode and exact product; the BF16
+    product (any blob) within its fp32 summation bound against the oracle's bf16 decode
+    multiplied in fp64."""
+    rng = np.random.default_rng([9, i])
+    rows = int(rng.integers(1, 201))
+    cols = 8 * int(rng.integers(1, 151))
+    m = int(rng.choice([1, 3, 16, 17, 33, 64, 100, 257]))
+    w = W.draw_tensor(rng, rows, cols, body="gauss", log_mu=float(rng.uniform(-5, -1)),
+                      log_sigma=0.4)
+    V = int(rng.choice([7, 45, 512]))
+    s = torch.cuda.current_stream().cuda_stream
+    say(f"  fused {i}: {w.shape}, V = {V}, m = {m}")
+    # INT8 product on the INT8 row container
+    blob, _ = oracle.encode(w, float(rng.uniform(3, 7)), container=oracle.CONT_INT8, tile_vectors=V)
+    info = E.blob_info(blob)
+    d_blob = E.to_device(blob)
+    x = rng.integers(-127, 128, (m, cols), dtype=np.int8)
+    d_x = torch.from_numpy(x).cuda()
+    y = torch.empty((m, rows), dtype=torch.int32, device="cuda")
+    dq = torch.empty(rows, dtype=torch.float32, device="cuda")
+    ws = E.decode_gemm_i8_workspace(info)
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    E.decode_gemm_i8(info, d_blob.data_ptr(), d_x.data_ptr(), m, y.data_ptr(), d_ws.data_ptr(), ws,
+                     dq.data_ptr(), status.data_ptr(), s)
+    torch.cuda.synchronize()
+    wd, ref_dq = oracle.decode(blob, oracle.INT8)
+    assert int(status.item()) == 0
+    assert np.array_equal(y.cpu().numpy(), oracle.gemm_i8_nt(x, wd))
+    assert np.array_equal(dq.cpu().numpy(), ref_dq)
+    # BF16 product on a direct blob
+    blob, _ = oracle.encode(w, float(rng.uniform(2, 6)), tile_vectors=V)
+    info = E.blob_info(blob)
+    d_blob = E.to_device(blob)
+    xb = torch.from_numpy(rng.standard_normal((m, cols)).astype(np.float32)).to(torch.bfloat16).cuda()
+    yb = torch.empty((m, rows), dtype=torch.float32, device="cuda")
+    ws = E.decode_gemm_bf16_workspace(info)
+    d_ws = torch.empty(ws, dtype=torch.uint8, device="cuda")
+    E.decode_gemm_bf16(info, d_blob.data_ptr(), xb.data_ptr(), m, yb.data_ptr(), d_ws.data_ptr(), ws,
+                       0, status.data_ptr(), s)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    wbits, _ = oracle.decode(blob, oracle.BF16)
+    wf = (wbits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    xf = xb.float().cpu().numpy().astype(np.float64)
+    exact = xf @ wf.T
+    bound = (cols + 18) * 2.0 ** -24 * (np.abs(xf) @ np.abs(wf).T)
+    assert (np.abs(yb.cpu().numpy().astype(np.float64) - exact) <= bound).all()
