@@ -208,3 +208,23 @@ def test_random_fused_products(E, oracle, i):
     exact = xf @ wf.T
     bound = (cols + 18) * 2.0 ** -24 * (np.abs(xf) @ np.abs(wf).T)
     assert (np.abs(yb.cpu().numpy().astype(np.float64) - exact) <= bound).all()
+
+
+N_ENCODE = 15
+
+
+@pytest.mark.parametrize("i", range(N_ENCODE))
+def test_random_gpu_encoder(E, oracle, i):
+    """The GPU encoder on random tensors (BF16 or FP32 input, every container, tile sizes,
+    rates and precisions as above): the blob equals the oracle encoder's byte for byte."""
+    w, target, kw, _, _ = draw_case(100 + i)
+    rng = np.random.default_rng([10, i])
+    if rng.integers(0, 2):
+        w = (w.astype(np.uint32) << 16).view(np.float32)   # the same values as FP32 input
+    say(f"  GPU encode {i}: {w.shape} {w.dtype} at {target:.2f} bpp {kw}")
+    ref, _ = oracle.encode(w, target, **kw)
+    src = torch.from_numpy(w.view(np.int16) if w.dtype == np.uint16 else w).cuda()
+    dt = E.FP32 if w.dtype == np.float32 else E.BF16
+    blob, _ = E.encode_gpu(src.data_ptr(), w.shape[0], w.shape[1], target, dtype=dt,
+                           stream=torch.cuda.current_stream().cuda_stream, **kw)
+    assert np.array_equal(blob, ref)
